@@ -1,0 +1,181 @@
+/*
+ * predecoder.h -- C ABI of the MI355X (gfx950) pre-decoder hot path.
+ *
+ * Implements the inference step of the local 3D-convolutional pre-decoder for
+ * the rotated surface code ("Fast and accurate AI-based pre-decoders for
+ * surface codes", arXiv 2604.12841): a fully convolutional 3D CNN over the
+ * space-time volume of detector events (Sec. III.B, Fig. ConvArch), whose four
+ * output channels are read as data-qubit Z/X corrections and X/Z
+ * stabilizer-measurement (timelike) corrections (Sec. III.B.5, Eqs.
+ * ZcorreJK-SynZCorrJK), thresholded at logit > 0 (the sigmoid of the BCE
+ * objective, Sec. III.B.4), and applied to the syndrome history to give the
+ * residual syndrome that is handed to a global decoder (Eqs. Resk1X, ReskG1X,
+ * Resk1Z, ReskG1Z).
+ *
+ * Geometry.  Distance d (odd, >= 3), T rounds.  Stabilizers live on the
+ * (d+1) x (d+1) plaquette grid, sites (i, j) with 0 <= i, j <= d:
+ *   X site  <=>  (i + j) even and 1 <= i <= d-1
+ *   Z site  <=>  (i + j) odd  and 1 <= j <= d-1
+ * Plaquette (i, j) acts on the data qubits (i-1, j-1), (i-1, j), (i, j-1),
+ * (i, j) that lie inside [0, d-1]^2 (weight 4 in the bulk, weight 2 on the
+ * boundary).  X_L is a horizontal and Z_L a vertical string (Sec. II, Fig. 2).
+ * Data qubit (r, c) is identified with grid site (r, c), r, c < d.  There are
+ * K = (d^2 - 1) / 2 stabilizers of each type (Eqs. DetectorX/DetectorZ).
+ *
+ * Bit-packed formats (all LSB-first: bit b of a sample row is bit (b & 63) of
+ * 64-bit word (b >> 6); every sample row is a whole number of words; padding
+ * bits are ignored on input and written as 0 on output):
+ *   detectors / residual, W_det = predecoder_det_words(d, T) words per sample:
+ *     b = t * (d^2 - 1) + n; n < K enumerates the X sites in row-major (i, j)
+ *     order, n >= K the Z sites in row-major order.  A detector bit is the
+ *     XOR of one stabilizer's outcomes in rounds t and t-1 (Sec. III.B.1).
+ *   flips, W_flip = predecoder_flip_words(d, T) words per sample:
+ *     b = t * (3 d^2 - 1) + n with n running over
+ *       [0, d^2)          Z data-qubit correction (output channel 0), (r, c) row-major
+ *       [d^2, 2 d^2)      X data-qubit correction (output channel 1)
+ *       [2 d^2, 2 d^2+K)  X-stabilizer measurement flip (channel 2), X-site order
+ *       [2 d^2+K, 3d^2-1) Z-stabilizer measurement flip (channel 3), Z-site order
+ *
+ * Residual (Eqs. Resk1X..ReskG1Z, with a measurement flip in round t also
+ * flipping round t+1, and nothing before round 0):
+ *   R_X[t](s) = D_X[t](s) ^ m_X[t](s) ^ m_X[t-1](s) ^ XOR_{q in supp(s)} z_corr[t](q)
+ *   R_Z[t](s) = D_Z[t](s) ^ m_Z[t](s) ^ m_Z[t-1](s) ^ XOR_{q in supp(s)} x_corr[t](q)
+ * applied at every round 0 <= t < T (including the last one).
+ *
+ * Network.  A list of conv3d layers (stride 1, no dilation, zero padding
+ * (k-1)/2, cross-correlation as in PyTorch Conv3d):
+ *   layers[0].c_in == 2  (channel 0: X-type detectors, channel 1: Z-type,
+ *                         placed at their stabilizer sites, zero elsewhere)
+ *   layers[l].c_in == layers[l-1].c_out
+ *   layers[n-1]: the head, c_out == 4, act == PD_ACT_NONE.
+ * Hidden layers apply their activation; GELU is the tanh form
+ * 0.5 y (1 + tanh(sqrt(2/pi) (y + 0.044715 y^3))) (Table hyperparameters).
+ * Weights are host fp32, layer after layer, each as w[c_out][c_in][kt][ki][kj]
+ * followed by b[c_out]; tap (kt, ki, kj) multiplies x[t+kt-p][i+ki-p][j+kj-p].
+ *
+ * Precision.  PD_DTYPE_BF16: weights and every conv/head input are rounded
+ * to bf16 (round to nearest even), products are accumulated in fp32, biases
+ * and the activation are fp32, logits are fp32.  PD_DTYPE_FP32: fp32 end to
+ * end.  flip = (logit > 0); a logit of exactly 0 is no flip.
+ *
+ * Supported shapes (others give PD_ERR_UNSUPPORTED): 3 <= d <= 63,
+ * 1 <= T <= 1023; hidden layers k == 3; head k == 1.  BF16: hidden widths
+ * 64 or 128.  FP32: hidden widths 8 .. 128, multiples of 8.
+ *
+ * Errors.  Every function is nothrow and never aborts.  Host-checkable misuse
+ * gives PD_ERR_INVALID_ARG before any device call; a failed HIP call or
+ * launch (including "no device") gives PD_ERR_DEVICE; a failed allocation
+ * gives PD_ERR_OUT_OF_MEMORY.  After an error the outputs are unspecified
+ * and the handle stays usable.
+ *
+ * Ownership and streams.  Input/output buffers of run/residual/unpack are
+ * caller-owned DEVICE memory.  The handle owns its copy of the weights, its
+ * workspace and its tables.  Work is enqueued on the caller's HIP stream
+ * (hipStream_t passed as void*; NULL = the null stream) and the host never
+ * waits for it, except in predecoder_stage_times.  One handle must not be
+ * used from two streams at once (the workspace is shared): use one handle
+ * per stream.
+ */
+#ifndef PREDECODER_H
+#define PREDECODER_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum pd_status {
+  PD_OK = 0,
+  PD_ERR_INVALID_ARG = 1,
+  PD_ERR_UNSUPPORTED = 2,
+  PD_ERR_OUT_OF_MEMORY = 3,
+  PD_ERR_DEVICE = 4
+} pd_status;
+
+typedef enum pd_act { PD_ACT_NONE = 0, PD_ACT_GELU_TANH = 1, PD_ACT_RELU = 2 } pd_act;
+
+typedef enum pd_dtype { PD_DTYPE_FP32 = 0, PD_DTYPE_BF16 = 1 } pd_dtype;
+
+/* One conv3d layer: k x k x k kernel, c_in -> c_out, activation act. */
+typedef struct pd_layer {
+  int32_t c_in;
+  int32_t c_out;
+  int32_t k;
+  int32_t act;
+} pd_layer;
+
+typedef struct pd_predecoder pd_predecoder; /* opaque */
+
+/* Builds a pre-decoder for distance d and T rounds (Sec. III.B; the network
+ * is fully convolutional, so the same weights apply to any (d, T)).
+ * weights: host fp32, n_weights == predecoder_weight_count(layers, n_layers),
+ *          copied (the caller keeps ownership).
+ * dtype:   PD_DTYPE_BF16 or PD_DTYPE_FP32.
+ * max_batch: largest batch any later call may pass; sizes the workspace.
+ * out:     receives the handle (NULL on error).
+ * Allocates device memory on the current HIP device; launches nothing. */
+pd_status predecoder_create(const float* weights, size_t n_weights, int32_t d, int32_t T,
+                            const pd_layer* layers, int32_t n_layers, int32_t dtype,
+                            int32_t max_batch, pd_predecoder** out);
+
+/* The whole hot path for `batch` independent volumes (Sec. III.B.5):
+ * unpack -> conv layers (+bias, activation) -> head -> threshold ->
+ * residual and bit repack.
+ * det:      device, [batch][W_det] uint64, packed detectors (read only).
+ * flips:    device, [batch][W_flip] uint64, packed thresholded corrections.
+ * residual: device, [batch][W_det] uint64, packed residual syndrome.
+ * logits:   device or NULL; if given, [batch][4][T][d+1][d+1] fp32 head
+ *           outputs at every grid site (channel order as in `flips`).
+ * 1 <= batch <= max_batch.  Asynchronous on hip_stream. */
+pd_status predecoder_run(pd_predecoder* h, void* hip_stream, const uint64_t* det, int32_t batch,
+                         uint64_t* flips, uint64_t* residual, float* logits);
+
+/* The residual stage alone (Eqs. Resk1X..ReskG1Z) from caller-given packed
+ * flips: det [batch][W_det], flips [batch][W_flip] -> residual [batch][W_det],
+ * all device.  Asynchronous on hip_stream. */
+pd_status predecoder_residual(pd_predecoder* h, void* hip_stream, const uint64_t* det,
+                              const uint64_t* flips, int32_t batch, uint64_t* residual);
+
+/* The unpack stage alone (Sec. III.B.1, Eqs. encTrainX1/2: detector events
+ * placed at their stabilizer sites, 0 elsewhere): det [batch][W_det] ->
+ * planes, device, [batch][T][d+1][d+1][2] in the handle's dtype (bf16 bit
+ * patterns as uint16 for PD_DTYPE_BF16, fp32 for PD_DTYPE_FP32).
+ * Asynchronous on hip_stream. */
+pd_status predecoder_unpack(pd_predecoder* h, void* hip_stream, const uint64_t* det,
+                            int32_t batch, void* planes);
+
+/* Number of timed stages of predecoder_run: unpack, one per layer (the last
+ * one is the head with its threshold), and the residual/repack stage. */
+int32_t predecoder_num_stages(const pd_predecoder* h);
+
+/* Runs the full path n_iter times on hip_stream with HIP events between the
+ * stages and writes the mean milliseconds of each stage to ms_per_stage
+ * (host, predecoder_num_stages(h) floats).  Arguments as predecoder_run
+ * (logits not written).  Blocks the host until the stream has drained. */
+pd_status predecoder_stage_times(pd_predecoder* h, void* hip_stream, const uint64_t* det,
+                                 int32_t batch, uint64_t* flips, uint64_t* residual, int32_t n_iter,
+                                 float* ms_per_stage);
+
+/* Frees every device allocation of the handle.  NULL is ignored. */
+void predecoder_destroy(pd_predecoder* h);
+
+/* Static, human-readable name of a status code. */
+const char* predecoder_status_string(pd_status s);
+
+/* ceil(T (d^2 - 1) / 64): detector/residual words per sample; -1 on bad args. */
+int64_t predecoder_det_words(int32_t d, int32_t T);
+
+/* ceil(T (3 d^2 - 1) / 64): flip words per sample; -1 on bad args. */
+int64_t predecoder_flip_words(int32_t d, int32_t T);
+
+/* Sum over layers of c_out * c_in * k^3 + c_out (weights plus biases, the
+ * parameter count of Table models); 0 on bad args. */
+size_t predecoder_weight_count(const pd_layer* layers, int32_t n_layers);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PREDECODER_H */

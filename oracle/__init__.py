@@ -1,0 +1,172 @@
+"""CPU oracle of the pre-decoder hot path (arXiv 2604.12841, Sec. III.B).
+
+TEST INFRASTRUCTURE ONLY: the tests, the smoke check and the CPU-baseline leg
+of the benchmark are the only callers.  The product path never imports this
+package; the two share no code.
+
+The arithmetic lives in ``oracle.c`` (plain C, fp64); this module builds it
+with gcc on first use, loads it with ctypes and marshals numpy arrays.
+Array layouts are channel-major per sample: planes/logits [B][C][T][d+1][d+1].
+"""
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+
+def build(force=False):
+    """Compile oracle.c into liboracle.so (gcc, OpenMP over samples and output channels)."""
+    if force or not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-O3", "-fopenmp", "-fPIC", "-shared", "-std=c11", _SRC,
+                               "-o", tmp, "-lm"])
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        build()
+        lib = ctypes.CDLL(_LIB_PATH)
+        i32, i64, vp = ctypes.c_int, ctypes.c_int64, ctypes.c_void_p
+        lib.oracle_site_kind.argtypes = [i32, i32, i32]
+        lib.oracle_site_kind.restype = i32
+        lib.oracle_plaquette_support.argtypes = [i32, i32, i32, vp]
+        lib.oracle_plaquette_support.restype = i32
+        lib.oracle_stabilizer_order.argtypes = [i32, vp, vp]
+        lib.oracle_stabilizer_order.restype = i32
+        lib.oracle_det_words.argtypes = [i32, i32]
+        lib.oracle_det_words.restype = i64
+        lib.oracle_flip_words.argtypes = [i32, i32]
+        lib.oracle_flip_words.restype = i64
+        lib.oracle_unpack.argtypes = [i32, i32, i32, vp, vp]
+        lib.oracle_unpack.restype = None
+        lib.oracle_round_bf16.argtypes = [ctypes.c_float]
+        lib.oracle_round_bf16.restype = ctypes.c_float
+        lib.oracle_gelu_tanh.argtypes = [ctypes.c_double]
+        lib.oracle_gelu_tanh.restype = ctypes.c_double
+        lib.oracle_weight_count.argtypes = [i32, vp]
+        lib.oracle_weight_count.restype = i64
+        lib.oracle_forward.argtypes = [i32, i32, i32, vp, i32, vp, vp, i32, vp]
+        lib.oracle_forward.restype = None
+        lib.oracle_flips_residual.argtypes = [i32, i32, i32, vp, vp, vp, vp]
+        lib.oracle_flips_residual.restype = None
+        lib.oracle_residual_from_flips.argtypes = [i32, i32, i32, vp, vp, vp]
+        lib.oracle_residual_from_flips.restype = None
+        _lib = lib
+    return _lib
+
+
+def _ptr(a):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def det_words(d, T):
+    return int(_load().oracle_det_words(d, T))
+
+
+def flip_words(d, T):
+    return int(_load().oracle_flip_words(d, T))
+
+
+def site_kind(d):
+    """[d+1, d+1] int array: 1 = X stabilizer, 2 = Z stabilizer, 0 = none."""
+    lib = _load()
+    H = d + 1
+    return np.array([[lib.oracle_site_kind(d, i, j) for j in range(H)] for i in range(H)], dtype=np.int32)
+
+
+def plaquette_support(d, i, j):
+    """Data qubits (r, c) acted on by the plaquette at grid site (i, j)."""
+    rc = np.zeros(8, dtype=np.int32)
+    n = _load().oracle_plaquette_support(d, i, j, _ptr(rc))
+    return [(int(rc[2 * e]), int(rc[2 * e + 1])) for e in range(n)]
+
+
+def stabilizer_order(d):
+    """(site_of, index_of): compact stabilizer index <-> flattened grid site."""
+    H = d + 1
+    site_of = np.zeros(d * d - 1, dtype=np.int32)
+    index_of = np.zeros(H * H, dtype=np.int32)
+    _load().oracle_stabilizer_order(d, _ptr(site_of), _ptr(index_of))
+    return site_of, index_of
+
+
+def unpack(d, T, det):
+    """Packed detectors [B][W_det] uint64 -> planes [B][2][T][d+1][d+1] float64."""
+    det = np.ascontiguousarray(det, dtype=np.uint64)
+    B = det.shape[0]
+    H = d + 1
+    out = np.zeros((B, 2, T, H, H), dtype=np.float64)
+    _load().oracle_unpack(d, T, B, _ptr(det), _ptr(out))
+    return out
+
+
+def round_bf16(x):
+    """Elementwise fp32 -> bf16 (round to nearest even) -> fp32."""
+    lib = _load()
+    x = np.asarray(x, dtype=np.float32)
+    return np.array([lib.oracle_round_bf16(float(v)) for v in x.ravel()], dtype=np.float32).reshape(x.shape)
+
+
+def gelu_tanh(x):
+    lib = _load()
+    x = np.asarray(x, dtype=np.float64)
+    return np.array([lib.oracle_gelu_tanh(float(v)) for v in x.ravel()], dtype=np.float64).reshape(x.shape)
+
+
+def weight_count(layers):
+    spec = np.array([list(l) for l in layers], dtype=np.int32).ravel()
+    return int(_load().oracle_weight_count(len(layers), _ptr(spec)))
+
+
+def forward(d, T, planes, layers, weights, bf16):
+    """Network forward.  planes [B][c_in][T][H][H] float64; layers: list of
+    (c_in, c_out, k, act); weights: flat fp32.  Returns logits
+    [B][c_out_last][T][H][H] float64 (fp32-valued in bf16 mode)."""
+    planes = np.ascontiguousarray(planes, dtype=np.float64)
+    weights = np.ascontiguousarray(weights, dtype=np.float32)
+    spec = np.ascontiguousarray(np.array([list(l) for l in layers], dtype=np.int32).ravel())
+    if weights.size != weight_count(layers):
+        raise ValueError("weight count mismatch")
+    B = planes.shape[0]
+    H = d + 1
+    co = layers[-1][1]
+    out = np.zeros((B, co, T, H, H), dtype=np.float64)
+    _load().oracle_forward(d, T, B, _ptr(planes), len(layers), _ptr(spec), _ptr(weights),
+                           1 if bf16 else 0, _ptr(out))
+    return out
+
+
+def flips_residual(d, T, logits, det):
+    """logits [B][4][T][H][H] + packed det -> (packed flips, packed residual)."""
+    logits = np.ascontiguousarray(logits, dtype=np.float64)
+    det = np.ascontiguousarray(det, dtype=np.uint64)
+    B = logits.shape[0]
+    flips = np.zeros((B, flip_words(d, T)), dtype=np.uint64)
+    res = np.zeros((B, det_words(d, T)), dtype=np.uint64)
+    _load().oracle_flips_residual(d, T, B, _ptr(logits), _ptr(det), _ptr(flips), _ptr(res))
+    return flips, res
+
+
+def residual_from_flips(d, T, det, flips):
+    det = np.ascontiguousarray(det, dtype=np.uint64)
+    flips = np.ascontiguousarray(flips, dtype=np.uint64)
+    B = det.shape[0]
+    res = np.zeros((B, det_words(d, T)), dtype=np.uint64)
+    _load().oracle_residual_from_flips(d, T, B, _ptr(det), _ptr(flips), _ptr(res))
+    return res
+
+
+def run(d, T, det, layers, weights, bf16):
+    """The whole path: (logits, flips, residual)."""
+    logits = forward(d, T, unpack(d, T, det), layers, weights, bf16)
+    flips, res = flips_residual(d, T, logits, det)
+    return logits, flips, res

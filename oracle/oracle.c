@@ -1,0 +1,388 @@
+/*
+ * oracle.c -- plain, slow CPU reference of the pre-decoder hot path.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only tests, the smoke check and the CPU-baseline
+ * leg of the benchmark may load this library.  It shares no code, header,
+ * table or constant generator with the GPU path: it carries its own geometry,
+ * bit packing, bf16 rounding and activation.
+ *
+ * Everything follows the definitions of arXiv 2604.12841 as written:
+ *   - detector events d_{i,k} = s_{i,k} XOR s_{i,k-1} placed on a grid
+ *     (Sec. III.B.1, Eqs. encTrainX1/encTrainX2, Fig. StabMap);
+ *   - a fully convolutional 3D CNN, output the same size as the input
+ *     (Sec. III.B, Fig. ConvArch), stride 1, zero padding;
+ *   - GELU, tanh form (Table hyperparameters);
+ *   - corrections read from the four output channels (Eqs. ZcorreJK,
+ *     XcorreJK, SynXCorrJK, SynZCorrJK), thresholded at sigmoid > 1/2, i.e.
+ *     logit > 0 (the BCE objective of Sec. III.B.4 applies a sigmoid);
+ *   - syndromes induced by the data corrections (Eqs. SXJK, SZJK) and the
+ *     residual syndrome (Eqs. Resk1X, ReskG1X, Resk1Z, ReskG1Z).
+ *
+ * Floating point is fp64.  In bf16 mode the quantisation points of the GPU
+ * path are reproduced (weights and every conv/head input rounded to bf16 with
+ * round-to-nearest-even; the pre-activation is rounded to fp32 before the
+ * activation; the activation is evaluated in fp64 and rounded to fp32 and then
+ * to bf16; logits are rounded to fp32).  Products of bf16 values are exact in
+ * fp64, so the only difference from an exact sum is fp64 rounding.
+ *
+ * Array layout is channel-major per sample (like PyTorch NCDHW):
+ * x[b][c][t][i][j] with i, j in [0, d] on the (d+1) x (d+1) plaquette grid.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ---------------------------------------------------------------------- */
+/* Geometry of the rotated surface code on the (d+1) x (d+1) plaquette grid */
+/* (Sec. II, Fig. 2: X_L horizontal, Z_L vertical; Fig. StabMap).           */
+/* ---------------------------------------------------------------------- */
+
+/* Kind of grid site (i, j): 1 = X stabilizer, 2 = Z stabilizer, 0 = none. */
+int oracle_site_kind(int d, int i, int j) {
+  if (i < 0 || j < 0 || i > d || j > d) return 0;
+  if (((i + j) % 2 == 0) && i >= 1 && i <= d - 1) return 1;
+  if (((i + j) % 2 == 1) && j >= 1 && j <= d - 1) return 2;
+  return 0;
+}
+
+/* Data qubits acted on by plaquette (i, j): the corners (i-1, j-1), (i-1, j),
+ * (i, j-1), (i, j) that lie in [0, d-1]^2.  Writes up to 4 (r, c) pairs into
+ * rc[8] and returns how many. */
+int oracle_plaquette_support(int d, int i, int j, int* rc) {
+  int n = 0;
+  for (int dr = -1; dr <= 0; ++dr)
+    for (int dc = -1; dc <= 0; ++dc) {
+      int r = i + dr, c = j + dc;
+      if (r >= 0 && r < d && c >= 0 && c < d) {
+        rc[2 * n] = r;
+        rc[2 * n + 1] = c;
+        ++n;
+      }
+    }
+  return n;
+}
+
+/* Compact enumeration of stabilizers: the X sites in row-major (i, j) order,
+ * then the Z sites in row-major order.  site_of[n] = i * (d+1) + j for
+ * n < d^2 - 1; index_of[i * (d+1) + j] = n or -1.  Returns d^2 - 1. */
+int oracle_stabilizer_order(int d, int* site_of, int* index_of) {
+  int H = d + 1, n = 0;
+  for (int s = 0; s < H * H; ++s) index_of[s] = -1;
+  for (int kind = 1; kind <= 2; ++kind)
+    for (int i = 0; i <= d; ++i)
+      for (int j = 0; j <= d; ++j)
+        if (oracle_site_kind(d, i, j) == kind) {
+          site_of[n] = i * H + j;
+          index_of[i * H + j] = n;
+          ++n;
+        }
+  return n;
+}
+
+int64_t oracle_det_words(int d, int T) { return ((int64_t)T * (d * d - 1) + 63) / 64; }
+int64_t oracle_flip_words(int d, int T) { return ((int64_t)T * (3 * d * d - 1) + 63) / 64; }
+
+static int get_bit(const uint64_t* row, int64_t b) { return (int)((row[b >> 6] >> (b & 63)) & 1u); }
+static void set_bit(uint64_t* row, int64_t b, int v) {
+  if (v) row[b >> 6] |= (uint64_t)1 << (b & 63);
+}
+
+/* ---------------------------------------------------------------------- */
+/* Unpack (Sec. III.B.1): X-type detector events of round t at their X     */
+/* sites in channel 0, Z-type at their Z sites in channel 1, 0 elsewhere.  */
+/* planes: [B][2][T][d+1][d+1].                                            */
+/* ---------------------------------------------------------------------- */
+void oracle_unpack(int d, int T, int B, const uint64_t* det, double* planes) {
+  int H = d + 1, S = d * d - 1;
+  int64_t W = oracle_det_words(d, T);
+  int* site_of = (int*)malloc(sizeof(int) * S);
+  int* index_of = (int*)malloc(sizeof(int) * H * H);
+  oracle_stabilizer_order(d, site_of, index_of);
+  for (int b = 0; b < B; ++b)
+    for (int c = 0; c < 2; ++c)
+      for (int t = 0; t < T; ++t)
+        for (int i = 0; i < H; ++i)
+          for (int j = 0; j < H; ++j) {
+            int kind = oracle_site_kind(d, i, j);
+            double v = 0.0;
+            if (kind == c + 1) {
+              int n = index_of[i * H + j];
+              v = (double)get_bit(det + (int64_t)b * W, (int64_t)t * S + n);
+            }
+            planes[((((int64_t)b * 2 + c) * T + t) * H + i) * H + j] = v;
+          }
+  free(site_of);
+  free(index_of);
+}
+
+/* ---------------------------------------------------------------------- */
+/* Number formats and the activation                                       */
+/* ---------------------------------------------------------------------- */
+
+/* fp32 -> bf16 -> fp32 with round-to-nearest, ties to even, on the fp32 bit
+ * pattern (bf16 keeps the top 16 bits).  NaN stays NaN. */
+float oracle_round_bf16(float x) {
+  uint32_t u;
+  memcpy(&u, &x, 4);
+  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) {
+    u |= 0x00400000u; /* quiet NaN */
+  } else {
+    uint32_t lsb = (u >> 16) & 1u;
+    u += 0x7fffu + lsb;
+  }
+  u &= 0xffff0000u;
+  float y;
+  memcpy(&y, &u, 4);
+  return y;
+}
+
+/* GELU, tanh approximation (Table hyperparameters):
+ *   0.5 y (1 + tanh(sqrt(2/pi) (y + 0.044715 y^3))). */
+double oracle_gelu_tanh(double y) {
+  const double pi = 3.14159265358979323846;
+  double u = sqrt(2.0 / pi) * (y + 0.044715 * y * y * y);
+  return 0.5 * y * (1.0 + tanh(u));
+}
+
+enum { ACT_NONE = 0, ACT_GELU_TANH = 1, ACT_RELU = 2 };
+
+static double activation(int act, double y) {
+  if (act == ACT_GELU_TANH) return oracle_gelu_tanh(y);
+  if (act == ACT_RELU) return y > 0.0 ? y : 0.0;
+  return y;
+}
+
+int64_t oracle_weight_count(int n_layers, const int* spec) {
+  int64_t n = 0;
+  for (int l = 0; l < n_layers; ++l) {
+    int64_t ci = spec[4 * l], co = spec[4 * l + 1], k = spec[4 * l + 2];
+    n += co * ci * k * k * k + co;
+  }
+  return n;
+}
+
+/* ---------------------------------------------------------------------- */
+/* Forward pass of the fully convolutional network (Sec. III.B).           */
+/*   y[co][t][i][j] = b[co] + sum_{ci,kt,ki,kj} w[co][ci][kt][ki][kj] *    */
+/*                    x[ci][t+kt-p][i+ki-p][j+kj-p],  p = (k-1)/2,          */
+/* with x = 0 outside [0,T) x [0,d] x [0,d]; hidden layers apply their     */
+/* activation, the last layer is linear (it gives the logits).              */
+/* spec: n_layers x {c_in, c_out, k, act}.  weights: fp32, per layer        */
+/* w[c_out][c_in][k][k][k] then b[c_out].  planes: [B][c_in0][T][H][H].     */
+/* logits: [B][c_out_last][T][H][H].  bf16 != 0 selects the bf16 quantisation*/
+/* points described at the top of this file.                                */
+/* Samples and output channels are independent; they are spread over       */
+/* OpenMP threads (the arithmetic of each output is unchanged).             */
+/* ---------------------------------------------------------------------- */
+void oracle_forward(int d, int T, int B, const double* planes, int n_layers, const int* spec,
+                    const float* weights, int bf16, double* logits) {
+  int H = d + 1;
+  int64_t V = (int64_t)T * H * H;
+  int cmax = spec[0];
+  for (int l = 0; l < n_layers; ++l)
+    if (spec[4 * l + 1] > cmax) cmax = spec[4 * l + 1];
+
+  /* Per-layer weights in fp64 (rounded to bf16 first in bf16 mode). */
+  double** w = (double**)malloc(sizeof(double*) * n_layers);
+  double** bias = (double**)malloc(sizeof(double*) * n_layers);
+  const float* src = weights;
+  for (int l = 0; l < n_layers; ++l) {
+    int ci = spec[4 * l], co = spec[4 * l + 1], k = spec[4 * l + 2];
+    int64_t nw = (int64_t)co * ci * k * k * k;
+    w[l] = (double*)malloc(sizeof(double) * nw);
+    bias[l] = (double*)malloc(sizeof(double) * co);
+    for (int64_t e = 0; e < nw; ++e) w[l][e] = bf16 ? (double)oracle_round_bf16(src[e]) : (double)src[e];
+    for (int e = 0; e < co; ++e) bias[l][e] = (double)src[nw + e];
+    src += nw + co;
+  }
+
+  double* xa = (double*)malloc(sizeof(double) * (size_t)B * cmax * V);
+  double* xb = (double*)malloc(sizeof(double) * (size_t)B * cmax * V);
+  int c0 = spec[0];
+  for (int b = 0; b < B; ++b)
+    for (int64_t e = 0; e < c0 * V; ++e) {
+      double v = planes[(int64_t)b * c0 * V + e];
+      xa[(int64_t)b * cmax * V + e] = bf16 ? (double)oracle_round_bf16((float)v) : v;
+    }
+
+  for (int l = 0; l < n_layers; ++l) {
+    int ci_n = spec[4 * l], co_n = spec[4 * l + 1], k = spec[4 * l + 2], act = spec[4 * l + 3];
+    int p = (k - 1) / 2, last = (l == n_layers - 1);
+    const double* wl = w[l];
+    const double* bl = bias[l];
+#pragma omp parallel for collapse(2) schedule(dynamic)
+    for (int b = 0; b < B; ++b)
+      for (int co = 0; co < co_n; ++co) {
+        const double* x = xa + (int64_t)b * cmax * V;
+        double* y = xb + (int64_t)b * cmax * V + (int64_t)co * V;
+        for (int t = 0; t < T; ++t)
+          for (int i = 0; i < H; ++i)
+            for (int j = 0; j < H; ++j) {
+              double acc = 0.0;
+              for (int ci = 0; ci < ci_n; ++ci)
+                for (int kt = 0; kt < k; ++kt) {
+                  int tt = t + kt - p;
+                  if (tt < 0 || tt >= T) continue;
+                  for (int ki = 0; ki < k; ++ki) {
+                    int ii = i + ki - p;
+                    if (ii < 0 || ii >= H) continue;
+                    for (int kj = 0; kj < k; ++kj) {
+                      int jj = j + kj - p;
+                      if (jj < 0 || jj >= H) continue;
+                      acc += wl[(((int64_t)co * ci_n + ci) * k + kt) * k * k + ki * k + kj] *
+                             x[(((int64_t)ci * T + tt) * H + ii) * H + jj];
+                    }
+                  }
+                }
+              double v;
+              if (bf16) {
+                float pre = (float)(acc + bl[co]);
+                if (last) {
+                  v = (double)pre; /* fp32 logit */
+                } else {
+                  float a = (float)activation(act, (double)pre);
+                  v = (double)oracle_round_bf16(a);
+                }
+              } else {
+                v = last ? acc + bl[co] : activation(act, acc + bl[co]);
+              }
+              y[((int64_t)t * H + i) * H + j] = v;
+            }
+      }
+    double* tmp = xa;
+    xa = xb;
+    xb = tmp;
+  }
+  int co_last = spec[4 * (n_layers - 1) + 1];
+  for (int b = 0; b < B; ++b)
+    memcpy(logits + (int64_t)b * co_last * V, xa + (int64_t)b * cmax * V, sizeof(double) * co_last * V);
+
+  for (int l = 0; l < n_layers; ++l) {
+    free(w[l]);
+    free(bias[l]);
+  }
+  free(w);
+  free(bias);
+  free(xa);
+  free(xb);
+}
+
+/* ---------------------------------------------------------------------- */
+/* Corrections and residual (Sec. III.B.5).                                */
+/* ---------------------------------------------------------------------- */
+
+/* Residual of one sample from unpacked corrections on the grid:
+ *   zc[t][r][c], xc[t][r][c]  data-qubit Z / X corrections (r, c < d),
+ *   mx[t][i][j], mz[t][i][j]  X / Z measurement corrections at their sites.
+ * R[t](s) = D[t](s) ^ m[t](s) ^ m[t-1](s) ^ (parity of the data corrections
+ * on the support of s): M_X reads Z corrections, M_Z reads X corrections
+ * (Eqs. SXJK, SZJK); a measurement correction in round t flips the outcome
+ * in rounds t and t+1, so the detector of round t sees m[t] and m[t-1]
+ * (Eqs. Resk1X..ReskG1Z; nothing before round 0). */
+static void residual_one(int d, int T, const uint64_t* det, const uint8_t* zc, const uint8_t* xc,
+                         const uint8_t* mx, const uint8_t* mz, uint64_t* res) {
+  int H = d + 1, S = d * d - 1;
+  int64_t W = oracle_det_words(d, T);
+  int* site_of = (int*)malloc(sizeof(int) * S);
+  int* index_of = (int*)malloc(sizeof(int) * H * H);
+  oracle_stabilizer_order(d, site_of, index_of);
+  memset(res, 0, sizeof(uint64_t) * W);
+  for (int t = 0; t < T; ++t)
+    for (int n = 0; n < S; ++n) {
+      int s = site_of[n], i = s / H, j = s % H;
+      int kind = oracle_site_kind(d, i, j);
+      const uint8_t* m = (kind == 1) ? mx : mz;
+      const uint8_t* data = (kind == 1) ? zc : xc;
+      int64_t b = (int64_t)t * S + n;
+      int v = get_bit(det, b);
+      v ^= m[(t * H + i) * H + j];
+      if (t > 0) v ^= m[((t - 1) * H + i) * H + j];
+      int rc[8];
+      int q = oracle_plaquette_support(d, i, j, rc);
+      for (int e = 0; e < q; ++e) v ^= data[(t * H + rc[2 * e]) * H + rc[2 * e + 1]];
+      set_bit(res, b, v);
+    }
+  free(site_of);
+  free(index_of);
+}
+
+/* Thresholds logits [B][4][T][H][H] (flip = logit > 0, Eqs. ZcorreJK..
+ * SynZCorrJK with the sigmoid of Sec. III.B.4), keeps each channel only where
+ * it is defined (data qubits for 0/1, X sites for 2, Z sites for 3), packs the
+ * flips and computes the residual. */
+void oracle_flips_residual(int d, int T, int B, const double* logits, const uint64_t* det,
+                           uint64_t* flips, uint64_t* residual) {
+  int H = d + 1, S = d * d - 1, K = S / 2;
+  int64_t V = (int64_t)T * H * H;
+  int64_t Wd = oracle_det_words(d, T), Wf = oracle_flip_words(d, T);
+  int* site_of = (int*)malloc(sizeof(int) * S);
+  int* index_of = (int*)malloc(sizeof(int) * H * H);
+  oracle_stabilizer_order(d, site_of, index_of);
+  uint8_t* f = (uint8_t*)malloc(4 * V);
+  for (int b = 0; b < B; ++b) {
+    const double* lg = logits + (int64_t)b * 4 * V;
+    for (int ch = 0; ch < 4; ++ch)
+      for (int t = 0; t < T; ++t)
+        for (int i = 0; i < H; ++i)
+          for (int j = 0; j < H; ++j) {
+            int kind = oracle_site_kind(d, i, j);
+            int defined = (ch < 2) ? (i < d && j < d) : (kind == ch - 1);
+            int64_t e = ((int64_t)ch * T + t) * H * H + i * H + j;
+            f[e] = (uint8_t)(defined && lg[e] > 0.0);
+          }
+    uint64_t* fr = flips + (int64_t)b * Wf;
+    memset(fr, 0, sizeof(uint64_t) * Wf);
+    for (int t = 0; t < T; ++t) {
+      int64_t base = (int64_t)t * (3 * d * d - 1);
+      for (int r = 0; r < d; ++r)
+        for (int c = 0; c < d; ++c) {
+          set_bit(fr, base + r * d + c, f[(0 * T + t) * H * H + r * H + c]);
+          set_bit(fr, base + d * d + r * d + c, f[(1 * T + t) * H * H + r * H + c]);
+        }
+      for (int n = 0; n < S; ++n) {
+        int s = site_of[n];
+        int ch = (n < K) ? 2 : 3;
+        set_bit(fr, base + 2 * d * d + n, f[((int64_t)ch * T + t) * H * H + s]);
+      }
+    }
+    residual_one(d, T, det + (int64_t)b * Wd, f, f + V, f + 2 * V, f + 3 * V,
+                 residual + (int64_t)b * Wd);
+  }
+  free(f);
+  free(site_of);
+  free(index_of);
+}
+
+/* Residual from packed flips (same format as oracle_flips_residual writes). */
+void oracle_residual_from_flips(int d, int T, int B, const uint64_t* det, const uint64_t* flips,
+                                uint64_t* residual) {
+  int H = d + 1, S = d * d - 1, K = S / 2;
+  int64_t V = (int64_t)T * H * H;
+  int64_t Wd = oracle_det_words(d, T), Wf = oracle_flip_words(d, T);
+  int* site_of = (int*)malloc(sizeof(int) * S);
+  int* index_of = (int*)malloc(sizeof(int) * H * H);
+  oracle_stabilizer_order(d, site_of, index_of);
+  uint8_t* f = (uint8_t*)malloc(4 * V);
+  for (int b = 0; b < B; ++b) {
+    const uint64_t* fr = flips + (int64_t)b * Wf;
+    memset(f, 0, 4 * V);
+    for (int t = 0; t < T; ++t) {
+      int64_t base = (int64_t)t * (3 * d * d - 1);
+      for (int r = 0; r < d; ++r)
+        for (int c = 0; c < d; ++c) {
+          f[(0 * T + t) * H * H + r * H + c] = (uint8_t)get_bit(fr, base + r * d + c);
+          f[(1 * T + t) * H * H + r * H + c] = (uint8_t)get_bit(fr, base + d * d + r * d + c);
+        }
+      for (int n = 0; n < S; ++n) {
+        int ch = (n < K) ? 2 : 3;
+        f[((int64_t)ch * T + t) * H * H + site_of[n]] = (uint8_t)get_bit(fr, base + 2 * d * d + n);
+      }
+    }
+    residual_one(d, T, det + (int64_t)b * Wd, f, f + V, f + 2 * V, f + 3 * V,
+                 residual + (int64_t)b * Wd);
+  }
+  free(f);
+  free(site_of);
+  free(index_of);
+}

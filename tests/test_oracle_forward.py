@@ -1,0 +1,200 @@
+"""Pins of the oracle's network forward (Sec. III.B, Fig. ConvArch, Eq.
+ReceptiveFieldFormula, Table hyperparameters) against closed forms, the
+library convolution of PyTorch (CPU, fp64) and invariants of a fully
+convolutional network."""
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+import oracle
+from paper_2604_12841_amd import workload
+
+GELU, NONE, RELU = workload.GELU_TANH, workload.NONE, workload.RELU
+
+
+def torch_forward(planes, layers, weights, bf16):
+    """Reference with torch.nn.functional.conv3d (fp64, CPU), applying the
+    same quantisation points as the bf16 path: weights and conv inputs in
+    bf16, pre-activation rounded to fp32, activation in fp64 rounded to fp32
+    then bf16, logits in fp32."""
+    x = torch.from_numpy(planes).double()
+    off = 0
+    q = (lambda t: t.float().to(torch.bfloat16).double()) if bf16 else (lambda t: t)
+    x = q(x)
+    for li, (ci, co, k, act) in enumerate(layers):
+        nw = co * ci * k ** 3
+        w = torch.from_numpy(weights[off:off + nw].reshape(co, ci, k, k, k).copy()).double()
+        b = torch.from_numpy(weights[off + nw:off + nw + co].copy()).double()
+        off += nw + co
+        y = F.conv3d(x, q(w), b, padding=(k - 1) // 2)
+        last = li == len(layers) - 1
+        if bf16:
+            y = y.float().double()
+        if not last:
+            if act == GELU:
+                y = F.gelu(y, approximate="tanh")
+            elif act == RELU:
+                y = F.relu(y)
+            if bf16:
+                y = y.float().to(torch.bfloat16).double()
+        x = y
+    return x.numpy()
+
+
+def random_planes(rng, B, c, T, H, density=0.3):
+    return (rng.random((B, c, T, H, H)) < density).astype(np.float64)
+
+
+def test_bf16_rounding_matches_torch():
+    rng = np.random.default_rng(1)
+    x = np.concatenate([
+        rng.standard_normal(2000).astype(np.float32) * 10,
+        # exact ties between two bf16 values (low 16 bits 0x8000), both parities
+        (np.arange(1, 200, dtype=np.uint32) << 16 | 0x8000).view(np.float32),
+        np.array([0.0, -0.0, 1.0, -1.0, 3.0e38, 1e-40], dtype=np.float32),
+    ])
+    ref = torch.from_numpy(x).to(torch.bfloat16).float().numpy()
+    np.testing.assert_array_equal(oracle.round_bf16(x), ref)
+
+
+def test_gelu_tanh_matches_library_and_limits():
+    x = np.linspace(-12, 12, 4001)
+    ref = F.gelu(torch.from_numpy(x), approximate="tanh").numpy()
+    np.testing.assert_allclose(oracle.gelu_tanh(x), ref, rtol=0, atol=1e-15)
+    assert oracle.gelu_tanh(np.array([0.0]))[0] == 0.0
+    assert abs(oracle.gelu_tanh(np.array([30.0]))[0] - 30.0) < 1e-12
+    assert abs(oracle.gelu_tanh(np.array([-30.0]))[0]) < 1e-12
+
+
+def test_cross_correlation_orientation_on_2x2x2():
+    """Impulse at voxel (0,0,0) of a 2x2x2 volume (d = 1 grid, T = 2): with
+    cross-correlation and zero padding p = 1, output (t,i,j) equals the tap
+    w[1-t][1-i][1-j]."""
+    w = np.array([100 * a + 10 * b + c for a in range(3) for b in range(3) for c in range(3)],
+                 dtype=np.float32)
+    weights = np.concatenate([w, np.zeros(1, np.float32)])
+    planes = np.zeros((1, 1, 2, 2, 2))
+    planes[0, 0, 0, 0, 0] = 1.0
+    y = oracle.forward(1, 2, planes, [(1, 1, 3, NONE)], weights, bf16=False)[0, 0]
+    for t in range(2):
+        for i in range(2):
+            for j in range(2):
+                assert y[t, i, j] == 100 * (1 - t) + 10 * (1 - i) + (1 - j)
+
+
+def test_all_ones_on_2x2x2():
+    """All-ones input and weights on a 2x2x2 volume: every voxel sees all 8
+    voxels within its 3x3x3 window, so y = 8 * c_in + b."""
+    ci, co = 2, 3
+    weights = np.concatenate([np.ones(co * ci * 27, np.float32), np.array([0.5, -1.0, 2.0], np.float32)])
+    y = oracle.forward(1, 2, np.ones((1, ci, 2, 2, 2)), [(ci, co, 3, NONE)], weights, bf16=False)[0]
+    for o, b in enumerate([0.5, -1.0, 2.0]):
+        assert (y[o] == 8 * ci + b).all()
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+@pytest.mark.parametrize("d,T,n_hidden,width,B", [
+    (5, 5, 4, 32, 2),      # workload 1 shape
+    (9, 9, 6, 64, 2),      # workload 2 shape
+    (13, 13, 2, 16, 2),    # workload 3 grid, reduced network
+    (25, 25, 1, 8, 1),     # workload 4 grid, reduced network
+    (31, 31, 1, 8, 1),     # workload 5 grid, reduced network
+    (3, 1, 3, 8, 3),       # single round
+])
+def test_forward_matches_torch_conv3d(bf16, d, T, n_hidden, width, B):
+    rng = np.random.default_rng(d * 1000 + T * 10 + n_hidden)
+    layers = workload.layer_spec(n_hidden, width)
+    weights = workload.he_normal_weights(layers, seed=d + T)
+    planes = random_planes(rng, B, 2, T, d + 1, density=0.05)
+    got = oracle.forward(d, T, planes, layers, weights, bf16=bf16)
+    ref = torch_forward(planes, layers, weights, bf16)
+    np.testing.assert_allclose(got, ref, rtol=0, atol=1e-9 if not bf16 else 1e-6)
+
+
+def test_forward_relu_matches_torch():
+    rng = np.random.default_rng(3)
+    layers = workload.layer_spec(3, 16, act=RELU)
+    weights = workload.he_normal_weights(layers, seed=3)
+    planes = random_planes(rng, 2, 2, 4, 6)
+    for bf16 in (False, True):
+        np.testing.assert_allclose(oracle.forward(5, 4, planes, layers, weights, bf16),
+                                   torch_forward(planes, layers, weights, bf16), rtol=0, atol=1e-6)
+
+
+@pytest.mark.parametrize("n_hidden", [1, 3, 4])
+def test_impulse_response_is_receptive_field_cube(n_hidden):
+    """With zero biases (GELU(0) = 0) an impulse reaches exactly the voxels
+    within (R-1)/2 of it in t, i and j, R = 1 + sum(k - 1) (Eq.
+    ReceptiveFieldFormula; the 1x1x1 head adds nothing)."""
+    d, T = 13, 13
+    layers = workload.layer_spec(n_hidden, 8)
+    weights = workload.he_normal_weights(layers, seed=11, bias_std=0.0)
+    planes = np.zeros((1, 2, T, d + 1, d + 1))
+    c = (6, 7, 5)
+    planes[0, 1, c[0], c[1], c[2]] = 1.0
+    y = oracle.forward(d, T, planes, layers, weights, bf16=False)[0]
+    R = 1 + sum(k - 1 for (_, _, k, _) in layers)
+    h = (R - 1) // 2
+    support = (np.abs(y).max(axis=0) > 0)
+    tt, ii, jj = np.meshgrid(np.arange(T), np.arange(d + 1), np.arange(d + 1), indexing="ij")
+    cube = (np.abs(tt - c[0]) <= h) & (np.abs(ii - c[1]) <= h) & (np.abs(jj - c[2]) <= h)
+    np.testing.assert_array_equal(support, cube)
+
+
+def test_translation_equivariance_in_the_bulk():
+    """Shifting the input by (1,1,1) shifts the output wherever the receptive
+    field stays inside the volume in both positions."""
+    d, T = 13, 12
+    H = d + 1
+    layers = workload.layer_spec(2, 8)
+    weights = workload.he_normal_weights(layers, seed=5)
+    rng = np.random.default_rng(5)
+    x = np.zeros((1, 2, T, H, H))
+    x[0, :, 2:T - 3, 2:H - 3, 2:H - 3] = rng.random((2, T - 5, H - 5, H - 5)) < 0.2
+    xs = np.zeros_like(x)
+    xs[0, :, 1:, 1:, 1:] = x[0, :, :-1, :-1, :-1]
+    y = oracle.forward(d, T, x, layers, weights, bf16=False)[0]
+    ys = oracle.forward(d, T, xs, layers, weights, bf16=False)[0]
+    h = 2  # (R - 1) / 2 for two 3x3x3 layers
+    sl = (slice(None), slice(h, T - 1 - h), slice(h, H - 1 - h), slice(h, H - 1 - h))
+    sl1 = (slice(None), slice(h + 1, T - h), slice(h + 1, H - h), slice(h + 1, H - h))
+    np.testing.assert_allclose(ys[sl1], y[sl], rtol=0, atol=1e-12)
+
+
+def test_linearity_without_activation():
+    d, T = 5, 4
+    layers = [(2, 8, 3, NONE), (8, 8, 3, NONE), (8, 4, 1, NONE)]
+    weights = workload.he_normal_weights(layers, seed=9, bias_std=0.0)
+    rng = np.random.default_rng(9)
+    a = rng.standard_normal((1, 2, T, d + 1, d + 1))
+    b = rng.standard_normal((1, 2, T, d + 1, d + 1))
+    fa, fb = (oracle.forward(d, T, v, layers, weights, False) for v in (a, b))
+    fab = oracle.forward(d, T, 2.5 * a - b, layers, weights, False)
+    np.testing.assert_allclose(fab, 2.5 * fa - fb, rtol=0, atol=1e-10)
+
+
+def _param_rows(golden_dir):
+    rows = []
+    for line in open(golden_dir + "/param_counts.txt"):
+        if line.startswith("#") or not line.strip():
+            continue
+        m, filt, ks, printed = line.split()
+        rows.append((int(m), [int(v) for v in filt.split(",")], [int(v) for v in ks.split(",")], int(printed)))
+    return rows
+
+
+def test_parameter_counts_of_paper_models(golden_dir):
+    """Table models: the count of the layer list (4 input channels, a bias
+    per filter) reproduces the printed num_params of Models 2-5 exactly; Model
+    1's printed 912,272 is one digit off its layer list's 912,772."""
+    for model, filt, ks, printed in _param_rows(golden_dir):
+        layers, ci = [], 4
+        for f, k in zip(filt, ks):
+            layers.append((ci, f, k, GELU))
+            ci = f
+        n = oracle.weight_count(layers)
+        if model == 1:
+            assert n == 912772 and printed == 912272
+        else:
+            assert n == printed

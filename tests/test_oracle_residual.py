@@ -1,0 +1,175 @@
+"""Pins of the oracle's threshold, flip packing and residual (Sec. III.B.5,
+Eqs. ZcorreJK..SynZCorrJK, SXJK, SZJK, Resk1X..ReskG1Z) and of the workload
+generator's detector events (Sec. III.B.1)."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2604_12841_amd import workload
+
+CASES = [(3, 1, 4, 0.05), (5, 5, 16, 0.05), (9, 9, 8, 0.02), (13, 13, 4, 0.01)]
+
+
+def _logits_from_flip_bits(d, T, fbits):
+    """Logits [B][4][T][H][H] that threshold to the given flip bits
+    [B][T][3d^2-1] (+1 where set, -1 elsewhere)."""
+    B = fbits.shape[0]
+    H = d + 1
+    K = (d * d - 1) // 2
+    site_of, _ = oracle.stabilizer_order(d)
+    lg = -np.ones((B, 4, T, H, H))
+    for t in range(T):
+        f = fbits[:, t]
+        z = f[:, :d * d].reshape(B, d, d)
+        x = f[:, d * d:2 * d * d].reshape(B, d, d)
+        lg[:, 0, t, :d, :d] = np.where(z, 1.0, -1.0)
+        lg[:, 1, t, :d, :d] = np.where(x, 1.0, -1.0)
+        for n in range(2 * K):
+            i, j = divmod(int(site_of[n]), H)
+            ch = 2 if n < K else 3
+            lg[:, ch, t, i, j] = np.where(f[:, 2 * d * d + n], 1.0, -1.0)
+    return lg
+
+
+@pytest.mark.parametrize("d,T,B,p", CASES)
+def test_generator_cumulative_equals_differential(d, T, B, p):
+    """Detectors from the cumulative outcomes s(t) equal the differential form
+    D(t) = H e(t) ^ m(t) ^ m(t-1) (Sec. III.B.1 with s(-1) = 0)."""
+    noise = workload.sample_noise(d, T, B, p, p, seed=d + T)
+    det = workload.detectors_from_noise(d, noise)
+    hx, hz = workload.check_matrices(d)
+    ez = noise["e_z"].reshape(B, T, d * d).astype(np.int64)
+    ex = noise["e_x"].reshape(B, T, d * d).astype(np.int64)
+    mx, mz = noise["m_x"].astype(np.int64), noise["m_z"].astype(np.int64)
+    pad = lambda m: np.concatenate([np.zeros_like(m[:, :1]), m[:, :-1]], axis=1)
+    dx = (ez @ hx.T.astype(np.int64)) % 2 ^ mx ^ pad(mx)
+    dz = (ex @ hz.T.astype(np.int64)) % 2 ^ mz ^ pad(mz)
+    np.testing.assert_array_equal(det, np.concatenate([dx, dz], axis=2))
+
+
+@pytest.mark.parametrize("d,T,B,p", CASES)
+def test_ground_truth_flips_give_zero_residual(d, T, B, p):
+    """Applying the sampled errors themselves as corrections cancels every
+    term of Eqs. Resk1X..ReskG1Z: the residual is identically zero."""
+    det, noise = workload.make_inputs(d, T, B, p, p, seed=100 + d)
+    gt = workload.ground_truth_flips(d, noise)
+    flips = workload.pack_rows(gt.reshape(B, -1))
+    res = oracle.residual_from_flips(d, T, det, flips)
+    assert not res.any()
+    # the same through thresholded logits
+    f2, r2 = oracle.flips_residual(d, T, _logits_from_flip_bits(d, T, gt), det)
+    np.testing.assert_array_equal(f2, flips)
+    assert not r2.any()
+    assert det.any()  # the case is not vacuous
+
+
+@pytest.mark.parametrize("d,T,B,p", CASES)
+def test_zero_flips_leave_detectors(d, T, B, p):
+    det, _ = workload.make_inputs(d, T, B, p, p, seed=200 + d)
+    lg = -np.abs(np.random.default_rng(d).standard_normal((B, 4, T, d + 1, d + 1))) - 1e-3
+    flips, res = oracle.flips_residual(d, T, lg, det)
+    assert not flips.any()
+    np.testing.assert_array_equal(res, det)
+
+
+def test_logit_zero_is_no_flip():
+    d, T = 3, 2
+    det = np.zeros((1, oracle.det_words(d, T)), dtype=np.uint64)
+    flips, res = oracle.flips_residual(d, T, np.zeros((1, 4, T, d + 1, d + 1)), det)
+    assert not flips.any() and not res.any()
+
+
+@pytest.mark.parametrize("d,T,B,p", CASES[:3])
+def test_residual_xor_linearity(d, T, B, p):
+    """res(f ^ g) = res(f) ^ res(g) ^ det: the residual is affine in the flips."""
+    det, _ = workload.make_inputs(d, T, B, p, p, seed=300 + d)
+    rng = np.random.default_rng(d)
+    nb = T * (3 * d * d - 1)
+    f = workload.pack_rows((rng.random((B, nb)) < 0.1).astype(np.uint8))
+    g = workload.pack_rows((rng.random((B, nb)) < 0.1).astype(np.uint8))
+    rf = oracle.residual_from_flips(d, T, det, f)
+    rg = oracle.residual_from_flips(d, T, det, g)
+    rfg = oracle.residual_from_flips(d, T, det, f ^ g)
+    np.testing.assert_array_equal(rfg, rf ^ rg ^ det)
+
+
+@pytest.mark.parametrize("d", [3, 5, 7])
+def test_single_data_flip_toggles_its_plaquettes(d):
+    """One Z correction on data qubit (r, c) in round t toggles exactly the
+    X-type residual bits of round t whose plaquettes contain (r, c): one for a
+    qubit on the top or bottom row, two otherwise; an X correction likewise
+    toggles one (left/right column) or two Z-type bits."""
+    T = 3
+    S = d * d - 1
+    K = S // 2
+    det = np.zeros((1, oracle.det_words(d, T)), dtype=np.uint64)
+    nb = T * (3 * d * d - 1)
+    for t in range(T):
+        for r in range(d):
+            for c in range(d):
+                for typ in (0, 1):
+                    bits = np.zeros((1, nb), dtype=np.uint8)
+                    bits[0, t * (3 * d * d - 1) + typ * d * d + r * d + c] = 1
+                    res = oracle.residual_from_flips(d, T, det, workload.pack_rows(bits))
+                    rb = workload.unpack_rows(res, T * S)[0].reshape(T, S)
+                    assert not np.delete(rb, t, axis=0).any()
+                    if typ == 0:
+                        assert not rb[t, K:].any()
+                        expect = 1 if r in (0, d - 1) else 2
+                        assert rb[t, :K].sum() == expect
+                    else:
+                        assert not rb[t, :K].any()
+                        expect = 1 if c in (0, d - 1) else 2
+                        assert rb[t, K:].sum() == expect
+
+
+@pytest.mark.parametrize("d", [3, 5])
+def test_measurement_flip_toggles_two_rounds(d):
+    """A timelike correction on stabilizer n in round t flips its outcome in
+    rounds t and t+1, so the residual changes at (t, n) and (t+1, n); in the
+    last round only at (t, n)."""
+    T = 4
+    S = d * d - 1
+    det = np.zeros((1, oracle.det_words(d, T)), dtype=np.uint64)
+    nb = T * (3 * d * d - 1)
+    for t in range(T):
+        for n in range(S):
+            bits = np.zeros((1, nb), dtype=np.uint8)
+            bits[0, t * (3 * d * d - 1) + 2 * d * d + n] = 1
+            res = oracle.residual_from_flips(d, T, det, workload.pack_rows(bits))
+            rb = workload.unpack_rows(res, T * S)[0].reshape(T, S)
+            expect = np.zeros((T, S), dtype=np.uint8)
+            expect[t, n] = 1
+            if t + 1 < T:
+                expect[t + 1, n] = 1
+            np.testing.assert_array_equal(rb, expect)
+
+
+def test_flip_packing_positions():
+    """Each channel is read only where it is defined (data qubits for the Z/X
+    corrections, X sites for channel 2, Z sites for channel 3) and lands at the
+    compact flip index of the ABI."""
+    d, T = 5, 2
+    H = d + 1
+    kind = oracle.site_kind(d)
+    _, index_of = oracle.stabilizer_order(d)
+    K = (d * d - 1) // 2
+    det = np.zeros((1, oracle.det_words(d, T)), dtype=np.uint64)
+    nb = T * (3 * d * d - 1)
+    for ch in range(4):
+        for t in range(T):
+            for i in range(H):
+                for j in range(H):
+                    lg = -np.ones((1, 4, T, H, H))
+                    lg[0, ch, t, i, j] = 1.0
+                    flips, _ = oracle.flips_residual(d, T, lg, det)
+                    got = np.nonzero(workload.unpack_rows(flips, nb)[0])[0].tolist()
+                    base = t * (3 * d * d - 1)
+                    if ch < 2:
+                        expect = [base + ch * d * d + i * d + j] if (i < d and j < d) else []
+                    else:
+                        ok = kind[i, j] == ch - 1
+                        expect = [base + 2 * d * d + index_of[i * H + j]] if ok else []
+                        if ok:
+                            assert (index_of[i * H + j] < K) == (ch == 2)
+                    assert got == expect
