@@ -1,0 +1,150 @@
+"""Throughput of the pre-decoder hot path on one MI355X.
+
+A step is one predecoder_run over one batch: unpack -> 8 conv3d layers
+(bias + GELU fused) -> 1x1x1 head + threshold -> residual + bit repack, for
+the d=13, T=13, batch-4096 workload (8 hidden layers of 128 channels, bf16
+operands with fp32 accumulation, phenomenological noise p=q=0.003).  Inputs
+are resident in HBM before the timed region.
+
+Prints one JSON line: rounds/s (= batch * T / step time), us/round, the
+roofline of the dominant kernel (a hidden 128->128 conv layer, MFMA-bound,
+algorithmic FLOPs / its mean HIP-event duration) and the CPU oracle timed on a
+bounded sample of the same workload.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def flops_per_sample(layers, d, T):
+    V = T * (d + 1) ** 2
+    return sum(2 * ci * co * k ** 3 for (ci, co, k, _a) in layers) * V
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", type=int, default=3, help="workload id (1..5)")
+    ap.add_argument("--batch", type=int, default=None)
+    ap.add_argument("--stage-iters", type=int, default=5)
+    ap.add_argument("--cpu-samples", type=int, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the path is data-parallel over independent volumes and "
+              "this build runs on a single MI355X; --gpus %d is not supported" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2604_12841_amd as pdx
+    from paper_2604_12841_amd import workload
+
+    cfg = workload.CONFIGS[args.workload]
+    d, T = cfg["d"], cfg["T"]
+    B = args.batch or cfg["batch"]
+    layers = workload.config_layers(args.workload)
+    weights = workload.config_weights(args.workload)
+    det, _ = workload.config_inputs(args.workload, B)
+
+    torch.cuda.set_device(0)
+    pre = pdx.Predecoder(weights, d, T, layers, cfg["dtype"], max_batch=B)
+    ddet = torch.from_numpy(det.view(np.int64)).cuda()
+    flips = torch.empty((B, pre.flip_words), dtype=torch.int64, device="cuda")
+    res = torch.empty((B, pre.det_words), dtype=torch.int64, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    for _ in range(args.warmup):
+        pre.run(ddet, flips, res, stream=stream)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        pre.run(ddet, flips, res, stream=stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    print("step %.3f ms" % ms, file=sys.stderr, flush=True)
+
+    # Per-stage HIP-event times on the same stream (unpack, each layer, head, residual).
+    stages = pre.stage_times(ddet, flips, res, args.stage_iters, stream=stream)
+    n = len(layers)
+    hidden = [i for i in range(1, n - 1) if layers[i][0] == layers[i][1]]
+    conv_ms = float(np.mean([stages[1 + i] for i in hidden]))
+    ci, co = layers[hidden[0]][0], layers[hidden[0]][1]
+    V = T * (d + 1) ** 2
+    conv_flops = 2.0 * ci * co * 27 * V * B
+    achieved = conv_flops / (conv_ms * 1e-3) / 1e12
+    print("stages ms:", ["%.3f" % s for s in stages], file=sys.stderr, flush=True)
+
+    total_flops = flops_per_sample(layers, d, T) * B
+    rounds = B * T
+    out = {
+        "metric": "syndrome rounds/sec and us/round (pre-decode+residual) at d=13,T=13; MFMA %",
+        "value": rounds / (ms * 1e-3),
+        "unit": "rounds/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "us_per_round": ms * 1e3 / rounds,
+        "mfma_frac_end_to_end": total_flops / (ms * 1e-3) / (PEAK_BF16_TFLOPS * 1e12),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if cfg["dtype"] == "bf16" else "f32",
+        "data": "synthetic (seeded phenomenological noise, He-normal random weights)",
+        "config": {
+            "workload": "rotated surface code d=%d, T=%d rounds, batch %d; %d conv3d 3x3x3 layers x %d "
+                        "channels + 1x1x1 head, %s operands / fp32 accumulate; p=q=%g"
+                        % (d, T, B, cfg["n_hidden"], cfg["width"], cfg["dtype"], cfg["p"]),
+            "d": d, "T": T, "batch": B, "layers": cfg["n_hidden"], "width": cfg["width"],
+        },
+        "stage_ms": {"unpack": stages[0],
+                     **{"layer%d" % (i + 1): stages[1 + i] for i in range(n - 1)},
+                     "head_threshold": stages[n], "residual_repack": stages[n + 1]},
+        "roofline": {
+            "kernel": "conv3d 3x3x3 %d->%d implicit GEMM (bf16 MFMA) + bias/GELU epilogue" % (ci, co),
+            "bound": "mfma",
+            "achieved": achieved,
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": achieved / PEAK_BF16_TFLOPS,
+            "traffic": None,
+        },
+    }
+
+    if not args.no_cpu_baseline:
+        import oracle
+        ns = args.cpu_samples or {1: 64, 2: 64, 3: 8, 4: 1, 5: 1}[args.workload]
+        ns = min(ns, B)
+        oracle.build()
+        oracle.unpack(d, T, det[:1])  # load the library outside the timed region
+        t0 = time.perf_counter()
+        oracle.run(d, T, det[:ns], layers, weights, bf16=(cfg["dtype"] == "bf16"))
+        dt = time.perf_counter() - t0
+        cores = int(os.environ.get("OMP_NUM_THREADS", 0)) or len(os.sched_getaffinity(0))
+        out["cpu_baseline"] = {
+            "value": ns * T / dt, "unit": "rounds/s", "cores": cores, "kind": "oracle",
+            "sample": "%d of the %d samples (%.1f s, fp64 oracle with bf16 rounding points, "
+                      "OpenMP over samples x output channels)" % (ns, B, dt),
+        }
+    pre.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

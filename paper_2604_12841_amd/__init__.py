@@ -1,0 +1,178 @@
+"""MI355X (gfx950) pre-decoder for the rotated surface code (arXiv 2604.12841).
+
+Thin ctypes binding over the C ABI in include/predecoder.h: it only marshals
+arguments.  Every step of the path (unpack, conv layers, head, threshold,
+residual, bit repack) runs in the HIP kernels of libpredecoder.so, which is
+built in-tree by ``paper_2604_12841_amd.build``.  There is no CPU fallback:
+if the library is missing, loading it raises.
+
+Device buffers are torch tensors on the GPU (torch is used only for device
+memory and streams); streams are passed as their raw hipStream_t handles.
+"""
+import ctypes
+import os
+
+__all__ = ["Predecoder", "PredecoderError", "lib", "det_words", "flip_words", "weight_count",
+           "status_string", "ACT_NONE", "ACT_GELU_TANH", "ACT_RELU", "DTYPE_FP32", "DTYPE_BF16",
+           "LIB_PATH", "EXPORTS"]
+
+ACT_NONE, ACT_GELU_TANH, ACT_RELU = 0, 1, 2
+DTYPE_FP32, DTYPE_BF16 = 0, 1
+PD_OK, PD_ERR_INVALID_ARG, PD_ERR_UNSUPPORTED, PD_ERR_OUT_OF_MEMORY, PD_ERR_DEVICE = range(5)
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpredecoder.so")
+
+# Every symbol declared in include/predecoder.h.
+EXPORTS = ("predecoder_create", "predecoder_run", "predecoder_residual", "predecoder_unpack",
+           "predecoder_num_stages", "predecoder_stage_times", "predecoder_destroy",
+           "predecoder_status_string", "predecoder_det_words", "predecoder_flip_words",
+           "predecoder_weight_count")
+
+
+class PredecoderError(RuntimeError):
+    def __init__(self, status, what):
+        super().__init__("%s: %s (status %d)" % (what, status_string(status), status))
+        self.status = status
+
+
+class Layer(ctypes.Structure):
+    _fields_ = [("c_in", ctypes.c_int32), ("c_out", ctypes.c_int32), ("k", ctypes.c_int32),
+                ("act", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libpredecoder.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libpredecoder.so is not built: run paper_2604_12841_amd/build.py")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+        LP = ctypes.POINTER(Layer)
+        L.predecoder_create.argtypes = [vp, sz, i32, i32, LP, i32, i32, i32, ctypes.POINTER(vp)]
+        L.predecoder_create.restype = i32
+        L.predecoder_run.argtypes = [vp, vp, vp, i32, vp, vp, vp]
+        L.predecoder_run.restype = i32
+        L.predecoder_residual.argtypes = [vp, vp, vp, vp, i32, vp]
+        L.predecoder_residual.restype = i32
+        L.predecoder_unpack.argtypes = [vp, vp, vp, i32, vp]
+        L.predecoder_unpack.restype = i32
+        L.predecoder_num_stages.argtypes = [vp]
+        L.predecoder_num_stages.restype = i32
+        L.predecoder_stage_times.argtypes = [vp, vp, vp, i32, vp, vp, i32, ctypes.POINTER(ctypes.c_float)]
+        L.predecoder_stage_times.restype = i32
+        L.predecoder_destroy.argtypes = [vp]
+        L.predecoder_destroy.restype = None
+        L.predecoder_status_string.argtypes = [i32]
+        L.predecoder_status_string.restype = ctypes.c_char_p
+        L.predecoder_det_words.argtypes = [i32, i32]
+        L.predecoder_det_words.restype = i64
+        L.predecoder_flip_words.argtypes = [i32, i32]
+        L.predecoder_flip_words.restype = i64
+        L.predecoder_weight_count.argtypes = [LP, i32]
+        L.predecoder_weight_count.restype = sz
+        _lib = L
+    return _lib
+
+
+def status_string(status):
+    return lib().predecoder_status_string(int(status)).decode()
+
+
+def det_words(d, T):
+    return int(lib().predecoder_det_words(d, T))
+
+
+def flip_words(d, T):
+    return int(lib().predecoder_flip_words(d, T))
+
+
+def _layers(layers):
+    arr = (Layer * len(layers))()
+    for i, l in enumerate(layers):
+        arr[i] = Layer(*[int(v) for v in l])
+    return arr
+
+
+def weight_count(layers):
+    return int(lib().predecoder_weight_count(_layers(layers), len(layers)))
+
+
+def _ptr(t):
+    """Raw device pointer of a tensor (or None)."""
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("device buffers must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+class Predecoder:
+    """One pre-decoder handle: weights, workspace and tables for (d, T, max_batch)."""
+
+    def __init__(self, weights, d, T, layers, dtype="bf16", max_batch=1):
+        import numpy as np
+        w = np.ascontiguousarray(np.asarray(weights, dtype=np.float32))
+        self.d, self.T, self.layers, self.max_batch = d, T, [tuple(l) for l in layers], max_batch
+        self.dtype = DTYPE_BF16 if dtype in ("bf16", DTYPE_BF16) else DTYPE_FP32
+        self.det_words = det_words(d, T)
+        self.flip_words = flip_words(d, T)
+        h = ctypes.c_void_p()
+        st = lib().predecoder_create(w.ctypes.data_as(ctypes.c_void_p), w.size, d, T, _layers(layers),
+                                     len(layers), self.dtype, max_batch, ctypes.byref(h))
+        if st != PD_OK:
+            raise PredecoderError(st, "predecoder_create")
+        self._h = h
+
+    def _check(self, st, what):
+        if st != PD_OK:
+            raise PredecoderError(st, what)
+
+    def run(self, det, flips, residual, logits=None, batch=None, stream=None):
+        """det [B][W_det] uint64-valued int64 tensor -> flips [B][W_flip], residual [B][W_det] (in place)."""
+        batch = det.shape[0] if batch is None else batch
+        self._check(lib().predecoder_run(self._h, _stream(stream), _ptr(det), batch, _ptr(flips),
+                                         _ptr(residual), _ptr(logits)), "predecoder_run")
+
+    def residual(self, det, flips, residual, batch=None, stream=None):
+        batch = det.shape[0] if batch is None else batch
+        self._check(lib().predecoder_residual(self._h, _stream(stream), _ptr(det), _ptr(flips), batch,
+                                              _ptr(residual)), "predecoder_residual")
+
+    def unpack(self, det, planes, batch=None, stream=None):
+        batch = det.shape[0] if batch is None else batch
+        self._check(lib().predecoder_unpack(self._h, _stream(stream), _ptr(det), batch, _ptr(planes)),
+                    "predecoder_unpack")
+
+    @property
+    def num_stages(self):
+        return int(lib().predecoder_num_stages(self._h))
+
+    def stage_times(self, det, flips, residual, n_iter, batch=None, stream=None):
+        """Mean milliseconds of each stage over n_iter runs (blocks until done)."""
+        batch = det.shape[0] if batch is None else batch
+        out = (ctypes.c_float * self.num_stages)()
+        self._check(lib().predecoder_stage_times(self._h, _stream(stream), _ptr(det), batch, _ptr(flips),
+                                                 _ptr(residual), n_iter, out), "predecoder_stage_times")
+        return list(out)
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().predecoder_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,575 @@
+// api.hip -- host side of the C ABI declared in include/predecoder.h.
+//
+// create: validates the arguments on the host (no device call before that),
+// builds the GPU-side geometry tables, plans the conv tiling, reorders the
+// weights into MFMA fragment order (rounding to bf16 with round-to-nearest-
+// even for the bf16 path), allocates the zero-halo activation buffers for
+// max_batch samples and clears them once.
+// run: enqueues unpack -> conv layers -> head -> residual/repack on the
+// caller's stream and returns; it never synchronises.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "../../include/predecoder.h"
+#include "internal.h"
+
+using pd::Geom;
+using pd::Tiling;
+
+struct pd_predecoder {
+  Geom g;
+  int dtype = 0;
+  int max_batch = 0;
+  int device = 0;
+  std::vector<pd_layer> layers;
+  Tiling tiling{};               // shared by every 3x3x3 layer (bf16 path)
+  void* planes = nullptr;        // [max_batch * S][2]
+  void* act[2] = {nullptr, nullptr};  // [max_batch * S][cmax]
+  uint8_t* nib = nullptr;        // [max_batch][T][H][H] flip nibbles
+  int32_t* tables = nullptr;
+  std::vector<void*> wdev;       // per conv layer: fragments (bf16) or [tap][ci][co] (fp32)
+  std::vector<float*> bdev;      // per conv layer: bias fp32
+  float* head_w = nullptr;       // [4][c_in] fp32 (bf16-valued on the bf16 path)
+  float* head_b = nullptr;       // [4]
+  int cmax = 0;
+};
+
+namespace {
+
+const int kMaxD = 63;
+const int kMaxT = 1023;
+
+bool layer_chain_ok(const pd_layer* l, int n) {
+  if (n < 1) return false;
+  if (l[0].c_in != 2) return false;
+  if (l[n - 1].c_out != 4) return false;
+  if (l[n - 1].act != PD_ACT_NONE) return false;
+  for (int i = 0; i < n; ++i) {
+    if (l[i].c_in < 1 || l[i].c_out < 1) return false;
+    if (l[i].k < 1 || (l[i].k % 2) == 0) return false;
+    if (l[i].act < PD_ACT_NONE || l[i].act > PD_ACT_RELU) return false;
+    if (i > 0 && l[i].c_in != l[i - 1].c_out) return false;
+  }
+  return true;
+}
+
+Geom make_geom(int d, int T) {
+  Geom g;
+  g.d = d;
+  g.T = T;
+  g.H = d + 1;
+  g.Wp = d + 3;
+  g.P = g.Wp * g.Wp;
+  g.S = (long long)(T + 2) * g.P;
+  g.V = T * g.H * g.H;
+  g.nstab = d * d - 1;
+  g.K = g.nstab / 2;
+  g.nflip = 3 * d * d - 1;
+  g.Wd = ((long long)T * g.nstab + 63) / 64;
+  g.Wf = ((long long)T * g.nflip + 63) / 64;
+  return g;
+}
+
+// GPU-side geometry tables (see internal.h).  X site <=> (i+j) even and
+// 1 <= i <= d-1; Z site <=> (i+j) odd and 1 <= j <= d-1; plaquette (i, j)
+// acts on the data qubits (i-1..i, j-1..j) inside [0, d-1]^2.
+std::vector<int32_t> build_tables(const Geom& g) {
+  std::vector<int32_t> t(pd::tables_size(g), -1);
+  int32_t* site_of = t.data() + pd::tables_site_of(g);
+  int32_t* comp = t.data() + pd::tables_comp_of_site(g);
+  int32_t* supp = t.data() + pd::tables_supp(g);
+  const int d = g.d, H = g.H;
+  int n = 0;
+  for (int pass = 0; pass < 2; ++pass)
+    for (int i = 0; i <= d; ++i)
+      for (int j = 0; j <= d; ++j) {
+        bool x = ((i + j) & 1) == 0 && i >= 1 && i <= d - 1;
+        bool z = ((i + j) & 1) == 1 && j >= 1 && j <= d - 1;
+        if ((pass == 0 && x) || (pass == 1 && z)) {
+          site_of[n] = i * H + j;
+          comp[i * H + j] = n;
+          ++n;
+        }
+      }
+  for (int i = 0; i <= d; ++i)
+    for (int j = 0; j <= d; ++j) {
+      int q = 0;
+      for (int r = i - 1; r <= i; ++r)
+        for (int c = j - 1; c <= j; ++c)
+          if (r >= 0 && r < d && c >= 0 && c < d) supp[(i * H + j) * 4 + q++] = r * H + c;
+    }
+  return t;
+}
+
+// fp32 -> bf16 bits, round to nearest even on the fp32 bit pattern.
+uint16_t bf16_bits(float f) {
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x7fffffu)) return (uint16_t)((u >> 16) | 0x40);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+float bf16_value(float f) {
+  uint32_t u = (uint32_t)bf16_bits(f) << 16;
+  float r;
+  std::memcpy(&r, &u, 4);
+  return r;
+}
+
+// Tiling plan for the 3x3x3 layers: the candidate with the fewest MFMA rows
+// per sample whose double-buffered 32-channel staging fits in LDS.
+const int kMaxSpan = 1216;  // 2 * 1216 voxels * 64 B + row tables <= 160 KiB
+
+long long flat_span(const Geom& g, long long seg_len, long long nseg, int batch) {
+  // exact maximum staged span over all tiles of `batch` samples
+  long long best = 0, halo = g.P + g.Wp + 1;
+  long long tiles = (seg_len + pd::kTileRows - 1) / pd::kTileRows;
+  for (long long s = 0; s < nseg; ++s)
+    for (long long k = 0; k < tiles; ++k) {
+      long long u0 = s * seg_len + k * pd::kTileRows;
+      long long u1 = std::min(u0 + pd::kTileRows, std::min((s + 1) * seg_len, (long long)batch * g.V)) - 1;
+      if (u1 < u0) continue;
+      auto pidx = [&](long long u) {
+        long long b = u / g.V, v = u % g.V;
+        int HH = g.H * g.H;
+        int t = (int)(v / HH), r = (int)(v % HH);
+        return pd::padded_index(g, (int)b, t, r / g.H, r % g.H);
+      };
+      best = std::max(best, pidx(u1) - pidx(u0) + 2 * halo + 1);
+    }
+  return best;
+}
+
+Tiling plan_tiling(const Geom& g, int max_batch) {
+  Tiling best{};
+  long long best_rows = -1;
+  int best_span = 0;
+  auto consider = [&](const Tiling& t, long long rows_per_sample) {
+    if (t.span > kMaxSpan) return;
+    if (best_rows < 0 || rows_per_sample < best_rows ||
+        (rows_per_sample == best_rows && t.span < best_span)) {
+      best = t;
+      best_rows = rows_per_sample;
+      best_span = t.span;
+    }
+  };
+  // flat, tiles inside one sample
+  {
+    Tiling t{};
+    t.mode = 0;
+    t.seg_len = g.V;
+    t.tiles_per_seg = (g.V + pd::kTileRows - 1) / pd::kTileRows;
+    t.sa = g.P;
+    t.sb = g.Wp;
+    t.span = (int)std::min<long long>(flat_span(g, g.V, 1, 1), 1 << 30);
+    consider(t, (long long)t.tiles_per_seg * pd::kTileRows);
+  }
+  // flat across samples (rows per sample ~ V); the span bound covers any batch
+  if (max_batch > 1) {
+    Tiling t{};
+    t.mode = 0;
+    t.seg_len = -1;  // set per run to batch * V
+    t.tiles_per_seg = 0;
+    t.sa = g.P;
+    t.sb = g.Wp;
+    int nb = std::min(max_batch, 256);
+    t.span = (int)std::min<long long>(flat_span(g, (long long)nb * g.V, 1, nb), 1 << 30);
+    consider(t, (long long)g.V + 1);  // +1: prefer per-sample tiles at equal cost
+  }
+  // boxes
+  for (int BJ = 1; BJ <= std::min(g.H, 256); ++BJ)
+    for (int BI = 1; BI <= std::min(g.H, 256 / BJ); ++BI) {
+      int BT = std::min(g.T, 256 / (BI * BJ));
+      if (BT < 1) continue;
+      Tiling t{};
+      t.mode = 1;
+      t.BT = BT;
+      t.BI = BI;
+      t.BJ = BJ;
+      t.ntT = (g.T + BT - 1) / BT;
+      t.ntI = (g.H + BI - 1) / BI;
+      t.ntJ = (g.H + BJ - 1) / BJ;
+      t.sa = (BI + 2) * (BJ + 2);
+      t.sb = BJ + 2;
+      t.span = (BT + 2) * (BI + 2) * (BJ + 2);
+      consider(t, (long long)t.ntT * t.ntI * t.ntJ * pd::kTileRows);
+    }
+  return best;
+}
+
+void tiling_for_batch(Tiling* t, const Geom& g, int batch) {
+  if (t->mode == 0) {
+    if (t->seg_len < 0 || t->tiles_per_seg == 0) {
+      // flat across samples
+      t->seg_len = (long long)batch * g.V;
+      t->tiles_per_seg = (int)((t->seg_len + pd::kTileRows - 1) / pd::kTileRows);
+      t->ntiles = t->tiles_per_seg;
+    } else {
+      t->ntiles = (long long)batch * t->tiles_per_seg;
+    }
+  } else {
+    t->ntiles = (long long)batch * t->ntT * t->ntI * t->ntJ;
+  }
+}
+
+bool supported(const Geom& g, const pd_layer* l, int n, int dtype) {
+  if (g.d > kMaxD || g.T > kMaxT) return false;
+  if (n < 2) return false;  // at least one hidden 3x3x3 layer before the head
+  for (int i = 0; i < n - 1; ++i) {
+    if (l[i].k != 3) return false;
+    int co = l[i].c_out;
+    if (dtype == PD_DTYPE_BF16) {
+      if (co != 64 && co != 128) return false;
+    } else {
+      if (co % 8 != 0 || co > 128) return false;
+    }
+  }
+  if (l[n - 1].k != 1 || l[n - 1].c_in > 128) return false;
+  if (dtype == PD_DTYPE_BF16 && (l[n - 1].c_in % 8) != 0) return false;
+  return true;
+}
+
+template <typename T>
+pd_status dev_alloc(T** p, size_t bytes) {
+  *p = nullptr;
+  if (bytes == 0) bytes = 16;
+  hipError_t e = hipMalloc((void**)p, bytes);
+  if (e == hipErrorOutOfMemory || e == hipErrorMemoryAllocation) {
+    (void)hipGetLastError();
+    return PD_ERR_OUT_OF_MEMORY;
+  }
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return PD_ERR_DEVICE;
+  }
+  return PD_OK;
+}
+
+template <typename T>
+pd_status upload(T** p, const void* host, size_t bytes) {
+  pd_status s = dev_alloc(p, bytes);
+  if (s != PD_OK) return s;
+  if (hipMemcpy(*p, host, bytes, hipMemcpyHostToDevice) != hipSuccess) return PD_ERR_DEVICE;
+  return PD_OK;
+}
+
+void free_all(pd_predecoder* h) {
+  auto f = [](void* p) {
+    if (p) (void)hipFree(p);
+  };
+  f(h->planes);
+  f(h->act[0]);
+  f(h->act[1]);
+  f(h->nib);
+  f(h->tables);
+  for (void* p : h->wdev) f(p);
+  for (float* p : h->bdev) f(p);
+  f(h->head_w);
+  f(h->head_b);
+  h->planes = h->act[0] = h->act[1] = nullptr;
+  h->nib = nullptr;
+  h->tables = nullptr;
+  h->wdev.clear();
+  h->bdev.clear();
+  h->head_w = h->head_b = nullptr;
+}
+
+// bf16 B fragments for v_mfma_f32_32x32x16_bf16: lane l of fragment
+// (k-step, column block nb) holds B[k0 + 8 (l / 32) + e][32 nb + l % 32],
+// e = 0..7.  Layer 1 (c_in = 2): k = 2 * tap + ci over 4 k-steps (taps >= 27
+// are zero).  Hidden layers: [chunk of 32 c_in][tap][2 k-steps][nb] with
+// ci = 32 chunk + 16 ks + 8 (l / 32) + e.
+std::vector<uint16_t> conv_fragments(const float* w, int cin, int cout) {
+  const int nbt = cout / 32;
+  std::vector<uint16_t> f;
+  auto W = [&](int co, int ci, int tap) { return w[((size_t)co * cin + ci) * 27 + tap]; };
+  if (cin == 2) {
+    f.assign((size_t)4 * nbt * 64 * 8, 0);
+    for (int ks = 0; ks < 4; ++ks)
+      for (int nb = 0; nb < nbt; ++nb)
+        for (int l = 0; l < 64; ++l)
+          for (int e = 0; e < 8; ++e) {
+            int k = ks * 16 + 8 * (l / 32) + e;
+            int tap = k / 2, ci = k % 2, co = nb * 32 + l % 32;
+            f[(((size_t)ks * nbt + nb) * 64 + l) * 8 + e] = tap < 27 ? bf16_bits(W(co, ci, tap)) : 0;
+          }
+  } else {
+    const int nch = cin / 32;
+    f.assign((size_t)nch * 27 * 2 * nbt * 64 * 8, 0);
+    for (int c = 0; c < nch; ++c)
+      for (int tap = 0; tap < 27; ++tap)
+        for (int ks = 0; ks < 2; ++ks)
+          for (int nb = 0; nb < nbt; ++nb)
+            for (int l = 0; l < 64; ++l)
+              for (int e = 0; e < 8; ++e) {
+                int ci = c * 32 + ks * 16 + 8 * (l / 32) + e, co = nb * 32 + l % 32;
+                size_t idx = (((((size_t)c * 27 + tap) * 2 + ks) * nbt + nb) * 64 + l) * 8 + e;
+                f[idx] = bf16_bits(W(co, ci, tap));
+              }
+  }
+  return f;
+}
+
+pd_status check_launch(hipError_t e) {
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return PD_ERR_DEVICE;
+  }
+  return PD_OK;
+}
+
+// Enqueues the whole path.  ev (optional) receives one event record before
+// each stage and one after the last.
+pd_status enqueue_run(pd_predecoder* h, hipStream_t st, const uint64_t* det, int batch, uint64_t* flips,
+                      uint64_t* residual, float* logits, hipEvent_t* ev) {
+  const Geom& g = h->g;
+  const int fp32 = h->dtype == PD_DTYPE_FP32;
+  const int n = (int)h->layers.size();
+  int e = 0;
+  auto mark = [&]() -> pd_status {
+    if (ev && hipEventRecord(ev[e++], st) != hipSuccess) return PD_ERR_DEVICE;
+    return PD_OK;
+  };
+  pd_status s;
+  if ((s = mark()) != PD_OK) return s;
+  s = check_launch(pd::launch_unpack(g, h->tables + pd::tables_comp_of_site(g), det, batch, h->planes, 1,
+                                     fp32, st));
+  if (s != PD_OK) return s;
+  const void* x = h->planes;
+  Tiling tl = h->tiling;
+  tiling_for_batch(&tl, g, batch);
+  for (int l = 0; l < n - 1; ++l) {
+    if ((s = mark()) != PD_OK) return s;
+    void* y = h->act[l & 1];
+    const pd_layer& L = h->layers[l];
+    if (fp32)
+      s = check_launch(pd::launch_conv_fp32(g, L.c_in, L.c_out, L.act, (const float*)x, (float*)y,
+                                            (const float*)h->wdev[l], h->bdev[l], batch, st));
+    else
+      s = check_launch(pd::launch_conv_bf16(g, tl, L.c_in, L.c_out, L.act, x, y, h->wdev[l], h->bdev[l],
+                                            batch, st));
+    if (s != PD_OK) return s;
+    x = y;
+  }
+  if ((s = mark()) != PD_OK) return s;
+  s = check_launch(pd::launch_head(g, h->layers[n - 1].c_in, fp32, x, h->head_w, h->head_b, h->tables,
+                                   h->nib, logits, batch, st));
+  if (s != PD_OK) return s;
+  if ((s = mark()) != PD_OK) return s;
+  s = check_launch(pd::launch_residual_pack(g, h->tables, det, h->nib, flips, residual, batch, st));
+  if (s != PD_OK) return s;
+  return mark();
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* predecoder_status_string(pd_status s) {
+  switch (s) {
+    case PD_OK: return "ok";
+    case PD_ERR_INVALID_ARG: return "invalid argument";
+    case PD_ERR_UNSUPPORTED: return "unsupported shape";
+    case PD_ERR_OUT_OF_MEMORY: return "out of device memory";
+    case PD_ERR_DEVICE: return "device error";
+  }
+  return "unknown status";
+}
+
+int64_t predecoder_det_words(int32_t d, int32_t T) {
+  if (d < 1 || T < 1) return -1;
+  return ((int64_t)T * ((int64_t)d * d - 1) + 63) / 64;
+}
+
+int64_t predecoder_flip_words(int32_t d, int32_t T) {
+  if (d < 1 || T < 1) return -1;
+  return ((int64_t)T * (3 * (int64_t)d * d - 1) + 63) / 64;
+}
+
+size_t predecoder_weight_count(const pd_layer* layers, int32_t n_layers) {
+  if (!layers || n_layers < 1) return 0;
+  size_t n = 0;
+  for (int i = 0; i < n_layers; ++i) {
+    const pd_layer& l = layers[i];
+    if (l.c_in < 1 || l.c_out < 1 || l.k < 1) return 0;
+    n += (size_t)l.c_out * l.c_in * l.k * l.k * l.k + l.c_out;
+  }
+  return n;
+}
+
+int32_t predecoder_num_stages(const pd_predecoder* h) {
+  if (!h) return -1;
+  return (int32_t)h->layers.size() + 2;
+}
+
+pd_status predecoder_create(const float* weights, size_t n_weights, int32_t d, int32_t T,
+                            const pd_layer* layers, int32_t n_layers, int32_t dtype, int32_t max_batch,
+                            pd_predecoder** out) {
+  if (!out) return PD_ERR_INVALID_ARG;
+  *out = nullptr;
+  if (!weights || !layers) return PD_ERR_INVALID_ARG;
+  if (d < 3 || (d % 2) == 0 || T < 1) return PD_ERR_INVALID_ARG;
+  if (dtype != PD_DTYPE_FP32 && dtype != PD_DTYPE_BF16) return PD_ERR_INVALID_ARG;
+  if (max_batch < 1) return PD_ERR_INVALID_ARG;
+  if (!layer_chain_ok(layers, n_layers)) return PD_ERR_INVALID_ARG;
+  if (n_weights != predecoder_weight_count(layers, n_layers)) return PD_ERR_INVALID_ARG;
+  Geom g = make_geom(d, T);
+  if (!supported(g, layers, n_layers, dtype)) return PD_ERR_UNSUPPORTED;
+
+  int ndev = 0;
+  if (hipGetDeviceCount(&ndev) != hipSuccess || ndev < 1) {
+    (void)hipGetLastError();
+    return PD_ERR_DEVICE;
+  }
+  pd_predecoder* h = new (std::nothrow) pd_predecoder();
+  if (!h) return PD_ERR_OUT_OF_MEMORY;
+  h->g = g;
+  h->dtype = dtype;
+  h->max_batch = max_batch;
+  h->layers.assign(layers, layers + n_layers);
+  if (hipGetDevice(&h->device) != hipSuccess) {
+    delete h;
+    return PD_ERR_DEVICE;
+  }
+  int cmax = 2;
+  for (int i = 0; i < n_layers - 1; ++i) cmax = std::max(cmax, (int)layers[i].c_out);
+  h->cmax = cmax;
+  if (dtype == PD_DTYPE_BF16) {
+    h->tiling = plan_tiling(g, max_batch);
+    if (h->tiling.span <= 0 || h->tiling.span > kMaxSpan) {
+      delete h;
+      return PD_ERR_UNSUPPORTED;
+    }
+  }
+
+  pd_status s = PD_OK;
+  const size_t elem = dtype == PD_DTYPE_BF16 ? 2 : 4;
+  const size_t vox = (size_t)max_batch * (size_t)g.S;
+  auto fail = [&](pd_status st) {
+    free_all(h);
+    delete h;
+    return st;
+  };
+  if ((s = dev_alloc(&h->planes, vox * 2 * elem)) != PD_OK) return fail(s);
+  if ((s = dev_alloc(&h->act[0], vox * cmax * elem)) != PD_OK) return fail(s);
+  if ((s = dev_alloc(&h->act[1], vox * cmax * elem)) != PD_OK) return fail(s);
+  if ((s = dev_alloc(&h->nib, (size_t)max_batch * g.V)) != PD_OK) return fail(s);
+  std::vector<int32_t> tab = build_tables(g);
+  if ((s = upload(&h->tables, tab.data(), tab.size() * sizeof(int32_t))) != PD_OK) return fail(s);
+  if (hipMemset(h->planes, 0, vox * 2 * elem) != hipSuccess ||
+      hipMemset(h->act[0], 0, vox * cmax * elem) != hipSuccess ||
+      hipMemset(h->act[1], 0, vox * cmax * elem) != hipSuccess)
+    return fail(PD_ERR_DEVICE);
+
+  const float* src = weights;
+  for (int i = 0; i < n_layers; ++i) {
+    const pd_layer& L = layers[i];
+    const size_t nw = (size_t)L.c_out * L.c_in * L.k * L.k * L.k;
+    const float* w = src;
+    const float* b = src + nw;
+    src += nw + L.c_out;
+    if (i == n_layers - 1) {
+      std::vector<float> hw((size_t)4 * L.c_in);
+      for (int o = 0; o < 4; ++o)
+        for (int c = 0; c < L.c_in; ++c) {
+          float v = w[(size_t)o * L.c_in + c];
+          hw[(size_t)o * L.c_in + c] = dtype == PD_DTYPE_BF16 ? bf16_value(v) : v;
+        }
+      if ((s = upload(&h->head_w, hw.data(), hw.size() * 4)) != PD_OK) return fail(s);
+      if ((s = upload(&h->head_b, b, 4 * sizeof(float))) != PD_OK) return fail(s);
+      break;
+    }
+    void* wd = nullptr;
+    if (dtype == PD_DTYPE_BF16) {
+      std::vector<uint16_t> f = conv_fragments(w, L.c_in, L.c_out);
+      s = upload(&wd, f.data(), f.size() * 2);
+    } else {
+      std::vector<float> r((size_t)27 * L.c_in * L.c_out);
+      for (int co = 0; co < L.c_out; ++co)
+        for (int ci = 0; ci < L.c_in; ++ci)
+          for (int tap = 0; tap < 27; ++tap)
+            r[((size_t)tap * L.c_in + ci) * L.c_out + co] = w[((size_t)co * L.c_in + ci) * 27 + tap];
+      s = upload(&wd, r.data(), r.size() * 4);
+    }
+    h->wdev.push_back(wd);
+    if (s != PD_OK) return fail(s);
+    float* bd = nullptr;
+    s = upload(&bd, b, (size_t)L.c_out * 4);
+    h->bdev.push_back(bd);
+    if (s != PD_OK) return fail(s);
+  }
+  if (hipDeviceSynchronize() != hipSuccess) return fail(PD_ERR_DEVICE);
+  *out = h;
+  return PD_OK;
+}
+
+pd_status predecoder_run(pd_predecoder* h, void* hip_stream, const uint64_t* det, int32_t batch,
+                         uint64_t* flips, uint64_t* residual, float* logits) {
+  if (!h || !det || !flips || !residual) return PD_ERR_INVALID_ARG;
+  if (batch < 1 || batch > h->max_batch) return PD_ERR_INVALID_ARG;
+  return enqueue_run(h, (hipStream_t)hip_stream, det, batch, flips, residual, logits, nullptr);
+}
+
+pd_status predecoder_residual(pd_predecoder* h, void* hip_stream, const uint64_t* det,
+                              const uint64_t* flips, int32_t batch, uint64_t* residual) {
+  if (!h || !det || !flips || !residual) return PD_ERR_INVALID_ARG;
+  if (batch < 1 || batch > h->max_batch) return PD_ERR_INVALID_ARG;
+  return check_launch(
+      pd::launch_residual_from_flips(h->g, h->tables, det, flips, residual, batch, (hipStream_t)hip_stream));
+}
+
+pd_status predecoder_unpack(pd_predecoder* h, void* hip_stream, const uint64_t* det, int32_t batch,
+                            void* planes) {
+  if (!h || !det || !planes) return PD_ERR_INVALID_ARG;
+  if (batch < 1 || batch > h->max_batch) return PD_ERR_INVALID_ARG;
+  return check_launch(pd::launch_unpack(h->g, h->tables + pd::tables_comp_of_site(h->g), det, batch, planes, 0,
+                                        h->dtype == PD_DTYPE_FP32, (hipStream_t)hip_stream));
+}
+
+pd_status predecoder_stage_times(pd_predecoder* h, void* hip_stream, const uint64_t* det, int32_t batch,
+                                 uint64_t* flips, uint64_t* residual, int32_t n_iter, float* ms_per_stage) {
+  if (!h || !det || !flips || !residual || !ms_per_stage) return PD_ERR_INVALID_ARG;
+  if (batch < 1 || batch > h->max_batch || n_iter < 1 || n_iter > 100000) return PD_ERR_INVALID_ARG;
+  const int ns = predecoder_num_stages(h);
+  const int ne = ns + 1;
+  std::vector<hipEvent_t> ev((size_t)n_iter * ne, nullptr);
+  pd_status s = PD_OK;
+  for (auto& e : ev)
+    if (hipEventCreate(&e) != hipSuccess) {
+      s = PD_ERR_DEVICE;
+      break;
+    }
+  hipStream_t st = (hipStream_t)hip_stream;
+  for (int it = 0; it < n_iter && s == PD_OK; ++it)
+    s = enqueue_run(h, st, det, batch, flips, residual, nullptr, ev.data() + (size_t)it * ne);
+  if (s == PD_OK && hipStreamSynchronize(st) != hipSuccess) s = PD_ERR_DEVICE;
+  if (s == PD_OK) {
+    for (int k = 0; k < ns; ++k) ms_per_stage[k] = 0.0f;
+    for (int it = 0; it < n_iter && s == PD_OK; ++it)
+      for (int k = 0; k < ns; ++k) {
+        float ms = 0.0f;
+        if (hipEventElapsedTime(&ms, ev[(size_t)it * ne + k], ev[(size_t)it * ne + k + 1]) != hipSuccess) {
+          s = PD_ERR_DEVICE;
+          break;
+        }
+        ms_per_stage[k] += ms / n_iter;
+      }
+  }
+  for (auto& e : ev)
+    if (e) (void)hipEventDestroy(e);
+  (void)hipGetLastError();
+  return s;
+}
+
+void predecoder_destroy(pd_predecoder* h) {
+  if (!h) return;
+  (void)hipDeviceSynchronize();
+  free_all(h);
+  delete h;
+}
+
+}  // extern "C"

@@ -1,0 +1,87 @@
+// internal.h -- shared declarations between the C-ABI host code and the
+// gfx950 kernels of the pre-decoder.  Not installed; the public contract is
+// include/predecoder.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pd {
+
+// Padded activation layout (NTHWC with a one-voxel zero halo in t, i and j):
+//   voxel (b, t, i, j), 0 <= t < T, 0 <= i, j <= d, lives at padded index
+//   b * S + (t + 1) * P + (i + 1) * Wp + (j + 1),  Wp = d + 3, P = Wp^2,
+//   S = (T + 2) * P,
+// channels contiguous.  The halo is zeroed once at create and never written,
+// so a 3x3x3 tap is a pure index shift.
+struct Geom {
+  int d, T, H, Wp, P;
+  long long S;  // padded voxels per sample
+  int V;        // interior voxels per sample, T * H * H
+  int K;        // stabilizers of each type, (d^2 - 1) / 2
+  int nstab;    // d^2 - 1
+  int nflip;    // 3 d^2 - 1
+  long long Wd, Wf;  // packed words per sample
+};
+
+__host__ __device__ inline long long padded_index(const Geom& g, int b, int t, int i, int j) {
+  return (long long)b * g.S + (long long)(t + 1) * g.P + (long long)(i + 1) * g.Wp + (j + 1);
+}
+
+// Output-row tiling of one conv launch.  A tile is up to 256 output voxels:
+//  mode 0 (flat): 256 consecutive voxels of a segment of `seg_len` voxels in
+//    (b, t, i, j) order (seg_len = V keeps tiles inside one sample, B * V lets
+//    them cross samples); the staged input is the contiguous padded span
+//    from the first row's padded index - (P + Wp + 1) to the last row's
+//    + (P + Wp + 1).
+//  mode 1 (box): a BT x BI x BJ box of (t, i, j); the staged input is the
+//    (BT+2) x (BI+2) x (BJ+2) padded box around it.
+// In both modes the LDS voxel of row r for tap (dt, di, dj) in {0,1,2}^3 is
+// row_base(r) + dt * sa + di * sb + dj.
+struct Tiling {
+  int mode;
+  long long seg_len;
+  int tiles_per_seg;
+  int BT, BI, BJ, ntT, ntI, ntJ;
+  int sa, sb;
+  int span;      // staged voxels per tile (upper bound), sizes the LDS buffers
+  long long ntiles;
+};
+
+constexpr int kTileRows = 256;
+
+// Kernel launchers (all asynchronous on `stream`; return the launch error).
+hipError_t launch_unpack(const Geom& g, const int32_t* comp_of_site, const uint64_t* det, int batch,
+                         void* out, int out_padded, int fp32, hipStream_t stream);
+
+hipError_t launch_conv_bf16(const Geom& g, const Tiling& tl, int cin, int cout, int act,
+                            const void* x, void* y, const void* wfrag, const float* bias, int batch,
+                            hipStream_t stream);
+size_t conv_bf16_lds_bytes(int cin, int span);
+
+hipError_t launch_conv_fp32(const Geom& g, int cin, int cout, int act, const float* x, float* y,
+                            const float* w, const float* bias, int batch, hipStream_t stream);
+
+hipError_t launch_head(const Geom& g, int cin, int fp32, const void* x, const float* w_head,
+                       const float* b_head, const int32_t* tables, uint8_t* nib, float* logits,
+                       int batch, hipStream_t stream);
+
+hipError_t launch_residual_pack(const Geom& g, const int32_t* tables, const uint64_t* det,
+                                const uint8_t* nib, uint64_t* flips, uint64_t* residual, int batch,
+                                hipStream_t stream);
+
+hipError_t launch_residual_from_flips(const Geom& g, const int32_t* tables, const uint64_t* det,
+                                      const uint64_t* flips, uint64_t* residual, int batch,
+                                      hipStream_t stream);
+
+// Device tables (int32), one allocation, offsets in elements:
+//   [0, nstab)             site_of[n]: grid index i*H+j of compact stabilizer n
+//   [nstab, nstab+H*H)     comp_of_site[s]: compact index of site s, or -1
+//   [.., .. + 4*H*H)       supp[s][4]: grid indices of the data qubits of
+//                          plaquette s (data qubit (r,c) is grid site (r,c)), -1 pads
+__host__ __device__ inline int tables_site_of(const Geom&) { return 0; }
+__host__ __device__ inline int tables_comp_of_site(const Geom& g) { return g.nstab; }
+__host__ __device__ inline int tables_supp(const Geom& g) { return g.nstab + g.H * g.H; }
+__host__ __device__ inline int tables_size(const Geom& g) { return g.nstab + 5 * g.H * g.H; }
+
+}  // namespace pd

@@ -1,0 +1,121 @@
+"""Comparison of the GPU path with the CPU oracle (test helper).
+
+Parity rule: logits agree to a max abs error <= tol (2e-2 for bf16, 1e-4 for
+fp32); thresholded flips and residual bits agree exactly, except at sites
+whose oracle |logit| < tol ("excused": either outcome is within the
+tolerance).  A residual bit is excused when any of the flips it XORs in is.
+Excused counts are reported; non-excused mismatches must be 0.
+"""
+import functools
+
+import numpy as np
+
+import oracle
+from paper_2604_12841_amd import workload
+
+TOL = {"bf16": 2e-2, "fp32": 1e-4}
+
+
+@functools.lru_cache(maxsize=None)
+def flip_sites(d):
+    """(ch, i, j) of each compact flip index n in [0, 3d^2 - 1)."""
+    site_of, _ = oracle.stabilizer_order(d)
+    H = d + 1
+    K = (d * d - 1) // 2
+    out = [(0, r, c) for r in range(d) for c in range(d)]
+    out += [(1, r, c) for r in range(d) for c in range(d)]
+    for n in range(d * d - 1):
+        i, j = divmod(int(site_of[n]), H)
+        out.append((2 if n < K else 3, i, j))
+    return np.array(out, dtype=np.int64)
+
+
+@functools.lru_cache(maxsize=None)
+def residual_contributions(d):
+    """For each stabilizer n: (flip index of its measurement correction,
+    list of flip indices of the data corrections on its support)."""
+    site_of, _ = oracle.stabilizer_order(d)
+    H = d + 1
+    K = (d * d - 1) // 2
+    meas, data = [], []
+    for n in range(d * d - 1):
+        i, j = divmod(int(site_of[n]), H)
+        meas.append(2 * d * d + n)
+        ch = 0 if n < K else 1
+        sup = [ch * d * d + r * d + c for (r, c) in oracle.plaquette_support(d, i, j)]
+        data.append(sup + [-1] * (4 - len(sup)))
+    return np.array(meas), np.array(data)
+
+
+def excused_masks(d, T, logits, tol):
+    """(flip_excused [B][T*(3d^2-1)], residual_excused [B][T*(d^2-1)]) bool."""
+    fs = flip_sites(d)
+    B = logits.shape[0]
+    F = 3 * d * d - 1
+    S = d * d - 1
+    lf = logits[:, fs[:, 0][None, :].repeat(T, 0), np.arange(T)[:, None], fs[:, 1][None, :], fs[:, 2][None, :]]
+    fex = (np.abs(lf) < tol).reshape(B, T, F)
+    meas, data = residual_contributions(d)
+    rex = fex[:, :, meas].copy()
+    rex[:, 1:] |= fex[:, :-1, meas]
+    for q in range(4):
+        idx = data[:, q]
+        ok = idx >= 0
+        part = np.zeros((B, T, S), dtype=bool)
+        part[:, :, ok] = fex[:, :, idx[ok]]
+        rex |= part
+    return fex.reshape(B, T * F), rex.reshape(B, T * S)
+
+
+def compare(d, T, dtype, ref_logits, ref_flips, ref_res, got_flips, got_res, got_logits=None):
+    """Returns a dict of parity statistics (see module docstring)."""
+    tol = TOL[dtype]
+    B = ref_logits.shape[0]
+    F = T * (3 * d * d - 1)
+    S = T * (d * d - 1)
+    fex, rex = excused_masks(d, T, ref_logits, tol)
+    rf = workload.unpack_rows(ref_flips, F).astype(bool)
+    gf = workload.unpack_rows(got_flips, F).astype(bool)
+    rr = workload.unpack_rows(ref_res, S).astype(bool)
+    gr = workload.unpack_rows(got_res, S).astype(bool)
+    out = dict(
+        flip_mismatch=int(((rf != gf) & ~fex).sum()),
+        flip_excused=int(fex.sum()),
+        flip_excused_mismatch=int(((rf != gf) & fex).sum()),
+        res_mismatch=int(((rr != gr) & ~rex).sum()),
+        res_excused=int(rex.sum()),
+        flips_set=int(rf.sum()),
+        residual_set=int(rr.sum()),
+        bits=B * (F + S),
+        # padding bits beyond the last flip / residual bit must be zero
+        flip_padding_ok=bool(_padding_zero(got_flips, F)),
+        res_padding_ok=bool(_padding_zero(got_res, S)),
+    )
+    if got_logits is not None:
+        out["max_abs_logit_err"] = float(np.max(np.abs(got_logits.astype(np.float64) - ref_logits)))
+    return out
+
+
+def _padding_zero(words, nbits):
+    words = np.asarray(words, dtype=np.uint64)
+    rem = nbits % 64
+    if rem == 0:
+        return True
+    return bool((words[:, -1] >> np.uint64(rem) == 0).all())
+
+
+def assert_parity(stats, dtype):
+    tol = TOL[dtype]
+    assert stats["flip_padding_ok"] and stats["res_padding_ok"], stats
+    assert stats["flip_mismatch"] == 0, stats
+    assert stats["res_mismatch"] == 0, stats
+    if "max_abs_logit_err" in stats:
+        assert stats["max_abs_logit_err"] <= tol, stats
+
+
+def config_case(cfg_id, batch=None, act=workload.GELU_TANH):
+    c = workload.CONFIGS[cfg_id]
+    layers = workload.config_layers(cfg_id, act)
+    weights = workload.config_weights(cfg_id, act)
+    det, noise = workload.config_inputs(cfg_id, batch)
+    return c["d"], c["T"], c["dtype"], layers, weights, det, noise

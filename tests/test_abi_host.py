@@ -1,0 +1,151 @@
+"""Host-side checks of the C ABI (no kernel launches): the library loads and
+exports every function declared in include/predecoder.h, the size helpers and
+the parameter-count rule agree with the paper's tables, and create() rejects
+misuse before touching the device."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2604_12841_amd as pdx
+from conftest import ROOT, gpu_available
+from paper_2604_12841_amd import workload
+
+HEADER = os.path.join(ROOT, "include", "predecoder.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(predecoder_\w+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared_functions()
+    assert len(names) >= 10
+    L = pdx.lib()
+    for n in names:
+        assert hasattr(L, n), n
+    assert sorted(pdx.EXPORTS) == names
+
+
+def test_word_counts():
+    for d, T in [(3, 1), (5, 5), (9, 9), (13, 13), (25, 25), (31, 31)]:
+        assert pdx.det_words(d, T) == -(-T * (d * d - 1) // 64)
+        assert pdx.flip_words(d, T) == -(-T * (3 * d * d - 1) // 64)
+    assert pdx.det_words(13, 13) == 35 and pdx.flip_words(13, 13) == 103
+    assert pdx.det_words(0, 5) == -1 and pdx.flip_words(5, 0) == -1
+
+
+def test_weight_count_matches_paper_tables(golden_dir):
+    for line in open(os.path.join(golden_dir, "param_counts.txt")):
+        if line.startswith("#") or not line.strip():
+            continue
+        m, filt, ks, printed = line.split()
+        layers, ci = [], 4
+        for f, k in zip(filt.split(","), ks.split(",")):
+            layers.append((ci, int(f), int(k), 1))
+            ci = int(f)
+        n = pdx.weight_count(layers)
+        assert n == (912772 if m == "1" else int(printed))
+    # Model 6: conv layers of the residual network (BatchNorm adds 2 per channel)
+    convs, bn = [], 0
+    lines = [l.split() for l in open(os.path.join(golden_dir, "model6.txt")) if l.strip() and not l.startswith("#")]
+    printed = int(lines[0][0])
+    for p in lines[1:]:
+        if p[0] == "conv":
+            convs.append((int(p[1]), int(p[2]), int(p[3]), 1))
+        else:
+            bn += 2 * int(p[1])
+    assert sum(pdx.weight_count([c]) for c in convs) + bn == printed
+    assert pdx.weight_count([]) == 0
+
+
+def test_workload_weight_sizes():
+    for cfg in workload.CONFIGS:
+        layers = workload.config_layers(cfg)
+        assert workload.config_weights(cfg).size == pdx.weight_count(layers)
+
+
+def test_status_strings():
+    for s in range(5):
+        assert pdx.status_string(s)
+    assert "invalid" in pdx.status_string(pdx.PD_ERR_INVALID_ARG)
+
+
+def _create(weights, d, T, layers, dtype=pdx.DTYPE_BF16, max_batch=4, n_weights=None, out=True):
+    L = pdx.lib()
+    w = np.ascontiguousarray(weights, dtype=np.float32)
+    arr = pdx._layers(layers) if layers is not None else None
+    h = ctypes.c_void_p()
+    st = L.predecoder_create(w.ctypes.data_as(ctypes.c_void_p) if w.size else None,
+                             w.size if n_weights is None else n_weights, d, T, arr,
+                             len(layers) if layers else 0, dtype, max_batch, ctypes.byref(h) if out else None)
+    if st == pdx.PD_OK:
+        L.predecoder_destroy(h)
+    return st
+
+
+LAYERS = workload.layer_spec(2, 64)
+W = workload.he_normal_weights(LAYERS, 0)
+
+
+@pytest.mark.parametrize("case", [
+    dict(d=4), dict(d=1), dict(d=-3), dict(T=0), dict(dtype=7), dict(max_batch=0),
+    dict(layers=[(3, 64, 3, 1), (64, 64, 3, 1), (64, 4, 1, 0)]),   # first c_in must be 2
+    dict(layers=[(2, 64, 3, 1), (64, 64, 3, 1), (64, 5, 1, 0)]),   # head must give 4 channels
+    dict(layers=[(2, 64, 3, 1), (32, 64, 3, 1), (64, 4, 1, 0)]),   # broken chain
+    dict(layers=[(2, 64, 4, 1), (64, 64, 3, 1), (64, 4, 1, 0)]),   # even kernel
+    dict(layers=[(2, 64, 3, 1), (64, 64, 3, 1), (64, 4, 1, 1)]),   # activated head
+    dict(layers=[(2, 64, 3, 9), (64, 64, 3, 1), (64, 4, 1, 0)]),   # unknown activation
+    dict(n_weights=W.size - 1),
+    dict(out=False),
+])
+def test_create_rejects_misuse(case):
+    args = dict(weights=W, d=5, T=3, layers=LAYERS)
+    args.update(case)
+    assert _create(**args) == pdx.PD_ERR_INVALID_ARG
+
+
+def test_create_rejects_null_pointers():
+    L = pdx.lib()
+    h = ctypes.c_void_p()
+    arr = pdx._layers(LAYERS)
+    assert L.predecoder_create(None, W.size, 5, 3, arr, len(LAYERS), 1, 4, ctypes.byref(h)) == pdx.PD_ERR_INVALID_ARG
+    w = np.ascontiguousarray(W)
+    assert L.predecoder_create(w.ctypes.data_as(ctypes.c_void_p), W.size, 5, 3, None, 3, 1, 4,
+                               ctypes.byref(h)) == pdx.PD_ERR_INVALID_ARG
+    assert h.value is None
+
+
+@pytest.mark.parametrize("layers,dtype", [
+    ([(2, 64, 5, 1), (64, 4, 1, 0)], pdx.DTYPE_BF16),          # 5x5x5 hidden layer
+    ([(2, 96, 3, 1), (96, 4, 1, 0)], pdx.DTYPE_BF16),          # width 96 on the bf16 path
+    ([(2, 64, 3, 1), (64, 4, 3, 0)], pdx.DTYPE_BF16),          # 3x3x3 head
+    ([(2, 4, 1, 0)], pdx.DTYPE_BF16),                          # no hidden layer
+    ([(2, 20, 3, 1), (20, 4, 1, 0)], pdx.DTYPE_FP32),          # fp32 width not a multiple of 8
+])
+def test_create_unsupported_shapes(layers, dtype):
+    w = workload.he_normal_weights(layers, 0)
+    assert _create(w, 5, 3, layers, dtype=dtype) == pdx.PD_ERR_UNSUPPORTED
+
+
+def test_create_unsupported_distance():
+    assert _create(W, 65, 3, LAYERS) == pdx.PD_ERR_UNSUPPORTED
+    assert _create(W, 5, 1024, LAYERS) == pdx.PD_ERR_UNSUPPORTED
+
+
+@pytest.mark.skipif(gpu_available(), reason="checks the no-device error path")
+def test_create_without_device_reports_device_error():
+    assert _create(W, 5, 3, LAYERS) == pdx.PD_ERR_DEVICE
+
+
+def test_run_rejects_null_handle():
+    L = pdx.lib()
+    assert L.predecoder_run(None, None, None, 1, None, None, None) == pdx.PD_ERR_INVALID_ARG
+    assert L.predecoder_residual(None, None, None, None, 1, None) == pdx.PD_ERR_INVALID_ARG
+    assert L.predecoder_unpack(None, None, None, 1, None) == pdx.PD_ERR_INVALID_ARG
+    assert L.predecoder_num_stages(None) == -1
+    L.predecoder_destroy(None)
