@@ -36,6 +36,7 @@ struct pd_predecoder {
   float* head_w = nullptr;       // [4][c_in] fp32 (bf16-valued on the bf16 path)
   float* head_b = nullptr;       // [4]
   int cmax = 0;
+  int n_cu = 256;                // compute units: one persistent conv workgroup each
 };
 
 namespace {
@@ -122,7 +123,6 @@ float bf16_value(float f) {
 
 // Tiling plan for the 3x3x3 layers: the candidate with the fewest MFMA rows
 // per sample whose double-buffered 32-channel staging fits in LDS.
-const int kMaxSpan = 1216;  // 2 * 1216 voxels * 64 B + row tables <= 160 KiB
 
 long long flat_span(const Geom& g, long long seg_len, long long nseg, int batch) {
   // exact maximum staged span over all tiles of `batch` samples
@@ -145,6 +145,7 @@ long long flat_span(const Geom& g, long long seg_len, long long nseg, int batch)
 }
 
 Tiling plan_tiling(const Geom& g, int max_batch) {
+  const int kMaxSpan = pd::conv_bf16_max_span();
   Tiling best{};
   long long best_rows = -1;
   int best_span = 0;
@@ -349,16 +350,20 @@ pd_status enqueue_run(pd_predecoder* h, hipStream_t st, const uint64_t* det, int
     if (fp32)
       s = check_launch(pd::launch_conv_fp32(g, L.c_in, L.c_out, L.act, (const float*)x, (float*)y,
                                             (const float*)h->wdev[l], h->bdev[l], batch, st));
-    else
+    else  // the last hidden layer carries the head and the threshold in its epilogue
       s = check_launch(pd::launch_conv_bf16(g, tl, L.c_in, L.c_out, L.act, x, y, h->wdev[l], h->bdev[l],
-                                            batch, st));
+                                            l == n - 2, h->head_w, h->head_b,
+                                            h->tables + pd::tables_comp_of_site(g), h->nib, logits, batch,
+                                            h->n_cu, st));
     if (s != PD_OK) return s;
     x = y;
   }
   if ((s = mark()) != PD_OK) return s;
-  s = check_launch(pd::launch_head(g, h->layers[n - 1].c_in, fp32, x, h->head_w, h->head_b, h->tables,
-                                   h->nib, logits, batch, st));
-  if (s != PD_OK) return s;
+  if (fp32) {
+    s = check_launch(pd::launch_head(g, h->layers[n - 1].c_in, fp32, x, h->head_w, h->head_b, h->tables,
+                                     h->nib, logits, batch, st));
+    if (s != PD_OK) return s;
+  }
   if ((s = mark()) != PD_OK) return s;
   s = check_launch(pd::launch_residual_pack(g, h->tables, det, h->nib, flips, residual, batch, st));
   if (s != PD_OK) return s;
@@ -419,6 +424,9 @@ pd_status predecoder_create(const float* weights, size_t n_weights, int32_t d, i
   if (n_weights != predecoder_weight_count(layers, n_layers)) return PD_ERR_INVALID_ARG;
   Geom g = make_geom(d, T);
   if (!supported(g, layers, n_layers, dtype)) return PD_ERR_UNSUPPORTED;
+  // kernels index voxels of a batch with 32-bit integers
+  if ((long long)max_batch * g.V >= (1ll << 31) || (long long)max_batch * (g.Wd + g.Wf) >= (1ll << 31))
+    return PD_ERR_UNSUPPORTED;
 
   int ndev = 0;
   if (hipGetDeviceCount(&ndev) != hipSuccess || ndev < 1) {
@@ -431,7 +439,10 @@ pd_status predecoder_create(const float* weights, size_t n_weights, int32_t d, i
   h->dtype = dtype;
   h->max_batch = max_batch;
   h->layers.assign(layers, layers + n_layers);
-  if (hipGetDevice(&h->device) != hipSuccess) {
+  if (hipGetDevice(&h->device) != hipSuccess ||
+      hipDeviceGetAttribute(&h->n_cu, hipDeviceAttributeMultiprocessorCount, h->device) != hipSuccess ||
+      h->n_cu < 1) {
+    (void)hipGetLastError();
     delete h;
     return PD_ERR_DEVICE;
   }
@@ -440,7 +451,7 @@ pd_status predecoder_create(const float* weights, size_t n_weights, int32_t d, i
   h->cmax = cmax;
   if (dtype == PD_DTYPE_BF16) {
     h->tiling = plan_tiling(g, max_batch);
-    if (h->tiling.span <= 0 || h->tiling.span > kMaxSpan) {
+    if (h->tiling.span <= 0 || h->tiling.span > pd::conv_bf16_max_span()) {
       delete h;
       return PD_ERR_UNSUPPORTED;
     }

@@ -1,34 +1,38 @@
-// conv_bf16.hip -- K2 + K3: one 3x3x3 conv3d layer (Sec. III.B, Fig.
-// ConvArch; stride 1, zero padding, cross-correlation) as an implicit GEMM on
-// the gfx950 matrix cores, with the bias + activation + bf16 rounding
-// epilogue fused in.
+// conv_bf16.hip -- K2 + K3 (+ K4 for the last layer): one 3x3x3 conv3d layer
+// (Sec. III.B, Fig. ConvArch; stride 1, zero padding, cross-correlation) as an
+// implicit GEMM on the gfx950 matrix cores, with the bias + activation + bf16
+// rounding epilogue fused in; for the last hidden layer the epilogue also
+// applies the 1x1x1 head and the threshold (logit > 0) and writes one flip
+// nibble per voxel instead of the activations.
 //
-//   out[m][co] = act(bias[co] + sum_{tap, ci} X[m + shift(tap)][ci] * W[tap][ci][co])
+//   out[co][m] = act(bias[co] + sum_{tap, ci} W[co][ci][tap] * X[m + shift(tap)][ci])
 //
-// GEMM view: M = output voxels, N = c_out, K = 27 * c_in.  Activations live in
-// the zero-halo NTHWC layout of internal.h, so every tap is an index shift
-// and no bounds checks are needed in the K loop.
+// GEMM view (transposed so the epilogue holds 4 consecutive channels per
+// lane): rows = c_out, columns = output voxels, K = 27 * c_in.  Activations
+// live in the zero-halo NTHWC layout of internal.h, so every tap is an index
+// shift and the K loop has no bounds checks.
 //
-// Work split (one workgroup = 256 threads = 4 wave64):
-//   * a tile is 256 output voxels (see Tiling) x all c_out channels;
-//   * wave w owns rows [128 * (w & 1), +128) and columns
-//     [(c_out / 2) * (w >> 1), +c_out / 2): 4 x (c_out / 64) blocks of
-//     v_mfma_f32_32x32x16_bf16, fp32 accumulators in registers;
-//   * the input footprint of the tile is staged in LDS, 32 input channels
-//     (64 bytes per voxel) at a time, double buffered; the next chunk is
-//     copied with global_load_lds_dwordx4 (HBM/L2 -> LDS without registers)
-//     while the current one feeds the MFMAs;
-//   * each voxel's four 16-byte granules are XOR-swizzled by (voxel >> 1) & 3
-//     so the 32 rows of an A fragment (consecutive voxels, 64-byte stride)
-//     hit distinct LDS banks;
-//   * weights are pre-arranged at create time in MFMA B-fragment order and
-//     read straight from global memory (one coalesced 16-byte load per lane
-//     per fragment; a layer is <= 0.9 MB and stays L2-resident);
-//   * epilogue: acc + bias -> activation (fp32) -> bf16 (RNE, v_cvt_pk_bf16_f32)
-//     -> LDS transpose -> 16-byte coalesced stores into the interior of the
+// Work split: persistent workgroups of 256 threads (4 wave64), one per CU.
+// A tile is 256 output voxels x all c_out channels; wave w owns voxels
+// [128 (w & 1), +128) and channels [(c_out / 2)(w >> 1), +c_out / 2), i.e.
+// 4 x (c_out / 64) blocks of v_mfma_f32_32x32x16_bf16 with fp32 accumulators.
+//   * The input footprint of a tile is staged in LDS 32 input channels (64
+//     bytes per voxel) at a time, double buffered, with global_load_lds_dwordx4
+//     (HBM/L2 -> LDS, no registers).  The next chunk -- or, during the last
+//     chunk, the next tile's first chunk -- is in flight while the current one
+//     feeds the MFMAs.
+//   * The four 16-byte granules of a voxel are XOR-swizzled by (voxel >> 1) & 3
+//     so the 32 voxels of a fragment (64-byte stride) spread over the banks.
+//   * The 54 k-steps of a chunk (27 taps x 2) are fully unrolled and software
+//     pipelined: activation fragments are read from LDS one step ahead, weight
+//     fragments (pre-arranged at create time in MFMA operand order, one
+//     coalesced 16-byte load per lane; a layer is <= 0.9 MB and stays in L2)
+//     five steps ahead through a 6-deep register ring.
+//   * Epilogue from registers: + bias, activation in fp32, bf16 (RNE,
+//     v_cvt_pk_bf16_f32), 8-byte stores of 4 channels into the interior of the
 //     output (the halo is never written).
-// Layer 1 (c_in = 2) uses the same tile machinery with K = 27 taps x 2
-// channels padded to 64: each lane gathers 4 taps x 2 channels per fragment.
+// Layer 1 (c_in = 2) uses the same tiles with K = 27 taps x 2 channels padded
+// to 64 (4 k-steps): each lane gathers 4 taps x 2 channels per fragment.
 #include "internal.h"
 
 namespace pd {
@@ -36,14 +40,29 @@ namespace pd {
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(16))) float f32x16;
 typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
-
-constexpr int KC = 32;              // input channels per LDS chunk
-constexpr int kOutPad = 16;         // bytes of padding per row of the output tile
+typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
 typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) char lds_char;
+typedef __attribute__((address_space(3))) const u32x4 lds_u32x4;
+typedef __attribute__((address_space(3))) const uint32_t lds_u32;
+typedef __attribute__((address_space(3))) float lds_float;
+typedef __attribute__((address_space(3))) u32x4 lds_u32x4_w;
+typedef __attribute__((address_space(3))) uint32_t lds_u32_w;
+
+constexpr int KC = 32;     // input channels per LDS chunk
+constexpr int STEPS = 54;  // k-steps per chunk: 27 taps x 2 (16 channels each)
+constexpr int BRING = 6;   // weight-fragment ring depth (prefetch distance BRING - 1)
+// Every chunk is staged with exactly RMAX rounds of 256 16-byte granules
+// (1024 voxels at most); rounds past the footprint load voxel 0 and store to a
+// scratch region, so every wave issues the same fixed sequence.
+constexpr int RMAX = 16;
+constexpr int ABUF = RMAX * 256 * 16;   // bytes per staging buffer
+constexpr int PLANE_RMAX = 4;           // layer 1: rounds of 256 voxels x 4 bytes
+constexpr int TRASH = 256 * 16;         // destination of unused rounds
 
 __device__ __forceinline__ float activation(float y, int act) {
   if (act == 1) {  // GELU, tanh form: 0.5 y (1 + tanh(u)) = y / (1 + exp(-2u))
-    const float k0 = 0.7978845608028654f;      // sqrt(2 / pi)
+    const float k0 = 0.7978845608028654f;          // sqrt(2 / pi)
     const float kl = -2.0f * 1.4426950408889634f;  // -2 log2(e)
     float u = k0 * (y + 0.044715f * y * y * y);
     float e = __builtin_amdgcn_exp2f(kl * u);
@@ -53,52 +72,53 @@ __device__ __forceinline__ float activation(float y, int act) {
   return y;
 }
 
-__device__ __forceinline__ uint16_t to_bf16_bits(float v) {
+__device__ __forceinline__ uint32_t bf16_bits(float v) {
   __bf16 h = (__bf16)v;
-  return __builtin_bit_cast(uint16_t, h);
+  return (uint32_t)__builtin_bit_cast(uint16_t, h);
 }
+__device__ __forceinline__ float bf16_round(float v) { return __uint_as_float(bf16_bits(v) << 16); }
 
-// Decodes row r (0..255) of tile `tile`: returns false if the row is outside
-// the volume; otherwise the padded index of the output voxel.
-__host__ __device__ inline bool tile_row(const Geom& g, const Tiling& tl, long long tile, int r,
-                                         int batch, long long* pidx, int* lds_base,
-                                         long long* stage_origin) {
+// Row r (0..255) of tile `tile`: false if the row is outside the volume,
+// else its padded output index.  Also the LDS voxel of the row's (0,0,0) tap
+// and the padded index of staged voxel 0.  32-bit arithmetic: the host
+// guarantees max_batch * V < 2^31.
+__host__ __device__ inline bool tile_row(const Geom& g, const Tiling& tl, int tile, int r, int batch,
+                                         long long* pidx, int* lds_base, long long* stage_origin) {
+  const int HH = g.H * g.H;
   if (tl.mode == 0) {
-    long long seg = tile / tl.tiles_per_seg;
-    long long k0 = (tile - seg * tl.tiles_per_seg) * (long long)kTileRows;
-    long long u0 = seg * tl.seg_len + k0;
-    int b0 = (int)(u0 / g.V);
-    int v0 = (int)(u0 - (long long)b0 * g.V);
-    int HH = g.H * g.H;
-    int t0 = v0 / HH, s0 = v0 - t0 * HH;
-    long long p0 = padded_index(g, b0, t0, s0 / g.H, s0 % g.H);
+    const int seg = tile / tl.tiles_per_seg;
+    const int k0 = (tile - seg * tl.tiles_per_seg) * kTileRows;
+    const int u0 = seg * (int)tl.seg_len + k0;
+    const int b0 = u0 / g.V;
+    const int v0 = u0 - b0 * g.V;
+    const int t0 = v0 / HH, s0 = v0 - t0 * HH;
+    const long long p0 = padded_index(g, b0, t0, s0 / g.H, s0 % g.H);
     *stage_origin = p0 - (g.P + g.Wp + 1);
-    long long u = u0 + r;
-    bool ok = (k0 + r < tl.seg_len) && (u < (long long)batch * g.V);
-    if (!ok) {
+    const int u = u0 + r;
+    if (k0 + r >= tl.seg_len || u >= batch * g.V) {
       *lds_base = 0;
       return false;
     }
-    int b = (int)(u / g.V);
-    int v = (int)(u - (long long)b * g.V);
-    int t = v / HH, s = v - t * HH;
-    long long p = padded_index(g, b, t, s / g.H, s % g.H);
+    const int b = u / g.V;
+    const int v = u - b * g.V;
+    const int t = v / HH, s = v - t * HH;
+    const long long p = padded_index(g, b, t, s / g.H, s % g.H);
     *pidx = p;
     *lds_base = (int)(p - p0);
     return true;
   } else {
-    long long per = (long long)tl.ntT * tl.ntI * tl.ntJ;
-    int b = (int)(tile / per);
-    int rem = (int)(tile - (long long)b * per);
-    int tt = rem / (tl.ntI * tl.ntJ);
-    int ti = (rem / tl.ntJ) % tl.ntI;
-    int tj = rem % tl.ntJ;
-    int t0 = tt * tl.BT, i0 = ti * tl.BI, j0 = tj * tl.BJ;
+    const int per = tl.ntT * tl.ntI * tl.ntJ;
+    const int b = tile / per;
+    const int rem = tile - b * per;
+    const int tt = rem / (tl.ntI * tl.ntJ);
+    const int ti = (rem / tl.ntJ) % tl.ntI;
+    const int tj = rem % tl.ntJ;
+    const int t0 = tt * tl.BT, i0 = ti * tl.BI, j0 = tj * tl.BJ;
     *stage_origin = (long long)b * g.S + (long long)t0 * g.P + (long long)i0 * g.Wp + j0;
-    int bij = tl.BI * tl.BJ;
-    int a = r / bij, c = (r / tl.BJ) % tl.BI, e = r % tl.BJ;
-    int t = t0 + a, i = i0 + c, j = j0 + e;
-    bool ok = (r < tl.BT * bij) && t < g.T && i < g.H && j < g.H;
+    const int bij = tl.BI * tl.BJ;
+    const int a = r / bij, c = (r / tl.BJ) % tl.BI, e = r % tl.BJ;
+    const int t = t0 + a, i = i0 + c, j = j0 + e;
+    const bool ok = (r < tl.BT * bij) && t < g.T && i < g.H && j < g.H;
     *lds_base = ok ? (a * (tl.BI + 2) + c) * (tl.BJ + 2) + e : 0;
     if (!ok) return false;
     *pidx = padded_index(g, b, t, i, j);
@@ -106,17 +126,29 @@ __host__ __device__ inline bool tile_row(const Geom& g, const Tiling& tl, long l
   }
 }
 
-// Padded box origin of a box-mode tile, in padded coordinates.
+// Padded (t, i, j) of a box-mode tile's staging origin.
 struct BoxOrigin {
   int t0, i0, j0;
 };
+
+__host__ __device__ inline BoxOrigin box_origin(const Geom& g, const Tiling& tl, long long origin) {
+  BoxOrigin bo{0, 0, 0};
+  if (tl.mode == 1) {
+    const long long rem = origin % g.S;
+    bo.t0 = (int)(rem / g.P);
+    const int r2 = (int)(rem - (long long)bo.t0 * g.P);
+    bo.i0 = r2 / g.Wp;
+    bo.j0 = r2 - bo.i0 * g.Wp;
+  }
+  return bo;
+}
 
 // Global padded voxel of staged voxel vv (clamped to voxel 0, a zero halo
 // voxel, when outside the batch or outside the sample's padded box).
 __host__ __device__ inline long long staged_voxel(const Geom& g, const Tiling& tl, long long origin,
                                                   const BoxOrigin& bo, int vv, long long limit) {
   if (tl.mode == 0) {
-    long long p = origin + vv;
+    const long long p = origin + vv;
     return (p < limit) ? p : 0;
   }
   const int bj2 = tl.BJ + 2, bij2 = (tl.BI + 2) * bj2;
@@ -128,243 +160,424 @@ __host__ __device__ inline long long staged_voxel(const Geom& g, const Tiling& t
   return origin + (long long)a * g.P + (long long)c * g.Wp + e;
 }
 
-template <int CIN, int COUT>
+// Tile handled by persistent workgroup `wg` at iteration `it`: the 8 XCDs
+// receive workgroups round-robin, so workgroup wg runs on XCD wg % 8; each
+// XCD gets a contiguous range of tiles (neighbouring tiles share halo voxels
+// in its L2) and its workgroups stride through it.  -1 when done.
+__host__ __device__ inline int tile_of(int wg, int nwg, int it, int ntiles) {
+  const int xcd = wg & 7, k = wg >> 3, per_xcd_wg = nwg >> 3;
+  const int per_xcd = (ntiles + 7) >> 3;
+  const int idx = k + it * per_xcd_wg;
+  if (idx >= per_xcd) return -1;
+  const int t = xcd * per_xcd + idx;
+  return t < ntiles ? t : -1;
+}
+
+// Staging source of a tile: its staged-voxel origin and box origin.
+struct StageSrc {
+  long long origin;
+  BoxOrigin bo;
+};
+
+// Granule q = 256 k + 64 wave + lane of the staging buffer holds logical
+// granule (q & 3) ^ ((vv >> 1) & 3) of staged voxel vv = q >> 2 (32 channels
+// of chunk `chunk`).  Returns that granule (a dummy one past the footprint).
+template <int CIN>
+__device__ __forceinline__ u32x4 stage_load(const Geom& g, const Tiling& tl, const uint16_t* __restrict__ x,
+                                            const StageSrc& src, long long limit, int chunk, int ngran, int k,
+                                            int wave, int lane) {
+  const int q = k * 256 + wave * 64 + lane;
+  const int vv = q >> 2;
+  const int sg = (q & 3) ^ ((vv >> 1) & 3);
+  const long long gv = staged_voxel(g, tl, src.origin, src.bo, q < ngran ? vv : 0, limit);
+  return *reinterpret_cast<const u32x4*>(x + gv * CIN + chunk * KC + sg * 8);
+}
+
+// Layer 1: both channels (4 bytes) of staged voxel 256 k + 64 wave + lane.
+__device__ __forceinline__ uint32_t plane_load(const Geom& g, const Tiling& tl, const uint16_t* __restrict__ x,
+                                               const StageSrc& src, long long limit, int k, int wave, int lane) {
+  const int vv = k * 256 + wave * 64 + lane;
+  const long long gv = staged_voxel(g, tl, src.origin, src.bo, vv < tl.span ? vv : 0, limit);
+  return reinterpret_cast<const uint32_t*>(x)[gv];
+}
+
+template <int CIN, int COUT, bool HEAD>
 __global__ void __launch_bounds__(256) conv_bf16_kernel(Geom g, Tiling tl, int act,
                                                         const uint16_t* __restrict__ x,
                                                         uint16_t* __restrict__ y,
                                                         const u32x4* __restrict__ wfrag,
-                                                        const float* __restrict__ bias, int batch,
-                                                        int abuf_bytes, int region_bytes) {
+                                                        const float* __restrict__ bias,
+                                                        const float* __restrict__ head_w,
+                                                        const float* __restrict__ head_b,
+                                                        const int32_t* __restrict__ comp_of_site,
+                                                        uint8_t* __restrict__ nib, float* __restrict__ logits,
+                                                        int batch) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  constexpr int NB = COUT / 64;   // 32-wide column blocks per wave
-  constexpr int NBT = COUT / 32;  // column blocks in total
-  constexpr int MB = 4;           // 32-row blocks per wave
+  constexpr int NB = COUT / 64;   // 32-channel blocks per wave
+  constexpr int NBT = COUT / 32;  // 32-channel blocks in total
+  constexpr int MB = 4;           // 32-voxel blocks per wave
+  constexpr int NCHUNK = (CIN == 2) ? 1 : CIN / KC;
+  constexpr int TSTEPS = NCHUNK * STEPS;  // k-steps per tile (hidden layers)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave & 1, wn = wave >> 1;
-
-  // Consecutive workgroups are dispatched round-robin over the 8 XCDs; give
-  // each XCD a contiguous run of tiles so neighbouring tiles (which share
-  // halo voxels) meet in the same L2.
-  const unsigned per_xcd = gridDim.x >> 3;
-  const long long tile = (long long)(blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
-  if (tile >= tl.ntiles) return;
-
-  char* abuf0 = smem;
-  char* abuf1 = smem + abuf_bytes;
-  char* region_end = smem + region_bytes;
-  long long* row_pidx = reinterpret_cast<long long*>(region_end);
-  int* row_base = reinterpret_cast<int*>(region_end + 256 * sizeof(long long));
-
-  long long origin = 0;
-  {
-    long long p = -1;
-    int lb = 0;
-    bool ok = tile_row(g, tl, tile, tid, batch, &p, &lb, &origin);
-    row_pidx[tid] = ok ? p : -1;
-    row_base[tid] = lb;
-  }
+  const int half = lane >> 5, l32 = lane & 31;
+  const int ntiles = (int)tl.ntiles;
   const long long limit = (long long)batch * g.S;
-  BoxOrigin bo{0, 0, 0};
-  if (tl.mode == 1) {
-    long long rem = origin - (origin / g.S) * g.S;
-    bo.t0 = (int)(rem / g.P);
-    int r2 = (int)(rem - (long long)bo.t0 * g.P);
-    bo.i0 = r2 / g.Wp;
-    bo.j0 = r2 - bo.i0 * g.Wp;
-  }
-  __syncthreads();
+  const int ngran = tl.span * 4;  // 16-byte granules of a staged chunk
 
-  int rb[MB];
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb) rb[mb] = row_base[wm * 128 + mb * 32 + (lane & 31)];
+  // LDS: [staging buffer 0][staging buffer 1][scratch round][head partials
+  // [2][256][4] fp32][bias [COUT]][head weights [4][COUT]]
+  lds_char* const lds = (lds_char*)smem;
+  lds_char* const trash = lds + 2 * ABUF;
+  lds_float* const head_part = (lds_float*)(trash + TRASH);
+  lds_float* const bias_s = head_part + 2 * 256 * 4;
+  lds_float* const headw_s = bias_s + COUT;
+  for (int e = tid; e < COUT; e += 256) bias_s[e] = bias[e];
+  if (HEAD)
+    for (int e = tid; e < 4 * COUT; e += 256) headw_s[e] = head_w[e];
 
-  f32x16 acc[MB][NB];
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[mb][nb][v] = 0.0f;
+  int tile = tile_of(blockIdx.x, gridDim.x, 0, ntiles);
+  if (tile < 0) return;
 
+  auto source_of = [&](int t) {
+    StageSrc src;
+    long long p;
+    int lb;
+    tile_row(g, tl, t, 0, batch, &p, &lb, &src.origin);
+    src.bo = box_origin(g, tl, src.origin);
+    return src;
+  };
+  StageSrc cur_src = source_of(tile);
+
+  // First tile: stage its first chunk synchronously.
   if constexpr (CIN == 2) {
-    // ---- Layer 1: stage the 2-channel planes (4 bytes per voxel) once ----
-    const int nvox = tl.span;
-    for (int base = 0; base < nvox; base += 256) {
-      int vv = base + tid;
-      long long gv = staged_voxel(g, tl, origin, bo, vv < nvox ? vv : 0, limit);
-      const uint32_t* src = reinterpret_cast<const uint32_t*>(x) + gv;
-      __builtin_amdgcn_global_load_lds(src, (lds_void*)(abuf0 + (base + wave * 64) * 4), 4, 0, 0);
-    }
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
-    const uint32_t* a32 = reinterpret_cast<const uint32_t*>(abuf0);
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      u32x4 bfr[NB];
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) bfr[nb] = wfrag[(ks * NBT + wn * NB + nb) * 64 + lane];
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb) {
-        u32x4 av;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          int tap = ks * 8 + (lane >> 5) * 4 + q;
-          uint32_t val = 0;
-          if (tap < 27) {
-            int dt = tap / 9, di = (tap / 3) % 3, dj = tap % 3;
-            val = a32[rb[mb] + dt * tl.sa + di * tl.sb + dj];
-          }
-          av[q] = val;
-        }
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              __builtin_bit_cast(bf16x8, av), __builtin_bit_cast(bf16x8, bfr[nb]), acc[mb][nb], 0, 0, 0);
-      }
+    for (int k = 0; k < PLANE_RMAX; ++k) {
+      const uint32_t v = plane_load(g, tl, x, cur_src, limit, k, wave, lane);
+      *(lds_u32_w*)(lds + (k * 256 + wave * 64 + lane) * 4) = v;
     }
   } else {
-    // ---- Hidden layers: chunks of 32 input channels, double buffered ----
-    constexpr int NCHUNK = CIN / KC;
-    const int ngran = tl.span * 4;  // 16-byte granules per chunk
-    auto stage = [&](int chunk, char* buf) {
-      for (int base = 0; base < ngran; base += 256) {
-        int q = base + wave * 64 + lane;
-        int vv = q >> 2;
-        int ps = q & 3;
-        int s = ps ^ ((vv >> 1) & 3);
-        long long gv = staged_voxel(g, tl, origin, bo, q < ngran ? vv : 0, limit);
-        const uint16_t* src = x + gv * CIN + chunk * KC + s * 8;
-        __builtin_amdgcn_global_load_lds(src, (lds_void*)(buf + (base + wave * 64) * 16), 16, 0, 0);
-      }
-    };
-    stage(0, abuf0);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
-    for (int chunk = 0; chunk < NCHUNK; ++chunk) {
-      char* cur = (chunk & 1) ? abuf1 : abuf0;
-      if (chunk + 1 < NCHUNK) stage(chunk + 1, (chunk & 1) ? abuf0 : abuf1);
-      const u32x4* wchunk = wfrag + (long long)chunk * 27 * 2 * NBT * 64 + (wn * NB) * 64 + lane;
-      // weights of tap + 1 are fetched while tap runs (one tap = 2 k-steps)
-      u32x4 bnext[2][NB];
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks)
+    for (int k = 0; k < RMAX; ++k) {
+      const u32x4 v = stage_load<CIN>(g, tl, x, cur_src, limit, 0, ngran, k, wave, lane);
+      *(lds_u32x4_w*)(lds + (k * 256 + wave * 64 + lane) * 16) = v;
+    }
+  }
+
+  // weight-fragment ring (hidden layers): slot k holds the fragments of
+  // tile-step gs with gs % BRING == k
+  const u32x4* wlane = wfrag + (wn * NB) * 64 + lane;
+  u32x4 bq[BRING][NB];
+  if constexpr (CIN != 2) {
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) bnext[ks][nb] = wchunk[(ks * NBT + nb) * 64];
-#pragma unroll 1
-      for (int tap = 0; tap < 27; ++tap) {
-        const int dt = tap / 9, di = (tap / 3) % 3, dj = tap - (tap / 3) * 3;
-        const int toff = dt * tl.sa + di * tl.sb + dj;
-        u32x4 bcur[2][NB];
+    for (int st = 0; st < BRING - 1; ++st)
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks)
+      for (int nb = 0; nb < NB; ++nb) bq[st][nb] = wlane[(st * NBT + nb) * 64];
+  }
+  __syncthreads();  // staged chunk, bias and head weights visible
+
+  int gchunk = 0;  // chunks processed by this workgroup (selects the LDS buffer)
+  for (int it = 0; tile >= 0; ++it) {
+    const int next = tile_of(blockIdx.x, gridDim.x, it + 1, ntiles);
+    const StageSrc next_src = source_of(next >= 0 ? next : tile);
+    // rows of this lane: voxel 32 mb + l32 of the wave's 128
+    int rb[MB];
+    long long pidx[MB];
 #pragma unroll
-          for (int nb = 0; nb < NB; ++nb) bcur[ks][nb] = bnext[ks][nb];
-        if (tap + 1 < 27) {
+    for (int mb = 0; mb < MB; ++mb) {
+      long long p = -1, o;
+      int lb = 0;
+      bool ok = tile_row(g, tl, tile, wm * 128 + mb * 32 + l32, batch, &p, &lb, &o);
+      rb[mb] = lb;
+      pidx[mb] = ok ? p : -1;
+    }
+
+    f32x16 acc[MB][NB];
 #pragma unroll
-          for (int ks = 0; ks < 2; ++ks)
+    for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-            for (int nb = 0; nb < NB; ++nb) bnext[ks][nb] = wchunk[(((tap + 1) * 2 + ks) * NBT + nb) * 64];
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[mb][nb][v] = 0.0f;
+
+    if constexpr (CIN == 2) {
+      lds_char* const cur = lds + (gchunk & 1) * ABUF;
+      lds_char* const oth = (next >= 0) ? lds + ((gchunk + 1) & 1) * ABUF : trash;
+      // next tile's planes into registers while this tile computes
+      uint32_t nxt[PLANE_RMAX];
+#pragma unroll
+      for (int k = 0; k < PLANE_RMAX; ++k) nxt[k] = plane_load(g, tl, x, next_src, limit, k, wave, lane);
+      lds_u32* a32 = (lds_u32*)cur;
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        u32x4 wf[NB];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) wf[nb] = wlane[(ks * NBT + nb) * 64];
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          u32x4 av;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int tap = ks * 8 + half * 4 + q;
+            uint32_t val = 0;
+            if (tap < 27) {
+              const int dt = tap / 9, di = (tap / 3) % 3, dj = tap % 3;
+              val = a32[rb[mb] + dt * tl.sa + di * tl.sb + dj];
+            }
+            av[q] = val;
+          }
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb)
+            acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                __builtin_bit_cast(bf16x8, wf[nb]), __builtin_bit_cast(bf16x8, av), acc[mb][nb], 0, 0, 0);
         }
+      }
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-          const int seg = ks * 2 + (lane >> 5);
-          u32x4 av[MB];
+      for (int k = 0; k < PLANE_RMAX; ++k)
+        *(lds_u32_w*)(oth + ((next >= 0 ? k * 256 : 0) + wave * 64 + lane) * 4) = nxt[k];
+      ++gchunk;
+    } else {
+      for (int chunk = 0; chunk < NCHUNK; ++chunk, ++gchunk) {
+        lds_char* const cur = lds + (gchunk & 1) * ABUF;
+        // the chunk staged next: the following chunk of this tile, else the
+        // first chunk of the next tile, else nothing (scratch)
+        const bool more = chunk + 1 < NCHUNK;
+        const bool real = more || next >= 0;
+        const StageSrc& ssrc = more ? cur_src : next_src;
+        const int schunk = more ? chunk + 1 : 0;
+        const int sgran = real ? ngran : 0;
+        lds_char* const oth = lds + ((gchunk + 1) & 1) * ABUF;
+        u32x4 stg[3];
+
+        // Opaque copies of the row bases: keeps the 4 x 54 per-step LDS
+        // addresses of this chunk from being hoisted out of the chunk loop
+        // (they would occupy 216 VGPRs).
+        int rbc[MB];
 #pragma unroll
-          for (int mb = 0; mb < MB; ++mb) {
-            const int vox = rb[mb] + toff;
-            const int off = vox * 64 + ((seg ^ ((vox >> 1) & 3)) << 4);
-            av[mb] = *reinterpret_cast<const u32x4*>(cur + off);
+        for (int mb = 0; mb < MB; ++mb) {
+          rbc[mb] = rb[mb];
+          asm volatile("" : "+v"(rbc[mb]));
+        }
+        u32x4 av[2][MB];
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          const int vox = rbc[mb];
+          av[0][mb] = *(lds_u32x4*)(cur + vox * 64 + ((half ^ ((vox >> 1) & 3)) << 4));
+        }
+        const int gbase = chunk * STEPS;  // tile-step of this chunk's step 0
+#pragma unroll
+        for (int st = 0; st < STEPS; ++st) {
+          // staging of the next chunk: round k is loaded at step 3k and
+          // stored to LDS at step 3k + 6
+          if (st % 3 == 0 && st / 3 < RMAX)
+            stg[(st / 3) % 3] = stage_load<CIN>(g, tl, x, ssrc, limit, schunk, sgran, st / 3, wave, lane);
+          if (st >= 6 && (st - 6) % 3 == 0 && (st - 6) / 3 < RMAX) {
+            const int k = (st - 6) / 3;
+            lds_char* dst = (k * 256 < sgran) ? oth + (k * 256 + wave * 64 + lane) * 16
+                                              : trash + (wave * 64 + lane) * 16;
+            *(lds_u32x4_w*)dst = stg[k % 3];
+          }
+          // activation fragments of step st + 1
+          if (st + 1 < STEPS) {
+            const int tap = (st + 1) >> 1, ks = (st + 1) & 1;
+            const int dt = tap / 9, di = (tap / 3) % 3, dj = tap % 3;
+            const int toff = dt * tl.sa + di * tl.sb + dj;
+            const int sg = ks * 2 + half;
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) {
+              const int vox = rbc[mb] + toff;
+              av[(st + 1) & 1][mb] = *(lds_u32x4*)(cur + vox * 64 + ((sg ^ ((vox >> 1) & 3)) << 4));
+            }
+          }
+          // weight fragments of tile-step gs + BRING - 1 (wrapping into the next tile)
+          {
+            int gs = gbase + st + BRING - 1;
+            if (gs >= TSTEPS) gs -= TSTEPS;
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) bq[(st + BRING - 1) % BRING][nb] = wlane[(gs * NBT + nb) * 64];
           }
 #pragma unroll
           for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb)
               acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                  __builtin_bit_cast(bf16x8, av[mb]), __builtin_bit_cast(bf16x8, bcur[ks][nb]), acc[mb][nb],
-                  0, 0, 0);
+                  __builtin_bit_cast(bf16x8, bq[st % BRING][nb]), __builtin_bit_cast(bf16x8, av[st & 1][mb]),
+                  acc[mb][nb], 0, 0, 0);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        // every wave's staging writes done, every wave done reading `cur`
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+        __builtin_amdgcn_s_barrier();
+      }
+    }
+
+    // ---- epilogue: lane holds channels co .. co + 3 of voxel row (mb, l32) ----
+    if constexpr (!HEAD) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int co = wn * (COUT / 2) + nb * 32 + q * 8 + half * 4;
+          const float4 bv = {bias_s[co], bias_s[co + 1], bias_s[co + 2], bias_s[co + 3]};
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) {
+            if (pidx[mb] < 0) continue;
+            const float v0 = activation(acc[mb][nb][4 * q + 0] + bv.x, act);
+            const float v1 = activation(acc[mb][nb][4 * q + 1] + bv.y, act);
+            const float v2 = activation(acc[mb][nb][4 * q + 2] + bv.z, act);
+            const float v3 = activation(acc[mb][nb][4 * q + 3] + bv.w, act);
+            u32x2 packed;
+            packed.x = bf16_bits(v0) | (bf16_bits(v1) << 16);
+            packed.y = bf16_bits(v2) | (bf16_bits(v3) << 16);
+            *reinterpret_cast<u32x2*>(y + pidx[mb] * COUT + co) = packed;
+          }
         }
       }
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      __syncthreads();
-    }
-  }
-
-  // ---- Epilogue: bias + activation + bf16, transposed through LDS ----
-  __syncthreads();
-  constexpr int OSTRIDE = COUT * 2 + kOutPad;
-  char* otile = smem;
+    } else {
+      // 1x1x1 head on the bf16-rounded activations, partial over this lane's channels
+      float part[MB][4];
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    const int col = wn * (COUT / 2) + nb * 32 + (lane & 31);
-    const float bcol = bias[col];
+      for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb)
+        for (int o = 0; o < 4; ++o) part[mb][o] = 0.0f;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = wm * 128 + mb * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
-        float val = activation(acc[mb][nb][v] + bcol, act);
-        *reinterpret_cast<uint16_t*>(otile + row * OSTRIDE + col * 2) = to_bf16_bits(val);
+      for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int co = wn * (COUT / 2) + nb * 32 + q * 8 + half * 4;
+          const float4 bv = {bias_s[co], bias_s[co + 1], bias_s[co + 2], bias_s[co + 3]};
+          float4 hw[4];
+#pragma unroll
+          for (int o = 0; o < 4; ++o)
+            hw[o] = {headw_s[o * COUT + co], headw_s[o * COUT + co + 1], headw_s[o * COUT + co + 2],
+                     headw_s[o * COUT + co + 3]};
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) {
+            const float a0 = bf16_round(activation(acc[mb][nb][4 * q + 0] + bv.x, act));
+            const float a1 = bf16_round(activation(acc[mb][nb][4 * q + 1] + bv.y, act));
+            const float a2 = bf16_round(activation(acc[mb][nb][4 * q + 2] + bv.z, act));
+            const float a3 = bf16_round(activation(acc[mb][nb][4 * q + 3] + bv.w, act));
+#pragma unroll
+            for (int o = 0; o < 4; ++o)
+              part[mb][o] += hw[o].x * a0 + hw[o].y * a1 + hw[o].z * a2 + hw[o].w * a3;
+          }
+        }
       }
-  }
-  __syncthreads();
-  constexpr int GPR = COUT / 8;  // 16-byte granules per row
-  for (int q = tid; q < 256 * GPR; q += 256) {
-    const int row = q / GPR, gc = q % GPR;
-    const long long p = row_pidx[row];
-    if (p >= 0) {
-      u32x4 v = *reinterpret_cast<const u32x4*>(otile + row * OSTRIDE + gc * 16);
-      *reinterpret_cast<u32x4*>(y + p * COUT + gc * 8) = v;
+      // sum the two half-waves (same voxels, the other channel quads)
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int o = 0; o < 4; ++o) part[mb][o] += __shfl_xor(part[mb][o], 32);
+      // the two column waves meet in LDS
+      if (half == 0) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          float4 pv = {part[mb][0], part[mb][1], part[mb][2], part[mb][3]};
+          lds_float* hp = head_part + ((wn * 256) + wm * 128 + mb * 32 + l32) * 4;
+          hp[0] = pv.x;
+          hp[1] = pv.y;
+          hp[2] = pv.z;
+          hp[3] = pv.w;
+        }
+      }
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): partials written
+      __builtin_amdgcn_s_barrier();
+      // one thread per voxel row: logits, threshold, flip nibble
+      {
+        const int r = tid;  // tile row 0..255
+        long long p = -1, o2;
+        int lb;
+        if (tile_row(g, tl, tile, r, batch, &p, &lb, &o2)) {
+          const lds_float* h0 = head_part + r * 4;
+          const lds_float* h1 = head_part + (256 + r) * 4;
+          const float lg[4] = {head_b[0] + (h0[0] + h1[0]), head_b[1] + (h0[1] + h1[1]),
+                               head_b[2] + (h0[2] + h1[2]), head_b[3] + (h0[3] + h1[3])};
+          // padded index -> (b, t, i, j)
+          const int b = (int)(p / g.S);
+          const int rem = (int)(p - (long long)b * g.S);
+          const int t = rem / g.P - 1;
+          const int r2 = rem - (t + 1) * g.P;
+          const int i = r2 / g.Wp - 1, j = r2 - (i + 1) * g.Wp - 1;
+          const int HH = g.H * g.H;
+          const int s = i * g.H + j;
+          const int n = comp_of_site[s];
+          const bool data = (i < g.d) && (j < g.d);
+          unsigned bits = 0;
+          if (data && lg[0] > 0.0f) bits |= 1u;
+          if (data && lg[1] > 0.0f) bits |= 2u;
+          if (n >= 0 && n < g.K && lg[2] > 0.0f) bits |= 4u;
+          if (n >= g.K && lg[3] > 0.0f) bits |= 8u;
+          nib[(long long)b * g.V + (long long)t * HH + s] = (uint8_t)bits;
+          if (logits) {
+#pragma unroll
+            for (int o = 0; o < 4; ++o) logits[(((long long)b * 4 + o) * g.T + t) * HH + s] = lg[o];
+          }
+        }
+      }
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): partials read
+      __builtin_amdgcn_s_barrier();        // head_part is rewritten by the next tile
     }
+    if constexpr (CIN == 2) {
+      // next tile's planes written by every wave; this tile's reads done
+      __builtin_amdgcn_s_waitcnt(0xc07f);
+      __builtin_amdgcn_s_barrier();
+    }
+    tile = next;
+    cur_src = next_src;
   }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
-// LDS layout of one launch: [staging buffer 0][staging buffer 1] (the output
-// tile reuses this region) followed by the per-row tables.
-static void lds_layout(int cin, int cout, int span, size_t* abuf, size_t* region, size_t* total) {
-  if (cin == 2)
-    *abuf = ((size_t)span * 4 + 1023) / 1024 * 1024;  // whole 256-voxel staging rounds
-  else
-    *abuf = ((size_t)span * 64 + 4095) / 4096 * 4096;  // whole 256-granule staging rounds
-  size_t out = 256 * (size_t)(cout * 2 + kOutPad);
-  *region = 2 * *abuf > out ? 2 * *abuf : out;
-  *total = *region + 256 * (sizeof(long long) + sizeof(int));
-}
+// LDS bytes of one launch (layout at the top of the kernel).
+static size_t lds_bytes(int cout) { return 2 * ABUF + TRASH + (2 * 256 * 4 + 5 * cout) * sizeof(float); }
 
 size_t conv_bf16_lds_bytes(int cin, int span) {
-  size_t a, r, t;
-  lds_layout(cin, 128, span, &a, &r, &t);
-  return t;
+  (void)cin;
+  (void)span;
+  return lds_bytes(128);
 }
 
-template <int CIN, int COUT>
+int conv_bf16_max_span() { return RMAX * 256 / 4; }
+
+template <int CIN, int COUT, bool HEAD>
 static hipError_t launch_one(const Geom& g, const Tiling& tl, int act, const void* x, void* y,
-                             const void* wfrag, const float* bias, int batch, hipStream_t stream) {
-  size_t abuf, region, lds;
-  lds_layout(CIN, COUT, tl.span, &abuf, &region, &lds);
+                             const void* wfrag, const float* bias, const float* head_w, const float* head_b,
+                             const int32_t* comp_of_site, uint8_t* nib, float* logits, int batch,
+                             int n_workgroups, hipStream_t stream) {
+  const size_t lds = lds_bytes(COUT);
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)conv_bf16_kernel<CIN, COUT>,
+    hipError_t e = hipFuncSetAttribute((const void*)conv_bf16_kernel<CIN, COUT, HEAD>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  long long nt = tl.ntiles;
-  unsigned grid = (unsigned)(((nt + 7) / 8) * 8);
-  hipLaunchKernelGGL((conv_bf16_kernel<CIN, COUT>), dim3(grid), dim3(256), lds, stream, g, tl, act,
-                     (const uint16_t*)x, (uint16_t*)y, (const u32x4*)wfrag, bias, batch, (int)abuf,
-                     (int)region);
+  const long long nwg = conv_workgroups(tl.ntiles, n_workgroups);
+  hipLaunchKernelGGL((conv_bf16_kernel<CIN, COUT, HEAD>), dim3((unsigned)nwg), dim3(256), lds, stream, g, tl,
+                     act, (const uint16_t*)x, (uint16_t*)y, (const u32x4*)wfrag, bias, head_w, head_b,
+                     comp_of_site, nib, logits, batch);
   return hipGetLastError();
 }
 
-hipError_t launch_conv_bf16(const Geom& g, const Tiling& tl, int cin, int cout, int act, const void* x,
-                            void* y, const void* wfrag, const float* bias, int batch,
-                            hipStream_t stream) {
-  if (cin == 2 && cout == 64) return launch_one<2, 64>(g, tl, act, x, y, wfrag, bias, batch, stream);
-  if (cin == 2 && cout == 128) return launch_one<2, 128>(g, tl, act, x, y, wfrag, bias, batch, stream);
-  if (cin == 64 && cout == 64) return launch_one<64, 64>(g, tl, act, x, y, wfrag, bias, batch, stream);
-  if (cin == 128 && cout == 128) return launch_one<128, 128>(g, tl, act, x, y, wfrag, bias, batch, stream);
-  if (cin == 64 && cout == 128) return launch_one<64, 128>(g, tl, act, x, y, wfrag, bias, batch, stream);
-  if (cin == 128 && cout == 64) return launch_one<128, 64>(g, tl, act, x, y, wfrag, bias, batch, stream);
+#define PD_CONV_CASE(CI, CO)                                                                                 \
+  if (cin == CI && cout == CO) {                                                                            \
+    if (head)                                                                                                \
+      return launch_one<CI, CO, true>(g, tl, act, x, y, wfrag, bias, head_w, head_b, comp_of_site, nib,       \
+                                      logits, batch, n_workgroups, stream);                                  \
+    return launch_one<CI, CO, false>(g, tl, act, x, y, wfrag, bias, head_w, head_b, comp_of_site, nib,        \
+                                     logits, batch, n_workgroups, stream);                                   \
+  }
+
+hipError_t launch_conv_bf16(const Geom& g, const Tiling& tl, int cin, int cout, int act, const void* x, void* y,
+                            const void* wfrag, const float* bias, int head, const float* head_w,
+                            const float* head_b, const int32_t* comp_of_site, uint8_t* nib, float* logits,
+                            int batch, int n_workgroups, hipStream_t stream) {
+  PD_CONV_CASE(2, 64)
+  PD_CONV_CASE(2, 128)
+  PD_CONV_CASE(64, 64)
+  PD_CONV_CASE(128, 128)
+  PD_CONV_CASE(64, 128)
+  PD_CONV_CASE(128, 64)
   return hipErrorInvalidValue;
 }
 

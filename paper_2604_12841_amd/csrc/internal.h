@@ -54,10 +54,24 @@ constexpr int kTileRows = 256;
 hipError_t launch_unpack(const Geom& g, const int32_t* comp_of_site, const uint64_t* det, int batch,
                          void* out, int out_padded, int fp32, hipStream_t stream);
 
-hipError_t launch_conv_bf16(const Geom& g, const Tiling& tl, int cin, int cout, int act,
-                            const void* x, void* y, const void* wfrag, const float* bias, int batch,
-                            hipStream_t stream);
+// One 3x3x3 bf16 layer.  head != 0: the 1x1x1 head (head_w [4][cout] fp32,
+// bf16-valued; head_b [4]) and the threshold are applied in the epilogue,
+// which writes flip nibbles (and logits if non-null) instead of y.
+hipError_t launch_conv_bf16(const Geom& g, const Tiling& tl, int cin, int cout, int act, const void* x,
+                            void* y, const void* wfrag, const float* bias, int head, const float* head_w,
+                            const float* head_b, const int32_t* comp_of_site, uint8_t* nib, float* logits,
+                            int batch, int n_workgroups, hipStream_t stream);
 size_t conv_bf16_lds_bytes(int cin, int span);
+int conv_bf16_max_span();  // staged voxels a tile may need
+
+// Persistent workgroups of a conv launch: one per CU (n_workgroups), a
+// multiple of 8 (one per XCD round-robin slot), never more than the tiles
+// need.
+__host__ __device__ inline long long conv_workgroups(long long ntiles, long long n_workgroups) {
+  long long cap = (ntiles + 7) / 8 * 8;
+  long long n = (n_workgroups + 7) / 8 * 8;
+  return n < cap ? n : cap;
+}
 
 hipError_t launch_conv_fp32(const Geom& g, int cin, int cout, int act, const float* x, float* y,
                             const float* w, const float* bias, int batch, hipStream_t stream);
