@@ -22,6 +22,9 @@ FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-I" + os.path.join(ROOT, "include"), "-I" + CSRC,
     "-Wall", "-Wno-unused-function",
+    # the conv kernel's 54-step K loop must unroll fully (its register rings
+    # are indexed by the step)
+    "-mllvm", "-pragma-unroll-threshold=100000",
 ]
 
 

@@ -125,21 +125,22 @@ float bf16_value(float f) {
 // per sample whose double-buffered 32-channel staging fits in LDS.
 
 long long flat_span(const Geom& g, long long seg_len, long long nseg, int batch) {
-  // exact maximum staged span over all tiles of `batch` samples
-  long long best = 0, halo = g.P + g.Wp + 1;
+  // exact maximum staged span (line space, see pd::Tiling) over all tiles of
+  // `batch` samples
+  long long best = 0, halo = pd::line_plane(g) + g.H + 1;
   long long tiles = (seg_len + pd::kTileRows - 1) / pd::kTileRows;
   for (long long s = 0; s < nseg; ++s)
     for (long long k = 0; k < tiles; ++k) {
       long long u0 = s * seg_len + k * pd::kTileRows;
       long long u1 = std::min(u0 + pd::kTileRows, std::min((s + 1) * seg_len, (long long)batch * g.V)) - 1;
       if (u1 < u0) continue;
-      auto pidx = [&](long long u) {
+      auto lidx = [&](long long u) {
         long long b = u / g.V, v = u % g.V;
         int HH = g.H * g.H;
         int t = (int)(v / HH), r = (int)(v % HH);
-        return pd::padded_index(g, (int)b, t, r / g.H, r % g.H);
+        return pd::line_index(g, (int)b, t, r / g.H, r % g.H);
       };
-      best = std::max(best, pidx(u1) - pidx(u0) + 2 * halo + 1);
+      best = std::max(best, lidx(u1) - lidx(u0) + 2 * halo + 1);
     }
   return best;
 }
@@ -164,8 +165,8 @@ Tiling plan_tiling(const Geom& g, int max_batch) {
     t.mode = 0;
     t.seg_len = g.V;
     t.tiles_per_seg = (g.V + pd::kTileRows - 1) / pd::kTileRows;
-    t.sa = g.P;
-    t.sb = g.Wp;
+    t.sa = pd::line_plane(g);
+    t.sb = g.H;
     t.span = (int)std::min<long long>(flat_span(g, g.V, 1, 1), 1 << 30);
     consider(t, (long long)t.tiles_per_seg * pd::kTileRows);
   }
@@ -175,8 +176,8 @@ Tiling plan_tiling(const Geom& g, int max_batch) {
     t.mode = 0;
     t.seg_len = -1;  // set per run to batch * V
     t.tiles_per_seg = 0;
-    t.sa = g.P;
-    t.sb = g.Wp;
+    t.sa = pd::line_plane(g);
+    t.sb = g.H;
     int nb = std::min(max_batch, 256);
     t.span = (int)std::min<long long>(flat_span(g, (long long)nb * g.V, 1, nb), 1 << 30);
     consider(t, (long long)g.V + 1);  // +1: prefer per-sample tiles at equal cost
@@ -197,12 +198,17 @@ Tiling plan_tiling(const Geom& g, int max_batch) {
       t.sa = (BI + 2) * (BJ + 2);
       t.sb = BJ + 2;
       t.span = (BT + 2) * (BI + 2) * (BJ + 2);
-      consider(t, (long long)t.ntT * t.ntI * t.ntJ * pd::kTileRows);
+      // a 16-lane LDS read spans two staged lines unless BJ is a multiple of
+      // 16, which costs about one extra LDS cycle per read: weigh it as rows
+      const long long rows = (long long)t.ntT * t.ntI * t.ntJ * pd::kTileRows;
+      consider(t, (BJ % 16 == 0) ? rows : rows + rows / 4);
     }
   return best;
 }
 
 void tiling_for_batch(Tiling* t, const Geom& g, int batch) {
+  t->div_a = pd::make_fastdiv((uint32_t)t->sa);
+  t->div_b = pd::make_fastdiv((uint32_t)t->sb);
   if (t->mode == 0) {
     if (t->seg_len < 0 || t->tiles_per_seg == 0) {
       // flat across samples
@@ -342,7 +348,7 @@ pd_status enqueue_run(pd_predecoder* h, hipStream_t st, const uint64_t* det, int
   if (s != PD_OK) return s;
   const void* x = h->planes;
   Tiling tl = h->tiling;
-  tiling_for_batch(&tl, g, batch);
+  if (!fp32) tiling_for_batch(&tl, g, batch);
   for (int l = 0; l < n - 1; ++l) {
     if ((s = mark()) != PD_OK) return s;
     void* y = h->act[l & 1];
@@ -425,7 +431,9 @@ pd_status predecoder_create(const float* weights, size_t n_weights, int32_t d, i
   Geom g = make_geom(d, T);
   if (!supported(g, layers, n_layers, dtype)) return PD_ERR_UNSUPPORTED;
   // kernels index voxels of a batch with 32-bit integers
-  if ((long long)max_batch * g.V >= (1ll << 31) || (long long)max_batch * (g.Wd + g.Wf) >= (1ll << 31))
+  if ((long long)max_batch * g.V >= (1ll << 31) || (long long)max_batch * (g.Wd + g.Wf) >= (1ll << 31) ||
+      (long long)max_batch * g.S >= (1ll << 31) ||
+      (long long)max_batch * (T + 2) * pd::line_plane(g) >= (1ll << 31))
     return PD_ERR_UNSUPPORTED;
 
   int ndev = 0;

@@ -21,8 +21,11 @@
 //     (HBM/L2 -> LDS, no registers).  The next chunk -- or, during the last
 //     chunk, the next tile's first chunk -- is in flight while the current one
 //     feeds the MFMAs.
-//   * The four 16-byte granules of a voxel are XOR-swizzled by (voxel >> 1) & 3
-//     so the 32 voxels of a fragment (64-byte stride) spread over the banks.
+//   * The four 16-byte granules of a voxel are XOR-swizzled by (voxel >> 2) & 3.
+//     The LDS serves a 16-byte read 16 lanes at a time over 64 banks; with
+//     the swizzle any 16 consecutive staged voxels hit 16 distinct bank
+//     groups, and the tilings keep the 16 voxels of a read consecutive (flat
+//     tiles stage only the real columns; box tiles are 16 voxels wide in j).
 //   * The 54 k-steps of a chunk (27 taps x 2) are fully unrolled and software
 //     pipelined: activation fragments are read from LDS one step ahead, weight
 //     fragments (pre-arranged at create time in MFMA operand order, one
@@ -60,6 +63,23 @@ constexpr int ABUF = RMAX * 256 * 16;   // bytes per staging buffer
 constexpr int PLANE_RMAX = 4;           // layer 1: rounds of 256 voxels x 4 bytes
 constexpr int TRASH = 256 * 16;         // destination of unused rounds
 
+// LDS layout of one workgroup (byte offsets): two staging buffers, the
+// scratch round, a 256-byte zero region (256-aligned, for halo-column reads),
+// the head partial sums [2][256][4] fp32, the bias [COUT] and the head
+// weights [4][COUT].
+template <int COUT>
+struct LdsLayout {
+  static constexpr int buf1 = ABUF;
+  static constexpr int trash = 2 * ABUF;
+  static constexpr int zero = trash + TRASH;
+  static constexpr int head = zero + 256;
+  static constexpr int bias = head + 2 * 256 * 4 * 4;
+  static constexpr int headw = bias + COUT * 4;
+  static constexpr int total = headw + 4 * COUT * 4;
+  static_assert(zero % 256 == 0, "zero region must be 256-aligned");
+  static_assert(total <= 160 * 1024, "LDS budget");
+};
+
 __device__ __forceinline__ float activation(float y, int act) {
   if (act == 1) {  // GELU, tanh form: 0.5 y (1 + tanh(u)) = y / (1 + exp(-2u))
     const float k0 = 0.7978845608028654f;          // sqrt(2 / pi)
@@ -79,11 +99,13 @@ __device__ __forceinline__ uint32_t bf16_bits(float v) {
 __device__ __forceinline__ float bf16_round(float v) { return __uint_as_float(bf16_bits(v) << 16); }
 
 // Row r (0..255) of tile `tile`: false if the row is outside the volume,
-// else its padded output index.  Also the LDS voxel of the row's (0,0,0) tap
-// and the padded index of staged voxel 0.  32-bit arithmetic: the host
-// guarantees max_batch * V < 2^31.
+// else its padded output index (pidx) and its column j (col).  Also the LDS
+// voxel of the row's (0,0,0) tap (lds_base) and the staging origin: the
+// line-space index of staged voxel 0 (mode 0) or its padded index (mode 1).
+// 32-bit voxel counts: the host guarantees max_batch * V < 2^31.
 __host__ __device__ inline bool tile_row(const Geom& g, const Tiling& tl, int tile, int r, int batch,
-                                         long long* pidx, int* lds_base, long long* stage_origin) {
+                                         long long* pidx, int* lds_base, long long* stage_origin,
+                                         int* col = nullptr) {
   const int HH = g.H * g.H;
   if (tl.mode == 0) {
     const int seg = tile / tl.tiles_per_seg;
@@ -92,19 +114,21 @@ __host__ __device__ inline bool tile_row(const Geom& g, const Tiling& tl, int ti
     const int b0 = u0 / g.V;
     const int v0 = u0 - b0 * g.V;
     const int t0 = v0 / HH, s0 = v0 - t0 * HH;
-    const long long p0 = padded_index(g, b0, t0, s0 / g.H, s0 % g.H);
-    *stage_origin = p0 - (g.P + g.Wp + 1);
+    const long long l0 = line_index(g, b0, t0, s0 / g.H, s0 % g.H);
+    *stage_origin = l0 - (line_plane(g) + g.H + 1);
     const int u = u0 + r;
     if (k0 + r >= tl.seg_len || u >= batch * g.V) {
       *lds_base = 0;
+      if (col) *col = -1;
       return false;
     }
     const int b = u / g.V;
     const int v = u - b * g.V;
     const int t = v / HH, s = v - t * HH;
-    const long long p = padded_index(g, b, t, s / g.H, s % g.H);
-    *pidx = p;
-    *lds_base = (int)(p - p0);
+    const int i = s / g.H, j = s - i * g.H;
+    *pidx = padded_index(g, b, t, i, j);
+    *lds_base = (int)(line_index(g, b, t, i, j) - l0);
+    if (col) *col = j;
     return true;
   } else {
     const int per = tl.ntT * tl.ntI * tl.ntJ;
@@ -120,6 +144,7 @@ __host__ __device__ inline bool tile_row(const Geom& g, const Tiling& tl, int ti
     const int t = t0 + a, i = i0 + c, j = j0 + e;
     const bool ok = (r < tl.BT * bij) && t < g.T && i < g.H && j < g.H;
     *lds_base = ok ? (a * (tl.BI + 2) + c) * (tl.BJ + 2) + e : 0;
+    if (col) *col = ok ? j : -1;
     if (!ok) return false;
     *pidx = padded_index(g, b, t, i, j);
     return true;
@@ -148,7 +173,7 @@ __host__ __device__ inline BoxOrigin box_origin(const Geom& g, const Tiling& tl,
 __host__ __device__ inline long long staged_voxel(const Geom& g, const Tiling& tl, long long origin,
                                                   const BoxOrigin& bo, int vv, long long limit) {
   if (tl.mode == 0) {
-    const long long p = origin + vv;
+    const long long p = line_to_padded(g, origin + vv);
     return (p < limit) ? p : 0;
   }
   const int bj2 = tl.BJ + 2, bij2 = (tl.BI + 2) * bj2;
@@ -173,23 +198,48 @@ __host__ __device__ inline int tile_of(int wg, int nwg, int it, int ntiles) {
   return t < ntiles ? t : -1;
 }
 
-// Staging source of a tile: its staged-voxel origin and box origin.
+// Staging source of a tile: its staging origin (see tile_row) and box origin.
 struct StageSrc {
   long long origin;
   BoxOrigin bo;
 };
 
-// Granule q = 256 k + 64 wave + lane of the staging buffer holds logical
-// granule (q & 3) ^ ((vv >> 1) & 3) of staged voxel vv = q >> 2 (32 channels
-// of chunk `chunk`).  Returns that granule (a dummy one past the footprint).
-template <int CIN>
+// Global padded voxel of staged voxel vv; -1 when it is outside the batch or
+// the sample's padded box (such voxels only feed rows that are discarded).
+template <int MODE>
+__host__ __device__ inline long long staged_voxel_fast(const Geom& g, const Tiling& tl, const StageSrc& src,
+                                                       int vv, long long limit) {
+  if constexpr (MODE == 0) {
+    const uint32_t u = (uint32_t)(src.origin + vv);  // < 2^31 (host check)
+    const uint32_t tp = fastdiv(u, tl.div_a);
+    const uint32_t rem = u - tp * (uint32_t)tl.sa;
+    const uint32_t ip = fastdiv(rem, tl.div_b);
+    const uint32_t jj = rem - ip * (uint32_t)g.H;
+    const long long p = (long long)tp * g.P + (long long)ip * g.Wp + jj + 1;
+    return p < limit ? p : -1;
+  } else {
+  const int a = (int)fastdiv((uint32_t)vv, tl.div_a);
+  const int rem = vv - a * tl.sa;
+  const int c = (int)fastdiv((uint32_t)rem, tl.div_b);
+  const int e = rem - c * tl.sb;
+  if (src.bo.t0 + a >= g.T + 2 || src.bo.i0 + c >= g.Wp || src.bo.j0 + e >= g.Wp) return -1;
+  return src.origin + (long long)a * g.P + (long long)c * g.Wp + e;
+  }
+}
+
+// Staging granule q = 256 k + 64 wave + lane: the buffer's granule q holds
+// logical granule (q & 3) ^ ((vv >> 2) & 3) of staged voxel vv = q >> 2 (of
+// 32-channel chunk `chunk`).  Granules past the footprint (or of voxels
+// outside the volume) read voxel 0 instead.
+template <int CIN, int MODE>
 __device__ __forceinline__ u32x4 stage_load(const Geom& g, const Tiling& tl, const uint16_t* __restrict__ x,
                                             const StageSrc& src, long long limit, int chunk, int ngran, int k,
                                             int wave, int lane) {
   const int q = k * 256 + wave * 64 + lane;
   const int vv = q >> 2;
-  const int sg = (q & 3) ^ ((vv >> 1) & 3);
-  const long long gv = staged_voxel(g, tl, src.origin, src.bo, q < ngran ? vv : 0, limit);
+  const int sg = (q & 3) ^ ((vv >> 2) & 3);
+  long long gv = staged_voxel_fast<MODE>(g, tl, src, vv, limit);
+  gv = (q < ngran && gv >= 0) ? gv : 0;
   return *reinterpret_cast<const u32x4*>(x + gv * CIN + chunk * KC + sg * 8);
 }
 
@@ -201,7 +251,7 @@ __device__ __forceinline__ uint32_t plane_load(const Geom& g, const Tiling& tl, 
   return reinterpret_cast<const uint32_t*>(x)[gv];
 }
 
-template <int CIN, int COUT, bool HEAD>
+template <int CIN, int COUT, bool HEAD, int MODE>
 __global__ void __launch_bounds__(256) conv_bf16_kernel(Geom g, Tiling tl, int act,
                                                         const uint16_t* __restrict__ x,
                                                         uint16_t* __restrict__ y,
@@ -227,12 +277,16 @@ __global__ void __launch_bounds__(256) conv_bf16_kernel(Geom g, Tiling tl, int a
 
   // LDS: [staging buffer 0][staging buffer 1][scratch round][head partials
   // [2][256][4] fp32][bias [COUT]][head weights [4][COUT]]
+  using L = LdsLayout<COUT>;
   lds_char* const lds = (lds_char*)smem;
-  lds_char* const trash = lds + 2 * ABUF;
-  lds_float* const head_part = (lds_float*)(trash + TRASH);
-  lds_float* const bias_s = head_part + 2 * 256 * 4;
-  lds_float* const headw_s = bias_s + COUT;
+  lds_char* const trash = lds + L::trash;
+  lds_char* const zero = lds + L::zero;
+  lds_float* const head_part = (lds_float*)(lds + L::head);
+  lds_float* const bias_s = (lds_float*)(lds + L::bias);
+  lds_float* const headw_s = (lds_float*)(lds + L::headw);
   for (int e = tid; e < COUT; e += 256) bias_s[e] = bias[e];
+  if (tid < 64) ((lds_u32_w*)zero)[tid] = 0u;
+  const uint32_t zero_addr = (uint32_t)(uintptr_t)zero;
   if (HEAD)
     for (int e = tid; e < 4 * COUT; e += 256) headw_s[e] = head_w[e];
 
@@ -259,7 +313,7 @@ __global__ void __launch_bounds__(256) conv_bf16_kernel(Geom g, Tiling tl, int a
   } else {
 #pragma unroll
     for (int k = 0; k < RMAX; ++k) {
-      const u32x4 v = stage_load<CIN>(g, tl, x, cur_src, limit, 0, ngran, k, wave, lane);
+      const u32x4 v = stage_load<CIN, MODE>(g, tl, x, cur_src, limit, 0, ngran, k, wave, lane);
       *(lds_u32x4_w*)(lds + (k * 256 + wave * 64 + lane) * 16) = v;
     }
   }
@@ -283,13 +337,16 @@ __global__ void __launch_bounds__(256) conv_bf16_kernel(Geom g, Tiling tl, int a
     // rows of this lane: voxel 32 mb + l32 of the wave's 128
     int rb[MB];
     long long pidx[MB];
+    uint32_t em0[MB], em2[MB];  // flat tiles: reads of the left / right halo column go to `zero`
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
       long long p = -1, o;
-      int lb = 0;
-      bool ok = tile_row(g, tl, tile, wm * 128 + mb * 32 + l32, batch, &p, &lb, &o);
+      int lb = 0, col = -1;
+      bool ok = tile_row(g, tl, tile, wm * 128 + mb * 32 + l32, batch, &p, &lb, &o, &col);
       rb[mb] = lb;
       pidx[mb] = ok ? p : -1;
+      em0[mb] = (MODE == 0 && col == 0) ? 0xFFFFFF00u : 0u;
+      em2[mb] = (MODE == 0 && col == g.H - 1) ? 0xFFFFFF00u : 0u;
     }
 
     f32x16 acc[MB][NB];
@@ -323,6 +380,7 @@ __global__ void __launch_bounds__(256) conv_bf16_kernel(Geom g, Tiling tl, int a
             if (tap < 27) {
               const int dt = tap / 9, di = (tap / 3) % 3, dj = tap % 3;
               val = a32[rb[mb] + dt * tl.sa + di * tl.sb + dj];
+              if ((dj == 0 && em0[mb]) || (dj == 2 && em2[mb])) val = 0;
             }
             av[q] = val;
           }
@@ -353,48 +411,70 @@ __global__ void __launch_bounds__(256) conv_bf16_kernel(Geom g, Tiling tl, int a
         // addresses of this chunk from being hoisted out of the chunk loop
         // (they would occupy 216 VGPRs).
         int rbc[MB];
+        uint32_t e0c[MB], e2c[MB];
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
           rbc[mb] = rb[mb];
-          asm volatile("" : "+v"(rbc[mb]));
+          e0c[mb] = em0[mb];
+          e2c[mb] = em2[mb];
+          asm volatile("" : "+v"(rbc[mb]), "+v"(e0c[mb]), "+v"(e2c[mb]));
         }
+        // LDS address of the fragment of row block mb at voxel offset toff,
+        // granule sg; halo-column taps of flat tiles go to the zero region
+        // (same bank group, so the read stays conflict-free)
+        auto frag_addr = [&](int mb, int st) -> uint32_t {
+          const int tap = st >> 1, ks = st & 1;
+          const int dt = tap / 9, di = (tap / 3) % 3, dj = tap % 3;
+          const int vox = rbc[mb] + dt * tl.sa + di * tl.sb + dj;
+          const int sg = ks * 2 + half;
+          uint32_t a = (uint32_t)(uintptr_t)(cur + vox * 64 + ((sg ^ ((vox >> 2) & 3)) << 4));
+          if (MODE == 0 && dj == 0) a = (a & ~e0c[mb]) | (zero_addr & e0c[mb]);
+          if (MODE == 0 && dj == 2) a = (a & ~e2c[mb]) | (zero_addr & e2c[mb]);
+          return a;
+        };
+        // Each step has two scheduling regions: (A) the LDS reads of the next
+        // step's activation fragments (addresses computed a step earlier) and
+        // the weight loads five steps ahead; (B) this step's 8 MFMAs, with the
+        // address arithmetic for two steps ahead and the staging work in
+        // their shadow.  A fragment read is issued a full step (8 MFMAs)
+        // before its use.
         u32x4 av[2][MB];
+        uint32_t an[MB];  // LDS addresses of the fragments of step st + 1
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb) {
-          const int vox = rbc[mb];
-          av[0][mb] = *(lds_u32x4*)(cur + vox * 64 + ((half ^ ((vox >> 1) & 3)) << 4));
-        }
+        for (int mb = 0; mb < MB; ++mb) av[0][mb] = *(lds_u32x4*)(uintptr_t)frag_addr(mb, 0);
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) an[mb] = frag_addr(mb, 1);
         const int gbase = chunk * STEPS;  // tile-step of this chunk's step 0
 #pragma unroll
         for (int st = 0; st < STEPS; ++st) {
+          // ---- region A ----
+          if (st + 1 < STEPS) {
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) av[(st + 1) & 1][mb] = *(lds_u32x4*)(uintptr_t)an[mb];
+          }
+          {
+            int gs = gbase + st + BRING - 1;  // wraps into the next tile's steps
+            if (gs >= TSTEPS) gs -= TSTEPS;
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) bq[(st + BRING - 1) % BRING][nb] = wlane[(gs * NBT + nb) * 64];
+          }
+          __builtin_amdgcn_sched_barrier(0);
+          // ---- region B ----
+          if (st + 2 < STEPS) {
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) an[mb] = frag_addr(mb, st + 2);
+          }
           // staging of the next chunk: round k is loaded at step 3k and
           // stored to LDS at step 3k + 6
-          if (st % 3 == 0 && st / 3 < RMAX)
-            stg[(st / 3) % 3] = stage_load<CIN>(g, tl, x, ssrc, limit, schunk, sgran, st / 3, wave, lane);
+          if (st % 3 == 0 && st / 3 < RMAX) {
+            const int k = st / 3;
+            stg[k % 3] = stage_load<CIN, MODE>(g, tl, x, ssrc, limit, schunk, sgran, k, wave, lane);
+          }
           if (st >= 6 && (st - 6) % 3 == 0 && (st - 6) / 3 < RMAX) {
             const int k = (st - 6) / 3;
             lds_char* dst = (k * 256 < sgran) ? oth + (k * 256 + wave * 64 + lane) * 16
                                               : trash + (wave * 64 + lane) * 16;
             *(lds_u32x4_w*)dst = stg[k % 3];
-          }
-          // activation fragments of step st + 1
-          if (st + 1 < STEPS) {
-            const int tap = (st + 1) >> 1, ks = (st + 1) & 1;
-            const int dt = tap / 9, di = (tap / 3) % 3, dj = tap % 3;
-            const int toff = dt * tl.sa + di * tl.sb + dj;
-            const int sg = ks * 2 + half;
-#pragma unroll
-            for (int mb = 0; mb < MB; ++mb) {
-              const int vox = rbc[mb] + toff;
-              av[(st + 1) & 1][mb] = *(lds_u32x4*)(cur + vox * 64 + ((sg ^ ((vox >> 1) & 3)) << 4));
-            }
-          }
-          // weight fragments of tile-step gs + BRING - 1 (wrapping into the next tile)
-          {
-            int gs = gbase + st + BRING - 1;
-            if (gs >= TSTEPS) gs -= TSTEPS;
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb) bq[(st + BRING - 1) % BRING][nb] = wlane[(gs * NBT + nb) * 64];
           }
 #pragma unroll
           for (int mb = 0; mb < MB; ++mb)
@@ -529,7 +609,9 @@ __global__ void __launch_bounds__(256) conv_bf16_kernel(Geom g, Tiling tl, int a
 }
 
 // LDS bytes of one launch (layout at the top of the kernel).
-static size_t lds_bytes(int cout) { return 2 * ABUF + TRASH + (2 * 256 * 4 + 5 * cout) * sizeof(float); }
+static size_t lds_bytes(int cout) {
+  return cout == 64 ? (size_t)LdsLayout<64>::total : (size_t)LdsLayout<128>::total;
+}
 
 size_t conv_bf16_lds_bytes(int cin, int span) {
   (void)cin;
@@ -539,7 +621,7 @@ size_t conv_bf16_lds_bytes(int cin, int span) {
 
 int conv_bf16_max_span() { return RMAX * 256 / 4; }
 
-template <int CIN, int COUT, bool HEAD>
+template <int CIN, int COUT, bool HEAD, int MODE>
 static hipError_t launch_one(const Geom& g, const Tiling& tl, int act, const void* x, void* y,
                              const void* wfrag, const float* bias, const float* head_w, const float* head_b,
                              const int32_t* comp_of_site, uint8_t* nib, float* logits, int batch,
@@ -547,13 +629,13 @@ static hipError_t launch_one(const Geom& g, const Tiling& tl, int act, const voi
   const size_t lds = lds_bytes(COUT);
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)conv_bf16_kernel<CIN, COUT, HEAD>,
+    hipError_t e = hipFuncSetAttribute((const void*)conv_bf16_kernel<CIN, COUT, HEAD, MODE>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
   const long long nwg = conv_workgroups(tl.ntiles, n_workgroups);
-  hipLaunchKernelGGL((conv_bf16_kernel<CIN, COUT, HEAD>), dim3((unsigned)nwg), dim3(256), lds, stream, g, tl,
+  hipLaunchKernelGGL((conv_bf16_kernel<CIN, COUT, HEAD, MODE>), dim3((unsigned)nwg), dim3(256), lds, stream, g, tl,
                      act, (const uint16_t*)x, (uint16_t*)y, (const u32x4*)wfrag, bias, head_w, head_b,
                      comp_of_site, nib, logits, batch);
   return hipGetLastError();
@@ -561,11 +643,17 @@ static hipError_t launch_one(const Geom& g, const Tiling& tl, int act, const voi
 
 #define PD_CONV_CASE(CI, CO)                                                                                 \
   if (cin == CI && cout == CO) {                                                                            \
+    if (head && tl.mode == 0)                                                                                \
+      return launch_one<CI, CO, true, 0>(g, tl, act, x, y, wfrag, bias, head_w, head_b, comp_of_site, nib,    \
+                                         logits, batch, n_workgroups, stream);                               \
     if (head)                                                                                                \
-      return launch_one<CI, CO, true>(g, tl, act, x, y, wfrag, bias, head_w, head_b, comp_of_site, nib,       \
-                                      logits, batch, n_workgroups, stream);                                  \
-    return launch_one<CI, CO, false>(g, tl, act, x, y, wfrag, bias, head_w, head_b, comp_of_site, nib,        \
-                                     logits, batch, n_workgroups, stream);                                   \
+      return launch_one<CI, CO, true, 1>(g, tl, act, x, y, wfrag, bias, head_w, head_b, comp_of_site, nib,    \
+                                         logits, batch, n_workgroups, stream);                               \
+    if (tl.mode == 0)                                                                                        \
+      return launch_one<CI, CO, false, 0>(g, tl, act, x, y, wfrag, bias, head_w, head_b, comp_of_site, nib,   \
+                                          logits, batch, n_workgroups, stream);                              \
+    return launch_one<CI, CO, false, 1>(g, tl, act, x, y, wfrag, bias, head_w, head_b, comp_of_site, nib,     \
+                                        logits, batch, n_workgroups, stream);                                \
   }
 
 hipError_t launch_conv_bf16(const Geom& g, const Tiling& tl, int cin, int cout, int act, const void* x, void* y,

@@ -31,13 +31,45 @@ __host__ __device__ inline long long padded_index(const Geom& g, int b, int t, i
 // Output-row tiling of one conv launch.  A tile is up to 256 output voxels:
 //  mode 0 (flat): 256 consecutive voxels of a segment of `seg_len` voxels in
 //    (b, t, i, j) order (seg_len = V keeps tiles inside one sample, B * V lets
-//    them cross samples); the staged input is the contiguous padded span
-//    from the first row's padded index - (P + Wp + 1) to the last row's
-//    + (P + Wp + 1).
+//    them cross samples).  The staged input lives in "line space": voxel
+//    (b, t, i, j) with -1 <= t <= T, -1 <= i <= d+1 and only the real columns
+//    0 <= j <= d has line-space index
+//        u = (b (T+2) + t + 1) * PU + (i + 1) * H + j,   PU = (H+2) H,
+//    which is linear in (t, i, j), so consecutive output voxels are
+//    consecutive staged voxels.  The zero halo columns are not staged: a tap
+//    that falls on one reads a zero region instead.  The staged span runs
+//    from u(first row) - (PU + H + 1) to u(last row) + (PU + H + 1).
 //  mode 1 (box): a BT x BI x BJ box of (t, i, j); the staged input is the
-//    (BT+2) x (BI+2) x (BJ+2) padded box around it.
+//    (BT+2) x (BI+2) x (BJ+2) padded box around it, halo included.
 // In both modes the LDS voxel of row r for tap (dt, di, dj) in {0,1,2}^3 is
 // row_base(r) + dt * sa + di * sb + dj.
+// Division by a runtime constant d >= 2 for numerators n < 2^31:
+// q = mulhi(n, m) >> s with s = ceil(log2 d) - 1, m = floor(2^(32+s) / d) + 1.
+// (m < 2^32 because 2^s < d; the error m d - 2^(32+s) <= d keeps
+// n (m d - 2^(32+s)) < 2^(32+s) for n < 2^31 <= 2^(32+s) / d.)
+struct FastDiv {
+  uint32_t m;
+  int s;
+};
+
+inline FastDiv make_fastdiv(uint32_t d) {
+  if (d < 2) return FastDiv{0u, 0};  // unused divisor; fastdiv is only valid for d >= 2
+  int c = 0;
+  while ((1u << c) < d) ++c;  // ceil(log2 d)
+  FastDiv f;
+  f.s = c - 1;
+  f.m = (uint32_t)((((unsigned long long)1) << (32 + f.s)) / d + 1);
+  return f;
+}
+
+__host__ __device__ inline uint32_t fastdiv(uint32_t n, FastDiv f) {
+#ifdef __HIP_DEVICE_COMPILE__
+  return __umulhi(n, f.m) >> f.s;
+#else
+  return (uint32_t)(((unsigned long long)n * f.m) >> 32) >> f.s;
+#endif
+}
+
 struct Tiling {
   int mode;
   long long seg_len;
@@ -46,7 +78,25 @@ struct Tiling {
   int sa, sb;
   int span;      // staged voxels per tile (upper bound), sizes the LDS buffers
   long long ntiles;
+  FastDiv div_a, div_b;  // staging decode: mode 0 by PU and H; mode 1 by (BI+2)(BJ+2) and BJ+2
 };
+
+__host__ __device__ inline int line_plane(const Geom& g) { return (g.H + 2) * g.H; }
+
+// Line-space index of voxel (b, t, i, j) (mode 0 staging, see Tiling).
+__host__ __device__ inline long long line_index(const Geom& g, int b, int t, int i, int j) {
+  return ((long long)b * (g.T + 2) + t + 1) * line_plane(g) + (long long)(i + 1) * g.H + j;
+}
+
+// Padded activation index of line-space voxel u.
+__host__ __device__ inline long long line_to_padded(const Geom& g, long long u) {
+  const int pu = line_plane(g);
+  const long long tp = u / pu;
+  const int rem = (int)(u - tp * pu);
+  const int ip = rem / g.H;
+  const int jj = rem - ip * g.H;
+  return tp * g.P + (long long)ip * g.Wp + jj + 1;
+}
 
 constexpr int kTileRows = 256;
 
