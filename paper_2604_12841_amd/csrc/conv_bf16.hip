@@ -21,11 +21,14 @@
 //     (HBM/L2 -> LDS, no registers).  The next chunk -- or, during the last
 //     chunk, the next tile's first chunk -- is in flight while the current one
 //     feeds the MFMAs.
-//   * The four 16-byte granules of a voxel are XOR-swizzled by (voxel >> 2) & 3.
-//     The LDS serves a 16-byte read 16 lanes at a time over 64 banks; with
-//     the swizzle any 16 consecutive staged voxels hit 16 distinct bank
-//     groups, and the tilings keep the 16 voxels of a read consecutive (flat
-//     tiles stage only the real columns; box tiles are 16 voxels wide in j).
+//   * A staged voxel occupies 80 bytes of LDS (its 64 bytes of channels plus
+//     16 of padding).  The LDS serves a 16-byte read 16 lanes at a time over
+//     64 banks (16 groups of 16 bytes); granule g of voxel v sits in bank
+//     group (5 v + g) mod 16, so any 16 consecutive staged voxels hit 16
+//     distinct groups, and the tilings keep the 16 voxels of a read
+//     consecutive (flat tiles stage only the real columns; box tiles are 16
+//     voxels wide in j).  Addresses stay linear: a fragment address is a
+//     per-lane base plus a tap offset common to the wave.
 //   * The 54 k-steps of a chunk (27 taps x 2) are fully unrolled and software
 //     pipelined: activation fragments are read from LDS one step ahead, weight
 //     fragments (pre-arranged at create time in MFMA operand order, one
@@ -51,29 +54,42 @@ typedef __attribute__((address_space(3))) const uint32_t lds_u32;
 typedef __attribute__((address_space(3))) float lds_float;
 typedef __attribute__((address_space(3))) u32x4 lds_u32x4_w;
 typedef __attribute__((address_space(3))) uint32_t lds_u32_w;
+typedef __attribute__((address_space(3))) u32x2 lds_u32x2_w;
+typedef __attribute__((address_space(3))) int lds_i32;
 
 constexpr int KC = 32;     // input channels per LDS chunk
 constexpr int STEPS = 54;  // k-steps per chunk: 27 taps x 2 (16 channels each)
 constexpr int BRING = 6;   // weight-fragment ring depth (prefetch distance BRING - 1)
-// Every chunk is staged with exactly RMAX rounds of 256 16-byte granules
-// (1024 voxels at most); rounds past the footprint load voxel 0 and store to a
+constexpr int NT = 512;    // threads per workgroup: 8 wave64, two per SIMD
+// Every chunk is staged with exactly RMAX rounds of NT 16-byte granules (896
+// voxels at most); rounds past the footprint load voxel 0 and store to a
 // scratch region, so every wave issues the same fixed sequence.
-constexpr int RMAX = 16;
-constexpr int ABUF = RMAX * 256 * 16;   // bytes per staging buffer
-constexpr int PLANE_RMAX = 4;           // layer 1: rounds of 256 voxels x 4 bytes
-constexpr int TRASH = 256 * 16;         // destination of unused rounds
+constexpr int RMAX = 7;
+constexpr int VSTRIDE = 80;                            // LDS bytes per staged voxel
+constexpr int ABUF = RMAX * (NT / 4) * VSTRIDE;        // bytes per staging buffer
+constexpr int PLANE_RMAX = 2;                          // layer 1: rounds of NT voxels x 4 bytes
+constexpr int TRASH = NT * 16;                         // destination of unused rounds
+
+// Wave split of the 256 x COUT output tile: WN waves across the channels (32
+// each), WM across the voxels (ROWS each, MB blocks of 32).
+template <int COUT>
+struct WaveSplit {
+  static constexpr int WN = COUT / 32;
+  static constexpr int WM = (NT / 64) / WN;
+  static constexpr int ROWS = 256 / WM;
+  static constexpr int MB = ROWS / 32;
+};
 
 // LDS layout of one workgroup (byte offsets): two staging buffers, the
 // scratch round, a 256-byte zero region (256-aligned, for halo-column reads),
-// the head partial sums [2][256][4] fp32, the bias [COUT] and the head
-// weights [4][COUT].
+// the bias [COUT] and the head weights [4][COUT].  The epilogues reuse the
+// staging buffer the tile read last (output tile, row table, head partials).
 template <int COUT>
 struct LdsLayout {
   static constexpr int buf1 = ABUF;
   static constexpr int trash = 2 * ABUF;
   static constexpr int zero = trash + TRASH;
-  static constexpr int head = zero + 256;
-  static constexpr int bias = head + 2 * 256 * 4 * 4;
+  static constexpr int bias = zero + 256;
   static constexpr int headw = bias + COUT * 4;
   static constexpr int total = headw + 4 * COUT * 4;
   static_assert(zero % 256 == 0, "zero region must be 256-aligned");
@@ -227,68 +243,65 @@ __host__ __device__ inline long long staged_voxel_fast(const Geom& g, const Tili
   }
 }
 
-// Staging granule q = 256 k + 64 wave + lane: the buffer's granule q holds
-// logical granule (q & 3) ^ ((vv >> 2) & 3) of staged voxel vv = q >> 2 (of
-// 32-channel chunk `chunk`).  Granules past the footprint (or of voxels
+// Staging granule q = NT k + tid is granule q & 3 (16 bytes) of
+// staged voxel vv = q >> 2 (of 32-channel chunk `chunk`); it goes to LDS byte
+// vv * VSTRIDE + 16 (q & 3).  Granules past the footprint (or of voxels
 // outside the volume) read voxel 0 instead.
 template <int CIN, int MODE>
 __device__ __forceinline__ u32x4 stage_load(const Geom& g, const Tiling& tl, const uint16_t* __restrict__ x,
                                             const StageSrc& src, long long limit, int chunk, int ngran, int k,
-                                            int wave, int lane) {
-  const int q = k * 256 + wave * 64 + lane;
+                                            int tid) {
+  const int q = k * NT + tid;
   const int vv = q >> 2;
-  const int sg = (q & 3) ^ ((vv >> 2) & 3);
+  const int sg = q & 3;
   long long gv = staged_voxel_fast<MODE>(g, tl, src, vv, limit);
   gv = (q < ngran && gv >= 0) ? gv : 0;
   return *reinterpret_cast<const u32x4*>(x + gv * CIN + chunk * KC + sg * 8);
 }
 
-// Layer 1: both channels (4 bytes) of staged voxel 256 k + 64 wave + lane.
+// Layer 1: both channels (4 bytes) of staged voxel NT k + tid.
 __device__ __forceinline__ uint32_t plane_load(const Geom& g, const Tiling& tl, const uint16_t* __restrict__ x,
-                                               const StageSrc& src, long long limit, int k, int wave, int lane) {
-  const int vv = k * 256 + wave * 64 + lane;
+                                               const StageSrc& src, long long limit, int k, int tid) {
+  const int vv = k * NT + tid;
   const long long gv = staged_voxel(g, tl, src.origin, src.bo, vv < tl.span ? vv : 0, limit);
   return reinterpret_cast<const uint32_t*>(x)[gv];
 }
 
 template <int CIN, int COUT, bool HEAD, int MODE>
-__global__ void __launch_bounds__(256) conv_bf16_kernel(Geom g, Tiling tl, int act,
-                                                        const uint16_t* __restrict__ x,
-                                                        uint16_t* __restrict__ y,
-                                                        const u32x4* __restrict__ wfrag,
-                                                        const float* __restrict__ bias,
-                                                        const float* __restrict__ head_w,
-                                                        const float* __restrict__ head_b,
-                                                        const int32_t* __restrict__ comp_of_site,
-                                                        uint8_t* __restrict__ nib, float* __restrict__ logits,
-                                                        int batch) {
+__global__ void __launch_bounds__(NT) conv_bf16_kernel(Geom g, Tiling tl, int act,
+                                                       const uint16_t* __restrict__ x,
+                                                       uint16_t* __restrict__ y,
+                                                       const u32x4* __restrict__ wfrag,
+                                                       const float* __restrict__ bias,
+                                                       const float* __restrict__ head_w,
+                                                       const float* __restrict__ head_b,
+                                                       const int32_t* __restrict__ comp_of_site,
+                                                       uint8_t* __restrict__ nib, float* __restrict__ logits,
+                                                       int batch) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  constexpr int NB = COUT / 64;   // 32-channel blocks per wave
-  constexpr int NBT = COUT / 32;  // 32-channel blocks in total
-  constexpr int MB = 4;           // 32-voxel blocks per wave
+  using W = WaveSplit<COUT>;
+  constexpr int MB = W::MB;       // 32-voxel blocks per wave
+  constexpr int NBT = COUT / 32;  // 32-channel blocks in total (one per column wave)
   constexpr int NCHUNK = (CIN == 2) ? 1 : CIN / KC;
   constexpr int TSTEPS = NCHUNK * STEPS;  // k-steps per tile (hidden layers)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave & 1, wn = wave >> 1;
+  const int wm = wave % W::WM, wn = wave / W::WM;
   const int half = lane >> 5, l32 = lane & 31;
   const int ntiles = (int)tl.ntiles;
   const long long limit = (long long)batch * g.S;
   const int ngran = tl.span * 4;  // 16-byte granules of a staged chunk
 
-  // LDS: [staging buffer 0][staging buffer 1][scratch round][head partials
-  // [2][256][4] fp32][bias [COUT]][head weights [4][COUT]]
   using L = LdsLayout<COUT>;
   lds_char* const lds = (lds_char*)smem;
   lds_char* const trash = lds + L::trash;
   lds_char* const zero = lds + L::zero;
-  lds_float* const head_part = (lds_float*)(lds + L::head);
   lds_float* const bias_s = (lds_float*)(lds + L::bias);
   lds_float* const headw_s = (lds_float*)(lds + L::headw);
-  for (int e = tid; e < COUT; e += 256) bias_s[e] = bias[e];
+  for (int e = tid; e < COUT; e += NT) bias_s[e] = bias[e];
   if (tid < 64) ((lds_u32_w*)zero)[tid] = 0u;
   const uint32_t zero_addr = (uint32_t)(uintptr_t)zero;
   if (HEAD)
-    for (int e = tid; e < 4 * COUT; e += 256) headw_s[e] = head_w[e];
+    for (int e = tid; e < 4 * COUT; e += NT) headw_s[e] = head_w[e];
 
   int tile = tile_of(blockIdx.x, gridDim.x, 0, ntiles);
   if (tile < 0) return;
@@ -307,26 +320,29 @@ __global__ void __launch_bounds__(256) conv_bf16_kernel(Geom g, Tiling tl, int a
   if constexpr (CIN == 2) {
 #pragma unroll
     for (int k = 0; k < PLANE_RMAX; ++k) {
-      const uint32_t v = plane_load(g, tl, x, cur_src, limit, k, wave, lane);
-      *(lds_u32_w*)(lds + (k * 256 + wave * 64 + lane) * 4) = v;
+      const uint32_t v = plane_load(g, tl, x, cur_src, limit, k, tid);
+      *(lds_u32_w*)(lds + (k * NT + tid) * 4) = v;
     }
   } else {
 #pragma unroll
     for (int k = 0; k < RMAX; ++k) {
-      const u32x4 v = stage_load<CIN, MODE>(g, tl, x, cur_src, limit, 0, ngran, k, wave, lane);
-      *(lds_u32x4_w*)(lds + (k * 256 + wave * 64 + lane) * 16) = v;
+      const u32x4 v = stage_load<CIN, MODE>(g, tl, x, cur_src, limit, 0, ngran, k, tid);
+      const int q = k * NT + tid;
+      *(lds_u32x4_w*)(lds + (q >> 2) * VSTRIDE + (q & 3) * 16) = v;
     }
   }
 
-  // weight-fragment ring (hidden layers): slot k holds the fragments of
-  // tile-step gs with gs % BRING == k
-  const u32x4* wlane = wfrag + (wn * NB) * 64 + lane;
-  u32x4 bq[BRING][NB];
+  // weight fragment (tile-step gs) of this wave's 32 channels: a uniform base
+  // plus this lane's 16-byte slot, so the load can use a scalar base
+  const uint32_t woff = (uint32_t)((wn * 64 + lane) * 16);
+  auto wload = [&](int gs) -> u32x4 {
+    return *reinterpret_cast<const u32x4*>(reinterpret_cast<const char*>(wfrag) + (size_t)gs * NBT * 1024 + woff);
+  };
+  // weight-fragment ring (hidden layers): slot k holds tile-step gs, gs % BRING == k
+  u32x4 bq[BRING];
   if constexpr (CIN != 2) {
 #pragma unroll
-    for (int st = 0; st < BRING - 1; ++st)
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) bq[st][nb] = wlane[(st * NBT + nb) * 64];
+    for (int st = 0; st < BRING - 1; ++st) bq[st] = wload(st);
   }
   __syncthreads();  // staged chunk, bias and head weights visible
 
@@ -334,28 +350,26 @@ __global__ void __launch_bounds__(256) conv_bf16_kernel(Geom g, Tiling tl, int a
   for (int it = 0; tile >= 0; ++it) {
     const int next = tile_of(blockIdx.x, gridDim.x, it + 1, ntiles);
     const StageSrc next_src = source_of(next >= 0 ? next : tile);
-    // rows of this lane: voxel 32 mb + l32 of the wave's 128
+    // rows of this lane: voxel wm ROWS + 32 mb + l32 of the tile
     int rb[MB];
-    long long pidx[MB];
+    int pidx[MB];
     uint32_t em0[MB], em2[MB];  // flat tiles: reads of the left / right halo column go to `zero`
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
       long long p = -1, o;
       int lb = 0, col = -1;
-      bool ok = tile_row(g, tl, tile, wm * 128 + mb * 32 + l32, batch, &p, &lb, &o, &col);
+      bool ok = tile_row(g, tl, tile, wm * W::ROWS + mb * 32 + l32, batch, &p, &lb, &o, &col);
       rb[mb] = lb;
-      pidx[mb] = ok ? p : -1;
+      pidx[mb] = ok ? (int)p : -1;
       em0[mb] = (MODE == 0 && col == 0) ? 0xFFFFFF00u : 0u;
       em2[mb] = (MODE == 0 && col == g.H - 1) ? 0xFFFFFF00u : 0u;
     }
 
-    f32x16 acc[MB][NB];
+    f32x16 acc[MB];
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) acc[mb][nb][v] = 0.0f;
+      for (int v = 0; v < 16; ++v) acc[mb][v] = 0.0f;
 
     if constexpr (CIN == 2) {
       lds_char* const cur = lds + (gchunk & 1) * ABUF;
@@ -363,13 +377,11 @@ __global__ void __launch_bounds__(256) conv_bf16_kernel(Geom g, Tiling tl, int a
       // next tile's planes into registers while this tile computes
       uint32_t nxt[PLANE_RMAX];
 #pragma unroll
-      for (int k = 0; k < PLANE_RMAX; ++k) nxt[k] = plane_load(g, tl, x, next_src, limit, k, wave, lane);
+      for (int k = 0; k < PLANE_RMAX; ++k) nxt[k] = plane_load(g, tl, x, next_src, limit, k, tid);
       lds_u32* a32 = (lds_u32*)cur;
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
-        u32x4 wf[NB];
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) wf[nb] = wlane[(ks * NBT + nb) * 64];
+        const u32x4 wf = wload(ks);
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
           u32x4 av;
@@ -384,15 +396,13 @@ __global__ void __launch_bounds__(256) conv_bf16_kernel(Geom g, Tiling tl, int a
             }
             av[q] = val;
           }
-#pragma unroll
-          for (int nb = 0; nb < NB; ++nb)
-            acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                __builtin_bit_cast(bf16x8, wf[nb]), __builtin_bit_cast(bf16x8, av), acc[mb][nb], 0, 0, 0);
+          acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, wf),
+                                                            __builtin_bit_cast(bf16x8, av), acc[mb], 0, 0, 0);
         }
       }
 #pragma unroll
       for (int k = 0; k < PLANE_RMAX; ++k)
-        *(lds_u32_w*)(oth + ((next >= 0 ? k * 256 : 0) + wave * 64 + lane) * 4) = nxt[k];
+        *(lds_u32_w*)(oth + ((next >= 0 ? k * NT : 0) + tid) * 4) = nxt[k];
       ++gchunk;
     } else {
       for (int chunk = 0; chunk < NCHUNK; ++chunk, ++gchunk) {
@@ -405,39 +415,38 @@ __global__ void __launch_bounds__(256) conv_bf16_kernel(Geom g, Tiling tl, int a
         const int schunk = more ? chunk + 1 : 0;
         const int sgran = real ? ngran : 0;
         lds_char* const oth = lds + ((gchunk + 1) & 1) * ABUF;
-        u32x4 stg[3];
+        u32x4 stg;
 
-        // Opaque copies of the row bases: keeps the 4 x 54 per-step LDS
-        // addresses of this chunk from being hoisted out of the chunk loop
-        // (they would occupy 216 VGPRs).
-        int rbc[MB];
-        uint32_t e0c[MB], e2c[MB];
+        // Per-lane LDS bases of the row blocks (this lane's voxel, its
+        // granule half) -- opaque so the per-step addresses are not hoisted
+        // out of the chunk loop -- and the halo-column masks.
+        uint32_t rbase[MB], e0c[MB], e2c[MB];
+        const uint32_t cur_u = (uint32_t)(uintptr_t)cur;
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
-          rbc[mb] = rb[mb];
+          rbase[mb] = cur_u + (uint32_t)(rb[mb] * VSTRIDE + half * 16);
           e0c[mb] = em0[mb];
           e2c[mb] = em2[mb];
-          asm volatile("" : "+v"(rbc[mb]), "+v"(e0c[mb]), "+v"(e2c[mb]));
+          asm volatile("" : "+v"(rbase[mb]), "+v"(e0c[mb]), "+v"(e2c[mb]));
         }
-        // LDS address of the fragment of row block mb at voxel offset toff,
-        // granule sg; halo-column taps of flat tiles go to the zero region
-        // (same bank group, so the read stays conflict-free)
+        // LDS address of the fragment of row block mb for k-step st: the
+        // tap's voxel offset and the k-step's granule pair are common to the
+        // wave; halo-column taps of flat tiles go to the zero region (same
+        // bank group, so the read stays conflict-free)
         auto frag_addr = [&](int mb, int st) -> uint32_t {
           const int tap = st >> 1, ks = st & 1;
           const int dt = tap / 9, di = (tap / 3) % 3, dj = tap % 3;
-          const int vox = rbc[mb] + dt * tl.sa + di * tl.sb + dj;
-          const int sg = ks * 2 + half;
-          uint32_t a = (uint32_t)(uintptr_t)(cur + vox * 64 + ((sg ^ ((vox >> 2) & 3)) << 4));
+          const uint32_t toff = (uint32_t)((dt * tl.sa + di * tl.sb + dj) * VSTRIDE + ks * 32);
+          uint32_t a = rbase[mb] + toff;
           if (MODE == 0 && dj == 0) a = (a & ~e0c[mb]) | (zero_addr & e0c[mb]);
           if (MODE == 0 && dj == 2) a = (a & ~e2c[mb]) | (zero_addr & e2c[mb]);
           return a;
         };
         // Each step has two scheduling regions: (A) the LDS reads of the next
         // step's activation fragments (addresses computed a step earlier) and
-        // the weight loads five steps ahead; (B) this step's 8 MFMAs, with the
+        // the weight load five steps ahead; (B) this step's MFMAs, with the
         // address arithmetic for two steps ahead and the staging work in
-        // their shadow.  A fragment read is issued a full step (8 MFMAs)
-        // before its use.
+        // their shadow.  The other wave of the SIMD fills the gaps.
         u32x4 av[2][MB];
         uint32_t an[MB];  // LDS addresses of the fragments of step st + 1
 #pragma unroll
@@ -455,8 +464,7 @@ __global__ void __launch_bounds__(256) conv_bf16_kernel(Geom g, Tiling tl, int a
           {
             int gs = gbase + st + BRING - 1;  // wraps into the next tile's steps
             if (gs >= TSTEPS) gs -= TSTEPS;
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb) bq[(st + BRING - 1) % BRING][nb] = wlane[(gs * NBT + nb) * 64];
+            bq[(st + BRING - 1) % BRING] = wload(gs);
           }
           __builtin_amdgcn_sched_barrier(0);
           // ---- region B ----
@@ -464,25 +472,21 @@ __global__ void __launch_bounds__(256) conv_bf16_kernel(Geom g, Tiling tl, int a
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb) an[mb] = frag_addr(mb, st + 2);
           }
-          // staging of the next chunk: round k is loaded at step 3k and
-          // stored to LDS at step 3k + 6
-          if (st % 3 == 0 && st / 3 < RMAX) {
-            const int k = st / 3;
-            stg[k % 3] = stage_load<CIN, MODE>(g, tl, x, ssrc, limit, schunk, sgran, k, wave, lane);
+          // staging of the next chunk: round k is loaded at step 6k and
+          // stored to LDS at step 6k + 6, just before round k + 1 is loaded
+          if (st >= 6 && st % 6 == 0 && st / 6 - 1 < RMAX) {
+            const int k = st / 6 - 1;
+            const int q = k * NT + tid;
+            lds_char* dst = (k * NT < sgran) ? oth + (q >> 2) * VSTRIDE + (q & 3) * 16 : trash + tid * 16;
+            *(lds_u32x4_w*)dst = stg;
           }
-          if (st >= 6 && (st - 6) % 3 == 0 && (st - 6) / 3 < RMAX) {
-            const int k = (st - 6) / 3;
-            lds_char* dst = (k * 256 < sgran) ? oth + (k * 256 + wave * 64 + lane) * 16
-                                              : trash + (wave * 64 + lane) * 16;
-            *(lds_u32x4_w*)dst = stg[k % 3];
-          }
+          if (st % 6 == 0 && st / 6 < RMAX)
+            stg = stage_load<CIN, MODE>(g, tl, x, ssrc, limit, schunk, sgran, st / 6, tid);
 #pragma unroll
           for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb)
-              acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                  __builtin_bit_cast(bf16x8, bq[st % BRING][nb]), __builtin_bit_cast(bf16x8, av[st & 1][mb]),
-                  acc[mb][nb], 0, 0, 0);
+            acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, bq[st % BRING]),
+                                                              __builtin_bit_cast(bf16x8, av[st & 1][mb]), acc[mb],
+                                                              0, 0, 0);
           __builtin_amdgcn_sched_barrier(0);
         }
         // every wave's staging writes done, every wave done reading `cur`
@@ -491,87 +495,112 @@ __global__ void __launch_bounds__(256) conv_bf16_kernel(Geom g, Tiling tl, int a
       }
     }
 
-    // ---- epilogue: lane holds channels co .. co + 3 of voxel row (mb, l32) ----
+    // ---- epilogue: lane holds channels co .. co + 3 (co = 32 wn + 8 q +
+    // 4 half) of voxel row wm ROWS + 32 mb + l32; the buffer this tile read
+    // last is free for the output tile / head partials ----
+    lds_char* const obuf = lds + ((gchunk - 1) & 1) * ABUF;
+    if constexpr (CIN == 2) {
+      // layer 1 read its planes from this buffer: every wave must be done
+      __builtin_amdgcn_s_waitcnt(0xc07f);
+      __builtin_amdgcn_s_barrier();
+    }
     if constexpr (!HEAD) {
+      // bias + activation + bf16 into an LDS copy of the output tile, then
+      // whole voxel rows go out as coalesced 16-byte stores (full cache lines)
+      constexpr int OSTR = COUT * 2 + 16;  // padded row stride of the output tile
+      static_assert(256 * OSTR + 256 * 4 <= ABUF, "output tile fits a staging buffer");
+      lds_i32* const orow = (lds_i32*)(obuf + 256 * OSTR);  // padded output index per row, -1 if none
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
+      for (int q = 0; q < 4; ++q) {
+        const int co = wn * 32 + q * 8 + half * 4;
+        const float4 bv = {bias_s[co], bias_s[co + 1], bias_s[co + 2], bias_s[co + 3]};
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int co = wn * (COUT / 2) + nb * 32 + q * 8 + half * 4;
-          const float4 bv = {bias_s[co], bias_s[co + 1], bias_s[co + 2], bias_s[co + 3]};
-#pragma unroll
-          for (int mb = 0; mb < MB; ++mb) {
-            if (pidx[mb] < 0) continue;
-            const float v0 = activation(acc[mb][nb][4 * q + 0] + bv.x, act);
-            const float v1 = activation(acc[mb][nb][4 * q + 1] + bv.y, act);
-            const float v2 = activation(acc[mb][nb][4 * q + 2] + bv.z, act);
-            const float v3 = activation(acc[mb][nb][4 * q + 3] + bv.w, act);
-            u32x2 packed;
-            packed.x = bf16_bits(v0) | (bf16_bits(v1) << 16);
-            packed.y = bf16_bits(v2) | (bf16_bits(v3) << 16);
-            *reinterpret_cast<u32x2*>(y + pidx[mb] * COUT + co) = packed;
-          }
+        for (int mb = 0; mb < MB; ++mb) {
+          const float v0 = activation(acc[mb][4 * q + 0] + bv.x, act);
+          const float v1 = activation(acc[mb][4 * q + 1] + bv.y, act);
+          const float v2 = activation(acc[mb][4 * q + 2] + bv.z, act);
+          const float v3 = activation(acc[mb][4 * q + 3] + bv.w, act);
+          u32x2 packed;
+          packed.x = bf16_bits(v0) | (bf16_bits(v1) << 16);
+          packed.y = bf16_bits(v2) | (bf16_bits(v3) << 16);
+          const int row = wm * W::ROWS + mb * 32 + l32;
+          *(lds_u32x2_w*)(obuf + row * OSTR + co * 2) = packed;
         }
       }
+      if (wn == 0 && half == 0) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) orow[wm * W::ROWS + mb * 32 + l32] = pidx[mb];
+      }
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+      __builtin_amdgcn_s_barrier();
+      constexpr int GPR = COUT / 8;  // 16-byte granules per voxel row
+#pragma unroll
+      for (int it2 = 0; it2 < 256 * GPR / NT; ++it2) {
+        const int qq = it2 * NT + tid;
+        const int row = qq / GPR, c = qq % GPR;
+        const int p = orow[row];
+        const u32x4 v = *(lds_u32x4*)(obuf + row * OSTR + c * 16);
+        if (p >= 0) *reinterpret_cast<u32x4*>(y + (long long)p * COUT + c * 8) = v;
+      }
     } else {
-      // 1x1x1 head on the bf16-rounded activations, partial over this lane's channels
+      // 1x1x1 head on the bf16-rounded activations: partial sums over this
+      // lane's channels, then over the half-waves, then over the column waves
+      lds_float* const head_part = (lds_float*)obuf;  // [WN][256][4]
       float part[MB][4];
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
         for (int o = 0; o < 4; ++o) part[mb][o] = 0.0f;
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
+      for (int q = 0; q < 4; ++q) {
+        const int co = wn * 32 + q * 8 + half * 4;
+        const float4 bv = {bias_s[co], bias_s[co + 1], bias_s[co + 2], bias_s[co + 3]};
+        float4 hw[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int co = wn * (COUT / 2) + nb * 32 + q * 8 + half * 4;
-          const float4 bv = {bias_s[co], bias_s[co + 1], bias_s[co + 2], bias_s[co + 3]};
-          float4 hw[4];
+        for (int o = 0; o < 4; ++o)
+          hw[o] = {headw_s[o * COUT + co], headw_s[o * COUT + co + 1], headw_s[o * COUT + co + 2],
+                   headw_s[o * COUT + co + 3]};
 #pragma unroll
-          for (int o = 0; o < 4; ++o)
-            hw[o] = {headw_s[o * COUT + co], headw_s[o * COUT + co + 1], headw_s[o * COUT + co + 2],
-                     headw_s[o * COUT + co + 3]};
+        for (int mb = 0; mb < MB; ++mb) {
+          const float a0 = bf16_round(activation(acc[mb][4 * q + 0] + bv.x, act));
+          const float a1 = bf16_round(activation(acc[mb][4 * q + 1] + bv.y, act));
+          const float a2 = bf16_round(activation(acc[mb][4 * q + 2] + bv.z, act));
+          const float a3 = bf16_round(activation(acc[mb][4 * q + 3] + bv.w, act));
 #pragma unroll
-          for (int mb = 0; mb < MB; ++mb) {
-            const float a0 = bf16_round(activation(acc[mb][nb][4 * q + 0] + bv.x, act));
-            const float a1 = bf16_round(activation(acc[mb][nb][4 * q + 1] + bv.y, act));
-            const float a2 = bf16_round(activation(acc[mb][nb][4 * q + 2] + bv.z, act));
-            const float a3 = bf16_round(activation(acc[mb][nb][4 * q + 3] + bv.w, act));
-#pragma unroll
-            for (int o = 0; o < 4; ++o)
-              part[mb][o] += hw[o].x * a0 + hw[o].y * a1 + hw[o].z * a2 + hw[o].w * a3;
-          }
+          for (int o = 0; o < 4; ++o) part[mb][o] += hw[o].x * a0 + hw[o].y * a1 + hw[o].z * a2 + hw[o].w * a3;
         }
       }
-      // sum the two half-waves (same voxels, the other channel quads)
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
         for (int o = 0; o < 4; ++o) part[mb][o] += __shfl_xor(part[mb][o], 32);
-      // the two column waves meet in LDS
       if (half == 0) {
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
-          float4 pv = {part[mb][0], part[mb][1], part[mb][2], part[mb][3]};
-          lds_float* hp = head_part + ((wn * 256) + wm * 128 + mb * 32 + l32) * 4;
-          hp[0] = pv.x;
-          hp[1] = pv.y;
-          hp[2] = pv.z;
-          hp[3] = pv.w;
+          lds_float* hp = head_part + (wn * 256 + wm * W::ROWS + mb * 32 + l32) * 4;
+          hp[0] = part[mb][0];
+          hp[1] = part[mb][1];
+          hp[2] = part[mb][2];
+          hp[3] = part[mb][3];
         }
       }
       __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): partials written
       __builtin_amdgcn_s_barrier();
       // one thread per voxel row: logits, threshold, flip nibble
-      {
-        const int r = tid;  // tile row 0..255
+      if (tid < 256) {
+        const int r = tid;
         long long p = -1, o2;
         int lb;
         if (tile_row(g, tl, tile, r, batch, &p, &lb, &o2)) {
-          const lds_float* h0 = head_part + r * 4;
-          const lds_float* h1 = head_part + (256 + r) * 4;
-          const float lg[4] = {head_b[0] + (h0[0] + h1[0]), head_b[1] + (h0[1] + h1[1]),
-                               head_b[2] + (h0[2] + h1[2]), head_b[3] + (h0[3] + h1[3])};
+          float lg[4] = {head_b[0], head_b[1], head_b[2], head_b[3]};
+#pragma unroll
+          for (int w2 = 0; w2 < W::WN; ++w2) {
+            const lds_float* hp = head_part + (w2 * 256 + r) * 4;
+            lg[0] += hp[0];
+            lg[1] += hp[1];
+            lg[2] += hp[2];
+            lg[3] += hp[3];
+          }
           // padded index -> (b, t, i, j)
           const int b = (int)(p / g.S);
           const int rem = (int)(p - (long long)b * g.S);
@@ -594,14 +623,10 @@ __global__ void __launch_bounds__(256) conv_bf16_kernel(Geom g, Tiling tl, int a
           }
         }
       }
-      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): partials read
-      __builtin_amdgcn_s_barrier();        // head_part is rewritten by the next tile
     }
-    if constexpr (CIN == 2) {
-      // next tile's planes written by every wave; this tile's reads done
-      __builtin_amdgcn_s_waitcnt(0xc07f);
-      __builtin_amdgcn_s_barrier();
-    }
+    // the epilogue's buffer is where the next tile's second chunk is staged
+    __builtin_amdgcn_s_waitcnt(0xc07f);
+    __builtin_amdgcn_s_barrier();
     tile = next;
     cur_src = next_src;
   }
@@ -619,7 +644,7 @@ size_t conv_bf16_lds_bytes(int cin, int span) {
   return lds_bytes(128);
 }
 
-int conv_bf16_max_span() { return RMAX * 256 / 4; }
+int conv_bf16_max_span() { return RMAX * NT / 4; }
 
 template <int CIN, int COUT, bool HEAD, int MODE>
 static hipError_t launch_one(const Geom& g, const Tiling& tl, int act, const void* x, void* y,
@@ -635,7 +660,7 @@ static hipError_t launch_one(const Geom& g, const Tiling& tl, int act, const voi
     attr_set = true;
   }
   const long long nwg = conv_workgroups(tl.ntiles, n_workgroups);
-  hipLaunchKernelGGL((conv_bf16_kernel<CIN, COUT, HEAD, MODE>), dim3((unsigned)nwg), dim3(256), lds, stream, g, tl,
+  hipLaunchKernelGGL((conv_bf16_kernel<CIN, COUT, HEAD, MODE>), dim3((unsigned)nwg), dim3(NT), lds, stream, g, tl,
                      act, (const uint16_t*)x, (uint16_t*)y, (const u32x4*)wfrag, bias, head_w, head_b,
                      comp_of_site, nib, logits, batch);
   return hipGetLastError();
