@@ -12,8 +12,11 @@ algorithmic FLOPs / its mean HIP-event duration) and the CPU oracle timed on a
 bounded sample of the same workload.
 """
 import argparse
+import glob
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -24,6 +27,32 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
+
+
+def kernel_source_hash():
+    """sha256 over the HIP sources (csrc/*.hip, *.h, sorted by name)."""
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2604_12841_amd", "csrc", "*.hip")) +
+                    glob.glob(os.path.join(ROOT, "paper_2604_12841_amd", "csrc", "*.h"))):
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def counted_traffic(profile):
+    """HBM bytes per launch of the dominant kernel from a committed counter
+    summary (FETCH_SIZE + WRITE_SIZE, calibrated), or None when the summary is
+    missing or was taken on different kernel sources."""
+    path = os.path.join(ROOT, "profiles", profile)
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m_hash = re.search(r"kernel_sources_sha256:\s*([0-9a-f]{64})", text)
+    m_bytes = re.search(r"traffic_bytes_per_launch:\s*([0-9]+)", text)
+    if not m_hash or not m_bytes or m_hash.group(1) != kernel_source_hash():
+        return None
+    return int(m_bytes.group(1))
 
 
 def flops_per_sample(layers, d, T):
@@ -41,6 +70,8 @@ def main():
     ap.add_argument("--stage-iters", type=int, default=5)
     ap.add_argument("--cpu-samples", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="also run one plain device copy of this many MiB (calibrates HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the path is data-parallel over independent volumes and "
@@ -82,7 +113,9 @@ def main():
     # Per-stage HIP-event times on the same stream (unpack, each layer, head, residual).
     stages = pre.stage_times(ddet, flips, res, args.stage_iters, stream=stream)
     n = len(layers)
-    hidden = [i for i in range(1, n - 1) if layers[i][0] == layers[i][1]]
+    # hidden C->C layers whose epilogue writes activations (the last hidden
+    # layer also applies the head and is timed separately in stage_ms)
+    hidden = [i for i in range(1, n - 2) if layers[i][0] == layers[i][1]]
     conv_ms = float(np.mean([stages[1 + i] for i in hidden]))
     ci, co = layers[hidden[0]][0], layers[hidden[0]][1]
     V = T * (d + 1) ** 2
@@ -123,26 +156,35 @@ def main():
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": achieved / PEAK_BF16_TFLOPS,
-            "traffic": None,
+            "traffic": counted_traffic("conv_bf16_%dx%d_d%d_T%d_B%d_counters.md" % (ci, co, d, T, B)),
         },
     }
 
     if not args.no_cpu_baseline:
         import oracle
-        ns = args.cpu_samples or {1: 64, 2: 64, 3: 8, 4: 1, 5: 1}[args.workload]
+        ns = args.cpu_samples or {1: 64, 2: 128, 3: 48, 4: 1, 5: 4}[args.workload]
         ns = min(ns, B)
         oracle.build()
         oracle.unpack(d, T, det[:1])  # load the library outside the timed region
         t0 = time.perf_counter()
         oracle.run(d, T, det[:ns], layers, weights, bf16=(cfg["dtype"] == "bf16"))
         dt = time.perf_counter() - t0
-        cores = int(os.environ.get("OMP_NUM_THREADS", 0)) or len(os.sched_getaffinity(0))
+        cores = oracle.num_threads()
         out["cpu_baseline"] = {
             "value": ns * T / dt, "unit": "rounds/s", "cores": cores, "kind": "oracle",
             "sample": "%d of the %d samples (%.1f s, fp64 oracle with bf16 rounding points, "
-                      "OpenMP over samples x output channels)" % (ns, B, dt),
+                      "OpenMP over samples x output channels, %d host CPUs visible)"
+                      % (ns, B, dt, len(os.sched_getaffinity(0))),
         }
     pre.close()
+    if args.copy_mib:
+        n = args.copy_mib << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        out["copy_calibration_mib"] = args.copy_mib
     print(json.dumps(out), flush=True)
 
 

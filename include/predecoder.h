@@ -4,11 +4,11 @@
  * Implements the inference step of the local 3D-convolutional pre-decoder for
  * the rotated surface code ("Fast and accurate AI-based pre-decoders for
  * surface codes", arXiv 2604.12841): a fully convolutional 3D CNN over the
- * space-time volume of detector events (Sec. III.B, Fig. ConvArch), whose four
+ * space-time volume of detector events (Sec. IV.B, Fig. ConvArch), whose four
  * output channels are read as data-qubit Z/X corrections and X/Z
- * stabilizer-measurement (timelike) corrections (Sec. III.B.5, Eqs.
+ * stabilizer-measurement (timelike) corrections (Sec. IV.B.6, Eqs.
  * ZcorreJK-SynZCorrJK), thresholded at logit > 0 (the sigmoid of the BCE
- * objective, Sec. III.B.4), and applied to the syndrome history to give the
+ * objective, Sec. IV.B.5), and applied to the syndrome history to give the
  * residual syndrome that is handed to a global decoder (Eqs. Resk1X, ReskG1X,
  * Resk1Z, ReskG1Z).
  *
@@ -18,7 +18,7 @@
  *   Z site  <=>  (i + j) odd  and 1 <= j <= d-1
  * Plaquette (i, j) acts on the data qubits (i-1, j-1), (i-1, j), (i, j-1),
  * (i, j) that lie inside [0, d-1]^2 (weight 4 in the bulk, weight 2 on the
- * boundary).  X_L is a horizontal and Z_L a vertical string (Sec. II, Fig. 2).
+ * boundary).  X_L is a horizontal and Z_L a vertical string (Sec. III, Fig. SurfaceCodeExamp).
  * Data qubit (r, c) is identified with grid site (r, c), r, c < d.  There are
  * K = (d^2 - 1) / 2 stabilizers of each type (Eqs. DetectorX/DetectorZ).
  *
@@ -28,7 +28,7 @@
  *   detectors / residual, W_det = predecoder_det_words(d, T) words per sample:
  *     b = t * (d^2 - 1) + n; n < K enumerates the X sites in row-major (i, j)
  *     order, n >= K the Z sites in row-major order.  A detector bit is the
- *     XOR of one stabilizer's outcomes in rounds t and t-1 (Sec. III.B.1).
+ *     XOR of one stabilizer's outcomes in rounds t and t-1 (Sec. IV.B.1).
  *   flips, W_flip = predecoder_flip_words(d, T) words per sample:
  *     b = t * (3 d^2 - 1) + n with n running over
  *       [0, d^2)          Z data-qubit correction (output channel 0), (r, c) row-major
@@ -108,7 +108,7 @@ typedef struct pd_layer {
 
 typedef struct pd_predecoder pd_predecoder; /* opaque */
 
-/* Builds a pre-decoder for distance d and T rounds (Sec. III.B; the network
+/* Builds a pre-decoder for distance d and T rounds (Sec. IV.B; the network
  * is fully convolutional, so the same weights apply to any (d, T)).
  * weights: host fp32, n_weights == predecoder_weight_count(layers, n_layers),
  *          copied (the caller keeps ownership).
@@ -120,7 +120,7 @@ pd_status predecoder_create(const float* weights, size_t n_weights, int32_t d, i
                             const pd_layer* layers, int32_t n_layers, int32_t dtype,
                             int32_t max_batch, pd_predecoder** out);
 
-/* The whole hot path for `batch` independent volumes (Sec. III.B.5):
+/* The whole hot path for `batch` independent volumes (Sec. IV.B.6):
  * unpack -> conv layers (+bias, activation) -> head -> threshold ->
  * residual and bit repack.
  * det:      device, [batch][W_det] uint64, packed detectors (read only).
@@ -138,7 +138,7 @@ pd_status predecoder_run(pd_predecoder* h, void* hip_stream, const uint64_t* det
 pd_status predecoder_residual(pd_predecoder* h, void* hip_stream, const uint64_t* det,
                               const uint64_t* flips, int32_t batch, uint64_t* residual);
 
-/* The unpack stage alone (Sec. III.B.1, Eqs. encTrainX1/2: detector events
+/* The unpack stage alone (Sec. IV.B.1, Eqs. encTrainX1/2: detector events
  * placed at their stabilizer sites, 0 elsewhere): det [batch][W_det] ->
  * planes, device, [batch][T][d+1][d+1][2] in the handle's dtype (bf16 bit
  * patterns as uint16 for PD_DTYPE_BF16, fp32 for PD_DTYPE_FP32).

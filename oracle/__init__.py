@@ -1,4 +1,4 @@
-"""CPU oracle of the pre-decoder hot path (arXiv 2604.12841, Sec. III.B).
+"""CPU oracle of the pre-decoder hot path (arXiv 2604.12841, Sec. IV.B).
 
 TEST INFRASTRUCTURE ONLY: the tests, the smoke check and the CPU-baseline leg
 of the benchmark are the only callers.  The product path never imports this
@@ -163,6 +163,13 @@ def residual_from_flips(d, T, det, flips):
     res = np.zeros((B, det_words(d, T)), dtype=np.uint64)
     _load().oracle_residual_from_flips(d, T, B, _ptr(det), _ptr(flips), _ptr(res))
     return res
+
+
+def num_threads():
+    """Threads the oracle's parallel loops use."""
+    lib = _load()
+    lib.oracle_num_threads.restype = ctypes.c_int
+    return int(lib.oracle_num_threads())
 
 
 def run(d, T, det, layers, weights, bf16):

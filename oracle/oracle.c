@@ -8,13 +8,13 @@
  *
  * Everything follows the definitions of arXiv 2604.12841 as written:
  *   - detector events d_{i,k} = s_{i,k} XOR s_{i,k-1} placed on a grid
- *     (Sec. III.B.1, Eqs. encTrainX1/encTrainX2, Fig. StabMap);
+ *     (Sec. IV.B.1, Eqs. encTrainX1/encTrainX2, Fig. StabMap);
  *   - a fully convolutional 3D CNN, output the same size as the input
- *     (Sec. III.B, Fig. ConvArch), stride 1, zero padding;
+ *     (Sec. IV.B, Fig. ConvArch), stride 1, zero padding;
  *   - GELU, tanh form (Table hyperparameters);
  *   - corrections read from the four output channels (Eqs. ZcorreJK,
  *     XcorreJK, SynXCorrJK, SynZCorrJK), thresholded at sigmoid > 1/2, i.e.
- *     logit > 0 (the BCE objective of Sec. III.B.4 applies a sigmoid);
+ *     logit > 0 (the BCE objective of Sec. IV.B.5 applies a sigmoid);
  *   - syndromes induced by the data corrections (Eqs. SXJK, SZJK) and the
  *     residual syndrome (Eqs. Resk1X, ReskG1X, Resk1Z, ReskG1Z).
  *
@@ -29,13 +29,14 @@
  * x[b][c][t][i][j] with i, j in [0, d] on the (d+1) x (d+1) plaquette grid.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
 
 /* ---------------------------------------------------------------------- */
 /* Geometry of the rotated surface code on the (d+1) x (d+1) plaquette grid */
-/* (Sec. II, Fig. 2: X_L horizontal, Z_L vertical; Fig. StabMap).           */
+/* (Sec. III, Fig. SurfaceCodeExamp: X_L horizontal, Z_L vertical; Fig. StabMap).           */
 /* ---------------------------------------------------------------------- */
 
 /* Kind of grid site (i, j): 1 = X stabilizer, 2 = Z stabilizer, 0 = none. */
@@ -89,7 +90,7 @@ static void set_bit(uint64_t* row, int64_t b, int v) {
 }
 
 /* ---------------------------------------------------------------------- */
-/* Unpack (Sec. III.B.1): X-type detector events of round t at their X     */
+/* Unpack (Sec. IV.B.1): X-type detector events of round t at their X     */
 /* sites in channel 0, Z-type at their Z sites in channel 1, 0 elsewhere.  */
 /* planes: [B][2][T][d+1][d+1].                                            */
 /* ---------------------------------------------------------------------- */
@@ -163,7 +164,7 @@ int64_t oracle_weight_count(int n_layers, const int* spec) {
 }
 
 /* ---------------------------------------------------------------------- */
-/* Forward pass of the fully convolutional network (Sec. III.B).           */
+/* Forward pass of the fully convolutional network (Sec. IV.B).           */
 /*   y[co][t][i][j] = b[co] + sum_{ci,kt,ki,kj} w[co][ci][kt][ki][kj] *    */
 /*                    x[ci][t+kt-p][i+ki-p][j+kj-p],  p = (k-1)/2,          */
 /* with x = 0 outside [0,T) x [0,d] x [0,d]; hidden layers apply their     */
@@ -269,7 +270,7 @@ void oracle_forward(int d, int T, int B, const double* planes, int n_layers, con
 }
 
 /* ---------------------------------------------------------------------- */
-/* Corrections and residual (Sec. III.B.5).                                */
+/* Corrections and residual (Sec. IV.B.6).                                */
 /* ---------------------------------------------------------------------- */
 
 /* Residual of one sample from unpacked corrections on the grid:
@@ -308,7 +309,7 @@ static void residual_one(int d, int T, const uint64_t* det, const uint8_t* zc, c
 }
 
 /* Thresholds logits [B][4][T][H][H] (flip = logit > 0, Eqs. ZcorreJK..
- * SynZCorrJK with the sigmoid of Sec. III.B.4), keeps each channel only where
+ * SynZCorrJK with the sigmoid of Sec. IV.B.5), keeps each channel only where
  * it is defined (data qubits for 0/1, X sites for 2, Z sites for 3), packs the
  * flips and computes the residual. */
 void oracle_flips_residual(int d, int T, int B, const double* logits, const uint64_t* det,
@@ -386,3 +387,7 @@ void oracle_residual_from_flips(int d, int T, int B, const uint64_t* det, const 
   free(site_of);
   free(index_of);
 }
+
+/* Threads an OpenMP parallel region of the oracle uses (reported with the
+ * CPU timing; not part of the method). */
+int oracle_num_threads(void) { return omp_get_max_threads(); }

@@ -1,5 +1,5 @@
 // conv_bf16.hip -- K2 + K3 (+ K4 for the last layer): one 3x3x3 conv3d layer
-// (Sec. III.B, Fig. ConvArch; stride 1, zero padding, cross-correlation) as an
+// (Sec. IV.B, Fig. ConvArch; stride 1, zero padding, cross-correlation) as an
 // implicit GEMM on the gfx950 matrix cores, with the bias + activation + bf16
 // rounding epilogue fused in; for the last hidden layer the epilogue also
 // applies the 1x1x1 head and the threshold (logit > 0) and writes one flip
@@ -12,15 +12,16 @@
 // live in the zero-halo NTHWC layout of internal.h, so every tap is an index
 // shift and the K loop has no bounds checks.
 //
-// Work split: persistent workgroups of 256 threads (4 wave64), one per CU.
-// A tile is 256 output voxels x all c_out channels; wave w owns voxels
-// [128 (w & 1), +128) and channels [(c_out / 2)(w >> 1), +c_out / 2), i.e.
-// 4 x (c_out / 64) blocks of v_mfma_f32_32x32x16_bf16 with fp32 accumulators.
+// Work split: persistent workgroups of 512 threads (8 wave64, two per SIMD),
+// one per CU.  A tile is 256 output voxels x all c_out channels; wave w owns
+// voxels [128 (w % 2), +128) and channels [32 (w / 2), +32) for c_out = 128
+// (64-voxel x 32-channel blocks for c_out = 64), i.e. 4 (2) blocks of
+// v_mfma_f32_32x32x16_bf16 with fp32 accumulators.
 //   * The input footprint of a tile is staged in LDS 32 input channels (64
-//     bytes per voxel) at a time, double buffered, with global_load_lds_dwordx4
-//     (HBM/L2 -> LDS, no registers).  The next chunk -- or, during the last
-//     chunk, the next tile's first chunk -- is in flight while the current one
-//     feeds the MFMAs.
+//     bytes per voxel) at a time, double buffered, through registers: the
+//     next chunk -- or, during the last chunk, the next tile's first chunk --
+//     is loaded from HBM/L2 in 7 rounds spread over the current chunk's
+//     k-steps and written to the other buffer.
 //   * A staged voxel occupies 80 bytes of LDS (its 64 bytes of channels plus
 //     16 of padding).  The LDS serves a 16-byte read 16 lanes at a time over
 //     64 banks (16 groups of 16 bytes); granule g of voxel v sits in bank
@@ -34,9 +35,9 @@
 //     fragments (pre-arranged at create time in MFMA operand order, one
 //     coalesced 16-byte load per lane; a layer is <= 0.9 MB and stays in L2)
 //     five steps ahead through a 6-deep register ring.
-//   * Epilogue from registers: + bias, activation in fp32, bf16 (RNE,
-//     v_cvt_pk_bf16_f32), 8-byte stores of 4 channels into the interior of the
-//     output (the halo is never written).
+//   * Epilogue: + bias, activation in fp32, bf16 (RNE), written to an LDS
+//     copy of the output tile and stored as whole voxel rows with 16-byte
+//     stores into the interior of the output (the halo is never written).
 // Layer 1 (c_in = 2) uses the same tiles with K = 27 taps x 2 channels padded
 // to 64 (4 k-steps): each lane gathers 4 taps x 2 channels per fragment.
 #include "internal.h"

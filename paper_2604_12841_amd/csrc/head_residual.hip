@@ -2,7 +2,7 @@
 //
 // K4 (head + threshold): the 1x1x1 output layer (c_in -> 4) at every grid
 // voxel, the threshold logit > 0 (sigmoid > 1/2 of the BCE objective,
-// Sec. III.B.4), and the read-out of the four correction channels where they
+// Sec. IV.B.5), and the read-out of the four correction channels where they
 // are defined (Eqs. ZcorreJK, XcorreJK, SynXCorrJK, SynZCorrJK): channels 0/1
 // at data qubits (grid sites (r, c), r, c < d), channel 2 at X sites, channel 3
 // at Z sites.  The four flip bits of a voxel are kept as one nibble per voxel

@@ -1,4 +1,4 @@
-// unpack.hip -- K1: packed detector events -> 2-channel planes (Sec. III.B.1:
+// unpack.hip -- K1: packed detector events -> 2-channel planes (Sec. IV.B.1:
 // each detector event is placed at its stabilizer's grid site, X-type in
 // channel 0 and Z-type in channel 1; every other grid location is 0).
 //

@@ -11,10 +11,10 @@ The stabilizer layout used to turn sampled errors into detector events is
 built here from data-qubit coordinates (an ancilla at half-integer position
 (r - 1/2, c - 1/2) checks the data qubits at (r - 1/2 +- 1/2, c - 1/2 +- 1/2)),
 independently of both the oracle and the GPU tables; it matches the rotated
-code of Sec. II (X_L horizontal, Z_L vertical) and the compact detector order
+code of Sec. III (X_L horizontal, Z_L vertical) and the compact detector order
 of the ABI (X ancillas row-major, then Z ancillas row-major).
 
-Detector events follow Sec. III.B.1: d_{i,k} = s_{i,k} XOR s_{i,k-1} with
+Detector events follow Sec. IV.B.1: d_{i,k} = s_{i,k} XOR s_{i,k-1} with
 s_{i,-1} = 0, where the reported outcome s_{i,k} is the parity of the
 accumulated data errors on the stabilizer's support XOR that round's
 measurement error.

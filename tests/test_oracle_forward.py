@@ -1,4 +1,4 @@
-"""Pins of the oracle's network forward (Sec. III.B, Fig. ConvArch, Eq.
+"""Pins of the oracle's network forward (Sec. IV.B, Fig. ConvArch, Eq.
 ReceptiveFieldFormula, Table hyperparameters) against closed forms, the
 library convolution of PyTorch (CPU, fp64) and invariants of a fully
 convolutional network."""

@@ -1,5 +1,5 @@
 """Pins of the oracle's surface-code geometry, bit packing and unpack stage
-against values and facts fixed by the paper (Sec. II, Sec. III.B.1) and by
+against values and facts fixed by the paper (Sec. III, Sec. IV.B.1) and by
 independent constructions."""
 import os
 
@@ -66,7 +66,7 @@ def test_counts_and_kinds(d):
     kind = oracle.site_kind(d)
     K = (d * d - 1) // 2  # K_x = K_z = (D^2 - 1) / 2, Eqs. DetectorX/DetectorZ
     assert (kind == 1).sum() == K and (kind == 2).sum() == K
-    # S(d) = d^2 - 1 stabilizers per round (Sec. II)
+    # S(d) = d^2 - 1 stabilizers per round (Sec. III)
     site_of, index_of = oracle.stabilizer_order(d)
     assert len(set(site_of.tolist())) == d * d - 1
     assert (index_of >= 0).sum() == d * d - 1
@@ -89,7 +89,7 @@ def test_stabilizers_commute_and_weights(d):
 
 @pytest.mark.parametrize("d", DISTANCES)
 def test_logical_operator_orientation(d):
-    """X_L is a horizontal and Z_L a vertical string (Sec. II, Fig. 2): a
+    """X_L is a horizontal and Z_L a vertical string (Sec. III, Fig. SurfaceCodeExamp): a
     column of Z errors has no X-type syndrome, a row of X errors has no Z-type
     syndrome."""
     hx, hz = _check_matrices_oracle(d)
@@ -142,7 +142,7 @@ def test_packing_matches_numpy_packbits():
 
 @pytest.mark.parametrize("d,T", [(3, 2), (5, 5), (13, 3)])
 def test_unpack_places_bits_at_sites(d, T):
-    """Unpack (Sec. III.B.1): the detector event of stabilizer n in round t
+    """Unpack (Sec. IV.B.1): the detector event of stabilizer n in round t
     appears at its grid site, channel 0 for X-type and 1 for Z-type; every
     other grid location is 0."""
     rng = np.random.default_rng(d * 100 + T)

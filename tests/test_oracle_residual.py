@@ -1,6 +1,6 @@
-"""Pins of the oracle's threshold, flip packing and residual (Sec. III.B.5,
+"""Pins of the oracle's threshold, flip packing and residual (Sec. IV.B.6,
 Eqs. ZcorreJK..SynZCorrJK, SXJK, SZJK, Resk1X..ReskG1Z) and of the workload
-generator's detector events (Sec. III.B.1)."""
+generator's detector events (Sec. IV.B.1)."""
 import numpy as np
 import pytest
 
@@ -34,7 +34,7 @@ def _logits_from_flip_bits(d, T, fbits):
 @pytest.mark.parametrize("d,T,B,p", CASES)
 def test_generator_cumulative_equals_differential(d, T, B, p):
     """Detectors from the cumulative outcomes s(t) equal the differential form
-    D(t) = H e(t) ^ m(t) ^ m(t-1) (Sec. III.B.1 with s(-1) = 0)."""
+    D(t) = H e(t) ^ m(t) ^ m(t-1) (Sec. IV.B.1 with s(-1) = 0)."""
     noise = workload.sample_noise(d, T, B, p, p, seed=d + T)
     det = workload.detectors_from_noise(d, noise)
     hx, hz = workload.check_matrices(d)
