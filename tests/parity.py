@@ -119,3 +119,38 @@ def config_case(cfg_id, batch=None, act=workload.GELU_TANH):
     weights = workload.config_weights(cfg_id, act)
     det, noise = workload.config_inputs(cfg_id, batch)
     return c["d"], c["T"], c["dtype"], layers, weights, det, noise
+
+
+# ---- GPU-side helpers shared by the GPU tests (torch is imported lazily so
+# the CPU suite does not need a device) ----
+
+def say(*a):
+    import sys
+    print(*a, file=sys.stderr, flush=True)
+
+
+def dev_u64(a):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.uint64).view(np.int64)).cuda()
+
+
+def host_u64(t):
+    return t.cpu().numpy().view(np.uint64)
+
+
+def run_gpu(pre, det, want_logits=True, canary=True, batch=None):
+    """One predecoder_run of the first `batch` rows of det (default: all) into
+    freshly filled outputs (-1 / NaN canaries); returns host arrays."""
+    import torch
+    B = det.shape[0] if batch is None else batch
+    d, T = pre.d, pre.T
+    ddet = dev_u64(det[:B])
+    fill = -1 if canary else 0
+    flips = torch.full((B, pre.flip_words), fill, dtype=torch.int64, device="cuda")
+    res = torch.full((B, pre.det_words), fill, dtype=torch.int64, device="cuda")
+    logits = None
+    if want_logits:
+        logits = torch.full((B, 4, T, d + 1, d + 1), float("nan"), dtype=torch.float32, device="cuda")
+    pre.run(ddet, flips, res, logits)
+    torch.cuda.synchronize()
+    return host_u64(flips), host_u64(res), (logits.cpu().numpy() if want_logits else None)

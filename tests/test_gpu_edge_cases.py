@@ -1,0 +1,113 @@
+"""Edge cases of the HIP path against the oracle: batches below the handle's
+maximum and ragged tails, batch errors, the smallest and largest grids,
+extreme detector patterns, the other activations and width changes."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2604_12841_amd as pdx
+from paper_2604_12841_amd import workload
+from parity import assert_parity, compare, run_gpu, say
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def cuda():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch.device("cuda")
+
+
+def check(d, T, layers, weights, det, dtype, pre=None, batch=None):
+    own = pre is None
+    if own:
+        pre = pdx.Predecoder(weights, d, T, layers, dtype, max_batch=det.shape[0])
+    B = det.shape[0] if batch is None else batch
+    flips, res, logits = run_gpu(pre, det, batch=B)
+    if own:
+        pre.close()
+    ref = oracle.run(d, T, det[:B], layers, weights, bf16=(dtype == "bf16"))
+    st = compare(d, T, dtype, ref[0], ref[1], ref[2], flips, res, logits)
+    say("  stats", st)
+    assert_parity(st, dtype)
+    return flips, res, logits
+
+
+def test_batches_below_max_and_ragged(cuda):
+    d, T = 13, 13
+    layers = workload.layer_spec(3, 128)
+    w = workload.he_normal_weights(layers, seed=31)
+    det, _ = workload.make_inputs(d, T, 32, 0.005, 0.005, seed=32)
+    say("batches 1, 7, 32 on one handle with max_batch 32, d 13")
+    pre = pdx.Predecoder(w, d, T, layers, "bf16", max_batch=32)
+    f1, r1, l1 = check(d, T, layers, w, det, "bf16", pre=pre, batch=1)
+    f7, r7, l7 = check(d, T, layers, w, det, "bf16", pre=pre, batch=7)
+    f32, r32, l32 = run_gpu(pre, det, batch=32)
+    pre.close()
+    # sample 0 is bit-identical whatever the batch around it
+    np.testing.assert_array_equal(l1[0], l7[0])
+    np.testing.assert_array_equal(l1[0], l32[0])
+    np.testing.assert_array_equal(f7, f32[:7])
+    np.testing.assert_array_equal(r7, r32[:7])
+
+
+def test_batch_errors(cuda):
+    d, T = 5, 5
+    layers = workload.layer_spec(2, 64)
+    w = workload.he_normal_weights(layers, seed=3)
+    det, _ = workload.make_inputs(d, T, 4, 0.01, 0.01, seed=4)
+    pre = pdx.Predecoder(w, d, T, layers, "bf16", max_batch=2)
+    ddet = torch.from_numpy(det.view(np.int64)).cuda()
+    flips = torch.zeros((4, pre.flip_words), dtype=torch.int64, device="cuda")
+    res = torch.zeros((4, pre.det_words), dtype=torch.int64, device="cuda")
+    for bad in (0, 3, -1):
+        with pytest.raises(pdx.PredecoderError) as e:
+            pre.run(ddet, flips, res, batch=bad)
+        assert e.value.status == pdx.PD_ERR_INVALID_ARG
+    # the handle stays usable after an error
+    check(d, T, layers, w, det[:2], "bf16", pre=pre)
+    pre.close()
+
+
+@pytest.mark.parametrize("d,T,B", [(3, 1, 5), (3, 2, 1), (5, 1, 3), (11, 40, 2), (63, 3, 1)])
+def test_grid_extremes(cuda, d, T, B):
+    layers = workload.layer_spec(2, 64)
+    w = workload.he_normal_weights(layers, seed=100 + d)
+    det, _ = workload.make_inputs(d, T, B, 0.01, 0.01, seed=200 + T)
+    say("grid d", d, "T", T, "B", B)
+    check(d, T, layers, w, det, "bf16")
+
+
+@pytest.mark.parametrize("pattern", ["zeros", "ones"])
+def test_extreme_detectors(cuda, pattern):
+    d, T, B = 9, 9, 3
+    layers = workload.layer_spec(3, 64)
+    w = workload.he_normal_weights(layers, seed=41)
+    W = pdx.det_words(d, T)
+    # all-ones also sets the padding bits, which the path must ignore
+    det = np.zeros((B, W), np.uint64) if pattern == "zeros" else np.full((B, W), np.uint64(2**64 - 1))
+    say("detectors all", pattern)
+    check(d, T, layers, w, det, "bf16")
+
+
+@pytest.mark.parametrize("act", [pdx.ACT_RELU, pdx.ACT_NONE])
+@pytest.mark.parametrize("dtype,width", [("bf16", 64), ("bf16", 128), ("fp32", 32)])
+def test_other_activations(cuda, act, dtype, width):
+    d, T, B = 7, 5, 3
+    layers = workload.layer_spec(3, width, act=act)
+    w = workload.he_normal_weights(layers, seed=51)
+    det, _ = workload.make_inputs(d, T, B, 0.02, 0.02, seed=52)
+    say("activation", act, dtype, "width", width)
+    check(d, T, layers, w, det, dtype)
+
+
+def test_width_changes(cuda):
+    d, T, B = 9, 7, 2
+    layers = [(2, 64, 3, pdx.ACT_GELU_TANH), (64, 128, 3, pdx.ACT_GELU_TANH), (128, 64, 3, pdx.ACT_GELU_TANH),
+              (64, 128, 3, pdx.ACT_GELU_TANH), (128, 4, 1, pdx.ACT_NONE)]
+    w = workload.he_normal_weights(layers, seed=61)
+    det, _ = workload.make_inputs(d, T, B, 0.01, 0.01, seed=62)
+    say("width changes 2-64-128-64-128-4")
+    check(d, T, layers, w, det, "bf16")

@@ -3,45 +3,16 @@
 Every case prints its name, seed and shape before touching the GPU.  The
 oracle and the GPU consume the same seeded arrays from the workload module.
 """
-import sys
-
 import numpy as np
 import pytest
 
 import oracle
 import paper_2604_12841_amd as pdx
 from paper_2604_12841_amd import workload
-from parity import TOL, assert_parity, compare, config_case
+from parity import assert_parity, compare, config_case, dev_u64, host_u64, run_gpu, say
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
-
-
-def say(*a):
-    print(*a, file=sys.stderr, flush=True)
-
-
-def dev_u64(a):
-    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.uint64).view(np.int64)).cuda()
-
-
-def host_u64(t):
-    return t.cpu().numpy().view(np.uint64)
-
-
-def run_gpu(pre, det, want_logits=True, canary=True):
-    B = det.shape[0]
-    d, T = pre.d, pre.T
-    ddet = dev_u64(det)
-    fill = -1 if canary else 0
-    flips = torch.full((B, pre.flip_words), fill, dtype=torch.int64, device="cuda")
-    res = torch.full((B, pre.det_words), fill, dtype=torch.int64, device="cuda")
-    logits = None
-    if want_logits:
-        logits = torch.full((B, 4, T, d + 1, d + 1), float("nan"), dtype=torch.float32, device="cuda")
-    pre.run(ddet, flips, res, logits)
-    torch.cuda.synchronize()
-    return host_u64(flips), host_u64(res), (logits.cpu().numpy() if want_logits else None)
 
 
 @pytest.fixture(scope="module")
