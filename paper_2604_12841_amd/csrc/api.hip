@@ -356,6 +356,8 @@ pd_status enqueue_run(pd_predecoder* h, hipStream_t st, const uint64_t* det, int
     if (fp32)
       s = check_launch(pd::launch_conv_fp32(g, L.c_in, L.c_out, L.act, (const float*)x, (float*)y,
                                             (const float*)h->wdev[l], h->bdev[l], batch, st));
+    else if (l == 0 && n - 2 > 0)  // first layer, not also the last hidden one
+      s = check_launch(pd::launch_conv_first(g, L.c_out, L.act, x, y, h->wdev[l], h->bdev[l], batch, st));
     else  // the last hidden layer carries the head and the threshold in its epilogue
       s = check_launch(pd::launch_conv_bf16(g, tl, L.c_in, L.c_out, L.act, x, y, h->wdev[l], h->bdev[l],
                                             l == n - 2, h->head_w, h->head_b,

@@ -1,0 +1,191 @@
+// conv_first.hip -- K2: the first 3x3x3 conv3d layer (Sec. IV.B, Fig.
+// ConvArch; c_in = 2 detector-event channels -> c_out = 64 or 128) with the
+// bias + activation + bf16 epilogue fused in, when it is not also the last
+// hidden layer.
+//
+// K = 27 taps x 2 channels is tiny (padded to 64 = 4 MFMA k-steps), so the
+// layer is bound by its epilogue (one activation per output value) and its
+// output write, not by the matrix cores.  It streams: each wave takes a few
+// blocks of 32 consecutive interior voxels x all c_out channels.
+//   * B operand (16 k x 32 voxels): lane l gathers, for voxel l % 32, taps
+//     ks*8 + 4*(l/32) + q (q = 0..3) as one 4-byte load each (the two bf16
+//     channels of a plane voxel) straight from the zero-halo planes, which
+//     stay in L2; taps past 26 contribute zero.
+//   * A operand: the layer's weight fragments (4 k-steps x c_out/32 blocks,
+//     16 bytes per lane each), staged in LDS once per workgroup.
+//   * Epilogue: + bias, activation, bf16; the wave transposes its 32 x c_out
+//     tile through its own LDS slice and writes whole voxel rows with
+//     16-byte stores.
+#include "internal.h"
+
+namespace pd {
+namespace {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(16))) float f32x16;
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
+typedef __attribute__((address_space(3))) char lds_char;
+typedef __attribute__((address_space(3))) u32x2 lds_u32x2_w;
+typedef __attribute__((address_space(3))) const u32x4 lds_u32x4;
+typedef __attribute__((address_space(3))) u32x4 lds_u32x4_w;
+
+constexpr int WAVES = 4;  // waves per workgroup
+constexpr int BPW = 2;    // 32-voxel blocks per wave
+
+__device__ __forceinline__ float activation(float y, int act) {
+  if (act == 1) {  // GELU, tanh form: 0.5 y (1 + tanh(u)) = y / (1 + exp(-2u))
+    const float k0 = 0.7978845608028654f;          // sqrt(2 / pi)
+    const float kl = -2.0f * 1.4426950408889634f;  // -2 log2(e)
+    const float u = k0 * (y + 0.044715f * y * y * y);
+    const float e = __builtin_amdgcn_exp2f(kl * u);
+    return y * __builtin_amdgcn_rcpf(1.0f + e);
+  }
+  if (act == 2) return y > 0.0f ? y : 0.0f;
+  return y;
+}
+
+__device__ __forceinline__ uint32_t bf16_bits(float v) {
+  __bf16 h = (__bf16)v;
+  return (uint32_t)__builtin_bit_cast(uint16_t, h);
+}
+
+// Divisors of the interior-voxel decode u -> (b, t, i, j).
+struct Decode {
+  FastDiv by_v, by_hh, by_h;
+};
+
+// Padded index of interior voxel u (u < nvox < 2^31).
+__device__ __forceinline__ long long voxel_padded(const Geom& g, const Decode& dc, int u) {
+  const int HH = g.H * g.H;
+  const int b = (int)fastdiv((uint32_t)u, dc.by_v);
+  const int v = u - b * g.V;
+  const int t = (int)fastdiv((uint32_t)v, dc.by_hh);
+  const int s = v - t * HH;
+  const int i = (int)fastdiv((uint32_t)s, dc.by_h);
+  return padded_index(g, b, t, i, s - i * g.H);
+}
+
+// B fragments for this lane's voxel (padded index p): taps ks*8 + 4*half + q.
+__device__ __forceinline__ void gather(const Geom& g, const uint32_t* __restrict__ planes, long long p, bool valid,
+                                       int half, u32x4 (&bx)[4]) {
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int tap = ks * 8 + half * 4 + q;  // >= 27 only for ks = 3
+      uint32_t val = 0;
+      if (valid && tap < 27) {
+        const int dt = tap / 9, di = (tap / 3) % 3, dj = tap % 3;
+        val = planes[p + (long long)(dt - 1) * g.P + (long long)(di - 1) * g.Wp + (dj - 1)];
+      }
+      bx[ks][q] = val;
+    }
+}
+
+// Each workgroup stages the weight fragments in LDS once; each of its waves
+// then handles BPW consecutive 32-voxel blocks.
+template <int COUT>
+__global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, int act, const uint32_t* __restrict__ planes,
+                                                                uint16_t* __restrict__ y,
+                                                                const u32x4* __restrict__ wfrag,
+                                                                const float* __restrict__ bias, Decode dc,
+                                                                int nvox) {
+  constexpr int NB = COUT / 32;
+  constexpr int OSTR = COUT * 2 + 16;  // padded LDS row stride (bytes)
+  constexpr int GPR = COUT / 8;        // 16-byte granules per voxel row
+  constexpr int WFR = 4 * NB * 64;     // weight fragments x lanes (16 bytes each)
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int half = lane >> 5, l32 = lane & 31;
+  lds_u32x4_w* const wl = (lds_u32x4_w*)smem;
+  lds_char* const tile = (lds_char*)smem + WFR * 16 + wave * 32 * OSTR;
+  int* const prow = (int*)((lds_char*)smem + WFR * 16 + WAVES * 32 * OSTR) + wave * 32;  // row -> padded index
+  for (int e = tid; e < WFR; e += 64 * WAVES) wl[e] = wfrag[e];
+  __syncthreads();
+
+#pragma unroll 1
+  for (int j = 0; j < BPW; ++j) {
+    const int u0 = ((blockIdx.x * WAVES + wave) * BPW + j) * 32;
+    if (u0 >= nvox) break;
+    const bool valid = u0 + l32 < nvox;
+    const long long p = valid ? voxel_padded(g, dc, u0 + l32) : -1;
+    u32x4 bx[4];
+    gather(g, planes, p, valid, half, bx);
+    if (half == 0) ((__attribute__((address_space(3))) int*)prow)[l32] = (int)p;
+    // channel halves of 64 (NH blocks of 32) one after the other: fewer
+    // live accumulators, more waves per SIMD to hide the gathers
+    constexpr int NH = NB < 2 ? NB : 2;
+#pragma unroll
+    for (int h0 = 0; h0 < NB; h0 += NH) {
+      f32x16 acc[NH];
+#pragma unroll
+      for (int nb = 0; nb < NH; ++nb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[nb][v] = 0.0f;
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+        for (int nb = 0; nb < NH; ++nb) {
+          const u32x4 wf = *(const lds_u32x4*)(smem + ((ks * NB + h0 + nb) * 64 + lane) * 16);
+          acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, wf),
+                                                            __builtin_bit_cast(bf16x8, bx[ks]), acc[nb], 0, 0, 0);
+        }
+      // epilogue of these channels: lane holds co .. co + 3 (co = 32 nb +
+      // 8 q + 4 half) of voxel row l32
+#pragma unroll
+      for (int nb = 0; nb < NH; ++nb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int co = (h0 + nb) * 32 + q * 8 + half * 4;
+          const float v0 = activation(acc[nb][4 * q + 0] + bias[co + 0], act);
+          const float v1 = activation(acc[nb][4 * q + 1] + bias[co + 1], act);
+          const float v2 = activation(acc[nb][4 * q + 2] + bias[co + 2], act);
+          const float v3 = activation(acc[nb][4 * q + 3] + bias[co + 3], act);
+          u32x2 packed;
+          packed.x = bf16_bits(v0) | (bf16_bits(v1) << 16);
+          packed.y = bf16_bits(v2) | (bf16_bits(v3) << 16);
+          *(lds_u32x2_w*)(tile + l32 * OSTR + co * 2) = packed;
+        }
+    }
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's tile is in LDS
+    __builtin_amdgcn_wave_barrier();
+    // whole rows: 32 rows x GPR granules of 16 bytes, 64 lanes at a time
+#pragma unroll
+    for (int k = 0; k < 32 * GPR / 64; ++k) {
+      const int qq = k * 64 + lane;
+      const int row = qq / GPR, c = qq % GPR;
+      const int pr = ((__attribute__((address_space(3))) const int*)prow)[row];
+      const u32x4 val = *(lds_u32x4*)(tile + row * OSTR + c * 16);
+      if (pr >= 0) *reinterpret_cast<u32x4*>(y + (long long)pr * COUT + c * 8) = val;
+    }
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // the tile's LDS reads are done before the next block writes it
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
+}  // namespace
+
+hipError_t launch_conv_first(const Geom& g, int cout, int act, const void* planes, void* y, const void* wfrag,
+                             const float* bias, int batch, hipStream_t stream) {
+  const long long nvox = (long long)batch * g.V;  // < 2^31 (host check)
+  const long long nblk = (nvox + 32 * WAVES * BPW - 1) / (32 * WAVES * BPW);
+  Decode dc;
+  dc.by_v = make_fastdiv((uint32_t)g.V);
+  dc.by_hh = make_fastdiv((uint32_t)(g.H * g.H));
+  dc.by_h = make_fastdiv((uint32_t)g.H);
+  if (cout == 64) {
+    const size_t lds = (size_t)4 * 2 * 64 * 16 + (size_t)WAVES * 32 * (64 * 2 + 16 + 4);
+    hipLaunchKernelGGL(conv_first_kernel<64>, dim3((unsigned)nblk), dim3(64 * WAVES), lds, stream, g, act,
+                       (const uint32_t*)planes, (uint16_t*)y, (const u32x4*)wfrag, bias, dc, (int)nvox);
+  } else if (cout == 128) {
+    const size_t lds = (size_t)4 * 4 * 64 * 16 + (size_t)WAVES * 32 * (128 * 2 + 16 + 4);
+    hipLaunchKernelGGL(conv_first_kernel<128>, dim3((unsigned)nblk), dim3(64 * WAVES), lds, stream, g, act,
+                       (const uint32_t*)planes, (uint16_t*)y, (const u32x4*)wfrag, bias, dc, (int)nvox);
+  } else {
+    return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace pd

@@ -111,6 +111,11 @@ hipError_t launch_conv_bf16(const Geom& g, const Tiling& tl, int cin, int cout, 
                             void* y, const void* wfrag, const float* bias, int head, const float* head_w,
                             const float* head_b, const int32_t* comp_of_site, uint8_t* nib, float* logits,
                             int batch, int n_workgroups, hipStream_t stream);
+// The first 3x3x3 layer (c_in = 2, c_out = 64 or 128) when it is not also
+// the last hidden layer: planes [batch * S] (2 bf16 channels each), weight
+// fragments as for launch_conv_bf16.
+hipError_t launch_conv_first(const Geom& g, int cout, int act, const void* planes, void* y, const void* wfrag,
+                             const float* bias, int batch, hipStream_t stream);
 size_t conv_bf16_lds_bytes(int cin, int span);
 int conv_bf16_max_span();  // staged voxels a tile may need
 
