@@ -156,7 +156,7 @@ def main():
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": achieved / PEAK_BF16_TFLOPS,
-            "traffic": counted_traffic("conv_bf16_%dx%d_d%d_T%d_B%d_counters.md" % (ci, co, d, T, B)),
+            "traffic": counted_traffic("conv_hidden_%dx%d_d%d_T%d_B%d_counters.md" % (ci, co, d, T, B)),
         },
     }
 

@@ -146,7 +146,7 @@ long long flat_span(const Geom& g, long long seg_len, long long nseg, int batch)
 }
 
 Tiling plan_tiling(const Geom& g, int max_batch) {
-  const int kMaxSpan = pd::conv_bf16_max_span();
+  const int kMaxSpan = std::min(pd::conv_single_max_span(), pd::conv_hidden_max_span());
   Tiling best{};
   long long best_rows = -1;
   int best_span = 0;
@@ -285,11 +285,11 @@ void free_all(pd_predecoder* h) {
   h->head_w = h->head_b = nullptr;
 }
 
-// bf16 B fragments for v_mfma_f32_32x32x16_bf16: lane l of fragment
-// (k-step, column block nb) holds B[k0 + 8 (l / 32) + e][32 nb + l % 32],
+// bf16 A fragments (weights) for v_mfma_f32_32x32x16_bf16: lane l of
+// fragment (k-step, channel block nb) holds W[co = 32 nb + l % 32][k0 + 8 (l / 32) + e],
 // e = 0..7.  Layer 1 (c_in = 2): k = 2 * tap + ci over 4 k-steps (taps >= 27
-// are zero).  Hidden layers: [chunk of 32 c_in][tap][2 k-steps][nb] with
-// ci = 32 chunk + 16 ks + 8 (l / 32) + e.
+// are zero).  Hidden layers: [chunk of 16 c_in][tap][nb] with
+// ci = 16 chunk + 8 (l / 32) + e.
 std::vector<uint16_t> conv_fragments(const float* w, int cin, int cout) {
   const int nbt = cout / 32;
   std::vector<uint16_t> f;
@@ -305,18 +305,17 @@ std::vector<uint16_t> conv_fragments(const float* w, int cin, int cout) {
             f[(((size_t)ks * nbt + nb) * 64 + l) * 8 + e] = tap < 27 ? bf16_bits(W(co, ci, tap)) : 0;
           }
   } else {
-    const int nch = cin / 32;
-    f.assign((size_t)nch * 27 * 2 * nbt * 64 * 8, 0);
+    const int nch = cin / 16;
+    f.assign((size_t)nch * 27 * nbt * 64 * 8, 0);
     for (int c = 0; c < nch; ++c)
       for (int tap = 0; tap < 27; ++tap)
-        for (int ks = 0; ks < 2; ++ks)
-          for (int nb = 0; nb < nbt; ++nb)
-            for (int l = 0; l < 64; ++l)
-              for (int e = 0; e < 8; ++e) {
-                int ci = c * 32 + ks * 16 + 8 * (l / 32) + e, co = nb * 32 + l % 32;
-                size_t idx = (((((size_t)c * 27 + tap) * 2 + ks) * nbt + nb) * 64 + l) * 8 + e;
-                f[idx] = bf16_bits(W(co, ci, tap));
-              }
+        for (int nb = 0; nb < nbt; ++nb)
+          for (int l = 0; l < 64; ++l)
+            for (int e = 0; e < 8; ++e) {
+              int ci = c * 16 + 8 * (l / 32) + e, co = nb * 32 + l % 32;
+              size_t idx = ((((size_t)c * 27 + tap) * nbt + nb) * 64 + l) * 8 + e;
+              f[idx] = bf16_bits(W(co, ci, tap));
+            }
   }
   return f;
 }
@@ -358,11 +357,15 @@ pd_status enqueue_run(pd_predecoder* h, hipStream_t st, const uint64_t* det, int
                                             (const float*)h->wdev[l], h->bdev[l], batch, st));
     else if (l == 0 && n - 2 > 0)  // first layer, not also the last hidden one
       s = check_launch(pd::launch_conv_first(g, L.c_out, L.act, x, y, h->wdev[l], h->bdev[l], batch, st));
+    else if (l == 0)  // a single hidden layer: layer 1 carries the head
+      s = check_launch(pd::launch_conv_single(g, tl, L.c_out, L.act, x, h->wdev[l], h->bdev[l], h->head_w,
+                                              h->head_b, h->tables + pd::tables_comp_of_site(g), h->nib, logits,
+                                              batch, h->n_cu, st));
     else  // the last hidden layer carries the head and the threshold in its epilogue
-      s = check_launch(pd::launch_conv_bf16(g, tl, L.c_in, L.c_out, L.act, x, y, h->wdev[l], h->bdev[l],
-                                            l == n - 2, h->head_w, h->head_b,
-                                            h->tables + pd::tables_comp_of_site(g), h->nib, logits, batch,
-                                            h->n_cu, st));
+      s = check_launch(pd::launch_conv_hidden(g, tl, L.c_in, L.c_out, L.act, x, y, h->wdev[l], h->bdev[l],
+                                              l == n - 2, h->head_w, h->head_b,
+                                              h->tables + pd::tables_comp_of_site(g), h->nib, logits, batch,
+                                              h->n_cu * pd::conv_hidden_workgroups_per_cu(), st));
     if (s != PD_OK) return s;
     x = y;
   }
@@ -461,7 +464,7 @@ pd_status predecoder_create(const float* weights, size_t n_weights, int32_t d, i
   h->cmax = cmax;
   if (dtype == PD_DTYPE_BF16) {
     h->tiling = plan_tiling(g, max_batch);
-    if (h->tiling.span <= 0 || h->tiling.span > pd::conv_bf16_max_span()) {
+    if (h->tiling.span <= 0 || h->tiling.span > std::min(pd::conv_single_max_span(), pd::conv_hidden_max_span())) {
       delete h;
       return PD_ERR_UNSUPPORTED;
     }

@@ -1,0 +1,535 @@
+// conv_hidden.hip -- K3 (+ K4 for the last layer): a hidden 3x3x3 conv3d
+// layer, c_in = 64 or 128 -> c_out = 64 or 128 (Sec. IV.B, Fig. ConvArch;
+// stride 1, zero padding, cross-correlation) as an implicit GEMM on the
+// gfx950 matrix cores, with the bias + activation + bf16 rounding epilogue
+// fused in; for the last hidden layer the epilogue also applies the 1x1x1
+// head and the threshold (logit > 0) and writes one flip nibble per voxel.
+//
+//   out[co][m] = act(bias[co] + sum_{tap, ci} W[co][ci][tap] * X[m + shift(tap)][ci])
+//
+// GEMM view (transposed so the epilogue holds 4 consecutive channels per
+// lane): rows = c_out, columns = output voxels, K = 27 * c_in; weights are
+// the A operand, activations the B operand of v_mfma_f32_32x32x16_bf16.
+// Activations live in the zero-halo NTHWC layout of internal.h, so every tap
+// is an index shift and the K loop has no bounds checks.
+//
+// Work split: persistent workgroups of 256 threads (4 wave64), two per CU, so
+// each SIMD runs one wave of each and one workgroup's epilogue, barriers and
+// staging stalls overlap the other's matrix work.  A tile is 256 output voxels
+// x all c_out channels; a wave owns 128 voxels x 64 channels for c_out = 128
+// (64 x 64 for c_out = 64): 4 (2) voxel blocks x 2 channel blocks of MFMA
+// with fp32 accumulators, so each activation fragment read from LDS feeds two
+// MFMAs and each weight fragment MB.
+//   * The tile's input footprint is staged in LDS 16 input channels (32
+//     bytes per voxel) at a time, double buffered, through registers: the
+//     next chunk -- or, during the last chunk, the next tile's first chunk --
+//     is loaded in 7 rounds spread over the current chunk's 27 k-steps (one
+//     per tap) and written to the other buffer.
+//   * A staged voxel occupies 48 bytes of LDS.  The LDS serves a 16-byte read
+//     16 lanes at a time over 16 groups of 16 bytes; granule g of voxel v sits
+//     in group (3 v + g) mod 16, so 16 consecutive staged voxels hit 16
+//     distinct groups.  Flat tiles stage only the real columns; reads of the
+//     left / right halo column are redirected to a 256-byte zero region with
+//     the same low address bits (same group).
+//   * The 27 k-steps of a chunk are unrolled and software pipelined:
+//     activation fragments are read one step ahead, weight fragments
+//     (arranged at create time in MFMA operand order, one coalesced 16-byte
+//     load per lane; a layer is <= 0.9 MB and stays in L2) two steps ahead
+//     through a 3-deep register ring that runs on across chunks and tiles.
+//   * Epilogue: + bias, activation in fp32, bf16 (RNE), stored straight from
+//     the accumulators (8 bytes per lane, two half-waves covering 16
+//     consecutive bytes of a voxel row); no workgroup barrier, so a wave can
+//     start the next tile while the others finish theirs.
+#include "internal.h"
+#include "tiles.h"
+
+namespace pd {
+namespace {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(16))) float f32x16;
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
+typedef __attribute__((address_space(3))) char lds_char;
+typedef __attribute__((address_space(3))) const u32x4 lds_u32x4;
+typedef __attribute__((address_space(3))) float lds_float;
+typedef __attribute__((address_space(3))) u32x4 lds_u32x4_w;
+typedef __attribute__((address_space(3))) uint32_t lds_u32_w;
+
+constexpr int NT = 256;       // threads per workgroup: 4 wave64
+constexpr int KC = 16;        // input channels per LDS chunk (one MFMA k-step)
+constexpr int STEPS = 27;     // k-steps per chunk: one per tap
+constexpr int BRING = 3;      // weight-fragment ring depth (prefetch distance BRING - 1)
+constexpr int VSTRIDE = 48;   // LDS bytes per staged voxel (32 of channels + 16 of padding)
+constexpr int BUF_VOX = 800;            // staged voxels a staging buffer holds
+constexpr int MAX_SPAN = BUF_VOX - 1;    // staged voxels per tile (the last slot takes overflow writes)
+// Every chunk is staged with RMAX rounds of NT 16-byte granules, stored
+// unconditionally (a conditional store would let the compiler sink the load
+// next to it): granules past the footprint load zeros into slots past the
+// footprint, and granules past the buffer all go to its last slot.
+constexpr int RMAX = 7;
+static_assert(RMAX * NT >= 2 * MAX_SPAN, "staging rounds cover the largest footprint");
+static_assert(STEPS % BRING == 0, "the weight ring lines up with chunk boundaries");
+static_assert(RMAX * 3 + 3 <= STEPS, "staging rounds fit in a chunk");
+constexpr int ABUF = BUF_VOX * VSTRIDE;  // bytes per staging buffer
+
+// LDS byte (relative to a staging buffer) of staging granule q.
+__host__ __device__ inline int stage_slot(int q) {
+  const int c = q < 2 * BUF_VOX - 1 ? q : 2 * BUF_VOX - 1;
+  return (c >> 1) * VSTRIDE + (c & 1) * 16;
+}
+
+// Wave split of the 256 x COUT output tile: WN waves across the channels
+// (64 each, NB = 2 blocks of 32), WM across the voxels (ROWS each, MB blocks
+// of 32).
+template <int COUT>
+struct Split {
+  static constexpr int NB = 2;
+  static constexpr int WN = COUT / 64;
+  static constexpr int WM = (NT / 64) / WN;
+  static constexpr int ROWS = kTileRows / WM;
+  static constexpr int MB = ROWS / 32;
+  static_assert(WM * WN * 64 == NT && WN * NB * 32 == COUT && WM * MB * 32 == kTileRows, "wave split");
+};
+
+// LDS layout of one workgroup (byte offsets): two staging buffers, a
+// 256-byte zero region (256-aligned, for halo-column reads), the bias
+// [COUT] and the head weights [4][COUT].  The head epilogue puts its
+// partial sums in the staging buffer the tile read last.
+template <int COUT>
+struct Lds {
+  static constexpr int zero = 2 * ABUF;
+  static constexpr int bias = zero + 256;
+  static constexpr int headw = bias + COUT * 4;
+  static constexpr int total = headw + 4 * COUT * 4;
+  static_assert(zero % 256 == 0, "zero region must be 256-aligned");
+  static_assert(2 * total <= 160 * 1024, "two workgroups per CU");
+  static_assert((COUT / 64) * kTileRows * 4 * 4 <= ABUF, "head partials fit a staging buffer");
+};
+
+__device__ __forceinline__ float activation(float y, int act) {
+  if (act == 1) {  // GELU, tanh form: 0.5 y (1 + tanh(u)) = y / (1 + exp(-2u))
+    const float k0 = 0.7978845608028654f;          // sqrt(2 / pi)
+    const float kl = -2.0f * 1.4426950408889634f;  // -2 log2(e)
+    const float u = k0 * (y + 0.044715f * y * y * y);
+    const float e = __builtin_amdgcn_exp2f(kl * u);
+    return y * __builtin_amdgcn_rcpf(1.0f + e);
+  }
+  if (act == 2) return y > 0.0f ? y : 0.0f;
+  return y;
+}
+
+__device__ __forceinline__ uint32_t bf16_bits(float v) {
+  __bf16 h = (__bf16)v;
+  return (uint32_t)__builtin_bit_cast(uint16_t, h);
+}
+__device__ __forceinline__ float bf16_round(float v) { return __uint_as_float(bf16_bits(v) << 16); }
+
+// Staging granule q = NT k + tid is granule q & 1 (16 bytes) of staged voxel
+// q >> 1; it goes to LDS byte (q >> 1) * VSTRIDE + 16 (q & 1).  The loads are
+// buffer loads relative to the tile's staging base (a padded voxel index no
+// larger than any voxel the tile stages): per round, a lane's byte offset is
+// the same for every chunk of the tile.  Granules past the footprint, and
+// voxels outside the volume, get an offset past the buffer's range, for
+// which the load returns zeros.
+constexpr uint32_t kNoVoxel = 0x80000000u;
+constexpr uint32_t kStageRange = 0x7FFFFFF0u;  // buffer range in bytes; every real offset is far below
+
+// A value the whole wave agrees on, marked as such for the compiler (the
+// 64-bit index arithmetic would otherwise leave it in vector registers, and
+// a buffer resource built from it would need a per-lane loop).
+__host__ __device__ inline long long wave_uniform(long long v) {
+#ifndef __HIP_DEVICE_COMPILE__
+  return v;
+#else
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((unsigned long long)v >> 32));
+  return (long long)(((unsigned long long)hi << 32) | lo);
+#endif
+}
+
+template <int MODE>
+__host__ __device__ inline long long stage_base(const Geom& g, const StageSrc& src) {
+  if constexpr (MODE == 0) return wave_uniform(src.origin <= 0 ? 0 : line_to_padded(g, src.origin));
+  return wave_uniform(src.origin);
+}
+
+template <int CIN, int MODE>
+__host__ __device__ inline uint32_t stage_offset(const Geom& g, const Tiling& tl, const StageSrc& src,
+                                                 long long base, long long limit, int ngran, int k, int tid) {
+  const int q = k * NT + tid;
+  const long long gv = staged_voxel_fast<MODE>(g, tl, src, q >> 1, limit);
+  return (q < ngran && gv >= 0) ? (uint32_t)((gv - base) * (CIN * 2) + (q & 1) * 16) : kNoVoxel;
+}
+
+// Buffer resource over the activations from padded voxel `base`, channel
+// offset `ch` on.
+template <int CIN>
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t stage_rsrc(const uint16_t* x, long long base, int ch) {
+  return __builtin_amdgcn_make_buffer_rsrc((void*)(x + base * CIN + ch), 0, kStageRange, 0x00020000);
+}
+
+template <int CIN, int COUT, bool HEAD, int MODE>
+__global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
+conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, uint16_t* __restrict__ y,
+                   const u32x4* __restrict__ wfrag, const float* __restrict__ bias,
+                   const float* __restrict__ head_w, const float* __restrict__ head_b,
+                   const int32_t* __restrict__ comp_of_site, uint8_t* __restrict__ nib,
+                   float* __restrict__ logits, int batch) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  using W = Split<COUT>;
+  using L = Lds<COUT>;
+  constexpr int MB = W::MB;
+  constexpr int NB = W::NB;
+  constexpr int NBT = COUT / 32;  // 32-channel blocks in total
+  constexpr int NCHUNK = CIN / KC;
+  constexpr int TSTEPS = NCHUNK * STEPS;  // k-steps per tile
+  static_assert(TSTEPS % BRING == 0, "the weight ring lines up with tile boundaries");
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave % W::WM, wn = wave / W::WM;
+  const int half = lane >> 5, l32 = lane & 31;
+  const int ntiles = (int)tl.ntiles;
+  const long long limit = (long long)batch * g.S;
+  const int ngran = tl.span * 2;  // 16-byte granules of a staged chunk
+
+  lds_char* const lds = (lds_char*)smem;
+  lds_char* const zero = lds + L::zero;
+  lds_float* const bias_s = (lds_float*)(lds + L::bias);
+  lds_float* const headw_s = (lds_float*)(lds + L::headw);
+  for (int e = tid; e < COUT; e += NT) bias_s[e] = bias[e];
+  if (tid < 64) ((lds_u32_w*)zero)[tid] = 0u;
+  const uint32_t zero_addr = (uint32_t)(uintptr_t)zero;
+  if (HEAD)
+    for (int e = tid; e < 4 * COUT; e += NT) headw_s[e] = head_w[e];
+
+  int tile = tile_of(blockIdx.x, gridDim.x, 0, ntiles);
+  if (tile < 0) return;
+
+  auto source_of = [&](int t) {
+    StageSrc src;
+    long long p;
+    int lb;
+    tile_row(g, tl, t, 0, batch, &p, &lb, &src.origin);
+    src.bo = box_origin(g, tl, src.origin);
+    return src;
+  };
+  long long cur_base = stage_base<MODE>(g, source_of(tile));
+  uint32_t soff[RMAX];  // this lane's staging offsets of the tile being staged
+  {
+    const StageSrc src = source_of(tile);
+#pragma unroll
+    for (int k = 0; k < RMAX; ++k) soff[k] = stage_offset<CIN, MODE>(g, tl, src, cur_base, limit, ngran, k, tid);
+  }
+
+  // First tile: stage its first chunk synchronously.
+  {
+    const __amdgpu_buffer_rsrc_t rs = stage_rsrc<CIN>(x, cur_base, 0);
+#pragma unroll
+    for (int k = 0; k < RMAX; ++k) {
+      const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(rs, soff[k], 0, 0);
+      *(lds_u32x4_w*)(lds + stage_slot(k * NT + tid)) = v;
+    }
+  }
+
+  // weight fragment (tile-step gs, block nb of this wave's channels): a
+  // buffer load with this lane's 16-byte slot as the vector offset and the
+  // fragment's offset as the scalar one (no per-load address arithmetic)
+  const __amdgpu_buffer_rsrc_t wres =
+      __builtin_amdgcn_make_buffer_rsrc((void*)wfrag, 0, TSTEPS * NBT * 1024, 0x00020000);
+  const uint32_t woff = (uint32_t)((wn * NB * 64 + lane) * 16);
+  auto wload = [&](int gs, int nb) -> u32x4 {
+    return __builtin_amdgcn_raw_buffer_load_b128(wres, woff, (gs * NBT + nb) * 1024, 0);
+  };
+  // weight-fragment ring: slot k holds tile-step gs, gs % BRING == k
+  u32x4 bq[BRING][NB];
+#pragma unroll
+  for (int st = 0; st < BRING - 1; ++st)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) bq[st][nb] = wload(st, nb);
+  __syncthreads();  // staged chunk, bias, zero region and head weights visible
+
+  int gchunk = 0;  // chunks processed by this workgroup (selects the LDS buffer)
+  for (int it = 0; tile >= 0; ++it) {
+    const int next = tile_of(blockIdx.x, gridDim.x, it + 1, ntiles);
+    const StageSrc next_src = source_of(next >= 0 ? next : tile);
+    const long long next_base = stage_base<MODE>(g, next_src);
+    // rows of this lane: voxel wm ROWS + 32 mb + l32 of the tile; LDS
+    // offset of the row's (0,0,0) tap within a staging buffer (plus this
+    // lane's granule) and, for flat tiles, the masks that send reads of the
+    // left / right halo column to `zero`
+    uint32_t rrel[MB], em0[MB], em2[MB];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      long long p = -1, o;
+      int lb = 0, col = -1;
+      tile_row(g, tl, tile, wm * W::ROWS + mb * 32 + l32, batch, &p, &lb, &o, &col);
+      rrel[mb] = (uint32_t)(lb * VSTRIDE + half * 16);
+      em0[mb] = (MODE == 0 && col == 0) ? 0xFFFFFF00u : 0u;
+      em2[mb] = (MODE == 0 && col == g.H - 1) ? 0xFFFFFF00u : 0u;
+    }
+
+    f32x16 acc[MB][NB];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[mb][nb][v] = 0.0f;
+
+    for (int chunk = 0; chunk < NCHUNK; ++chunk, ++gchunk) {
+      lds_char* const cur = lds + (gchunk & 1) * ABUF;
+      lds_char* const oth = lds + ((gchunk + 1) & 1) * ABUF;
+      // the chunk staged next: the following chunk of this tile, else the
+      // first chunk of the next tile, else nothing
+      const bool more = chunk + 1 < NCHUNK;
+      const int sgran = (more || next >= 0) ? ngran : 0;
+      // the next tile's offsets replace soff round by round during the
+      // last chunk (past the last tile: none, every granule empty)
+      const __amdgpu_buffer_rsrc_t srs =
+          more ? stage_rsrc<CIN>(x, cur_base, (chunk + 1) * KC) : stage_rsrc<CIN>(x, next_base, 0);
+      u32x4 stg;
+
+      uint32_t rbase[MB];
+      const uint32_t cur_u = (uint32_t)(uintptr_t)cur;
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) rbase[mb] = cur_u + rrel[mb];
+      // LDS address of the fragment of row block mb for tap st: the tap's
+      // voxel offset is common to the wave; halo-column taps of flat tiles go
+      // to the zero region (v_bfi keeps the low 8 address bits: same bank
+      // group, so the read stays conflict-free).  rbase is made opaque before
+      // each use so that every step computes its own addresses instead of
+      // the compiler computing all of them at the top of the chunk.
+      auto frag_read = [&](int mb, int st) -> u32x4 {
+        asm volatile("" : "+v"(rbase[mb]));
+        const int dt = st / 9, di = (st / 3) % 3, dj = st % 3;
+        const uint32_t toff = (uint32_t)((dt * tl.sa + di * tl.sb + dj) * VSTRIDE);
+        uint32_t a = rbase[mb] + toff;
+        if (MODE == 0 && dj != 1) {
+          uint32_t r;
+          asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(r) : "v"(dj == 0 ? em0[mb] : em2[mb]), "s"(zero_addr), "v"(a));
+          a = r;
+        }
+        return *(lds_u32x4*)(uintptr_t)a;
+      };
+      // One register set of activation fragments: av[mb] is re-read for the
+      // next step as soon as this step's two MFMAs on it have issued, so it
+      // has the other row blocks' MFMAs to arrive.  Weight fragments are
+      // loaded two steps ahead, staging rounds in the shadow of row block 0.
+      u32x4 av[MB];
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) av[mb] = frag_read(mb, 0);
+      const int gbase = chunk * STEPS;  // tile-step of this chunk's step 0
+#pragma unroll
+      for (int st = 0; st < STEPS; ++st) {
+        {
+          int gs = gbase + st + BRING - 1;  // wraps into the next tile's steps
+          if (gs >= TSTEPS) gs -= TSTEPS;
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) bq[(st + BRING - 1) % BRING][nb] = wload(gs, nb);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb)
+            acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, bq[st % BRING][nb]),
+                                                                  __builtin_bit_cast(bf16x8, av[mb]), acc[mb][nb],
+                                                                  0, 0, 0);
+          __builtin_amdgcn_sched_barrier(0);
+          if (st + 1 < STEPS) av[mb] = frag_read(mb, st + 1);
+          if (mb == 0) {
+            // staging of the next chunk: round k is loaded at step 3k and
+            // stored to LDS at step 3k + 3, just before round k + 1 is loaded
+            if (st >= 3 && st % 3 == 0 && st / 3 - 1 < RMAX)
+              *(lds_u32x4_w*)(oth + stage_slot((st / 3 - 1) * NT + tid)) = stg;
+            if (st % 3 == 0 && st / 3 < RMAX) {
+              const int k = st / 3;
+              if (!more) soff[k] = stage_offset<CIN, MODE>(g, tl, next_src, next_base, limit, sgran, k, tid);
+              stg = __builtin_amdgcn_raw_buffer_load_b128(srs, soff[k], 0, 0);
+            }
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+      // every wave's staging writes done, every wave done reading `cur`
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+      __builtin_amdgcn_s_barrier();
+    }
+
+    // output row of each row block (recomputed: not kept live through the K loop)
+    int pidx[MB];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      long long p = -1, o;
+      int lb;
+      pidx[mb] = tile_row(g, tl, tile, wm * W::ROWS + mb * 32 + l32, batch, &p, &lb, &o) ? (int)p : -1;
+    }
+
+    // ---- epilogue: lane holds channels co .. co + 3 (co = 64 wn + 32 nb +
+    // 8 q + 4 half) of voxel row wm ROWS + 32 mb + l32 ----
+    if constexpr (!HEAD) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int co = (wn * NB + nb) * 32 + q * 8 + half * 4;
+          const float4 bv = {bias_s[co], bias_s[co + 1], bias_s[co + 2], bias_s[co + 3]};
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) {
+            const float v0 = activation(acc[mb][nb][4 * q + 0] + bv.x, act);
+            const float v1 = activation(acc[mb][nb][4 * q + 1] + bv.y, act);
+            const float v2 = activation(acc[mb][nb][4 * q + 2] + bv.z, act);
+            const float v3 = activation(acc[mb][nb][4 * q + 3] + bv.w, act);
+            u32x2 packed;
+            packed.x = bf16_bits(v0) | (bf16_bits(v1) << 16);
+            packed.y = bf16_bits(v2) | (bf16_bits(v3) << 16);
+            if (pidx[mb] >= 0) *reinterpret_cast<u32x2*>(y + (long long)pidx[mb] * COUT + co) = packed;
+          }
+        }
+    } else {
+      // 1x1x1 head on the bf16-rounded activations: partial sums over this
+      // lane's channels, then over the half-waves, then over the channel
+      // waves through LDS (the buffer this tile read last)
+      lds_float* const head_part = (lds_float*)(lds + ((gchunk - 1) & 1) * ABUF);  // [WN][256][4]
+      float part[MB][4];
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int o = 0; o < 4; ++o) part[mb][o] = 0.0f;
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int co = (wn * NB + nb) * 32 + q * 8 + half * 4;
+          const float4 bv = {bias_s[co], bias_s[co + 1], bias_s[co + 2], bias_s[co + 3]};
+          float4 hw[4];
+#pragma unroll
+          for (int o = 0; o < 4; ++o)
+            hw[o] = {headw_s[o * COUT + co], headw_s[o * COUT + co + 1], headw_s[o * COUT + co + 2],
+                     headw_s[o * COUT + co + 3]};
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) {
+            const float a0 = bf16_round(activation(acc[mb][nb][4 * q + 0] + bv.x, act));
+            const float a1 = bf16_round(activation(acc[mb][nb][4 * q + 1] + bv.y, act));
+            const float a2 = bf16_round(activation(acc[mb][nb][4 * q + 2] + bv.z, act));
+            const float a3 = bf16_round(activation(acc[mb][nb][4 * q + 3] + bv.w, act));
+#pragma unroll
+            for (int o = 0; o < 4; ++o)
+              part[mb][o] += hw[o].x * a0 + hw[o].y * a1 + hw[o].z * a2 + hw[o].w * a3;
+          }
+        }
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int o = 0; o < 4; ++o) part[mb][o] += __shfl_xor(part[mb][o], 32);
+      if (half == 0) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          lds_float* hp = head_part + (wn * kTileRows + wm * W::ROWS + mb * 32 + l32) * 4;
+          hp[0] = part[mb][0];
+          hp[1] = part[mb][1];
+          hp[2] = part[mb][2];
+          hp[3] = part[mb][3];
+        }
+      }
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): partials written
+      __builtin_amdgcn_s_barrier();
+      // one thread per voxel row: logits, threshold, flip nibble
+      static_assert(NT == kTileRows, "one thread per tile row");
+      {
+        const int r = tid;
+        long long p = -1, o2;
+        int lb;
+        if (tile_row(g, tl, tile, r, batch, &p, &lb, &o2)) {
+          float lg[4] = {head_b[0], head_b[1], head_b[2], head_b[3]};
+#pragma unroll
+          for (int w2 = 0; w2 < W::WN; ++w2) {
+            const lds_float* hp = head_part + (w2 * kTileRows + r) * 4;
+            lg[0] += hp[0];
+            lg[1] += hp[1];
+            lg[2] += hp[2];
+            lg[3] += hp[3];
+          }
+          // padded index -> (b, t, i, j)
+          const int b = (int)(p / g.S);
+          const int rem = (int)(p - (long long)b * g.S);
+          const int t = rem / g.P - 1;
+          const int r2 = rem - (t + 1) * g.P;
+          const int i = r2 / g.Wp - 1, j = r2 - (i + 1) * g.Wp - 1;
+          const int HH = g.H * g.H;
+          const int s = i * g.H + j;
+          const int n = comp_of_site[s];
+          const bool data = (i < g.d) && (j < g.d);
+          unsigned bits = 0;
+          if (data && lg[0] > 0.0f) bits |= 1u;
+          if (data && lg[1] > 0.0f) bits |= 2u;
+          if (n >= 0 && n < g.K && lg[2] > 0.0f) bits |= 4u;
+          if (n >= g.K && lg[3] > 0.0f) bits |= 8u;
+          nib[(long long)b * g.V + (long long)t * HH + s] = (uint8_t)bits;
+          if (logits) {
+#pragma unroll
+            for (int o = 0; o < 4; ++o) logits[(((long long)b * 4 + o) * g.T + t) * HH + s] = lg[o];
+          }
+        }
+      }
+      // the partials' buffer is where the next tile's second chunk is staged
+      __builtin_amdgcn_s_waitcnt(0xc07f);
+      __builtin_amdgcn_s_barrier();
+    }
+    tile = next;
+    cur_base = next_base;
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
+template <int CIN, int COUT, bool HEAD, int MODE>
+hipError_t launch_one(const Geom& g, const Tiling& tl, int act, const void* x, void* y, const void* wfrag,
+                      const float* bias, const float* head_w, const float* head_b, const int32_t* comp_of_site,
+                      uint8_t* nib, float* logits, int batch, int n_workgroups, hipStream_t stream) {
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute((const void*)conv_hidden_kernel<CIN, COUT, HEAD, MODE>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, Lds<COUT>::total);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  const long long nwg = conv_workgroups(tl.ntiles, n_workgroups);
+  hipLaunchKernelGGL((conv_hidden_kernel<CIN, COUT, HEAD, MODE>), dim3((unsigned)nwg), dim3(NT),
+                     (size_t)Lds<COUT>::total, stream, g, tl, act, (const uint16_t*)x, (uint16_t*)y,
+                     (const u32x4*)wfrag, bias, head_w, head_b, comp_of_site, nib, logits, batch);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int conv_hidden_max_span() { return MAX_SPAN; }
+int conv_hidden_workgroups_per_cu() { return 2; }
+
+#define PD_HIDDEN_CASE(CI, CO)                                                                               \
+  if (cin == CI && cout == CO) {                                                                            \
+    if (head && tl.mode == 0)                                                                                \
+      return launch_one<CI, CO, true, 0>(g, tl, act, x, y, wfrag, bias, head_w, head_b, comp_of_site, nib,    \
+                                         logits, batch, n_workgroups, stream);                               \
+    if (head)                                                                                                \
+      return launch_one<CI, CO, true, 1>(g, tl, act, x, y, wfrag, bias, head_w, head_b, comp_of_site, nib,    \
+                                         logits, batch, n_workgroups, stream);                               \
+    if (tl.mode == 0)                                                                                        \
+      return launch_one<CI, CO, false, 0>(g, tl, act, x, y, wfrag, bias, head_w, head_b, comp_of_site, nib,   \
+                                          logits, batch, n_workgroups, stream);                              \
+    return launch_one<CI, CO, false, 1>(g, tl, act, x, y, wfrag, bias, head_w, head_b, comp_of_site, nib,     \
+                                        logits, batch, n_workgroups, stream);                                \
+  }
+
+hipError_t launch_conv_hidden(const Geom& g, const Tiling& tl, int cin, int cout, int act, const void* x,
+                              void* y, const void* wfrag, const float* bias, int head, const float* head_w,
+                              const float* head_b, const int32_t* comp_of_site, uint8_t* nib, float* logits,
+                              int batch, int n_workgroups, hipStream_t stream) {
+  if (tl.span <= 0 || tl.span > MAX_SPAN) return hipErrorInvalidValue;
+  PD_HIDDEN_CASE(64, 64)
+  PD_HIDDEN_CASE(128, 128)
+  PD_HIDDEN_CASE(64, 128)
+  PD_HIDDEN_CASE(128, 64)
+  return hipErrorInvalidValue;
+}
+
+}  // namespace pd

@@ -104,20 +104,33 @@ constexpr int kTileRows = 256;
 hipError_t launch_unpack(const Geom& g, const int32_t* comp_of_site, const uint64_t* det, int batch,
                          void* out, int out_padded, int fp32, hipStream_t stream);
 
-// One 3x3x3 bf16 layer.  head != 0: the 1x1x1 head (head_w [4][cout] fp32,
-// bf16-valued; head_b [4]) and the threshold are applied in the epilogue,
-// which writes flip nibbles (and logits if non-null) instead of y.
-hipError_t launch_conv_bf16(const Geom& g, const Tiling& tl, int cin, int cout, int act, const void* x,
-                            void* y, const void* wfrag, const float* bias, int head, const float* head_w,
-                            const float* head_b, const int32_t* comp_of_site, uint8_t* nib, float* logits,
-                            int batch, int n_workgroups, hipStream_t stream);
 // The first 3x3x3 layer (c_in = 2, c_out = 64 or 128) when it is not also
 // the last hidden layer: planes [batch * S] (2 bf16 channels each), weight
-// fragments as for launch_conv_bf16.
+// fragments [4 k-steps][c_out / 32][64 lanes][8 bf16].
 hipError_t launch_conv_first(const Geom& g, int cout, int act, const void* planes, void* y, const void* wfrag,
                              const float* bias, int batch, hipStream_t stream);
-size_t conv_bf16_lds_bytes(int cin, int span);
-int conv_bf16_max_span();  // staged voxels a tile may need
+
+// A network with one hidden layer: layer 1 (as launch_conv_first) with the
+// 1x1x1 head (head_w [4][cout] fp32, bf16-valued; head_b [4]) and the
+// threshold in its epilogue, which writes flip nibbles (and logits if
+// non-null).  n_workgroups: one per CU.
+hipError_t launch_conv_single(const Geom& g, const Tiling& tl, int cout, int act, const void* planes,
+                              const void* wfrag, const float* bias, const float* head_w, const float* head_b,
+                              const int32_t* comp_of_site, uint8_t* nib, float* logits, int batch,
+                              int n_workgroups, hipStream_t stream);
+int conv_single_max_span();  // staged voxels a tile may need
+
+// A hidden 3x3x3 bf16 layer (c_in, c_out in {64, 128}) on the zero-halo
+// activations x -> y.  head != 0: the head and the threshold are applied in
+// the epilogue as for launch_conv_single, instead of writing y.  Weight
+// fragments in 16-channel chunks (conv_fragments in api.hip);
+// n_workgroups = conv_hidden_workgroups_per_cu() per CU.
+hipError_t launch_conv_hidden(const Geom& g, const Tiling& tl, int cin, int cout, int act, const void* x,
+                              void* y, const void* wfrag, const float* bias, int head, const float* head_w,
+                              const float* head_b, const int32_t* comp_of_site, uint8_t* nib, float* logits,
+                              int batch, int n_workgroups, hipStream_t stream);
+int conv_hidden_max_span();
+int conv_hidden_workgroups_per_cu();
 
 // Persistent workgroups of a conv launch: one per CU (n_workgroups), a
 // multiple of 8 (one per XCD round-robin slot), never more than the tiles

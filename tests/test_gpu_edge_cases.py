@@ -111,3 +111,13 @@ def test_width_changes(cuda):
     det, _ = workload.make_inputs(d, T, B, 0.01, 0.01, seed=62)
     say("width changes 2-64-128-64-128-4")
     check(d, T, layers, w, det, "bf16")
+
+
+@pytest.mark.parametrize("width,d,T,B", [(64, 9, 7, 3), (128, 13, 5, 2), (128, 25, 3, 1), (64, 31, 2, 1)])
+def test_single_hidden_layer(cuda, width, d, T, B):
+    # layer 1 carries the head and the threshold (flat and box tilings)
+    layers = workload.layer_spec(1, width)
+    w = workload.he_normal_weights(layers, seed=71 + d)
+    det, _ = workload.make_inputs(d, T, B, 0.01, 0.01, seed=72 + d)
+    say("one hidden layer, width", width, "d", d, "T", T, "B", B)
+    check(d, T, layers, w, det, "bf16")
