@@ -36,10 +36,11 @@
 //     (arranged at create time in MFMA operand order, one coalesced 16-byte
 //     load per lane; a layer is <= 0.9 MB and stays in L2) two steps ahead
 //     through a 3-deep register ring that runs on across chunks and tiles.
-//   * Epilogue: + bias, activation in fp32, bf16 (RNE), stored straight from
-//     the accumulators (8 bytes per lane, two half-waves covering 16
-//     consecutive bytes of a voxel row); no workgroup barrier, so a wave can
-//     start the next tile while the others finish theirs.
+//   * Epilogue: + bias, activation in fp32, bf16 (RNE); each wave transposes
+//     its rows through its own slice of the staging buffer the tile read last
+//     and writes whole 128-byte lines.  No barrier ends the tile: a wave
+//     starts the next one at once, and only that tile's first staging store
+//     (three k-steps in) waits for the others to leave the buffer.
 #include "internal.h"
 #include "tiles.h"
 
@@ -55,6 +56,7 @@ typedef __attribute__((address_space(3))) const u32x4 lds_u32x4;
 typedef __attribute__((address_space(3))) float lds_float;
 typedef __attribute__((address_space(3))) u32x4 lds_u32x4_w;
 typedef __attribute__((address_space(3))) uint32_t lds_u32_w;
+typedef __attribute__((address_space(3))) u32x2 lds_u32x2_w;
 
 constexpr int NT = 256;       // threads per workgroup: 4 wave64
 constexpr int KC = 16;        // input channels per LDS chunk (one MFMA k-step)
@@ -105,6 +107,8 @@ struct Lds {
   static_assert(zero % 256 == 0, "zero region must be 256-aligned");
   static_assert(2 * total <= 160 * 1024, "two workgroups per CU");
   static_assert((COUT / 64) * kTileRows * 4 * 4 <= ABUF, "head partials fit a staging buffer");
+  static_assert((NT / 64) * 64 * 128 <= ABUF, "epilogue transposition slices fit a staging buffer");
+  static_assert(Split<COUT>::MB % 2 == 0, "the epilogue transposes row blocks in pairs");
 };
 
 __device__ __forceinline__ float activation(float y, int act) {
@@ -340,8 +344,12 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
           if (mb == 0) {
             // staging of the next chunk: round k is loaded at step 3k and
             // stored to LDS at step 3k + 3, just before round k + 1 is loaded
-            if (st >= 3 && st % 3 == 0 && st / 3 - 1 < RMAX)
+            if (st >= 3 && st % 3 == 0 && st / 3 - 1 < RMAX) {
+              // a tile's first chunk stages into the buffer the previous
+              // epilogue transposed through: wait for every wave to leave it
+              if (!HEAD && st == 3 && chunk == 0) __builtin_amdgcn_s_barrier();
               *(lds_u32x4_w*)(oth + stage_slot((st / 3 - 1) * NT + tid)) = stg;
+            }
             if (st % 3 == 0 && st / 3 < RMAX) {
               const int k = st / 3;
               if (!more) soff[k] = stage_offset<CIN, MODE>(g, tl, next_src, next_base, limit, sgran, k, tid);
@@ -368,24 +376,48 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
     // ---- epilogue: lane holds channels co .. co + 3 (co = 64 wn + 32 nb +
     // 8 q + 4 half) of voxel row wm ROWS + 32 mb + l32 ----
     if constexpr (!HEAD) {
+      // bias + activation + bf16, transposed through this wave's slice of
+      // the staging buffer the tile read last (64 rows x 128 bytes, granule
+      // c of row r at c ^ (r % 8)), then stored as whole 128-byte halves of
+      // voxel rows, 8 rows per instruction.  The next tile's first staging
+      // store waits at a barrier until every wave is done here.
+      lds_char* const tb = lds + ((gchunk - 1) & 1) * ABUF + wave * (64 * 128);
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
+      for (int ps = 0; ps < MB / 2; ++ps) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int co = (wn * NB + nb) * 32 + q * 8 + half * 4;
-          const float4 bv = {bias_s[co], bias_s[co + 1], bias_s[co + 2], bias_s[co + 3]};
+        for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-          for (int mb = 0; mb < MB; ++mb) {
-            const float v0 = activation(acc[mb][nb][4 * q + 0] + bv.x, act);
-            const float v1 = activation(acc[mb][nb][4 * q + 1] + bv.y, act);
-            const float v2 = activation(acc[mb][nb][4 * q + 2] + bv.z, act);
-            const float v3 = activation(acc[mb][nb][4 * q + 3] + bv.w, act);
-            u32x2 packed;
-            packed.x = bf16_bits(v0) | (bf16_bits(v1) << 16);
-            packed.y = bf16_bits(v2) | (bf16_bits(v3) << 16);
-            if (pidx[mb] >= 0) *reinterpret_cast<u32x2*>(y + (long long)pidx[mb] * COUT + co) = packed;
+          for (int q = 0; q < 4; ++q) {
+            const int c = nb * 4 + q;  // 16-byte granule of the wave's 64 channels
+            const int co = wn * 64 + c * 8 + half * 4;
+            const float4 bv = {bias_s[co], bias_s[co + 1], bias_s[co + 2], bias_s[co + 3]};
+#pragma unroll
+            for (int m = 0; m < 2; ++m) {
+              const int mb = 2 * ps + m;
+              const float v0 = activation(acc[mb][nb][4 * q + 0] + bv.x, act);
+              const float v1 = activation(acc[mb][nb][4 * q + 1] + bv.y, act);
+              const float v2 = activation(acc[mb][nb][4 * q + 2] + bv.z, act);
+              const float v3 = activation(acc[mb][nb][4 * q + 3] + bv.w, act);
+              u32x2 packed;
+              packed.x = bf16_bits(v0) | (bf16_bits(v1) << 16);
+              packed.y = bf16_bits(v2) | (bf16_bits(v3) << 16);
+              const int r = m * 32 + l32;
+              *(lds_u32x2_w*)(tb + r * 128 + ((c ^ (r & 7)) << 4) + half * 8) = packed;
+            }
           }
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's rows are in LDS
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int it2 = 0; it2 < 8; ++it2) {
+          const int gi = it2 * 64 + lane;
+          const int r = gi >> 3, c = gi & 7;
+          const u32x4 v = *(lds_u32x4*)(tb + r * 128 + ((c ^ (r & 7)) << 4));
+          const int pr = __shfl(pidx[2 * ps + (it2 >> 2)], r & 31);
+          if (pr >= 0) *reinterpret_cast<u32x4*>(y + (long long)pr * COUT + wn * 64 + c * 8) = v;
         }
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // the reads are done before the next pass writes
+        __builtin_amdgcn_wave_barrier();
+      }
     } else {
       // 1x1x1 head on the bf16-rounded activations: partial sums over this
       // lane's channels, then over the half-waves, then over the channel
