@@ -16,6 +16,7 @@
 //   * Epilogue: + bias, activation, bf16; the wave transposes its 32 x c_out
 //     tile through its own LDS slice and writes whole voxel rows with
 //     16-byte stores.
+#include "activation.h"
 #include "internal.h"
 
 namespace pd {
@@ -32,23 +33,6 @@ typedef __attribute__((address_space(3))) u32x4 lds_u32x4_w;
 
 constexpr int WAVES = 4;  // waves per workgroup
 constexpr int BPW = 2;    // 32-voxel blocks per wave
-
-__device__ __forceinline__ float activation(float y, int act) {
-  if (act == 1) {  // GELU, tanh form: 0.5 y (1 + tanh(u)) = y / (1 + exp(-2u))
-    const float k0 = 0.7978845608028654f;          // sqrt(2 / pi)
-    const float kl = -2.0f * 1.4426950408889634f;  // -2 log2(e)
-    const float u = k0 * (y + 0.044715f * y * y * y);
-    const float e = __builtin_amdgcn_exp2f(kl * u);
-    return y * __builtin_amdgcn_rcpf(1.0f + e);
-  }
-  if (act == 2) return y > 0.0f ? y : 0.0f;
-  return y;
-}
-
-__device__ __forceinline__ uint32_t bf16_bits(float v) {
-  __bf16 h = (__bf16)v;
-  return (uint32_t)__builtin_bit_cast(uint16_t, h);
-}
 
 // Divisors of the interior-voxel decode u -> (b, t, i, j).
 struct Decode {
@@ -85,8 +69,8 @@ __device__ __forceinline__ void gather(const Geom& g, const uint32_t* __restrict
 
 // Each workgroup stages the weight fragments in LDS once; each of its waves
 // then handles BPW consecutive 32-voxel blocks.
-template <int COUT>
-__global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, int act, const uint32_t* __restrict__ planes,
+template <int COUT, int ACT>
+__global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, const uint32_t* __restrict__ planes,
                                                                 uint16_t* __restrict__ y,
                                                                 const u32x4* __restrict__ wfrag,
                                                                 const float* __restrict__ bias, Decode dc,
@@ -138,10 +122,10 @@ __global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, int act,
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const int co = (h0 + nb) * 32 + q * 8 + half * 4;
-          const float v0 = activation(acc[nb][4 * q + 0] + bias[co + 0], act);
-          const float v1 = activation(acc[nb][4 * q + 1] + bias[co + 1], act);
-          const float v2 = activation(acc[nb][4 * q + 2] + bias[co + 2], act);
-          const float v3 = activation(acc[nb][4 * q + 3] + bias[co + 3], act);
+          const float v0 = act_fn<ACT>(acc[nb][4 * q + 0] + bias[co + 0]);
+          const float v1 = act_fn<ACT>(acc[nb][4 * q + 1] + bias[co + 1]);
+          const float v2 = act_fn<ACT>(acc[nb][4 * q + 2] + bias[co + 2]);
+          const float v3 = act_fn<ACT>(acc[nb][4 * q + 3] + bias[co + 3]);
           u32x2 packed;
           packed.x = bf16_bits(v0) | (bf16_bits(v1) << 16);
           packed.y = bf16_bits(v2) | (bf16_bits(v3) << 16);
@@ -174,17 +158,19 @@ hipError_t launch_conv_first(const Geom& g, int cout, int act, const void* plane
   dc.by_v = make_fastdiv((uint32_t)g.V);
   dc.by_hh = make_fastdiv((uint32_t)(g.H * g.H));
   dc.by_h = make_fastdiv((uint32_t)g.H);
-  if (cout == 64) {
-    const size_t lds = (size_t)4 * 2 * 64 * 16 + (size_t)WAVES * 32 * (64 * 2 + 16 + 4);
-    hipLaunchKernelGGL(conv_first_kernel<64>, dim3((unsigned)nblk), dim3(64 * WAVES), lds, stream, g, act,
-                       (const uint32_t*)planes, (uint16_t*)y, (const u32x4*)wfrag, bias, dc, (int)nvox);
-  } else if (cout == 128) {
-    const size_t lds = (size_t)4 * 4 * 64 * 16 + (size_t)WAVES * 32 * (128 * 2 + 16 + 4);
-    hipLaunchKernelGGL(conv_first_kernel<128>, dim3((unsigned)nblk), dim3(64 * WAVES), lds, stream, g, act,
-                       (const uint32_t*)planes, (uint16_t*)y, (const u32x4*)wfrag, bias, dc, (int)nvox);
-  } else {
-    return hipErrorInvalidValue;
-  }
+  auto launch = [&](auto CO, auto A) {
+    constexpr int C = decltype(CO)::value;
+    const size_t lds = (size_t)4 * (C / 32) * 64 * 16 + (size_t)WAVES * 32 * (C * 2 + 16 + 4);
+    hipLaunchKernelGGL((conv_first_kernel<C, decltype(A)::value>), dim3((unsigned)nblk), dim3(64 * WAVES), lds,
+                       stream, g, (const uint32_t*)planes, (uint16_t*)y, (const u32x4*)wfrag, bias, dc, (int)nvox);
+  };
+  if ((cout != 64 && cout != 128) || act < 0 || act > 2) return hipErrorInvalidValue;
+  with_activation(act, [&](auto A) {
+    if (cout == 64)
+      launch(std::integral_constant<int, 64>(), A);
+    else
+      launch(std::integral_constant<int, 128>(), A);
+  });
   return hipGetLastError();
 }
 

@@ -41,6 +41,7 @@
 //     and writes whole 128-byte lines.  No barrier ends the tile: a wave
 //     starts the next one at once, and only that tile's first staging store
 //     (three k-steps in) waits for the others to leave the buffer.
+#include "activation.h"
 #include "internal.h"
 #include "tiles.h"
 
@@ -110,24 +111,6 @@ struct Lds {
   static_assert((NT / 64) * 64 * 128 <= ABUF, "epilogue transposition slices fit a staging buffer");
   static_assert(Split<COUT>::MB % 2 == 0, "the epilogue transposes row blocks in pairs");
 };
-
-__device__ __forceinline__ float activation(float y, int act) {
-  if (act == 1) {  // GELU, tanh form: 0.5 y (1 + tanh(u)) = y / (1 + exp(-2u))
-    const float k0 = 0.7978845608028654f;          // sqrt(2 / pi)
-    const float kl = -2.0f * 1.4426950408889634f;  // -2 log2(e)
-    const float u = k0 * (y + 0.044715f * y * y * y);
-    const float e = __builtin_amdgcn_exp2f(kl * u);
-    return y * __builtin_amdgcn_rcpf(1.0f + e);
-  }
-  if (act == 2) return y > 0.0f ? y : 0.0f;
-  return y;
-}
-
-__device__ __forceinline__ uint32_t bf16_bits(float v) {
-  __bf16 h = (__bf16)v;
-  return (uint32_t)__builtin_bit_cast(uint16_t, h);
-}
-__device__ __forceinline__ float bf16_round(float v) { return __uint_as_float(bf16_bits(v) << 16); }
 
 // Staging granule q = NT k + tid is granule q & 1 (16 bytes) of staged voxel
 // q >> 1; it goes to LDS byte (q >> 1) * VSTRIDE + 16 (q & 1).  The loads are
@@ -346,8 +329,9 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
             // stored to LDS at step 3k + 3, just before round k + 1 is loaded
             if (st >= 3 && st % 3 == 0 && st / 3 - 1 < RMAX) {
               // a tile's first chunk stages into the buffer the previous
-              // epilogue transposed through: wait for every wave to leave it
-              if (!HEAD && st == 3 && chunk == 0) __builtin_amdgcn_s_barrier();
+              // epilogue used (transposition or head partials): wait for
+              // every wave to leave it
+              if (st == 3 && chunk == 0) __builtin_amdgcn_s_barrier();
               *(lds_u32x4_w*)(oth + stage_slot((st / 3 - 1) * NT + tid)) = stg;
             }
             if (st % 3 == 0 && st / 3 < RMAX) {
@@ -382,42 +366,45 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
       // voxel rows, 8 rows per instruction.  The next tile's first staging
       // store waits at a barrier until every wave is done here.
       lds_char* const tb = lds + ((gchunk - 1) & 1) * ABUF + wave * (64 * 128);
+      with_activation(act, [&](auto A) {
+        constexpr int ACT = decltype(A)::value;
 #pragma unroll
-      for (int ps = 0; ps < MB / 2; ++ps) {
+        for (int ps = 0; ps < MB / 2; ++ps) {
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
+          for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int c = nb * 4 + q;  // 16-byte granule of the wave's 64 channels
-            const int co = wn * 64 + c * 8 + half * 4;
-            const float4 bv = {bias_s[co], bias_s[co + 1], bias_s[co + 2], bias_s[co + 3]};
+            for (int q = 0; q < 4; ++q) {
+              const int c = nb * 4 + q;  // 16-byte granule of the wave's 64 channels
+              const int co = wn * 64 + c * 8 + half * 4;
+              const float4 bv = {bias_s[co], bias_s[co + 1], bias_s[co + 2], bias_s[co + 3]};
 #pragma unroll
-            for (int m = 0; m < 2; ++m) {
-              const int mb = 2 * ps + m;
-              const float v0 = activation(acc[mb][nb][4 * q + 0] + bv.x, act);
-              const float v1 = activation(acc[mb][nb][4 * q + 1] + bv.y, act);
-              const float v2 = activation(acc[mb][nb][4 * q + 2] + bv.z, act);
-              const float v3 = activation(acc[mb][nb][4 * q + 3] + bv.w, act);
-              u32x2 packed;
-              packed.x = bf16_bits(v0) | (bf16_bits(v1) << 16);
-              packed.y = bf16_bits(v2) | (bf16_bits(v3) << 16);
-              const int r = m * 32 + l32;
-              *(lds_u32x2_w*)(tb + r * 128 + ((c ^ (r & 7)) << 4) + half * 8) = packed;
+              for (int m = 0; m < 2; ++m) {
+                const int mb = 2 * ps + m;
+                const float v0 = act_fn<ACT>(acc[mb][nb][4 * q + 0] + bv.x);
+                const float v1 = act_fn<ACT>(acc[mb][nb][4 * q + 1] + bv.y);
+                const float v2 = act_fn<ACT>(acc[mb][nb][4 * q + 2] + bv.z);
+                const float v3 = act_fn<ACT>(acc[mb][nb][4 * q + 3] + bv.w);
+                u32x2 packed;
+                packed.x = bf16_bits(v0) | (bf16_bits(v1) << 16);
+                packed.y = bf16_bits(v2) | (bf16_bits(v3) << 16);
+                const int r = m * 32 + l32;
+                *(lds_u32x2_w*)(tb + r * 128 + ((c ^ (r & 7)) << 4) + half * 8) = packed;
+              }
             }
-          }
-        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's rows are in LDS
-        __builtin_amdgcn_wave_barrier();
+          __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's rows are in LDS
+          __builtin_amdgcn_wave_barrier();
 #pragma unroll
-        for (int it2 = 0; it2 < 8; ++it2) {
-          const int gi = it2 * 64 + lane;
-          const int r = gi >> 3, c = gi & 7;
-          const u32x4 v = *(lds_u32x4*)(tb + r * 128 + ((c ^ (r & 7)) << 4));
-          const int pr = __shfl(pidx[2 * ps + (it2 >> 2)], r & 31);
-          if (pr >= 0) *reinterpret_cast<u32x4*>(y + (long long)pr * COUT + wn * 64 + c * 8) = v;
+          for (int it2 = 0; it2 < 8; ++it2) {
+            const int gi = it2 * 64 + lane;
+            const int r = gi >> 3, c = gi & 7;
+            const u32x4 v = *(lds_u32x4*)(tb + r * 128 + ((c ^ (r & 7)) << 4));
+            const int pr = __shfl(pidx[2 * ps + (it2 >> 2)], r & 31);
+            if (pr >= 0) *reinterpret_cast<u32x4*>(y + (long long)pr * COUT + wn * 64 + c * 8) = v;
+          }
+          __builtin_amdgcn_s_waitcnt(0xc07f);  // the reads are done before the next pass writes
+          __builtin_amdgcn_wave_barrier();
         }
-        __builtin_amdgcn_s_waitcnt(0xc07f);  // the reads are done before the next pass writes
-        __builtin_amdgcn_wave_barrier();
-      }
+      });
     } else {
       // 1x1x1 head on the bf16-rounded activations: partial sums over this
       // lane's channels, then over the half-waves, then over the channel
@@ -428,28 +415,31 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
       for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
         for (int o = 0; o < 4; ++o) part[mb][o] = 0.0f;
+      with_activation(act, [&](auto A) {
+        constexpr int ACT = decltype(A)::value;
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
+        for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int co = (wn * NB + nb) * 32 + q * 8 + half * 4;
-          const float4 bv = {bias_s[co], bias_s[co + 1], bias_s[co + 2], bias_s[co + 3]};
-          float4 hw[4];
-#pragma unroll
-          for (int o = 0; o < 4; ++o)
-            hw[o] = {headw_s[o * COUT + co], headw_s[o * COUT + co + 1], headw_s[o * COUT + co + 2],
-                     headw_s[o * COUT + co + 3]};
-#pragma unroll
-          for (int mb = 0; mb < MB; ++mb) {
-            const float a0 = bf16_round(activation(acc[mb][nb][4 * q + 0] + bv.x, act));
-            const float a1 = bf16_round(activation(acc[mb][nb][4 * q + 1] + bv.y, act));
-            const float a2 = bf16_round(activation(acc[mb][nb][4 * q + 2] + bv.z, act));
-            const float a3 = bf16_round(activation(acc[mb][nb][4 * q + 3] + bv.w, act));
+          for (int q = 0; q < 4; ++q) {
+            const int co = (wn * NB + nb) * 32 + q * 8 + half * 4;
+            const float4 bv = {bias_s[co], bias_s[co + 1], bias_s[co + 2], bias_s[co + 3]};
+            float4 hw[4];
 #pragma unroll
             for (int o = 0; o < 4; ++o)
-              part[mb][o] += hw[o].x * a0 + hw[o].y * a1 + hw[o].z * a2 + hw[o].w * a3;
+              hw[o] = {headw_s[o * COUT + co], headw_s[o * COUT + co + 1], headw_s[o * COUT + co + 2],
+                       headw_s[o * COUT + co + 3]};
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) {
+              const float a0 = bf16_round(act_fn<ACT>(acc[mb][nb][4 * q + 0] + bv.x));
+              const float a1 = bf16_round(act_fn<ACT>(acc[mb][nb][4 * q + 1] + bv.y));
+              const float a2 = bf16_round(act_fn<ACT>(acc[mb][nb][4 * q + 2] + bv.z));
+              const float a3 = bf16_round(act_fn<ACT>(acc[mb][nb][4 * q + 3] + bv.w));
+#pragma unroll
+              for (int o = 0; o < 4; ++o)
+                part[mb][o] += hw[o].x * a0 + hw[o].y * a1 + hw[o].z * a2 + hw[o].w * a3;
+            }
           }
-        }
+      });
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
@@ -470,9 +460,8 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
       static_assert(NT == kTileRows, "one thread per tile row");
       {
         const int r = tid;
-        long long p = -1, o2;
-        int lb;
-        if (tile_row(g, tl, tile, r, batch, &p, &lb, &o2)) {
+        int b, t, i, j;
+        if (tile_row_coords(g, tl, tile, r, batch, &b, &t, &i, &j)) {
           float lg[4] = {head_b[0], head_b[1], head_b[2], head_b[3]};
 #pragma unroll
           for (int w2 = 0; w2 < W::WN; ++w2) {
@@ -482,12 +471,6 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
             lg[2] += hp[2];
             lg[3] += hp[3];
           }
-          // padded index -> (b, t, i, j)
-          const int b = (int)(p / g.S);
-          const int rem = (int)(p - (long long)b * g.S);
-          const int t = rem / g.P - 1;
-          const int r2 = rem - (t + 1) * g.P;
-          const int i = r2 / g.Wp - 1, j = r2 - (i + 1) * g.Wp - 1;
           const int HH = g.H * g.H;
           const int s = i * g.H + j;
           const int n = comp_of_site[s];
@@ -504,9 +487,6 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
           }
         }
       }
-      // the partials' buffer is where the next tile's second chunk is staged
-      __builtin_amdgcn_s_waitcnt(0xc07f);
-      __builtin_amdgcn_s_barrier();
     }
     tile = next;
     cur_base = next_base;

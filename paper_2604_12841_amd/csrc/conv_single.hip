@@ -20,6 +20,7 @@
 // buffered: the next tile's planes are loaded into registers while this tile
 // computes.  Each lane gathers its B fragment (4 taps x 2 channels) from the
 // staged planes; taps on a flat tile's halo columns read as zero.
+#include "activation.h"
 #include "internal.h"
 #include "tiles.h"
 
@@ -62,23 +63,6 @@ struct Lds {
   static constexpr int total = part + Split<COUT>::WN * kTileRows * 4 * 4;
   static_assert(total <= 64 * 1024, "LDS budget");
 };
-
-__device__ __forceinline__ float activation(float y, int act) {
-  if (act == 1) {  // GELU, tanh form: 0.5 y (1 + tanh(u)) = y / (1 + exp(-2u))
-    const float k0 = 0.7978845608028654f;          // sqrt(2 / pi)
-    const float kl = -2.0f * 1.4426950408889634f;  // -2 log2(e)
-    const float u = k0 * (y + 0.044715f * y * y * y);
-    const float e = __builtin_amdgcn_exp2f(kl * u);
-    return y * __builtin_amdgcn_rcpf(1.0f + e);
-  }
-  if (act == 2) return y > 0.0f ? y : 0.0f;
-  return y;
-}
-
-__device__ __forceinline__ float bf16_round(float v) {
-  __bf16 h = (__bf16)v;
-  return __uint_as_float((uint32_t)__builtin_bit_cast(uint16_t, h) << 16);
-}
 
 // Both channels (4 bytes) of staged voxel NT k + tid (voxel 0, a zero halo
 // voxel, past the footprint).
@@ -203,25 +187,28 @@ __global__ void __launch_bounds__(NT) conv_single_kernel(Geom g, Tiling tl, int 
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
       for (int o = 0; o < 4; ++o) part[mb][o] = 0.0f;
+    with_activation(act, [&](auto A) {
+      constexpr int ACT = decltype(A)::value;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int co = wn * 32 + q * 8 + half * 4;
-      const float4 bv = {bias_s[co], bias_s[co + 1], bias_s[co + 2], bias_s[co + 3]};
-      float4 hw[4];
+      for (int q = 0; q < 4; ++q) {
+        const int co = wn * 32 + q * 8 + half * 4;
+        const float4 bv = {bias_s[co], bias_s[co + 1], bias_s[co + 2], bias_s[co + 3]};
+        float4 hw[4];
 #pragma unroll
-      for (int o = 0; o < 4; ++o)
-        hw[o] = {headw_s[o * COUT + co], headw_s[o * COUT + co + 1], headw_s[o * COUT + co + 2],
-                 headw_s[o * COUT + co + 3]};
+        for (int o = 0; o < 4; ++o)
+          hw[o] = {headw_s[o * COUT + co], headw_s[o * COUT + co + 1], headw_s[o * COUT + co + 2],
+                   headw_s[o * COUT + co + 3]};
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) {
-        const float a0 = bf16_round(activation(acc[mb][4 * q + 0] + bv.x, act));
-        const float a1 = bf16_round(activation(acc[mb][4 * q + 1] + bv.y, act));
-        const float a2 = bf16_round(activation(acc[mb][4 * q + 2] + bv.z, act));
-        const float a3 = bf16_round(activation(acc[mb][4 * q + 3] + bv.w, act));
+        for (int mb = 0; mb < MB; ++mb) {
+          const float a0 = bf16_round(act_fn<ACT>(acc[mb][4 * q + 0] + bv.x));
+          const float a1 = bf16_round(act_fn<ACT>(acc[mb][4 * q + 1] + bv.y));
+          const float a2 = bf16_round(act_fn<ACT>(acc[mb][4 * q + 2] + bv.z));
+          const float a3 = bf16_round(act_fn<ACT>(acc[mb][4 * q + 3] + bv.w));
 #pragma unroll
-        for (int o = 0; o < 4; ++o) part[mb][o] += hw[o].x * a0 + hw[o].y * a1 + hw[o].z * a2 + hw[o].w * a3;
+          for (int o = 0; o < 4; ++o) part[mb][o] += hw[o].x * a0 + hw[o].y * a1 + hw[o].z * a2 + hw[o].w * a3;
+        }
       }
-    }
+    });
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
@@ -241,9 +228,8 @@ __global__ void __launch_bounds__(NT) conv_single_kernel(Geom g, Tiling tl, int 
     // one thread per voxel row: logits, threshold, flip nibble
     if (tid < kTileRows) {
       const int r = tid;
-      long long p = -1, o2;
-      int lb;
-      if (tile_row(g, tl, tile, r, batch, &p, &lb, &o2)) {
+      int b, t, i, j;
+      if (tile_row_coords(g, tl, tile, r, batch, &b, &t, &i, &j)) {
         float lg[4] = {head_b[0], head_b[1], head_b[2], head_b[3]};
 #pragma unroll
         for (int w2 = 0; w2 < W::WN; ++w2) {
@@ -253,12 +239,6 @@ __global__ void __launch_bounds__(NT) conv_single_kernel(Geom g, Tiling tl, int 
           lg[2] += hp[2];
           lg[3] += hp[3];
         }
-        // padded index -> (b, t, i, j)
-        const int b = (int)(p / g.S);
-        const int rem = (int)(p - (long long)b * g.S);
-        const int t = rem / g.P - 1;
-        const int r2 = rem - (t + 1) * g.P;
-        const int i = r2 / g.Wp - 1, j = r2 - (i + 1) * g.Wp - 1;
         const int HH = g.H * g.H;
         const int s = i * g.H + j;
         const int n = comp_of_site[s];

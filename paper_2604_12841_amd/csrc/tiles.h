@@ -60,6 +60,34 @@ __host__ __device__ inline bool tile_row(const Geom& g, const Tiling& tl, int ti
   }
 }
 
+// Sample and grid coordinates (b, t, i, j) of row r of tile `tile`; false if
+// the row is outside the volume.  32-bit arithmetic (max_batch * V < 2^31).
+__host__ __device__ inline bool tile_row_coords(const Geom& g, const Tiling& tl, int tile, int r, int batch,
+                                                int* b, int* t, int* i, int* j) {
+  const int HH = g.H * g.H;
+  if (tl.mode == 0) {
+    const int seg = tile / tl.tiles_per_seg;
+    const int k0 = (tile - seg * tl.tiles_per_seg) * kTileRows;
+    const int u = seg * (int)tl.seg_len + k0 + r;
+    if (k0 + r >= tl.seg_len || u >= batch * g.V) return false;
+    *b = u / g.V;
+    const int v = u - *b * g.V;
+    *t = v / HH;
+    const int s = v - *t * HH;
+    *i = s / g.H;
+    *j = s - *i * g.H;
+    return true;
+  }
+  const int per = tl.ntT * tl.ntI * tl.ntJ;
+  *b = tile / per;
+  const int rem = tile - *b * per;
+  const int bij = tl.BI * tl.BJ;
+  *t = (rem / (tl.ntI * tl.ntJ)) * tl.BT + r / bij;
+  *i = ((rem / tl.ntJ) % tl.ntI) * tl.BI + (r / tl.BJ) % tl.BI;
+  *j = (rem % tl.ntJ) * tl.BJ + r % tl.BJ;
+  return r < tl.BT * bij && *t < g.T && *i < g.H && *j < g.H;
+}
+
 // Padded (t, i, j) of a box-mode tile's staging origin.
 struct BoxOrigin {
   int t0, i0, j0;
