@@ -13,13 +13,16 @@
 namespace pd {
 
 // Activation codes of the C ABI: 0 none, 1 GELU (tanh form), 2 ReLU.
+// GELU: 0.5 y (1 + tanh(u)) = y / (1 + exp(-2u)) with
+// u = sqrt(2/pi) (y + 0.044715 y^3), evaluated as
+// y / (1 + exp2(y (c1 + c3 y^2))), c1 = -2 log2(e) sqrt(2/pi),
+// c3 = 0.044715 c1 (three multiply-adds, one exp2, one reciprocal).
 template <int ACT>
 __device__ __forceinline__ float act_fn(float y) {
-  if constexpr (ACT == 1) {  // 0.5 y (1 + tanh(u)) = y / (1 + exp(-2u)), u = sqrt(2/pi) (y + 0.044715 y^3)
-    const float k0 = 0.7978845608028654f;          // sqrt(2 / pi)
-    const float kl = -2.0f * 1.4426950408889634f;  // -2 log2(e)
-    const float u = k0 * (y + 0.044715f * y * y * y);
-    const float e = __builtin_amdgcn_exp2f(kl * u);
+  if constexpr (ACT == 1) {
+    constexpr float c1 = -2.0 * 1.4426950408889634 * 0.7978845608028654;
+    constexpr float c3 = -2.0 * 1.4426950408889634 * 0.7978845608028654 * 0.044715;
+    const float e = __builtin_amdgcn_exp2f(y * __builtin_fmaf(c3, y * y, c1));
     return y * __builtin_amdgcn_rcpf(1.0f + e);
   } else if constexpr (ACT == 2) {
     return y > 0.0f ? y : 0.0f;
@@ -42,6 +45,15 @@ __host__ __device__ inline void with_activation(int act, F&& f) {
 __device__ __forceinline__ uint32_t bf16_bits(float v) {
   __bf16 h = (__bf16)v;
   return (uint32_t)__builtin_bit_cast(uint16_t, h);
+}
+
+// Two values rounded to bf16 and packed, lo in bits 0-15 (one conversion
+// instruction on gfx950).
+__device__ __forceinline__ uint32_t bf16_pack(float lo, float hi) {
+  typedef __attribute__((ext_vector_type(2))) float f32x2_t;
+  typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+  const f32x2_t f = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
 }
 
 __device__ __forceinline__ float bf16_round(float v) { return __uint_as_float(bf16_bits(v) << 16); }

@@ -127,8 +127,8 @@ __global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, const ui
           const float v2 = act_fn<ACT>(acc[nb][4 * q + 2] + bias[co + 2]);
           const float v3 = act_fn<ACT>(acc[nb][4 * q + 3] + bias[co + 3]);
           u32x2 packed;
-          packed.x = bf16_bits(v0) | (bf16_bits(v1) << 16);
-          packed.y = bf16_bits(v2) | (bf16_bits(v3) << 16);
+          packed.x = bf16_pack(v0, v1);
+          packed.y = bf16_pack(v2, v3);
           *(lds_u32x2_w*)(tile + l32 * OSTR + co * 2) = packed;
         }
     }

@@ -385,8 +385,8 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
                 const float v2 = act_fn<ACT>(acc[mb][nb][4 * q + 2] + bv.z);
                 const float v3 = act_fn<ACT>(acc[mb][nb][4 * q + 3] + bv.w);
                 u32x2 packed;
-                packed.x = bf16_bits(v0) | (bf16_bits(v1) << 16);
-                packed.y = bf16_bits(v2) | (bf16_bits(v3) << 16);
+                packed.x = bf16_pack(v0, v1);
+                packed.y = bf16_pack(v2, v3);
                 const int r = m * 32 + l32;
                 *(lds_u32x2_w*)(tb + r * 128 + ((c ^ (r & 7)) << 4) + half * 8) = packed;
               }
