@@ -71,15 +71,22 @@ constexpr int MAX_SPAN = BUF_VOX - 1;    // staged voxels per tile (the last slo
 // next to it): granules past the footprint load zeros into slots past the
 // footprint, and granules past the buffer all go to its last slot.
 constexpr int RMAX = 7;
-static_assert(RMAX * NT >= 2 * MAX_SPAN, "staging rounds cover the largest footprint");
+static_assert(RMAX * NT >= 2 * MAX_SPAN && (RMAX * NT) % 32 == 0, "staging rounds cover the largest footprint");
 static_assert(STEPS % BRING == 0, "the weight ring lines up with chunk boundaries");
 static_assert(RMAX * 3 + 3 <= STEPS, "staging rounds fit in a chunk");
 constexpr int ABUF = BUF_VOX * VSTRIDE;  // bytes per staging buffer
 
-// LDS byte (relative to a staging buffer) of staging granule q.
+// Staging granule q = NT k + tid: in each run of 32, the first 16 take
+// granule 0 of 16 consecutive staged voxels and the next 16 their granule 1,
+// so the 16 lanes of an LDS write cycle hit 16 distinct bank groups.
+__host__ __device__ inline int stage_voxel(int q) { return ((q >> 5) << 4) | (q & 15); }
+__host__ __device__ inline int stage_gran(int q) { return (q >> 4) & 1; }
+
+// LDS byte (relative to a staging buffer) of staging granule q; voxels past
+// the buffer all go to its last slot.
 __host__ __device__ inline int stage_slot(int q) {
-  const int c = q < 2 * BUF_VOX - 1 ? q : 2 * BUF_VOX - 1;
-  return (c >> 1) * VSTRIDE + (c & 1) * 16;
+  const int v = stage_voxel(q);
+  return (v < BUF_VOX - 1 ? v : BUF_VOX - 1) * VSTRIDE + stage_gran(q) * 16;
 }
 
 // Wave split of the 256 x COUT output tile: WN waves across the channels
@@ -112,8 +119,8 @@ struct Lds {
   static_assert(Split<COUT>::MB % 2 == 0, "the epilogue transposes row blocks in pairs");
 };
 
-// Staging granule q = NT k + tid is granule q & 1 (16 bytes) of staged voxel
-// q >> 1; it goes to LDS byte (q >> 1) * VSTRIDE + 16 (q & 1).  The loads are
+// Staging granule q = NT k + tid is granule stage_gran(q) (16 bytes) of
+// staged voxel stage_voxel(q), bound for LDS byte stage_slot(q).  The loads are
 // buffer loads relative to the tile's staging base (a padded voxel index no
 // larger than any voxel the tile stages): per round, a lane's byte offset is
 // the same for every chunk of the tile.  Granules past the footprint, and
@@ -143,10 +150,11 @@ __host__ __device__ inline long long stage_base(const Geom& g, const StageSrc& s
 
 template <int CIN, int MODE>
 __host__ __device__ inline uint32_t stage_offset(const Geom& g, const Tiling& tl, const StageSrc& src,
-                                                 long long base, long long limit, int ngran, int k, int tid) {
+                                                 long long base, long long limit, int span, int k, int tid) {
   const int q = k * NT + tid;
-  const long long gv = staged_voxel_fast<MODE>(g, tl, src, q >> 1, limit);
-  return (q < ngran && gv >= 0) ? (uint32_t)((gv - base) * (CIN * 2) + (q & 1) * 16) : kNoVoxel;
+  const int vv = stage_voxel(q);
+  const long long gv = staged_voxel_fast<MODE>(g, tl, src, vv, limit);
+  return (vv < span && gv >= 0) ? (uint32_t)((gv - base) * (CIN * 2) + stage_gran(q) * 16) : kNoVoxel;
 }
 
 // Buffer resource over the activations from padded voxel `base`, channel
@@ -177,7 +185,6 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
   const int half = lane >> 5, l32 = lane & 31;
   const int ntiles = (int)tl.ntiles;
   const long long limit = (long long)batch * g.S;
-  const int ngran = tl.span * 2;  // 16-byte granules of a staged chunk
 
   lds_char* const lds = (lds_char*)smem;
   lds_char* const zero = lds + L::zero;
@@ -205,7 +212,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
   {
     const StageSrc src = source_of(tile);
 #pragma unroll
-    for (int k = 0; k < RMAX; ++k) soff[k] = stage_offset<CIN, MODE>(g, tl, src, cur_base, limit, ngran, k, tid);
+    for (int k = 0; k < RMAX; ++k) soff[k] = stage_offset<CIN, MODE>(g, tl, src, cur_base, limit, tl.span, k, tid);
   }
 
   // First tile: stage its first chunk synchronously.
@@ -269,7 +276,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
       // the chunk staged next: the following chunk of this tile, else the
       // first chunk of the next tile, else nothing
       const bool more = chunk + 1 < NCHUNK;
-      const int sgran = (more || next >= 0) ? ngran : 0;
+      const int sspan = (more || next >= 0) ? tl.span : 0;  // staged voxels of the chunk staged next
       // the next tile's offsets replace soff round by round during the
       // last chunk (past the last tile: none, every granule empty)
       const __amdgpu_buffer_rsrc_t srs =
@@ -336,7 +343,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
             }
             if (st % 3 == 0 && st / 3 < RMAX) {
               const int k = st / 3;
-              if (!more) soff[k] = stage_offset<CIN, MODE>(g, tl, next_src, next_base, limit, sgran, k, tid);
+              if (!more) soff[k] = stage_offset<CIN, MODE>(g, tl, next_src, next_base, limit, sspan, k, tid);
               stg = __builtin_amdgcn_raw_buffer_load_b128(srs, soff[k], 0, 0);
             }
           }
