@@ -6,7 +6,10 @@ package; the two share no code.
 
 The arithmetic lives in ``oracle.c`` (plain C, fp64); this module builds it
 with gcc on first use, loads it with ctypes and marshals numpy arrays.
-Array layouts are channel-major per sample: planes/logits [B][C][T][d+1][d+1].
+Array layouts are channel-major per sample: planes/logits [B][C][T][H][H],
+H = d + 1 on the plaquette grid or H = d in the paper's own layout
+(``layout="paper"``: four input channels on the D x D data-qubit grid,
+Sec. IV.B.1).
 """
 import ctypes
 import os
@@ -60,6 +63,14 @@ def _load():
         lib.oracle_flips_residual.restype = None
         lib.oracle_residual_from_flips.argtypes = [i32, i32, i32, vp, vp, vp]
         lib.oracle_residual_from_flips.restype = None
+        lib.oracle_stabilizer_qubit.argtypes = [i32, i32, i32, vp, vp]
+        lib.oracle_stabilizer_qubit.restype = i32
+        lib.oracle_unpack_paper.argtypes = [i32, i32, i32, vp, i32, i32, vp]
+        lib.oracle_unpack_paper.restype = None
+        lib.oracle_forward_grid.argtypes = [i32, i32, i32, vp, i32, vp, vp, i32, vp]
+        lib.oracle_forward_grid.restype = None
+        lib.oracle_flips_residual_paper.argtypes = [i32, i32, i32, vp, vp, vp, vp]
+        lib.oracle_flips_residual_paper.restype = None
         _lib = lib
     return _lib
 
@@ -127,7 +138,7 @@ def weight_count(layers):
     return int(_load().oracle_weight_count(len(layers), _ptr(spec)))
 
 
-def forward(d, T, planes, layers, weights, bf16):
+def forward(d, T, planes, layers, weights, bf16, layout="plaquette"):
     """Network forward.  planes [B][c_in][T][H][H] float64; layers: list of
     (c_in, c_out, k, act); weights: flat fp32.  Returns logits
     [B][c_out_last][T][H][H] float64 (fp32-valued in bf16 mode)."""
@@ -137,12 +148,47 @@ def forward(d, T, planes, layers, weights, bf16):
     if weights.size != weight_count(layers):
         raise ValueError("weight count mismatch")
     B = planes.shape[0]
-    H = d + 1
+    H = d if layout == "paper" else d + 1
+    if planes.shape[1:] != (layers[0][0], T, H, H):
+        raise ValueError("planes shape mismatch")
     co = layers[-1][1]
     out = np.zeros((B, co, T, H, H), dtype=np.float64)
-    _load().oracle_forward(d, T, B, _ptr(planes), len(layers), _ptr(spec), _ptr(weights),
-                           1 if bf16 else 0, _ptr(out))
+    _load().oracle_forward_grid(H, T, B, _ptr(planes), len(layers), _ptr(spec), _ptr(weights),
+                                1 if bf16 else 0, _ptr(out))
     return out
+
+
+BOUNDARY = {None: 0, "none": 0, "Z": 1, "X": 2}
+
+
+def stabilizer_qubit(d, i, j):
+    """(kind, r, c): the data qubit the stabilizer at plaquette (i, j) is drawn
+    onto in the paper's layout (kind 1 X, 2 Z; (0, -1, -1) for no stabilizer)."""
+    r, c = np.zeros(1, np.int32), np.zeros(1, np.int32)
+    kind = _load().oracle_stabilizer_qubit(d, i, j, _ptr(r), _ptr(c))
+    return (int(kind), int(r[0]), int(c[0])) if kind else (0, -1, -1)
+
+
+def unpack_paper(d, T, det, first=None, last=None):
+    """Packed detectors -> planes [B][4][T][d][d] of the paper's layout
+    (x_type, z_type, x_present, z_present); first / last: basis ("Z", "X" or
+    None) of the preparation before round 0 / the measurement after round T-1."""
+    det = np.ascontiguousarray(det, dtype=np.uint64)
+    B = det.shape[0]
+    out = np.zeros((B, 4, T, d, d), dtype=np.float64)
+    _load().oracle_unpack_paper(d, T, B, _ptr(det), BOUNDARY[first], BOUNDARY[last], _ptr(out))
+    return out
+
+
+def flips_residual_paper(d, T, logits, det):
+    """logits [B][4][T][d][d] of the paper's layout + packed det -> (packed flips, packed residual)."""
+    logits = np.ascontiguousarray(logits, dtype=np.float64)
+    det = np.ascontiguousarray(det, dtype=np.uint64)
+    B = logits.shape[0]
+    flips = np.zeros((B, flip_words(d, T)), dtype=np.uint64)
+    res = np.zeros((B, det_words(d, T)), dtype=np.uint64)
+    _load().oracle_flips_residual_paper(d, T, B, _ptr(logits), _ptr(det), _ptr(flips), _ptr(res))
+    return flips, res
 
 
 def flips_residual(d, T, logits, det):
@@ -172,8 +218,12 @@ def num_threads():
     return int(lib.oracle_num_threads())
 
 
-def run(d, T, det, layers, weights, bf16):
+def run(d, T, det, layers, weights, bf16, layout="plaquette", first=None, last=None):
     """The whole path: (logits, flips, residual)."""
-    logits = forward(d, T, unpack(d, T, det), layers, weights, bf16)
-    flips, res = flips_residual(d, T, logits, det)
+    if layout == "paper":
+        logits = forward(d, T, unpack_paper(d, T, det, first, last), layers, weights, bf16, layout)
+        flips, res = flips_residual_paper(d, T, logits, det)
+    else:
+        logits = forward(d, T, unpack(d, T, det), layers, weights, bf16)
+        flips, res = flips_residual(d, T, logits, det)
     return logits, flips, res

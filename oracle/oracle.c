@@ -26,7 +26,9 @@
  * fp64, so the only difference from an exact sum is fp64 rounding.
  *
  * Array layout is channel-major per sample (like PyTorch NCDHW):
- * x[b][c][t][i][j] with i, j in [0, d] on the (d+1) x (d+1) plaquette grid.
+ * x[b][c][t][i][j] with i, j in [0, d] on the (d+1) x (d+1) plaquette grid,
+ * or, in the paper's own layout (Sec. IV.B.1), i, j in [0, d-1] on the D x D
+ * data-qubit grid (D = d) with four input channels.
  */
 #include <math.h>
 #include <omp.h>
@@ -118,6 +120,73 @@ void oracle_unpack(int d, int T, int B, const uint64_t* det, double* planes) {
 }
 
 /* ---------------------------------------------------------------------- */
+/* The paper's own layout (Sec. IV.B.1, Fig. StabMap, Eqs. encTrainX1-4):  */
+/* the grid is the D x D array of data qubits (D = d) and every stabilizer */
+/* is drawn onto one data qubit of its support: a weight-four X (Z)        */
+/* stabilizer onto its top-left (top-right) qubit, a weight-two X          */
+/* stabilizer onto its top qubit and a weight-two Z stabilizer onto its    */
+/* right qubit.                                                             */
+/* ---------------------------------------------------------------------- */
+
+/* Data qubit (r, c) of plaquette (i, j) under that drawing; returns 0 when
+ * (i, j) holds no stabilizer.  "Top" is the smaller row, "left" the smaller
+ * column. */
+int oracle_stabilizer_qubit(int d, int i, int j, int* r, int* c) {
+  int kind = oracle_site_kind(d, i, j);
+  if (kind == 0) return 0;
+  int rc[8];
+  int n = oracle_plaquette_support(d, i, j, rc);
+  /* the support in row-major order: rc[0..1] is the top-left qubit of a
+   * weight-four plaquette and the top (left) qubit of a vertical (horizontal)
+   * weight-two one */
+  if (kind == 1) {
+    *r = rc[0];
+    *c = rc[1];
+  } else {
+    /* top-right of four; of a horizontal pair (same row), the right one */
+    *r = rc[0];
+    *c = (n == 4) ? rc[3] : rc[2 * (n - 1) + 1];
+  }
+  return kind;
+}
+
+/* Planes of the paper's layout: [B][4][T][d][d], channels
+ *   0 x_type: X-type detector event of round t at its stabilizer's qubit,
+ *   1 z_type: the same for Z-type,
+ *   2 x_present: weight / 4 of the X stabilizer drawn at the qubit,
+ *   3 z_present: the same for Z (Eqs. encTrainX1-encTrainX4),
+ * and 0 wherever no stabilizer is drawn.  first / last (0 none, 1 Z, 2 X) is
+ * the basis the qubit is prepared in before round 0 / measured in after round
+ * T-1: preparing |0> (Z) or measuring Z clears x_present in that round,
+ * preparing |+> (X) or measuring X clears z_present. */
+void oracle_unpack_paper(int d, int T, int B, const uint64_t* det, int first, int last, double* planes) {
+  int H = d + 1, S = d * d - 1;
+  int64_t W = oracle_det_words(d, T);
+  int64_t V = (int64_t)T * d * d;
+  int* site_of = (int*)malloc(sizeof(int) * S);
+  int* index_of = (int*)malloc(sizeof(int) * H * H);
+  oracle_stabilizer_order(d, site_of, index_of);
+  memset(planes, 0, sizeof(double) * (size_t)B * 4 * V);
+  for (int b = 0; b < B; ++b)
+    for (int t = 0; t < T; ++t)
+      for (int i = 0; i <= d; ++i)
+        for (int j = 0; j <= d; ++j) {
+          int r, c, rc[8];
+          int kind = oracle_stabilizer_qubit(d, i, j, &r, &c);
+          if (kind == 0) continue;
+          int n = index_of[i * H + j];
+          double weight = (double)oracle_plaquette_support(d, i, j, rc) / 4.0;
+          int cleared = (t == 0 && first == kind) || (t == T - 1 && last == kind);
+          int64_t at = (int64_t)t * d * d + r * d + c;
+          double* pb = planes + (int64_t)b * 4 * V;
+          pb[(kind - 1) * V + at] = (double)get_bit(det + (int64_t)b * W, (int64_t)t * S + n);
+          pb[(kind + 1) * V + at] = cleared ? 0.0 : weight;
+        }
+  free(site_of);
+  free(index_of);
+}
+
+/* ---------------------------------------------------------------------- */
 /* Number formats and the activation                                       */
 /* ---------------------------------------------------------------------- */
 
@@ -167,7 +236,7 @@ int64_t oracle_weight_count(int n_layers, const int* spec) {
 /* Forward pass of the fully convolutional network (Sec. IV.B).           */
 /*   y[co][t][i][j] = b[co] + sum_{ci,kt,ki,kj} w[co][ci][kt][ki][kj] *    */
 /*                    x[ci][t+kt-p][i+ki-p][j+kj-p],  p = (k-1)/2,          */
-/* with x = 0 outside [0,T) x [0,d] x [0,d]; hidden layers apply their     */
+/* with x = 0 outside [0,T) x [0,H) x [0,H); hidden layers apply their     */
 /* activation, the last layer is linear (it gives the logits).              */
 /* spec: n_layers x {c_in, c_out, k, act}.  weights: fp32, per layer        */
 /* w[c_out][c_in][k][k][k] then b[c_out].  planes: [B][c_in0][T][H][H].     */
@@ -176,9 +245,8 @@ int64_t oracle_weight_count(int n_layers, const int* spec) {
 /* Samples and output channels are independent; they are spread over       */
 /* OpenMP threads (the arithmetic of each output is unchanged).             */
 /* ---------------------------------------------------------------------- */
-void oracle_forward(int d, int T, int B, const double* planes, int n_layers, const int* spec,
-                    const float* weights, int bf16, double* logits) {
-  int H = d + 1;
+void oracle_forward_grid(int H, int T, int B, const double* planes, int n_layers, const int* spec,
+                         const float* weights, int bf16, double* logits) {
   int64_t V = (int64_t)T * H * H;
   int cmax = spec[0];
   for (int l = 0; l < n_layers; ++l)
@@ -269,6 +337,12 @@ void oracle_forward(int d, int T, int B, const double* planes, int n_layers, con
   free(xb);
 }
 
+/* The same on the (d+1) x (d+1) plaquette grid. */
+void oracle_forward(int d, int T, int B, const double* planes, int n_layers, const int* spec,
+                    const float* weights, int bf16, double* logits) {
+  oracle_forward_grid(d + 1, T, B, planes, n_layers, spec, weights, bf16, logits);
+}
+
 /* ---------------------------------------------------------------------- */
 /* Corrections and residual (Sec. IV.B.6).                                */
 /* ---------------------------------------------------------------------- */
@@ -345,6 +419,51 @@ void oracle_flips_residual(int d, int T, int B, const double* logits, const uint
         int s = site_of[n];
         int ch = (n < K) ? 2 : 3;
         set_bit(fr, base + 2 * d * d + n, f[((int64_t)ch * T + t) * H * H + s]);
+      }
+    }
+    residual_one(d, T, det + (int64_t)b * Wd, f, f + V, f + 2 * V, f + 3 * V,
+                 residual + (int64_t)b * Wd);
+  }
+  free(f);
+  free(site_of);
+  free(index_of);
+}
+
+/* The paper's layout: logits [B][4][T][d][d].  Channels 0/1 are the Z / X
+ * data corrections of qubit (r, c) (Eqs. ZcorreJK, XcorreJK); channel 2 (3) at
+ * the qubit an X (Z) stabilizer is drawn onto is that stabilizer's
+ * measurement correction (Eqs. SynXCorrJK, SynZCorrJK).  Flips are packed as
+ * in oracle_flips_residual and the residual is the same function of them. */
+void oracle_flips_residual_paper(int d, int T, int B, const double* logits, const uint64_t* det,
+                                 uint64_t* flips, uint64_t* residual) {
+  int H = d + 1, S = d * d - 1;
+  int64_t V = (int64_t)T * H * H, VD = (int64_t)T * d * d;
+  int64_t Wd = oracle_det_words(d, T), Wf = oracle_flip_words(d, T);
+  int* site_of = (int*)malloc(sizeof(int) * S);
+  int* index_of = (int*)malloc(sizeof(int) * H * H);
+  oracle_stabilizer_order(d, site_of, index_of);
+  uint8_t* f = (uint8_t*)malloc(4 * V); /* on the plaquette grid, as residual_one reads them */
+  for (int b = 0; b < B; ++b) {
+    const double* lg = logits + (int64_t)b * 4 * VD;
+    memset(f, 0, 4 * V);
+    uint64_t* fr = flips + (int64_t)b * Wf;
+    memset(fr, 0, sizeof(uint64_t) * Wf);
+    for (int t = 0; t < T; ++t) {
+      int64_t base = (int64_t)t * (3 * d * d - 1);
+      for (int r = 0; r < d; ++r)
+        for (int c = 0; c < d; ++c)
+          for (int ch = 0; ch < 2; ++ch) {
+            int v = lg[ch * VD + (int64_t)t * d * d + r * d + c] > 0.0;
+            f[ch * V + ((int64_t)t * H + r) * H + c] = (uint8_t)v;
+            set_bit(fr, base + ch * d * d + r * d + c, v);
+          }
+      for (int n = 0; n < S; ++n) {
+        int s = site_of[n], i = s / H, j = s % H, r, c;
+        int kind = oracle_stabilizer_qubit(d, i, j, &r, &c);
+        int ch = kind + 1; /* 2 for X, 3 for Z */
+        int v = lg[ch * VD + (int64_t)t * d * d + r * d + c] > 0.0;
+        f[ch * V + (int64_t)t * H * H + s] = (uint8_t)v;
+        set_bit(fr, base + 2 * d * d + n, v);
       }
     }
     residual_one(d, T, det + (int64_t)b * Wd, f, f + V, f + 2 * V, f + 3 * V,

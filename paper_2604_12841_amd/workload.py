@@ -49,6 +49,33 @@ def layer_spec(n_hidden, width, act=GELU_TANH, c_in=2, c_out=4):
     return layers
 
 
+# The models of Table models (Sec. VI) in the paper's own layout: four input
+# channels (x_type, z_type, x_present, z_present on the D x D grid), the
+# listed filters and kernel sizes per conv layer, the last layer (4 filters)
+# without activation.
+PAPER_MODELS = {
+    1: ([128, 128, 128, 4], [3, 3, 3, 3]),
+    2: ([256, 256, 256, 4], [3, 3, 3, 3]),
+    3: ([128, 128, 128, 4], [5, 5, 5, 5]),
+    4: ([128, 128, 128, 128, 128, 4], [3, 3, 3, 3, 3, 3]),
+    5: ([256, 256, 256, 256, 256, 4], [3, 3, 3, 3, 3, 3]),
+}
+
+
+def paper_model_layers(model, act=GELU_TANH):
+    filters, kernels = PAPER_MODELS[model]
+    return paper_layer_spec(filters, kernels, act)
+
+
+def paper_layer_spec(filters, kernels, act=GELU_TANH, c_in=4):
+    layers = []
+    ci = c_in
+    for n, (co, k) in enumerate(zip(filters, kernels)):
+        layers.append((ci, co, k, NONE if n == len(filters) - 1 else act))
+        ci = co
+    return layers
+
+
 def config_layers(cfg_id, act=GELU_TANH):
     c = CONFIGS[cfg_id]
     return layer_spec(c["n_hidden"], c["width"], act)
