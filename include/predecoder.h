@@ -42,12 +42,31 @@
  *   R_Z[t](s) = D_Z[t](s) ^ m_Z[t](s) ^ m_Z[t-1](s) ^ XOR_{q in supp(s)} x_corr[t](q)
  * applied at every round 0 <= t < T (including the last one).
  *
+ * Input layouts (pd_options.layout):
+ *   PD_LAYOUT_PLAQUETTE (default): the (d+1) x (d+1) plaquette grid above,
+ *     two channels (X-type, Z-type detector events at their stabilizer
+ *     sites, zero elsewhere).
+ *   PD_LAYOUT_PAPER: the paper's own encoding (Sec. IV.B.1, Fig. StabMap,
+ *     Eqs. encTrainX1-encTrainX4): the D x D grid of data qubits (D = d), every
+ *     stabilizer drawn onto one qubit of its support -- a weight-four X (Z)
+ *     stabilizer onto its top-left (top-right) qubit, a weight-two X
+ *     stabilizer (left / right edge) onto its upper qubit, a weight-two Z
+ *     stabilizer (top / bottom edge) onto its right qubit -- and four
+ *     channels: x_type, z_type (the detector events of the stabilizer drawn
+ *     at the qubit), x_present, z_present (its weight / 4, i.e. 1 or 0.5).
+ *     pd_options.first_round / last_round name the basis the logical qubit
+ *     is prepared in before round 0 / measured in after round T-1: Z clears
+ *     x_present in that round, X clears z_present, PD_BOUNDARY_NONE neither
+ *     (a block in the middle of a stream).  The output channels are read at
+ *     the same positions: channels 0/1 at every qubit, channel 2 (3) at the
+ *     qubit an X (Z) stabilizer is drawn onto.  Logits are [4][T][d][d].
+ *
  * Network.  A list of conv3d layers (stride 1, no dilation, zero padding
  * (k-1)/2, cross-correlation as in PyTorch Conv3d):
- *   layers[0].c_in == 2  (channel 0: X-type detectors, channel 1: Z-type,
- *                         placed at their stabilizer sites, zero elsewhere)
+ *   layers[0].c_in == 2 (plaquette layout) or 4 (paper layout)
  *   layers[l].c_in == layers[l-1].c_out
- *   layers[n-1]: the head, c_out == 4, act == PD_ACT_NONE.
+ *   layers[n-1]: the output layer, c_out == 4, act == PD_ACT_NONE: a 1x1x1
+ *                head, or (paper layout) a 3x3x3 layer as in Table models.
  * Hidden layers apply their activation; GELU is the tanh form
  * 0.5 y (1 + tanh(sqrt(2/pi) (y + 0.044715 y^3))) (Table hyperparameters).
  * Weights are host fp32, layer after layer, each as w[c_out][c_in][kt][ki][kj]
@@ -59,8 +78,9 @@
  * end.  flip = (logit > 0); a logit of exactly 0 is no flip.
  *
  * Supported shapes (others give PD_ERR_UNSUPPORTED): 3 <= d <= 63,
- * 1 <= T <= 1023; hidden layers k == 3; head k == 1.  BF16: hidden widths
- * 64 or 128.  FP32: hidden widths 8 .. 128, multiples of 8.
+ * 1 <= T <= 1023; hidden layers k == 3; output layer k == 1, or k == 3 on
+ * the paper layout.  BF16: hidden widths 64 or 128.  FP32 (plaquette layout
+ * only): hidden widths 8 .. 128, multiples of 8.
  *
  * Errors.  Every function is nothrow and never aborts.  Host-checkable misuse
  * gives PD_ERR_INVALID_ARG before any device call; a failed HIP call or
@@ -98,6 +118,19 @@ typedef enum pd_act { PD_ACT_NONE = 0, PD_ACT_GELU_TANH = 1, PD_ACT_RELU = 2 } p
 
 typedef enum pd_dtype { PD_DTYPE_FP32 = 0, PD_DTYPE_BF16 = 1 } pd_dtype;
 
+typedef enum pd_layout { PD_LAYOUT_PLAQUETTE = 0, PD_LAYOUT_PAPER = 1 } pd_layout;
+
+/* Basis of the logical preparation / final measurement next to a block. */
+typedef enum pd_boundary { PD_BOUNDARY_NONE = 0, PD_BOUNDARY_Z = 1, PD_BOUNDARY_X = 2 } pd_boundary;
+
+/* Options of predecoder_create_ex (see "Input layouts" above).  first_round
+ * and last_round must be PD_BOUNDARY_NONE on the plaquette layout. */
+typedef struct pd_options {
+  int32_t layout;      /* pd_layout */
+  int32_t first_round; /* pd_boundary: basis prepared before round 0 */
+  int32_t last_round;  /* pd_boundary: basis measured after round T-1 */
+} pd_options;
+
 /* One conv3d layer: k x k x k kernel, c_in -> c_out, activation act. */
 typedef struct pd_layer {
   int32_t c_in;
@@ -120,14 +153,23 @@ pd_status predecoder_create(const float* weights, size_t n_weights, int32_t d, i
                             const pd_layer* layers, int32_t n_layers, int32_t dtype,
                             int32_t max_batch, pd_predecoder** out);
 
+/* predecoder_create with options (opts NULL = plaquette layout, no boundary
+ * rounds): the input layout of Sec. IV.B.1 and the bases of the preparation
+ * and final measurement.  Invalid option values give PD_ERR_INVALID_ARG; the
+ * paper layout with PD_DTYPE_FP32 gives PD_ERR_UNSUPPORTED. */
+pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d, int32_t T,
+                               const pd_layer* layers, int32_t n_layers, int32_t dtype,
+                               int32_t max_batch, const pd_options* opts, pd_predecoder** out);
+
 /* The whole hot path for `batch` independent volumes (Sec. IV.B.6):
  * unpack -> conv layers (+bias, activation) -> head -> threshold ->
  * residual and bit repack.
  * det:      device, [batch][W_det] uint64, packed detectors (read only).
  * flips:    device, [batch][W_flip] uint64, packed thresholded corrections.
  * residual: device, [batch][W_det] uint64, packed residual syndrome.
- * logits:   device or NULL; if given, [batch][4][T][d+1][d+1] fp32 head
- *           outputs at every grid site (channel order as in `flips`).
+ * logits:   device or NULL; if given, [batch][4][T][H][H] fp32 outputs of
+ *           the last layer at every grid site (channel order as in `flips`;
+ *           H = d + 1 on the plaquette layout, d on the paper layout).
  * 1 <= batch <= max_batch.  Asynchronous on hip_stream. */
 pd_status predecoder_run(pd_predecoder* h, void* hip_stream, const uint64_t* det, int32_t batch,
                          uint64_t* flips, uint64_t* residual, float* logits);
@@ -138,10 +180,11 @@ pd_status predecoder_run(pd_predecoder* h, void* hip_stream, const uint64_t* det
 pd_status predecoder_residual(pd_predecoder* h, void* hip_stream, const uint64_t* det,
                               const uint64_t* flips, int32_t batch, uint64_t* residual);
 
-/* The unpack stage alone (Sec. IV.B.1, Eqs. encTrainX1/2: detector events
- * placed at their stabilizer sites, 0 elsewhere): det [batch][W_det] ->
- * planes, device, [batch][T][d+1][d+1][2] in the handle's dtype (bf16 bit
- * patterns as uint16 for PD_DTYPE_BF16, fp32 for PD_DTYPE_FP32).
+/* The unpack stage alone (Sec. IV.B.1, Eqs. encTrainX1-4: the input planes
+ * of the handle's layout): det [batch][W_det] -> planes, device,
+ * [batch][T][H][H][c_in] (c_in = 2 on the plaquette layout, 4 on the paper
+ * layout) in the handle's dtype (bf16 bit patterns as uint16 for
+ * PD_DTYPE_BF16, fp32 for PD_DTYPE_FP32).
  * Asynchronous on hip_stream. */
 pd_status predecoder_unpack(pd_predecoder* h, void* hip_stream, const uint64_t* det,
                             int32_t batch, void* planes);

@@ -12,18 +12,23 @@ memory and streams); streams are passed as their raw hipStream_t handles.
 import ctypes
 import os
 
-__all__ = ["Predecoder", "PredecoderError", "lib", "det_words", "flip_words", "weight_count",
+__all__ = ["Predecoder", "PredecoderError", "Options", "lib", "det_words", "flip_words", "weight_count",
            "status_string", "ACT_NONE", "ACT_GELU_TANH", "ACT_RELU", "DTYPE_FP32", "DTYPE_BF16",
-           "LIB_PATH", "EXPORTS"]
+           "LAYOUT_PLAQUETTE", "LAYOUT_PAPER", "BOUNDARY_NONE", "BOUNDARY_Z", "BOUNDARY_X", "LIB_PATH",
+           "EXPORTS"]
 
 ACT_NONE, ACT_GELU_TANH, ACT_RELU = 0, 1, 2
 DTYPE_FP32, DTYPE_BF16 = 0, 1
+LAYOUT_PLAQUETTE, LAYOUT_PAPER = 0, 1
+BOUNDARY_NONE, BOUNDARY_Z, BOUNDARY_X = 0, 1, 2
+_LAYOUTS = {"plaquette": LAYOUT_PLAQUETTE, "paper": LAYOUT_PAPER}
+_BOUNDARIES = {None: BOUNDARY_NONE, "none": BOUNDARY_NONE, "Z": BOUNDARY_Z, "X": BOUNDARY_X}
 PD_OK, PD_ERR_INVALID_ARG, PD_ERR_UNSUPPORTED, PD_ERR_OUT_OF_MEMORY, PD_ERR_DEVICE = range(5)
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpredecoder.so")
 
 # Every symbol declared in include/predecoder.h.
-EXPORTS = ("predecoder_create", "predecoder_run", "predecoder_residual", "predecoder_unpack",
+EXPORTS = ("predecoder_create", "predecoder_create_ex", "predecoder_run", "predecoder_residual", "predecoder_unpack",
            "predecoder_num_stages", "predecoder_stage_times", "predecoder_destroy",
            "predecoder_status_string", "predecoder_det_words", "predecoder_flip_words",
            "predecoder_weight_count")
@@ -40,6 +45,10 @@ class Layer(ctypes.Structure):
                 ("act", ctypes.c_int32)]
 
 
+class Options(ctypes.Structure):
+    _fields_ = [("layout", ctypes.c_int32), ("first_round", ctypes.c_int32), ("last_round", ctypes.c_int32)]
+
+
 _lib = None
 
 
@@ -54,6 +63,9 @@ def lib():
         LP = ctypes.POINTER(Layer)
         L.predecoder_create.argtypes = [vp, sz, i32, i32, LP, i32, i32, i32, ctypes.POINTER(vp)]
         L.predecoder_create.restype = i32
+        L.predecoder_create_ex.argtypes = [vp, sz, i32, i32, LP, i32, i32, i32, ctypes.POINTER(Options),
+                                           ctypes.POINTER(vp)]
+        L.predecoder_create_ex.restype = i32
         L.predecoder_run.argtypes = [vp, vp, vp, i32, vp, vp, vp]
         L.predecoder_run.restype = i32
         L.predecoder_residual.argtypes = [vp, vp, vp, vp, i32, vp]
@@ -120,16 +132,23 @@ def _stream(stream):
 class Predecoder:
     """One pre-decoder handle: weights, workspace and tables for (d, T, max_batch)."""
 
-    def __init__(self, weights, d, T, layers, dtype="bf16", max_batch=1):
+    def __init__(self, weights, d, T, layers, dtype="bf16", max_batch=1, layout="plaquette", first=None,
+                 last=None):
+        """layout: "plaquette" or "paper" (Sec. IV.B.1); first / last: basis ("Z", "X" or None) of the
+        preparation before round 0 / the measurement after round T-1 (paper layout)."""
         import numpy as np
         w = np.ascontiguousarray(np.asarray(weights, dtype=np.float32))
         self.d, self.T, self.layers, self.max_batch = d, T, [tuple(l) for l in layers], max_batch
         self.dtype = DTYPE_BF16 if dtype in ("bf16", DTYPE_BF16) else DTYPE_FP32
+        self.layout = _LAYOUTS[layout] if isinstance(layout, str) else int(layout)
+        self.grid = d if self.layout == LAYOUT_PAPER else d + 1
         self.det_words = det_words(d, T)
         self.flip_words = flip_words(d, T)
+        opts = Options(self.layout, _BOUNDARIES[first] if not isinstance(first, int) else first,
+                       _BOUNDARIES[last] if not isinstance(last, int) else last)
         h = ctypes.c_void_p()
-        st = lib().predecoder_create(w.ctypes.data_as(ctypes.c_void_p), w.size, d, T, _layers(layers),
-                                     len(layers), self.dtype, max_batch, ctypes.byref(h))
+        st = lib().predecoder_create_ex(w.ctypes.data_as(ctypes.c_void_p), w.size, d, T, _layers(layers),
+                                        len(layers), self.dtype, max_batch, ctypes.byref(opts), ctypes.byref(h))
         if st != PD_OK:
             raise PredecoderError(st, "predecoder_create")
         self._h = h

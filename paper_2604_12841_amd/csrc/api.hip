@@ -21,7 +21,7 @@ using pd::Geom;
 using pd::Tiling;
 
 struct pd_predecoder {
-  Geom g;
+  Geom g;                        // includes the layout and the boundary bases
   int dtype = 0;
   int max_batch = 0;
   int device = 0;
@@ -44,9 +44,9 @@ namespace {
 const int kMaxD = 63;
 const int kMaxT = 1023;
 
-bool layer_chain_ok(const pd_layer* l, int n) {
+bool layer_chain_ok(const pd_layer* l, int n, int layout) {
   if (n < 1) return false;
-  if (l[0].c_in != 2) return false;
+  if (l[0].c_in != (layout == PD_LAYOUT_PAPER ? 4 : 2)) return false;
   if (l[n - 1].c_out != 4) return false;
   if (l[n - 1].act != PD_ACT_NONE) return false;
   for (int i = 0; i < n; ++i) {
@@ -58,12 +58,16 @@ bool layer_chain_ok(const pd_layer* l, int n) {
   return true;
 }
 
-Geom make_geom(int d, int T) {
+Geom make_geom(int d, int T, int layout = PD_LAYOUT_PLAQUETTE, int first = PD_BOUNDARY_NONE,
+               int last = PD_BOUNDARY_NONE) {
   Geom g;
   g.d = d;
   g.T = T;
-  g.H = d + 1;
-  g.Wp = d + 3;
+  g.layout = layout;
+  g.first = first;
+  g.last = last;
+  g.H = layout == PD_LAYOUT_PAPER ? d : d + 1;  // the data qubits, or the plaquettes
+  g.Wp = g.H + 2;
   g.P = g.Wp * g.Wp;
   g.S = (long long)(T + 2) * g.P;
   g.V = T * g.H * g.H;
@@ -75,34 +79,45 @@ Geom make_geom(int d, int T) {
   return g;
 }
 
-// GPU-side geometry tables (see internal.h).  X site <=> (i+j) even and
-// 1 <= i <= d-1; Z site <=> (i+j) odd and 1 <= j <= d-1; plaquette (i, j)
-// acts on the data qubits (i-1..i, j-1..j) inside [0, d-1]^2.
+// GPU-side geometry tables (see internal.h).  Plaquette (i, j), 0 <= i, j <=
+// d, holds an X stabilizer iff (i+j) is even and 1 <= i <= d-1, a Z
+// stabilizer iff (i+j) is odd and 1 <= j <= d-1, and acts on the data qubits
+// (i-1..i, j-1..j) inside [0, d-1]^2.  In the paper's layout (Sec. IV.B.1,
+// Fig. StabMap) a stabilizer's events enter, and its measurement flip is read,
+// at one qubit of its support: a weight-four X (Z) stabilizer at its top-left
+// (top-right) qubit, a weight-two X stabilizer (on the left / right edge) at
+// its upper qubit, a weight-two Z stabilizer (top / bottom edge) at its right
+// qubit.
 std::vector<int32_t> build_tables(const Geom& g) {
   std::vector<int32_t> t(pd::tables_size(g), -1);
   int32_t* site_of = t.data() + pd::tables_site_of(g);
-  int32_t* comp = t.data() + pd::tables_comp_of_site(g);
+  int32_t* comp_x = t.data() + pd::tables_comp_x(g);
+  int32_t* comp_z = t.data() + pd::tables_comp_z(g);
   int32_t* supp = t.data() + pd::tables_supp(g);
   const int d = g.d, H = g.H;
+  const bool paper = g.layout == PD_LAYOUT_PAPER;
   int n = 0;
   for (int pass = 0; pass < 2; ++pass)
     for (int i = 0; i <= d; ++i)
       for (int j = 0; j <= d; ++j) {
-        bool x = ((i + j) & 1) == 0 && i >= 1 && i <= d - 1;
-        bool z = ((i + j) & 1) == 1 && j >= 1 && j <= d - 1;
-        if ((pass == 0 && x) || (pass == 1 && z)) {
-          site_of[n] = i * H + j;
-          comp[i * H + j] = n;
-          ++n;
+        const bool x = ((i + j) & 1) == 0 && i >= 1 && i <= d - 1;
+        const bool z = ((i + j) & 1) == 1 && j >= 1 && j <= d - 1;
+        if (!((pass == 0 && x) || (pass == 1 && z))) continue;
+        int q = 0;
+        for (int r = i - 1; r <= i; ++r)
+          for (int c = j - 1; c <= j; ++c)
+            if (r >= 0 && r < d && c >= 0 && c < d) supp[n * 4 + q++] = r * H + c;
+        int site = i * H + j;
+        if (paper) {
+          if (x)  // top-left of four; upper qubit of an edge pair (column 0 or d-1)
+            site = (i - 1) * H + (j == 0 ? 0 : (j == d ? d - 1 : j - 1));
+          else  // top-right of four; right qubit of an edge pair (row 0 or d-1)
+            site = (i == 0 ? 0 : (i == d ? d - 1 : i - 1)) * H + j;
         }
+        site_of[n] = site;
+        (x ? comp_x : comp_z)[site] = n;
+        ++n;
       }
-  for (int i = 0; i <= d; ++i)
-    for (int j = 0; j <= d; ++j) {
-      int q = 0;
-      for (int r = i - 1; r <= i; ++r)
-        for (int c = j - 1; c <= j; ++c)
-          if (r >= 0 && r < d && c >= 0 && c < d) supp[(i * H + j) * 4 + q++] = r * H + c;
-    }
   return t;
 }
 
@@ -226,6 +241,7 @@ void tiling_for_batch(Tiling* t, const Geom& g, int batch) {
 bool supported(const Geom& g, const pd_layer* l, int n, int dtype) {
   if (g.d > kMaxD || g.T > kMaxT) return false;
   if (n < 2) return false;  // at least one hidden 3x3x3 layer before the head
+  if (g.layout == PD_LAYOUT_PAPER && dtype != PD_DTYPE_BF16) return false;
   for (int i = 0; i < n - 1; ++i) {
     if (l[i].k != 3) return false;
     int co = l[i].c_out;
@@ -235,8 +251,10 @@ bool supported(const Geom& g, const pd_layer* l, int n, int dtype) {
       if (co % 8 != 0 || co > 128) return false;
     }
   }
-  if (l[n - 1].k != 1 || l[n - 1].c_in > 128) return false;
-  if (dtype == PD_DTYPE_BF16 && (l[n - 1].c_in % 8) != 0) return false;
+  const pd_layer& out = l[n - 1];
+  if (out.k == 3) return g.layout == PD_LAYOUT_PAPER;  // a 3x3x3 output layer (c_in 64 or 128, checked above)
+  if (out.k != 1 || out.c_in > 128) return false;
+  if (dtype == PD_DTYPE_BF16 && (out.c_in % 8) != 0) return false;
   return true;
 }
 
@@ -287,22 +305,26 @@ void free_all(pd_predecoder* h) {
 
 // bf16 A fragments (weights) for v_mfma_f32_32x32x16_bf16: lane l of
 // fragment (k-step, channel block nb) holds W[co = 32 nb + l % 32][k0 + 8 (l / 32) + e],
-// e = 0..7.  Layer 1 (c_in = 2): k = 2 * tap + ci over 4 k-steps (taps >= 27
-// are zero).  Hidden layers: [chunk of 16 c_in][tap][nb] with
-// ci = 16 chunk + 8 (l / 32) + e.
+// e = 0..7; output channels past c_out (the 4 filters of an output layer fill
+// one block of 32) are zero.  Layer 1 (c_in = 2 or 4): k = c_in * tap + ci over
+// ceil(27 c_in / 16) k-steps (taps >= 27 are zero).  Other layers: [chunk of
+// 16 c_in][tap][nb] with ci = 16 chunk + 8 (l / 32) + e.
 std::vector<uint16_t> conv_fragments(const float* w, int cin, int cout) {
-  const int nbt = cout / 32;
+  const int nbt = cout < 32 ? 1 : cout / 32;
   std::vector<uint16_t> f;
-  auto W = [&](int co, int ci, int tap) { return w[((size_t)co * cin + ci) * 27 + tap]; };
-  if (cin == 2) {
-    f.assign((size_t)4 * nbt * 64 * 8, 0);
-    for (int ks = 0; ks < 4; ++ks)
+  auto W = [&](int co, int ci, int tap) -> uint16_t {
+    return co < cout ? bf16_bits(w[((size_t)co * cin + ci) * 27 + tap]) : 0;
+  };
+  if (cin == 2 || cin == 4) {
+    const int ks_n = (27 * cin + 15) / 16;
+    f.assign((size_t)ks_n * nbt * 64 * 8, 0);
+    for (int ks = 0; ks < ks_n; ++ks)
       for (int nb = 0; nb < nbt; ++nb)
         for (int l = 0; l < 64; ++l)
           for (int e = 0; e < 8; ++e) {
             int k = ks * 16 + 8 * (l / 32) + e;
-            int tap = k / 2, ci = k % 2, co = nb * 32 + l % 32;
-            f[(((size_t)ks * nbt + nb) * 64 + l) * 8 + e] = tap < 27 ? bf16_bits(W(co, ci, tap)) : 0;
+            int tap = k / cin, ci = k % cin, co = nb * 32 + l % 32;
+            f[(((size_t)ks * nbt + nb) * 64 + l) * 8 + e] = tap < 27 ? W(co, ci, tap) : 0;
           }
   } else {
     const int nch = cin / 16;
@@ -314,7 +336,7 @@ std::vector<uint16_t> conv_fragments(const float* w, int cin, int cout) {
             for (int e = 0; e < 8; ++e) {
               int ci = c * 16 + 8 * (l / 32) + e, co = nb * 32 + l % 32;
               size_t idx = ((((size_t)c * 27 + tap) * nbt + nb) * 64 + l) * 8 + e;
-              f[idx] = bf16_bits(W(co, ci, tap));
+              f[idx] = W(co, ci, tap);
             }
   }
   return f;
@@ -335,6 +357,10 @@ pd_status enqueue_run(pd_predecoder* h, hipStream_t st, const uint64_t* det, int
   const Geom& g = h->g;
   const int fp32 = h->dtype == PD_DTYPE_FP32;
   const int n = (int)h->layers.size();
+  // the last layer: a 1x1x1 head (fused into the last hidden layer's
+  // epilogue on the bf16 path) or a 3x3x3 output layer of its own
+  const bool out3 = h->layers[n - 1].k == 3;
+  const int hidden_wgs = h->n_cu * pd::conv_hidden_workgroups_per_cu();
   int e = 0;
   auto mark = [&]() -> pd_status {
     if (ev && hipEventRecord(ev[e++], st) != hipSuccess) return PD_ERR_DEVICE;
@@ -342,39 +368,47 @@ pd_status enqueue_run(pd_predecoder* h, hipStream_t st, const uint64_t* det, int
   };
   pd_status s;
   if ((s = mark()) != PD_OK) return s;
-  s = check_launch(pd::launch_unpack(g, h->tables + pd::tables_comp_of_site(g), det, batch, h->planes, 1,
-                                     fp32, st));
+  s = check_launch(pd::launch_unpack(g, h->tables, det, batch, h->planes, 1, fp32, st));
   if (s != PD_OK) return s;
   const void* x = h->planes;
   Tiling tl = h->tiling;
   if (!fp32) tiling_for_batch(&tl, g, batch);
+  bool head_done = false;  // nibbles written by a fused head
   for (int l = 0; l < n - 1; ++l) {
     if ((s = mark()) != PD_OK) return s;
     void* y = h->act[l & 1];
     const pd_layer& L = h->layers[l];
-    if (fp32)
+    const bool fuse_head = !fp32 && !out3 && l == n - 2;
+    if (fp32) {
       s = check_launch(pd::launch_conv_fp32(g, L.c_in, L.c_out, L.act, (const float*)x, (float*)y,
                                             (const float*)h->wdev[l], h->bdev[l], batch, st));
-    else if (l == 0 && n - 2 > 0)  // first layer, not also the last hidden one
-      s = check_launch(pd::launch_conv_first(g, L.c_out, L.act, x, y, h->wdev[l], h->bdev[l], batch, st));
-    else if (l == 0)  // a single hidden layer: layer 1 carries the head
+    } else if (l == 0 && fuse_head && L.c_in == 2) {  // one hidden layer: layer 1 carries the head
       s = check_launch(pd::launch_conv_single(g, tl, L.c_out, L.act, x, h->wdev[l], h->bdev[l], h->head_w,
-                                              h->head_b, h->tables + pd::tables_comp_of_site(g), h->nib, logits,
-                                              batch, h->n_cu, st));
-    else  // the last hidden layer carries the head and the threshold in its epilogue
+                                              h->head_b, h->tables, h->nib, logits, batch, h->n_cu, st));
+      head_done = true;
+    } else if (l == 0) {
+      s = check_launch(pd::launch_conv_first(g, L.c_in, L.c_out, L.act, x, y, h->wdev[l], h->bdev[l], batch,
+                                             st));
+    } else {  // the last hidden layer may carry the head and the threshold in its epilogue
       s = check_launch(pd::launch_conv_hidden(g, tl, L.c_in, L.c_out, L.act, x, y, h->wdev[l], h->bdev[l],
-                                              l == n - 2, h->head_w, h->head_b,
-                                              h->tables + pd::tables_comp_of_site(g), h->nib, logits, batch,
-                                              h->n_cu * pd::conv_hidden_workgroups_per_cu(), st));
+                                              fuse_head ? 1 : 0, h->head_w, h->head_b, h->tables, h->nib,
+                                              logits, batch, hidden_wgs, st));
+      head_done = fuse_head;
+    }
     if (s != PD_OK) return s;
     x = y;
   }
   if ((s = mark()) != PD_OK) return s;
-  if (fp32) {
+  if (out3) {
+    const pd_layer& L = h->layers[n - 1];
+    s = check_launch(pd::launch_conv_hidden(g, tl, L.c_in, L.c_out, L.act, x, nullptr, h->wdev[n - 1],
+                                            h->bdev[n - 1], 2, nullptr, nullptr, h->tables, h->nib, logits,
+                                            batch, hidden_wgs, st));
+  } else if (!head_done) {  // fp32, or a one-hidden-layer network on the paper's layout
     s = check_launch(pd::launch_head(g, h->layers[n - 1].c_in, fp32, x, h->head_w, h->head_b, h->tables,
                                      h->nib, logits, batch, st));
-    if (s != PD_OK) return s;
   }
+  if (s != PD_OK) return s;
   if ((s = mark()) != PD_OK) return s;
   s = check_launch(pd::launch_residual_pack(g, h->tables, det, h->nib, flips, residual, batch, st));
   if (s != PD_OK) return s;
@@ -425,15 +459,29 @@ int32_t predecoder_num_stages(const pd_predecoder* h) {
 pd_status predecoder_create(const float* weights, size_t n_weights, int32_t d, int32_t T,
                             const pd_layer* layers, int32_t n_layers, int32_t dtype, int32_t max_batch,
                             pd_predecoder** out) {
+  return predecoder_create_ex(weights, n_weights, d, T, layers, n_layers, dtype, max_batch, nullptr, out);
+}
+
+pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d, int32_t T,
+                               const pd_layer* layers, int32_t n_layers, int32_t dtype, int32_t max_batch,
+                               const pd_options* opts, pd_predecoder** out) {
   if (!out) return PD_ERR_INVALID_ARG;
   *out = nullptr;
   if (!weights || !layers) return PD_ERR_INVALID_ARG;
   if (d < 3 || (d % 2) == 0 || T < 1) return PD_ERR_INVALID_ARG;
   if (dtype != PD_DTYPE_FP32 && dtype != PD_DTYPE_BF16) return PD_ERR_INVALID_ARG;
   if (max_batch < 1) return PD_ERR_INVALID_ARG;
-  if (!layer_chain_ok(layers, n_layers)) return PD_ERR_INVALID_ARG;
+  const pd_options o = opts ? *opts : pd_options{PD_LAYOUT_PLAQUETTE, PD_BOUNDARY_NONE, PD_BOUNDARY_NONE};
+  if (o.layout != PD_LAYOUT_PLAQUETTE && o.layout != PD_LAYOUT_PAPER) return PD_ERR_INVALID_ARG;
+  if (o.first_round < PD_BOUNDARY_NONE || o.first_round > PD_BOUNDARY_X || o.last_round < PD_BOUNDARY_NONE ||
+      o.last_round > PD_BOUNDARY_X)
+    return PD_ERR_INVALID_ARG;
+  // the plaquette layout has no geometric channels to clear
+  if (o.layout == PD_LAYOUT_PLAQUETTE && (o.first_round != PD_BOUNDARY_NONE || o.last_round != PD_BOUNDARY_NONE))
+    return PD_ERR_INVALID_ARG;
+  if (!layer_chain_ok(layers, n_layers, o.layout)) return PD_ERR_INVALID_ARG;
   if (n_weights != predecoder_weight_count(layers, n_layers)) return PD_ERR_INVALID_ARG;
-  Geom g = make_geom(d, T);
+  Geom g = make_geom(d, T, o.layout, o.first_round, o.last_round);
   if (!supported(g, layers, n_layers, dtype)) return PD_ERR_UNSUPPORTED;
   // kernels index voxels of a batch with 32-bit integers
   if ((long long)max_batch * g.V >= (1ll << 31) || (long long)max_batch * (g.Wd + g.Wf) >= (1ll << 31) ||
@@ -478,13 +526,14 @@ pd_status predecoder_create(const float* weights, size_t n_weights, int32_t d, i
     delete h;
     return st;
   };
-  if ((s = dev_alloc(&h->planes, vox * 2 * elem)) != PD_OK) return fail(s);
+  const size_t cin0 = (size_t)layers[0].c_in;
+  if ((s = dev_alloc(&h->planes, vox * cin0 * elem)) != PD_OK) return fail(s);
   if ((s = dev_alloc(&h->act[0], vox * cmax * elem)) != PD_OK) return fail(s);
   if ((s = dev_alloc(&h->act[1], vox * cmax * elem)) != PD_OK) return fail(s);
   if ((s = dev_alloc(&h->nib, (size_t)max_batch * g.V)) != PD_OK) return fail(s);
   std::vector<int32_t> tab = build_tables(g);
   if ((s = upload(&h->tables, tab.data(), tab.size() * sizeof(int32_t))) != PD_OK) return fail(s);
-  if (hipMemset(h->planes, 0, vox * 2 * elem) != hipSuccess ||
+  if (hipMemset(h->planes, 0, vox * cin0 * elem) != hipSuccess ||
       hipMemset(h->act[0], 0, vox * cmax * elem) != hipSuccess ||
       hipMemset(h->act[1], 0, vox * cmax * elem) != hipSuccess)
     return fail(PD_ERR_DEVICE);
@@ -496,6 +545,20 @@ pd_status predecoder_create(const float* weights, size_t n_weights, int32_t d, i
     const float* w = src;
     const float* b = src + nw;
     src += nw + L.c_out;
+    if (i == n_layers - 1 && L.k == 3) {  // a 3x3x3 output layer: 4 filters padded to one block of 32
+      std::vector<uint16_t> f = conv_fragments(w, L.c_in, L.c_out);
+      void* wd = nullptr;
+      s = upload(&wd, f.data(), f.size() * 2);
+      h->wdev.push_back(wd);
+      if (s != PD_OK) return fail(s);
+      std::vector<float> bp(32, 0.0f);
+      for (int o2 = 0; o2 < L.c_out; ++o2) bp[o2] = b[o2];
+      float* bd = nullptr;
+      s = upload(&bd, bp.data(), bp.size() * 4);
+      h->bdev.push_back(bd);
+      if (s != PD_OK) return fail(s);
+      break;
+    }
     if (i == n_layers - 1) {
       std::vector<float> hw((size_t)4 * L.c_in);
       for (int o = 0; o < 4; ++o)
@@ -550,7 +613,7 @@ pd_status predecoder_unpack(pd_predecoder* h, void* hip_stream, const uint64_t* 
                             void* planes) {
   if (!h || !det || !planes) return PD_ERR_INVALID_ARG;
   if (batch < 1 || batch > h->max_batch) return PD_ERR_INVALID_ARG;
-  return check_launch(pd::launch_unpack(h->g, h->tables + pd::tables_comp_of_site(h->g), det, batch, planes, 0,
+  return check_launch(pd::launch_unpack(h->g, h->tables, det, batch, planes, 0,
                                         h->dtype == PD_DTYPE_FP32, (hipStream_t)hip_stream));
 }
 

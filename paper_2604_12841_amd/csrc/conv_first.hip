@@ -1,17 +1,18 @@
 // conv_first.hip -- K2: the first 3x3x3 conv3d layer (Sec. IV.B, Fig.
-// ConvArch; c_in = 2 detector-event channels -> c_out = 64 or 128) with the
-// bias + activation + bf16 epilogue fused in, when it is not also the last
-// hidden layer.
+// ConvArch; c_in = 2 detector-event channels on the plaquette grid, or the 4
+// channels of the paper's layout, -> c_out = 64 or 128) with the bias +
+// activation + bf16 epilogue fused in, when it is not also the last hidden
+// layer.
 //
-// K = 27 taps x 2 channels is tiny (padded to 64 = 4 MFMA k-steps), so the
-// layer is bound by its epilogue (one activation per output value) and its
-// output write, not by the matrix cores.  It streams: each wave takes a few
-// blocks of 32 consecutive interior voxels x all c_out channels.
-//   * B operand (16 k x 32 voxels): lane l gathers, for voxel l % 32, taps
-//     ks*8 + 4*(l/32) + q (q = 0..3) as one 4-byte load each (the two bf16
-//     channels of a plane voxel) straight from the zero-halo planes, which
-//     stay in L2; taps past 26 contribute zero.
-//   * A operand: the layer's weight fragments (4 k-steps x c_out/32 blocks,
+// K = 27 taps x c_in channels is tiny (padded to 4 or 7 MFMA k-steps of 16),
+// so the layer is bound by its epilogue (one activation per output value)
+// and its output write, not by the matrix cores.  It streams: each wave takes
+// a few blocks of 32 consecutive interior voxels x all c_out channels.
+//   * B operand (16 k x 32 voxels, k = c_in tap + channel): lane l gathers,
+//     for voxel l % 32, the 8 / c_in taps of its half of the k-step, each as
+//     one load of all c_in bf16 channels of a plane voxel, straight from the
+//     zero-halo planes, which stay in L2; taps past 26 contribute zero.
+//   * A operand: the layer's weight fragments (k-steps x c_out/32 blocks,
 //     16 bytes per lane each), staged in LDS once per workgroup.
 //   * Epilogue: + bias, activation, bf16; the wave transposes its 32 x c_out
 //     tile through its own LDS slice and writes whole voxel rows with
@@ -50,27 +51,39 @@ __device__ __forceinline__ long long voxel_padded(const Geom& g, const Decode& d
   return padded_index(g, b, t, i, s - i * g.H);
 }
 
-// B fragments for this lane's voxel (padded index p): taps ks*8 + 4*half + q.
-__device__ __forceinline__ void gather(const Geom& g, const uint32_t* __restrict__ planes, long long p, bool valid,
-                                       int half, u32x4 (&bx)[4]) {
+// k-steps of 16 covering K = 27 c_in.
+template <int CIN>
+constexpr int ksteps() {
+  return (27 * CIN + 15) / 16;
+}
+
+// B fragments for this lane's voxel (padded index p): k = 16 ks + 8 half + e,
+// i.e. taps (16 ks + 8 half) / CIN + q, q < 8 / CIN, all CIN channels each.
+template <int CIN>
+__device__ __forceinline__ void gather(const Geom& g, const void* __restrict__ planes, long long p, bool valid,
+                                       int half, u32x4 (&bx)[ksteps<CIN>()]) {
+  constexpr int TPF = 8 / CIN;  // taps per lane per k-step
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks)
+  for (int ks = 0; ks < ksteps<CIN>(); ++ks)
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int tap = ks * 8 + half * 4 + q;  // >= 27 only for ks = 3
-      uint32_t val = 0;
-      if (valid && tap < 27) {
-        const int dt = tap / 9, di = (tap / 3) % 3, dj = tap % 3;
-        val = planes[p + (long long)(dt - 1) * g.P + (long long)(di - 1) * g.Wp + (dj - 1)];
+    for (int q = 0; q < TPF; ++q) {
+      const int tap = (16 * ks + 8 * half) / CIN + q;  // >= 27 only in the last k-step
+      const long long at = p + (long long)(tap / 9 - 1) * g.P + (long long)((tap / 3) % 3 - 1) * g.Wp + (tap % 3 - 1);
+      const bool in = valid && tap < 27;
+      if constexpr (CIN == 2) {
+        bx[ks][q] = in ? reinterpret_cast<const uint32_t*>(planes)[at] : 0u;
+      } else {
+        const u32x2 v = in ? reinterpret_cast<const u32x2*>(planes)[at] : u32x2{0u, 0u};
+        bx[ks][2 * q] = v.x;
+        bx[ks][2 * q + 1] = v.y;
       }
-      bx[ks][q] = val;
     }
 }
 
 // Each workgroup stages the weight fragments in LDS once; each of its waves
 // then handles BPW consecutive 32-voxel blocks.
-template <int COUT, int ACT>
-__global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, const uint32_t* __restrict__ planes,
+template <int CIN, int COUT, int ACT>
+__global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, const void* __restrict__ planes,
                                                                 uint16_t* __restrict__ y,
                                                                 const u32x4* __restrict__ wfrag,
                                                                 const float* __restrict__ bias, Decode dc,
@@ -78,7 +91,8 @@ __global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, const ui
   constexpr int NB = COUT / 32;
   constexpr int OSTR = COUT * 2 + 16;  // padded LDS row stride (bytes)
   constexpr int GPR = COUT / 8;        // 16-byte granules per voxel row
-  constexpr int WFR = 4 * NB * 64;     // weight fragments x lanes (16 bytes each)
+  constexpr int KS = ksteps<CIN>();
+  constexpr int WFR = KS * NB * 64;    // weight fragments x lanes (16 bytes each)
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, l32 = lane & 31;
@@ -94,8 +108,8 @@ __global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, const ui
     if (u0 >= nvox) break;
     const bool valid = u0 + l32 < nvox;
     const long long p = valid ? voxel_padded(g, dc, u0 + l32) : -1;
-    u32x4 bx[4];
-    gather(g, planes, p, valid, half, bx);
+    u32x4 bx[KS];
+    gather<CIN>(g, planes, p, valid, half, bx);
     if (half == 0) ((__attribute__((address_space(3))) int*)prow)[l32] = (int)p;
     // channel halves of 64 (NH blocks of 32) one after the other: fewer
     // live accumulators, more waves per SIMD to hide the gathers
@@ -108,7 +122,7 @@ __global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, const ui
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[nb][v] = 0.0f;
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks)
+      for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
         for (int nb = 0; nb < NH; ++nb) {
           const u32x4 wf = *(const lds_u32x4*)(smem + ((ks * NB + h0 + nb) * 64 + lane) * 16);
@@ -150,26 +164,30 @@ __global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, const ui
 
 }  // namespace
 
-hipError_t launch_conv_first(const Geom& g, int cout, int act, const void* planes, void* y, const void* wfrag,
-                             const float* bias, int batch, hipStream_t stream) {
+hipError_t launch_conv_first(const Geom& g, int cin, int cout, int act, const void* planes, void* y,
+                             const void* wfrag, const float* bias, int batch, hipStream_t stream) {
   const long long nvox = (long long)batch * g.V;  // < 2^31 (host check)
   const long long nblk = (nvox + 32 * WAVES * BPW - 1) / (32 * WAVES * BPW);
   Decode dc;
   dc.by_v = make_fastdiv((uint32_t)g.V);
   dc.by_hh = make_fastdiv((uint32_t)(g.H * g.H));
   dc.by_h = make_fastdiv((uint32_t)g.H);
-  auto launch = [&](auto CO, auto A) {
-    constexpr int C = decltype(CO)::value;
-    const size_t lds = (size_t)4 * (C / 32) * 64 * 16 + (size_t)WAVES * 32 * (C * 2 + 16 + 4);
-    hipLaunchKernelGGL((conv_first_kernel<C, decltype(A)::value>), dim3((unsigned)nblk), dim3(64 * WAVES), lds,
-                       stream, g, (const uint32_t*)planes, (uint16_t*)y, (const u32x4*)wfrag, bias, dc, (int)nvox);
+  auto launch = [&](auto CI, auto CO, auto A) {
+    constexpr int C = decltype(CO)::value, I = decltype(CI)::value;
+    const size_t lds = (size_t)ksteps<I>() * (C / 32) * 64 * 16 + (size_t)WAVES * 32 * (C * 2 + 16 + 4);
+    hipLaunchKernelGGL((conv_first_kernel<I, C, decltype(A)::value>), dim3((unsigned)nblk), dim3(64 * WAVES), lds,
+                       stream, g, planes, (uint16_t*)y, (const u32x4*)wfrag, bias, dc, (int)nvox);
   };
-  if ((cout != 64 && cout != 128) || act < 0 || act > 2) return hipErrorInvalidValue;
+  if ((cin != 2 && cin != 4) || (cout != 64 && cout != 128) || act < 0 || act > 2) return hipErrorInvalidValue;
   with_activation(act, [&](auto A) {
-    if (cout == 64)
-      launch(std::integral_constant<int, 64>(), A);
-    else
-      launch(std::integral_constant<int, 128>(), A);
+    using I2 = std::integral_constant<int, 2>;
+    using I4 = std::integral_constant<int, 4>;
+    using C64 = std::integral_constant<int, 64>;
+    using C128 = std::integral_constant<int, 128>;
+    if (cin == 2 && cout == 64) launch(I2(), C64(), A);
+    if (cin == 2 && cout == 128) launch(I2(), C128(), A);
+    if (cin == 4 && cout == 64) launch(I4(), C64(), A);
+    if (cin == 4 && cout == 128) launch(I4(), C128(), A);
   });
   return hipGetLastError();
 }

@@ -89,17 +89,23 @@ __host__ __device__ inline int stage_slot(int q) {
   return (v < BUF_VOX - 1 ? v : BUF_VOX - 1) * VSTRIDE + stage_gran(q) * 16;
 }
 
+// Epilogue modes: the activations of a hidden layer, a hidden layer with the
+// 1x1x1 head fused in, or the 3x3x3 output layer itself (4 filters, padded to
+// one block of 32 MFMA rows).
+enum Epi { EPI_ACT = 0, EPI_HEAD = 1, EPI_OUT = 2 };
+
 // Wave split of the 256 x COUT output tile: WN waves across the channels
-// (64 each, NB = 2 blocks of 32), WM across the voxels (ROWS each, MB blocks
-// of 32).
+// (NB blocks of 32 each: 2, or 1 for the 32-row output layer), WM across the
+// voxels (ROWS each, MB blocks of 32).
 template <int COUT>
 struct Split {
-  static constexpr int NB = 2;
-  static constexpr int WN = COUT / 64;
+  static constexpr int NB = COUT >= 64 ? 2 : 1;
+  static constexpr int WN = COUT / (32 * NB);
   static constexpr int WM = (NT / 64) / WN;
   static constexpr int ROWS = kTileRows / WM;
   static constexpr int MB = ROWS / 32;
   static_assert(WM * WN * 64 == NT && WN * NB * 32 == COUT && WM * MB * 32 == kTileRows, "wave split");
+  static_assert(MB % 2 == 0, "the epilogue transposes row blocks in pairs");
 };
 
 // LDS layout of one workgroup (byte offsets): two staging buffers, a
@@ -114,9 +120,8 @@ struct Lds {
   static constexpr int total = headw + 4 * COUT * 4;
   static_assert(zero % 256 == 0, "zero region must be 256-aligned");
   static_assert(2 * total <= 160 * 1024, "two workgroups per CU");
-  static_assert((COUT / 64) * kTileRows * 4 * 4 <= ABUF, "head partials fit a staging buffer");
+  static_assert(Split<COUT>::WN * kTileRows * 4 * 4 <= ABUF, "head partials fit a staging buffer");
   static_assert((NT / 64) * 64 * 128 <= ABUF, "epilogue transposition slices fit a staging buffer");
-  static_assert(Split<COUT>::MB % 2 == 0, "the epilogue transposes row blocks in pairs");
 };
 
 // Staging granule q = NT k + tid is granule stage_gran(q) (16 bytes) of
@@ -164,12 +169,12 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t stage_rsrc(const uint16_t* x, 
   return __builtin_amdgcn_make_buffer_rsrc((void*)(x + base * CIN + ch), 0, kStageRange, 0x00020000);
 }
 
-template <int CIN, int COUT, bool HEAD, int MODE>
+template <int CIN, int COUT, int EPI, int MODE>
 __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, uint16_t* __restrict__ y,
                    const u32x4* __restrict__ wfrag, const float* __restrict__ bias,
                    const float* __restrict__ head_w, const float* __restrict__ head_b,
-                   const int32_t* __restrict__ comp_of_site, uint8_t* __restrict__ nib,
+                   const int32_t* __restrict__ tables, uint8_t* __restrict__ nib,
                    float* __restrict__ logits, int batch) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   using W = Split<COUT>;
@@ -193,7 +198,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
   for (int e = tid; e < COUT; e += NT) bias_s[e] = bias[e];
   if (tid < 64) ((lds_u32_w*)zero)[tid] = 0u;
   const uint32_t zero_addr = (uint32_t)(uintptr_t)zero;
-  if (HEAD)
+  if (EPI == EPI_HEAD)
     for (int e = tid; e < 4 * COUT; e += NT) headw_s[e] = head_w[e];
 
   int tile = tile_of(blockIdx.x, gridDim.x, 0, ntiles);
@@ -366,7 +371,27 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
 
     // ---- epilogue: lane holds channels co .. co + 3 (co = 64 wn + 32 nb +
     // 8 q + 4 half) of voxel row wm ROWS + 32 mb + l32 ----
-    if constexpr (!HEAD) {
+    if constexpr (EPI == EPI_OUT) {
+      // the output layer: rows 0..3 of the channel block are the four logits
+      // (+ bias, no activation), held by the lanes of the first half-wave
+      if (half == 0) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          int b, t, i, j;
+          if (tile_row_coords(g, tl, tile, wm * W::ROWS + mb * 32 + l32, batch, &b, &t, &i, &j)) {
+            const float lg[4] = {acc[mb][0][0] + bias_s[0], acc[mb][0][1] + bias_s[1], acc[mb][0][2] + bias_s[2],
+                                 acc[mb][0][3] + bias_s[3]};
+            const int HH = g.H * g.H;
+            const int s = i * g.H + j;
+            nib[(long long)b * g.V + (long long)t * HH + s] = (uint8_t)flip_nibble(g, tables, i, j, lg);
+            if (logits) {
+#pragma unroll
+              for (int o = 0; o < 4; ++o) logits[(((long long)b * 4 + o) * g.T + t) * HH + s] = lg[o];
+            }
+          }
+        }
+      }
+    } else if constexpr (EPI == EPI_ACT) {
       // bias + activation + bf16, transposed through this wave's slice of
       // the staging buffer the tile read last (64 rows x 128 bytes, granule
       // c of row r at c ^ (r % 8)), then stored as whole 128-byte halves of
@@ -480,14 +505,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
           }
           const int HH = g.H * g.H;
           const int s = i * g.H + j;
-          const int n = comp_of_site[s];
-          const bool data = (i < g.d) && (j < g.d);
-          unsigned bits = 0;
-          if (data && lg[0] > 0.0f) bits |= 1u;
-          if (data && lg[1] > 0.0f) bits |= 2u;
-          if (n >= 0 && n < g.K && lg[2] > 0.0f) bits |= 4u;
-          if (n >= g.K && lg[3] > 0.0f) bits |= 8u;
-          nib[(long long)b * g.V + (long long)t * HH + s] = (uint8_t)bits;
+          nib[(long long)b * g.V + (long long)t * HH + s] = (uint8_t)flip_nibble(g, tables, i, j, lg);
           if (logits) {
 #pragma unroll
             for (int o = 0; o < 4; ++o) logits[(((long long)b * 4 + o) * g.T + t) * HH + s] = lg[o];
@@ -501,21 +519,21 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
-template <int CIN, int COUT, bool HEAD, int MODE>
+template <int CIN, int COUT, int EPI, int MODE>
 hipError_t launch_one(const Geom& g, const Tiling& tl, int act, const void* x, void* y, const void* wfrag,
-                      const float* bias, const float* head_w, const float* head_b, const int32_t* comp_of_site,
+                      const float* bias, const float* head_w, const float* head_b, const int32_t* tables,
                       uint8_t* nib, float* logits, int batch, int n_workgroups, hipStream_t stream) {
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)conv_hidden_kernel<CIN, COUT, HEAD, MODE>,
+    hipError_t e = hipFuncSetAttribute((const void*)conv_hidden_kernel<CIN, COUT, EPI, MODE>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, Lds<COUT>::total);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
   const long long nwg = conv_workgroups(tl.ntiles, n_workgroups);
-  hipLaunchKernelGGL((conv_hidden_kernel<CIN, COUT, HEAD, MODE>), dim3((unsigned)nwg), dim3(NT),
+  hipLaunchKernelGGL((conv_hidden_kernel<CIN, COUT, EPI, MODE>), dim3((unsigned)nwg), dim3(NT),
                      (size_t)Lds<COUT>::total, stream, g, tl, act, (const uint16_t*)x, (uint16_t*)y,
-                     (const u32x4*)wfrag, bias, head_w, head_b, comp_of_site, nib, logits, batch);
+                     (const u32x4*)wfrag, bias, head_w, head_b, tables, nib, logits, batch);
   return hipGetLastError();
 }
 
@@ -524,30 +542,31 @@ hipError_t launch_one(const Geom& g, const Tiling& tl, int act, const void* x, v
 int conv_hidden_max_span() { return MAX_SPAN; }
 int conv_hidden_workgroups_per_cu() { return 2; }
 
-#define PD_HIDDEN_CASE(CI, CO)                                                                               \
-  if (cin == CI && cout == CO) {                                                                            \
-    if (head && tl.mode == 0)                                                                                \
-      return launch_one<CI, CO, true, 0>(g, tl, act, x, y, wfrag, bias, head_w, head_b, comp_of_site, nib,    \
-                                         logits, batch, n_workgroups, stream);                               \
-    if (head)                                                                                                \
-      return launch_one<CI, CO, true, 1>(g, tl, act, x, y, wfrag, bias, head_w, head_b, comp_of_site, nib,    \
-                                         logits, batch, n_workgroups, stream);                               \
-    if (tl.mode == 0)                                                                                        \
-      return launch_one<CI, CO, false, 0>(g, tl, act, x, y, wfrag, bias, head_w, head_b, comp_of_site, nib,   \
-                                          logits, batch, n_workgroups, stream);                              \
-    return launch_one<CI, CO, false, 1>(g, tl, act, x, y, wfrag, bias, head_w, head_b, comp_of_site, nib,     \
-                                        logits, batch, n_workgroups, stream);                                \
+#define PD_HIDDEN_CASE(CI, CO, E)                                                                  \
+  if (cin == CI && cout == CO && head == E) {                                                     \
+    if (tl.mode == 0)                                                                              \
+      return launch_one<CI, CO, E, 0>(g, tl, act, x, y, wfrag, bias, head_w, head_b, tables, nib,   \
+                                      logits, batch, n_workgroups, stream);                        \
+    return launch_one<CI, CO, E, 1>(g, tl, act, x, y, wfrag, bias, head_w, head_b, tables, nib,     \
+                                    logits, batch, n_workgroups, stream);                          \
   }
 
 hipError_t launch_conv_hidden(const Geom& g, const Tiling& tl, int cin, int cout, int act, const void* x,
                               void* y, const void* wfrag, const float* bias, int head, const float* head_w,
-                              const float* head_b, const int32_t* comp_of_site, uint8_t* nib, float* logits,
+                              const float* head_b, const int32_t* tables, uint8_t* nib, float* logits,
                               int batch, int n_workgroups, hipStream_t stream) {
   if (tl.span <= 0 || tl.span > MAX_SPAN) return hipErrorInvalidValue;
-  PD_HIDDEN_CASE(64, 64)
-  PD_HIDDEN_CASE(128, 128)
-  PD_HIDDEN_CASE(64, 128)
-  PD_HIDDEN_CASE(128, 64)
+  PD_HIDDEN_CASE(64, 64, EPI_ACT)
+  PD_HIDDEN_CASE(128, 128, EPI_ACT)
+  PD_HIDDEN_CASE(64, 128, EPI_ACT)
+  PD_HIDDEN_CASE(128, 64, EPI_ACT)
+  PD_HIDDEN_CASE(64, 64, EPI_HEAD)
+  PD_HIDDEN_CASE(128, 128, EPI_HEAD)
+  PD_HIDDEN_CASE(64, 128, EPI_HEAD)
+  PD_HIDDEN_CASE(128, 64, EPI_HEAD)
+  if (cout == 4) cout = 32;  // the output layer's 4 filters fill one padded block
+  PD_HIDDEN_CASE(64, 32, EPI_OUT)
+  PD_HIDDEN_CASE(128, 32, EPI_OUT)
   return hipErrorInvalidValue;
 }
 

@@ -79,7 +79,7 @@ __global__ void __launch_bounds__(NT) conv_single_kernel(Geom g, Tiling tl, int 
                                                          const float* __restrict__ bias,
                                                          const float* __restrict__ head_w,
                                                          const float* __restrict__ head_b,
-                                                         const int32_t* __restrict__ comp_of_site,
+                                                         const int32_t* __restrict__ tables,
                                                          uint8_t* __restrict__ nib, float* __restrict__ logits,
                                                          int batch) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -241,14 +241,7 @@ __global__ void __launch_bounds__(NT) conv_single_kernel(Geom g, Tiling tl, int 
         }
         const int HH = g.H * g.H;
         const int s = i * g.H + j;
-        const int n = comp_of_site[s];
-        const bool data = (i < g.d) && (j < g.d);
-        unsigned bits = 0;
-        if (data && lg[0] > 0.0f) bits |= 1u;
-        if (data && lg[1] > 0.0f) bits |= 2u;
-        if (n >= 0 && n < g.K && lg[2] > 0.0f) bits |= 4u;
-        if (n >= g.K && lg[3] > 0.0f) bits |= 8u;
-        nib[(long long)b * g.V + (long long)t * HH + s] = (uint8_t)bits;
+        nib[(long long)b * g.V + (long long)t * HH + s] = (uint8_t)flip_nibble(g, tables, i, j, lg);
         if (logits) {
 #pragma unroll
           for (int o = 0; o < 4; ++o) logits[(((long long)b * 4 + o) * g.T + t) * HH + s] = lg[o];
@@ -265,12 +258,12 @@ __global__ void __launch_bounds__(NT) conv_single_kernel(Geom g, Tiling tl, int 
 
 template <int COUT, int MODE>
 hipError_t launch_one(const Geom& g, const Tiling& tl, int act, const void* planes, const void* wfrag,
-                      const float* bias, const float* head_w, const float* head_b, const int32_t* comp_of_site,
+                      const float* bias, const float* head_w, const float* head_b, const int32_t* tables,
                       uint8_t* nib, float* logits, int batch, int n_workgroups, hipStream_t stream) {
   const long long nwg = conv_workgroups(tl.ntiles, n_workgroups);
   hipLaunchKernelGGL((conv_single_kernel<COUT, MODE>), dim3((unsigned)nwg), dim3(NT), (size_t)Lds<COUT>::total,
                      stream, g, tl, act, (const uint32_t*)planes, (const u32x4*)wfrag, bias, head_w, head_b,
-                     comp_of_site, nib, logits, batch);
+                     tables, nib, logits, batch);
   return hipGetLastError();
 }
 
@@ -280,18 +273,18 @@ int conv_single_max_span() { return MAX_SPAN; }
 
 hipError_t launch_conv_single(const Geom& g, const Tiling& tl, int cout, int act, const void* planes,
                               const void* wfrag, const float* bias, const float* head_w, const float* head_b,
-                              const int32_t* comp_of_site, uint8_t* nib, float* logits, int batch,
+                              const int32_t* tables, uint8_t* nib, float* logits, int batch,
                               int n_workgroups, hipStream_t stream) {
   if (tl.span <= 0 || tl.span > MAX_SPAN) return hipErrorInvalidValue;
   if (cout == 64)
-    return tl.mode == 0 ? launch_one<64, 0>(g, tl, act, planes, wfrag, bias, head_w, head_b, comp_of_site, nib,
+    return tl.mode == 0 ? launch_one<64, 0>(g, tl, act, planes, wfrag, bias, head_w, head_b, tables, nib,
                                             logits, batch, n_workgroups, stream)
-                        : launch_one<64, 1>(g, tl, act, planes, wfrag, bias, head_w, head_b, comp_of_site, nib,
+                        : launch_one<64, 1>(g, tl, act, planes, wfrag, bias, head_w, head_b, tables, nib,
                                             logits, batch, n_workgroups, stream);
   if (cout == 128)
-    return tl.mode == 0 ? launch_one<128, 0>(g, tl, act, planes, wfrag, bias, head_w, head_b, comp_of_site, nib,
+    return tl.mode == 0 ? launch_one<128, 0>(g, tl, act, planes, wfrag, bias, head_w, head_b, tables, nib,
                                              logits, batch, n_workgroups, stream)
-                        : launch_one<128, 1>(g, tl, act, planes, wfrag, bias, head_w, head_b, comp_of_site, nib,
+                        : launch_one<128, 1>(g, tl, act, planes, wfrag, bias, head_w, head_b, tables, nib,
                                              logits, batch, n_workgroups, stream);
   return hipErrorInvalidValue;
 }

@@ -4,9 +4,10 @@
 // voxel, the threshold logit > 0 (sigmoid > 1/2 of the BCE objective,
 // Sec. IV.B.5), and the read-out of the four correction channels where they
 // are defined (Eqs. ZcorreJK, XcorreJK, SynXCorrJK, SynZCorrJK): channels 0/1
-// at data qubits (grid sites (r, c), r, c < d), channel 2 at X sites, channel 3
-// at Z sites.  The four flip bits of a voxel are kept as one nibble per voxel
-// in a small workspace; fp32 logits are written only when asked for.
+// at data qubits (grid sites (r, c), r, c < d), channel 2 where an X
+// stabilizer sits (or is drawn, in the paper's layout), channel 3 likewise
+// for Z.  The four flip bits of a voxel are kept as one nibble per voxel in a
+// small workspace; fp32 logits are written only when asked for.
 //
 // K5 (residual + repack): one wave64 per packed 64-bit output word.  Lane l
 // computes bit 64 w + l of either the residual row (Eqs. Resk1X..ReskG1Z:
@@ -25,7 +26,7 @@ template <bool FP32>
 __global__ void __launch_bounds__(256) head_kernel(Geom g, int cin, const void* __restrict__ x,
                                                    const float* __restrict__ w_head,
                                                    const float* __restrict__ b_head,
-                                                   const int32_t* __restrict__ comp_of_site,
+                                                   const int32_t* __restrict__ tables,
                                                    uint8_t* __restrict__ nib, float* __restrict__ logits,
                                                    int batch) {
   __shared__ float w[4 * 128];
@@ -64,14 +65,7 @@ __global__ void __launch_bounds__(256) head_kernel(Geom g, int cin, const void* 
       }
     }
   }
-  const int n = comp_of_site[s];
-  const bool data = (i < g.d) && (j < g.d);
-  unsigned bits = 0;
-  if (data && acc[0] > 0.0f) bits |= 1u;
-  if (data && acc[1] > 0.0f) bits |= 2u;
-  if (n >= 0 && n < g.K && acc[2] > 0.0f) bits |= 4u;
-  if (n >= g.K && acc[3] > 0.0f) bits |= 8u;
-  nib[gid] = (uint8_t)bits;
+  nib[gid] = (uint8_t)flip_nibble(g, tables, i, j, acc);
   if (logits) {
 #pragma unroll
     for (int o = 0; o < 4; ++o) logits[(((long long)b * 4 + o) * g.T + t) * HH + s] = acc[o];
@@ -92,7 +86,7 @@ __device__ __forceinline__ unsigned residual_bit(const Geom& g, const int32_t* _
   if (t > 0) r ^= flip(mch, t - 1, s);
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const int qs = supp[s * 4 + q];
+    const int qs = supp[n * 4 + q];
     if (qs >= 0) r ^= flip(dch, t, qs);
   }
   return r;
@@ -160,7 +154,8 @@ __global__ void __launch_bounds__(256) residual_from_flips_kernel(Geom g, const 
   const int b = (int)(wid / g.Wd);
   const long long w = wid - (long long)b * g.Wd;
   const int32_t* site_of = tables + tables_site_of(g);
-  const int32_t* comp = tables + tables_comp_of_site(g);
+  const int32_t* comp_x = tables + tables_comp_x(g);
+  const int32_t* comp_z = tables + tables_comp_z(g);
   const int32_t* supp = tables + tables_supp(g);
   const uint64_t* fr = flips + (long long)b * g.Wf;
   const int dd = g.d * g.d;
@@ -170,7 +165,7 @@ __global__ void __launch_bounds__(256) residual_from_flips_kernel(Geom g, const 
       const int r = s / g.H, c = s - (s / g.H) * g.H;
       fk += ch * dd + r * g.d + c;
     } else {
-      fk += 2 * dd + comp[s];
+      fk += 2 * dd + (ch == 2 ? comp_x[s] : comp_z[s]);
     }
     return (unsigned)((fr[fk >> 6] >> (fk & 63)) & 1ull);
   };
@@ -190,13 +185,12 @@ hipError_t launch_head(const Geom& g, int cin, int fp32, const void* x, const fl
                               int batch, hipStream_t stream) {
   long long total = (long long)batch * g.V;
   unsigned grid = (unsigned)((total + 255) / 256);
-  const int32_t* comp = tables + tables_comp_of_site(g);
   if (fp32)
     hipLaunchKernelGGL(head_kernel<true>, dim3(grid), dim3(256), 0, stream, g, cin, x, w_head, b_head,
-                       comp, nib, logits, batch);
+                       tables, nib, logits, batch);
   else
     hipLaunchKernelGGL(head_kernel<false>, dim3(grid), dim3(256), 0, stream, g, cin, x, w_head, b_head,
-                       comp, nib, logits, batch);
+                       tables, nib, logits, batch);
   return hipGetLastError();
 }
 

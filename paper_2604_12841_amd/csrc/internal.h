@@ -8,9 +8,10 @@
 
 namespace pd {
 
-// Padded activation layout (NTHWC with a one-voxel zero halo in t, i and j):
-//   voxel (b, t, i, j), 0 <= t < T, 0 <= i, j <= d, lives at padded index
-//   b * S + (t + 1) * P + (i + 1) * Wp + (j + 1),  Wp = d + 3, P = Wp^2,
+// Padded activation layout (NTHWC with a one-voxel zero halo in t, i and j;
+// H = d + 1 on the plaquette grid, d on the paper layout):
+//   voxel (b, t, i, j), 0 <= t < T, 0 <= i, j < H, lives at padded index
+//   b * S + (t + 1) * P + (i + 1) * Wp + (j + 1),  Wp = H + 2, P = Wp^2,
 //   S = (T + 2) * P,
 // channels contiguous.  The halo is zeroed once at create and never written,
 // so a 3x3x3 tap is a pure index shift.
@@ -22,6 +23,15 @@ struct Geom {
   int nstab;    // d^2 - 1
   int nflip;    // 3 d^2 - 1
   long long Wd, Wf;  // packed words per sample
+  // Input layout: 0 = plaquette grid, H = d + 1, two channels (detector events
+  // at their stabilizer sites); 1 = the paper's own layout (Sec. IV.B.1), H = d
+  // (the data qubits), four channels (x_type, z_type, x_present, z_present),
+  // every stabilizer drawn onto one qubit of its support.
+  int layout;
+  // Basis prepared before round 0 / measured after round T-1 (0 none, 1 Z,
+  // 2 X): in the paper's layout, Z clears x_present and X clears z_present
+  // in that round.
+  int first, last;
 };
 
 __host__ __device__ inline long long padded_index(const Geom& g, int b, int t, int i, int j) {
@@ -101,14 +111,15 @@ __host__ __device__ inline long long line_to_padded(const Geom& g, long long u) 
 constexpr int kTileRows = 256;
 
 // Kernel launchers (all asynchronous on `stream`; return the launch error).
-hipError_t launch_unpack(const Geom& g, const int32_t* comp_of_site, const uint64_t* det, int batch,
-                         void* out, int out_padded, int fp32, hipStream_t stream);
+// Detector events -> input planes (c_in = 2 or 4 channels by layout).
+hipError_t launch_unpack(const Geom& g, const int32_t* tables, const uint64_t* det, int batch, void* out,
+                         int out_padded, int fp32, hipStream_t stream);
 
-// The first 3x3x3 layer (c_in = 2, c_out = 64 or 128) when it is not also
-// the last hidden layer: planes [batch * S] (2 bf16 channels each), weight
-// fragments [4 k-steps][c_out / 32][64 lanes][8 bf16].
-hipError_t launch_conv_first(const Geom& g, int cout, int act, const void* planes, void* y, const void* wfrag,
-                             const float* bias, int batch, hipStream_t stream);
+// The first 3x3x3 layer (c_in = 2 or 4, c_out = 64 or 128) when it is not
+// also the last hidden layer: planes [batch * S][c_in] bf16, weight fragments
+// [ceil(27 c_in / 16) k-steps][c_out / 32][64 lanes][8 bf16].
+hipError_t launch_conv_first(const Geom& g, int cin, int cout, int act, const void* planes, void* y,
+                             const void* wfrag, const float* bias, int batch, hipStream_t stream);
 
 // A network with one hidden layer: layer 1 (as launch_conv_first) with the
 // 1x1x1 head (head_w [4][cout] fp32, bf16-valued; head_b [4]) and the
@@ -116,18 +127,22 @@ hipError_t launch_conv_first(const Geom& g, int cout, int act, const void* plane
 // non-null).  n_workgroups: one per CU.
 hipError_t launch_conv_single(const Geom& g, const Tiling& tl, int cout, int act, const void* planes,
                               const void* wfrag, const float* bias, const float* head_w, const float* head_b,
-                              const int32_t* comp_of_site, uint8_t* nib, float* logits, int batch,
+                              const int32_t* tables, uint8_t* nib, float* logits, int batch,
                               int n_workgroups, hipStream_t stream);
 int conv_single_max_span();  // staged voxels a tile may need
 
-// A hidden 3x3x3 bf16 layer (c_in, c_out in {64, 128}) on the zero-halo
-// activations x -> y.  head != 0: the head and the threshold are applied in
-// the epilogue as for launch_conv_single, instead of writing y.  Weight
-// fragments in 16-channel chunks (conv_fragments in api.hip);
-// n_workgroups = conv_hidden_workgroups_per_cu() per CU.
+// A 3x3x3 bf16 layer on the zero-halo activations x (c_in in {64, 128}).
+//   head == 0: a hidden layer (c_out in {64, 128}) writing y;
+//   head == 1: a hidden layer whose epilogue applies the 1x1x1 head and the
+//              threshold as launch_conv_single does, instead of writing y;
+//   head == 2: the output layer itself (c_out = 4, no activation): its
+//              outputs are the logits, thresholded into flip nibbles.
+// Weight fragments in 16-channel chunks (conv_fragments in api.hip; c_out = 4
+// padded to 32 channels, bias to 32 values); n_workgroups =
+// conv_hidden_workgroups_per_cu() per CU.
 hipError_t launch_conv_hidden(const Geom& g, const Tiling& tl, int cin, int cout, int act, const void* x,
                               void* y, const void* wfrag, const float* bias, int head, const float* head_w,
-                              const float* head_b, const int32_t* comp_of_site, uint8_t* nib, float* logits,
+                              const float* head_b, const int32_t* tables, uint8_t* nib, float* logits,
                               int batch, int n_workgroups, hipStream_t stream);
 int conv_hidden_max_span();
 int conv_hidden_workgroups_per_cu();
@@ -157,13 +172,35 @@ hipError_t launch_residual_from_flips(const Geom& g, const int32_t* tables, cons
                                       hipStream_t stream);
 
 // Device tables (int32), one allocation, offsets in elements:
-//   [0, nstab)             site_of[n]: grid index i*H+j of compact stabilizer n
-//   [nstab, nstab+H*H)     comp_of_site[s]: compact index of site s, or -1
-//   [.., .. + 4*H*H)       supp[s][4]: grid indices of the data qubits of
-//                          plaquette s (data qubit (r,c) is grid site (r,c)), -1 pads
+//   [0, nstab)           site_of[n]: grid index of compact stabilizer n -- where
+//                        its detector event enters and its measurement flip is
+//                        read (its plaquette site, or in the paper's layout the
+//                        qubit it is drawn onto)
+//   comp_x[H*H]          compact index of the X stabilizer at grid site s, or -1
+//   comp_z[H*H]          the same for Z (in the paper's layout an X and a Z
+//                        stabilizer can share a site)
+//   supp[nstab][4]       grid indices of the data qubits of stabilizer n (data
+//                        qubit (r, c) is grid site r*H+c), -1 pads
 __host__ __device__ inline int tables_site_of(const Geom&) { return 0; }
-__host__ __device__ inline int tables_comp_of_site(const Geom& g) { return g.nstab; }
-__host__ __device__ inline int tables_supp(const Geom& g) { return g.nstab + g.H * g.H; }
-__host__ __device__ inline int tables_size(const Geom& g) { return g.nstab + 5 * g.H * g.H; }
+__host__ __device__ inline int tables_comp_x(const Geom& g) { return g.nstab; }
+__host__ __device__ inline int tables_comp_z(const Geom& g) { return g.nstab + g.H * g.H; }
+__host__ __device__ inline int tables_supp(const Geom& g) { return g.nstab + 2 * g.H * g.H; }
+__host__ __device__ inline int tables_size(const Geom& g) { return 5 * g.nstab + 2 * g.H * g.H; }
+
+// Flip nibble of grid site s (bit 0 Z data, 1 X data, 2 X measurement, 3 Z
+// measurement correction) from the four logits, keeping each channel only
+// where it is defined (Eqs. ZcorreJK..SynZCorrJK): data qubits for 0/1, the
+// site of an X / Z stabilizer for 2 / 3; a logit of exactly 0 is no flip.
+__device__ __forceinline__ unsigned flip_nibble(const Geom& g, const int32_t* __restrict__ tables, int i, int j,
+                                                const float* lg) {
+  const int s = i * g.H + j;
+  const bool data = (i < g.d) && (j < g.d);
+  unsigned bits = 0;
+  if (data && lg[0] > 0.0f) bits |= 1u;
+  if (data && lg[1] > 0.0f) bits |= 2u;
+  if (tables[tables_comp_x(g) + s] >= 0 && lg[2] > 0.0f) bits |= 4u;
+  if (tables[tables_comp_z(g) + s] >= 0 && lg[3] > 0.0f) bits |= 8u;
+  return bits;
+}
 
 }  // namespace pd

@@ -1,19 +1,26 @@
-// unpack.hip -- K1: packed detector events -> 2-channel planes (Sec. IV.B.1:
-// each detector event is placed at its stabilizer's grid site, X-type in
-// channel 0 and Z-type in channel 1; every other grid location is 0).
+// unpack.hip -- K1: packed detector events -> input planes (Sec. IV.B.1).
 //
-// One thread per interior voxel (b, t, i, j); the thread reads the one bit it
+// Plaquette layout: two channels on the (d+1) x (d+1) grid, each detector
+// event at its stabilizer's site, X-type in channel 0 and Z-type in channel 1
+// (every other grid location is 0).
+// Paper layout (Eqs. encTrainX1-encTrainX4): four channels on the D x D grid
+// of data qubits, every stabilizer drawn onto one qubit of its support:
+// x_type / z_type carry the detector events of the X / Z stabilizer drawn at
+// the qubit, x_present / z_present its weight / 4 (1 or 0.5), cleared in the
+// first round for the basis the qubit is prepared in (Z clears x_present, X
+// clears z_present) and in the last round for the basis it is measured in.
+//
+// One thread per interior voxel (b, t, i, j); the thread reads the bits it
 // needs (the packed row of a sample is a few hundred bytes, so these reads hit
-// L1/L2) and writes both channels with one 4-byte (bf16 pair) or 8-byte (fp32
-// pair) store.  Consecutive threads write consecutive voxels of a grid row.
-// HBM-bound: reads W_det * 8 bytes and writes 2 * V * sizeof(elem) bytes per
-// sample.
+// L1/L2) and writes all channels of the voxel with one store.  Consecutive
+// threads write consecutive voxels of a grid row.  HBM-bound: reads W_det * 8
+// bytes and writes c_in * V * sizeof(elem) bytes per sample.
 #include "internal.h"
 
 namespace pd {
 
-template <bool FP32, bool PADDED>
-__global__ void __launch_bounds__(256) unpack_kernel(Geom g, const int32_t* __restrict__ comp_of_site,
+template <bool FP32, bool PADDED, bool PAPER>
+__global__ void __launch_bounds__(256) unpack_kernel(Geom g, const int32_t* __restrict__ tables,
                                                      const uint64_t* __restrict__ det, int batch,
                                                      void* __restrict__ out) {
   long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
@@ -24,13 +31,14 @@ __global__ void __launch_bounds__(256) unpack_kernel(Geom g, const int32_t* __re
   int HH = g.H * g.H;
   int t = v / HH;
   int s = v - t * HH;
-  int n = comp_of_site[s];
-  unsigned bit = 0;
-  if (n >= 0) {
-    long long k = (long long)t * g.nstab + n;
-    bit = (unsigned)((det[(long long)b * g.Wd + (k >> 6)] >> (k & 63)) & 1ull);
-  }
-  unsigned ch = (n >= g.K) ? 1u : 0u;  // X sites come first in the compact order
+  const uint64_t* row = det + (long long)b * g.Wd;
+  auto event = [&](int n) -> unsigned {
+    if (n < 0) return 0u;
+    const long long k = (long long)t * g.nstab + n;
+    return (unsigned)((row[k >> 6] >> (k & 63)) & 1ull);
+  };
+  const int nx = tables[tables_comp_x(g) + s], nz = tables[tables_comp_z(g) + s];
+  const unsigned ex = event(nx), ez = event(nz);
   long long o;
   if (PADDED) {
     int i = s / g.H, j = s - (s / g.H) * g.H;
@@ -38,32 +46,57 @@ __global__ void __launch_bounds__(256) unpack_kernel(Geom g, const int32_t* __re
   } else {
     o = gid;
   }
-  if (FP32) {
-    float2 val;
-    val.x = (bit && ch == 0) ? 1.0f : 0.0f;
-    val.y = (bit && ch == 1) ? 1.0f : 0.0f;
-    reinterpret_cast<float2*>(out)[o] = val;
+  if constexpr (PAPER) {
+    // weight / 4 of the stabilizer drawn here: 1 for four qubits, 0.5 for two
+    auto present = [&](int n, int kind) -> float {
+      if (n < 0) return 0.0f;
+      if ((t == 0 && g.first == kind) || (t == g.T - 1 && g.last == kind)) return 0.0f;
+      const int32_t* sp = tables + tables_supp(g) + n * 4;
+      return (sp[2] >= 0) ? 1.0f : 0.5f;
+    };
+    const float px = present(nx, 1), pz = present(nz, 2);
+    static_assert(!FP32, "the paper's layout runs in bf16");
+    // bf16 patterns: 1.0 = 0x3F80, 0.5 = 0x3F00
+    auto bf = [](float f) -> uint32_t { return f == 1.0f ? 0x3F80u : (f == 0.5f ? 0x3F00u : 0u); };
+    uint2 val;
+    val.x = (ex ? 0x3F80u : 0u) | ((ez ? 0x3F80u : 0u) << 16);
+    val.y = bf(px) | (bf(pz) << 16);
+    reinterpret_cast<uint2*>(out)[o] = val;
   } else {
-    uint32_t one = 0x3F80u;  // bf16 1.0
-    uint32_t val = bit ? (one << (16 * ch)) : 0u;
-    reinterpret_cast<uint32_t*>(out)[o] = val;
+    if (FP32) {
+      float2 val;
+      val.x = ex ? 1.0f : 0.0f;
+      val.y = ez ? 1.0f : 0.0f;
+      reinterpret_cast<float2*>(out)[o] = val;
+    } else {
+      reinterpret_cast<uint32_t*>(out)[o] = (ex ? 0x3F80u : 0u) | ((ez ? 0x3F80u : 0u) << 16);
+    }
   }
 }
 
-hipError_t launch_unpack(const Geom& g, const int32_t* comp_of_site, const uint64_t* det, int batch,
-                         void* out, int out_padded, int fp32, hipStream_t stream) {
+hipError_t launch_unpack(const Geom& g, const int32_t* tables, const uint64_t* det, int batch, void* out,
+                         int out_padded, int fp32, hipStream_t stream) {
   long long total = (long long)batch * g.V;
   unsigned grid = (unsigned)((total + 255) / 256);
-  if (fp32) {
+  auto go = [&](auto kernel) {
+    hipLaunchKernelGGL(kernel, dim3(grid), dim3(256), 0, stream, g, tables, det, batch, out);
+  };
+  if (g.layout == 1) {
+    if (fp32) return hipErrorInvalidValue;
     if (out_padded)
-      hipLaunchKernelGGL((unpack_kernel<true, true>), dim3(grid), dim3(256), 0, stream, g, comp_of_site, det, batch, out);
+      go(unpack_kernel<false, true, true>);
     else
-      hipLaunchKernelGGL((unpack_kernel<true, false>), dim3(grid), dim3(256), 0, stream, g, comp_of_site, det, batch, out);
+      go(unpack_kernel<false, false, true>);
+  } else if (fp32) {
+    if (out_padded)
+      go(unpack_kernel<true, true, false>);
+    else
+      go(unpack_kernel<true, false, false>);
   } else {
     if (out_padded)
-      hipLaunchKernelGGL((unpack_kernel<false, true>), dim3(grid), dim3(256), 0, stream, g, comp_of_site, det, batch, out);
+      go(unpack_kernel<false, true, false>);
     else
-      hipLaunchKernelGGL((unpack_kernel<false, false>), dim3(grid), dim3(256), 0, stream, g, comp_of_site, det, batch, out);
+      go(unpack_kernel<false, false, false>);
   }
   return hipGetLastError();
 }

@@ -17,8 +17,9 @@ TOL = {"bf16": 2e-2, "fp32": 1e-4}
 
 
 @functools.lru_cache(maxsize=None)
-def flip_sites(d):
-    """(ch, i, j) of each compact flip index n in [0, 3d^2 - 1)."""
+def flip_sites(d, layout="plaquette"):
+    """(ch, i, j) of each compact flip index n in [0, 3d^2 - 1): where its
+    logit sits on the grid of the layout."""
     site_of, _ = oracle.stabilizer_order(d)
     H = d + 1
     K = (d * d - 1) // 2
@@ -26,6 +27,8 @@ def flip_sites(d):
     out += [(1, r, c) for r in range(d) for c in range(d)]
     for n in range(d * d - 1):
         i, j = divmod(int(site_of[n]), H)
+        if layout == "paper":
+            _, i, j = oracle.stabilizer_qubit(d, i, j)
         out.append((2 if n < K else 3, i, j))
     return np.array(out, dtype=np.int64)
 
@@ -47,9 +50,9 @@ def residual_contributions(d):
     return np.array(meas), np.array(data)
 
 
-def excused_masks(d, T, logits, tol):
+def excused_masks(d, T, logits, tol, layout="plaquette"):
     """(flip_excused [B][T*(3d^2-1)], residual_excused [B][T*(d^2-1)]) bool."""
-    fs = flip_sites(d)
+    fs = flip_sites(d, layout)
     B = logits.shape[0]
     F = 3 * d * d - 1
     S = d * d - 1
@@ -67,13 +70,14 @@ def excused_masks(d, T, logits, tol):
     return fex.reshape(B, T * F), rex.reshape(B, T * S)
 
 
-def compare(d, T, dtype, ref_logits, ref_flips, ref_res, got_flips, got_res, got_logits=None):
+def compare(d, T, dtype, ref_logits, ref_flips, ref_res, got_flips, got_res, got_logits=None,
+            layout="plaquette"):
     """Returns a dict of parity statistics (see module docstring)."""
     tol = TOL[dtype]
     B = ref_logits.shape[0]
     F = T * (3 * d * d - 1)
     S = T * (d * d - 1)
-    fex, rex = excused_masks(d, T, ref_logits, tol)
+    fex, rex = excused_masks(d, T, ref_logits, tol, layout)
     rf = workload.unpack_rows(ref_flips, F).astype(bool)
     gf = workload.unpack_rows(got_flips, F).astype(bool)
     rr = workload.unpack_rows(ref_res, S).astype(bool)
@@ -150,7 +154,7 @@ def run_gpu(pre, det, want_logits=True, canary=True, batch=None):
     res = torch.full((B, pre.det_words), fill, dtype=torch.int64, device="cuda")
     logits = None
     if want_logits:
-        logits = torch.full((B, 4, T, d + 1, d + 1), float("nan"), dtype=torch.float32, device="cuda")
+        logits = torch.full((B, 4, T, pre.grid, pre.grid), float("nan"), dtype=torch.float32, device="cuda")
     pre.run(ddet, flips, res, logits)
     torch.cuda.synchronize()
     return host_u64(flips), host_u64(res), (logits.cpu().numpy() if want_logits else None)

@@ -149,3 +149,45 @@ def test_run_rejects_null_handle():
     assert L.predecoder_unpack(None, None, None, 1, None) == pdx.PD_ERR_INVALID_ARG
     assert L.predecoder_num_stages(None) == -1
     L.predecoder_destroy(None)
+
+
+def _create_ex(weights, d, T, layers, layout, first=0, last=0, dtype=pdx.DTYPE_BF16, max_batch=2):
+    L = pdx.lib()
+    w = np.ascontiguousarray(weights, dtype=np.float32)
+    opts = pdx.Options(layout, first, last)
+    h = ctypes.c_void_p()
+    st = L.predecoder_create_ex(w.ctypes.data_as(ctypes.c_void_p), w.size, d, T, pdx._layers(layers),
+                                len(layers), dtype, max_batch, ctypes.byref(opts), ctypes.byref(h))
+    if st == pdx.PD_OK:
+        L.predecoder_destroy(h)
+    return st
+
+
+PAPER = workload.paper_layer_spec([64, 64, 4], [3, 3, 3])
+WP = workload.he_normal_weights(PAPER, 0)
+
+
+@pytest.mark.parametrize("case", [
+    dict(layout=2),                                          # unknown layout
+    dict(first=3), dict(last=-1),                            # unknown basis
+    dict(layout=pdx.LAYOUT_PLAQUETTE, layers=LAYERS, weights=W, first=pdx.BOUNDARY_Z),  # nothing to clear
+    dict(layers=LAYERS, weights=W),                          # paper layout takes 4 input channels
+    dict(layout=pdx.LAYOUT_PLAQUETTE),                       # plaquette layout takes 2
+])
+def test_create_ex_rejects_misuse(case):
+    args = dict(weights=WP, d=5, T=3, layers=PAPER, layout=pdx.LAYOUT_PAPER)
+    args.update(case)
+    assert _create_ex(**args) == pdx.PD_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("model,dtype", [(1, pdx.DTYPE_FP32), (2, pdx.DTYPE_BF16), (3, pdx.DTYPE_BF16)])
+def test_create_ex_unsupported_models(model, dtype):
+    # fp32 on the paper layout; width 256 (Model 2); 5x5x5 kernels (Model 3)
+    layers = workload.paper_model_layers(model)
+    w = np.zeros(pdx.weight_count(layers), np.float32)
+    assert _create_ex(w, 5, 3, layers, pdx.LAYOUT_PAPER, dtype=dtype) == pdx.PD_ERR_UNSUPPORTED
+
+
+@pytest.mark.skipif(gpu_available(), reason="checks the no-device error path")
+def test_create_ex_without_device_reports_device_error():
+    assert _create_ex(WP, 5, 3, PAPER, pdx.LAYOUT_PAPER, pdx.BOUNDARY_Z, pdx.BOUNDARY_X) == pdx.PD_ERR_DEVICE

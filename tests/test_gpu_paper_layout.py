@@ -1,0 +1,84 @@
+"""The paper's own layout on the GPU against the oracle (Sec. IV.B.1, Table
+models): four input channels on the D x D data-qubit grid with the geometric
+channels cleared in the preparation / measurement rounds, a 4-channel first
+layer, and a 3x3x3 output layer of four filters (or a 1x1x1 head)."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2604_12841_amd as pdx
+from paper_2604_12841_amd import workload
+from parity import assert_parity, compare, dev_u64, run_gpu, say
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def cuda():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch.device("cuda")
+
+
+def check(d, T, B, layers, seed, first="Z", last="Z", p=0.01):
+    w = workload.he_normal_weights(layers, seed=seed)
+    det, _ = workload.make_inputs(d, T, B, p, p, seed=seed + 1)
+    say("paper layout d", d, "T", T, "B", B, "layers", layers, "first", first, "last", last)
+    pre = pdx.Predecoder(w, d, T, layers, "bf16", max_batch=B, layout="paper", first=first, last=last)
+    flips, res, logits = run_gpu(pre, det)
+    pre.close()
+    ref = oracle.run(d, T, det, layers, w, bf16=True, layout="paper", first=first, last=last)
+    st = compare(d, T, "bf16", ref[0], ref[1], ref[2], flips, res, logits, layout="paper")
+    say("  stats", st)
+    assert_parity(st, "bf16")
+
+
+@pytest.mark.parametrize("d,T,B,filters", [
+    (5, 5, 3, [64, 64, 4]),
+    (7, 7, 2, [128, 128, 128, 4]),        # Model 1's layer list
+    (9, 5, 2, [128] * 5 + [4]),           # Model 4's layer list
+    (13, 13, 2, [128, 128, 128, 4]),      # Model 1 at 13^3
+    (3, 1, 4, [64, 4]),                   # one hidden layer, a single round
+])
+def test_paper_models_3x3x3_output(cuda, d, T, B, filters):
+    check(d, T, B, workload.paper_layer_spec(filters, [3] * len(filters)), seed=300 + d)
+
+
+def test_paper_model_on_box_tiles(cuda):
+    # d = 31 gives box tiles (the 31 x 31 grid is too wide for flat ones)
+    check(31, 3, 1, workload.paper_layer_spec([64, 64, 4], [3, 3, 3]), seed=331)
+
+
+@pytest.mark.parametrize("first,last", [(None, None), ("X", "X"), ("Z", "X"), ("X", None)])
+def test_boundary_bases(cuda, first, last):
+    check(5, 4, 2, workload.paper_layer_spec([64, 64, 4], [3, 3, 3]), seed=340, first=first, last=last)
+
+
+@pytest.mark.parametrize("filters", [[64, 64, 4], [128, 4]])
+def test_paper_layout_with_1x1x1_head(cuda, filters):
+    kernels = [3] * (len(filters) - 1) + [1]
+    check(7, 5, 3, workload.paper_layer_spec(filters, kernels), seed=350 + len(filters))
+
+
+def test_paper_unpack_planes_exact(cuda):
+    d, T, B = 7, 4, 3
+    layers = workload.paper_layer_spec([64, 4], [3, 3])
+    w = workload.he_normal_weights(layers, seed=360)
+    det, _ = workload.make_inputs(d, T, B, 0.05, 0.05, seed=361)
+    pre = pdx.Predecoder(w, d, T, layers, "bf16", max_batch=B, layout="paper", first="X", last="Z")
+    planes = torch.full((B, T, d, d, 4), -1, dtype=torch.int16, device="cuda")
+    pre.unpack(dev_u64(det), planes)
+    torch.cuda.synchronize()
+    pre.close()
+    got = planes.cpu().view(torch.bfloat16).float().numpy()
+    ref = oracle.unpack_paper(d, T, det, "X", "Z").transpose(0, 2, 3, 4, 1)
+    np.testing.assert_array_equal(got, ref)
+
+
+def test_paper_layout_fp32_is_unsupported(cuda):
+    layers = workload.paper_layer_spec([64, 4], [3, 3])
+    w = workload.he_normal_weights(layers, seed=370)
+    with pytest.raises(pdx.PredecoderError) as e:
+        pdx.Predecoder(w, 5, 3, layers, "fp32", max_batch=1, layout="paper")
+    assert e.value.status == pdx.PD_ERR_UNSUPPORTED
