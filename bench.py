@@ -55,8 +55,9 @@ def counted_traffic(profile):
     return int(m_bytes.group(1))
 
 
-def flops_per_sample(layers, d, T):
-    V = T * (d + 1) ** 2
+def flops_per_sample(layers, H, T):
+    """Conv FLOPs per sample on a T x H x H grid (H = d + 1, or d in the paper's layout)."""
+    V = T * H ** 2
     return sum(2 * ci * co * k ** 3 for (ci, co, k, _a) in layers) * V
 
 
@@ -72,6 +73,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="also run one plain device copy of this many MiB (calibrates HBM byte counters)")
+    ap.add_argument("--paper-model", type=int, default=None,
+                    help="time a model of Table models (1 or 4) in the paper's own layout (D x D grid, four "
+                         "input channels, 3x3x3 output layer) at d = T = --d instead of a workload")
+    ap.add_argument("--d", type=int, default=13, help="distance (and rounds) for --paper-model")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the path is data-parallel over independent volumes and "
@@ -83,15 +88,31 @@ def main():
     import paper_2604_12841_amd as pdx
     from paper_2604_12841_amd import workload
 
-    cfg = workload.CONFIGS[args.workload]
-    d, T = cfg["d"], cfg["T"]
-    B = args.batch or cfg["batch"]
-    layers = workload.config_layers(args.workload)
-    weights = workload.config_weights(args.workload)
-    det, _ = workload.config_inputs(args.workload, B)
+    paper = args.paper_model is not None
+    if paper:
+        # Table models in the paper's layout: memory experiment in the Z basis
+        # (x_present cleared in the first and last round), d = T
+        d = T = args.d
+        B = args.batch or 1
+        layers = workload.paper_model_layers(args.paper_model)
+        weights = workload.he_normal_weights(layers, 4000 + args.paper_model)
+        det, _ = workload.make_inputs(d, T, B, 0.003, 0.003, 5000 + d)
+        cfg = dict(dtype="bf16", p=0.003, n_hidden=len(layers) - 1, width=layers[0][1])
+        grid = d
+    else:
+        cfg = workload.CONFIGS[args.workload]
+        d, T = cfg["d"], cfg["T"]
+        B = args.batch or cfg["batch"]
+        layers = workload.config_layers(args.workload)
+        weights = workload.config_weights(args.workload)
+        det, _ = workload.config_inputs(args.workload, B)
+        grid = d + 1
 
     torch.cuda.set_device(0)
-    pre = pdx.Predecoder(weights, d, T, layers, cfg["dtype"], max_batch=B)
+    if paper:
+        pre = pdx.Predecoder(weights, d, T, layers, "bf16", max_batch=B, layout="paper", first="Z", last="Z")
+    else:
+        pre = pdx.Predecoder(weights, d, T, layers, cfg["dtype"], max_batch=B)
     ddet = torch.from_numpy(det.view(np.int64)).cuda()
     flips = torch.empty((B, pre.flip_words), dtype=torch.int64, device="cuda")
     res = torch.empty((B, pre.det_words), dtype=torch.int64, device="cuda")
@@ -113,17 +134,19 @@ def main():
     # Per-stage HIP-event times on the same stream (unpack, each layer, head, residual).
     stages = pre.stage_times(ddet, flips, res, args.stage_iters, stream=stream)
     n = len(layers)
-    # hidden C->C layers whose epilogue writes activations (the last hidden
-    # layer also applies the head and is timed separately in stage_ms)
-    hidden = [i for i in range(1, n - 2) if layers[i][0] == layers[i][1]]
+    # hidden C->C layers whose epilogue writes activations (with a 1x1x1 head
+    # the last hidden layer also applies the head and is timed separately in
+    # stage_ms; a 3x3x3 output layer is a stage of its own)
+    last_hidden = n - 1 if layers[-1][2] == 3 else n - 2
+    hidden = [i for i in range(1, last_hidden) if layers[i][0] == layers[i][1]]
     conv_ms = float(np.mean([stages[1 + i] for i in hidden]))
     ci, co = layers[hidden[0]][0], layers[hidden[0]][1]
-    V = T * (d + 1) ** 2
+    V = T * grid ** 2
     conv_flops = 2.0 * ci * co * 27 * V * B
     achieved = conv_flops / (conv_ms * 1e-3) / 1e12
     print("stages ms:", ["%.3f" % s for s in stages], file=sys.stderr, flush=True)
 
-    total_flops = flops_per_sample(layers, d, T) * B
+    total_flops = flops_per_sample(layers, grid, T) * B
     rounds = B * T
     out = {
         "metric": "syndrome rounds/sec and us/round (pre-decode+residual) at d=13,T=13; MFMA %",
@@ -159,6 +182,32 @@ def main():
             "traffic": counted_traffic("conv_hidden_%dx%d_d%d_T%d_B%d_counters.md" % (ci, co, d, T, B)),
         },
     }
+
+    if paper:
+        # the paper times Table models at batch 1 (Table runtimes, GB300, FP8,
+        # TensorRT): 13^3 / 21^3 / 31^3 = 2.397 / 1.872 / 2.609 us/round for
+        # Model 1 and 3.252 / 2.703 / 3.774 for Model 4 -- another machine and
+        # precision, context only
+        ctx = {1: {13: 2.397, 21: 1.872, 31: 2.609}, 4: {13: 3.252, 21: 2.703, 31: 3.774}}
+        out.update({
+            "metric": "us/round (pre-decode+residual), Table models Model %d in the paper's layout at d=T=%d"
+                      % (args.paper_model, d),
+            "value": ms * 1e3 / rounds,
+            "unit": "us/round",
+            "higher_is_better": False,
+            "rounds_per_s": rounds / (ms * 1e-3),
+            "config": {"workload": "Model %d of Table models (%s), paper layout: D x D grid, 4 input channels, "
+                                   "3x3x3 output layer; d=T=%d, batch %d; bf16 / fp32 accumulate; p=q=0.003"
+                                   % (args.paper_model, layers, d, B),
+                       "d": d, "T": T, "batch": B, "model": args.paper_model},
+            "paper_context_us_per_round": ctx.get(args.paper_model, {}).get(d),
+        })
+        out["roofline"]["traffic"] = None
+        out["stage_ms"] = {"unpack": stages[0], **{"layer%d" % (i + 1): stages[1 + i] for i in range(n)},
+                           "residual_repack": stages[n + 1]}
+        pre.close()
+        print(json.dumps(out), flush=True)
+        return
 
     if not args.no_cpu_baseline:
         import oracle
