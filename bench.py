@@ -74,7 +74,7 @@ def main():
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="also run one plain device copy of this many MiB (calibrates HBM byte counters)")
     ap.add_argument("--paper-model", type=int, default=None,
-                    help="time a model of Table models (1 or 4) in the paper's own layout (D x D grid, four "
+                    help="time a model of Table models (1, 2, 4 or 5) in the paper's own layout (D x D grid, four "
                          "input channels, 3x3x3 output layer) at d = T = --d instead of a workload")
     ap.add_argument("--d", type=int, default=13, help="distance (and rounds) for --paper-model")
     args = ap.parse_args()
@@ -186,9 +186,10 @@ def main():
     if paper:
         # the paper times Table models at batch 1 (Table runtimes, GB300, FP8,
         # TensorRT): 13^3 / 21^3 / 31^3 = 2.397 / 1.872 / 2.609 us/round for
-        # Model 1 and 3.252 / 2.703 / 3.774 for Model 4 -- another machine and
-        # precision, context only
-        ctx = {1: {13: 2.397, 21: 1.872, 31: 2.609}, 4: {13: 3.252, 21: 2.703, 31: 3.774}}
+        # Model 1, 3.252 / 2.703 / 3.774 for Model 4 and 4.364 / 5.056 / 9.263
+        # for Model 5 -- another machine and precision, context only
+        ctx = {1: {13: 2.397, 21: 1.872, 31: 2.609}, 4: {13: 3.252, 21: 2.703, 31: 3.774},
+               5: {13: 4.364, 21: 5.056, 31: 9.263}}
         out.update({
             "metric": "us/round (pre-decode+residual), Table models Model %d in the paper's layout at d=T=%d"
                       % (args.paper_model, d),

@@ -32,6 +32,8 @@ struct pd_predecoder {
   uint8_t* nib = nullptr;        // [max_batch][T][H][H] flip nibbles
   int32_t* tables = nullptr;
   std::vector<void*> wdev;       // per conv layer: fragments (bf16) or [tap][ci][co] (fp32)
+  std::vector<size_t> wslice;    // per conv layer: bytes of the fragments of one 128-channel slice of a
+                                 // 256-wide layer (run as two slices), 0 otherwise
   std::vector<float*> bdev;      // per conv layer: bias fp32
   float* head_w = nullptr;       // [4][c_in] fp32 (bf16-valued on the bf16 path)
   float* head_b = nullptr;       // [4]
@@ -242,16 +244,21 @@ bool supported(const Geom& g, const pd_layer* l, int n, int dtype) {
   if (g.d > kMaxD || g.T > kMaxT) return false;
   if (n < 2) return false;  // at least one hidden 3x3x3 layer before the head
   if (g.layout == PD_LAYOUT_PAPER && dtype != PD_DTYPE_BF16) return false;
+  bool wide = false;
   for (int i = 0; i < n - 1; ++i) {
     if (l[i].k != 3) return false;
     int co = l[i].c_out;
     if (dtype == PD_DTYPE_BF16) {
-      if (co != 64 && co != 128) return false;
+      if (co != 64 && co != 128 && co != 256) return false;
+      wide = wide || co == 256;
     } else {
       if (co % 8 != 0 || co > 128) return false;
     }
   }
   const pd_layer& out = l[n - 1];
+  // 256-wide layers run as two 128-channel slices; a 1x1x1 head needs all
+  // channels of its input in one workgroup, so they go with a 3x3x3 output layer
+  if (wide && out.k != 3) return false;
   if (out.k == 3) return g.layout == PD_LAYOUT_PAPER;  // a 3x3x3 output layer (c_in 64 or 128, checked above)
   if (out.k != 1 || out.c_in > 128) return false;
   if (dtype == PD_DTYPE_BF16 && (out.c_in % 8) != 0) return false;
@@ -299,6 +306,7 @@ void free_all(pd_predecoder* h) {
   h->nib = nullptr;
   h->tables = nullptr;
   h->wdev.clear();
+  h->wslice.clear();
   h->bdev.clear();
   h->head_w = h->head_b = nullptr;
 }
@@ -386,14 +394,22 @@ pd_status enqueue_run(pd_predecoder* h, hipStream_t st, const uint64_t* det, int
       s = check_launch(pd::launch_conv_single(g, tl, L.c_out, L.act, x, h->wdev[l], h->bdev[l], h->head_w,
                                               h->head_b, h->tables, h->nib, logits, batch, h->n_cu, st));
       head_done = true;
-    } else if (l == 0) {
-      s = check_launch(pd::launch_conv_first(g, L.c_in, L.c_out, L.act, x, y, h->wdev[l], h->bdev[l], batch,
-                                             st));
-    } else {  // the last hidden layer may carry the head and the threshold in its epilogue
-      s = check_launch(pd::launch_conv_hidden(g, tl, L.c_in, L.c_out, L.act, x, y, h->wdev[l], h->bdev[l],
-                                              fuse_head ? 1 : 0, h->head_w, h->head_b, h->tables, h->nib,
-                                              logits, batch, hidden_wgs, st));
-      head_done = fuse_head;
+    } else {
+      // a 256-wide layer runs as two slices of 128 output channels over the
+      // same input (slice k: its fragments, biases and output channels)
+      const int nsl = h->wslice[l] ? 2 : 1, cw = L.c_out / nsl;
+      for (int k = 0; k < nsl && s == PD_OK; ++k) {
+        const void* wk = (const char*)h->wdev[l] + k * h->wslice[l];
+        void* yk = (uint16_t*)y + (size_t)k * cw;
+        if (l == 0)
+          s = check_launch(pd::launch_conv_first(g, L.c_in, cw, L.act, x, yk, L.c_out, wk, h->bdev[l] + k * cw,
+                                                 batch, st));
+        else  // the last hidden layer may carry the head and the threshold in its epilogue
+          s = check_launch(pd::launch_conv_hidden(g, tl, L.c_in, cw, L.act, x, yk, L.c_out, wk,
+                                                  h->bdev[l] + k * cw, fuse_head ? 1 : 0, h->head_w, h->head_b,
+                                                  h->tables, h->nib, logits, batch, hidden_wgs, st));
+      }
+      head_done = fuse_head && l > 0;
     }
     if (s != PD_OK) return s;
     x = y;
@@ -401,7 +417,7 @@ pd_status enqueue_run(pd_predecoder* h, hipStream_t st, const uint64_t* det, int
   if ((s = mark()) != PD_OK) return s;
   if (out3) {
     const pd_layer& L = h->layers[n - 1];
-    s = check_launch(pd::launch_conv_hidden(g, tl, L.c_in, L.c_out, L.act, x, nullptr, h->wdev[n - 1],
+    s = check_launch(pd::launch_conv_hidden(g, tl, L.c_in, L.c_out, L.act, x, nullptr, 0, h->wdev[n - 1],
                                             h->bdev[n - 1], 2, nullptr, nullptr, h->tables, h->nib, logits,
                                             batch, hidden_wgs, st));
   } else if (!head_done) {  // fp32, or a one-hidden-layer network on the paper's layout
@@ -550,6 +566,7 @@ pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d
       void* wd = nullptr;
       s = upload(&wd, f.data(), f.size() * 2);
       h->wdev.push_back(wd);
+      h->wslice.push_back(0);
       if (s != PD_OK) return fail(s);
       std::vector<float> bp(32, 0.0f);
       for (int o2 = 0; o2 < L.c_out; ++o2) bp[o2] = b[o2];
@@ -571,8 +588,17 @@ pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d
       break;
     }
     void* wd = nullptr;
+    size_t slice = 0;
     if (dtype == PD_DTYPE_BF16) {
-      std::vector<uint16_t> f = conv_fragments(w, L.c_in, L.c_out);
+      std::vector<uint16_t> f;
+      if (L.c_out == 256) {  // two slices of 128 output channels, back to back
+        f = conv_fragments(w, L.c_in, 128);
+        slice = f.size() * 2;
+        std::vector<uint16_t> f2 = conv_fragments(w + (size_t)128 * L.c_in * 27, L.c_in, 128);
+        f.insert(f.end(), f2.begin(), f2.end());
+      } else {
+        f = conv_fragments(w, L.c_in, L.c_out);
+      }
       s = upload(&wd, f.data(), f.size() * 2);
     } else {
       std::vector<float> r((size_t)27 * L.c_in * L.c_out);
@@ -583,6 +609,7 @@ pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d
       s = upload(&wd, r.data(), r.size() * 4);
     }
     h->wdev.push_back(wd);
+    h->wslice.push_back(slice);
     if (s != PD_OK) return fail(s);
     float* bd = nullptr;
     s = upload(&bd, b, (size_t)L.c_out * 4);

@@ -84,7 +84,7 @@ __device__ __forceinline__ void gather(const Geom& g, const void* __restrict__ p
 // then handles BPW consecutive 32-voxel blocks.
 template <int CIN, int COUT, int ACT>
 __global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, const void* __restrict__ planes,
-                                                                uint16_t* __restrict__ y,
+                                                                uint16_t* __restrict__ y, int ystride,
                                                                 const u32x4* __restrict__ wfrag,
                                                                 const float* __restrict__ bias, Decode dc,
                                                                 int nvox) {
@@ -155,7 +155,7 @@ __global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, const vo
       const int row = qq / GPR, c = qq % GPR;
       const int pr = ((__attribute__((address_space(3))) const int*)prow)[row];
       const u32x4 val = *(lds_u32x4*)(tile + row * OSTR + c * 16);
-      if (pr >= 0) *reinterpret_cast<u32x4*>(y + (long long)pr * COUT + c * 8) = val;
+      if (pr >= 0) *reinterpret_cast<u32x4*>(y + (long long)pr * ystride + c * 8) = val;
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);  // the tile's LDS reads are done before the next block writes it
     __builtin_amdgcn_wave_barrier();
@@ -164,7 +164,7 @@ __global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, const vo
 
 }  // namespace
 
-hipError_t launch_conv_first(const Geom& g, int cin, int cout, int act, const void* planes, void* y,
+hipError_t launch_conv_first(const Geom& g, int cin, int cout, int act, const void* planes, void* y, int ystride,
                              const void* wfrag, const float* bias, int batch, hipStream_t stream) {
   const long long nvox = (long long)batch * g.V;  // < 2^31 (host check)
   const long long nblk = (nvox + 32 * WAVES * BPW - 1) / (32 * WAVES * BPW);
@@ -176,7 +176,7 @@ hipError_t launch_conv_first(const Geom& g, int cin, int cout, int act, const vo
     constexpr int C = decltype(CO)::value, I = decltype(CI)::value;
     const size_t lds = (size_t)ksteps<I>() * (C / 32) * 64 * 16 + (size_t)WAVES * 32 * (C * 2 + 16 + 4);
     hipLaunchKernelGGL((conv_first_kernel<I, C, decltype(A)::value>), dim3((unsigned)nblk), dim3(64 * WAVES), lds,
-                       stream, g, planes, (uint16_t*)y, (const u32x4*)wfrag, bias, dc, (int)nvox);
+                       stream, g, planes, (uint16_t*)y, ystride, (const u32x4*)wfrag, bias, dc, (int)nvox);
   };
   if ((cin != 2 && cin != 4) || (cout != 64 && cout != 128) || act < 0 || act > 2) return hipErrorInvalidValue;
   with_activation(act, [&](auto A) {

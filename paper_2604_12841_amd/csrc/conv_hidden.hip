@@ -172,7 +172,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t stage_rsrc(const uint16_t* x, 
 template <int CIN, int COUT, int EPI, int MODE>
 __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, uint16_t* __restrict__ y,
-                   const u32x4* __restrict__ wfrag, const float* __restrict__ bias,
+                   int ystride, const u32x4* __restrict__ wfrag, const float* __restrict__ bias,
                    const float* __restrict__ head_w, const float* __restrict__ head_b,
                    const int32_t* __restrict__ tables, uint8_t* __restrict__ nib,
                    float* __restrict__ logits, int batch) {
@@ -431,7 +431,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
             const int r = gi >> 3, c = gi & 7;
             const u32x4 v = *(lds_u32x4*)(tb + r * 128 + ((c ^ (r & 7)) << 4));
             const int pr = __shfl(pidx[2 * ps + (it2 >> 2)], r & 31);
-            if (pr >= 0) *reinterpret_cast<u32x4*>(y + (long long)pr * COUT + wn * 64 + c * 8) = v;
+            if (pr >= 0) *reinterpret_cast<u32x4*>(y + (long long)pr * ystride + wn * 64 + c * 8) = v;
           }
           __builtin_amdgcn_s_waitcnt(0xc07f);  // the reads are done before the next pass writes
           __builtin_amdgcn_wave_barrier();
@@ -520,7 +520,8 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
 }
 
 template <int CIN, int COUT, int EPI, int MODE>
-hipError_t launch_one(const Geom& g, const Tiling& tl, int act, const void* x, void* y, const void* wfrag,
+hipError_t launch_one(const Geom& g, const Tiling& tl, int act, const void* x, void* y, int ystride,
+                      const void* wfrag,
                       const float* bias, const float* head_w, const float* head_b, const int32_t* tables,
                       uint8_t* nib, float* logits, int batch, int n_workgroups, hipStream_t stream) {
   static bool attr_set = false;
@@ -532,7 +533,7 @@ hipError_t launch_one(const Geom& g, const Tiling& tl, int act, const void* x, v
   }
   const long long nwg = conv_workgroups(tl.ntiles, n_workgroups);
   hipLaunchKernelGGL((conv_hidden_kernel<CIN, COUT, EPI, MODE>), dim3((unsigned)nwg), dim3(NT),
-                     (size_t)Lds<COUT>::total, stream, g, tl, act, (const uint16_t*)x, (uint16_t*)y,
+                     (size_t)Lds<COUT>::total, stream, g, tl, act, (const uint16_t*)x, (uint16_t*)y, ystride,
                      (const u32x4*)wfrag, bias, head_w, head_b, tables, nib, logits, batch);
   return hipGetLastError();
 }
@@ -542,17 +543,18 @@ hipError_t launch_one(const Geom& g, const Tiling& tl, int act, const void* x, v
 int conv_hidden_max_span() { return MAX_SPAN; }
 int conv_hidden_workgroups_per_cu() { return 2; }
 
-#define PD_HIDDEN_CASE(CI, CO, E)                                                                  \
-  if (cin == CI && cout == CO && head == E) {                                                     \
-    if (tl.mode == 0)                                                                              \
-      return launch_one<CI, CO, E, 0>(g, tl, act, x, y, wfrag, bias, head_w, head_b, tables, nib,   \
-                                      logits, batch, n_workgroups, stream);                        \
-    return launch_one<CI, CO, E, 1>(g, tl, act, x, y, wfrag, bias, head_w, head_b, tables, nib,     \
-                                    logits, batch, n_workgroups, stream);                          \
+#define PD_HIDDEN_CASE(CI, CO, E)                                                              \
+  if (cin == CI && cout == CO && head == E) {                                                 \
+    if (tl.mode == 0)                                                                          \
+      return launch_one<CI, CO, E, 0>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b, \
+                                      tables, nib, logits, batch, n_workgroups, stream);       \
+    return launch_one<CI, CO, E, 1>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b,   \
+                                    tables, nib, logits, batch, n_workgroups, stream);         \
   }
 
 hipError_t launch_conv_hidden(const Geom& g, const Tiling& tl, int cin, int cout, int act, const void* x,
-                              void* y, const void* wfrag, const float* bias, int head, const float* head_w,
+                              void* y, int ystride, const void* wfrag, const float* bias, int head,
+                              const float* head_w,
                               const float* head_b, const int32_t* tables, uint8_t* nib, float* logits,
                               int batch, int n_workgroups, hipStream_t stream) {
   if (tl.span <= 0 || tl.span > MAX_SPAN) return hipErrorInvalidValue;
@@ -560,6 +562,8 @@ hipError_t launch_conv_hidden(const Geom& g, const Tiling& tl, int cin, int cout
   PD_HIDDEN_CASE(128, 128, EPI_ACT)
   PD_HIDDEN_CASE(64, 128, EPI_ACT)
   PD_HIDDEN_CASE(128, 64, EPI_ACT)
+  PD_HIDDEN_CASE(256, 128, EPI_ACT)
+  PD_HIDDEN_CASE(256, 64, EPI_ACT)
   PD_HIDDEN_CASE(64, 64, EPI_HEAD)
   PD_HIDDEN_CASE(128, 128, EPI_HEAD)
   PD_HIDDEN_CASE(64, 128, EPI_HEAD)
@@ -567,6 +571,7 @@ hipError_t launch_conv_hidden(const Geom& g, const Tiling& tl, int cin, int cout
   if (cout == 4) cout = 32;  // the output layer's 4 filters fill one padded block
   PD_HIDDEN_CASE(64, 32, EPI_OUT)
   PD_HIDDEN_CASE(128, 32, EPI_OUT)
+  PD_HIDDEN_CASE(256, 32, EPI_OUT)
   return hipErrorInvalidValue;
 }
 

@@ -117,9 +117,11 @@ hipError_t launch_unpack(const Geom& g, const int32_t* tables, const uint64_t* d
 
 // The first 3x3x3 layer (c_in = 2 or 4, c_out = 64 or 128) when it is not
 // also the last hidden layer: planes [batch * S][c_in] bf16, weight fragments
-// [ceil(27 c_in / 16) k-steps][c_out / 32][64 lanes][8 bf16].
+// [ceil(27 c_in / 16) k-steps][c_out / 32][64 lanes][8 bf16].  Output voxel
+// rows are ystride channels apart (a wider layer is run as slices of c_out
+// channels, y pointing at the slice's first channel).
 hipError_t launch_conv_first(const Geom& g, int cin, int cout, int act, const void* planes, void* y,
-                             const void* wfrag, const float* bias, int batch, hipStream_t stream);
+                             int ystride, const void* wfrag, const float* bias, int batch, hipStream_t stream);
 
 // A network with one hidden layer: layer 1 (as launch_conv_first) with the
 // 1x1x1 head (head_w [4][cout] fp32, bf16-valued; head_b [4]) and the
@@ -131,8 +133,10 @@ hipError_t launch_conv_single(const Geom& g, const Tiling& tl, int cout, int act
                               int n_workgroups, hipStream_t stream);
 int conv_single_max_span();  // staged voxels a tile may need
 
-// A 3x3x3 bf16 layer on the zero-halo activations x (c_in in {64, 128}).
-//   head == 0: a hidden layer (c_out in {64, 128}) writing y;
+// A 3x3x3 bf16 layer on the zero-halo activations x (c_in in {64, 128, 256}).
+//   head == 0: a hidden layer (c_out in {64, 128}) writing y, whose voxel rows
+//              are ystride channels apart (a 256-wide layer runs as two slices
+//              of 128, y pointing at the slice's first channel);
 //   head == 1: a hidden layer whose epilogue applies the 1x1x1 head and the
 //              threshold as launch_conv_single does, instead of writing y;
 //   head == 2: the output layer itself (c_out = 4, no activation): its
@@ -141,9 +145,9 @@ int conv_single_max_span();  // staged voxels a tile may need
 // padded to 32 channels, bias to 32 values); n_workgroups =
 // conv_hidden_workgroups_per_cu() per CU.
 hipError_t launch_conv_hidden(const Geom& g, const Tiling& tl, int cin, int cout, int act, const void* x,
-                              void* y, const void* wfrag, const float* bias, int head, const float* head_w,
-                              const float* head_b, const int32_t* tables, uint8_t* nib, float* logits,
-                              int batch, int n_workgroups, hipStream_t stream);
+                              void* y, int ystride, const void* wfrag, const float* bias, int head,
+                              const float* head_w, const float* head_b, const int32_t* tables, uint8_t* nib,
+                              float* logits, int batch, int n_workgroups, hipStream_t stream);
 int conv_hidden_max_span();
 int conv_hidden_workgroups_per_cu();
 

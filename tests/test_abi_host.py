@@ -180,10 +180,13 @@ def test_create_ex_rejects_misuse(case):
     assert _create_ex(**args) == pdx.PD_ERR_INVALID_ARG
 
 
-@pytest.mark.parametrize("model,dtype", [(1, pdx.DTYPE_FP32), (2, pdx.DTYPE_BF16), (3, pdx.DTYPE_BF16)])
-def test_create_ex_unsupported_models(model, dtype):
-    # fp32 on the paper layout; width 256 (Model 2); 5x5x5 kernels (Model 3)
-    layers = workload.paper_model_layers(model)
+@pytest.mark.parametrize("layers,dtype", [
+    (workload.paper_model_layers(1), pdx.DTYPE_FP32),                  # fp32 on the paper layout
+    (workload.paper_model_layers(3), pdx.DTYPE_BF16),                  # 5x5x5 kernels (Model 3)
+    (workload.paper_layer_spec([256, 256, 4], [3, 3, 1]), pdx.DTYPE_BF16),  # width 256 with a 1x1x1 head
+    (workload.paper_layer_spec([192, 4], [3, 3]), pdx.DTYPE_BF16),     # width 192
+])
+def test_create_ex_unsupported_models(layers, dtype):
     w = np.zeros(pdx.weight_count(layers), np.float32)
     assert _create_ex(w, 5, 3, layers, pdx.LAYOUT_PAPER, dtype=dtype) == pdx.PD_ERR_UNSUPPORTED
 

@@ -45,6 +45,16 @@ def test_paper_models_3x3x3_output(cuda, d, T, B, filters):
     check(d, T, B, workload.paper_layer_spec(filters, [3] * len(filters)), seed=300 + d)
 
 
+@pytest.mark.parametrize("d,T,B,filters", [
+    (5, 3, 2, [256, 256, 4]),              # Model 2's widths
+    (5, 3, 1, [256] * 5 + [4]),           # Model 5's layer list
+    (7, 4, 2, [128, 256, 128, 4]),         # 128 -> 256 -> 128 slices
+    (9, 3, 1, [256, 64, 4]),               # 256 -> 64
+])
+def test_width_256_as_two_slices(cuda, d, T, B, filters):
+    check(d, T, B, workload.paper_layer_spec(filters, [3] * len(filters)), seed=380 + d + len(filters))
+
+
 def test_paper_model_on_box_tiles(cuda):
     # d = 31 gives box tiles (the 31 x 31 grid is too wide for flat ones)
     check(31, 3, 1, workload.paper_layer_spec([64, 64, 4], [3, 3, 3]), seed=331)
