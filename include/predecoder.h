@@ -75,7 +75,11 @@
  * Precision.  PD_DTYPE_BF16: weights and every conv/head input are rounded
  * to bf16 (round to nearest even), products are accumulated in fp32, biases
  * and the activation are fp32, logits are fp32.  PD_DTYPE_FP32: fp32 end to
- * end.  flip = (logit > 0); a logit of exactly 0 is no flip.
+ * end.  flip = (logit > 0); a logit of exactly 0 is no flip.  Results are
+ * bit-reproducible for a given handle and batch size; small batches split the
+ * conv K loops over several workgroups, so two batch sizes can differ in the
+ * fp32 summation order, and through an activation rounded to the other bf16
+ * neighbour, by up to a few 1e-3 in the logits.
  *
  * Supported shapes (others give PD_ERR_UNSUPPORTED): 3 <= d <= 63,
  * 1 <= T <= 1023; hidden layers k == 3; output layer k == 1, or k == 3 on

@@ -39,6 +39,8 @@ struct pd_predecoder {
   float* head_b = nullptr;       // [4]
   int cmax = 0;
   int n_cu = 256;                // compute units: one persistent conv workgroup each
+  float* partial = nullptr;      // split K loops of small batches: fp32 sums of up to max_units units
+  long long max_units = 0;
 };
 
 namespace {
@@ -302,6 +304,7 @@ void free_all(pd_predecoder* h) {
   for (float* p : h->bdev) f(p);
   f(h->head_w);
   f(h->head_b);
+  f(h->partial);
   h->planes = h->act[0] = h->act[1] = nullptr;
   h->nib = nullptr;
   h->tables = nullptr;
@@ -309,6 +312,7 @@ void free_all(pd_predecoder* h) {
   h->wslice.clear();
   h->bdev.clear();
   h->head_w = h->head_b = nullptr;
+  h->partial = nullptr;
 }
 
 // bf16 A fragments (weights) for v_mfma_f32_32x32x16_bf16: lane l of
@@ -369,6 +373,17 @@ pd_status enqueue_run(pd_predecoder* h, hipStream_t st, const uint64_t* det, int
   // epilogue on the bf16 path) or a 3x3x3 output layer of its own
   const bool out3 = h->layers[n - 1].k == 3;
   const int hidden_wgs = h->n_cu * pd::conv_hidden_workgroups_per_cu();
+  // Split a layer's K loop over 2^k workgroups per tile while tiles x parts
+  // stay within one unit per compute unit (small batches: a tile's K loop is
+  // then the layer's latency); parts must divide the layer's 16-channel
+  // chunks.  Past one unit per CU the parked fp32 sums cost more than the
+  // shorter loops gain.
+  auto split_for = [&](const Tiling& t, int cin) -> pd::Split_k {
+    pd::Split_k sk{0, h->partial, h->max_units};
+    while ((cin / 16) % (2 << sk.kshift) == 0 && (t.ntiles << (sk.kshift + 1)) <= h->max_units)
+      ++sk.kshift;
+    return sk;
+  };
   int e = 0;
   auto mark = [&]() -> pd_status {
     if (ev && hipEventRecord(ev[e++], st) != hipSuccess) return PD_ERR_DEVICE;
@@ -407,7 +422,8 @@ pd_status enqueue_run(pd_predecoder* h, hipStream_t st, const uint64_t* det, int
         else  // the last hidden layer may carry the head and the threshold in its epilogue
           s = check_launch(pd::launch_conv_hidden(g, tl, L.c_in, cw, L.act, x, yk, L.c_out, wk,
                                                   h->bdev[l] + k * cw, fuse_head ? 1 : 0, h->head_w, h->head_b,
-                                                  h->tables, h->nib, logits, batch, hidden_wgs, st));
+                                                  h->tables, h->nib, logits, batch, hidden_wgs,
+                                                  split_for(tl, L.c_in), st));
       }
       head_done = fuse_head && l > 0;
     }
@@ -419,7 +435,7 @@ pd_status enqueue_run(pd_predecoder* h, hipStream_t st, const uint64_t* det, int
     const pd_layer& L = h->layers[n - 1];
     s = check_launch(pd::launch_conv_hidden(g, tl, L.c_in, L.c_out, L.act, x, nullptr, 0, h->wdev[n - 1],
                                             h->bdev[n - 1], 2, nullptr, nullptr, h->tables, h->nib, logits,
-                                            batch, hidden_wgs, st));
+                                            batch, hidden_wgs, split_for(tl, L.c_in), st));
   } else if (!head_done) {  // fp32, or a one-hidden-layer network on the paper's layout
     s = check_launch(pd::launch_head(g, h->layers[n - 1].c_in, fp32, x, h->head_w, h->head_b, h->tables,
                                      h->nib, logits, batch, st));
@@ -547,6 +563,13 @@ pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d
   if ((s = dev_alloc(&h->act[0], vox * cmax * elem)) != PD_OK) return fail(s);
   if ((s = dev_alloc(&h->act[1], vox * cmax * elem)) != PD_OK) return fail(s);
   if ((s = dev_alloc(&h->nib, (size_t)max_batch * g.V)) != PD_OK) return fail(s);
+  if (dtype == PD_DTYPE_BF16) {
+    // parked fp32 sums of split K loops: room for one unit per compute unit
+    h->max_units = h->n_cu;
+    if ((s = dev_alloc(&h->partial, (size_t)h->max_units * pd::conv_hidden_partial_floats_per_unit() * 4)) !=
+        PD_OK)
+      return fail(s);
+  }
   std::vector<int32_t> tab = build_tables(g);
   if ((s = upload(&h->tables, tab.data(), tab.size() * sizeof(int32_t))) != PD_OK) return fail(s);
   if (hipMemset(h->planes, 0, vox * cin0 * elem) != hipSuccess ||

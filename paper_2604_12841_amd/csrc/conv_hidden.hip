@@ -91,8 +91,11 @@ __host__ __device__ inline int stage_slot(int q) {
 
 // Epilogue modes: the activations of a hidden layer, a hidden layer with the
 // 1x1x1 head fused in, or the 3x3x3 output layer itself (4 filters, padded to
-// one block of 32 MFMA rows).
-enum Epi { EPI_ACT = 0, EPI_HEAD = 1, EPI_OUT = 2 };
+// one block of 32 MFMA rows); EPI_PARK: one part of a split K loop, whose
+// fp32 sums are parked for split_finish_kernel.  Only EPI_PARK kernels split
+// (the others see a split of 1 at compile time and keep their registers for
+// the epilogue).
+enum Epi { EPI_ACT = 0, EPI_HEAD = 1, EPI_OUT = 2, EPI_PARK = 3 };
 
 // Wave split of the 256 x COUT output tile: WN waves across the channels
 // (NB blocks of 32 each: 2, or 1 for the 32-row output layer), WM across the
@@ -175,7 +178,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
                    int ystride, const u32x4* __restrict__ wfrag, const float* __restrict__ bias,
                    const float* __restrict__ head_w, const float* __restrict__ head_b,
                    const int32_t* __restrict__ tables, uint8_t* __restrict__ nib,
-                   float* __restrict__ logits, int batch) {
+                   float* __restrict__ logits, int batch, int kshift_arg, float* __restrict__ partial) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   using W = Split<COUT>;
   using L = Lds<COUT>;
@@ -183,13 +186,20 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
   constexpr int NB = W::NB;
   constexpr int NBT = COUT / 32;  // 32-channel blocks in total
   constexpr int NCHUNK = CIN / KC;
-  constexpr int TSTEPS = NCHUNK * STEPS;  // k-steps per tile
-  static_assert(TSTEPS % BRING == 0, "the weight ring lines up with tile boundaries");
+  constexpr int TSTEPS = NCHUNK * STEPS;  // k-steps of the layer
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave % W::WM, wn = wave / W::WM;
   const int half = lane >> 5, l32 = lane & 31;
   const int ntiles = (int)tl.ntiles;
   const long long limit = (long long)batch * g.S;
+  // Work units: (tile, part); part p of a tile runs its chunks [p NCU, (p+1) NCU)
+  // with ksplit = 2^kshift parts per tile (EPI_PARK only: small batches).
+  // With parts, each unit parks its fp32 sums in `partial` (unit u at
+  // u * 256 * COUT floats) and split_finish_kernel does the epilogue.
+  const int kshift = EPI == EPI_PARK ? kshift_arg : 0;
+  const int ksplit = 1 << kshift;
+  const int NCU = NCHUNK >> kshift;  // chunks per unit
+  const int nunits = ntiles << kshift;
 
   lds_char* const lds = (lds_char*)smem;
   lds_char* const zero = lds + L::zero;
@@ -201,8 +211,169 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
   if (EPI == EPI_HEAD)
     for (int e = tid; e < 4 * COUT; e += NT) headw_s[e] = head_w[e];
 
-  int tile = tile_of(blockIdx.x, gridDim.x, 0, ntiles);
-  if (tile < 0) return;
+  // Bias, activation and output of one tile from its accumulators (lane
+  // holds channels co .. co + 3, co = 64 wn + 32 nb + 8 q + 4 half, of voxel
+  // row wm ROWS + 32 mb + l32); ebuf: a staging buffer free for the
+  // transposition / head partials.
+  auto finish_tile = [&](int tile, lds_char* const ebuf, f32x16 (&acc)[MB][NB]) {
+      // output row of each row block (recomputed: not kept live through the K loop)
+      int pidx[MB];
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        long long p = -1, o;
+        int lb;
+        pidx[mb] = tile_row(g, tl, tile, wm * W::ROWS + mb * 32 + l32, batch, &p, &lb, &o) ? (int)p : -1;
+      }
+
+      // ---- epilogue: lane holds channels co .. co + 3 (co = 64 wn + 32 nb +
+      // 8 q + 4 half) of voxel row wm ROWS + 32 mb + l32 ----
+      if constexpr (EPI == EPI_OUT) {
+        // the output layer: rows 0..3 of the channel block are the four logits
+        // (+ bias, no activation), held by the lanes of the first half-wave
+        if (half == 0) {
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) {
+            int b, t, i, j;
+            if (tile_row_coords(g, tl, tile, wm * W::ROWS + mb * 32 + l32, batch, &b, &t, &i, &j)) {
+              const float lg[4] = {acc[mb][0][0] + bias_s[0], acc[mb][0][1] + bias_s[1], acc[mb][0][2] + bias_s[2],
+                                   acc[mb][0][3] + bias_s[3]};
+              const int HH = g.H * g.H;
+              const int s = i * g.H + j;
+              nib[(long long)b * g.V + (long long)t * HH + s] = (uint8_t)flip_nibble(g, tables, i, j, lg);
+              if (logits) {
+#pragma unroll
+                for (int o = 0; o < 4; ++o) logits[(((long long)b * 4 + o) * g.T + t) * HH + s] = lg[o];
+              }
+            }
+          }
+        }
+      } else if constexpr (EPI == EPI_ACT) {
+        // bias + activation + bf16, transposed through this wave's slice of
+        // the staging buffer the tile read last (64 rows x 128 bytes, granule
+        // c of row r at c ^ (r % 8)), then stored as whole 128-byte halves of
+        // voxel rows, 8 rows per instruction.  The next tile's first staging
+        // store waits at a barrier until every wave is done here.
+        lds_char* const tb = ebuf + wave * (64 * 128);
+        with_activation(act, [&](auto A) {
+          constexpr int ACT = decltype(A)::value;
+#pragma unroll
+          for (int ps = 0; ps < MB / 2; ++ps) {
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+              for (int q = 0; q < 4; ++q) {
+                const int c = nb * 4 + q;  // 16-byte granule of the wave's 64 channels
+                const int co = wn * 64 + c * 8 + half * 4;
+                const float4 bv = {bias_s[co], bias_s[co + 1], bias_s[co + 2], bias_s[co + 3]};
+#pragma unroll
+                for (int m = 0; m < 2; ++m) {
+                  const int mb = 2 * ps + m;
+                  const float v0 = act_fn<ACT>(acc[mb][nb][4 * q + 0] + bv.x);
+                  const float v1 = act_fn<ACT>(acc[mb][nb][4 * q + 1] + bv.y);
+                  const float v2 = act_fn<ACT>(acc[mb][nb][4 * q + 2] + bv.z);
+                  const float v3 = act_fn<ACT>(acc[mb][nb][4 * q + 3] + bv.w);
+                  u32x2 packed;
+                  packed.x = bf16_pack(v0, v1);
+                  packed.y = bf16_pack(v2, v3);
+                  const int r = m * 32 + l32;
+                  *(lds_u32x2_w*)(tb + r * 128 + ((c ^ (r & 7)) << 4) + half * 8) = packed;
+                }
+              }
+            __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's rows are in LDS
+            __builtin_amdgcn_wave_barrier();
+#pragma unroll
+            for (int it2 = 0; it2 < 8; ++it2) {
+              const int gi = it2 * 64 + lane;
+              const int r = gi >> 3, c = gi & 7;
+              const u32x4 v = *(lds_u32x4*)(tb + r * 128 + ((c ^ (r & 7)) << 4));
+              const int pr = __shfl(pidx[2 * ps + (it2 >> 2)], r & 31);
+              if (pr >= 0) *reinterpret_cast<u32x4*>(y + (long long)pr * ystride + wn * 64 + c * 8) = v;
+            }
+            __builtin_amdgcn_s_waitcnt(0xc07f);  // the reads are done before the next pass writes
+            __builtin_amdgcn_wave_barrier();
+          }
+        });
+      } else {
+        // 1x1x1 head on the bf16-rounded activations: partial sums over this
+        // lane's channels, then over the half-waves, then over the channel
+        // waves through LDS (the buffer this tile read last)
+        lds_float* const head_part = (lds_float*)(ebuf);  // [WN][256][4]
+        float part[MB][4];
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int o = 0; o < 4; ++o) part[mb][o] = 0.0f;
+        with_activation(act, [&](auto A) {
+          constexpr int ACT = decltype(A)::value;
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int co = (wn * NB + nb) * 32 + q * 8 + half * 4;
+              const float4 bv = {bias_s[co], bias_s[co + 1], bias_s[co + 2], bias_s[co + 3]};
+              float4 hw[4];
+#pragma unroll
+              for (int o = 0; o < 4; ++o)
+                hw[o] = {headw_s[o * COUT + co], headw_s[o * COUT + co + 1], headw_s[o * COUT + co + 2],
+                         headw_s[o * COUT + co + 3]};
+#pragma unroll
+              for (int mb = 0; mb < MB; ++mb) {
+                const float a0 = bf16_round(act_fn<ACT>(acc[mb][nb][4 * q + 0] + bv.x));
+                const float a1 = bf16_round(act_fn<ACT>(acc[mb][nb][4 * q + 1] + bv.y));
+                const float a2 = bf16_round(act_fn<ACT>(acc[mb][nb][4 * q + 2] + bv.z));
+                const float a3 = bf16_round(act_fn<ACT>(acc[mb][nb][4 * q + 3] + bv.w));
+#pragma unroll
+                for (int o = 0; o < 4; ++o)
+                  part[mb][o] += hw[o].x * a0 + hw[o].y * a1 + hw[o].z * a2 + hw[o].w * a3;
+              }
+            }
+        });
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int o = 0; o < 4; ++o) part[mb][o] += __shfl_xor(part[mb][o], 32);
+        if (half == 0) {
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) {
+            lds_float* hp = head_part + (wn * kTileRows + wm * W::ROWS + mb * 32 + l32) * 4;
+            hp[0] = part[mb][0];
+            hp[1] = part[mb][1];
+            hp[2] = part[mb][2];
+            hp[3] = part[mb][3];
+          }
+        }
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): partials written
+        __builtin_amdgcn_s_barrier();
+        // one thread per voxel row: logits, threshold, flip nibble
+        static_assert(NT == kTileRows, "one thread per tile row");
+        {
+          const int r = tid;
+          int b, t, i, j;
+          if (tile_row_coords(g, tl, tile, r, batch, &b, &t, &i, &j)) {
+            float lg[4] = {head_b[0], head_b[1], head_b[2], head_b[3]};
+#pragma unroll
+            for (int w2 = 0; w2 < W::WN; ++w2) {
+              const lds_float* hp = head_part + (w2 * kTileRows + r) * 4;
+              lg[0] += hp[0];
+              lg[1] += hp[1];
+              lg[2] += hp[2];
+              lg[3] += hp[3];
+            }
+            const int HH = g.H * g.H;
+            const int s = i * g.H + j;
+            nib[(long long)b * g.V + (long long)t * HH + s] = (uint8_t)flip_nibble(g, tables, i, j, lg);
+            if (logits) {
+#pragma unroll
+              for (int o = 0; o < 4; ++o) logits[(((long long)b * 4 + o) * g.T + t) * HH + s] = lg[o];
+            }
+          }
+        }
+      }
+  };
+
+  int unit = tile_of(blockIdx.x, gridDim.x, 0, nunits);
+  if (unit < 0) return;
+  int tile = unit >> kshift;
 
   auto source_of = [&](int t) {
     StageSrc src;
@@ -222,7 +393,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
 
   // First tile: stage its first chunk synchronously.
   {
-    const __amdgpu_buffer_rsrc_t rs = stage_rsrc<CIN>(x, cur_base, 0);
+    const __amdgpu_buffer_rsrc_t rs = stage_rsrc<CIN>(x, cur_base, (unit & (ksplit - 1)) * NCU * KC);
 #pragma unroll
     for (int k = 0; k < RMAX; ++k) {
       const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(rs, soff[k], 0, 0);
@@ -239,17 +410,21 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
   auto wload = [&](int gs, int nb) -> u32x4 {
     return __builtin_amdgcn_raw_buffer_load_b128(wres, woff, (gs * NBT + nb) * 1024, 0);
   };
-  // weight-fragment ring: slot k holds tile-step gs, gs % BRING == k
+  // weight-fragment ring: slot k holds the k-step gs (of the layer's
+  // NCHUNK x 27), gs % BRING == k
   u32x4 bq[BRING][NB];
 #pragma unroll
   for (int st = 0; st < BRING - 1; ++st)
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) bq[st][nb] = wload(st, nb);
+    for (int nb = 0; nb < NB; ++nb) bq[st][nb] = wload((unit & (ksplit - 1)) * NCU * STEPS + st, nb);
   __syncthreads();  // staged chunk, bias, zero region and head weights visible
 
   int gchunk = 0;  // chunks processed by this workgroup (selects the LDS buffer)
-  for (int it = 0; tile >= 0; ++it) {
-    const int next = tile_of(blockIdx.x, gridDim.x, it + 1, ntiles);
+  for (int it = 0; unit >= 0; ++it) {
+    const int c0 = (unit & (ksplit - 1)) * NCU;  // first chunk of this unit
+    const int next_unit = tile_of(blockIdx.x, gridDim.x, it + 1, nunits);
+    const int next = next_unit >= 0 ? next_unit >> kshift : -1;
+    const int next_c0 = next_unit >= 0 ? (next_unit & (ksplit - 1)) * NCU : 0;
     const StageSrc next_src = source_of(next >= 0 ? next : tile);
     const long long next_base = stage_base<MODE>(g, next_src);
     // rows of this lane: voxel wm ROWS + 32 mb + l32 of the tile; LDS
@@ -275,17 +450,18 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[mb][nb][v] = 0.0f;
 
-    for (int chunk = 0; chunk < NCHUNK; ++chunk, ++gchunk) {
+    for (int chunk = 0; chunk < NCU; ++chunk, ++gchunk) {
       lds_char* const cur = lds + (gchunk & 1) * ABUF;
       lds_char* const oth = lds + ((gchunk + 1) & 1) * ABUF;
-      // the chunk staged next: the following chunk of this tile, else the
-      // first chunk of the next tile, else nothing
-      const bool more = chunk + 1 < NCHUNK;
+      const int cc = c0 + chunk;  // the channel chunk this step loop reads
+      // the chunk staged next: the following chunk of this unit, else the
+      // first chunk of the next unit, else nothing
+      const bool more = chunk + 1 < NCU;
       const int sspan = (more || next >= 0) ? tl.span : 0;  // staged voxels of the chunk staged next
       // the next tile's offsets replace soff round by round during the
       // last chunk (past the last tile: none, every granule empty)
       const __amdgpu_buffer_rsrc_t srs =
-          more ? stage_rsrc<CIN>(x, cur_base, (chunk + 1) * KC) : stage_rsrc<CIN>(x, next_base, 0);
+          more ? stage_rsrc<CIN>(x, cur_base, (cc + 1) * KC) : stage_rsrc<CIN>(x, next_base, next_c0 * KC);
       u32x4 stg;
 
       uint32_t rbase[MB];
@@ -317,12 +493,14 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
       u32x4 av[MB];
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) av[mb] = frag_read(mb, 0);
-      const int gbase = chunk * STEPS;  // tile-step of this chunk's step 0
+      const int gbase = cc * STEPS;              // k-step of this chunk's step 0
+      const int nbase = next_c0 * STEPS - STEPS;  // ... of the next unit's first chunk, minus STEPS
 #pragma unroll
       for (int st = 0; st < STEPS; ++st) {
         {
-          int gs = gbase + st + BRING - 1;  // wraps into the next tile's steps
-          if (gs >= TSTEPS) gs -= TSTEPS;
+          // past the chunk's last step, the last chunk of a unit runs on
+          // into the next unit's first steps
+          const int gs = (st + BRING - 1 < STEPS || more ? gbase : nbase) + st + BRING - 1;
 #pragma unroll
           for (int nb = 0; nb < NB; ++nb) bq[(st + BRING - 1) % BRING][nb] = wload(gs, nb);
         }
@@ -360,170 +538,115 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
       __builtin_amdgcn_s_barrier();
     }
 
-    // output row of each row block (recomputed: not kept live through the K loop)
-    int pidx[MB];
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-      long long p = -1, o;
-      int lb;
-      pidx[mb] = tile_row(g, tl, tile, wm * W::ROWS + mb * 32 + l32, batch, &p, &lb, &o) ? (int)p : -1;
-    }
-
-    // ---- epilogue: lane holds channels co .. co + 3 (co = 64 wn + 32 nb +
-    // 8 q + 4 half) of voxel row wm ROWS + 32 mb + l32 ----
-    if constexpr (EPI == EPI_OUT) {
-      // the output layer: rows 0..3 of the channel block are the four logits
-      // (+ bias, no activation), held by the lanes of the first half-wave
-      if (half == 0) {
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb) {
-          int b, t, i, j;
-          if (tile_row_coords(g, tl, tile, wm * W::ROWS + mb * 32 + l32, batch, &b, &t, &i, &j)) {
-            const float lg[4] = {acc[mb][0][0] + bias_s[0], acc[mb][0][1] + bias_s[1], acc[mb][0][2] + bias_s[2],
-                                 acc[mb][0][3] + bias_s[3]};
-            const int HH = g.H * g.H;
-            const int s = i * g.H + j;
-            nib[(long long)b * g.V + (long long)t * HH + s] = (uint8_t)flip_nibble(g, tables, i, j, lg);
-            if (logits) {
-#pragma unroll
-              for (int o = 0; o < 4; ++o) logits[(((long long)b * 4 + o) * g.T + t) * HH + s] = lg[o];
-            }
-          }
-        }
-      }
-    } else if constexpr (EPI == EPI_ACT) {
-      // bias + activation + bf16, transposed through this wave's slice of
-      // the staging buffer the tile read last (64 rows x 128 bytes, granule
-      // c of row r at c ^ (r % 8)), then stored as whole 128-byte halves of
-      // voxel rows, 8 rows per instruction.  The next tile's first staging
-      // store waits at a barrier until every wave is done here.
-      lds_char* const tb = lds + ((gchunk - 1) & 1) * ABUF + wave * (64 * 128);
-      with_activation(act, [&](auto A) {
-        constexpr int ACT = decltype(A)::value;
-#pragma unroll
-        for (int ps = 0; ps < MB / 2; ++ps) {
-#pragma unroll
-          for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const int c = nb * 4 + q;  // 16-byte granule of the wave's 64 channels
-              const int co = wn * 64 + c * 8 + half * 4;
-              const float4 bv = {bias_s[co], bias_s[co + 1], bias_s[co + 2], bias_s[co + 3]};
-#pragma unroll
-              for (int m = 0; m < 2; ++m) {
-                const int mb = 2 * ps + m;
-                const float v0 = act_fn<ACT>(acc[mb][nb][4 * q + 0] + bv.x);
-                const float v1 = act_fn<ACT>(acc[mb][nb][4 * q + 1] + bv.y);
-                const float v2 = act_fn<ACT>(acc[mb][nb][4 * q + 2] + bv.z);
-                const float v3 = act_fn<ACT>(acc[mb][nb][4 * q + 3] + bv.w);
-                u32x2 packed;
-                packed.x = bf16_pack(v0, v1);
-                packed.y = bf16_pack(v2, v3);
-                const int r = m * 32 + l32;
-                *(lds_u32x2_w*)(tb + r * 128 + ((c ^ (r & 7)) << 4) + half * 8) = packed;
-              }
-            }
-          __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's rows are in LDS
-          __builtin_amdgcn_wave_barrier();
-#pragma unroll
-          for (int it2 = 0; it2 < 8; ++it2) {
-            const int gi = it2 * 64 + lane;
-            const int r = gi >> 3, c = gi & 7;
-            const u32x4 v = *(lds_u32x4*)(tb + r * 128 + ((c ^ (r & 7)) << 4));
-            const int pr = __shfl(pidx[2 * ps + (it2 >> 2)], r & 31);
-            if (pr >= 0) *reinterpret_cast<u32x4*>(y + (long long)pr * ystride + wn * 64 + c * 8) = v;
-          }
-          __builtin_amdgcn_s_waitcnt(0xc07f);  // the reads are done before the next pass writes
-          __builtin_amdgcn_wave_barrier();
-        }
-      });
-    } else {
-      // 1x1x1 head on the bf16-rounded activations: partial sums over this
-      // lane's channels, then over the half-waves, then over the channel
-      // waves through LDS (the buffer this tile read last)
-      lds_float* const head_part = (lds_float*)(lds + ((gchunk - 1) & 1) * ABUF);  // [WN][256][4]
-      float part[MB][4];
+    if constexpr (EPI == EPI_PARK) {
+      // split K loop: park this unit's fp32 sums as [tile row][channel]; a
+      // second kernel adds a tile's parts and applies the epilogue
+      float* const mine = partial + (size_t)unit * kTileRows * COUT;
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-        for (int o = 0; o < 4; ++o) part[mb][o] = 0.0f;
-      with_activation(act, [&](auto A) {
-        constexpr int ACT = decltype(A)::value;
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            const int co = (wn * NB + nb) * 32 + q * 8 + half * 4;
-            const float4 bv = {bias_s[co], bias_s[co + 1], bias_s[co + 2], bias_s[co + 3]};
-            float4 hw[4];
-#pragma unroll
-            for (int o = 0; o < 4; ++o)
-              hw[o] = {headw_s[o * COUT + co], headw_s[o * COUT + co + 1], headw_s[o * COUT + co + 2],
-                       headw_s[o * COUT + co + 3]};
-#pragma unroll
-            for (int mb = 0; mb < MB; ++mb) {
-              const float a0 = bf16_round(act_fn<ACT>(acc[mb][nb][4 * q + 0] + bv.x));
-              const float a1 = bf16_round(act_fn<ACT>(acc[mb][nb][4 * q + 1] + bv.y));
-              const float a2 = bf16_round(act_fn<ACT>(acc[mb][nb][4 * q + 2] + bv.z));
-              const float a3 = bf16_round(act_fn<ACT>(acc[mb][nb][4 * q + 3] + bv.w));
-#pragma unroll
-              for (int o = 0; o < 4; ++o)
-                part[mb][o] += hw[o].x * a0 + hw[o].y * a1 + hw[o].z * a2 + hw[o].w * a3;
-            }
+            const int row = wm * W::ROWS + mb * 32 + l32, co = (wn * NB + nb) * 32 + q * 8 + half * 4;
+            *reinterpret_cast<float4*>(mine + row * COUT + co) =
+                float4{acc[mb][nb][4 * q], acc[mb][nb][4 * q + 1], acc[mb][nb][4 * q + 2], acc[mb][nb][4 * q + 3]};
           }
-      });
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-        for (int o = 0; o < 4; ++o) part[mb][o] += __shfl_xor(part[mb][o], 32);
-      if (half == 0) {
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb) {
-          lds_float* hp = head_part + (wn * kTileRows + wm * W::ROWS + mb * 32 + l32) * 4;
-          hp[0] = part[mb][0];
-          hp[1] = part[mb][1];
-          hp[2] = part[mb][2];
-          hp[3] = part[mb][3];
-        }
-      }
-      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): partials written
-      __builtin_amdgcn_s_barrier();
-      // one thread per voxel row: logits, threshold, flip nibble
-      static_assert(NT == kTileRows, "one thread per tile row");
-      {
-        const int r = tid;
-        int b, t, i, j;
-        if (tile_row_coords(g, tl, tile, r, batch, &b, &t, &i, &j)) {
-          float lg[4] = {head_b[0], head_b[1], head_b[2], head_b[3]};
-#pragma unroll
-          for (int w2 = 0; w2 < W::WN; ++w2) {
-            const lds_float* hp = head_part + (w2 * kTileRows + r) * 4;
-            lg[0] += hp[0];
-            lg[1] += hp[1];
-            lg[2] += hp[2];
-            lg[3] += hp[3];
-          }
-          const int HH = g.H * g.H;
-          const int s = i * g.H + j;
-          nib[(long long)b * g.V + (long long)t * HH + s] = (uint8_t)flip_nibble(g, tables, i, j, lg);
-          if (logits) {
-#pragma unroll
-            for (int o = 0; o < 4; ++o) logits[(((long long)b * 4 + o) * g.T + t) * HH + s] = lg[o];
-          }
-        }
-      }
+    } else {
+      finish_tile(tile, lds + ((gchunk - 1) & 1) * ABUF, acc);
     }
+    unit = next_unit;
     tile = next;
     cur_base = next_base;
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
+// Second kernel of a split K loop: one thread per (tile row, 8 channels)
+// (activations) or per tile row (head, output layer) adds the tile's parts
+// in part order, then applies the epilogue of the unsplit kernel: bias,
+// activation, bf16 and a 16-byte store; or bias, activation, bf16 rounding,
+// the 1x1x1 head and the threshold; or, for the output layer, bias and the
+// threshold.
+template <int EPI, int ACT>
+__global__ void __launch_bounds__(256) split_finish_kernel(Geom g, Tiling tl, int cout, int kshift,
+                                                           const float* __restrict__ partial,
+                                                           const float* __restrict__ bias, uint16_t* __restrict__ y,
+                                                           int ystride, const float* __restrict__ head_w,
+                                                           const float* __restrict__ head_b,
+                                                           const int32_t* __restrict__ tables,
+                                                           uint8_t* __restrict__ nib, float* __restrict__ logits,
+                                                           int batch) {
+  const int groups = EPI == EPI_ACT ? cout / 8 : 1;
+  const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (gid >= tl.ntiles * kTileRows * groups) return;
+  const int tile = (int)(gid / (kTileRows * groups));
+  const int rem = (int)(gid - (long long)tile * kTileRows * groups);
+  const int r = rem / groups, grp = rem - r * groups;
+  const int ksplit = 1 << kshift;
+  // sum of channels c .. c + 7 of this row over the tile's parts, part order
+  auto sum8 = [&](int c, float (&v)[8]) {
+    for (int p = 0; p < ksplit; ++p) {
+      const float* src = partial + ((size_t)((tile << kshift) + p) * kTileRows + r) * cout + c;
+      const float4 a = *reinterpret_cast<const float4*>(src);
+      const float4 b = *reinterpret_cast<const float4*>(src + 4);
+      const float t[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = p == 0 ? t[e] : v[e] + t[e];
+    }
+  };
+  if constexpr (EPI == EPI_ACT) {
+    long long pidx, o;
+    int lb;
+    if (!tile_row(g, tl, tile, r, batch, &pidx, &lb, &o)) return;
+    float v[8];
+    sum8(grp * 8, v);
+    uint32_t w[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      w[e] = bf16_pack(act_fn<ACT>(v[2 * e] + bias[grp * 8 + 2 * e]),
+                       act_fn<ACT>(v[2 * e + 1] + bias[grp * 8 + 2 * e + 1]));
+    *reinterpret_cast<uint4*>(y + pidx * ystride + grp * 8) = uint4{w[0], w[1], w[2], w[3]};
+  } else {
+    int b, t, i, j;
+    if (!tile_row_coords(g, tl, tile, r, batch, &b, &t, &i, &j)) return;
+    float lg[4];
+    if constexpr (EPI == EPI_OUT) {
+      float v[8];
+      sum8(0, v);
+#pragma unroll
+      for (int o2 = 0; o2 < 4; ++o2) lg[o2] = v[o2] + bias[o2];
+    } else {
+#pragma unroll
+      for (int o2 = 0; o2 < 4; ++o2) lg[o2] = head_b[o2];
+      for (int c = 0; c < cout; c += 8) {
+        float v[8];
+        sum8(c, v);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float a = bf16_round(act_fn<ACT>(v[e] + bias[c + e]));
+#pragma unroll
+          for (int o2 = 0; o2 < 4; ++o2) lg[o2] += head_w[o2 * cout + c + e] * a;
+        }
+      }
+    }
+    const int HH = g.H * g.H;
+    const int s = i * g.H + j;
+    nib[(long long)b * g.V + (long long)t * HH + s] = (uint8_t)flip_nibble(g, tables, i, j, lg);
+    if (logits) {
+#pragma unroll
+      for (int o2 = 0; o2 < 4; ++o2) logits[(((long long)b * 4 + o2) * g.T + t) * HH + s] = lg[o2];
+    }
+  }
+}
+
+// Launches one instance of the hidden kernel (the LDS size attribute set on
+// its first use).
 template <int CIN, int COUT, int EPI, int MODE>
-hipError_t launch_one(const Geom& g, const Tiling& tl, int act, const void* x, void* y, int ystride,
-                      const void* wfrag,
-                      const float* bias, const float* head_w, const float* head_b, const int32_t* tables,
-                      uint8_t* nib, float* logits, int batch, int n_workgroups, hipStream_t stream) {
+hipError_t launch_hidden(const Geom& g, const Tiling& tl, int act, const void* x, void* y, int ystride,
+                         const void* wfrag, const float* bias, const float* head_w, const float* head_b,
+                         const int32_t* tables, uint8_t* nib, float* logits, int batch, int n_workgroups,
+                         int kshift, float* partial, hipStream_t stream) {
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute((const void*)conv_hidden_kernel<CIN, COUT, EPI, MODE>,
@@ -531,33 +654,63 @@ hipError_t launch_one(const Geom& g, const Tiling& tl, int act, const void* x, v
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  const long long nwg = conv_workgroups(tl.ntiles, n_workgroups);
+  const long long nwg = conv_workgroups(tl.ntiles << kshift, n_workgroups);
   hipLaunchKernelGGL((conv_hidden_kernel<CIN, COUT, EPI, MODE>), dim3((unsigned)nwg), dim3(NT),
                      (size_t)Lds<COUT>::total, stream, g, tl, act, (const uint16_t*)x, (uint16_t*)y, ystride,
-                     (const u32x4*)wfrag, bias, head_w, head_b, tables, nib, logits, batch);
+                     (const u32x4*)wfrag, bias, head_w, head_b, tables, nib, logits, batch, kshift, partial);
+  return hipSuccess;
+}
+
+template <int CIN, int COUT, int EPI, int MODE>
+hipError_t launch_one(const Geom& g, const Tiling& tl, int act, const void* x, void* y, int ystride,
+                      const void* wfrag, const float* bias, const float* head_w, const float* head_b,
+                      const int32_t* tables, uint8_t* nib, float* logits, int batch, int n_workgroups,
+                      const Split_k& sk, hipStream_t stream) {
+  hipError_t e;
+  if (sk.kshift == 0) {
+    e = launch_hidden<CIN, COUT, EPI, MODE>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b, tables, nib,
+                                            logits, batch, n_workgroups, 0, nullptr, stream);
+    return e != hipSuccess ? e : hipGetLastError();
+  }
+  // K loops split: park the parts, then add them and finish the tiles
+  e = launch_hidden<CIN, COUT, EPI_PARK, MODE>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b, tables, nib,
+                                               logits, batch, n_workgroups, sk.kshift, sk.partial, stream);
+  if (e != hipSuccess) return e;
+  const long long threads = tl.ntiles * kTileRows * (EPI == EPI_ACT ? COUT / 8 : 1);
+  with_activation(act, [&](auto A) {
+    hipLaunchKernelGGL((split_finish_kernel<EPI, decltype(A)::value>), dim3((unsigned)((threads + 255) / 256)),
+                       dim3(256), 0, stream, g, tl, COUT, sk.kshift, sk.partial, bias, (uint16_t*)y, ystride, head_w,
+                       head_b, tables, nib, logits, batch);
+  });
   return hipGetLastError();
 }
 
 }  // namespace
 
 int conv_hidden_max_span() { return MAX_SPAN; }
+size_t conv_hidden_partial_floats_per_unit() { return (size_t)kTileRows * 128; }
 int conv_hidden_workgroups_per_cu() { return 2; }
 
 #define PD_HIDDEN_CASE(CI, CO, E)                                                              \
   if (cin == CI && cout == CO && head == E) {                                                 \
     if (tl.mode == 0)                                                                          \
       return launch_one<CI, CO, E, 0>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b, \
-                                      tables, nib, logits, batch, n_workgroups, stream);       \
+                                      tables, nib, logits, batch, n_workgroups, sk, stream);   \
     return launch_one<CI, CO, E, 1>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b,   \
-                                    tables, nib, logits, batch, n_workgroups, stream);         \
+                                    tables, nib, logits, batch, n_workgroups, sk, stream);     \
   }
 
 hipError_t launch_conv_hidden(const Geom& g, const Tiling& tl, int cin, int cout, int act, const void* x,
                               void* y, int ystride, const void* wfrag, const float* bias, int head,
-                              const float* head_w,
-                              const float* head_b, const int32_t* tables, uint8_t* nib, float* logits,
-                              int batch, int n_workgroups, hipStream_t stream) {
+                              const float* head_w, const float* head_b, const int32_t* tables, uint8_t* nib,
+                              float* logits, int batch, int n_workgroups, const Split_k& sk,
+                              hipStream_t stream) {
   if (tl.span <= 0 || tl.span > MAX_SPAN) return hipErrorInvalidValue;
+  // parts per tile: a power of two dividing the layer's chunks, with room
+  // for every unit's sums
+  if (sk.kshift < 0 || (cin / KC) % (1 << sk.kshift) != 0 ||
+      (sk.kshift > 0 && (tl.ntiles << sk.kshift) > sk.max_units))
+    return hipErrorInvalidValue;
   PD_HIDDEN_CASE(64, 64, EPI_ACT)
   PD_HIDDEN_CASE(128, 128, EPI_ACT)
   PD_HIDDEN_CASE(64, 128, EPI_ACT)

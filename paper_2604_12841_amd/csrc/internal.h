@@ -144,11 +144,24 @@ int conv_single_max_span();  // staged voxels a tile may need
 // Weight fragments in 16-channel chunks (conv_fragments in api.hip; c_out = 4
 // padded to 32 channels, bias to 32 values); n_workgroups =
 // conv_hidden_workgroups_per_cu() per CU.
+// Small batches: each tile's K loop (its 16-channel chunks) split into
+// 2^kshift parts run by different workgroups of one launch, which park fp32
+// sums in `partial` (max_units units of conv_hidden_partial_floats_per_unit()
+// floats); a second launch adds each tile's parts in part order and runs the
+// epilogue.  kshift = 0: no split, one launch.
+struct Split_k {
+  int kshift;
+  float* partial;
+  long long max_units;
+};
+
 hipError_t launch_conv_hidden(const Geom& g, const Tiling& tl, int cin, int cout, int act, const void* x,
                               void* y, int ystride, const void* wfrag, const float* bias, int head,
                               const float* head_w, const float* head_b, const int32_t* tables, uint8_t* nib,
-                              float* logits, int batch, int n_workgroups, hipStream_t stream);
+                              float* logits, int batch, int n_workgroups, const Split_k& sk,
+                              hipStream_t stream);
 int conv_hidden_max_span();
+size_t conv_hidden_partial_floats_per_unit();
 int conv_hidden_workgroups_per_cu();
 
 // Persistent workgroups of a conv launch: one per CU (n_workgroups), a

@@ -71,9 +71,10 @@ def excused_masks(d, T, logits, tol, layout="plaquette"):
 
 
 def compare(d, T, dtype, ref_logits, ref_flips, ref_res, got_flips, got_res, got_logits=None,
-            layout="plaquette"):
-    """Returns a dict of parity statistics (see module docstring)."""
-    tol = TOL[dtype]
+            layout="plaquette", tol=None):
+    """Returns a dict of parity statistics (see module docstring); tol
+    defaults to the dtype's logit tolerance."""
+    tol = TOL[dtype] if tol is None else tol
     B = ref_logits.shape[0]
     F = T * (3 * d * d - 1)
     S = T * (d * d - 1)

@@ -8,8 +8,10 @@ The oracle cannot run a whole d=13 batch of 4096 in seconds, so:
   * for every sample, the residual equals the oracle's residual stage applied
     to the GPU's own flips (pure XOR work, cheap at any size), and the
     padding bits are zero;
-  * the sampled samples give bit-identical outputs when run alone in a
-    small batch (different tiling, same arithmetic order).
+  * the sampled samples, run alone in a small batch (whose K loops are
+    split over workgroups, so fp32 sums are taken in another order and a bf16
+    activation can round the other way), agree with the full batch to the
+    parity rule: logits within the tolerance, bits exact up to excused sites.
 """
 import numpy as np
 import pytest
@@ -51,11 +53,12 @@ def test_full_size_sampled(cuda, cfg):
     st = compare(d, T, dtype, ref_logits, ref_flips, ref_res, flips[idx], res[idx], logits[idx])
     say("  stats", st)
     assert_parity(st, dtype)
-    # the same samples alone: identical bits
+    # the same samples alone (a small batch, whose K loops are split over
+    # workgroups): equal to the full batch's results under the parity rule
     say("  same samples in a batch of", len(idx))
     small = pdx.Predecoder(weights, d, T, layers, dtype, max_batch=len(idx))
     f2, r2, l2 = run_gpu(small, det[idx])
     small.close()
-    np.testing.assert_array_equal(f2, flips[idx])
-    np.testing.assert_array_equal(r2, res[idx])
-    np.testing.assert_array_equal(l2, logits[idx])
+    st2 = compare(d, T, dtype, logits[idx].astype(np.float64), flips[idx], res[idx], f2, r2, l2)
+    say("  stats against the full batch", st2)
+    assert_parity(st2, dtype)
