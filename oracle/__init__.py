@@ -71,6 +71,14 @@ def _load():
         lib.oracle_forward_grid.restype = None
         lib.oracle_flips_residual_paper.argtypes = [i32, i32, i32, vp, vp, vp, vp]
         lib.oracle_flips_residual_paper.restype = None
+        lib.oracle_e4m3_value.argtypes = [i32]
+        lib.oracle_e4m3_value.restype = ctypes.c_double
+        lib.oracle_e4m3_code.argtypes = [ctypes.c_float]
+        lib.oracle_e4m3_code.restype = i32
+        lib.oracle_round_e4m3.argtypes = [ctypes.c_float]
+        lib.oracle_round_e4m3.restype = ctypes.c_double
+        lib.oracle_e4m3_scale_exp.argtypes = [ctypes.c_double]
+        lib.oracle_e4m3_scale_exp.restype = i32
         _lib = lib
     return _lib
 
@@ -127,6 +135,30 @@ def round_bf16(x):
     return np.array([lib.oracle_round_bf16(float(v)) for v in x.ravel()], dtype=np.float32).reshape(x.shape)
 
 
+def e4m3_value(code):
+    """Value of an OCP E4M3 code (NaN for 0x7f / 0xff)."""
+    return float(_load().oracle_e4m3_value(int(code)))
+
+
+def e4m3_code(x):
+    """Elementwise fp32 -> E4M3 code (nearest, ties to even, saturating at 448)."""
+    lib = _load()
+    x = np.asarray(x, dtype=np.float32)
+    return np.array([lib.oracle_e4m3_code(float(v)) for v in x.ravel()], dtype=np.uint8).reshape(x.shape)
+
+
+def round_e4m3(x):
+    """Elementwise fp32 -> E4M3 -> value."""
+    lib = _load()
+    x = np.asarray(x, dtype=np.float32)
+    return np.array([lib.oracle_round_e4m3(float(v)) for v in x.ravel()], dtype=np.float64).reshape(x.shape)
+
+
+def e4m3_scale_exp(amax):
+    """Scale exponent of a weight row in fp8 mode: smallest e with amax / 2^e <= 448."""
+    return int(_load().oracle_e4m3_scale_exp(float(amax)))
+
+
 def gelu_tanh(x):
     lib = _load()
     x = np.asarray(x, dtype=np.float64)
@@ -138,10 +170,11 @@ def weight_count(layers):
     return int(_load().oracle_weight_count(len(layers), _ptr(spec)))
 
 
-def forward(d, T, planes, layers, weights, bf16, layout="plaquette"):
+def forward(d, T, planes, layers, weights, bf16, layout="plaquette", fp8=False):
     """Network forward.  planes [B][c_in][T][H][H] float64; layers: list of
     (c_in, c_out, k, act); weights: flat fp32.  Returns logits
-    [B][c_out_last][T][H][H] float64 (fp32-valued in bf16 mode)."""
+    [B][c_out_last][T][H][H] float64 (fp32-valued in bf16 and fp8 mode).
+    bf16 / fp8 select the quantisation points of that precision (fp8 wins)."""
     planes = np.ascontiguousarray(planes, dtype=np.float64)
     weights = np.ascontiguousarray(weights, dtype=np.float32)
     spec = np.ascontiguousarray(np.array([list(l) for l in layers], dtype=np.int32).ravel())
@@ -153,8 +186,8 @@ def forward(d, T, planes, layers, weights, bf16, layout="plaquette"):
         raise ValueError("planes shape mismatch")
     co = layers[-1][1]
     out = np.zeros((B, co, T, H, H), dtype=np.float64)
-    _load().oracle_forward_grid(H, T, B, _ptr(planes), len(layers), _ptr(spec), _ptr(weights),
-                                1 if bf16 else 0, _ptr(out))
+    prec = 2 if fp8 else (1 if bf16 else 0)
+    _load().oracle_forward_grid(H, T, B, _ptr(planes), len(layers), _ptr(spec), _ptr(weights), prec, _ptr(out))
     return out
 
 
@@ -218,12 +251,12 @@ def num_threads():
     return int(lib.oracle_num_threads())
 
 
-def run(d, T, det, layers, weights, bf16, layout="plaquette", first=None, last=None):
+def run(d, T, det, layers, weights, bf16, layout="plaquette", first=None, last=None, fp8=False):
     """The whole path: (logits, flips, residual)."""
     if layout == "paper":
-        logits = forward(d, T, unpack_paper(d, T, det, first, last), layers, weights, bf16, layout)
+        logits = forward(d, T, unpack_paper(d, T, det, first, last), layers, weights, bf16, layout, fp8)
         flips, res = flips_residual_paper(d, T, logits, det)
     else:
-        logits = forward(d, T, unpack(d, T, det), layers, weights, bf16)
+        logits = forward(d, T, unpack(d, T, det), layers, weights, bf16, fp8=fp8)
         flips, res = flips_residual(d, T, logits, det)
     return logits, flips, res

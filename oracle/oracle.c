@@ -25,6 +25,18 @@
  * to bf16; logits are rounded to fp32).  Products of bf16 values are exact in
  * fp64, so the only difference from an exact sum is fp64 rounding.
  *
+ * In fp8 mode (the paper deploys its models in FP8, Sec. VI; it does not
+ * state the scaling, the reading here is this file's): OCP E4M3 (4 exponent
+ * bits, bias 7, 3 mantissa bits, no infinities, largest finite 448).  Weights
+ * of every layer get one power-of-two scale per output channel, 2^e with e
+ * the smallest integer such that max |w| / 2^e <= 448, and are stored as
+ * e4m3(w / 2^e) (so w is used as e4m3(w / 2^e) * 2^e, exactly); every conv
+ * or head input is rounded to e4m3 with no scale (the input planes, 0, 1/2
+ * and 1, are exact); rounding is to nearest, ties to the even code, and
+ * magnitudes above 448 saturate to 448.  The pre-activation is rounded to
+ * fp32 and the activation evaluated in fp64 and rounded to fp32, then to
+ * e4m3; biases and logits are fp32.
+ *
  * Array layout is channel-major per sample (like PyTorch NCDHW):
  * x[b][c][t][i][j] with i, j in [0, d] on the (d+1) x (d+1) plaquette grid,
  * or, in the paper's own layout (Sec. IV.B.1), i, j in [0, d-1] on the D x D
@@ -207,6 +219,62 @@ float oracle_round_bf16(float x) {
   return y;
 }
 
+/* OCP E4M3 code -> value (Sec. VI deploys FP8; the format is the OCP 8-bit
+ * floating point one): sign bit 7, exponent field bits 6..3 (bias 7),
+ * mantissa bits 2..0; exponent field 0 is subnormal (m 2^-9); code 0x7f /
+ * 0xff is NaN; there are no infinities. */
+double oracle_e4m3_value(int code) {
+  int sgn = (code >> 7) & 1, ex = (code >> 3) & 15, m = code & 7;
+  double v;
+  if (ex == 15 && m == 7) return NAN;
+  if (ex == 0)
+    v = ldexp((double)m, -9);
+  else
+    v = ldexp(1.0 + m / 8.0, ex - 7);
+  return sgn ? -v : v;
+}
+
+/* fp32 -> E4M3 code: the nearest finite value, ties to the even code (the
+ * one whose mantissa LSB is 0), |x| > 448 saturating to 448.  Found by
+ * searching the 127 non-negative finite codes, whose values increase with
+ * the code.  NaN gives 0x7f. */
+int oracle_e4m3_code(float x) {
+  if (isnan(x)) return 0x7f;
+  int sgn = signbit(x) ? 0x80 : 0;
+  double a = fabs((double)x);
+  int lo = 0, hi = 0x7e; /* largest code with value <= a, by bisection */
+  if (a >= oracle_e4m3_value(0x7e)) return sgn | 0x7e;
+  while (lo < hi) {
+    int mid = (lo + hi + 1) / 2;
+    if (oracle_e4m3_value(mid) <= a)
+      lo = mid;
+    else
+      hi = mid - 1;
+  }
+  double below = oracle_e4m3_value(lo), above = oracle_e4m3_value(lo + 1);
+  int code;
+  if (a - below < above - a)
+    code = lo;
+  else if (a - below > above - a)
+    code = lo + 1;
+  else
+    code = (lo & 1) ? lo + 1 : lo;
+  return sgn | code;
+}
+
+/* fp32 -> E4M3 -> value. */
+double oracle_round_e4m3(float x) { return oracle_e4m3_value(oracle_e4m3_code(x)); }
+
+/* Scale exponent of a weight row in fp8 mode: the smallest e with
+ * amax / 2^e <= 448 (0 for an all-zero row). */
+int oracle_e4m3_scale_exp(double amax) {
+  if (amax == 0.0) return 0;
+  int e = -160;
+  while (ldexp(amax, -e) > 448.0) ++e;
+  while (ldexp(amax, -(e - 1)) <= 448.0) --e;
+  return e;
+}
+
 /* GELU, tanh approximation (Table hyperparameters):
  *   0.5 y (1 + tanh(sqrt(2/pi) (y + 0.044715 y^3))). */
 double oracle_gelu_tanh(double y) {
@@ -240,19 +308,21 @@ int64_t oracle_weight_count(int n_layers, const int* spec) {
 /* activation, the last layer is linear (it gives the logits).              */
 /* spec: n_layers x {c_in, c_out, k, act}.  weights: fp32, per layer        */
 /* w[c_out][c_in][k][k][k] then b[c_out].  planes: [B][c_in0][T][H][H].     */
-/* logits: [B][c_out_last][T][H][H].  bf16 != 0 selects the bf16 quantisation*/
-/* points described at the top of this file.                                */
+/* logits: [B][c_out_last][T][H][H].  prec: 0 exact (fp64), 1 bf16, 2 fp8:  */
+/* the quantisation points described at the top of this file.               */
 /* Samples and output channels are independent; they are spread over       */
 /* OpenMP threads (the arithmetic of each output is unchanged).             */
 /* ---------------------------------------------------------------------- */
 void oracle_forward_grid(int H, int T, int B, const double* planes, int n_layers, const int* spec,
-                         const float* weights, int bf16, double* logits) {
+                         const float* weights, int prec, double* logits) {
+  const int bf16 = prec == 1, fp8 = prec == 2;
   int64_t V = (int64_t)T * H * H;
   int cmax = spec[0];
   for (int l = 0; l < n_layers; ++l)
     if (spec[4 * l + 1] > cmax) cmax = spec[4 * l + 1];
 
-  /* Per-layer weights in fp64 (rounded to bf16 first in bf16 mode). */
+  /* Per-layer weights in fp64 (rounded to bf16 first in bf16 mode; in fp8
+   * mode e4m3(w / 2^e) * 2^e with one e per output channel). */
   double** w = (double**)malloc(sizeof(double*) * n_layers);
   double** bias = (double**)malloc(sizeof(double*) * n_layers);
   const float* src = weights;
@@ -262,6 +332,16 @@ void oracle_forward_grid(int H, int T, int B, const double* planes, int n_layers
     w[l] = (double*)malloc(sizeof(double) * nw);
     bias[l] = (double*)malloc(sizeof(double) * co);
     for (int64_t e = 0; e < nw; ++e) w[l][e] = bf16 ? (double)oracle_round_bf16(src[e]) : (double)src[e];
+    if (fp8) {
+      int64_t row = nw / co;
+      for (int c = 0; c < co; ++c) {
+        double amax = 0.0;
+        for (int64_t e = 0; e < row; ++e) amax = fmax(amax, fabs((double)src[c * row + e]));
+        int ex = oracle_e4m3_scale_exp(amax);
+        for (int64_t e = 0; e < row; ++e)
+          w[l][c * row + e] = ldexp(oracle_round_e4m3((float)ldexp((double)src[c * row + e], -ex)), ex);
+      }
+    }
     for (int e = 0; e < co; ++e) bias[l][e] = (double)src[nw + e];
     src += nw + co;
   }
@@ -272,7 +352,8 @@ void oracle_forward_grid(int H, int T, int B, const double* planes, int n_layers
   for (int b = 0; b < B; ++b)
     for (int64_t e = 0; e < c0 * V; ++e) {
       double v = planes[(int64_t)b * c0 * V + e];
-      xa[(int64_t)b * cmax * V + e] = bf16 ? (double)oracle_round_bf16((float)v) : v;
+      xa[(int64_t)b * cmax * V + e] =
+          bf16 ? (double)oracle_round_bf16((float)v) : (fp8 ? oracle_round_e4m3((float)v) : v);
     }
 
   for (int l = 0; l < n_layers; ++l) {
@@ -305,7 +386,15 @@ void oracle_forward_grid(int H, int T, int B, const double* planes, int n_layers
                   }
                 }
               double v;
-              if (bf16) {
+              if (fp8) {
+                float pre = (float)(acc + bl[co]);
+                if (last) {
+                  v = (double)pre; /* fp32 logit */
+                } else {
+                  float a = (float)activation(act, (double)pre);
+                  v = oracle_round_e4m3(a);
+                }
+              } else if (bf16) {
                 float pre = (float)(acc + bl[co]);
                 if (last) {
                   v = (double)pre; /* fp32 logit */
@@ -339,8 +428,8 @@ void oracle_forward_grid(int H, int T, int B, const double* planes, int n_layers
 
 /* The same on the (d+1) x (d+1) plaquette grid. */
 void oracle_forward(int d, int T, int B, const double* planes, int n_layers, const int* spec,
-                    const float* weights, int bf16, double* logits) {
-  oracle_forward_grid(d + 1, T, B, planes, n_layers, spec, weights, bf16, logits);
+                    const float* weights, int prec, double* logits) {
+  oracle_forward_grid(d + 1, T, B, planes, n_layers, spec, weights, prec, logits);
 }
 
 /* ---------------------------------------------------------------------- */
