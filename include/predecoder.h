@@ -80,11 +80,24 @@
  * conv K loops over several workgroups, so two batch sizes can differ in the
  * fp32 summation order, and through an activation rounded to the other bf16
  * neighbour, by up to a few 1e-3 in the logits.
+ * PD_DTYPE_FP8 (the paper deploys its models in FP8, Sec. VI, without
+ * stating the scaling; this is the library's reading): OCP E4M3 values (4
+ * exponent bits, bias 7, 3 mantissa bits, largest finite 448).  Each output
+ * channel of each layer gets a power-of-two weight scale 2^e, e the smallest
+ * integer with max |w| / 2^e <= 448 over the channel's weights, and its
+ * weights are used as e4m3(w / 2^e) * 2^e; every conv or head input is an
+ * E4M3 value with no scale (the input planes, 0, 1/2 and 1, are exact);
+ * rounding is to nearest, ties to even, magnitudes above 448 saturate.
+ * Products are accumulated in fp32; bias, activation and logits are fp32.
+ * Same reproducibility rule as bf16; an activation rounded to the other
+ * E4M3 neighbour moves the logits further (the parity tolerance is larger).
  *
  * Supported shapes (others give PD_ERR_UNSUPPORTED): 3 <= d <= 63,
  * 1 <= T <= 1023; hidden layers k == 3; output layer k == 1, or k == 3 on
- * the paper layout.  BF16: hidden widths 64 or 128.  FP32 (plaquette layout
- * only): hidden widths 8 .. 128, multiples of 8.
+ * the paper layout.  BF16 and FP8: hidden widths 64, 128 or 256 (a layer
+ * after a 256-wide one needs a 3x3x3 output layer); FP8 needs two hidden
+ * layers when the output layer is 1x1x1.  FP32 (plaquette layout only):
+ * hidden widths 8 .. 128, multiples of 8.
  *
  * Errors.  Every function is nothrow and never aborts.  Host-checkable misuse
  * gives PD_ERR_INVALID_ARG before any device call; a failed HIP call or
@@ -120,7 +133,7 @@ typedef enum pd_status {
 
 typedef enum pd_act { PD_ACT_NONE = 0, PD_ACT_GELU_TANH = 1, PD_ACT_RELU = 2 } pd_act;
 
-typedef enum pd_dtype { PD_DTYPE_FP32 = 0, PD_DTYPE_BF16 = 1 } pd_dtype;
+typedef enum pd_dtype { PD_DTYPE_FP32 = 0, PD_DTYPE_BF16 = 1, PD_DTYPE_FP8 = 2 } pd_dtype;
 
 typedef enum pd_layout { PD_LAYOUT_PLAQUETTE = 0, PD_LAYOUT_PAPER = 1 } pd_layout;
 
@@ -149,7 +162,7 @@ typedef struct pd_predecoder pd_predecoder; /* opaque */
  * is fully convolutional, so the same weights apply to any (d, T)).
  * weights: host fp32, n_weights == predecoder_weight_count(layers, n_layers),
  *          copied (the caller keeps ownership).
- * dtype:   PD_DTYPE_BF16 or PD_DTYPE_FP32.
+ * dtype:   PD_DTYPE_BF16, PD_DTYPE_FP8 or PD_DTYPE_FP32.
  * max_batch: largest batch any later call may pass; sizes the workspace.
  * out:     receives the handle (NULL on error).
  * Allocates device memory on the current HIP device; launches nothing. */
@@ -187,11 +200,23 @@ pd_status predecoder_residual(pd_predecoder* h, void* hip_stream, const uint64_t
 /* The unpack stage alone (Sec. IV.B.1, Eqs. encTrainX1-4: the input planes
  * of the handle's layout): det [batch][W_det] -> planes, device,
  * [batch][T][H][H][c_in] (c_in = 2 on the plaquette layout, 4 on the paper
- * layout) in the handle's dtype (bf16 bit patterns as uint16 for
- * PD_DTYPE_BF16, fp32 for PD_DTYPE_FP32).
+ * layout) as bf16 bit patterns (uint16) for PD_DTYPE_BF16 and
+ * PD_DTYPE_FP8, fp32 for PD_DTYPE_FP32.
  * Asynchronous on hip_stream. */
 pd_status predecoder_unpack(pd_predecoder* h, void* hip_stream, const uint64_t* det,
                             int32_t batch, void* planes);
+
+/* The path up to hidden layer `layer` (0-based, a layer before the output
+ * layer or head): its output activations as the next layer reads them --
+ * after bias, activation and rounding to the handle's precision -- copied to
+ * out, device, [batch][T][H][H][c_out] (bf16 bit patterns as uint16 for
+ * PD_DTYPE_BF16, E4M3 codes as uint8 for PD_DTYPE_FP8).  For inspecting and
+ * testing one layer at a time (Sec. IV.B, Fig. ConvArch: the activations
+ * between the conv layers); a head that predecoder_run fuses into that layer
+ * is not run.  PD_ERR_INVALID_ARG for a layer out of range, PD_ERR_UNSUPPORTED
+ * for PD_DTYPE_FP32.  Asynchronous on hip_stream. */
+pd_status predecoder_activations(pd_predecoder* h, void* hip_stream, const uint64_t* det,
+                                 int32_t batch, int32_t layer, void* out);
 
 /* Number of timed stages of predecoder_run: unpack, one per layer (the last
  * one is the head with its threshold), and the residual/repack stage. */

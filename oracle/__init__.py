@@ -69,6 +69,8 @@ def _load():
         lib.oracle_unpack_paper.restype = None
         lib.oracle_forward_grid.argtypes = [i32, i32, i32, vp, i32, vp, vp, i32, vp]
         lib.oracle_forward_grid.restype = None
+        lib.oracle_forward_grid_fp8_perturbed.argtypes = [i32, i32, i32, vp, i32, vp, vp, ctypes.c_double, vp]
+        lib.oracle_forward_grid_fp8_perturbed.restype = None
         lib.oracle_flips_residual_paper.argtypes = [i32, i32, i32, vp, vp, vp, vp]
         lib.oracle_flips_residual_paper.restype = None
         lib.oracle_e4m3_value.argtypes = [i32]
@@ -170,11 +172,13 @@ def weight_count(layers):
     return int(_load().oracle_weight_count(len(layers), _ptr(spec)))
 
 
-def forward(d, T, planes, layers, weights, bf16, layout="plaquette", fp8=False):
+def forward(d, T, planes, layers, weights, bf16, layout="plaquette", fp8=False, fp8_sum_eps=0.0):
     """Network forward.  planes [B][c_in][T][H][H] float64; layers: list of
     (c_in, c_out, k, act); weights: flat fp32.  Returns logits
     [B][c_out_last][T][H][H] float64 (fp32-valued in bf16 and fp8 mode).
-    bf16 / fp8 select the quantisation points of that precision (fp8 wins)."""
+    bf16 / fp8 select the quantisation points of that precision (fp8 wins);
+    fp8_sum_eps > 0 (fp8 only): every sum of products moved by a hashed
+    u * eps * sum|products|, u in [-1, 1) (sizes the fp8 parity tolerance)."""
     planes = np.ascontiguousarray(planes, dtype=np.float64)
     weights = np.ascontiguousarray(weights, dtype=np.float32)
     spec = np.ascontiguousarray(np.array([list(l) for l in layers], dtype=np.int32).ravel())
@@ -186,8 +190,15 @@ def forward(d, T, planes, layers, weights, bf16, layout="plaquette", fp8=False):
         raise ValueError("planes shape mismatch")
     co = layers[-1][1]
     out = np.zeros((B, co, T, H, H), dtype=np.float64)
-    prec = 2 if fp8 else (1 if bf16 else 0)
-    _load().oracle_forward_grid(H, T, B, _ptr(planes), len(layers), _ptr(spec), _ptr(weights), prec, _ptr(out))
+    if fp8_sum_eps > 0:
+        if not fp8:
+            raise ValueError("fp8_sum_eps applies to the fp8 forward")
+        _load().oracle_forward_grid_fp8_perturbed(H, T, B, _ptr(planes), len(layers), _ptr(spec), _ptr(weights),
+                                                  float(fp8_sum_eps), _ptr(out))
+    else:
+        prec = 2 if fp8 else (1 if bf16 else 0)
+        _load().oracle_forward_grid(H, T, B, _ptr(planes), len(layers), _ptr(spec), _ptr(weights), prec,
+                                    _ptr(out))
     return out
 
 

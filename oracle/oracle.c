@@ -313,8 +313,21 @@ int64_t oracle_weight_count(int n_layers, const int* spec) {
 /* Samples and output channels are independent; they are spread over       */
 /* OpenMP threads (the arithmetic of each output is unchanged).             */
 /* ---------------------------------------------------------------------- */
-void oracle_forward_grid(int H, int T, int B, const double* planes, int n_layers, const int* spec,
-                         const float* weights, int prec, double* logits) {
+/* Counter-based value in [-1, 1) (splitmix64 finaliser of the key). */
+static double unit_hash(uint64_t key) {
+  uint64_t z = key + 0x9e3779b97f4a7c15ull;
+  z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+  z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+  z ^= z >> 31;
+  return (double)(z >> 11) * 0x1.0p-52 - 1.0;
+}
+
+/* eps > 0 (fp8 only; test infrastructure): every sum of products is moved
+ * by u eps sum |products|, u in [-1, 1) hashed from (layer, sample, channel,
+ * voxel): a summation whose error is bounded by eps relative to the sum of
+ * magnitudes, used to size the fp8 parity tolerance. */
+static void forward_impl(int H, int T, int B, const double* planes, int n_layers, const int* spec,
+                         const float* weights, int prec, double eps, double* logits) {
   const int bf16 = prec == 1, fp8 = prec == 2;
   int64_t V = (int64_t)T * H * H;
   int cmax = spec[0];
@@ -369,7 +382,7 @@ void oracle_forward_grid(int H, int T, int B, const double* planes, int n_layers
         for (int t = 0; t < T; ++t)
           for (int i = 0; i < H; ++i)
             for (int j = 0; j < H; ++j) {
-              double acc = 0.0;
+              double acc = 0.0, mag = 0.0;
               for (int ci = 0; ci < ci_n; ++ci)
                 for (int kt = 0; kt < k; ++kt) {
                   int tt = t + kt - p;
@@ -380,11 +393,17 @@ void oracle_forward_grid(int H, int T, int B, const double* planes, int n_layers
                     for (int kj = 0; kj < k; ++kj) {
                       int jj = j + kj - p;
                       if (jj < 0 || jj >= H) continue;
-                      acc += wl[(((int64_t)co * ci_n + ci) * k + kt) * k * k + ki * k + kj] *
-                             x[(((int64_t)ci * T + tt) * H + ii) * H + jj];
+                      const double pr = wl[(((int64_t)co * ci_n + ci) * k + kt) * k * k + ki * k + kj] *
+                                        x[(((int64_t)ci * T + tt) * H + ii) * H + jj];
+                      acc += pr;
+                      mag += fabs(pr);
                     }
                   }
                 }
+              if (eps > 0.0) {
+                const uint64_t key = ((((((uint64_t)l * 65536 + b) * 4096 + co) * 2048 + t) * 256 + i) * 256) + j;
+                acc += unit_hash(key) * eps * mag;
+              }
               double v;
               if (fp8) {
                 float pre = (float)(acc + bl[co]);
@@ -424,6 +443,17 @@ void oracle_forward_grid(int H, int T, int B, const double* planes, int n_layers
   free(bias);
   free(xa);
   free(xb);
+}
+
+void oracle_forward_grid(int H, int T, int B, const double* planes, int n_layers, const int* spec,
+                         const float* weights, int prec, double* logits) {
+  forward_impl(H, T, B, planes, n_layers, spec, weights, prec, 0.0, logits);
+}
+
+/* fp8 forward with the bounded summation error described at forward_impl. */
+void oracle_forward_grid_fp8_perturbed(int H, int T, int B, const double* planes, int n_layers, const int* spec,
+                                       const float* weights, double eps, double* logits) {
+  forward_impl(H, T, B, planes, n_layers, spec, weights, 2, eps, logits);
 }
 
 /* The same on the (d+1) x (d+1) plaquette grid. */

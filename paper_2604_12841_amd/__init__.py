@@ -13,12 +13,13 @@ import ctypes
 import os
 
 __all__ = ["Predecoder", "PredecoderError", "Options", "lib", "det_words", "flip_words", "weight_count",
-           "status_string", "ACT_NONE", "ACT_GELU_TANH", "ACT_RELU", "DTYPE_FP32", "DTYPE_BF16",
+           "status_string", "ACT_NONE", "ACT_GELU_TANH", "ACT_RELU", "DTYPE_FP32", "DTYPE_BF16", "DTYPE_FP8",
            "LAYOUT_PLAQUETTE", "LAYOUT_PAPER", "BOUNDARY_NONE", "BOUNDARY_Z", "BOUNDARY_X", "LIB_PATH",
            "EXPORTS"]
 
 ACT_NONE, ACT_GELU_TANH, ACT_RELU = 0, 1, 2
-DTYPE_FP32, DTYPE_BF16 = 0, 1
+DTYPE_FP32, DTYPE_BF16, DTYPE_FP8 = 0, 1, 2
+_DTYPES = {"fp32": DTYPE_FP32, "bf16": DTYPE_BF16, "fp8": DTYPE_FP8}
 LAYOUT_PLAQUETTE, LAYOUT_PAPER = 0, 1
 BOUNDARY_NONE, BOUNDARY_Z, BOUNDARY_X = 0, 1, 2
 _LAYOUTS = {"plaquette": LAYOUT_PLAQUETTE, "paper": LAYOUT_PAPER}
@@ -29,6 +30,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpredecod
 
 # Every symbol declared in include/predecoder.h.
 EXPORTS = ("predecoder_create", "predecoder_create_ex", "predecoder_run", "predecoder_residual", "predecoder_unpack",
+           "predecoder_activations",
            "predecoder_num_stages", "predecoder_stage_times", "predecoder_destroy",
            "predecoder_status_string", "predecoder_det_words", "predecoder_flip_words",
            "predecoder_weight_count")
@@ -72,6 +74,8 @@ def lib():
         L.predecoder_residual.restype = i32
         L.predecoder_unpack.argtypes = [vp, vp, vp, i32, vp]
         L.predecoder_unpack.restype = i32
+        L.predecoder_activations.argtypes = [vp, vp, vp, i32, i32, vp]
+        L.predecoder_activations.restype = i32
         L.predecoder_num_stages.argtypes = [vp]
         L.predecoder_num_stages.restype = i32
         L.predecoder_stage_times.argtypes = [vp, vp, vp, i32, vp, vp, i32, ctypes.POINTER(ctypes.c_float)]
@@ -139,7 +143,7 @@ class Predecoder:
         import numpy as np
         w = np.ascontiguousarray(np.asarray(weights, dtype=np.float32))
         self.d, self.T, self.layers, self.max_batch = d, T, [tuple(l) for l in layers], max_batch
-        self.dtype = DTYPE_BF16 if dtype in ("bf16", DTYPE_BF16) else DTYPE_FP32
+        self.dtype = _DTYPES[dtype] if isinstance(dtype, str) else int(dtype)
         self.layout = _LAYOUTS[layout] if isinstance(layout, str) else int(layout)
         self.grid = d if self.layout == LAYOUT_PAPER else d + 1
         self.det_words = det_words(d, T)
@@ -172,6 +176,13 @@ class Predecoder:
         batch = det.shape[0] if batch is None else batch
         self._check(lib().predecoder_unpack(self._h, _stream(stream), _ptr(det), batch, _ptr(planes)),
                     "predecoder_unpack")
+
+    def activations(self, det, layer, out, batch=None, stream=None):
+        """Output activations of hidden layer `layer` -> out [B][T][H][H][c_out] (bf16 bits as int16,
+        E4M3 codes as uint8)."""
+        batch = det.shape[0] if batch is None else batch
+        self._check(lib().predecoder_activations(self._h, _stream(stream), _ptr(det), batch, layer, _ptr(out)),
+                    "predecoder_activations")
 
     @property
     def num_stages(self):

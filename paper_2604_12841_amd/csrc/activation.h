@@ -2,7 +2,10 @@
 // kernels: the activation (Sec. IV.B; the GELU in its tanh form, ReLU, or
 // none), bf16 rounding (round to nearest even) and a dispatch that turns the
 // runtime activation code into a compile-time one, so an epilogue is one
-// straight-line body per activation instead of a branch per value.
+// straight-line body per activation instead of a branch per value; and the
+// OCP E4M3 conversions of the fp8 path (round to nearest even, magnitudes
+// above 448 saturated to 448 before the conversion instruction, which would
+// give NaN past the format's rounding range).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -57,5 +60,19 @@ __device__ __forceinline__ uint32_t bf16_pack(float lo, float hi) {
 }
 
 __device__ __forceinline__ float bf16_round(float v) { return __uint_as_float(bf16_bits(v) << 16); }
+
+__device__ __forceinline__ float e4m3_clamp(float v) { return __builtin_fminf(__builtin_fmaxf(v, -448.0f), 448.0f); }
+
+// Four values as E4M3 codes, v0 in bits 0-7 (two conversion instructions).
+__device__ __forceinline__ uint32_t e4m3_pack4(float v0, float v1, float v2, float v3) {
+  const int lo = __builtin_amdgcn_cvt_pk_fp8_f32(e4m3_clamp(v0), e4m3_clamp(v1), 0, false);
+  return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(e4m3_clamp(v2), e4m3_clamp(v3), lo, true);
+}
+
+// v rounded to E4M3 and back.
+__device__ __forceinline__ float e4m3_round(float v) {
+  const int c = __builtin_amdgcn_cvt_pk_fp8_f32(e4m3_clamp(v), 0.0f, 0, false);
+  return __builtin_amdgcn_cvt_f32_fp8(c, 0);
+}
 
 }  // namespace pd

@@ -10,6 +10,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstring>
 #include <new>
 #include <vector>
@@ -245,12 +246,16 @@ void tiling_for_batch(Tiling* t, const Geom& g, int batch) {
 bool supported(const Geom& g, const pd_layer* l, int n, int dtype) {
   if (g.d > kMaxD || g.T > kMaxT) return false;
   if (n < 2) return false;  // at least one hidden 3x3x3 layer before the head
-  if (g.layout == PD_LAYOUT_PAPER && dtype != PD_DTYPE_BF16) return false;
+  if (g.layout == PD_LAYOUT_PAPER && dtype == PD_DTYPE_FP32) return false;
+  const bool mfma = dtype != PD_DTYPE_FP32;
+  // fp8 with a 1x1x1 head needs its head fused into a hidden layer after the
+  // first (a lone hidden layer carrying the head runs in bf16 only)
+  if (dtype == PD_DTYPE_FP8 && l[n - 1].k == 1 && n < 3) return false;
   bool wide = false;
   for (int i = 0; i < n - 1; ++i) {
     if (l[i].k != 3) return false;
     int co = l[i].c_out;
-    if (dtype == PD_DTYPE_BF16) {
+    if (mfma) {
       if (co != 64 && co != 128 && co != 256) return false;
       wide = wide || co == 256;
     } else {
@@ -263,8 +268,67 @@ bool supported(const Geom& g, const pd_layer* l, int n, int dtype) {
   if (wide && out.k != 3) return false;
   if (out.k == 3) return g.layout == PD_LAYOUT_PAPER;  // a 3x3x3 output layer (c_in 64 or 128, checked above)
   if (out.k != 1 || out.c_in > 128) return false;
-  if (dtype == PD_DTYPE_BF16 && (out.c_in % 8) != 0) return false;
+  if (mfma && (out.c_in % 8) != 0) return false;
   return true;
+}
+
+// OCP E4M3 (fp8 path): the code of v, rounded to nearest with ties to even,
+// magnitudes of 448 and above saturating to 448 (code 0x7e); NaN is never
+// passed (weights are finite).
+uint8_t e4m3_code(float v) {
+  const uint8_t sgn = std::signbit(v) ? 0x80 : 0;
+  const double a = std::fabs((double)v);
+  if (a >= 448.0) return sgn | 0x7e;
+  int ex;
+  std::frexp(a, &ex);  // a = f 2^ex, f in [0.5, 1)
+  if (a == 0.0 || ex - 1 < -6) {  // subnormal range: multiples of 2^-9
+    const int q = (int)std::nearbyint(std::ldexp(a, 9));  // 8 becomes the smallest normal, code 0x08
+    return sgn | (uint8_t)q;
+  }
+  int e = ex - 1;  // a = m 2^e, m in [1, 2)
+  int m = (int)std::nearbyint((std::ldexp(a, -e) - 1.0) * 8.0);
+  if (m == 8) {
+    m = 0;
+    ++e;
+  }
+  const int code = ((e + 7) << 3) | m;
+  return sgn | (uint8_t)std::min(code, 0x7e);
+}
+
+float e4m3_value(uint8_t c) {
+  const int ex = (c >> 3) & 15, m = c & 7;
+  const double v = ex == 0 ? std::ldexp((double)m, -9) : std::ldexp(1.0 + m / 8.0, ex - 7);
+  return (float)((c & 0x80) ? -v : v);
+}
+
+// Power-of-two scale exponent of a weight row: the smallest e with
+// amax / 2^e <= 448 (0 for an all-zero row).
+int e4m3_scale_exp(float amax) {
+  if (amax == 0.0f) return 0;
+  int ex;
+  std::frexp((double)amax / 448.0, &ex);  // amax / 448 = f 2^ex, f in [0.5, 1)
+  // 2^(ex-1) <= amax / 448 < 2^ex: e = ex, or ex - 1 when amax / 448 is exactly 2^(ex-1)
+  return std::ldexp((double)amax, -(ex - 1)) <= 448.0 ? ex - 1 : ex;
+}
+
+// Weights of a layer in fp8: per output channel, codes e4m3(w / 2^e) and the
+// scale 2^e; wq receives the values the codes stand for (e4m3 value x 2^e).
+void quantize_e4m3(const float* w, int cout, size_t row, std::vector<uint8_t>* codes, std::vector<float>* scale,
+                   std::vector<float>* wq) {
+  codes->assign((size_t)cout * row, 0);
+  scale->assign(cout, 1.0f);
+  wq->assign((size_t)cout * row, 0.0f);
+  for (int co = 0; co < cout; ++co) {
+    float amax = 0.0f;
+    for (size_t e = 0; e < row; ++e) amax = std::max(amax, std::fabs(w[co * row + e]));
+    const int ex = e4m3_scale_exp(amax);
+    (*scale)[co] = std::ldexp(1.0f, ex);
+    for (size_t e = 0; e < row; ++e) {
+      const uint8_t c = e4m3_code(std::ldexp(w[co * row + e], -ex));
+      (*codes)[co * row + e] = c;
+      (*wq)[co * row + e] = std::ldexp(e4m3_value(c), ex);
+    }
+  }
 }
 
 template <typename T>
@@ -354,6 +418,25 @@ std::vector<uint16_t> conv_fragments(const float* w, int cin, int cout) {
   return f;
 }
 
+// fp8 A fragments (weight codes) for v_mfma_f32_32x32x64_f8f6f4: fragment
+// (chunk of 32 c_in, k-step s, channel block nb), lane l holds 32 bytes,
+// byte e = W[co = 32 nb + l % 32][ci = 32 chunk + e][tap 2 s + l / 32]
+// (tap 27: zero); output channels past c_out are zero.
+std::vector<uint8_t> conv_fragments_fp8(const uint8_t* codes, int cin, int cout) {
+  const int nbt = cout < 32 ? 1 : cout / 32, nch = cin / 32, ns = 14;
+  std::vector<uint8_t> f((size_t)nch * ns * nbt * 64 * 32, 0);
+  for (int c = 0; c < nch; ++c)
+    for (int st = 0; st < ns; ++st)
+      for (int nb = 0; nb < nbt; ++nb)
+        for (int l = 0; l < 64; ++l)
+          for (int e = 0; e < 32; ++e) {
+            const int co = nb * 32 + l % 32, ci = c * 32 + e, tap = 2 * st + l / 32;
+            if (co < cout && tap < 27)
+              f[((((size_t)c * ns + st) * nbt + nb) * 64 + l) * 32 + e] = codes[((size_t)co * cin + ci) * 27 + tap];
+          }
+  return f;
+}
+
 pd_status check_launch(hipError_t e) {
   if (e != hipSuccess) {
     (void)hipGetLastError();
@@ -363,14 +446,17 @@ pd_status check_launch(hipError_t e) {
 }
 
 // Enqueues the whole path.  ev (optional) receives one event record before
-// each stage and one after the last.
+// each stage and one after the last.  stop_layer >= 0: stop after that
+// hidden layer, whose activations are then written (no head fused into it).
 pd_status enqueue_run(pd_predecoder* h, hipStream_t st, const uint64_t* det, int batch, uint64_t* flips,
-                      uint64_t* residual, float* logits, hipEvent_t* ev) {
+                      uint64_t* residual, float* logits, hipEvent_t* ev, int stop_layer = -1) {
   const Geom& g = h->g;
   const int fp32 = h->dtype == PD_DTYPE_FP32;
+  const int fp8 = h->dtype == PD_DTYPE_FP8;
+  const int aelem = fp8 ? 1 : 2;  // bytes per activation value (MFMA paths)
   const int n = (int)h->layers.size();
   // the last layer: a 1x1x1 head (fused into the last hidden layer's
-  // epilogue on the bf16 path) or a 3x3x3 output layer of its own
+  // epilogue on the MFMA paths) or a 3x3x3 output layer of its own
   const bool out3 = h->layers[n - 1].k == 3;
   const int hidden_wgs = h->n_cu * pd::conv_hidden_workgroups_per_cu();
   // Split a layer's K loop over 2^k workgroups per tile while tiles x parts
@@ -378,9 +464,10 @@ pd_status enqueue_run(pd_predecoder* h, hipStream_t st, const uint64_t* det, int
   // then the layer's latency); parts must divide the layer's 16-channel
   // chunks.  Past one unit per CU the parked fp32 sums cost more than the
   // shorter loops gain.
+  const int kch = pd::conv_hidden_chunk_channels(fp8);
   auto split_for = [&](const Tiling& t, int cin) -> pd::Split_k {
     pd::Split_k sk{0, h->partial, h->max_units};
-    while ((cin / 16) % (2 << sk.kshift) == 0 && (t.ntiles << (sk.kshift + 1)) <= h->max_units)
+    while ((cin / kch) % (2 << sk.kshift) == 0 && (t.ntiles << (sk.kshift + 1)) <= h->max_units)
       ++sk.kshift;
     return sk;
   };
@@ -401,7 +488,7 @@ pd_status enqueue_run(pd_predecoder* h, hipStream_t st, const uint64_t* det, int
     if ((s = mark()) != PD_OK) return s;
     void* y = h->act[l & 1];
     const pd_layer& L = h->layers[l];
-    const bool fuse_head = !fp32 && !out3 && l == n - 2;
+    const bool fuse_head = !fp32 && !out3 && l == n - 2 && stop_layer < 0;
     if (fp32) {
       s = check_launch(pd::launch_conv_fp32(g, L.c_in, L.c_out, L.act, (const float*)x, (float*)y,
                                             (const float*)h->wdev[l], h->bdev[l], batch, st));
@@ -411,23 +498,25 @@ pd_status enqueue_run(pd_predecoder* h, hipStream_t st, const uint64_t* det, int
       head_done = true;
     } else {
       // a 256-wide layer runs as two slices of 128 output channels over the
-      // same input (slice k: its fragments, biases and output channels)
+      // same input (slice k: its fragments, biases (fp8: and scales) and
+      // output channels)
       const int nsl = h->wslice[l] ? 2 : 1, cw = L.c_out / nsl;
       for (int k = 0; k < nsl && s == PD_OK; ++k) {
         const void* wk = (const char*)h->wdev[l] + k * h->wslice[l];
-        void* yk = (uint16_t*)y + (size_t)k * cw;
+        void* yk = (char*)y + (size_t)k * cw * aelem;
         if (l == 0)
           s = check_launch(pd::launch_conv_first(g, L.c_in, cw, L.act, x, yk, L.c_out, wk, h->bdev[l] + k * cw,
-                                                 batch, st));
+                                                 batch, fp8, st));
         else  // the last hidden layer may carry the head and the threshold in its epilogue
           s = check_launch(pd::launch_conv_hidden(g, tl, L.c_in, cw, L.act, x, yk, L.c_out, wk,
-                                                  h->bdev[l] + k * cw, fuse_head ? 1 : 0, h->head_w, h->head_b,
-                                                  h->tables, h->nib, logits, batch, hidden_wgs,
-                                                  split_for(tl, L.c_in), st));
+                                                  h->bdev[l] + k * cw * (fp8 ? 2 : 1), fuse_head ? 1 : 0,
+                                                  h->head_w, h->head_b, h->tables, h->nib, logits, batch,
+                                                  hidden_wgs, split_for(tl, L.c_in), fp8, st));
       }
       head_done = fuse_head && l > 0;
     }
     if (s != PD_OK) return s;
+    if (l == stop_layer) return PD_OK;
     x = y;
   }
   if ((s = mark()) != PD_OK) return s;
@@ -435,7 +524,7 @@ pd_status enqueue_run(pd_predecoder* h, hipStream_t st, const uint64_t* det, int
     const pd_layer& L = h->layers[n - 1];
     s = check_launch(pd::launch_conv_hidden(g, tl, L.c_in, L.c_out, L.act, x, nullptr, 0, h->wdev[n - 1],
                                             h->bdev[n - 1], 2, nullptr, nullptr, h->tables, h->nib, logits,
-                                            batch, hidden_wgs, split_for(tl, L.c_in), st));
+                                            batch, hidden_wgs, split_for(tl, L.c_in), fp8, st));
   } else if (!head_done) {  // fp32, or a one-hidden-layer network on the paper's layout
     s = check_launch(pd::launch_head(g, h->layers[n - 1].c_in, fp32, x, h->head_w, h->head_b, h->tables,
                                      h->nib, logits, batch, st));
@@ -501,7 +590,7 @@ pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d
   *out = nullptr;
   if (!weights || !layers) return PD_ERR_INVALID_ARG;
   if (d < 3 || (d % 2) == 0 || T < 1) return PD_ERR_INVALID_ARG;
-  if (dtype != PD_DTYPE_FP32 && dtype != PD_DTYPE_BF16) return PD_ERR_INVALID_ARG;
+  if (dtype != PD_DTYPE_FP32 && dtype != PD_DTYPE_BF16 && dtype != PD_DTYPE_FP8) return PD_ERR_INVALID_ARG;
   if (max_batch < 1) return PD_ERR_INVALID_ARG;
   const pd_options o = opts ? *opts : pd_options{PD_LAYOUT_PLAQUETTE, PD_BOUNDARY_NONE, PD_BOUNDARY_NONE};
   if (o.layout != PD_LAYOUT_PLAQUETTE && o.layout != PD_LAYOUT_PAPER) return PD_ERR_INVALID_ARG;
@@ -542,7 +631,7 @@ pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d
   int cmax = 2;
   for (int i = 0; i < n_layers - 1; ++i) cmax = std::max(cmax, (int)layers[i].c_out);
   h->cmax = cmax;
-  if (dtype == PD_DTYPE_BF16) {
+  if (dtype != PD_DTYPE_FP32) {
     h->tiling = plan_tiling(g, max_batch);
     if (h->tiling.span <= 0 || h->tiling.span > std::min(pd::conv_single_max_span(), pd::conv_hidden_max_span())) {
       delete h;
@@ -551,7 +640,9 @@ pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d
   }
 
   pd_status s = PD_OK;
-  const size_t elem = dtype == PD_DTYPE_BF16 ? 2 : 4;
+  // planes: fp32 or bf16; activations: fp32, bf16 or E4M3
+  const size_t elem = dtype == PD_DTYPE_FP32 ? 4 : 2;
+  const size_t aelem = dtype == PD_DTYPE_FP32 ? 4 : (dtype == PD_DTYPE_FP8 ? 1 : 2);
   const size_t vox = (size_t)max_batch * (size_t)g.S;
   auto fail = [&](pd_status st) {
     free_all(h);
@@ -560,10 +651,10 @@ pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d
   };
   const size_t cin0 = (size_t)layers[0].c_in;
   if ((s = dev_alloc(&h->planes, vox * cin0 * elem)) != PD_OK) return fail(s);
-  if ((s = dev_alloc(&h->act[0], vox * cmax * elem)) != PD_OK) return fail(s);
-  if ((s = dev_alloc(&h->act[1], vox * cmax * elem)) != PD_OK) return fail(s);
+  if ((s = dev_alloc(&h->act[0], vox * cmax * aelem)) != PD_OK) return fail(s);
+  if ((s = dev_alloc(&h->act[1], vox * cmax * aelem)) != PD_OK) return fail(s);
   if ((s = dev_alloc(&h->nib, (size_t)max_batch * g.V)) != PD_OK) return fail(s);
-  if (dtype == PD_DTYPE_BF16) {
+  if (dtype != PD_DTYPE_FP32) {
     // parked fp32 sums of split K loops: room for one unit per compute unit
     h->max_units = h->n_cu;
     if ((s = dev_alloc(&h->partial, (size_t)h->max_units * pd::conv_hidden_partial_floats_per_unit() * 4)) !=
@@ -573,8 +664,8 @@ pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d
   std::vector<int32_t> tab = build_tables(g);
   if ((s = upload(&h->tables, tab.data(), tab.size() * sizeof(int32_t))) != PD_OK) return fail(s);
   if (hipMemset(h->planes, 0, vox * cin0 * elem) != hipSuccess ||
-      hipMemset(h->act[0], 0, vox * cmax * elem) != hipSuccess ||
-      hipMemset(h->act[1], 0, vox * cmax * elem) != hipSuccess)
+      hipMemset(h->act[0], 0, vox * cmax * aelem) != hipSuccess ||
+      hipMemset(h->act[1], 0, vox * cmax * aelem) != hipSuccess)
     return fail(PD_ERR_DEVICE);
 
   const float* src = weights;
@@ -584,15 +675,28 @@ pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d
     const float* w = src;
     const float* b = src + nw;
     src += nw + L.c_out;
+    // fp8: weight codes, per-channel scales and the values they stand for
+    std::vector<uint8_t> codes;
+    std::vector<float> scale, wq;
+    if (dtype == PD_DTYPE_FP8) quantize_e4m3(w, L.c_out, nw / L.c_out, &codes, &scale, &wq);
     if (i == n_layers - 1 && L.k == 3) {  // a 3x3x3 output layer: 4 filters padded to one block of 32
-      std::vector<uint16_t> f = conv_fragments(w, L.c_in, L.c_out);
       void* wd = nullptr;
-      s = upload(&wd, f.data(), f.size() * 2);
+      if (dtype == PD_DTYPE_FP8) {
+        std::vector<uint8_t> f = conv_fragments_fp8(codes.data(), L.c_in, L.c_out);
+        s = upload(&wd, f.data(), f.size());
+      } else {
+        std::vector<uint16_t> f = conv_fragments(w, L.c_in, L.c_out);
+        s = upload(&wd, f.data(), f.size() * 2);
+      }
       h->wdev.push_back(wd);
       h->wslice.push_back(0);
       if (s != PD_OK) return fail(s);
-      std::vector<float> bp(32, 0.0f);
-      for (int o2 = 0; o2 < L.c_out; ++o2) bp[o2] = b[o2];
+      // biases of the 32 padded channels, then (fp8) their weight scales
+      std::vector<float> bp(64, 0.0f);
+      for (int o2 = 0; o2 < L.c_out; ++o2) {
+        bp[o2] = b[o2];
+        bp[32 + o2] = dtype == PD_DTYPE_FP8 ? scale[o2] : 1.0f;
+      }
       float* bd = nullptr;
       s = upload(&bd, bp.data(), bp.size() * 4);
       h->bdev.push_back(bd);
@@ -604,7 +708,8 @@ pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d
       for (int o = 0; o < 4; ++o)
         for (int c = 0; c < L.c_in; ++c) {
           float v = w[(size_t)o * L.c_in + c];
-          hw[(size_t)o * L.c_in + c] = dtype == PD_DTYPE_BF16 ? bf16_value(v) : v;
+          hw[(size_t)o * L.c_in + c] =
+              dtype == PD_DTYPE_BF16 ? bf16_value(v) : (dtype == PD_DTYPE_FP8 ? wq[(size_t)o * L.c_in + c] : v);
         }
       if ((s = upload(&h->head_w, hw.data(), hw.size() * 4)) != PD_OK) return fail(s);
       if ((s = upload(&h->head_b, b, 4 * sizeof(float))) != PD_OK) return fail(s);
@@ -612,15 +717,33 @@ pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d
     }
     void* wd = nullptr;
     size_t slice = 0;
-    if (dtype == PD_DTYPE_BF16) {
+    std::vector<float> bias_dev(b, b + L.c_out);
+    if (dtype == PD_DTYPE_FP8 && i > 0) {
+      // E4M3 fragments; per 128-channel slice: its biases, then its scales
+      const int cw = L.c_out == 256 ? 128 : L.c_out;
+      std::vector<uint8_t> f = conv_fragments_fp8(codes.data(), L.c_in, cw);
+      bias_dev.assign(b, b + cw);
+      bias_dev.insert(bias_dev.end(), scale.begin(), scale.begin() + cw);
+      if (L.c_out == 256) {
+        slice = f.size();
+        std::vector<uint8_t> f2 = conv_fragments_fp8(codes.data() + (size_t)128 * L.c_in * 27, L.c_in, 128);
+        f.insert(f.end(), f2.begin(), f2.end());
+        bias_dev.insert(bias_dev.end(), b + 128, b + 256);
+        bias_dev.insert(bias_dev.end(), scale.begin() + 128, scale.end());
+      }
+      s = upload(&wd, f.data(), f.size());
+    } else if (dtype != PD_DTYPE_FP32) {
+      // bf16 fragments (fp8 layer 1: of the E4M3 values times their scales,
+      // exact in bf16)
+      const float* wv = dtype == PD_DTYPE_FP8 ? wq.data() : w;
       std::vector<uint16_t> f;
       if (L.c_out == 256) {  // two slices of 128 output channels, back to back
-        f = conv_fragments(w, L.c_in, 128);
+        f = conv_fragments(wv, L.c_in, 128);
         slice = f.size() * 2;
-        std::vector<uint16_t> f2 = conv_fragments(w + (size_t)128 * L.c_in * 27, L.c_in, 128);
+        std::vector<uint16_t> f2 = conv_fragments(wv + (size_t)128 * L.c_in * 27, L.c_in, 128);
         f.insert(f.end(), f2.begin(), f2.end());
       } else {
-        f = conv_fragments(w, L.c_in, L.c_out);
+        f = conv_fragments(wv, L.c_in, L.c_out);
       }
       s = upload(&wd, f.data(), f.size() * 2);
     } else {
@@ -635,7 +758,7 @@ pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d
     h->wslice.push_back(slice);
     if (s != PD_OK) return fail(s);
     float* bd = nullptr;
-    s = upload(&bd, b, (size_t)L.c_out * 4);
+    s = upload(&bd, bias_dev.data(), bias_dev.size() * 4);
     h->bdev.push_back(bd);
     if (s != PD_OK) return fail(s);
   }
@@ -657,6 +780,19 @@ pd_status predecoder_residual(pd_predecoder* h, void* hip_stream, const uint64_t
   if (batch < 1 || batch > h->max_batch) return PD_ERR_INVALID_ARG;
   return check_launch(
       pd::launch_residual_from_flips(h->g, h->tables, det, flips, residual, batch, (hipStream_t)hip_stream));
+}
+
+pd_status predecoder_activations(pd_predecoder* h, void* hip_stream, const uint64_t* det, int32_t batch,
+                                 int32_t layer, void* out) {
+  if (!h || !det || !out) return PD_ERR_INVALID_ARG;
+  if (batch < 1 || batch > h->max_batch) return PD_ERR_INVALID_ARG;
+  if (layer < 0 || layer >= (int)h->layers.size() - 1) return PD_ERR_INVALID_ARG;
+  if (h->dtype == PD_DTYPE_FP32) return PD_ERR_UNSUPPORTED;
+  const hipStream_t st = (hipStream_t)hip_stream;
+  pd_status s = enqueue_run(h, st, det, batch, nullptr, nullptr, nullptr, nullptr, layer);
+  if (s != PD_OK) return s;
+  const int bytes = h->layers[layer].c_out * (h->dtype == PD_DTYPE_FP8 ? 1 : 2);
+  return check_launch(pd::launch_extract(h->g, h->act[layer & 1], bytes, batch, out, st));
 }
 
 pd_status predecoder_unpack(pd_predecoder* h, void* hip_stream, const uint64_t* det, int32_t batch,

@@ -14,9 +14,9 @@
 //     zero-halo planes, which stay in L2; taps past 26 contribute zero.
 //   * A operand: the layer's weight fragments (k-steps x c_out/32 blocks,
 //     16 bytes per lane each), staged in LDS once per workgroup.
-//   * Epilogue: + bias, activation, bf16; the wave transposes its 32 x c_out
-//     tile through its own LDS slice and writes whole voxel rows with
-//     16-byte stores.
+//   * Epilogue: + bias, activation, bf16 (or, on the fp8 path, E4M3: one
+//     byte per value); the wave transposes its 32 x c_out tile through its
+//     own LDS slice and writes whole voxel rows with 16-byte stores.
 #include "activation.h"
 #include "internal.h"
 
@@ -31,6 +31,7 @@ typedef __attribute__((address_space(3))) char lds_char;
 typedef __attribute__((address_space(3))) u32x2 lds_u32x2_w;
 typedef __attribute__((address_space(3))) const u32x4 lds_u32x4;
 typedef __attribute__((address_space(3))) u32x4 lds_u32x4_w;
+typedef __attribute__((address_space(3))) uint32_t lds_u32_w;
 
 constexpr int WAVES = 4;  // waves per workgroup
 constexpr int BPW = 2;    // 32-voxel blocks per wave
@@ -82,15 +83,17 @@ __device__ __forceinline__ void gather(const Geom& g, const void* __restrict__ p
 
 // Each workgroup stages the weight fragments in LDS once; each of its waves
 // then handles BPW consecutive 32-voxel blocks.
-template <int CIN, int COUT, int ACT>
+// F8: y holds E4M3 codes.
+template <int CIN, int COUT, int ACT, bool F8>
 __global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, const void* __restrict__ planes,
-                                                                uint16_t* __restrict__ y, int ystride,
+                                                                void* __restrict__ y, int ystride,
                                                                 const u32x4* __restrict__ wfrag,
                                                                 const float* __restrict__ bias, Decode dc,
                                                                 int nvox) {
   constexpr int NB = COUT / 32;
-  constexpr int OSTR = COUT * 2 + 16;  // padded LDS row stride (bytes)
-  constexpr int GPR = COUT / 8;        // 16-byte granules per voxel row
+  constexpr int ESZ = F8 ? 1 : 2;        // bytes per output value
+  constexpr int OSTR = COUT * ESZ + 16;  // padded LDS row stride (bytes)
+  constexpr int GPR = COUT * ESZ / 16;   // 16-byte granules per voxel row
   constexpr int KS = ksteps<CIN>();
   constexpr int WFR = KS * NB * 64;    // weight fragments x lanes (16 bytes each)
   extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -140,10 +143,14 @@ __global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, const vo
           const float v1 = act_fn<ACT>(acc[nb][4 * q + 1] + bias[co + 1]);
           const float v2 = act_fn<ACT>(acc[nb][4 * q + 2] + bias[co + 2]);
           const float v3 = act_fn<ACT>(acc[nb][4 * q + 3] + bias[co + 3]);
-          u32x2 packed;
-          packed.x = bf16_pack(v0, v1);
-          packed.y = bf16_pack(v2, v3);
-          *(lds_u32x2_w*)(tile + l32 * OSTR + co * 2) = packed;
+          if constexpr (F8) {
+            *(lds_u32_w*)(tile + l32 * OSTR + co) = e4m3_pack4(v0, v1, v2, v3);
+          } else {
+            u32x2 packed;
+            packed.x = bf16_pack(v0, v1);
+            packed.y = bf16_pack(v2, v3);
+            *(lds_u32x2_w*)(tile + l32 * OSTR + co * 2) = packed;
+          }
         }
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's tile is in LDS
@@ -155,7 +162,7 @@ __global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, const vo
       const int row = qq / GPR, c = qq % GPR;
       const int pr = ((__attribute__((address_space(3))) const int*)prow)[row];
       const u32x4 val = *(lds_u32x4*)(tile + row * OSTR + c * 16);
-      if (pr >= 0) *reinterpret_cast<u32x4*>(y + (long long)pr * ystride + c * 8) = val;
+      if (pr >= 0) *reinterpret_cast<u32x4*>((char*)y + (long long)pr * ystride * ESZ + c * 16) = val;
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);  // the tile's LDS reads are done before the next block writes it
     __builtin_amdgcn_wave_barrier();
@@ -165,7 +172,7 @@ __global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, const vo
 }  // namespace
 
 hipError_t launch_conv_first(const Geom& g, int cin, int cout, int act, const void* planes, void* y, int ystride,
-                             const void* wfrag, const float* bias, int batch, hipStream_t stream) {
+                             const void* wfrag, const float* bias, int batch, int fp8, hipStream_t stream) {
   const long long nvox = (long long)batch * g.V;  // < 2^31 (host check)
   const long long nblk = (nvox + 32 * WAVES * BPW - 1) / (32 * WAVES * BPW);
   Decode dc;
@@ -175,8 +182,14 @@ hipError_t launch_conv_first(const Geom& g, int cin, int cout, int act, const vo
   auto launch = [&](auto CI, auto CO, auto A) {
     constexpr int C = decltype(CO)::value, I = decltype(CI)::value;
     const size_t lds = (size_t)ksteps<I>() * (C / 32) * 64 * 16 + (size_t)WAVES * 32 * (C * 2 + 16 + 4);
-    hipLaunchKernelGGL((conv_first_kernel<I, C, decltype(A)::value>), dim3((unsigned)nblk), dim3(64 * WAVES), lds,
-                       stream, g, planes, (uint16_t*)y, ystride, (const u32x4*)wfrag, bias, dc, (int)nvox);
+    if (fp8)
+      hipLaunchKernelGGL((conv_first_kernel<I, C, decltype(A)::value, true>), dim3((unsigned)nblk),
+                         dim3(64 * WAVES), lds, stream, g, planes, y, ystride, (const u32x4*)wfrag, bias, dc,
+                         (int)nvox);
+    else
+      hipLaunchKernelGGL((conv_first_kernel<I, C, decltype(A)::value, false>), dim3((unsigned)nblk),
+                         dim3(64 * WAVES), lds, stream, g, planes, y, ystride, (const u32x4*)wfrag, bias, dc,
+                         (int)nvox);
   };
   if ((cin != 2 && cin != 4) || (cout != 64 && cout != 128) || act < 0 || act > 2) return hipErrorInvalidValue;
   with_activation(act, [&](auto A) {

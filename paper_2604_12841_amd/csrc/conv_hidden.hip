@@ -52,6 +52,8 @@ typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(16))) float f32x16;
 typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
 typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
+typedef __attribute__((ext_vector_type(8))) uint32_t u32x8;
+typedef __attribute__((ext_vector_type(8))) int i32x8;
 typedef __attribute__((address_space(3))) char lds_char;
 typedef __attribute__((address_space(3))) const u32x4 lds_u32x4;
 typedef __attribute__((address_space(3))) float lds_float;
@@ -75,6 +77,26 @@ static_assert(RMAX * NT >= 2 * MAX_SPAN && (RMAX * NT) % 32 == 0, "staging round
 static_assert(STEPS % BRING == 0, "the weight ring lines up with chunk boundaries");
 static_assert(RMAX * 3 + 3 <= STEPS, "staging rounds fit in a chunk");
 constexpr int ABUF = BUF_VOX * VSTRIDE;  // bytes per staging buffer
+
+// The fp8 (E4M3) variant keeps the 32 staged bytes per voxel and chunk, now
+// 32 channels, and runs v_mfma_f32_32x32x64_f8f6f4: k = 64 is two taps x 32
+// channels, the first half-wave's lanes holding a voxel's 32 channels at tap
+// 2 s, the second half-wave's at tap 2 s + 1 (tap 27 does not exist: its
+// weights are zero).  14 k-steps per chunk; staging round k loads at step
+// 2 k and stores at step 2 k + 2 (the last one after the chunk's last
+// step); the weight ring is 2 deep (32 bytes per lane and block).
+template <bool F8>
+struct Prec {
+  static constexpr int KCH = F8 ? 32 : KC;        // input channels per chunk
+  static constexpr int NSTEP = F8 ? 14 : STEPS;   // k-steps per chunk
+  static constexpr int RING = F8 ? 2 : BRING;     // weight ring depth
+  static constexpr int SG = F8 ? 2 : 3;           // steps between staging rounds
+  static constexpr int ESZ = F8 ? 1 : 2;          // bytes per activation value
+  static constexpr int WFRAG = F8 ? 2048 : 1024;  // bytes of one weight fragment (64 lanes)
+  static_assert(NSTEP % RING == 0, "the weight ring lines up with chunk boundaries");
+  static_assert(SG * (RMAX - 1) < NSTEP, "staging rounds load within a chunk");
+  static_assert(KCH * ESZ == 32, "a chunk stages 32 bytes per voxel");
+};
 
 // Staging granule q = NT k + tid: in each run of 32, the first 16 take
 // granule 0 of 16 consecutive staged voxels and the next 16 their granule 1,
@@ -112,14 +134,16 @@ struct Split {
 };
 
 // LDS layout of one workgroup (byte offsets): two staging buffers, a
-// 256-byte zero region (256-aligned, for halo-column reads), the bias
-// [COUT] and the head weights [4][COUT].  The head epilogue puts its
-// partial sums in the staging buffer the tile read last.
+// 512-byte zero region (256-aligned, for halo-column reads; an fp8 lane
+// reads 32 bytes from a redirected address), the bias [COUT] and the
+// per-channel weight scales [COUT] (fp8) and the head weights [4][COUT].
+// The head epilogue puts its partial sums in the staging buffer the tile
+// read last.
 template <int COUT>
 struct Lds {
   static constexpr int zero = 2 * ABUF;
-  static constexpr int bias = zero + 256;
-  static constexpr int headw = bias + COUT * 4;
+  static constexpr int bias = zero + 512;
+  static constexpr int headw = bias + 2 * COUT * 4;
   static constexpr int total = headw + 4 * COUT * 4;
   static_assert(zero % 256 == 0, "zero region must be 256-aligned");
   static_assert(2 * total <= 160 * 1024, "two workgroups per CU");
@@ -156,25 +180,28 @@ __host__ __device__ inline long long stage_base(const Geom& g, const StageSrc& s
   return wave_uniform(src.origin);
 }
 
-template <int CIN, int MODE>
+// ROW: bytes per activation voxel row (c_in values).
+template <int ROW, int MODE>
 __host__ __device__ inline uint32_t stage_offset(const Geom& g, const Tiling& tl, const StageSrc& src,
                                                  long long base, long long limit, int span, int k, int tid) {
   const int q = k * NT + tid;
   const int vv = stage_voxel(q);
   const long long gv = staged_voxel_fast<MODE>(g, tl, src, vv, limit);
-  return (vv < span && gv >= 0) ? (uint32_t)((gv - base) * (CIN * 2) + stage_gran(q) * 16) : kNoVoxel;
+  return (vv < span && gv >= 0) ? (uint32_t)((gv - base) * ROW + stage_gran(q) * 16) : kNoVoxel;
 }
 
-// Buffer resource over the activations from padded voxel `base`, channel
-// offset `ch` on.
-template <int CIN>
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t stage_rsrc(const uint16_t* x, long long base, int ch) {
-  return __builtin_amdgcn_make_buffer_rsrc((void*)(x + base * CIN + ch), 0, kStageRange, 0x00020000);
+// Buffer resource over the activations from padded voxel `base`, byte
+// `cb` of the row on (rows of ROW bytes).
+template <int ROW>
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t stage_rsrc(const void* x, long long base, int cb) {
+  return __builtin_amdgcn_make_buffer_rsrc((void*)((const char*)x + base * ROW + cb), 0, kStageRange, 0x00020000);
 }
 
-template <int CIN, int COUT, int EPI, int MODE>
+// F8: E4M3 activations and weights (bias holds [COUT] biases then [COUT]
+// per-channel weight scales; y and x hold one byte per value).
+template <int CIN, int COUT, int EPI, int MODE, bool F8>
 __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
-conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, uint16_t* __restrict__ y,
+conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void* __restrict__ y,
                    int ystride, const u32x4* __restrict__ wfrag, const float* __restrict__ bias,
                    const float* __restrict__ head_w, const float* __restrict__ head_b,
                    const int32_t* __restrict__ tables, uint8_t* __restrict__ nib,
@@ -185,11 +212,15 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
   constexpr int MB = W::MB;
   constexpr int NB = W::NB;
   constexpr int NBT = COUT / 32;  // 32-channel blocks in total
-  constexpr int NCHUNK = CIN / KC;
-  constexpr int TSTEPS = NCHUNK * STEPS;  // k-steps of the layer
+  using P = Prec<F8>;
+  constexpr int KCH = P::KCH, NSTEP = P::NSTEP, RING = P::RING, SG = P::SG;
+  constexpr int ROW = CIN * P::ESZ;  // bytes per input voxel row
+  constexpr int NCHUNK = CIN / KCH;
+  constexpr int TSTEPS = NCHUNK * NSTEP;  // k-steps of the layer
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave % W::WM, wn = wave / W::WM;
   const int half = lane >> 5, l32 = lane & 31;
+  const uint32_t hmask = half ? 0xFFFFFFFFu : 0u;  // fp8: selects the half-wave's tap
   const int ntiles = (int)tl.ntiles;
   const long long limit = (long long)batch * g.S;
   // Work units: (tile, part); part p of a tile runs its chunks [p NCU, (p+1) NCU)
@@ -204,9 +235,10 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
   lds_char* const lds = (lds_char*)smem;
   lds_char* const zero = lds + L::zero;
   lds_float* const bias_s = (lds_float*)(lds + L::bias);
+  lds_float* const scale_s = bias_s + COUT;  // fp8: per-channel weight scales
   lds_float* const headw_s = (lds_float*)(lds + L::headw);
-  for (int e = tid; e < COUT; e += NT) bias_s[e] = bias[e];
-  if (tid < 64) ((lds_u32_w*)zero)[tid] = 0u;
+  for (int e = tid; e < (F8 ? 2 : 1) * COUT; e += NT) bias_s[e] = bias[e];
+  if (tid < 128) ((lds_u32_w*)zero)[tid] = 0u;
   const uint32_t zero_addr = (uint32_t)(uintptr_t)zero;
   if (EPI == EPI_HEAD)
     for (int e = tid; e < 4 * COUT; e += NT) headw_s[e] = head_w[e];
@@ -235,8 +267,10 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
           for (int mb = 0; mb < MB; ++mb) {
             int b, t, i, j;
             if (tile_row_coords(g, tl, tile, wm * W::ROWS + mb * 32 + l32, batch, &b, &t, &i, &j)) {
-              const float lg[4] = {acc[mb][0][0] + bias_s[0], acc[mb][0][1] + bias_s[1], acc[mb][0][2] + bias_s[2],
-                                   acc[mb][0][3] + bias_s[3]};
+              float lg[4];
+#pragma unroll
+              for (int o = 0; o < 4; ++o)
+                lg[o] = F8 ? __builtin_fmaf(acc[mb][0][o], scale_s[o], bias_s[o]) : acc[mb][0][o] + bias_s[o];
               const int HH = g.H * g.H;
               const int s = i * g.H + j;
               nib[(long long)b * g.V + (long long)t * HH + s] = (uint8_t)flip_nibble(g, tables, i, j, lg);
@@ -253,7 +287,9 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
         // c of row r at c ^ (r % 8)), then stored as whole 128-byte halves of
         // voxel rows, 8 rows per instruction.  The next tile's first staging
         // store waits at a barrier until every wave is done here.
+        // (fp8: 64 bytes per row, four 16-byte granules of 16 channels)
         lds_char* const tb = ebuf + wave * (64 * 128);
+        constexpr int GR = F8 ? 4 : 8;  // 16-byte granules of a row's 64 channels
         with_activation(act, [&](auto A) {
           constexpr int ACT = decltype(A)::value;
 #pragma unroll
@@ -262,32 +298,45 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
             for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
               for (int q = 0; q < 4; ++q) {
-                const int c = nb * 4 + q;  // 16-byte granule of the wave's 64 channels
-                const int co = wn * 64 + c * 8 + half * 4;
+                const int c8 = nb * 4 + q;  // 8-channel group of the wave's 64 channels
+                const int co = wn * 64 + c8 * 8 + half * 4;
                 const float4 bv = {bias_s[co], bias_s[co + 1], bias_s[co + 2], bias_s[co + 3]};
+                float4 sv = {1.0f, 1.0f, 1.0f, 1.0f};
+                if constexpr (F8) sv = float4{scale_s[co], scale_s[co + 1], scale_s[co + 2], scale_s[co + 3]};
 #pragma unroll
                 for (int m = 0; m < 2; ++m) {
                   const int mb = 2 * ps + m;
-                  const float v0 = act_fn<ACT>(acc[mb][nb][4 * q + 0] + bv.x);
-                  const float v1 = act_fn<ACT>(acc[mb][nb][4 * q + 1] + bv.y);
-                  const float v2 = act_fn<ACT>(acc[mb][nb][4 * q + 2] + bv.z);
-                  const float v3 = act_fn<ACT>(acc[mb][nb][4 * q + 3] + bv.w);
-                  u32x2 packed;
-                  packed.x = bf16_pack(v0, v1);
-                  packed.y = bf16_pack(v2, v3);
                   const int r = m * 32 + l32;
-                  *(lds_u32x2_w*)(tb + r * 128 + ((c ^ (r & 7)) << 4) + half * 8) = packed;
+                  if constexpr (F8) {
+                    const float v0 = act_fn<ACT>(__builtin_fmaf(acc[mb][nb][4 * q + 0], sv.x, bv.x));
+                    const float v1 = act_fn<ACT>(__builtin_fmaf(acc[mb][nb][4 * q + 1], sv.y, bv.y));
+                    const float v2 = act_fn<ACT>(__builtin_fmaf(acc[mb][nb][4 * q + 2], sv.z, bv.z));
+                    const float v3 = act_fn<ACT>(__builtin_fmaf(acc[mb][nb][4 * q + 3], sv.w, bv.w));
+                    const int c = c8 >> 1;  // granule; byte (c8 & 1) 8 + 4 half within it
+                    *(lds_u32_w*)(tb + r * 128 + ((c ^ (r & 7)) << 4) + (c8 & 1) * 8 + half * 4) =
+                        e4m3_pack4(v0, v1, v2, v3);
+                  } else {
+                    const float v0 = act_fn<ACT>(acc[mb][nb][4 * q + 0] + bv.x);
+                    const float v1 = act_fn<ACT>(acc[mb][nb][4 * q + 1] + bv.y);
+                    const float v2 = act_fn<ACT>(acc[mb][nb][4 * q + 2] + bv.z);
+                    const float v3 = act_fn<ACT>(acc[mb][nb][4 * q + 3] + bv.w);
+                    u32x2 packed;
+                    packed.x = bf16_pack(v0, v1);
+                    packed.y = bf16_pack(v2, v3);
+                    *(lds_u32x2_w*)(tb + r * 128 + ((c8 ^ (r & 7)) << 4) + half * 8) = packed;
+                  }
                 }
               }
             __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's rows are in LDS
             __builtin_amdgcn_wave_barrier();
 #pragma unroll
-            for (int it2 = 0; it2 < 8; ++it2) {
+            for (int it2 = 0; it2 < GR; ++it2) {
               const int gi = it2 * 64 + lane;
-              const int r = gi >> 3, c = gi & 7;
+              const int r = F8 ? gi >> 2 : gi >> 3, c = F8 ? gi & 3 : gi & 7;
               const u32x4 v = *(lds_u32x4*)(tb + r * 128 + ((c ^ (r & 7)) << 4));
-              const int pr = __shfl(pidx[2 * ps + (it2 >> 2)], r & 31);
-              if (pr >= 0) *reinterpret_cast<u32x4*>(y + (long long)pr * ystride + wn * 64 + c * 8) = v;
+              const int pr = __shfl(pidx[2 * ps + (F8 ? it2 >> 1 : it2 >> 2)], r & 31);
+              if (pr >= 0)
+                *reinterpret_cast<u32x4*>((char*)y + ((long long)pr * ystride + wn * 64) * P::ESZ + c * 16) = v;
             }
             __builtin_amdgcn_s_waitcnt(0xc07f);  // the reads are done before the next pass writes
             __builtin_amdgcn_wave_barrier();
@@ -311,6 +360,8 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
             for (int q = 0; q < 4; ++q) {
               const int co = (wn * NB + nb) * 32 + q * 8 + half * 4;
               const float4 bv = {bias_s[co], bias_s[co + 1], bias_s[co + 2], bias_s[co + 3]};
+              float4 sv = {1.0f, 1.0f, 1.0f, 1.0f};
+              if constexpr (F8) sv = float4{scale_s[co], scale_s[co + 1], scale_s[co + 2], scale_s[co + 3]};
               float4 hw[4];
 #pragma unroll
               for (int o = 0; o < 4; ++o)
@@ -318,10 +369,15 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
                          headw_s[o * COUT + co + 3]};
 #pragma unroll
               for (int mb = 0; mb < MB; ++mb) {
-                const float a0 = bf16_round(act_fn<ACT>(acc[mb][nb][4 * q + 0] + bv.x));
-                const float a1 = bf16_round(act_fn<ACT>(acc[mb][nb][4 * q + 1] + bv.y));
-                const float a2 = bf16_round(act_fn<ACT>(acc[mb][nb][4 * q + 2] + bv.z));
-                const float a3 = bf16_round(act_fn<ACT>(acc[mb][nb][4 * q + 3] + bv.w));
+                // the head's input: the activation rounded as the next layer would read it
+                auto rnd = [&](float v, float sc, float bb) {
+                  if constexpr (F8) return e4m3_round(act_fn<ACT>(__builtin_fmaf(v, sc, bb)));
+                  else return bf16_round(act_fn<ACT>(v + bb));
+                };
+                const float a0 = rnd(acc[mb][nb][4 * q + 0], sv.x, bv.x);
+                const float a1 = rnd(acc[mb][nb][4 * q + 1], sv.y, bv.y);
+                const float a2 = rnd(acc[mb][nb][4 * q + 2], sv.z, bv.z);
+                const float a3 = rnd(acc[mb][nb][4 * q + 3], sv.w, bv.w);
 #pragma unroll
                 for (int o = 0; o < 4; ++o)
                   part[mb][o] += hw[o].x * a0 + hw[o].y * a1 + hw[o].z * a2 + hw[o].w * a3;
@@ -388,12 +444,12 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
   {
     const StageSrc src = source_of(tile);
 #pragma unroll
-    for (int k = 0; k < RMAX; ++k) soff[k] = stage_offset<CIN, MODE>(g, tl, src, cur_base, limit, tl.span, k, tid);
+    for (int k = 0; k < RMAX; ++k) soff[k] = stage_offset<ROW, MODE>(g, tl, src, cur_base, limit, tl.span, k, tid);
   }
 
   // First tile: stage its first chunk synchronously.
   {
-    const __amdgpu_buffer_rsrc_t rs = stage_rsrc<CIN>(x, cur_base, (unit & (ksplit - 1)) * NCU * KC);
+    const __amdgpu_buffer_rsrc_t rs = stage_rsrc<ROW>(x, cur_base, (unit & (ksplit - 1)) * NCU * 32);
 #pragma unroll
     for (int k = 0; k < RMAX; ++k) {
       const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(rs, soff[k], 0, 0);
@@ -401,22 +457,25 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
     }
   }
 
-  // weight fragment (tile-step gs, block nb of this wave's channels): a
-  // buffer load with this lane's 16-byte slot as the vector offset and the
-  // fragment's offset as the scalar one (no per-load address arithmetic)
+  // weight fragment (k-step gs, block nb of this wave's channels): buffer
+  // loads with this lane's slot (16 bytes; fp8: 32) as the vector offset and
+  // the fragment's offset as the scalar one (no per-load address arithmetic)
+  constexpr int WQ = F8 ? 2 : 1;  // 16-byte pieces per lane and fragment
   const __amdgpu_buffer_rsrc_t wres =
-      __builtin_amdgcn_make_buffer_rsrc((void*)wfrag, 0, TSTEPS * NBT * 1024, 0x00020000);
-  const uint32_t woff = (uint32_t)((wn * NB * 64 + lane) * 16);
-  auto wload = [&](int gs, int nb) -> u32x4 {
-    return __builtin_amdgcn_raw_buffer_load_b128(wres, woff, (gs * NBT + nb) * 1024, 0);
+      __builtin_amdgcn_make_buffer_rsrc((void*)wfrag, 0, TSTEPS * NBT * P::WFRAG, 0x00020000);
+  const uint32_t woff = (uint32_t)((wn * NB * 64 + lane) * 16 * WQ);
+  auto wload = [&](int gs, int nb, u32x4 (&dst)[WQ]) {
+#pragma unroll
+    for (int h = 0; h < WQ; ++h)
+      dst[h] = __builtin_amdgcn_raw_buffer_load_b128(wres, woff + 16 * h, (gs * NBT + nb) * P::WFRAG, 0);
   };
   // weight-fragment ring: slot k holds the k-step gs (of the layer's
-  // NCHUNK x 27), gs % BRING == k
-  u32x4 bq[BRING][NB];
+  // NCHUNK x NSTEP), gs % RING == k
+  u32x4 bq[RING][NB][WQ];
 #pragma unroll
-  for (int st = 0; st < BRING - 1; ++st)
+  for (int st = 0; st < RING - 1; ++st)
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) bq[st][nb] = wload((unit & (ksplit - 1)) * NCU * STEPS + st, nb);
+    for (int nb = 0; nb < NB; ++nb) wload((unit & (ksplit - 1)) * NCU * NSTEP + st, nb, bq[st][nb]);
   __syncthreads();  // staged chunk, bias, zero region and head weights visible
 
   int gchunk = 0;  // chunks processed by this workgroup (selects the LDS buffer)
@@ -437,7 +496,8 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
       long long p = -1, o;
       int lb = 0, col = -1;
       tile_row(g, tl, tile, wm * W::ROWS + mb * 32 + l32, batch, &p, &lb, &o, &col);
-      rrel[mb] = (uint32_t)(lb * VSTRIDE + half * 16);
+      // (fp8: both granules of the voxel, the tap set by the half-wave)
+      rrel[mb] = (uint32_t)(lb * VSTRIDE + (F8 ? 0 : half * 16));
       em0[mb] = (MODE == 0 && col == 0) ? 0xFFFFFF00u : 0u;
       em2[mb] = (MODE == 0 && col == g.H - 1) ? 0xFFFFFF00u : 0u;
     }
@@ -461,7 +521,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
       // the next tile's offsets replace soff round by round during the
       // last chunk (past the last tile: none, every granule empty)
       const __amdgpu_buffer_rsrc_t srs =
-          more ? stage_rsrc<CIN>(x, cur_base, (cc + 1) * KC) : stage_rsrc<CIN>(x, next_base, next_c0 * KC);
+          more ? stage_rsrc<ROW>(x, cur_base, (cc + 1) * 32) : stage_rsrc<ROW>(x, next_base, next_c0 * 32);
       u32x4 stg;
 
       uint32_t rbase[MB];
@@ -474,65 +534,121 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
       // group, so the read stays conflict-free).  rbase is made opaque before
       // each use so that every step computes its own addresses instead of
       // the compiler computing all of them at the top of the chunk.
-      auto frag_read = [&](int mb, int st) -> u32x4 {
+      // LDS offset of tap `tap` relative to a row's (0,0,0) tap, and the
+      // mask that sends a halo-column tap of a flat tile to `zero`
+      auto tap_off = [&](int tap) -> uint32_t {
+        const int dt = tap / 9, di = (tap / 3) % 3, dj = tap % 3;
+        return (uint32_t)((dt * tl.sa + di * tl.sb + dj) * VSTRIDE);
+      };
+      auto tap_mask = [&](int mb, int tap) -> uint32_t {
+        const int dj = tap % 3;
+        return dj == 0 ? em0[mb] : (dj == 2 ? em2[mb] : 0u);
+      };
+      auto redirect = [&](uint32_t a, uint32_t m) -> uint32_t {
+        uint32_t r;
+        asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(r) : "v"(m), "s"(zero_addr), "v"(a));
+        return r;
+      };
+      // B fragment of row block mb for k-step st (bf16: tap st, this lane's
+      // granule; fp8: tap 2 st + half, both granules): the tap's voxel offset
+      // is common to the (half-)wave; halo-column taps of flat tiles go to
+      // the zero region (v_bfi keeps the low 8 address bits: same bank group,
+      // so the read stays conflict-free).  rbase is made opaque before each
+      // use so that every step computes its own addresses instead of the
+      // compiler computing all of them at the top of the chunk.
+      constexpr int AQ = F8 ? 2 : 1;  // 16-byte pieces of a B fragment
+      auto frag_read = [&](int mb, int st, u32x4 (&dst)[AQ]) {
         asm volatile("" : "+v"(rbase[mb]));
-        const int dt = st / 9, di = (st / 3) % 3, dj = st % 3;
-        const uint32_t toff = (uint32_t)((dt * tl.sa + di * tl.sb + dj) * VSTRIDE);
-        uint32_t a = rbase[mb] + toff;
-        if (MODE == 0 && dj != 1) {
-          uint32_t r;
-          asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(r) : "v"(dj == 0 ? em0[mb] : em2[mb]), "s"(zero_addr), "v"(a));
-          a = r;
+        if constexpr (F8) {
+          // the half-wave's tap and halo mask are selected with the lane's
+          // half mask, made opaque here so that no per-step selection is
+          // hoisted out of the chunk loop (it would hold 14 x 4 registers)
+          uint32_t hm = hmask;
+          asm volatile("" : "+v"(hm));
+          const int t0 = 2 * st, t1 = 2 * st + 1 < 27 ? 2 * st + 1 : 2 * st;  // tap 27: zero weights
+          const uint32_t o0 = tap_off(t0), o1 = tap_off(t1);
+          uint32_t a = rbase[mb] + o0 + ((o1 - o0) & hm);
+          if (MODE == 0) {
+            const int dj0 = t0 % 3, dj1 = t1 % 3;
+            const uint32_t m0 = tap_mask(mb, t0), m1 = tap_mask(mb, t1);
+            if (dj0 != 1 && dj1 != 1) {
+              uint32_t m;
+              asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(m) : "v"(hm), "v"(m1), "v"(m0));
+              a = redirect(a, m);
+            } else if (dj0 != 1) {
+              a = redirect(a, m0 & ~hm);
+            } else if (dj1 != 1) {
+              a = redirect(a, m1 & hm);
+            }
+          }
+          dst[0] = *(lds_u32x4*)(uintptr_t)a;
+          dst[AQ - 1] = *(lds_u32x4*)(uintptr_t)(a + 16);
+        } else {
+          uint32_t a = rbase[mb] + tap_off(st);
+          if (MODE == 0 && st % 3 != 1) a = redirect(a, tap_mask(mb, st));
+          dst[0] = *(lds_u32x4*)(uintptr_t)a;
         }
-        return *(lds_u32x4*)(uintptr_t)a;
+      };
+      auto mfma = [&](const u32x4 (&w)[WQ], const u32x4 (&a)[AQ], f32x16 c) -> f32x16 {
+        if constexpr (F8) {
+          const i32x8 wa = __builtin_bit_cast(i32x8, u32x8{w[0].x, w[0].y, w[0].z, w[0].w, w[WQ - 1].x,
+                                                           w[WQ - 1].y, w[WQ - 1].z, w[WQ - 1].w});
+          const i32x8 ab = __builtin_bit_cast(i32x8, u32x8{a[0].x, a[0].y, a[0].z, a[0].w, a[AQ - 1].x,
+                                                           a[AQ - 1].y, a[AQ - 1].z, a[AQ - 1].w});
+          return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(wa, ab, c, 0, 0, 0, 0, 0, 0);
+        } else {
+          return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, w[0]),
+                                                         __builtin_bit_cast(bf16x8, a[0]), c, 0, 0, 0);
+        }
       };
       // One register set of activation fragments: av[mb] is re-read for the
       // next step as soon as this step's two MFMAs on it have issued, so it
       // has the other row blocks' MFMAs to arrive.  Weight fragments are
-      // loaded two steps ahead, staging rounds in the shadow of row block 0.
-      u32x4 av[MB];
+      // loaded RING - 1 steps ahead, staging rounds in the shadow of row
+      // block 0.
+      u32x4 av[MB][AQ];
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) av[mb] = frag_read(mb, 0);
-      const int gbase = cc * STEPS;              // k-step of this chunk's step 0
-      const int nbase = next_c0 * STEPS - STEPS;  // ... of the next unit's first chunk, minus STEPS
+      for (int mb = 0; mb < MB; ++mb) frag_read(mb, 0, av[mb]);
+      const int gbase = cc * NSTEP;              // k-step of this chunk's step 0
+      const int nbase = next_c0 * NSTEP - NSTEP;  // ... of the next unit's first chunk, minus NSTEP
+      // staging of the next chunk: round k is loaded at step SG k and stored
+      // to LDS at step SG (k + 1), just before round k + 1 is loaded (a round
+      // that would be stored past the last step is stored after it)
+      auto stage_store = [&](int k) {
+        // a tile's first chunk stages into the buffer the previous epilogue
+        // used (transposition or head partials): wait for every wave to
+        // leave it
+        if (k == 0 && chunk == 0) __builtin_amdgcn_s_barrier();
+        *(lds_u32x4_w*)(oth + stage_slot(k * NT + tid)) = stg;
+      };
 #pragma unroll
-      for (int st = 0; st < STEPS; ++st) {
+      for (int st = 0; st < NSTEP; ++st) {
         {
           // past the chunk's last step, the last chunk of a unit runs on
           // into the next unit's first steps
-          const int gs = (st + BRING - 1 < STEPS || more ? gbase : nbase) + st + BRING - 1;
+          const int gs = (st + RING - 1 < NSTEP || more ? gbase : nbase) + st + RING - 1;
 #pragma unroll
-          for (int nb = 0; nb < NB; ++nb) bq[(st + BRING - 1) % BRING][nb] = wload(gs, nb);
+          for (int nb = 0; nb < NB; ++nb) wload(gs, nb, bq[(st + RING - 1) % RING][nb]);
         }
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
 #pragma unroll
-          for (int nb = 0; nb < NB; ++nb)
-            acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, bq[st % BRING][nb]),
-                                                                  __builtin_bit_cast(bf16x8, av[mb]), acc[mb][nb],
-                                                                  0, 0, 0);
+          for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = mfma(bq[st % RING][nb], av[mb], acc[mb][nb]);
           __builtin_amdgcn_sched_barrier(0);
-          if (st + 1 < STEPS) av[mb] = frag_read(mb, st + 1);
+          if (st + 1 < NSTEP) frag_read(mb, st + 1, av[mb]);
           if (mb == 0) {
-            // staging of the next chunk: round k is loaded at step 3k and
-            // stored to LDS at step 3k + 3, just before round k + 1 is loaded
-            if (st >= 3 && st % 3 == 0 && st / 3 - 1 < RMAX) {
-              // a tile's first chunk stages into the buffer the previous
-              // epilogue used (transposition or head partials): wait for
-              // every wave to leave it
-              if (st == 3 && chunk == 0) __builtin_amdgcn_s_barrier();
-              *(lds_u32x4_w*)(oth + stage_slot((st / 3 - 1) * NT + tid)) = stg;
-            }
-            if (st % 3 == 0 && st / 3 < RMAX) {
-              const int k = st / 3;
-              if (!more) soff[k] = stage_offset<CIN, MODE>(g, tl, next_src, next_base, limit, sspan, k, tid);
+            if (st >= SG && st % SG == 0 && st / SG - 1 < RMAX) stage_store(st / SG - 1);
+            if (st % SG == 0 && st / SG < RMAX) {
+              const int k = st / SG;
+              if (!more) soff[k] = stage_offset<ROW, MODE>(g, tl, next_src, next_base, limit, sspan, k, tid);
               stg = __builtin_amdgcn_raw_buffer_load_b128(srs, soff[k], 0, 0);
             }
           }
           __builtin_amdgcn_sched_barrier(0);
         }
       }
+      if constexpr (SG * RMAX >= NSTEP) stage_store(RMAX - 1);
       // every wave's staging writes done, every wave done reading `cur`
       __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
       __builtin_amdgcn_s_barrier();
@@ -567,11 +683,12 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const uint16_t* __restrict__ x, u
 // in part order, then applies the epilogue of the unsplit kernel: bias,
 // activation, bf16 and a 16-byte store; or bias, activation, bf16 rounding,
 // the 1x1x1 head and the threshold; or, for the output layer, bias and the
-// threshold.
-template <int EPI, int ACT>
+// threshold.  F8: the sums are scaled by the channel's weight scale (bias
+// + cout) before the bias, and activations are stored as E4M3.
+template <int EPI, int ACT, bool F8>
 __global__ void __launch_bounds__(256) split_finish_kernel(Geom g, Tiling tl, int cout, int kshift,
                                                            const float* __restrict__ partial,
-                                                           const float* __restrict__ bias, uint16_t* __restrict__ y,
+                                                           const float* __restrict__ bias, void* __restrict__ y,
                                                            int ystride, const float* __restrict__ head_w,
                                                            const float* __restrict__ head_b,
                                                            const int32_t* __restrict__ tables,
@@ -584,7 +701,9 @@ __global__ void __launch_bounds__(256) split_finish_kernel(Geom g, Tiling tl, in
   const int rem = (int)(gid - (long long)tile * kTileRows * groups);
   const int r = rem / groups, grp = rem - r * groups;
   const int ksplit = 1 << kshift;
-  // sum of channels c .. c + 7 of this row over the tile's parts, part order
+  // pre-activation of channels c .. c + 7 of this row: the sum over the
+  // tile's parts in part order (fp8: times the channel's weight scale), plus
+  // the bias
   auto sum8 = [&](int c, float (&v)[8]) {
     for (int p = 0; p < ksplit; ++p) {
       const float* src = partial + ((size_t)((tile << kshift) + p) * kTileRows + r) * cout + c;
@@ -594,6 +713,8 @@ __global__ void __launch_bounds__(256) split_finish_kernel(Geom g, Tiling tl, in
 #pragma unroll
       for (int e = 0; e < 8; ++e) v[e] = p == 0 ? t[e] : v[e] + t[e];
     }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = F8 ? __builtin_fmaf(v[e], bias[cout + c + e], bias[c + e]) : v[e] + bias[c + e];
   };
   if constexpr (EPI == EPI_ACT) {
     long long pidx, o;
@@ -601,12 +722,16 @@ __global__ void __launch_bounds__(256) split_finish_kernel(Geom g, Tiling tl, in
     if (!tile_row(g, tl, tile, r, batch, &pidx, &lb, &o)) return;
     float v[8];
     sum8(grp * 8, v);
-    uint32_t w[4];
+    if constexpr (F8) {
+      const uint32_t w0 = e4m3_pack4(act_fn<ACT>(v[0]), act_fn<ACT>(v[1]), act_fn<ACT>(v[2]), act_fn<ACT>(v[3]));
+      const uint32_t w1 = e4m3_pack4(act_fn<ACT>(v[4]), act_fn<ACT>(v[5]), act_fn<ACT>(v[6]), act_fn<ACT>(v[7]));
+      *reinterpret_cast<uint2*>((uint8_t*)y + pidx * ystride + grp * 8) = uint2{w0, w1};
+    } else {
+      uint32_t w[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
-      w[e] = bf16_pack(act_fn<ACT>(v[2 * e] + bias[grp * 8 + 2 * e]),
-                       act_fn<ACT>(v[2 * e + 1] + bias[grp * 8 + 2 * e + 1]));
-    *reinterpret_cast<uint4*>(y + pidx * ystride + grp * 8) = uint4{w[0], w[1], w[2], w[3]};
+      for (int e = 0; e < 4; ++e) w[e] = bf16_pack(act_fn<ACT>(v[2 * e]), act_fn<ACT>(v[2 * e + 1]));
+      *reinterpret_cast<uint4*>((uint16_t*)y + pidx * ystride + grp * 8) = uint4{w[0], w[1], w[2], w[3]};
+    }
   } else {
     int b, t, i, j;
     if (!tile_row_coords(g, tl, tile, r, batch, &b, &t, &i, &j)) return;
@@ -615,7 +740,7 @@ __global__ void __launch_bounds__(256) split_finish_kernel(Geom g, Tiling tl, in
       float v[8];
       sum8(0, v);
 #pragma unroll
-      for (int o2 = 0; o2 < 4; ++o2) lg[o2] = v[o2] + bias[o2];
+      for (int o2 = 0; o2 < 4; ++o2) lg[o2] = v[o2];
     } else {
 #pragma unroll
       for (int o2 = 0; o2 < 4; ++o2) lg[o2] = head_b[o2];
@@ -624,7 +749,7 @@ __global__ void __launch_bounds__(256) split_finish_kernel(Geom g, Tiling tl, in
         sum8(c, v);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const float a = bf16_round(act_fn<ACT>(v[e] + bias[c + e]));
+          const float a = F8 ? e4m3_round(act_fn<ACT>(v[e])) : bf16_round(act_fn<ACT>(v[e]));
 #pragma unroll
           for (int o2 = 0; o2 < 4; ++o2) lg[o2] += head_w[o2 * cout + c + e] * a;
         }
@@ -642,75 +767,62 @@ __global__ void __launch_bounds__(256) split_finish_kernel(Geom g, Tiling tl, in
 
 // Launches one instance of the hidden kernel (the LDS size attribute set on
 // its first use).
-template <int CIN, int COUT, int EPI, int MODE>
+template <int CIN, int COUT, int EPI, int MODE, bool F8>
 hipError_t launch_hidden(const Geom& g, const Tiling& tl, int act, const void* x, void* y, int ystride,
                          const void* wfrag, const float* bias, const float* head_w, const float* head_b,
                          const int32_t* tables, uint8_t* nib, float* logits, int batch, int n_workgroups,
                          int kshift, float* partial, hipStream_t stream) {
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)conv_hidden_kernel<CIN, COUT, EPI, MODE>,
+    hipError_t e = hipFuncSetAttribute((const void*)conv_hidden_kernel<CIN, COUT, EPI, MODE, F8>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, Lds<COUT>::total);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
   const long long nwg = conv_workgroups(tl.ntiles << kshift, n_workgroups);
-  hipLaunchKernelGGL((conv_hidden_kernel<CIN, COUT, EPI, MODE>), dim3((unsigned)nwg), dim3(NT),
-                     (size_t)Lds<COUT>::total, stream, g, tl, act, (const uint16_t*)x, (uint16_t*)y, ystride,
-                     (const u32x4*)wfrag, bias, head_w, head_b, tables, nib, logits, batch, kshift, partial);
+  hipLaunchKernelGGL((conv_hidden_kernel<CIN, COUT, EPI, MODE, F8>), dim3((unsigned)nwg), dim3(NT),
+                     (size_t)Lds<COUT>::total, stream, g, tl, act, x, y, ystride, (const u32x4*)wfrag, bias, head_w,
+                     head_b, tables, nib, logits, batch, kshift, partial);
   return hipSuccess;
 }
 
-template <int CIN, int COUT, int EPI, int MODE>
+template <int CIN, int COUT, int EPI, int MODE, bool F8>
 hipError_t launch_one(const Geom& g, const Tiling& tl, int act, const void* x, void* y, int ystride,
                       const void* wfrag, const float* bias, const float* head_w, const float* head_b,
                       const int32_t* tables, uint8_t* nib, float* logits, int batch, int n_workgroups,
                       const Split_k& sk, hipStream_t stream) {
   hipError_t e;
   if (sk.kshift == 0) {
-    e = launch_hidden<CIN, COUT, EPI, MODE>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b, tables, nib,
-                                            logits, batch, n_workgroups, 0, nullptr, stream);
+    e = launch_hidden<CIN, COUT, EPI, MODE, F8>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b, tables,
+                                                nib, logits, batch, n_workgroups, 0, nullptr, stream);
     return e != hipSuccess ? e : hipGetLastError();
   }
   // K loops split: park the parts, then add them and finish the tiles
-  e = launch_hidden<CIN, COUT, EPI_PARK, MODE>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b, tables, nib,
-                                               logits, batch, n_workgroups, sk.kshift, sk.partial, stream);
+  e = launch_hidden<CIN, COUT, EPI_PARK, MODE, F8>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b, tables,
+                                                   nib, logits, batch, n_workgroups, sk.kshift, sk.partial, stream);
   if (e != hipSuccess) return e;
   const long long threads = tl.ntiles * kTileRows * (EPI == EPI_ACT ? COUT / 8 : 1);
   with_activation(act, [&](auto A) {
-    hipLaunchKernelGGL((split_finish_kernel<EPI, decltype(A)::value>), dim3((unsigned)((threads + 255) / 256)),
-                       dim3(256), 0, stream, g, tl, COUT, sk.kshift, sk.partial, bias, (uint16_t*)y, ystride, head_w,
-                       head_b, tables, nib, logits, batch);
+    hipLaunchKernelGGL((split_finish_kernel<EPI, decltype(A)::value, F8>), dim3((unsigned)((threads + 255) / 256)),
+                       dim3(256), 0, stream, g, tl, COUT, sk.kshift, sk.partial, bias, y, ystride, head_w, head_b,
+                       tables, nib, logits, batch);
   });
   return hipGetLastError();
 }
 
-}  // namespace
-
-int conv_hidden_max_span() { return MAX_SPAN; }
-size_t conv_hidden_partial_floats_per_unit() { return (size_t)kTileRows * 128; }
-int conv_hidden_workgroups_per_cu() { return 2; }
-
-#define PD_HIDDEN_CASE(CI, CO, E)                                                              \
-  if (cin == CI && cout == CO && head == E) {                                                 \
-    if (tl.mode == 0)                                                                          \
-      return launch_one<CI, CO, E, 0>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b, \
-                                      tables, nib, logits, batch, n_workgroups, sk, stream);   \
-    return launch_one<CI, CO, E, 1>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b,   \
-                                    tables, nib, logits, batch, n_workgroups, sk, stream);     \
+template <bool F8>
+hipError_t launch_case(const Geom& g, const Tiling& tl, int cin, int cout, int act, const void* x, void* y,
+                       int ystride, const void* wfrag, const float* bias, int head, const float* head_w,
+                       const float* head_b, const int32_t* tables, uint8_t* nib, float* logits, int batch,
+                       int n_workgroups, const Split_k& sk, hipStream_t stream) {
+#define PD_HIDDEN_CASE(CI, CO, E)                                                                  \
+  if (cin == CI && cout == CO && head == E) {                                                     \
+    if (tl.mode == 0)                                                                              \
+      return launch_one<CI, CO, E, 0, F8>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b, \
+                                          tables, nib, logits, batch, n_workgroups, sk, stream);   \
+    return launch_one<CI, CO, E, 1, F8>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b,   \
+                                        tables, nib, logits, batch, n_workgroups, sk, stream);     \
   }
-
-hipError_t launch_conv_hidden(const Geom& g, const Tiling& tl, int cin, int cout, int act, const void* x,
-                              void* y, int ystride, const void* wfrag, const float* bias, int head,
-                              const float* head_w, const float* head_b, const int32_t* tables, uint8_t* nib,
-                              float* logits, int batch, int n_workgroups, const Split_k& sk,
-                              hipStream_t stream) {
-  if (tl.span <= 0 || tl.span > MAX_SPAN) return hipErrorInvalidValue;
-  // parts per tile: a power of two dividing the layer's chunks, with room
-  // for every unit's sums
-  if (sk.kshift < 0 || (cin / KC) % (1 << sk.kshift) != 0 ||
-      (sk.kshift > 0 && (tl.ntiles << sk.kshift) > sk.max_units))
-    return hipErrorInvalidValue;
   PD_HIDDEN_CASE(64, 64, EPI_ACT)
   PD_HIDDEN_CASE(128, 128, EPI_ACT)
   PD_HIDDEN_CASE(64, 128, EPI_ACT)
@@ -725,7 +837,34 @@ hipError_t launch_conv_hidden(const Geom& g, const Tiling& tl, int cin, int cout
   PD_HIDDEN_CASE(64, 32, EPI_OUT)
   PD_HIDDEN_CASE(128, 32, EPI_OUT)
   PD_HIDDEN_CASE(256, 32, EPI_OUT)
+#undef PD_HIDDEN_CASE
   return hipErrorInvalidValue;
 }
+
+}  // namespace
+
+int conv_hidden_max_span() { return MAX_SPAN; }
+size_t conv_hidden_partial_floats_per_unit() { return (size_t)kTileRows * 128; }
+int conv_hidden_workgroups_per_cu() { return 2; }
+
+hipError_t launch_conv_hidden(const Geom& g, const Tiling& tl, int cin, int cout, int act, const void* x,
+                              void* y, int ystride, const void* wfrag, const float* bias, int head,
+                              const float* head_w, const float* head_b, const int32_t* tables, uint8_t* nib,
+                              float* logits, int batch, int n_workgroups, const Split_k& sk, int fp8,
+                              hipStream_t stream) {
+  if (tl.span <= 0 || tl.span > MAX_SPAN) return hipErrorInvalidValue;
+  // parts per tile: a power of two dividing the layer's chunks, with room
+  // for every unit's sums
+  const int nchunk = cin / (fp8 ? Prec<true>::KCH : Prec<false>::KCH);
+  if (sk.kshift < 0 || nchunk % (1 << sk.kshift) != 0 || (sk.kshift > 0 && (tl.ntiles << sk.kshift) > sk.max_units))
+    return hipErrorInvalidValue;
+  if (fp8)
+    return launch_case<true>(g, tl, cin, cout, act, x, y, ystride, wfrag, bias, head, head_w, head_b, tables, nib,
+                             logits, batch, n_workgroups, sk, stream);
+  return launch_case<false>(g, tl, cin, cout, act, x, y, ystride, wfrag, bias, head, head_w, head_b, tables, nib,
+                            logits, batch, n_workgroups, sk, stream);
+}
+
+int conv_hidden_chunk_channels(int fp8) { return fp8 ? Prec<true>::KCH : Prec<false>::KCH; }
 
 }  // namespace pd

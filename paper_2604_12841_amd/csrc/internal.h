@@ -120,8 +120,12 @@ hipError_t launch_unpack(const Geom& g, const int32_t* tables, const uint64_t* d
 // [ceil(27 c_in / 16) k-steps][c_out / 32][64 lanes][8 bf16].  Output voxel
 // rows are ystride channels apart (a wider layer is run as slices of c_out
 // channels, y pointing at the slice's first channel).
+// fp8: y holds E4M3 codes (one byte per value; the planes and the bf16
+// weight fragments are unchanged, the weights being E4M3 values times their
+// power-of-two scales, which bf16 represents exactly).
 hipError_t launch_conv_first(const Geom& g, int cin, int cout, int act, const void* planes, void* y,
-                             int ystride, const void* wfrag, const float* bias, int batch, hipStream_t stream);
+                             int ystride, const void* wfrag, const float* bias, int batch, int fp8,
+                             hipStream_t stream);
 
 // A network with one hidden layer: layer 1 (as launch_conv_first) with the
 // 1x1x1 head (head_w [4][cout] fp32, bf16-valued; head_b [4]) and the
@@ -133,7 +137,10 @@ hipError_t launch_conv_single(const Geom& g, const Tiling& tl, int cout, int act
                               int n_workgroups, hipStream_t stream);
 int conv_single_max_span();  // staged voxels a tile may need
 
-// A 3x3x3 bf16 layer on the zero-halo activations x (c_in in {64, 128, 256}).
+// A 3x3x3 layer on the zero-halo activations x (c_in in {64, 128, 256}),
+// bf16, or fp8 (E4M3 activations and weight codes, bias holding c_out
+// biases then c_out per-channel weight scales, one byte per value in x and
+// y, fragments of conv_fragments_fp8 in 32-channel chunks).
 //   head == 0: a hidden layer (c_out in {64, 128}) writing y, whose voxel rows
 //              are ystride channels apart (a 256-wide layer runs as two slices
 //              of 128, y pointing at the slice's first channel);
@@ -144,7 +151,7 @@ int conv_single_max_span();  // staged voxels a tile may need
 // Weight fragments in 16-channel chunks (conv_fragments in api.hip; c_out = 4
 // padded to 32 channels, bias to 32 values); n_workgroups =
 // conv_hidden_workgroups_per_cu() per CU.
-// Small batches: each tile's K loop (its 16-channel chunks) split into
+// Small batches: each tile's K loop (its channel chunks) split into
 // 2^kshift parts run by different workgroups of one launch, which park fp32
 // sums in `partial` (max_units units of conv_hidden_partial_floats_per_unit()
 // floats); a second launch adds each tile's parts in part order and runs the
@@ -158,11 +165,16 @@ struct Split_k {
 hipError_t launch_conv_hidden(const Geom& g, const Tiling& tl, int cin, int cout, int act, const void* x,
                               void* y, int ystride, const void* wfrag, const float* bias, int head,
                               const float* head_w, const float* head_b, const int32_t* tables, uint8_t* nib,
-                              float* logits, int batch, int n_workgroups, const Split_k& sk,
+                              float* logits, int batch, int n_workgroups, const Split_k& sk, int fp8,
                               hipStream_t stream);
 int conv_hidden_max_span();
+int conv_hidden_chunk_channels(int fp8);  // input channels per K-loop chunk
 size_t conv_hidden_partial_floats_per_unit();
 int conv_hidden_workgroups_per_cu();
+
+// Copies the interior voxel rows (row_bytes each, a multiple of 16) of a
+// zero-halo activation buffer to out [batch][T][H][H] rows.
+hipError_t launch_extract(const Geom& g, const void* act, int row_bytes, int batch, void* out, hipStream_t stream);
 
 // Persistent workgroups of a conv launch: one per CU (n_workgroups), a
 // multiple of 8 (one per XCD round-robin slot), never more than the tiles

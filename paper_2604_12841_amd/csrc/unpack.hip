@@ -102,3 +102,33 @@ hipError_t launch_unpack(const Geom& g, const int32_t* tables, const uint64_t* d
 }
 
 }  // namespace pd
+
+namespace pd {
+
+// One thread per 16-byte granule of an interior voxel row: out[(b, t, i, j)]
+// <- act[padded (b, t, i, j)].
+__global__ void __launch_bounds__(256) extract_kernel(Geom g, const uint4* __restrict__ act, int gran, int batch,
+                                                      uint4* __restrict__ out) {
+  const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  const long long total = (long long)batch * g.V * gran;
+  if (gid >= total) return;
+  const long long vox = gid / gran;
+  const int q = (int)(gid - vox * gran);
+  const int b = (int)(vox / g.V);
+  const int v = (int)(vox - (long long)b * g.V);
+  const int HH = g.H * g.H;
+  const int t = v / HH, s = v - t * HH;
+  const int i = s / g.H, j = s - i * g.H;
+  out[gid] = act[padded_index(g, b, t, i, j) * gran + q];
+}
+
+hipError_t launch_extract(const Geom& g, const void* act, int row_bytes, int batch, void* out, hipStream_t stream) {
+  if (row_bytes <= 0 || row_bytes % 16 != 0) return hipErrorInvalidValue;
+  const int gran = row_bytes / 16;
+  const long long total = (long long)batch * g.V * gran;
+  hipLaunchKernelGGL(extract_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream, g,
+                     (const uint4*)act, gran, batch, (uint4*)out);
+  return hipGetLastError();
+}
+
+}  // namespace pd

@@ -1,0 +1,61 @@
+"""Writes fp8_tolerance.json: the parity bounds of the fp8 path, from the
+oracle alone.
+
+The fp8 matrix instruction (v_mfma_f32_32x32x64_f8f6f4) does not round its
+64-product sums exactly: on gfx950 its result differs from the exact sum by
+up to 1.1e-5 (about 2^-16.4) of the sum of the products' magnitudes (random
+E4M3 operands, 1024 sums).  An activation next to an E4M3 rounding boundary
+can then round to the other neighbour, and the difference (one E4M3 step)
+spreads through the later layers.  The model: the oracle's fp8 forward with
+every sum moved by u EPS sum|products| (u in [-1, 1), hashed), EPS = 2^-16,
+which bounds that error over any number of sums (triangle inequality), against
+the exact oracle.  On every fp8 parity case (tests/fp8_cases.py) this records
+the max abs logit difference (and, for information, the fraction of logits
+that differ by more than 1e-3); the bound is MARGIN times the largest.
+
+Run from the repository root:  python tests/golden/make_fp8_tolerance.py
+"""
+import json
+import os
+import sys
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, os.path.dirname(HERE))                   # tests/
+sys.path.insert(0, os.path.dirname(os.path.dirname(HERE)))  # repository root
+
+import oracle  # noqa: E402
+from fp8_cases import FP8_CASES, case_inputs  # noqa: E402
+
+MARGIN = 2.0
+FAR_ABS = 1e-3
+EPS = 2.0 ** -16
+
+
+def main():
+    rows = []
+    for case in FP8_CASES:
+        d, T, layers, weights, det, layout, first, last = case_inputs(case)
+        planes = oracle.unpack_paper(d, T, det, first, last) if layout == "paper" else oracle.unpack(d, T, det)
+        a = oracle.forward(d, T, planes, layers, weights, False, layout, fp8=True)
+        b = oracle.forward(d, T, planes, layers, weights, False, layout, fp8=True, fp8_sum_eps=EPS)
+        err = np.abs(a - b)
+        row = dict(name=case["name"], max_abs=float(err.max()), frac_far=float((err > FAR_ABS).mean()),
+                   median_abs_logit=float(np.median(np.abs(a))))
+        print(row, flush=True)
+        rows.append(row)
+    out = dict(
+        note="fp8 parity bounds: MARGIN x the largest difference between the oracle's exact fp8 forward and "
+             "the same with every sum moved by up to EPS sum|products| over the fp8 parity cases "
+             "(make_fp8_tolerance.py)",
+        margin=MARGIN, far_abs=FAR_ABS, eps=EPS,
+        tol_max_abs_logit_err=MARGIN * max(r["max_abs"] for r in rows),
+        cases=rows)
+    with open(os.path.join(HERE, "fp8_tolerance.json"), "w") as f:
+        json.dump(out, f, indent=1)
+    print("tol", out["tol_max_abs_logit_err"])
+
+
+if __name__ == "__main__":
+    main()

@@ -5,15 +5,28 @@ fp32); thresholded flips and residual bits agree exactly, except at sites
 whose oracle |logit| < tol ("excused": either outcome is within the
 tolerance).  A residual bit is excused when any of the flips it XORs in is.
 Excused counts are reported; non-excused mismatches must be 0.
+
+fp8 (whole networks): the fp8 matrix instruction sums its products with an
+error up to about 2^-16 of their magnitudes, so an activation next to an
+E4M3 rounding boundary can round either way, and the difference (one E4M3
+step) spreads through the later layers.  The max abs logit error is bounded
+by tests/golden/make_fp8_tolerance.py (the oracle with every sum moved by up
+to that error, times a margin); a flip is excused only where the site's own
+logit error reaches its oracle |logit| (the threshold outcome the two logits
+imply).  Tight per-site checks of the fp8 layers are in test_gpu_fp8.py.
 """
 import functools
+import json
+import os
 
 import numpy as np
 
 import oracle
 from paper_2604_12841_amd import workload
 
-TOL = {"bf16": 2e-2, "fp32": 1e-4}
+_FP8 = json.load(open(os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "fp8_tolerance.json")))
+TOL = {"bf16": 2e-2, "fp32": 1e-4, "fp8": _FP8["tol_max_abs_logit_err"]}
+FAR_ABS = 1e-3  # a logit "far" from the oracle's (reported)
 
 
 @functools.lru_cache(maxsize=None)
@@ -50,14 +63,17 @@ def residual_contributions(d):
     return np.array(meas), np.array(data)
 
 
-def excused_masks(d, T, logits, tol, layout="plaquette"):
-    """(flip_excused [B][T*(3d^2-1)], residual_excused [B][T*(d^2-1)]) bool."""
+def excused_masks(d, T, logits, tol, layout="plaquette", site_tol=None):
+    """(flip_excused [B][T*(3d^2-1)], residual_excused [B][T*(d^2-1)]) bool.
+    site_tol (shape of logits): per-site bound used instead of tol
+    (excused where |logit| <= site_tol)."""
     fs = flip_sites(d, layout)
     B = logits.shape[0]
     F = 3 * d * d - 1
     S = d * d - 1
-    lf = logits[:, fs[:, 0][None, :].repeat(T, 0), np.arange(T)[:, None], fs[:, 1][None, :], fs[:, 2][None, :]]
-    fex = (np.abs(lf) < tol).reshape(B, T, F)
+    sel = (slice(None), fs[:, 0][None, :].repeat(T, 0), np.arange(T)[:, None], fs[:, 1][None, :], fs[:, 2][None, :])
+    lf = logits[sel]
+    fex = ((np.abs(lf) < tol) if site_tol is None else (np.abs(lf) <= site_tol[sel])).reshape(B, T, F)
     meas, data = residual_contributions(d)
     rex = fex[:, :, meas].copy()
     rex[:, 1:] |= fex[:, :-1, meas]
@@ -78,7 +94,13 @@ def compare(d, T, dtype, ref_logits, ref_flips, ref_res, got_flips, got_res, got
     B = ref_logits.shape[0]
     F = T * (3 * d * d - 1)
     S = T * (d * d - 1)
-    fex, rex = excused_masks(d, T, ref_logits, tol, layout)
+    err = None if got_logits is None else np.abs(got_logits.astype(np.float64) - ref_logits)
+    if dtype == "fp8":
+        if err is None:
+            raise ValueError("the fp8 rule needs the logits")
+        fex, rex = excused_masks(d, T, ref_logits, tol, layout, site_tol=err + 1e-7)
+    else:
+        fex, rex = excused_masks(d, T, ref_logits, tol, layout)
     rf = workload.unpack_rows(ref_flips, F).astype(bool)
     gf = workload.unpack_rows(got_flips, F).astype(bool)
     rr = workload.unpack_rows(ref_res, S).astype(bool)
@@ -96,8 +118,9 @@ def compare(d, T, dtype, ref_logits, ref_flips, ref_res, got_flips, got_res, got
         flip_padding_ok=bool(_padding_zero(got_flips, F)),
         res_padding_ok=bool(_padding_zero(got_res, S)),
     )
-    if got_logits is not None:
-        out["max_abs_logit_err"] = float(np.max(np.abs(got_logits.astype(np.float64) - ref_logits)))
+    if err is not None:
+        out["max_abs_logit_err"] = float(err.max())
+        out["frac_far"] = float((err > FAR_ABS).mean())
     return out
 
 

@@ -126,6 +126,8 @@ def test_create_rejects_null_pointers():
     ([(2, 64, 3, 1), (64, 4, 3, 0)], pdx.DTYPE_BF16),          # 3x3x3 head
     ([(2, 4, 1, 0)], pdx.DTYPE_BF16),                          # no hidden layer
     ([(2, 20, 3, 1), (20, 4, 1, 0)], pdx.DTYPE_FP32),          # fp32 width not a multiple of 8
+    ([(2, 64, 3, 1), (64, 4, 1, 0)], pdx.DTYPE_FP8),           # fp8: one hidden layer with a 1x1x1 head
+    ([(2, 32, 3, 1), (32, 32, 3, 1), (32, 4, 1, 0)], pdx.DTYPE_FP8),  # fp8 width 32
 ])
 def test_create_unsupported_shapes(layers, dtype):
     w = workload.he_normal_weights(layers, 0)
@@ -185,6 +187,7 @@ def test_create_ex_rejects_misuse(case):
     (workload.paper_model_layers(3), pdx.DTYPE_BF16),                  # 5x5x5 kernels (Model 3)
     (workload.paper_layer_spec([256, 256, 4], [3, 3, 1]), pdx.DTYPE_BF16),  # width 256 with a 1x1x1 head
     (workload.paper_layer_spec([192, 4], [3, 3]), pdx.DTYPE_BF16),     # width 192
+    (workload.paper_model_layers(3), pdx.DTYPE_FP8),                   # 5x5x5 kernels in fp8
 ])
 def test_create_ex_unsupported_models(layers, dtype):
     w = np.zeros(pdx.weight_count(layers), np.float32)
