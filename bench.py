@@ -26,6 +26,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+PEAK_FP8_TFLOPS = 5000.0   # MI355X dense fp8 MFMA
 PEAK_HBM_GBS = 8000.0
 
 
@@ -77,6 +78,9 @@ def main():
                     help="time a model of Table models (1, 2, 4 or 5) in the paper's own layout (D x D grid, four "
                          "input channels, 3x3x3 output layer) at d = T = --d instead of a workload")
     ap.add_argument("--d", type=int, default=13, help="distance (and rounds) for --paper-model")
+    ap.add_argument("--dtype", choices=["bf16", "fp8"], default=None,
+                    help="operand precision (default: the workload's, bf16 for the benchmark workload); fp8 = "
+                         "E4M3 weights and activations with fp32 accumulation, the paper's deployment precision")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the path is data-parallel over independent volumes and "
@@ -97,7 +101,7 @@ def main():
         layers = workload.paper_model_layers(args.paper_model)
         weights = workload.he_normal_weights(layers, 4000 + args.paper_model)
         det, _ = workload.make_inputs(d, T, B, 0.003, 0.003, 5000 + d)
-        cfg = dict(dtype="bf16", p=0.003, n_hidden=len(layers) - 1, width=layers[0][1])
+        cfg = dict(dtype=args.dtype or "bf16", p=0.003, n_hidden=len(layers) - 1, width=layers[0][1])
         grid = d
     else:
         cfg = workload.CONFIGS[args.workload]
@@ -107,10 +111,17 @@ def main():
         weights = workload.config_weights(args.workload)
         det, _ = workload.config_inputs(args.workload, B)
         grid = d + 1
+        if args.dtype:
+            if cfg["dtype"] == "fp32":
+                print("--dtype applies to the bf16 workloads", file=sys.stderr)
+                sys.exit(2)
+            cfg = dict(cfg, dtype=args.dtype)
+    fp8 = cfg["dtype"] == "fp8"
+    peak = PEAK_FP8_TFLOPS if fp8 else PEAK_BF16_TFLOPS
 
     torch.cuda.set_device(0)
     if paper:
-        pre = pdx.Predecoder(weights, d, T, layers, "bf16", max_batch=B, layout="paper", first="Z", last="Z")
+        pre = pdx.Predecoder(weights, d, T, layers, cfg["dtype"], max_batch=B, layout="paper", first="Z", last="Z")
     else:
         pre = pdx.Predecoder(weights, d, T, layers, cfg["dtype"], max_batch=B)
     ddet = torch.from_numpy(det.view(np.int64)).cuda()
@@ -157,11 +168,11 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": ms,
         "us_per_round": ms * 1e3 / rounds,
-        "mfma_frac_end_to_end": total_flops / (ms * 1e-3) / (PEAK_BF16_TFLOPS * 1e12),
+        "mfma_frac_end_to_end": total_flops / (ms * 1e-3) / (peak * 1e12),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16" if cfg["dtype"] == "bf16" else "f32",
+        "dtype": {"bf16": "bf16", "fp8": "fp8-e4m3", "fp32": "f32"}[cfg["dtype"]],
         "data": "synthetic (seeded phenomenological noise, He-normal random weights)",
         "config": {
             "workload": "rotated surface code d=%d, T=%d rounds, batch %d; %d conv3d 3x3x3 layers x %d "
@@ -173,13 +184,15 @@ def main():
                      **{"layer%d" % (i + 1): stages[1 + i] for i in range(n - 1)},
                      "head_threshold": stages[n], "residual_repack": stages[n + 1]},
         "roofline": {
-            "kernel": "conv3d 3x3x3 %d->%d implicit GEMM (bf16 MFMA) + bias/GELU epilogue" % (ci, co),
+            "kernel": "conv3d 3x3x3 %d->%d implicit GEMM (%s MFMA) + bias/GELU epilogue"
+                      % (ci, co, "fp8 e4m3" if fp8 else "bf16"),
             "bound": "mfma",
             "achieved": achieved,
-            "peak": PEAK_BF16_TFLOPS,
+            "peak": peak,
             "unit": "TFLOP/s",
-            "frac": achieved / PEAK_BF16_TFLOPS,
-            "traffic": counted_traffic("conv_hidden_%dx%d_d%d_T%d_B%d_counters.md" % (ci, co, d, T, B)),
+            "frac": achieved / peak,
+            "traffic": counted_traffic("conv_hidden_%dx%d_d%d_T%d_B%d%s_counters.md"
+                                       % (ci, co, d, T, B, "_fp8" if fp8 else "")),
         },
     }
 
@@ -198,8 +211,8 @@ def main():
             "higher_is_better": False,
             "rounds_per_s": rounds / (ms * 1e-3),
             "config": {"workload": "Model %d of Table models (%s), paper layout: D x D grid, 4 input channels, "
-                                   "3x3x3 output layer; d=T=%d, batch %d; bf16 / fp32 accumulate; p=q=0.003"
-                                   % (args.paper_model, layers, d, B),
+                                   "3x3x3 output layer; d=T=%d, batch %d; %s / fp32 accumulate; p=q=0.003"
+                                   % (args.paper_model, layers, d, B, cfg["dtype"]),
                        "d": d, "T": T, "batch": B, "model": args.paper_model},
             "paper_context_us_per_round": ctx.get(args.paper_model, {}).get(d),
         })
@@ -217,14 +230,14 @@ def main():
         oracle.build()
         oracle.unpack(d, T, det[:1])  # load the library outside the timed region
         t0 = time.perf_counter()
-        oracle.run(d, T, det[:ns], layers, weights, bf16=(cfg["dtype"] == "bf16"))
+        oracle.run(d, T, det[:ns], layers, weights, bf16=(cfg["dtype"] == "bf16"), fp8=fp8)
         dt = time.perf_counter() - t0
         cores = oracle.num_threads()
         out["cpu_baseline"] = {
             "value": ns * T / dt, "unit": "rounds/s", "cores": cores, "kind": "oracle",
-            "sample": "%d of the %d samples (%.1f s, fp64 oracle with bf16 rounding points, "
+            "sample": "%d of the %d samples (%.1f s, fp64 oracle with %s rounding points, "
                       "OpenMP over samples x output channels, %d host CPUs visible)"
-                      % (ns, B, dt, len(os.sched_getaffinity(0))),
+                      % (ns, B, dt, cfg["dtype"], len(os.sched_getaffinity(0))),
         }
     pre.close()
     if args.copy_mib:
