@@ -246,6 +246,50 @@ int64_t predecoder_flip_words(int32_t d, int32_t T);
  * parameter count of Table models); 0 on bad args. */
 size_t predecoder_weight_count(const pd_layer* layers, int32_t n_layers);
 
+/* ---- Temporal windows over a long stream (Sec. VI, parallel windows in
+ * time, after the parallel-window scheme the paper cites) ----
+ *
+ * A stream of n_rounds rounds is cut into windows: window k commits the core
+ * rounds [k core, min((k+1) core, n_rounds)) and also reads `buffer` rounds
+ * before and after them (clipped to the stream).  The pre-decoder is local:
+ * an output more than its receptive-field half-width h = sum over layers of
+ * (k - 1) / 2 rounds from a window edge equals the output of one run over the
+ * whole stream, so with buffer >= h the stitched cores are the whole-stream
+ * corrections (up to the rounding-order rule of the handle's precision).  The
+ * paper uses core = buffer = d (d x d x 3d blocks).  Windows are run as one
+ * batch per window length (all windows of all streams at once: the paper
+ * decodes the commit and cleanup blocks concurrently on several GPUs, or
+ * several per GPU with a larger batch); the residual is then computed once
+ * over the stitched flips of the whole stream. */
+typedef struct pd_stream pd_stream; /* opaque */
+
+/* The window plan (host only): fills starts / lengths / core_starts /
+ * core_lengths (capacity entries each) and returns the number of windows,
+ * ceil(n_rounds / core); with NULL arrays returns that number only.  -1 for
+ * n_rounds < 1, core < 1, buffer < 0 or a capacity below the count. */
+int32_t predecoder_stream_windows(int32_t n_rounds, int32_t core, int32_t buffer, int32_t* starts,
+                                  int32_t* lengths, int32_t* core_starts, int32_t* core_lengths,
+                                  int32_t capacity);
+
+/* A driver for n_streams streams (independent logical qubits) of n_rounds
+ * rounds at distance d: the arguments of predecoder_create_ex (weights
+ * copied; the same precisions, layouts and shapes), plus the window plan.
+ * opts->first_round / last_round apply to the windows at the stream's ends.
+ * Creates one handle per window length; allocates device memory. */
+pd_status predecoder_stream_create(const float* weights, size_t n_weights, int32_t d, int32_t n_rounds,
+                                   int32_t core, int32_t buffer, const pd_layer* layers, int32_t n_layers,
+                                   int32_t dtype, int32_t n_streams, const pd_options* opts, pd_stream** out);
+
+/* det: device, [n_streams][W_det(d, n_rounds)] uint64 packed detectors;
+ * flips: device, [n_streams][W_flip(d, n_rounds)], the stitched corrections;
+ * residual: device, [n_streams][W_det(d, n_rounds)], the residual of the
+ * whole stream from them.  Asynchronous on hip_stream. */
+pd_status predecoder_stream_run(pd_stream* s, void* hip_stream, const uint64_t* det, uint64_t* flips,
+                                uint64_t* residual);
+
+/* Releases the driver (NULL is a no-op); waits for the device. */
+void predecoder_stream_destroy(pd_stream* s);
+
 #ifdef __cplusplus
 }
 #endif

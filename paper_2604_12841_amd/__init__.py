@@ -12,7 +12,7 @@ memory and streams); streams are passed as their raw hipStream_t handles.
 import ctypes
 import os
 
-__all__ = ["Predecoder", "PredecoderError", "Options", "lib", "det_words", "flip_words", "weight_count",
+__all__ = ["Predecoder", "Stream", "stream_windows", "PredecoderError", "Options", "lib", "det_words", "flip_words", "weight_count",
            "status_string", "ACT_NONE", "ACT_GELU_TANH", "ACT_RELU", "DTYPE_FP32", "DTYPE_BF16", "DTYPE_FP8",
            "LAYOUT_PLAQUETTE", "LAYOUT_PAPER", "BOUNDARY_NONE", "BOUNDARY_Z", "BOUNDARY_X", "LIB_PATH",
            "EXPORTS"]
@@ -33,7 +33,8 @@ EXPORTS = ("predecoder_create", "predecoder_create_ex", "predecoder_run", "prede
            "predecoder_activations",
            "predecoder_num_stages", "predecoder_stage_times", "predecoder_destroy",
            "predecoder_status_string", "predecoder_det_words", "predecoder_flip_words",
-           "predecoder_weight_count")
+           "predecoder_weight_count", "predecoder_stream_windows", "predecoder_stream_create",
+           "predecoder_stream_run", "predecoder_stream_destroy")
 
 
 class PredecoderError(RuntimeError):
@@ -90,6 +91,16 @@ def lib():
         L.predecoder_flip_words.restype = i64
         L.predecoder_weight_count.argtypes = [LP, i32]
         L.predecoder_weight_count.restype = sz
+        IP = ctypes.POINTER(i32)
+        L.predecoder_stream_windows.argtypes = [i32, i32, i32, IP, IP, IP, IP, i32]
+        L.predecoder_stream_windows.restype = i32
+        L.predecoder_stream_create.argtypes = [vp, sz, i32, i32, i32, i32, LP, i32, i32, i32, ctypes.POINTER(Options),
+                                               ctypes.POINTER(vp)]
+        L.predecoder_stream_create.restype = i32
+        L.predecoder_stream_run.argtypes = [vp, vp, vp, vp, vp]
+        L.predecoder_stream_run.restype = i32
+        L.predecoder_stream_destroy.argtypes = [vp]
+        L.predecoder_stream_destroy.restype = None
         _lib = L
     return _lib
 
@@ -199,6 +210,57 @@ class Predecoder:
     def close(self):
         if getattr(self, "_h", None):
             lib().predecoder_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def stream_windows(n_rounds, core, buffer):
+    """The temporal window plan: list of (start, length, core_start, core_length)."""
+    L = lib()
+    n = L.predecoder_stream_windows(n_rounds, core, buffer, None, None, None, None, 0)
+    if n < 0:
+        raise ValueError("invalid window plan")
+    arrs = [(ctypes.c_int32 * n)() for _ in range(4)]
+    L.predecoder_stream_windows(n_rounds, core, buffer, *arrs, n)
+    return [tuple(int(a[k]) for a in arrs) for k in range(n)]
+
+
+class Stream:
+    """Temporal window driver over n_streams streams of n_rounds rounds (Sec. VI, parallel windows in time)."""
+
+    def __init__(self, weights, d, n_rounds, layers, core, buffer, dtype="bf16", n_streams=1, layout="plaquette",
+                 first=None, last=None):
+        import numpy as np
+        w = np.ascontiguousarray(np.asarray(weights, dtype=np.float32))
+        self.d, self.n_rounds, self.n_streams = d, n_rounds, n_streams
+        self.det_words = det_words(d, n_rounds)
+        self.flip_words = flip_words(d, n_rounds)
+        lay = _LAYOUTS[layout] if isinstance(layout, str) else int(layout)
+        opts = Options(lay, _BOUNDARIES[first] if not isinstance(first, int) else first,
+                       _BOUNDARIES[last] if not isinstance(last, int) else last)
+        dt = _DTYPES[dtype] if isinstance(dtype, str) else int(dtype)
+        h = ctypes.c_void_p()
+        st = lib().predecoder_stream_create(w.ctypes.data_as(ctypes.c_void_p), w.size, d, n_rounds, core, buffer,
+                                            _layers(layers), len(layers), dt, n_streams, ctypes.byref(opts),
+                                            ctypes.byref(h))
+        if st != PD_OK:
+            raise PredecoderError(st, "predecoder_stream_create")
+        self._h = h
+
+    def run(self, det, flips, residual, stream=None):
+        """det [n_streams][W_det] -> flips [n_streams][W_flip], residual [n_streams][W_det] (device, in place)."""
+        st = lib().predecoder_stream_run(self._h, _stream(stream), _ptr(det), _ptr(flips), _ptr(residual))
+        if st != PD_OK:
+            raise PredecoderError(st, "predecoder_stream_run")
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().predecoder_stream_destroy(self._h)
             self._h = None
 
     def __del__(self):

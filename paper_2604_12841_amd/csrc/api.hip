@@ -10,6 +10,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <array>
 #include <cmath>
 #include <cstring>
 #include <new>
@@ -843,6 +844,162 @@ void predecoder_destroy(pd_predecoder* h) {
   (void)hipDeviceSynchronize();
   free_all(h);
   delete h;
+}
+
+int32_t predecoder_stream_windows(int32_t n_rounds, int32_t core, int32_t buffer, int32_t* starts, int32_t* lengths,
+                                  int32_t* core_starts, int32_t* core_lengths, int32_t capacity) {
+  if (n_rounds < 1 || core < 1 || buffer < 0) return -1;
+  const int32_t n = (n_rounds + core - 1) / core;
+  if (!starts || !lengths || !core_starts || !core_lengths) return n;
+  if (capacity < n) return -1;
+  for (int32_t k = 0; k < n; ++k) {
+    const int32_t c0 = k * core, c1 = std::min(n_rounds, c0 + core);
+    const int32_t w0 = std::max(0, c0 - buffer), w1 = std::min(n_rounds, c1 + buffer);
+    starts[k] = w0;
+    lengths[k] = w1 - w0;
+    core_starts[k] = c0;
+    core_lengths[k] = c1 - c0;
+  }
+  return n;
+}
+
+}  // extern "C"
+
+// Temporal window driver: windows of the planner grouped by (length,
+// touches round 0, touches the last round); one handle per group runs all
+// its windows of all streams as one batch.
+struct pd_stream {
+  int d = 0, n_rounds = 0, core = 0, buffer = 0, n_streams = 0;
+  pd::Geom g;                          // the whole stream (for its residual)
+  int32_t* tables = nullptr;           // its site tables
+  std::vector<pd::StreamWindow> win;   // host copy
+  pd::StreamWindow* win_dev = nullptr;
+  struct Group {
+    int len = 0, count = 0;
+    pd_predecoder* h = nullptr;
+    uint64_t *det = nullptr, *flips = nullptr, *res = nullptr;
+    pd::StreamWindow* win_dev = nullptr;  // this group's windows, in slot order
+  };
+  std::vector<Group> groups;
+  uint64_t** group_flips_dev = nullptr;
+  long long* group_words_dev = nullptr;
+};
+
+namespace {
+void stream_free(pd_stream* s) {
+  for (auto& g : s->groups) {
+    if (g.h) predecoder_destroy(g.h);
+    if (g.det) (void)hipFree(g.det);
+    if (g.flips) (void)hipFree(g.flips);
+    if (g.res) (void)hipFree(g.res);
+    if (g.win_dev) (void)hipFree(g.win_dev);
+  }
+  if (s->tables) (void)hipFree(s->tables);
+  if (s->win_dev) (void)hipFree(s->win_dev);
+  if (s->group_flips_dev) (void)hipFree(s->group_flips_dev);
+  if (s->group_words_dev) (void)hipFree(s->group_words_dev);
+  delete s;
+}
+}  // namespace
+
+extern "C" {
+
+pd_status predecoder_stream_create(const float* weights, size_t n_weights, int32_t d, int32_t n_rounds, int32_t core,
+                                   int32_t buffer, const pd_layer* layers, int32_t n_layers, int32_t dtype,
+                                   int32_t n_streams, const pd_options* opts, pd_stream** out) {
+  if (!out) return PD_ERR_INVALID_ARG;
+  *out = nullptr;
+  if (!weights || !layers || n_rounds < 1 || core < 1 || buffer < 0 || n_streams < 1) return PD_ERR_INVALID_ARG;
+  if (d < 3 || d % 2 == 0 || n_rounds > kMaxT) return d < 3 || d % 2 == 0 ? PD_ERR_INVALID_ARG : PD_ERR_UNSUPPORTED;
+  const pd_options o = opts ? *opts : pd_options{PD_LAYOUT_PLAQUETTE, PD_BOUNDARY_NONE, PD_BOUNDARY_NONE};
+  const int32_t nw = predecoder_stream_windows(n_rounds, core, buffer, nullptr, nullptr, nullptr, nullptr, 0);
+  if (nw < 1) return PD_ERR_INVALID_ARG;
+  std::vector<int32_t> st(nw), ln(nw), cs(nw), cl(nw);
+  predecoder_stream_windows(n_rounds, core, buffer, st.data(), ln.data(), cs.data(), cl.data(), nw);
+  pd_stream* s = new (std::nothrow) pd_stream();
+  if (!s) return PD_ERR_OUT_OF_MEMORY;
+  s->d = d;
+  s->n_rounds = n_rounds;
+  s->core = core;
+  s->buffer = buffer;
+  s->n_streams = n_streams;
+  // group key: length, first-round window, last-round window (the paper
+  // layout clears its geometric channels only at the stream's own ends)
+  std::vector<std::array<int, 3>> keys;
+  s->win.resize(nw);
+  for (int k = 0; k < nw; ++k) {
+    const std::array<int, 3> key{ln[k], st[k] == 0, st[k] + ln[k] == n_rounds};
+    int gi = (int)(std::find(keys.begin(), keys.end(), key) - keys.begin());
+    if (gi == (int)keys.size()) {
+      keys.push_back(key);
+      s->groups.emplace_back();
+      s->groups.back().len = ln[k];
+    }
+    s->win[k] = pd::StreamWindow{st[k], ln[k], cs[k], cl[k], gi, s->groups[gi].count++};
+  }
+  pd_status r = PD_OK;
+  auto fail = [&](pd_status e) {
+    stream_free(s);
+    return e;
+  };
+  for (size_t gi = 0; gi < s->groups.size(); ++gi) {
+    auto& G = s->groups[gi];
+    pd_options go = o;
+    if (!keys[gi][1]) go.first_round = PD_BOUNDARY_NONE;
+    if (!keys[gi][2]) go.last_round = PD_BOUNDARY_NONE;
+    r = predecoder_create_ex(weights, n_weights, d, G.len, layers, n_layers, dtype, G.count * n_streams, &go, &G.h);
+    if (r != PD_OK) return fail(r);
+    const size_t rows = (size_t)G.count * n_streams;
+    if ((r = dev_alloc(&G.det, rows * predecoder_det_words(d, G.len) * 8)) != PD_OK) return fail(r);
+    if ((r = dev_alloc(&G.flips, rows * predecoder_flip_words(d, G.len) * 8)) != PD_OK) return fail(r);
+    if ((r = dev_alloc(&G.res, rows * predecoder_det_words(d, G.len) * 8)) != PD_OK) return fail(r);
+    std::vector<pd::StreamWindow> mine;
+    for (const auto& w : s->win)
+      if (w.group == (int)gi) mine.push_back(w);
+    if ((r = upload(&G.win_dev, mine.data(), mine.size() * sizeof(pd::StreamWindow))) != PD_OK) return fail(r);
+  }
+  s->g = make_geom(d, n_rounds, o.layout, o.first_round, o.last_round);
+  std::vector<int32_t> tab = build_tables(s->g);
+  if ((r = upload(&s->tables, tab.data(), tab.size() * sizeof(int32_t))) != PD_OK) return fail(r);
+  if ((r = upload(&s->win_dev, s->win.data(), s->win.size() * sizeof(pd::StreamWindow))) != PD_OK) return fail(r);
+  std::vector<uint64_t*> gf;
+  std::vector<long long> gw;
+  for (auto& G : s->groups) {
+    gf.push_back(G.flips);
+    gw.push_back(predecoder_flip_words(d, G.len));
+  }
+  if ((r = upload(&s->group_flips_dev, gf.data(), gf.size() * sizeof(uint64_t*))) != PD_OK) return fail(r);
+  if ((r = upload(&s->group_words_dev, gw.data(), gw.size() * sizeof(long long))) != PD_OK) return fail(r);
+  if (hipDeviceSynchronize() != hipSuccess) return fail(PD_ERR_DEVICE);
+  *out = s;
+  return PD_OK;
+}
+
+pd_status predecoder_stream_run(pd_stream* s, void* hip_stream, const uint64_t* det, uint64_t* flips,
+                                uint64_t* residual) {
+  if (!s || !det || !flips || !residual) return PD_ERR_INVALID_ARG;
+  const hipStream_t st = (hipStream_t)hip_stream;
+  const int S = s->d * s->d - 1, F = 3 * s->d * s->d - 1;
+  const long long det_words = predecoder_det_words(s->d, s->n_rounds);
+  const long long flip_words = predecoder_flip_words(s->d, s->n_rounds);
+  pd_status r;
+  for (auto& G : s->groups) {
+    r = check_launch(pd::launch_stream_gather(det, det_words, G.win_dev, G.count, s->n_streams, S,
+                                              predecoder_det_words(s->d, G.len), G.det, st));
+    if (r != PD_OK) return r;
+    r = predecoder_run(G.h, hip_stream, G.det, G.count * s->n_streams, G.flips, G.res, nullptr);
+    if (r != PD_OK) return r;
+  }
+  r = check_launch(pd::launch_stream_scatter(s->win_dev, s->group_flips_dev, s->group_words_dev, s->n_streams,
+                                             s->core, s->n_rounds, F, flip_words, flips, st));
+  if (r != PD_OK) return r;
+  return check_launch(pd::launch_residual_from_flips(s->g, s->tables, det, flips, residual, s->n_streams, st));
+}
+
+void predecoder_stream_destroy(pd_stream* s) {
+  if (!s) return;
+  (void)hipDeviceSynchronize();
+  stream_free(s);
 }
 
 }  // extern "C"

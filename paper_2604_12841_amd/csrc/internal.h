@@ -176,6 +176,27 @@ int conv_hidden_workgroups_per_cu();
 // zero-halo activation buffer to out [batch][T][H][H] rows.
 hipError_t launch_extract(const Geom& g, const void* act, int row_bytes, int batch, void* out, hipStream_t stream);
 
+// Temporal windows over a stream of rounds (Sec. VI, parallel windows in
+// time): window k covers rounds [start, start + len) of every stream and
+// commits its core rounds [core_start, core_start + core_len); it is row
+// `slot * n_streams + s` of its group's batch (group: the windows of one
+// length and boundary kind, run by one handle).
+struct StreamWindow {
+  int start, len, core_start, core_len, group, slot;
+};
+
+// Window detector rows from stream rows (row_words words per stream row,
+// out_words per window row; S bits per round).
+hipError_t launch_stream_gather(const uint64_t* det, long long row_words, const StreamWindow* win, int n_win,
+                                int n_streams, int S, long long out_words, uint64_t* out, hipStream_t stream);
+// Stream flip rows (row_words words each; F bits per round) from the
+// windows' flip rows (group g: group_flips[g], group_words[g] words per row),
+// each round taken from the window whose core holds it (window k's core
+// starts at round k * core).
+hipError_t launch_stream_scatter(const StreamWindow* win, const uint64_t* const* group_flips,
+                                 const long long* group_words, int n_streams, int core, int n_rounds, int F,
+                                 long long row_words, uint64_t* flips, hipStream_t stream);
+
 // Persistent workgroups of a conv launch: one per CU (n_workgroups), a
 // multiple of 8 (one per XCD round-robin slot), never more than the tiles
 // need.
