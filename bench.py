@@ -62,6 +62,59 @@ def flops_per_sample(layers, H, T):
     return sum(2 * ci * co * k ** 3 for (ci, co, k, _a) in layers) * V
 
 
+def bench_stream(args, torch, pdx, workload):
+    """The temporal window driver (Sec. VI, parallel windows in time): a model
+    of Table models over --stream rounds at distance --d, --batch streams,
+    windows of d x d x 3d (core d, buffer d), everything on one GPU."""
+    d, n, B = args.d, args.stream, args.batch or 1
+    core, buf = args.core or d, d if args.buffer is None else args.buffer
+    dtype = args.dtype or "bf16"
+    layers = workload.paper_model_layers(args.paper_model)
+    weights = workload.he_normal_weights(layers, 4000 + args.paper_model)
+    det, _ = workload.make_inputs(d, n, B, 0.003, 0.003, 6000 + d)
+    torch.cuda.set_device(0)
+    s = pdx.Stream(weights, d, n, layers, core, buf, dtype, n_streams=B, layout="paper", first="Z", last="Z")
+    ddet = torch.from_numpy(det.view(np.int64)).cuda()
+    flips = torch.empty((B, s.flip_words), dtype=torch.int64, device="cuda")
+    res = torch.empty((B, s.det_words), dtype=torch.int64, device="cuda")
+    cur = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        s.run(ddet, flips, res, stream=cur)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(cur)
+    for _ in range(args.steps):
+        s.run(ddet, flips, res, stream=cur)
+    e1.record(cur)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    s.close()
+    plan = pdx.stream_windows(n, core, buf)
+    nwin = len(plan)
+    h = sum((k - 1) // 2 for (_, _, k, _) in layers)  # receptive-field half-width: buffer >= h is exact
+    # Table Time_Like_Parallel_Table (GB300, FP8, one GPU per d x d x 3d block
+    # or `batch` blocks per GPU): us/round for 1000 rounds -- context only
+    ctx = {(1, 13, 1): 0.11, (1, 13, 2): 0.13, (1, 13, 4): 0.179, (1, 21, 1): 0.179, (1, 21, 2): 0.244,
+           (1, 21, 4): 0.423, (4, 13, 1): 0.138, (4, 13, 2): 0.211, (4, 13, 4): 0.282, (4, 21, 1): 0.231,
+           (4, 21, 2): 0.324, (4, 21, 4): 0.551}
+    out = {
+        "metric": "us/round over a %d-round stream, temporal windows (Table models Model %d, paper layout, d=%d)"
+                  % (n, args.paper_model, d),
+        "value": ms * 1e3 / n, "unit": "us/round", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms, "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
+        "dtype": {"bf16": "bf16", "fp8": "fp8-e4m3"}[dtype],
+        "data": "synthetic (seeded phenomenological noise p=q=0.003, He-normal random weights)",
+        "config": {"workload": "%d stream(s) of %d rounds at d=%d, Model %d (%s); %d windows per stream (core %d, "
+                               "buffer %d rounds; exact for buffer >= %d), all run on one GPU as one batch per "
+                               "window length" % (B, n, d, args.paper_model, layers, nwin, core, buf, h),
+                   "d": d, "rounds": n, "streams": B, "model": args.paper_model, "windows_per_stream": nwin,
+                   "core": core, "buffer": buf, "computed_rounds_per_stream": sum(w[1] for w in plan)},
+        "us_per_round_per_stream": ms * 1e3 / n / B,
+        "paper_context_us_per_round": ctx.get((args.paper_model, d, B)) if (core, buf) == (d, d) else None,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -78,6 +131,11 @@ def main():
                     help="time a model of Table models (1, 2, 4 or 5) in the paper's own layout (D x D grid, four "
                          "input channels, 3x3x3 output layer) at d = T = --d instead of a workload")
     ap.add_argument("--d", type=int, default=13, help="distance (and rounds) for --paper-model")
+    ap.add_argument("--stream", type=int, default=None,
+                    help="with --paper-model: time the temporal window driver over a stream of this many rounds "
+                         "(windows of d x d x 3d rounds: core d, buffer d), --batch streams at once")
+    ap.add_argument("--core", type=int, default=None, help="--stream: committed rounds per window (default d)")
+    ap.add_argument("--buffer", type=int, default=None, help="--stream: rounds read on each side (default d)")
     ap.add_argument("--dtype", choices=["bf16", "fp8"], default=None,
                     help="operand precision (default: the workload's, bf16 for the benchmark workload); fp8 = "
                          "E4M3 weights and activations with fp32 accumulation, the paper's deployment precision")
@@ -93,6 +151,11 @@ def main():
     from paper_2604_12841_amd import workload
 
     paper = args.paper_model is not None
+    if args.stream is not None:
+        if not paper:
+            print("--stream needs --paper-model", file=sys.stderr)
+            sys.exit(2)
+        return bench_stream(args, torch, pdx, workload)
     if paper:
         # Table models in the paper's layout: memory experiment in the Z basis
         # (x_present cleared in the first and last round), d = T
