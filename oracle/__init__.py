@@ -73,6 +73,10 @@ def _load():
         lib.oracle_forward_grid_fp8_perturbed.restype = None
         lib.oracle_flips_residual_paper.argtypes = [i32, i32, i32, vp, vp, vp, vp]
         lib.oracle_flips_residual_paper.restype = None
+        lib.oracle_resnet_weight_count.argtypes = [i32, vp, i32]
+        lib.oracle_resnet_weight_count.restype = i64
+        lib.oracle_forward_resnet.argtypes = [i32, i32, i32, vp, i32, vp, vp, i32, vp]
+        lib.oracle_forward_resnet.restype = None
         lib.oracle_e4m3_value.argtypes = [i32]
         lib.oracle_e4m3_value.restype = ctypes.c_double
         lib.oracle_e4m3_code.argtypes = [ctypes.c_float]
@@ -269,5 +273,41 @@ def run(d, T, det, layers, weights, bf16, layout="plaquette", first=None, last=N
         flips, res = flips_residual_paper(d, T, logits, det)
     else:
         logits = forward(d, T, unpack(d, T, det), layers, weights, bf16, fp8=fp8)
+        flips, res = flips_residual(d, T, logits, det)
+    return logits, flips, res
+
+
+def resnet_weight_count(blocks, bn_per_channel=4):
+    """Floats of a residual network's weights; blocks: (c_in, c_mid, c_out, act).  bn_per_channel = 4
+    (scale, shift, running mean, running variance) as the weights are passed, 2 for the trainable count."""
+    spec = np.ascontiguousarray(np.array([list(b) for b in blocks], dtype=np.int32).ravel())
+    return int(_load().oracle_resnet_weight_count(len(blocks), _ptr(spec), bn_per_channel))
+
+
+def forward_resnet(d, T, planes, blocks, weights, bf16, layout="plaquette"):
+    """Residual network forward (Model 6, Sec. VI, Fig. Model8Representation).  planes [B][c_in][T][H][H];
+    blocks: (c_in, c_mid, c_out, act); returns logits [B][4][T][H][H]."""
+    planes = np.ascontiguousarray(planes, dtype=np.float64)
+    weights = np.ascontiguousarray(weights, dtype=np.float32)
+    spec = np.ascontiguousarray(np.array([list(b) for b in blocks], dtype=np.int32).ravel())
+    if weights.size != resnet_weight_count(blocks):
+        raise ValueError("weight count mismatch")
+    B = planes.shape[0]
+    H = d if layout == "paper" else d + 1
+    if planes.shape[1:] != (blocks[0][0], T, H, H) or blocks[-1][2] != 4:
+        raise ValueError("planes / blocks mismatch")
+    out = np.zeros((B, 4, T, H, H), dtype=np.float64)
+    _load().oracle_forward_resnet(H, T, B, _ptr(planes), len(blocks), _ptr(spec), _ptr(weights), 1 if bf16 else 0,
+                                  _ptr(out))
+    return out
+
+
+def run_resnet(d, T, det, blocks, weights, bf16, layout="paper", first=None, last=None):
+    """The whole path with a residual network: (logits, flips, residual)."""
+    if layout == "paper":
+        logits = forward_resnet(d, T, unpack_paper(d, T, det, first, last), blocks, weights, bf16, layout)
+        flips, res = flips_residual_paper(d, T, logits, det)
+    else:
+        logits = forward_resnet(d, T, unpack(d, T, det), blocks, weights, bf16)
         flips, res = flips_residual(d, T, logits, det)
     return logits, flips, res

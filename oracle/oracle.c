@@ -626,6 +626,172 @@ void oracle_residual_from_flips(int d, int T, int B, const uint64_t* det, const 
   free(index_of);
 }
 
+/* ---------------------------------------------------------------------- */
+/* Residual network (Model 6, Sec. VI, Fig. Model8Representation).        */
+/* ---------------------------------------------------------------------- */
+
+/* y[b][co][v] = bias[co] + sum_{ci, taps} w[co][ci][taps] x[b][ci][v + tap]
+ * on a T x H x H volume with zero padding, k = 1 or 3; exact fp64 sums. */
+static void conv_sums(int H, int T, int B, const double* x, int ci_n, int co_n, int k, const double* w,
+                      const double* bias, double* y) {
+  const int64_t V = (int64_t)T * H * H;
+  const int p = (k - 1) / 2;
+#pragma omp parallel for collapse(2) schedule(dynamic)
+  for (int b = 0; b < B; ++b)
+    for (int co = 0; co < co_n; ++co)
+      for (int t = 0; t < T; ++t)
+        for (int i = 0; i < H; ++i)
+          for (int j = 0; j < H; ++j) {
+            double acc = 0.0;
+            for (int ci = 0; ci < ci_n; ++ci)
+              for (int kt = 0; kt < k; ++kt) {
+                const int tt = t + kt - p;
+                if (tt < 0 || tt >= T) continue;
+                for (int ki = 0; ki < k; ++ki) {
+                  const int ii = i + ki - p;
+                  if (ii < 0 || ii >= H) continue;
+                  for (int kj = 0; kj < k; ++kj) {
+                    const int jj = j + kj - p;
+                    if (jj < 0 || jj >= H) continue;
+                    acc += w[(((int64_t)co * ci_n + ci) * k + kt) * k * k + ki * k + kj] *
+                           x[(((int64_t)b * ci_n + ci) * T + tt) * H * H + (int64_t)ii * H + jj];
+                  }
+                }
+              }
+            y[((int64_t)b * co_n + co) * V + ((int64_t)t * H + i) * H + j] = acc + bias[co];
+          }
+}
+
+/* Number of floats of a residual network's weights: per block (c_in, c_mid,
+ * c_out): conv1 c_mid c_in 27 + c_mid, BatchNorm 4 c_mid (scale, shift,
+ * running mean, running variance), conv2 c_out c_mid 27 + c_out, BatchNorm
+ * 4 c_out, and a projection c_out c_in + c_out when c_in != c_out.  bn_per
+ * channel = 2 counts the trainable parameters only (as the paper does). */
+int64_t oracle_resnet_weight_count(int n_blocks, const int* spec, int bn_per_channel) {
+  int64_t n = 0;
+  for (int k = 0; k < n_blocks; ++k) {
+    const int64_t ci = spec[4 * k], cm = spec[4 * k + 1], co = spec[4 * k + 2];
+    n += cm * ci * 27 + cm + bn_per_channel * cm + co * cm * 27 + co + bn_per_channel * co;
+    if (ci != co) n += co * ci + co;
+  }
+  return n;
+}
+
+/* Forward of a residual network: n_blocks blocks {c_in, c_mid, c_out, act},
+ * each (conv1: c_in -> c_mid, conv2: c_mid -> c_out)
+ *   h = act(BN1(conv1(x))), s = x (c_in == c_out) or P(x) (a 1x1x1
+ *   projection with bias), y = act(BN2(conv2(h)) + s), the last block
+ *   without its final act (its c_out = 4 channels are the logits);
+ * BN(z) = (z - mean) / sqrt(var + 1e-5) * scale + shift, running statistics.
+ * prec 0: exact, fp64, BatchNorm applied as written.  prec 1 (bf16): BatchNorm
+ * folded into its conv (g = scale / sqrt(var + eps) in fp64, weights
+ * bf16(fp32(w g)), bias fp32((b - mean) g + shift)), projection weights bf16
+ * and bias fp32; every stored tensor (h, P(x), y) rounded to bf16 after
+ * rounding the pre-activation (and the activation) to fp32; the sum
+ * BN2(conv2 h) + s rounded to fp32 once.  planes [B][c_in0][T][H][H];
+ * logits [B][4][T][H][H]. */
+void oracle_forward_resnet(int H, int T, int B, const double* planes, int n_blocks, const int* spec,
+                           const float* weights, int prec, double* logits) {
+  const double eps = 1e-5;
+  const int64_t V = (int64_t)T * H * H;
+  int cmax = spec[0];
+  for (int k = 0; k < n_blocks; ++k)
+    for (int q = 1; q < 3; ++q) cmax = spec[4 * k + q] > cmax ? spec[4 * k + q] : cmax;
+  double* x = (double*)malloc(sizeof(double) * (size_t)B * cmax * V);
+  double* h = (double*)malloc(sizeof(double) * (size_t)B * cmax * V);
+  double* s = (double*)malloc(sizeof(double) * (size_t)B * cmax * V);
+  double* y = (double*)malloc(sizeof(double) * (size_t)B * cmax * V);
+  const int c0 = spec[0];
+  for (int64_t e = 0; e < (int64_t)B * c0 * V; ++e) x[e] = prec ? (double)oracle_round_bf16((float)planes[e]) : planes[e];
+  const float* src = weights;
+  for (int k = 0; k < n_blocks; ++k) {
+    const int ci = spec[4 * k], cm = spec[4 * k + 1], co = spec[4 * k + 2], act = spec[4 * k + 3];
+    const int last = k == n_blocks - 1;
+    /* the two conv + BatchNorm pairs of the block, each as folded or as written */
+    double* cw[2];
+    double* cb[2];
+    double* bnp[2]; /* scale, shift, mean, var */
+    for (int c = 0; c < 2; ++c) {
+      const int cin = c == 0 ? ci : cm, cout = c == 0 ? cm : co;
+      const int64_t nw = (int64_t)cout * cin * 27;
+      cw[c] = (double*)malloc(sizeof(double) * nw);
+      cb[c] = (double*)malloc(sizeof(double) * cout);
+      bnp[c] = (double*)malloc(sizeof(double) * 4 * cout);
+      for (int e = 0; e < 4 * cout; ++e) bnp[c][e] = (double)src[nw + cout + e];
+      for (int o = 0; o < cout; ++o) {
+        const double g = bnp[c][o] / sqrt(bnp[c][3 * cout + o] + eps);
+        for (int64_t e = 0; e < (int64_t)cin * 27; ++e) {
+          const double wv = (double)src[o * (int64_t)cin * 27 + e];
+          cw[c][o * (int64_t)cin * 27 + e] = prec ? (double)oracle_round_bf16((float)(wv * g)) : wv;
+        }
+        const double bv = (double)src[nw + o];
+        cb[c][o] = prec ? (double)(float)((bv - bnp[c][2 * cout + o]) * g + bnp[c][cout + o]) : bv;
+      }
+      src += nw + cout + 4 * cout;
+    }
+    /* h = act(BN1(conv1 x)) */
+    conv_sums(H, T, B, x, ci, cm, 3, cw[0], cb[0], h);
+    for (int b = 0; b < B; ++b)
+      for (int o = 0; o < cm; ++o)
+        for (int64_t v = 0; v < V; ++v) {
+          double* z = &h[((int64_t)b * cm + o) * V + v];
+          if (prec) {
+            *z = (double)oracle_round_bf16((float)activation(act, (double)(float)*z));
+          } else {
+            const double g = bnp[0][o] / sqrt(bnp[0][3 * cm + o] + eps);
+            *z = activation(act, (*z - bnp[0][2 * cm + o]) * g + bnp[0][cm + o]);
+          }
+        }
+    /* shortcut */
+    if (ci != co) {
+      const int64_t np = (int64_t)co * ci;
+      double* pw = (double*)malloc(sizeof(double) * np);
+      double* pb = (double*)malloc(sizeof(double) * co);
+      for (int64_t e = 0; e < np; ++e) pw[e] = prec ? (double)oracle_round_bf16(src[e]) : (double)src[e];
+      for (int o = 0; o < co; ++o) pb[o] = (double)src[np + o];
+      src += np + co;
+      conv_sums(H, T, B, x, ci, co, 1, pw, pb, s);
+      if (prec)
+        for (int64_t e = 0; e < (int64_t)B * co * V; ++e) s[e] = (double)oracle_round_bf16((float)s[e]);
+      free(pw);
+      free(pb);
+    } else {
+      memcpy(s, x, sizeof(double) * (size_t)B * co * V);
+    }
+    /* y = act(BN2(conv2 h) + s) */
+    conv_sums(H, T, B, h, cm, co, 3, cw[1], cb[1], y);
+    for (int b = 0; b < B; ++b)
+      for (int o = 0; o < co; ++o)
+        for (int64_t v = 0; v < V; ++v) {
+          const int64_t e = ((int64_t)b * co + o) * V + v;
+          double pre;
+          if (prec) {
+            pre = (double)(float)(y[e] + s[e]);
+          } else {
+            const double g = bnp[1][o] / sqrt(bnp[1][3 * co + o] + eps);
+            pre = (y[e] - bnp[1][2 * co + o]) * g + bnp[1][co + o] + s[e];
+          }
+          if (last)
+            y[e] = pre;
+          else
+            y[e] = prec ? (double)oracle_round_bf16((float)activation(act, pre)) : activation(act, pre);
+        }
+    double* t = x;
+    x = y;
+    y = t;
+    for (int c = 0; c < 2; ++c) {
+      free(cw[c]);
+      free(cb[c]);
+      free(bnp[c]);
+    }
+  }
+  memcpy(logits, x, sizeof(double) * (size_t)B * 4 * V);
+  free(x);
+  free(h);
+  free(s);
+  free(y);
+}
+
 /* Threads an OpenMP parallel region of the oracle uses (reported with the
  * CPU timing; not part of the method). */
 int oracle_num_threads(void) { return omp_get_max_threads(); }

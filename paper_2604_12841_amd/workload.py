@@ -76,6 +76,48 @@ def paper_layer_spec(filters, kernels, act=GELU_TANH, c_in=4):
     return layers
 
 
+# Model 6 (Sec. VI, Fig. Model8Representation): four residual blocks
+# (c_in, c_mid, c_out, act), two 3x3x3 convs with BatchNorm each; the first
+# expands 4 -> 512 and the last compresses 512 -> 4, both with a 1x1x1
+# projection shortcut.
+MODEL6_BLOCKS = [(4, 512, 512, GELU_TANH), (512, 512, 512, GELU_TANH), (512, 512, 512, GELU_TANH),
+                 (512, 512, 4, GELU_TANH)]
+
+
+def resnet_blocks(widths, c_in=4, act=GELU_TANH):
+    """Blocks of a residual network with hidden width `widths[k]` in block k
+    and 4 output channels: (c_in, c_mid, c_out, act)."""
+    blocks, ci = [], c_in
+    for k, w in enumerate(widths):
+        co = 4 if k == len(widths) - 1 else w
+        blocks.append((ci, w, co, act))
+        ci = co
+    return blocks
+
+
+def resnet_weights(blocks, seed, bias_std=BIAS_STD):
+    """Random weights of a residual network in the order the C ABI takes
+    them, per block: conv1 w, b; BatchNorm1 scale, shift, running mean,
+    running variance; conv2 w, b; BatchNorm2 (same four); projection w, b
+    when c_in != c_out.  Convs He-normal, biases N(0, bias_std^2), BatchNorm
+    scale N(1, 0.1^2), shift N(0, 0.1^2), mean N(0, 0.1^2), variance
+    U(0.5, 1.5)."""
+    rng = np.random.default_rng(seed)
+    parts = []
+    for ci, cm, co, _act in blocks:
+        for cin, cout in ((ci, cm), (cm, co)):
+            parts.append(rng.standard_normal(cout * cin * 27) * np.sqrt(2.0 / (cin * 27)))
+            parts.append(rng.standard_normal(cout) * bias_std)
+            parts.append(1.0 + 0.1 * rng.standard_normal(cout))
+            parts.append(0.1 * rng.standard_normal(cout))
+            parts.append(0.1 * rng.standard_normal(cout))
+            parts.append(rng.uniform(0.5, 1.5, cout))
+        if ci != co:
+            parts.append(rng.standard_normal(co * ci) * np.sqrt(2.0 / ci))
+            parts.append(rng.standard_normal(co) * bias_std)
+    return np.concatenate(parts).astype(np.float32)
+
+
 def config_layers(cfg_id, act=GELU_TANH):
     c = CONFIGS[cfg_id]
     return layer_spec(c["n_hidden"], c["width"], act)
