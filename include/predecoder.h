@@ -246,6 +246,45 @@ int64_t predecoder_flip_words(int32_t d, int32_t T);
  * parameter count of Table models); 0 on bad args. */
 size_t predecoder_weight_count(const pd_layer* layers, int32_t n_layers);
 
+/* ---- Residual networks (Model 6, Sec. VI, Fig. Model8Representation) ----
+ *
+ * A block {c_in, c_mid, c_out, act}: conv1 (3x3x3, c_in -> c_mid) and
+ * BatchNorm, the activation, conv2 (3x3x3, c_mid -> c_out) and BatchNorm, plus
+ * the shortcut -- the block's input when c_in == c_out, else a 1x1x1
+ * projection with bias -- then the activation, except after the last block,
+ * whose c_out = 4 channels are the logits.  BatchNorm is the inference form
+ * (x - running mean) / sqrt(running var + 1e-5) * scale + shift.  Model 6 is
+ * {4,512,512}, {512,512,512} x 2, {512,512,4} with GELU (42,593,296 trainable
+ * parameters; the running statistics add 2 floats per BatchNorm channel).
+ * Weights, per block: conv1 w[c_mid][c_in][3][3][3], b[c_mid]; BatchNorm1
+ * scale, shift, running mean, running variance [c_mid] each; conv2
+ * w[c_out][c_mid][3][3][3], b[c_out]; BatchNorm2 (four [c_out]); projection
+ * w[c_out][c_in], b[c_out] when c_in != c_out.
+ * Precision: BatchNorm is folded into its conv at create (g = scale /
+ * sqrt(var + eps) in fp64; weights bf16(fp32(w g)); bias fp32((b - mean) g +
+ * shift)); projection weights bf16; every tensor stored between kernels
+ * (activations, projection outputs) bf16; the conv2 sum plus the shortcut is
+ * taken in fp32 before the activation.  Supported: PD_DTYPE_BF16, c_mid in
+ * {64, 128, 256, 512}, c_out == c_mid inside the network (others
+ * PD_ERR_UNSUPPORTED).  predecoder_run / residual / unpack / stage_times /
+ * destroy take the handle like any other (stages: unpack, one per block,
+ * residual); predecoder_activations gives PD_ERR_UNSUPPORTED. */
+typedef struct pd_block {
+  int32_t c_in, c_mid, c_out; /* conv1: c_in -> c_mid, conv2: c_mid -> c_out */
+  int32_t act;                /* pd_act after conv1 and after the shortcut add */
+} pd_block;
+
+/* Floats of a residual network's weights (layout above); 0 for invalid blocks. */
+size_t predecoder_resnet_weight_count(const pd_block* blocks, int32_t n_blocks);
+
+/* predecoder_create_ex for a residual network: blocks[0].c_in = 2
+ * (plaquette) or 4 (paper layout), blocks[n-1].c_out = 4, widths that meet;
+ * PD_ERR_INVALID_ARG otherwise (and for a weight count other than
+ * predecoder_resnet_weight_count). */
+pd_status predecoder_create_resnet(const float* weights, size_t n_weights, int32_t d, int32_t T,
+                                   const pd_block* blocks, int32_t n_blocks, int32_t dtype,
+                                   int32_t max_batch, const pd_options* opts, pd_predecoder** out);
+
 /* ---- Temporal windows over a long stream (Sec. VI, parallel windows in
  * time, after the parallel-window scheme the paper cites) ----
  *

@@ -284,9 +284,10 @@ def resnet_weight_count(blocks, bn_per_channel=4):
     return int(_load().oracle_resnet_weight_count(len(blocks), _ptr(spec), bn_per_channel))
 
 
-def forward_resnet(d, T, planes, blocks, weights, bf16, layout="plaquette"):
+def forward_resnet(d, T, planes, blocks, weights, bf16, layout="plaquette", acc32=False):
     """Residual network forward (Model 6, Sec. VI, Fig. Model8Representation).  planes [B][c_in][T][H][H];
-    blocks: (c_in, c_mid, c_out, act); returns logits [B][4][T][H][H]."""
+    blocks: (c_in, c_mid, c_out, act); returns logits [B][4][T][H][H].  acc32 (bf16 only): the conv sums
+    in fp32 (sizes the parity tolerance)."""
     planes = np.ascontiguousarray(planes, dtype=np.float64)
     weights = np.ascontiguousarray(weights, dtype=np.float32)
     spec = np.ascontiguousarray(np.array([list(b) for b in blocks], dtype=np.int32).ravel())
@@ -297,8 +298,8 @@ def forward_resnet(d, T, planes, blocks, weights, bf16, layout="plaquette"):
     if planes.shape[1:] != (blocks[0][0], T, H, H) or blocks[-1][2] != 4:
         raise ValueError("planes / blocks mismatch")
     out = np.zeros((B, 4, T, H, H), dtype=np.float64)
-    _load().oracle_forward_resnet(H, T, B, _ptr(planes), len(blocks), _ptr(spec), _ptr(weights), 1 if bf16 else 0,
-                                  _ptr(out))
+    prec = (2 if acc32 else 1) if bf16 else 0
+    _load().oracle_forward_resnet(H, T, B, _ptr(planes), len(blocks), _ptr(spec), _ptr(weights), prec, _ptr(out))
     return out
 
 

@@ -631,9 +631,10 @@ void oracle_residual_from_flips(int d, int T, int B, const uint64_t* det, const 
 /* ---------------------------------------------------------------------- */
 
 /* y[b][co][v] = bias[co] + sum_{ci, taps} w[co][ci][taps] x[b][ci][v + tap]
- * on a T x H x H volume with zero padding, k = 1 or 3; exact fp64 sums. */
+ * on a T x H x H volume with zero padding, k = 1 or 3; fp64 sums (acc32:
+ * fp32 sums in this loop order, another valid summation). */
 static void conv_sums(int H, int T, int B, const double* x, int ci_n, int co_n, int k, const double* w,
-                      const double* bias, double* y) {
+                      const double* bias, double* y, int acc32) {
   const int64_t V = (int64_t)T * H * H;
   const int p = (k - 1) / 2;
 #pragma omp parallel for collapse(2) schedule(dynamic)
@@ -643,6 +644,7 @@ static void conv_sums(int H, int T, int B, const double* x, int ci_n, int co_n, 
         for (int i = 0; i < H; ++i)
           for (int j = 0; j < H; ++j) {
             double acc = 0.0;
+            float accf = 0.0f;
             for (int ci = 0; ci < ci_n; ++ci)
               for (int kt = 0; kt < k; ++kt) {
                 const int tt = t + kt - p;
@@ -653,11 +655,16 @@ static void conv_sums(int H, int T, int B, const double* x, int ci_n, int co_n, 
                   for (int kj = 0; kj < k; ++kj) {
                     const int jj = j + kj - p;
                     if (jj < 0 || jj >= H) continue;
-                    acc += w[(((int64_t)co * ci_n + ci) * k + kt) * k * k + ki * k + kj] *
-                           x[(((int64_t)b * ci_n + ci) * T + tt) * H * H + (int64_t)ii * H + jj];
+                    const double pr = w[(((int64_t)co * ci_n + ci) * k + kt) * k * k + ki * k + kj] *
+                                      x[(((int64_t)b * ci_n + ci) * T + tt) * H * H + (int64_t)ii * H + jj];
+                    if (acc32)
+                      accf += (float)pr;
+                    else
+                      acc += pr;
                   }
                 }
               }
+            if (acc32) acc = (double)accf;
             y[((int64_t)b * co_n + co) * V + ((int64_t)t * H + i) * H + j] = acc + bias[co];
           }
 }
@@ -688,12 +695,15 @@ int64_t oracle_resnet_weight_count(int n_blocks, const int* spec, int bn_per_cha
  * bf16(fp32(w g)), bias fp32((b - mean) g + shift)), projection weights bf16
  * and bias fp32; every stored tensor (h, P(x), y) rounded to bf16 after
  * rounding the pre-activation (and the activation) to fp32; the sum
- * BN2(conv2 h) + s rounded to fp32 once.  planes [B][c_in0][T][H][H];
+ * BN2(conv2 h) + s rounded to fp32 once.  prec 2: prec 1 with the conv sums
+ * taken in fp32 (test infrastructure: another valid summation, which sizes
+ * the parity tolerance of residual networks).  planes [B][c_in0][T][H][H];
  * logits [B][4][T][H][H]. */
 void oracle_forward_resnet(int H, int T, int B, const double* planes, int n_blocks, const int* spec,
                            const float* weights, int prec, double* logits) {
   const double eps = 1e-5;
   const int64_t V = (int64_t)T * H * H;
+  const int acc32 = prec == 2;
   int cmax = spec[0];
   for (int k = 0; k < n_blocks; ++k)
     for (int q = 1; q < 3; ++q) cmax = spec[4 * k + q] > cmax ? spec[4 * k + q] : cmax;
@@ -730,7 +740,7 @@ void oracle_forward_resnet(int H, int T, int B, const double* planes, int n_bloc
       src += nw + cout + 4 * cout;
     }
     /* h = act(BN1(conv1 x)) */
-    conv_sums(H, T, B, x, ci, cm, 3, cw[0], cb[0], h);
+    conv_sums(H, T, B, x, ci, cm, 3, cw[0], cb[0], h, acc32);
     for (int b = 0; b < B; ++b)
       for (int o = 0; o < cm; ++o)
         for (int64_t v = 0; v < V; ++v) {
@@ -750,7 +760,7 @@ void oracle_forward_resnet(int H, int T, int B, const double* planes, int n_bloc
       for (int64_t e = 0; e < np; ++e) pw[e] = prec ? (double)oracle_round_bf16(src[e]) : (double)src[e];
       for (int o = 0; o < co; ++o) pb[o] = (double)src[np + o];
       src += np + co;
-      conv_sums(H, T, B, x, ci, co, 1, pw, pb, s);
+      conv_sums(H, T, B, x, ci, co, 1, pw, pb, s, acc32);
       if (prec)
         for (int64_t e = 0; e < (int64_t)B * co * V; ++e) s[e] = (double)oracle_round_bf16((float)s[e]);
       free(pw);
@@ -759,7 +769,7 @@ void oracle_forward_resnet(int H, int T, int B, const double* planes, int n_bloc
       memcpy(s, x, sizeof(double) * (size_t)B * co * V);
     }
     /* y = act(BN2(conv2 h) + s) */
-    conv_sums(H, T, B, h, cm, co, 3, cw[1], cb[1], y);
+    conv_sums(H, T, B, h, cm, co, 3, cw[1], cb[1], y, acc32);
     for (int b = 0; b < B; ++b)
       for (int o = 0; o < co; ++o)
         for (int64_t v = 0; v < V; ++v) {

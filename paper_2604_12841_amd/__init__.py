@@ -34,7 +34,8 @@ EXPORTS = ("predecoder_create", "predecoder_create_ex", "predecoder_run", "prede
            "predecoder_num_stages", "predecoder_stage_times", "predecoder_destroy",
            "predecoder_status_string", "predecoder_det_words", "predecoder_flip_words",
            "predecoder_weight_count", "predecoder_stream_windows", "predecoder_stream_create",
-           "predecoder_stream_run", "predecoder_stream_destroy")
+           "predecoder_stream_run", "predecoder_stream_destroy", "predecoder_resnet_weight_count",
+           "predecoder_create_resnet")
 
 
 class PredecoderError(RuntimeError):
@@ -45,6 +46,11 @@ class PredecoderError(RuntimeError):
 
 class Layer(ctypes.Structure):
     _fields_ = [("c_in", ctypes.c_int32), ("c_out", ctypes.c_int32), ("k", ctypes.c_int32),
+                ("act", ctypes.c_int32)]
+
+
+class Block(ctypes.Structure):
+    _fields_ = [("c_in", ctypes.c_int32), ("c_mid", ctypes.c_int32), ("c_out", ctypes.c_int32),
                 ("act", ctypes.c_int32)]
 
 
@@ -101,6 +107,12 @@ def lib():
         L.predecoder_stream_run.restype = i32
         L.predecoder_stream_destroy.argtypes = [vp]
         L.predecoder_stream_destroy.restype = None
+        BP = ctypes.POINTER(Block)
+        L.predecoder_resnet_weight_count.argtypes = [BP, i32]
+        L.predecoder_resnet_weight_count.restype = sz
+        L.predecoder_create_resnet.argtypes = [vp, sz, i32, i32, BP, i32, i32, i32, ctypes.POINTER(Options),
+                                               ctypes.POINTER(vp)]
+        L.predecoder_create_resnet.restype = i32
         _lib = L
     return _lib
 
@@ -122,6 +134,17 @@ def _layers(layers):
     for i, l in enumerate(layers):
         arr[i] = Layer(*[int(v) for v in l])
     return arr
+
+
+def _blocks(blocks):
+    arr = (Block * len(blocks))()
+    for i, b in enumerate(blocks):
+        arr[i] = Block(*[int(v) for v in b])
+    return arr
+
+
+def resnet_weight_count(blocks):
+    return int(lib().predecoder_resnet_weight_count(_blocks(blocks), len(blocks)))
 
 
 def weight_count(layers):
@@ -148,12 +171,15 @@ class Predecoder:
     """One pre-decoder handle: weights, workspace and tables for (d, T, max_batch)."""
 
     def __init__(self, weights, d, T, layers, dtype="bf16", max_batch=1, layout="plaquette", first=None,
-                 last=None):
+                 last=None, blocks=None):
         """layout: "plaquette" or "paper" (Sec. IV.B.1); first / last: basis ("Z", "X" or None) of the
-        preparation before round 0 / the measurement after round T-1 (paper layout)."""
+        preparation before round 0 / the measurement after round T-1 (paper layout).  blocks (with
+        layers None): a residual network of (c_in, c_mid, c_out, act) blocks (Model 6)."""
         import numpy as np
         w = np.ascontiguousarray(np.asarray(weights, dtype=np.float32))
-        self.d, self.T, self.layers, self.max_batch = d, T, [tuple(l) for l in layers], max_batch
+        self.d, self.T, self.max_batch = d, T, max_batch
+        self.layers = [tuple(l) for l in layers] if layers is not None else None
+        self.blocks = [tuple(b) for b in blocks] if blocks is not None else None
         self.dtype = _DTYPES[dtype] if isinstance(dtype, str) else int(dtype)
         self.layout = _LAYOUTS[layout] if isinstance(layout, str) else int(layout)
         self.grid = d if self.layout == LAYOUT_PAPER else d + 1
@@ -162,8 +188,13 @@ class Predecoder:
         opts = Options(self.layout, _BOUNDARIES[first] if not isinstance(first, int) else first,
                        _BOUNDARIES[last] if not isinstance(last, int) else last)
         h = ctypes.c_void_p()
-        st = lib().predecoder_create_ex(w.ctypes.data_as(ctypes.c_void_p), w.size, d, T, _layers(layers),
-                                        len(layers), self.dtype, max_batch, ctypes.byref(opts), ctypes.byref(h))
+        if blocks is not None:
+            st = lib().predecoder_create_resnet(w.ctypes.data_as(ctypes.c_void_p), w.size, d, T, _blocks(blocks),
+                                                len(blocks), self.dtype, max_batch, ctypes.byref(opts),
+                                                ctypes.byref(h))
+        else:
+            st = lib().predecoder_create_ex(w.ctypes.data_as(ctypes.c_void_p), w.size, d, T, _layers(layers),
+                                            len(layers), self.dtype, max_batch, ctypes.byref(opts), ctypes.byref(h))
         if st != PD_OK:
             raise PredecoderError(st, "predecoder_create")
         self._h = h

@@ -39,6 +39,20 @@ struct pd_predecoder {
   std::vector<float*> bdev;      // per conv layer: bias fp32
   float* head_w = nullptr;       // [4][c_in] fp32 (bf16-valued on the bf16 path)
   float* head_b = nullptr;       // [4]
+  // residual network (predecoder_create_resnet): its blocks; wdev / wslice /
+  // bdev hold conv1 and conv2 of block k at 2k and 2k + 1 (BatchNorm folded
+  // in), proj_w / proj_b its projection (null for an identity shortcut)
+  std::vector<pd_block> blocks;
+  std::vector<float*> proj_w, proj_b;
+  void* act3 = nullptr;          // third activation buffer [max_batch * S][cmax]
+  void* pbuf = nullptr;          // projection outputs [max_batch * S][pmax]
+  // Row width (bytes per voxel) of the data each activation buffer (act[0],
+  // act[1], act3) holds, 0 while it is all zero.  The 3x3x3 kernels read the
+  // zero halo around the interior voxels; a buffer written with one row
+  // width and then with another would show the old interior rows as halo, so
+  // it is zeroed first (prepare_rows).
+  int act_row[3] = {0, 0, 0};
+  size_t act_bytes = 0;          // size of each activation buffer
   int cmax = 0;
   int n_cu = 256;                // compute units: one persistent conv workgroup each
   float* partial = nullptr;      // split K loops of small batches: fp32 sums of up to max_units units
@@ -363,6 +377,13 @@ void free_all(pd_predecoder* h) {
   f(h->planes);
   f(h->act[0]);
   f(h->act[1]);
+  f(h->act3);
+  f(h->pbuf);
+  for (float* p : h->proj_w) f(p);
+  for (float* p : h->proj_b) f(p);
+  h->act3 = h->pbuf = nullptr;
+  h->proj_w.clear();
+  h->proj_b.clear();
   f(h->nib);
   f(h->tables);
   for (void* p : h->wdev) f(p);
@@ -438,6 +459,23 @@ std::vector<uint8_t> conv_fragments_fp8(const uint8_t* codes, int cin, int cout)
   return f;
 }
 
+// bf16 fragments of a layer whose outputs run in slices of 128 channels
+// when c_out > 128 (slices back to back; *slice = bytes of one slice, 0 when
+// there is a single launch).
+std::vector<uint16_t> fragments_sliced(const float* w, int cin, int cout, size_t* slice) {
+  if (cout <= 128) {
+    *slice = 0;
+    return conv_fragments(w, cin, cout);
+  }
+  std::vector<uint16_t> f;
+  for (int k = 0; k < cout / 128; ++k) {
+    std::vector<uint16_t> fk = conv_fragments(w + (size_t)k * 128 * cin * 27, cin, 128);
+    *slice = fk.size() * 2;
+    f.insert(f.end(), fk.begin(), fk.end());
+  }
+  return f;
+}
+
 pd_status check_launch(hipError_t e) {
   if (e != hipSuccess) {
     (void)hipGetLastError();
@@ -449,8 +487,112 @@ pd_status check_launch(hipError_t e) {
 // Enqueues the whole path.  ev (optional) receives one event record before
 // each stage and one after the last.  stop_layer >= 0: stop after that
 // hidden layer, whose activations are then written (no head fused into it).
+// Before a layer writes rows of row_bytes into activation buffer idx: zero
+// the buffer if it holds rows of another width (see act_row).
+pd_status prepare_rows(pd_predecoder* h, int idx, int row_bytes, hipStream_t st) {
+  void* bufs[3] = {h->act[0], h->act[1], h->act3};
+  if (h->act_row[idx] != 0 && h->act_row[idx] != row_bytes) {
+    pd_status s = check_launch(pd::launch_zero(bufs[idx], h->act_bytes, st));
+    if (s != PD_OK) return s;
+  }
+  h->act_row[idx] = row_bytes;
+  return PD_OK;
+}
+
+// The path of a residual network (Model 6, Sec. VI, Fig. Model8Representation):
+// per block, conv1 (+ folded BatchNorm, activation) x -> hb, the shortcut (x,
+// or its 1x1x1 projection into pbuf), conv2 (+ folded BatchNorm) hb -> the
+// next x with the shortcut added before the activation; the last block's
+// conv2 is the output layer (logits, threshold) with the shortcut added.
+// Three activation buffers rotate so that x, hb and the output differ.
+pd_status enqueue_resnet(pd_predecoder* h, hipStream_t st, const uint64_t* det, int batch, uint64_t* flips,
+                         uint64_t* residual, float* logits, hipEvent_t* ev) {
+  const Geom& g = h->g;
+  const int hidden_wgs = h->n_cu * pd::conv_hidden_workgroups_per_cu();
+  const int kch = pd::conv_hidden_chunk_channels(0);
+  auto split_for = [&](const Tiling& t, int cin) -> pd::Split_k {
+    pd::Split_k sk{0, h->partial, h->max_units};
+    while ((cin / kch) % (2 << sk.kshift) == 0 && (t.ntiles << (sk.kshift + 1)) <= h->max_units) ++sk.kshift;
+    return sk;
+  };
+  int e = 0;
+  auto mark = [&]() -> pd_status {
+    if (ev && hipEventRecord(ev[e++], st) != hipSuccess) return PD_ERR_DEVICE;
+    return PD_OK;
+  };
+  pd_status s;
+  if ((s = mark()) != PD_OK) return s;
+  if ((s = check_launch(pd::launch_unpack(g, h->tables, det, batch, h->planes, 1, 0, st))) != PD_OK) return s;
+  Tiling tl = h->tiling;
+  tiling_for_batch(&tl, g, batch);
+  void* bufs[3] = {h->act[0], h->act[1], h->act3};
+  const void* x = h->planes;
+  int xi = -1;  // index of x in bufs (-1: the planes)
+  const int nb = (int)h->blocks.size();
+  for (int k = 0; k < nb; ++k) {
+    if ((s = mark()) != PD_OK) return s;
+    const pd_block& B = h->blocks[k];
+    const bool last = k == nb - 1;
+    const int hi = (xi + 1) % 3, yi = (xi + 2 + (xi < 0 ? 1 : 0)) % 3;
+    void* hb = bufs[hi];
+    void* yb = bufs[yi];
+    if ((s = prepare_rows(h, hi, B.c_mid * 2, st)) != PD_OK) return s;
+    if (!last && (s = prepare_rows(h, yi, B.c_out * 2, st)) != PD_OK) return s;
+    // conv1: x -> hb
+    {
+      const int nsl = B.c_mid > 128 ? B.c_mid / 128 : 1, cw = B.c_mid / nsl;
+      for (int q = 0; q < nsl && s == PD_OK; ++q) {
+        const void* wq = (const char*)h->wdev[2 * k] + q * h->wslice[2 * k];
+        void* yq = (uint16_t*)hb + (size_t)q * cw;
+        if (k == 0)
+          s = check_launch(pd::launch_conv_first(g, B.c_in, cw, B.act, x, yq, B.c_mid, wq, h->bdev[2 * k] + q * cw,
+                                                 batch, 0, st));
+        else
+          s = check_launch(pd::launch_conv_hidden(g, tl, B.c_in, cw, B.act, x, yq, B.c_mid, wq,
+                                                  h->bdev[2 * k] + q * cw, 0, nullptr, nullptr, h->tables, h->nib,
+                                                  nullptr, batch, hidden_wgs, split_for(tl, B.c_in), 0, nullptr, 0,
+                                                  st));
+      }
+      if (s != PD_OK) return s;
+    }
+    // shortcut
+    const uint16_t* sc = (const uint16_t*)x;
+    int sc_stride = B.c_in;
+    if (h->proj_w[k]) {
+      s = check_launch(pd::launch_proj(g, x, B.c_in, B.c_in, h->proj_w[k], h->proj_b[k], B.c_out, h->pbuf, B.c_out,
+                                       batch, st));
+      if (s != PD_OK) return s;
+      sc = (const uint16_t*)h->pbuf;
+      sc_stride = B.c_out;
+    }
+    // conv2: hb -> the next x (or the logits) with the shortcut added
+    if (last) {
+      s = check_launch(pd::launch_conv_hidden(g, tl, B.c_mid, 4, 0, hb, nullptr, 0, h->wdev[2 * k + 1],
+                                              h->bdev[2 * k + 1], 2, nullptr, nullptr, h->tables, h->nib, logits,
+                                              batch, hidden_wgs, split_for(tl, B.c_mid), 0, sc, sc_stride, st));
+    } else {
+      const int nsl = B.c_out > 128 ? B.c_out / 128 : 1, cw = B.c_out / nsl;
+      for (int q = 0; q < nsl && s == PD_OK; ++q) {
+        const void* wq = (const char*)h->wdev[2 * k + 1] + q * h->wslice[2 * k + 1];
+        s = check_launch(pd::launch_conv_hidden(g, tl, B.c_mid, cw, B.act, hb, (uint16_t*)yb + (size_t)q * cw,
+                                                B.c_out, wq, h->bdev[2 * k + 1] + q * cw, 4, nullptr, nullptr,
+                                                h->tables, h->nib, nullptr, batch, hidden_wgs,
+                                                split_for(tl, B.c_mid), 0, sc + (size_t)q * cw, sc_stride, st));
+      }
+    }
+    if (s != PD_OK) return s;
+    x = yb;
+    xi = yi;
+  }
+  if ((s = mark()) != PD_OK) return s;
+  if ((s = check_launch(pd::launch_residual_pack(g, h->tables, det, h->nib, flips, residual, batch, st))) != PD_OK)
+    return s;
+  return mark();
+}
+
 pd_status enqueue_run(pd_predecoder* h, hipStream_t st, const uint64_t* det, int batch, uint64_t* flips,
                       uint64_t* residual, float* logits, hipEvent_t* ev, int stop_layer = -1) {
+  if (!h->blocks.empty()) return enqueue_resnet(h, st, det, batch, flips, residual, logits, ev);
   const Geom& g = h->g;
   const int fp32 = h->dtype == PD_DTYPE_FP32;
   const int fp8 = h->dtype == PD_DTYPE_FP8;
@@ -489,6 +631,7 @@ pd_status enqueue_run(pd_predecoder* h, hipStream_t st, const uint64_t* det, int
     if ((s = mark()) != PD_OK) return s;
     void* y = h->act[l & 1];
     const pd_layer& L = h->layers[l];
+    if ((s = prepare_rows(h, l & 1, L.c_out * (fp32 ? 4 : aelem), st)) != PD_OK) return s;
     const bool fuse_head = !fp32 && !out3 && l == n - 2 && stop_layer < 0;
     if (fp32) {
       s = check_launch(pd::launch_conv_fp32(g, L.c_in, L.c_out, L.act, (const float*)x, (float*)y,
@@ -512,7 +655,7 @@ pd_status enqueue_run(pd_predecoder* h, hipStream_t st, const uint64_t* det, int
           s = check_launch(pd::launch_conv_hidden(g, tl, L.c_in, cw, L.act, x, yk, L.c_out, wk,
                                                   h->bdev[l] + k * cw * (fp8 ? 2 : 1), fuse_head ? 1 : 0,
                                                   h->head_w, h->head_b, h->tables, h->nib, logits, batch,
-                                                  hidden_wgs, split_for(tl, L.c_in), fp8, st));
+                                                  hidden_wgs, split_for(tl, L.c_in), fp8, nullptr, 0, st));
       }
       head_done = fuse_head && l > 0;
     }
@@ -525,7 +668,7 @@ pd_status enqueue_run(pd_predecoder* h, hipStream_t st, const uint64_t* det, int
     const pd_layer& L = h->layers[n - 1];
     s = check_launch(pd::launch_conv_hidden(g, tl, L.c_in, L.c_out, L.act, x, nullptr, 0, h->wdev[n - 1],
                                             h->bdev[n - 1], 2, nullptr, nullptr, h->tables, h->nib, logits,
-                                            batch, hidden_wgs, split_for(tl, L.c_in), fp8, st));
+                                            batch, hidden_wgs, split_for(tl, L.c_in), fp8, nullptr, 0, st));
   } else if (!head_done) {  // fp32, or a one-hidden-layer network on the paper's layout
     s = check_launch(pd::launch_head(g, h->layers[n - 1].c_in, fp32, x, h->head_w, h->head_b, h->tables,
                                      h->nib, logits, batch, st));
@@ -575,7 +718,7 @@ size_t predecoder_weight_count(const pd_layer* layers, int32_t n_layers) {
 
 int32_t predecoder_num_stages(const pd_predecoder* h) {
   if (!h) return -1;
-  return (int32_t)h->layers.size() + 2;
+  return (int32_t)(h->blocks.empty() ? h->layers.size() : h->blocks.size()) + 2;
 }
 
 pd_status predecoder_create(const float* weights, size_t n_weights, int32_t d, int32_t T,
@@ -652,6 +795,7 @@ pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d
   };
   const size_t cin0 = (size_t)layers[0].c_in;
   if ((s = dev_alloc(&h->planes, vox * cin0 * elem)) != PD_OK) return fail(s);
+  h->act_bytes = vox * cmax * aelem;
   if ((s = dev_alloc(&h->act[0], vox * cmax * aelem)) != PD_OK) return fail(s);
   if ((s = dev_alloc(&h->act[1], vox * cmax * aelem)) != PD_OK) return fail(s);
   if ((s = dev_alloc(&h->nib, (size_t)max_batch * g.V)) != PD_OK) return fail(s);
@@ -768,6 +912,168 @@ pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d
   return PD_OK;
 }
 
+size_t predecoder_resnet_weight_count(const pd_block* b, int32_t n) {
+  if (!b || n < 1) return 0;
+  size_t total = 0;
+  for (int k = 0; k < n; ++k) {
+    const size_t ci = b[k].c_in, cm = b[k].c_mid, co = b[k].c_out;
+    if (b[k].c_in < 1 || b[k].c_mid < 1 || b[k].c_out < 1) return 0;
+    total += cm * ci * 27 + cm + 4 * cm + co * cm * 27 + co + 4 * co;
+    if (ci != co) total += co * ci + co;
+  }
+  return total;
+}
+
+pd_status predecoder_create_resnet(const float* weights, size_t n_weights, int32_t d, int32_t T,
+                                   const pd_block* blocks, int32_t n_blocks, int32_t dtype, int32_t max_batch,
+                                   const pd_options* opts, pd_predecoder** out) {
+  if (!out) return PD_ERR_INVALID_ARG;
+  *out = nullptr;
+  if (!weights || !blocks || n_blocks < 1) return PD_ERR_INVALID_ARG;
+  if (d < 3 || (d % 2) == 0 || T < 1 || max_batch < 1) return PD_ERR_INVALID_ARG;
+  if (dtype != PD_DTYPE_FP32 && dtype != PD_DTYPE_BF16 && dtype != PD_DTYPE_FP8) return PD_ERR_INVALID_ARG;
+  const pd_options o = opts ? *opts : pd_options{PD_LAYOUT_PLAQUETTE, PD_BOUNDARY_NONE, PD_BOUNDARY_NONE};
+  if (o.layout != PD_LAYOUT_PLAQUETTE && o.layout != PD_LAYOUT_PAPER) return PD_ERR_INVALID_ARG;
+  if (o.first_round < PD_BOUNDARY_NONE || o.first_round > PD_BOUNDARY_X || o.last_round < PD_BOUNDARY_NONE ||
+      o.last_round > PD_BOUNDARY_X)
+    return PD_ERR_INVALID_ARG;
+  if (o.layout == PD_LAYOUT_PLAQUETTE && (o.first_round != PD_BOUNDARY_NONE || o.last_round != PD_BOUNDARY_NONE))
+    return PD_ERR_INVALID_ARG;
+  // the chain: input channels of the layout, widths that meet, 4 outputs
+  if (blocks[0].c_in != (o.layout == PD_LAYOUT_PAPER ? 4 : 2) || blocks[n_blocks - 1].c_out != 4)
+    return PD_ERR_INVALID_ARG;
+  for (int k = 0; k < n_blocks; ++k) {
+    const pd_block& B = blocks[k];
+    if (B.c_in < 1 || B.c_mid < 1 || B.c_out < 1 || B.act < 0 || B.act > 2) return PD_ERR_INVALID_ARG;
+    if (k > 0 && B.c_in != blocks[k - 1].c_out) return PD_ERR_INVALID_ARG;
+  }
+  if (n_weights != predecoder_resnet_weight_count(blocks, n_blocks)) return PD_ERR_INVALID_ARG;
+  // what the kernels run: bf16; widths 64, 128, 256 or 512 with c_out = c_mid
+  // inside the network
+  if (dtype != PD_DTYPE_BF16) return PD_ERR_UNSUPPORTED;
+  auto width_ok = [](int c) { return c == 64 || c == 128 || c == 256 || c == 512; };
+  // conv1 of a later block runs the hidden kernel from c_in to slices of
+  // min(c_mid, 128) channels: the instantiated pairs
+  auto conv1_ok = [](int ci, int cw) {
+    return (ci == 64 && (cw == 64 || cw == 128)) || (ci == 128 && (cw == 64 || cw == 128)) ||
+           (ci == 256 && (cw == 64 || cw == 128)) || (ci == 512 && cw == 128);
+  };
+  for (int k = 0; k < n_blocks; ++k) {
+    const pd_block& B = blocks[k];
+    if (!width_ok(B.c_mid)) return PD_ERR_UNSUPPORTED;
+    if (k < n_blocks - 1 && B.c_out != B.c_mid) return PD_ERR_UNSUPPORTED;
+    if (k > 0 && !conv1_ok(B.c_in, B.c_mid > 128 ? 128 : B.c_mid)) return PD_ERR_UNSUPPORTED;
+  }
+  Geom g = make_geom(d, T, o.layout, o.first_round, o.last_round);
+  if (g.d > kMaxD || g.T > kMaxT) return PD_ERR_UNSUPPORTED;
+  if ((long long)max_batch * g.V >= (1ll << 31) || (long long)max_batch * (g.Wd + g.Wf) >= (1ll << 31) ||
+      (long long)max_batch * g.S >= (1ll << 31) ||
+      (long long)max_batch * (T + 2) * pd::line_plane(g) >= (1ll << 31))
+    return PD_ERR_UNSUPPORTED;
+  int ndev = 0;
+  if (hipGetDeviceCount(&ndev) != hipSuccess || ndev < 1) {
+    (void)hipGetLastError();
+    return PD_ERR_DEVICE;
+  }
+  pd_predecoder* h = new (std::nothrow) pd_predecoder();
+  if (!h) return PD_ERR_OUT_OF_MEMORY;
+  h->g = g;
+  h->dtype = dtype;
+  h->max_batch = max_batch;
+  h->blocks.assign(blocks, blocks + n_blocks);
+  if (hipGetDevice(&h->device) != hipSuccess ||
+      hipDeviceGetAttribute(&h->n_cu, hipDeviceAttributeMultiprocessorCount, h->device) != hipSuccess ||
+      h->n_cu < 1) {
+    (void)hipGetLastError();
+    delete h;
+    return PD_ERR_DEVICE;
+  }
+  h->tiling = plan_tiling(g, max_batch);
+  if (h->tiling.span <= 0 || h->tiling.span > pd::conv_hidden_max_span()) {
+    delete h;
+    return PD_ERR_UNSUPPORTED;
+  }
+  int cmax = 4, pmax = 4;
+  for (int k = 0; k < n_blocks; ++k) {
+    cmax = std::max(cmax, std::max((int)blocks[k].c_mid, (int)blocks[k].c_out));
+    if (blocks[k].c_in != blocks[k].c_out) pmax = std::max(pmax, (int)blocks[k].c_out);
+  }
+  h->cmax = cmax;
+  pd_status s = PD_OK;
+  auto fail = [&](pd_status st) {
+    free_all(h);
+    delete h;
+    return st;
+  };
+  const size_t vox = (size_t)max_batch * (size_t)g.S;
+  const size_t cin0 = (size_t)blocks[0].c_in;
+  if ((s = dev_alloc(&h->planes, vox * cin0 * 2)) != PD_OK) return fail(s);
+  h->act_bytes = vox * cmax * 2;
+  if ((s = dev_alloc(&h->act[0], vox * cmax * 2)) != PD_OK) return fail(s);
+  if ((s = dev_alloc(&h->act[1], vox * cmax * 2)) != PD_OK) return fail(s);
+  if ((s = dev_alloc(&h->act3, vox * cmax * 2)) != PD_OK) return fail(s);
+  if ((s = dev_alloc(&h->pbuf, vox * pmax * 2)) != PD_OK) return fail(s);
+  if ((s = dev_alloc(&h->nib, (size_t)max_batch * g.V)) != PD_OK) return fail(s);
+  h->max_units = h->n_cu;
+  if ((s = dev_alloc(&h->partial, (size_t)h->max_units * pd::conv_hidden_partial_floats_per_unit() * 4)) != PD_OK)
+    return fail(s);
+  std::vector<int32_t> tab = build_tables(g);
+  if ((s = upload(&h->tables, tab.data(), tab.size() * sizeof(int32_t))) != PD_OK) return fail(s);
+  if (hipMemset(h->planes, 0, vox * cin0 * 2) != hipSuccess || hipMemset(h->act[0], 0, vox * cmax * 2) != hipSuccess ||
+      hipMemset(h->act[1], 0, vox * cmax * 2) != hipSuccess || hipMemset(h->act3, 0, vox * cmax * 2) != hipSuccess ||
+      hipMemset(h->pbuf, 0, vox * pmax * 2) != hipSuccess)
+    return fail(PD_ERR_DEVICE);
+  // weights: per conv, BatchNorm folded in (g = scale / sqrt(var + 1e-5) in
+  // fp64; weights fp32(w g), rounded to bf16 by the fragment builder; bias
+  // fp32((b - mean) g + shift))
+  const float* src = weights;
+  for (int k = 0; k < n_blocks; ++k) {
+    const pd_block& B = blocks[k];
+    for (int c = 0; c < 2; ++c) {
+      const int cin = c == 0 ? B.c_in : B.c_mid, cout = c == 0 ? B.c_mid : B.c_out;
+      const size_t nw = (size_t)cout * cin * 27;
+      const float* w = src;
+      const float* b = src + nw;
+      const float* bn = b + cout;  // scale, shift, mean, var
+      src += nw + cout + 4 * (size_t)cout;
+      std::vector<float> wf(nw), bf(cout > 4 ? cout : 32, 0.0f);
+      for (int o2 = 0; o2 < cout; ++o2) {
+        const double gg = (double)bn[o2] / std::sqrt((double)bn[3 * cout + o2] + 1e-5);
+        for (size_t e = 0; e < (size_t)cin * 27; ++e) wf[o2 * (size_t)cin * 27 + e] = (float)((double)w[o2 * (size_t)cin * 27 + e] * gg);
+        bf[o2] = (float)(((double)b[o2] - bn[2 * cout + o2]) * gg + bn[cout + o2]);
+      }
+      size_t slice = 0;
+      std::vector<uint16_t> f = (c == 1 && k == n_blocks - 1) ? conv_fragments(wf.data(), cin, cout)
+                                                             : fragments_sliced(wf.data(), cin, cout, &slice);
+      void* wd = nullptr;
+      s = upload(&wd, f.data(), f.size() * 2);
+      h->wdev.push_back(wd);
+      h->wslice.push_back(slice);
+      if (s != PD_OK) return fail(s);
+      float* bd = nullptr;
+      s = upload(&bd, bf.data(), bf.size() * 4);
+      h->bdev.push_back(bd);
+      if (s != PD_OK) return fail(s);
+    }
+    float* pw = nullptr;
+    float* pb = nullptr;
+    if (B.c_in != B.c_out) {
+      const size_t np = (size_t)B.c_out * B.c_in;
+      std::vector<float> w16(np);
+      for (size_t e = 0; e < np; ++e) w16[e] = bf16_value(src[e]);
+      s = upload(&pw, w16.data(), np * 4);
+      if (s == PD_OK) s = upload(&pb, src + np, (size_t)B.c_out * 4);
+      src += np + B.c_out;
+    }
+    h->proj_w.push_back(pw);
+    h->proj_b.push_back(pb);
+    if (s != PD_OK) return fail(s);
+  }
+  if (hipDeviceSynchronize() != hipSuccess) return fail(PD_ERR_DEVICE);
+  *out = h;
+  return PD_OK;
+}
+
 pd_status predecoder_run(pd_predecoder* h, void* hip_stream, const uint64_t* det, int32_t batch,
                          uint64_t* flips, uint64_t* residual, float* logits) {
   if (!h || !det || !flips || !residual) return PD_ERR_INVALID_ARG;
@@ -787,6 +1093,7 @@ pd_status predecoder_activations(pd_predecoder* h, void* hip_stream, const uint6
                                  int32_t layer, void* out) {
   if (!h || !det || !out) return PD_ERR_INVALID_ARG;
   if (batch < 1 || batch > h->max_batch) return PD_ERR_INVALID_ARG;
+  if (!h->blocks.empty()) return PD_ERR_UNSUPPORTED;
   if (layer < 0 || layer >= (int)h->layers.size() - 1) return PD_ERR_INVALID_ARG;
   if (h->dtype == PD_DTYPE_FP32) return PD_ERR_UNSUPPORTED;
   const hipStream_t st = (hipStream_t)hip_stream;

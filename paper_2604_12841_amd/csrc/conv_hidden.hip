@@ -116,8 +116,10 @@ __host__ __device__ inline int stage_slot(int q) {
 // one block of 32 MFMA rows); EPI_PARK: one part of a split K loop, whose
 // fp32 sums are parked for split_finish_kernel.  Only EPI_PARK kernels split
 // (the others see a split of 1 at compile time and keep their registers for
-// the epilogue).
-enum Epi { EPI_ACT = 0, EPI_HEAD = 1, EPI_OUT = 2, EPI_PARK = 3 };
+// the epilogue).  EPI_ADD: EPI_ACT with a bf16 shortcut row added to the
+// pre-activation (the second conv of a residual block); the output layer adds
+// a shortcut too when one is given (the last block of a residual network).
+enum Epi { EPI_ACT = 0, EPI_HEAD = 1, EPI_OUT = 2, EPI_PARK = 3, EPI_ADD = 4 };
 
 // Wave split of the 256 x COUT output tile: WN waves across the channels
 // (NB blocks of 32 each: 2, or 1 for the 32-row output layer), WM across the
@@ -205,7 +207,8 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
                    int ystride, const u32x4* __restrict__ wfrag, const float* __restrict__ bias,
                    const float* __restrict__ head_w, const float* __restrict__ head_b,
                    const int32_t* __restrict__ tables, uint8_t* __restrict__ nib,
-                   float* __restrict__ logits, int batch, int kshift_arg, float* __restrict__ partial) {
+                   float* __restrict__ logits, int batch, int kshift_arg, float* __restrict__ partial,
+                   const uint16_t* __restrict__ sc, int sc_stride) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   using W = Split<COUT>;
   using L = Lds<COUT>;
@@ -271,6 +274,13 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
 #pragma unroll
               for (int o = 0; o < 4; ++o)
                 lg[o] = F8 ? __builtin_fmaf(acc[mb][0][o], scale_s[o], bias_s[o]) : acc[mb][0][o] + bias_s[o];
+              if (sc) {  // residual shortcut of the last block: 4 bf16 channels
+                const u32x2 sv = *reinterpret_cast<const u32x2*>(sc + padded_index(g, b, t, i, j) * sc_stride);
+                lg[0] += __uint_as_float(sv.x << 16);
+                lg[1] += __uint_as_float(sv.x & 0xFFFF0000u);
+                lg[2] += __uint_as_float(sv.y << 16);
+                lg[3] += __uint_as_float(sv.y & 0xFFFF0000u);
+              }
               const int HH = g.H * g.H;
               const int s = i * g.H + j;
               nib[(long long)b * g.V + (long long)t * HH + s] = (uint8_t)flip_nibble(g, tables, i, j, lg);
@@ -281,7 +291,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
             }
           }
         }
-      } else if constexpr (EPI == EPI_ACT) {
+      } else if constexpr (EPI == EPI_ACT || EPI == EPI_ADD) {
         // bias + activation + bf16, transposed through this wave's slice of
         // the staging buffer the tile read last (64 rows x 128 bytes, granule
         // c of row r at c ^ (r % 8)), then stored as whole 128-byte halves of
@@ -316,10 +326,18 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
                     *(lds_u32_w*)(tb + r * 128 + ((c ^ (r & 7)) << 4) + (c8 & 1) * 8 + half * 4) =
                         e4m3_pack4(v0, v1, v2, v3);
                   } else {
-                    const float v0 = act_fn<ACT>(acc[mb][nb][4 * q + 0] + bv.x);
-                    const float v1 = act_fn<ACT>(acc[mb][nb][4 * q + 1] + bv.y);
-                    const float v2 = act_fn<ACT>(acc[mb][nb][4 * q + 2] + bv.z);
-                    const float v3 = act_fn<ACT>(acc[mb][nb][4 * q + 3] + bv.w);
+                    float4 sh = {0.0f, 0.0f, 0.0f, 0.0f};
+                    if constexpr (EPI == EPI_ADD) {  // the block's shortcut, 4 bf16 channels of this row
+                      if (pidx[mb] >= 0) {
+                        const u32x2 sv = *reinterpret_cast<const u32x2*>(sc + (long long)pidx[mb] * sc_stride + co);
+                        sh = float4{__uint_as_float(sv.x << 16), __uint_as_float(sv.x & 0xFFFF0000u),
+                                    __uint_as_float(sv.y << 16), __uint_as_float(sv.y & 0xFFFF0000u)};
+                      }
+                    }
+                    const float v0 = act_fn<ACT>(acc[mb][nb][4 * q + 0] + bv.x + sh.x);
+                    const float v1 = act_fn<ACT>(acc[mb][nb][4 * q + 1] + bv.y + sh.y);
+                    const float v2 = act_fn<ACT>(acc[mb][nb][4 * q + 2] + bv.z + sh.z);
+                    const float v3 = act_fn<ACT>(acc[mb][nb][4 * q + 3] + bv.w + sh.w);
                     u32x2 packed;
                     packed.x = bf16_pack(v0, v1);
                     packed.y = bf16_pack(v2, v3);
@@ -693,8 +711,9 @@ __global__ void __launch_bounds__(256) split_finish_kernel(Geom g, Tiling tl, in
                                                            const float* __restrict__ head_b,
                                                            const int32_t* __restrict__ tables,
                                                            uint8_t* __restrict__ nib, float* __restrict__ logits,
-                                                           int batch) {
-  const int groups = EPI == EPI_ACT ? cout / 8 : 1;
+                                                           int batch, const uint16_t* __restrict__ sc, int sc_stride) {
+  constexpr bool ROWS8 = EPI == EPI_ACT || EPI == EPI_ADD;  // one thread per (row, 8 channels)
+  const int groups = ROWS8 ? cout / 8 : 1;
   const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   if (gid >= tl.ntiles * kTileRows * groups) return;
   const int tile = (int)(gid / (kTileRows * groups));
@@ -716,12 +735,21 @@ __global__ void __launch_bounds__(256) split_finish_kernel(Geom g, Tiling tl, in
 #pragma unroll
     for (int e = 0; e < 8; ++e) v[e] = F8 ? __builtin_fmaf(v[e], bias[cout + c + e], bias[c + e]) : v[e] + bias[c + e];
   };
-  if constexpr (EPI == EPI_ACT) {
+  if constexpr (ROWS8) {
     long long pidx, o;
     int lb;
     if (!tile_row(g, tl, tile, r, batch, &pidx, &lb, &o)) return;
     float v[8];
     sum8(grp * 8, v);
+    if constexpr (EPI == EPI_ADD) {  // the block's shortcut
+      const uint4 sv = *reinterpret_cast<const uint4*>(sc + pidx * sc_stride + grp * 8);
+      const uint32_t sw[4] = {sv.x, sv.y, sv.z, sv.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[2 * e] += __uint_as_float(sw[e] << 16);
+        v[2 * e + 1] += __uint_as_float(sw[e] & 0xFFFF0000u);
+      }
+    }
     if constexpr (F8) {
       const uint32_t w0 = e4m3_pack4(act_fn<ACT>(v[0]), act_fn<ACT>(v[1]), act_fn<ACT>(v[2]), act_fn<ACT>(v[3]));
       const uint32_t w1 = e4m3_pack4(act_fn<ACT>(v[4]), act_fn<ACT>(v[5]), act_fn<ACT>(v[6]), act_fn<ACT>(v[7]));
@@ -741,6 +769,13 @@ __global__ void __launch_bounds__(256) split_finish_kernel(Geom g, Tiling tl, in
       sum8(0, v);
 #pragma unroll
       for (int o2 = 0; o2 < 4; ++o2) lg[o2] = v[o2];
+      if (sc) {  // residual shortcut of the last block
+        const uint2 sv = *reinterpret_cast<const uint2*>(sc + padded_index(g, b, t, i, j) * sc_stride);
+        lg[0] += __uint_as_float(sv.x << 16);
+        lg[1] += __uint_as_float(sv.x & 0xFFFF0000u);
+        lg[2] += __uint_as_float(sv.y << 16);
+        lg[3] += __uint_as_float(sv.y & 0xFFFF0000u);
+      }
     } else {
 #pragma unroll
       for (int o2 = 0; o2 < 4; ++o2) lg[o2] = head_b[o2];
@@ -771,7 +806,7 @@ template <int CIN, int COUT, int EPI, int MODE, bool F8>
 hipError_t launch_hidden(const Geom& g, const Tiling& tl, int act, const void* x, void* y, int ystride,
                          const void* wfrag, const float* bias, const float* head_w, const float* head_b,
                          const int32_t* tables, uint8_t* nib, float* logits, int batch, int n_workgroups,
-                         int kshift, float* partial, hipStream_t stream) {
+                         int kshift, float* partial, const uint16_t* sc, int sc_stride, hipStream_t stream) {
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute((const void*)conv_hidden_kernel<CIN, COUT, EPI, MODE, F8>,
@@ -782,7 +817,7 @@ hipError_t launch_hidden(const Geom& g, const Tiling& tl, int act, const void* x
   const long long nwg = conv_workgroups(tl.ntiles << kshift, n_workgroups);
   hipLaunchKernelGGL((conv_hidden_kernel<CIN, COUT, EPI, MODE, F8>), dim3((unsigned)nwg), dim3(NT),
                      (size_t)Lds<COUT>::total, stream, g, tl, act, x, y, ystride, (const u32x4*)wfrag, bias, head_w,
-                     head_b, tables, nib, logits, batch, kshift, partial);
+                     head_b, tables, nib, logits, batch, kshift, partial, sc, sc_stride);
   return hipSuccess;
 }
 
@@ -790,22 +825,23 @@ template <int CIN, int COUT, int EPI, int MODE, bool F8>
 hipError_t launch_one(const Geom& g, const Tiling& tl, int act, const void* x, void* y, int ystride,
                       const void* wfrag, const float* bias, const float* head_w, const float* head_b,
                       const int32_t* tables, uint8_t* nib, float* logits, int batch, int n_workgroups,
-                      const Split_k& sk, hipStream_t stream) {
+                      const Split_k& sk, const uint16_t* sc, int sc_stride, hipStream_t stream) {
   hipError_t e;
   if (sk.kshift == 0) {
     e = launch_hidden<CIN, COUT, EPI, MODE, F8>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b, tables,
-                                                nib, logits, batch, n_workgroups, 0, nullptr, stream);
+                                                nib, logits, batch, n_workgroups, 0, nullptr, sc, sc_stride, stream);
     return e != hipSuccess ? e : hipGetLastError();
   }
   // K loops split: park the parts, then add them and finish the tiles
   e = launch_hidden<CIN, COUT, EPI_PARK, MODE, F8>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b, tables,
-                                                   nib, logits, batch, n_workgroups, sk.kshift, sk.partial, stream);
+                                                   nib, logits, batch, n_workgroups, sk.kshift, sk.partial, nullptr,
+                                                   0, stream);
   if (e != hipSuccess) return e;
-  const long long threads = tl.ntiles * kTileRows * (EPI == EPI_ACT ? COUT / 8 : 1);
+  const long long threads = tl.ntiles * kTileRows * (EPI == EPI_ACT || EPI == EPI_ADD ? COUT / 8 : 1);
   with_activation(act, [&](auto A) {
     hipLaunchKernelGGL((split_finish_kernel<EPI, decltype(A)::value, F8>), dim3((unsigned)((threads + 255) / 256)),
                        dim3(256), 0, stream, g, tl, COUT, sk.kshift, sk.partial, bias, y, ystride, head_w, head_b,
-                       tables, nib, logits, batch);
+                       tables, nib, logits, batch, sc, sc_stride);
   });
   return hipGetLastError();
 }
@@ -814,14 +850,16 @@ template <bool F8>
 hipError_t launch_case(const Geom& g, const Tiling& tl, int cin, int cout, int act, const void* x, void* y,
                        int ystride, const void* wfrag, const float* bias, int head, const float* head_w,
                        const float* head_b, const int32_t* tables, uint8_t* nib, float* logits, int batch,
-                       int n_workgroups, const Split_k& sk, hipStream_t stream) {
+                       int n_workgroups, const Split_k& sk, const uint16_t* sc, int sc_stride, hipStream_t stream) {
 #define PD_HIDDEN_CASE(CI, CO, E)                                                                  \
   if (cin == CI && cout == CO && head == E) {                                                     \
     if (tl.mode == 0)                                                                              \
       return launch_one<CI, CO, E, 0, F8>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b, \
-                                          tables, nib, logits, batch, n_workgroups, sk, stream);   \
+                                          tables, nib, logits, batch, n_workgroups, sk, sc,        \
+                                          sc_stride, stream);                                       \
     return launch_one<CI, CO, E, 1, F8>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b,   \
-                                        tables, nib, logits, batch, n_workgroups, sk, stream);     \
+                                        tables, nib, logits, batch, n_workgroups, sk, sc,          \
+                                        sc_stride, stream);                                         \
   }
   PD_HIDDEN_CASE(64, 64, EPI_ACT)
   PD_HIDDEN_CASE(128, 128, EPI_ACT)
@@ -837,6 +875,14 @@ hipError_t launch_case(const Geom& g, const Tiling& tl, int cin, int cout, int a
   PD_HIDDEN_CASE(64, 32, EPI_OUT)
   PD_HIDDEN_CASE(128, 32, EPI_OUT)
   PD_HIDDEN_CASE(256, 32, EPI_OUT)
+  if constexpr (!F8) {  // the residual network's layers (bf16)
+    PD_HIDDEN_CASE(512, 32, EPI_OUT)
+    PD_HIDDEN_CASE(512, 128, EPI_ACT)
+    PD_HIDDEN_CASE(64, 64, EPI_ADD)
+    PD_HIDDEN_CASE(128, 128, EPI_ADD)
+    PD_HIDDEN_CASE(256, 128, EPI_ADD)
+    PD_HIDDEN_CASE(512, 128, EPI_ADD)
+  }
 #undef PD_HIDDEN_CASE
   return hipErrorInvalidValue;
 }
@@ -851,7 +897,7 @@ hipError_t launch_conv_hidden(const Geom& g, const Tiling& tl, int cin, int cout
                               void* y, int ystride, const void* wfrag, const float* bias, int head,
                               const float* head_w, const float* head_b, const int32_t* tables, uint8_t* nib,
                               float* logits, int batch, int n_workgroups, const Split_k& sk, int fp8,
-                              hipStream_t stream) {
+                              const uint16_t* sc, int sc_stride, hipStream_t stream) {
   if (tl.span <= 0 || tl.span > MAX_SPAN) return hipErrorInvalidValue;
   // parts per tile: a power of two dividing the layer's chunks, with room
   // for every unit's sums
@@ -860,9 +906,9 @@ hipError_t launch_conv_hidden(const Geom& g, const Tiling& tl, int cin, int cout
     return hipErrorInvalidValue;
   if (fp8)
     return launch_case<true>(g, tl, cin, cout, act, x, y, ystride, wfrag, bias, head, head_w, head_b, tables, nib,
-                             logits, batch, n_workgroups, sk, stream);
+                             logits, batch, n_workgroups, sk, sc, sc_stride, stream);
   return launch_case<false>(g, tl, cin, cout, act, x, y, ystride, wfrag, bias, head, head_w, head_b, tables, nib,
-                            logits, batch, n_workgroups, sk, stream);
+                            logits, batch, n_workgroups, sk, sc, sc_stride, stream);
 }
 
 int conv_hidden_chunk_channels(int fp8) { return fp8 ? Prec<true>::KCH : Prec<false>::KCH; }

@@ -147,7 +147,12 @@ int conv_single_max_span();  // staged voxels a tile may need
 //   head == 1: a hidden layer whose epilogue applies the 1x1x1 head and the
 //              threshold as launch_conv_single does, instead of writing y;
 //   head == 2: the output layer itself (c_out = 4, no activation): its
-//              outputs are the logits, thresholded into flip nibbles.
+//              outputs are the logits, thresholded into flip nibbles; with
+//              sc non-null, the 4 bf16 channels of sc's row (sc_stride
+//              values apart) are added to the logits first;
+//   head == 4: a hidden layer with sc's row (bf16, sc_stride values apart,
+//              pointing at the slice's first channel) added to the
+//              pre-activation (residual blocks; bf16 only).
 // Weight fragments in 16-channel chunks (conv_fragments in api.hip; c_out = 4
 // padded to 32 channels, bias to 32 values); n_workgroups =
 // conv_hidden_workgroups_per_cu() per CU.
@@ -166,7 +171,7 @@ hipError_t launch_conv_hidden(const Geom& g, const Tiling& tl, int cin, int cout
                               void* y, int ystride, const void* wfrag, const float* bias, int head,
                               const float* head_w, const float* head_b, const int32_t* tables, uint8_t* nib,
                               float* logits, int batch, int n_workgroups, const Split_k& sk, int fp8,
-                              hipStream_t stream);
+                              const uint16_t* sc, int sc_stride, hipStream_t stream);
 int conv_hidden_max_span();
 int conv_hidden_chunk_channels(int fp8);  // input channels per K-loop chunk
 size_t conv_hidden_partial_floats_per_unit();
@@ -175,6 +180,17 @@ int conv_hidden_workgroups_per_cu();
 // Copies the interior voxel rows (row_bytes each, a multiple of 16) of a
 // zero-halo activation buffer to out [batch][T][H][H] rows.
 hipError_t launch_extract(const Geom& g, const void* act, int row_bytes, int batch, void* out, hipStream_t stream);
+
+// Zeroes `bytes` (a multiple of 16) of device memory with a kernel (usable
+// where a memset node is not wanted).
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t stream);
+
+// 1x1x1 projection shortcut (bf16): y[p][co] = bf16(b[co] + sum_ci w[co][ci]
+// x[p][ci]) over the interior voxels of the zero-halo layout; w [cout][cin]
+// fp32 holding bf16 values; strides in values (ystride a multiple of 4, and
+// xstride of 8 when cin is), cout a multiple of 4.
+hipError_t launch_proj(const Geom& g, const void* x, int cin, int xstride, const float* w, const float* b, int cout,
+                       void* y, int ystride, int batch, hipStream_t stream);
 
 // Temporal windows over a stream of rounds (Sec. VI, parallel windows in
 // time): window k covers rounds [start, start + len) of every stream and

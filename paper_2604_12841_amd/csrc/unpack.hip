@@ -132,3 +132,20 @@ hipError_t launch_extract(const Geom& g, const void* act, int row_bytes, int bat
 }
 
 }  // namespace pd
+
+namespace pd {
+
+__global__ void __launch_bounds__(256) zero_kernel(uint4* __restrict__ p, long long n) {
+  const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (gid < n) p[gid] = uint4{0u, 0u, 0u, 0u};
+}
+
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t stream) {
+  if (bytes % 16 != 0) return hipErrorInvalidValue;
+  const long long n = (long long)(bytes / 16);
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(zero_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, (uint4*)p, n);
+  return hipGetLastError();
+}
+
+}  // namespace pd

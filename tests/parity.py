@@ -132,8 +132,8 @@ def _padding_zero(words, nbits):
     return bool((words[:, -1] >> np.uint64(rem) == 0).all())
 
 
-def assert_parity(stats, dtype):
-    tol = TOL[dtype]
+def assert_parity(stats, dtype, tol=None):
+    tol = TOL[dtype] if tol is None else tol
     assert stats["flip_padding_ok"] and stats["res_padding_ok"], stats
     assert stats["flip_mismatch"] == 0, stats
     assert stats["res_mismatch"] == 0, stats

@@ -197,3 +197,57 @@ def test_create_ex_unsupported_models(layers, dtype):
 @pytest.mark.skipif(gpu_available(), reason="checks the no-device error path")
 def test_create_ex_without_device_reports_device_error():
     assert _create_ex(WP, 5, 3, PAPER, pdx.LAYOUT_PAPER, pdx.BOUNDARY_Z, pdx.BOUNDARY_X) == pdx.PD_ERR_DEVICE
+
+
+# ---- residual networks (Model 6) ----
+
+def _create_resnet(weights, d, T, blocks, layout=pdx.LAYOUT_PAPER, dtype=pdx.DTYPE_BF16, n_weights=None):
+    L = pdx.lib()
+    w = np.ascontiguousarray(weights, dtype=np.float32)
+    opts = pdx.Options(layout, 0, 0)
+    h = ctypes.c_void_p()
+    st = L.predecoder_create_resnet(w.ctypes.data_as(ctypes.c_void_p), w.size if n_weights is None else n_weights,
+                                    d, T, pdx._blocks(blocks), len(blocks), dtype, 2, ctypes.byref(opts),
+                                    ctypes.byref(h))
+    if st == pdx.PD_OK:
+        L.predecoder_destroy(h)
+    return st
+
+
+def test_resnet_weight_count_matches_oracle():
+    import oracle
+    for blocks in (workload.MODEL6_BLOCKS, workload.resnet_blocks([64, 64, 64]),
+                   [(4, 64, 64, 1), (64, 128, 128, 1), (128, 128, 4, 1)]):
+        assert pdx.resnet_weight_count(blocks) == oracle.resnet_weight_count(blocks)
+    assert pdx.resnet_weight_count([]) == 0
+
+
+RB = workload.resnet_blocks([64, 64, 64])
+RW = workload.resnet_weights(RB, 0)
+
+
+@pytest.mark.parametrize("blocks,n_weights", [
+    ([(2, 64, 64, 1), (64, 64, 4, 1)], None),          # paper layout takes 4 input channels
+    ([(4, 64, 64, 1), (64, 64, 5, 1)], None),          # 4 outputs
+    ([(4, 64, 64, 1), (32, 64, 4, 1)], None),          # broken chain
+    ([(4, 64, 64, 7), (64, 64, 4, 1)], None),          # unknown activation
+    (RB, RW.size - 1),                                 # weight count
+])
+def test_create_resnet_rejects_misuse(blocks, n_weights):
+    w = np.zeros(max(pdx.resnet_weight_count(blocks), 1), np.float32) if n_weights is None else RW
+    assert _create_resnet(w, 5, 3, blocks, n_weights=n_weights) == pdx.PD_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("blocks,dtype", [
+    (RB, pdx.DTYPE_FP8),                                # bf16 only
+    ([(4, 96, 96, 1), (96, 96, 4, 1)], pdx.DTYPE_BF16),  # width 96
+    ([(4, 64, 128, 1), (128, 128, 4, 1)], pdx.DTYPE_BF16),  # c_out != c_mid inside the network
+])
+def test_create_resnet_unsupported(blocks, dtype):
+    w = np.zeros(pdx.resnet_weight_count(blocks), np.float32)
+    assert _create_resnet(w, 5, 3, blocks, dtype=dtype) == pdx.PD_ERR_UNSUPPORTED
+
+
+@pytest.mark.skipif(gpu_available(), reason="checks the no-device error path")
+def test_create_resnet_without_device_reports_device_error():
+    assert _create_resnet(RW, 5, 3, RB) == pdx.PD_ERR_DEVICE

@@ -129,3 +129,31 @@ def test_single_hidden_layer(cuda, width, d, T, B):
     det, _ = workload.make_inputs(d, T, B, 0.01, 0.01, seed=72 + d)
     say("one hidden layer, width", width, "d", d, "T", T, "B", B)
     check(d, T, layers, w, det, "bf16")
+
+
+def test_buffer_reuse_at_other_row_widths(cuda):
+    """Widths that alternate unevenly over the two activation buffers (64,
+    128, 128, 64: each buffer is written at one width and later at another):
+    the zero halo the 3x3x3 layers read must stay zero."""
+    d, T = 5, 4
+    G = workload.GELU_TANH
+    layers = [(2, 64, 3, G), (64, 128, 3, G), (128, 128, 3, G), (128, 64, 3, G), (64, 4, 1, workload.NONE)]
+    weights = workload.he_normal_weights(layers, 91)
+    det, _ = workload.make_inputs(d, T, 3, 0.02, 0.02, 92)
+    pre = pdx.Predecoder(weights, d, T, layers, "bf16", max_batch=3)
+    flips, res, logits = run_gpu(pre, det)
+    f2, r2, l2 = run_gpu(pre, det)
+    pre.close()
+    st = compare(d, T, "bf16", *oracle.run(d, T, det, layers, weights, bf16=True), flips, res, logits)
+    say("  reuse at other widths bf16", st)
+    assert_parity(st, "bf16")
+    assert (logits == l2).all()
+    # the fp32 path (its own kernels and widths)
+    lf = [(2, 16, 3, G), (16, 32, 3, G), (32, 64, 3, G), (64, 16, 3, G), (16, 4, 1, workload.NONE)]
+    wf = workload.he_normal_weights(lf, 93)
+    pre = pdx.Predecoder(wf, d, T, lf, "fp32", max_batch=3)
+    flips, res, logits = run_gpu(pre, det)
+    pre.close()
+    st = compare(d, T, "fp32", *oracle.run(d, T, det, lf, wf, bf16=False), flips, res, logits)
+    say("  reuse at other widths fp32", st)
+    assert_parity(st, "fp32")
