@@ -62,6 +62,61 @@ def flops_per_sample(layers, H, T):
     return sum(2 * ci * co * k ** 3 for (ci, co, k, _a) in layers) * V
 
 
+def bench_model6(args, torch, pdx, workload):
+    """Model 6 (Sec. VI, Fig. Model8Representation: four residual blocks, 512
+    channels, BatchNorm folded at create) in the paper's layout at d = T =
+    --d, batch --batch, bf16 with fp32 accumulation."""
+    d = T = args.d
+    B = args.batch or 1
+    blocks = workload.MODEL6_BLOCKS
+    weights = workload.resnet_weights(blocks, 4006)
+    det, _ = workload.make_inputs(d, T, B, 0.003, 0.003, 5000 + d)
+    torch.cuda.set_device(0)
+    pre = pdx.Predecoder(weights, d, T, None, "bf16", max_batch=B, layout="paper", first="Z", last="Z",
+                         blocks=blocks)
+    ddet = torch.from_numpy(det.view(np.int64)).cuda()
+    flips = torch.empty((B, pre.flip_words), dtype=torch.int64, device="cuda")
+    res = torch.empty((B, pre.det_words), dtype=torch.int64, device="cuda")
+    cur = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        pre.run(ddet, flips, res, stream=cur)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(cur)
+    for _ in range(args.steps):
+        pre.run(ddet, flips, res, stream=cur)
+    e1.record(cur)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    stages = pre.stage_times(ddet, flips, res, args.stage_iters, stream=cur)
+    pre.close()
+    V = T * d * d
+
+    def block_flops(b):
+        ci, cm, co, _ = b
+        return 2.0 * V * (27 * ci * cm + 27 * cm * co + (ci * co if ci != co else 0))
+    total = sum(block_flops(b) for b in blocks) * B
+    mid = block_flops(blocks[1]) * B  # block 2: two 512 -> 512 convolutions
+    achieved = mid / (stages[2] * 1e-3) / 1e12
+    out = {
+        "metric": "us/round (pre-decode+residual), Model 6 (residual network) in the paper's layout at d=T=%d" % d,
+        "value": ms * 1e3 / (B * T), "unit": "us/round", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms, "rounds_per_s": B * T / (ms * 1e-3), "higher_is_better": False, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded phenomenological noise p=q=0.003, He-normal convs, random BatchNorm statistics)",
+        "config": {"workload": "Model 6 of Sec. VI (blocks %s, BatchNorm folded), paper layout, d=T=%d, batch %d; "
+                               "bf16 / fp32 accumulate" % (blocks, d, B),
+                   "d": d, "T": T, "batch": B, "model": 6},
+        "mfma_frac_end_to_end": total / (ms * 1e-3) / (PEAK_BF16_TFLOPS * 1e12),
+        "stage_ms": {"unpack": stages[0], **{"block%d" % (k + 1): stages[1 + k] for k in range(len(blocks))},
+                     "residual_repack": stages[-1]},
+        "roofline": {"kernel": "block 2: two conv3d 3x3x3 512->512 (bf16 MFMA, four 128-channel slices each)",
+                     "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None},
+    }
+    print(json.dumps(out), flush=True)
+
+
 def bench_stream(args, torch, pdx, workload):
     """The temporal window driver (Sec. VI, parallel windows in time): a model
     of Table models over --stream rounds at distance --d, --batch streams,
@@ -151,6 +206,8 @@ def main():
     from paper_2604_12841_amd import workload
 
     paper = args.paper_model is not None
+    if args.paper_model == 6:
+        return bench_model6(args, torch, pdx, workload)
     if args.stream is not None:
         if not paper:
             print("--stream needs --paper-model", file=sys.stderr)
