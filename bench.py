@@ -189,6 +189,8 @@ def main():
     ap.add_argument("--stream", type=int, default=None,
                     help="with --paper-model: time the temporal window driver over a stream of this many rounds "
                          "(windows of d x d x 3d rounds: core d, buffer d), --batch streams at once")
+    ap.add_argument("--graph", action="store_true",
+                    help="time replays of a recorded run (HIP graph) instead of predecoder_run calls")
     ap.add_argument("--core", type=int, default=None, help="--stream: committed rounds per window (default d)")
     ap.add_argument("--buffer", type=int, default=None, help="--stream: rounds read on each side (default d)")
     ap.add_argument("--dtype", choices=["bf16", "fp8"], default=None,
@@ -249,18 +251,22 @@ def main():
     res = torch.empty((B, pre.det_words), dtype=torch.int64, device="cuda")
     stream = torch.cuda.current_stream()
 
+    graph = pre.graph(ddet, flips, res) if args.graph else None
+    step = (lambda: graph.launch(stream=stream)) if graph else (lambda: pre.run(ddet, flips, res, stream=stream))
     for _ in range(args.warmup):
-        pre.run(ddet, flips, res, stream=stream)
+        step()
     torch.cuda.synchronize()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     e0.record(stream)
     for _ in range(args.steps):
-        pre.run(ddet, flips, res, stream=stream)
+        step()
     e1.record(stream)
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / args.steps
     print("step %.3f ms" % ms, file=sys.stderr, flush=True)
+    if graph:
+        graph.close()
 
     # Per-stage HIP-event times on the same stream (unpack, each layer, head, residual).
     stages = pre.stage_times(ddet, flips, res, args.stage_iters, stream=stream)
@@ -294,6 +300,7 @@ def main():
         "vs_baseline": None,
         "dtype": {"bf16": "bf16", "fp8": "fp8-e4m3", "fp32": "f32"}[cfg["dtype"]],
         "data": "synthetic (seeded phenomenological noise, He-normal random weights)",
+        "timed": "HIP graph replays of predecoder_run" if args.graph else "predecoder_run calls",
         "config": {
             "workload": "rotated surface code d=%d, T=%d rounds, batch %d; %d conv3d 3x3x3 layers x %d "
                         "channels + 1x1x1 head, %s operands / fp32 accumulate; p=q=%g"

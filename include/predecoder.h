@@ -246,6 +246,24 @@ int64_t predecoder_flip_words(int32_t d, int32_t T);
  * parameter count of Table models); 0 on bad args. */
 size_t predecoder_weight_count(const pd_layer* layers, int32_t n_layers);
 
+/* ---- Recorded runs (HIP graphs) ----
+ *
+ * predecoder_graph_create records one predecoder_run of `batch` samples with
+ * these buffers (device pointers, as for predecoder_run) into a HIP graph;
+ * predecoder_graph_launch replays it on hip_stream, reading whatever det then
+ * holds and writing flips / residual / logits (the same work and results as
+ * predecoder_run, with one launch on the host).  Creating runs the path once
+ * eagerly (on a stream of the graph's own, synchronously) so that the
+ * handle's buffers are in the state every run starts from.  The graph uses
+ * the handle's workspace: replays and runs of the same handle must not
+ * overlap.  For latency-bound small batches (the paper times its models with
+ * graph replays, Sec. VI). */
+typedef struct pd_graph pd_graph; /* opaque */
+pd_status predecoder_graph_create(pd_predecoder* h, const uint64_t* det, int32_t batch, uint64_t* flips,
+                                  uint64_t* residual, float* logits, pd_graph** out);
+pd_status predecoder_graph_launch(pd_graph* g, void* hip_stream);
+void predecoder_graph_destroy(pd_graph* g); /* NULL is a no-op; waits for the device */
+
 /* ---- Residual networks (Model 6, Sec. VI, Fig. Model8Representation) ----
  *
  * A block {c_in, c_mid, c_out, act}: conv1 (3x3x3, c_in -> c_mid) and

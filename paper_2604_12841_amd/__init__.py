@@ -35,7 +35,8 @@ EXPORTS = ("predecoder_create", "predecoder_create_ex", "predecoder_run", "prede
            "predecoder_status_string", "predecoder_det_words", "predecoder_flip_words",
            "predecoder_weight_count", "predecoder_stream_windows", "predecoder_stream_create",
            "predecoder_stream_run", "predecoder_stream_destroy", "predecoder_resnet_weight_count",
-           "predecoder_create_resnet")
+           "predecoder_create_resnet", "predecoder_graph_create", "predecoder_graph_launch",
+           "predecoder_graph_destroy")
 
 
 class PredecoderError(RuntimeError):
@@ -113,6 +114,12 @@ def lib():
         L.predecoder_create_resnet.argtypes = [vp, sz, i32, i32, BP, i32, i32, i32, ctypes.POINTER(Options),
                                                ctypes.POINTER(vp)]
         L.predecoder_create_resnet.restype = i32
+        L.predecoder_graph_create.argtypes = [vp, vp, i32, vp, vp, vp, ctypes.POINTER(vp)]
+        L.predecoder_graph_create.restype = i32
+        L.predecoder_graph_launch.argtypes = [vp, vp]
+        L.predecoder_graph_launch.restype = i32
+        L.predecoder_graph_destroy.argtypes = [vp]
+        L.predecoder_graph_destroy.restype = None
         _lib = L
     return _lib
 
@@ -226,6 +233,14 @@ class Predecoder:
         self._check(lib().predecoder_activations(self._h, _stream(stream), _ptr(det), batch, layer, _ptr(out)),
                     "predecoder_activations")
 
+    def graph(self, det, flips, residual, logits=None, batch=None):
+        """Records one run with these buffers; returns a Graph to replay it."""
+        batch = det.shape[0] if batch is None else batch
+        g = ctypes.c_void_p()
+        self._check(lib().predecoder_graph_create(self._h, _ptr(det), batch, _ptr(flips), _ptr(residual),
+                                                  _ptr(logits), ctypes.byref(g)), "predecoder_graph_create")
+        return Graph(g)
+
     @property
     def num_stages(self):
         return int(lib().predecoder_num_stages(self._h))
@@ -292,6 +307,29 @@ class Stream:
     def close(self):
         if getattr(self, "_h", None):
             lib().predecoder_stream_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class Graph:
+    """A recorded predecoder_run (Predecoder.graph)."""
+
+    def __init__(self, handle):
+        self._h = handle
+
+    def launch(self, stream=None):
+        st = lib().predecoder_graph_launch(self._h, _stream(stream))
+        if st != PD_OK:
+            raise PredecoderError(st, "predecoder_graph_launch")
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().predecoder_graph_destroy(self._h)
             self._h = None
 
     def __del__(self):

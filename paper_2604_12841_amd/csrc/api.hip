@@ -59,6 +59,13 @@ struct pd_predecoder {
   long long max_units = 0;
 };
 
+// One recorded predecoder_run (predecoder_graph_create).
+struct pd_graph {
+  hipStream_t stream = nullptr;
+  hipGraph_t graph = nullptr;
+  hipGraphExec_t exec = nullptr;
+};
+
 namespace {
 
 const int kMaxD = 63;
@@ -1151,6 +1158,57 @@ void predecoder_destroy(pd_predecoder* h) {
   (void)hipDeviceSynchronize();
   free_all(h);
   delete h;
+}
+
+pd_status predecoder_graph_create(pd_predecoder* h, const uint64_t* det, int32_t batch, uint64_t* flips,
+                                  uint64_t* residual, float* logits, pd_graph** out) {
+  if (!out) return PD_ERR_INVALID_ARG;
+  *out = nullptr;
+  if (!h || !det || !flips || !residual) return PD_ERR_INVALID_ARG;
+  if (batch < 1 || batch > h->max_batch) return PD_ERR_INVALID_ARG;
+  pd_graph* gr = new (std::nothrow) pd_graph();
+  if (!gr) return PD_ERR_OUT_OF_MEMORY;
+  auto fail = [&](pd_status e) {
+    (void)hipGetLastError();
+    if (gr->exec) (void)hipGraphExecDestroy(gr->exec);
+    if (gr->graph) (void)hipGraphDestroy(gr->graph);
+    if (gr->stream) (void)hipStreamDestroy(gr->stream);
+    delete gr;
+    return e;
+  };
+  // a stream of its own at the default priority (capture needs a stream
+  // other than the null stream)
+  if (hipStreamCreateWithFlags(&gr->stream, hipStreamNonBlocking) != hipSuccess) return fail(PD_ERR_DEVICE);
+  // one run first: the handle's buffers reach the state every later run
+  // starts from, so the recorded sequence (with any buffer clearing it
+  // needs) is the one each replay repeats
+  pd_status s = enqueue_run(h, gr->stream, det, batch, flips, residual, logits, nullptr);
+  if (s != PD_OK) return fail(s);
+  if (hipStreamSynchronize(gr->stream) != hipSuccess) return fail(PD_ERR_DEVICE);
+  if (hipStreamBeginCapture(gr->stream, hipStreamCaptureModeThreadLocal) != hipSuccess) return fail(PD_ERR_DEVICE);
+  s = enqueue_run(h, gr->stream, det, batch, flips, residual, logits, nullptr);
+  hipGraph_t graph = nullptr;
+  const hipError_t ec = hipStreamEndCapture(gr->stream, &graph);
+  gr->graph = graph;
+  if (s != PD_OK) return fail(s);
+  if (ec != hipSuccess || !graph) return fail(PD_ERR_DEVICE);
+  if (hipGraphInstantiate(&gr->exec, graph, nullptr, nullptr, 0) != hipSuccess) return fail(PD_ERR_DEVICE);
+  *out = gr;
+  return PD_OK;
+}
+
+pd_status predecoder_graph_launch(pd_graph* gr, void* hip_stream) {
+  if (!gr || !gr->exec) return PD_ERR_INVALID_ARG;
+  return check_launch(hipGraphLaunch(gr->exec, (hipStream_t)hip_stream));
+}
+
+void predecoder_graph_destroy(pd_graph* gr) {
+  if (!gr) return;
+  (void)hipDeviceSynchronize();
+  if (gr->exec) (void)hipGraphExecDestroy(gr->exec);
+  if (gr->graph) (void)hipGraphDestroy(gr->graph);
+  if (gr->stream) (void)hipStreamDestroy(gr->stream);
+  delete gr;
 }
 
 int32_t predecoder_stream_windows(int32_t n_rounds, int32_t core, int32_t buffer, int32_t* starts, int32_t* lengths,

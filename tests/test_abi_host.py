@@ -251,3 +251,11 @@ def test_create_resnet_unsupported(blocks, dtype):
 @pytest.mark.skipif(gpu_available(), reason="checks the no-device error path")
 def test_create_resnet_without_device_reports_device_error():
     assert _create_resnet(RW, 5, 3, RB) == pdx.PD_ERR_DEVICE
+
+
+def test_graph_create_rejects_null_handle():
+    import ctypes as c
+    g = c.c_void_p()
+    assert pdx.lib().predecoder_graph_create(None, None, 1, None, None, None, c.byref(g)) == pdx.PD_ERR_INVALID_ARG
+    assert pdx.lib().predecoder_graph_launch(None, None) == pdx.PD_ERR_INVALID_ARG
+    pdx.lib().predecoder_graph_destroy(None)
