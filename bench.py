@@ -66,7 +66,7 @@ def bench_model6(args, torch, pdx, workload):
     """Model 6 (Sec. VI, Fig. Model8Representation: four residual blocks, 512
     channels, BatchNorm folded at create) in the paper's layout at d = T =
     --d, batch --batch, bf16 with fp32 accumulation."""
-    d = T = args.d
+    d = T = args.d or 13
     B = args.batch or 1
     blocks = workload.MODEL6_BLOCKS
     weights = workload.resnet_weights(blocks, 4006)
@@ -121,7 +121,7 @@ def bench_stream(args, torch, pdx, workload):
     """The temporal window driver (Sec. VI, parallel windows in time): a model
     of Table models over --stream rounds at distance --d, --batch streams,
     windows of d x d x 3d (core d, buffer d), everything on one GPU."""
-    d, n, B = args.d, args.stream, args.batch or 1
+    d, n, B = args.d or 13, args.stream, args.batch or 1
     core, buf = args.core or d, d if args.buffer is None else args.buffer
     dtype = args.dtype or "bf16"
     layers = workload.paper_model_layers(args.paper_model)
@@ -185,7 +185,9 @@ def main():
     ap.add_argument("--paper-model", type=int, default=None,
                     help="time a model of Table models (1, 2, 4 or 5) in the paper's own layout (D x D grid, four "
                          "input channels, 3x3x3 output layer) at d = T = --d instead of a workload")
-    ap.add_argument("--d", type=int, default=13, help="distance (and rounds) for --paper-model")
+    ap.add_argument("--d", type=int, default=None,
+                    help="distance and rounds d = T: for --paper-model (default 13), or to run a workload's "
+                         "network and noise at another distance (a sweep over d)")
     ap.add_argument("--stream", type=int, default=None,
                     help="with --paper-model: time the temporal window driver over a stream of this many rounds "
                          "(windows of d x d x 3d rounds: core d, buffer d), --batch streams at once")
@@ -218,7 +220,7 @@ def main():
     if paper:
         # Table models in the paper's layout: memory experiment in the Z basis
         # (x_present cleared in the first and last round), d = T
-        d = T = args.d
+        d = T = args.d or 13
         B = args.batch or 1
         layers = workload.paper_model_layers(args.paper_model)
         weights = workload.he_normal_weights(layers, 4000 + args.paper_model)
@@ -227,11 +229,13 @@ def main():
         grid = d
     else:
         cfg = workload.CONFIGS[args.workload]
+        if args.d:
+            cfg = dict(cfg, d=args.d, T=args.d)
         d, T = cfg["d"], cfg["T"]
         B = args.batch or cfg["batch"]
         layers = workload.config_layers(args.workload)
         weights = workload.config_weights(args.workload)
-        det, _ = workload.config_inputs(args.workload, B)
+        det, _ = workload.make_inputs(d, T, B, cfg["p"], cfg["q"], 2000 + args.workload)
         grid = d + 1
         if args.dtype:
             if cfg["dtype"] == "fp32":
@@ -284,6 +288,7 @@ def main():
     print("stages ms:", ["%.3f" % s for s in stages], file=sys.stderr, flush=True)
 
     total_flops = flops_per_sample(layers, grid, T) * B
+    in_bytes = layers[0][0] * (4 if cfg["dtype"] == "fp32" else 2)  # input planes: c_in channels, bf16 or fp32
     rounds = B * T
     out = {
         "metric": "syndrome rounds/sec and us/round (pre-decode+residual) at d=13,T=13; MFMA %",
@@ -310,6 +315,14 @@ def main():
         "stage_ms": {"unpack": stages[0],
                      **{"layer%d" % (i + 1): stages[1 + i] for i in range(n - 1)},
                      "head_threshold": stages[n], "residual_repack": stages[n + 1]},
+        # algorithmic HBM bytes of the two bit-moving stages / their event
+        # times: unpack reads the packed detectors and writes the interior
+        # input planes; residual+repack reads the flip nibbles (one byte per
+        # voxel) and the detectors and writes the packed flip and residual rows
+        "stage_gbs": {
+            "unpack": B * (pre.det_words * 8 + V * in_bytes) / (stages[0] * 1e-3) / 1e9,
+            "residual_repack": B * (V + pre.det_words * 16 + pre.flip_words * 8) / (stages[n + 1] * 1e-3) / 1e9,
+        },
         "roofline": {
             "kernel": "conv3d 3x3x3 %d->%d implicit GEMM (%s MFMA) + bias/GELU epilogue"
                       % (ci, co, "fp8 e4m3" if fp8 else "bf16"),

@@ -9,13 +9,15 @@
 // for Z.  The four flip bits of a voxel are kept as one nibble per voxel in a
 // small workspace; fp32 logits are written only when asked for.
 //
-// K5 (residual + repack): one wave64 per packed 64-bit output word.  Lane l
-// computes bit 64 w + l of either the residual row (Eqs. Resk1X..ReskG1Z:
-// detector ^ measurement flip of this round ^ of the previous round ^ parity
-// of the data corrections on the plaquette, Eqs. SXJK/SZJK) or the flip row,
-// and __ballot packs the 64 bits of the wave into the word, which lane 0
-// stores.  Rows are whole words per sample, so no word is shared between
+// K5 (residual + repack): a wave64 builds one packed 64-bit output word at a
+// time from nibble rows staged in LDS.  Lane l computes bit 64 w + l of
+// either the residual row (Eqs. Resk1X..ReskG1Z: detector ^ measurement flip
+// of this round ^ of the previous round ^ parity of the data corrections on
+// the plaquette, Eqs. SXJK/SZJK) or the flip row, and __ballot packs the 64
+// bits of the wave into the word, which lane 0 stores.  Rows are whole words per sample, so no word is shared between
 // waves and no atomics are needed; padding bits come out 0.
+#include <algorithm>
+
 #include "internal.h"
 
 namespace pd {
@@ -92,55 +94,127 @@ __device__ __forceinline__ unsigned residual_bit(const Geom& g, const int32_t* _
   return r;
 }
 
+// K5 layout: a workgroup (four waves) takes a chunk of one sample's words --
+// up to cd residual words or cf flip words -- stages the nibble rows of the
+// rounds those words read (one more round before, for the previous-round
+// measurement flip) from HBM into LDS with coalesced dword loads, then each
+// wave builds words from LDS.  Every nibble byte of a sample is read from HBM
+// about once per word kind instead of once per stencil term.  Bit indices
+// within a sample fit 32 bits (T nflip < 2^31), so index splits are 32-bit
+// reciprocal divisions.
+struct ResidualPlan {
+  FastDiv by_stab, by_flip, by_d, by_chunks;
+  int cd, cf;  // words per residual / flip chunk
+  int nd, nf;  // residual / flip chunks per sample
+};
+
+// LDS bytes a launch may stage (rounds of T x H x H nibble rows).
+constexpr int kResidualLds = 32768;
+
 __global__ void __launch_bounds__(256) residual_pack_kernel(Geom g, const int32_t* __restrict__ tables,
                                                             const uint64_t* __restrict__ det,
                                                             const uint8_t* __restrict__ nib,
                                                             uint64_t* __restrict__ flips,
-                                                            uint64_t* __restrict__ residual, int batch) {
-  const int lane = threadIdx.x & 63;
-  const long long wid = (long long)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
-  const long long words = g.Wd + g.Wf;
-  if (wid >= (long long)batch * words) return;  // whole wave exits together
-  const int b = (int)(wid / words);
-  const long long w = wid - (long long)b * words;
+                                                            uint64_t* __restrict__ residual, ResidualPlan p) {
+  extern __shared__ uint32_t lds_words[];
+  uint8_t* lds = reinterpret_cast<uint8_t*>(lds_words);
+  const int b = (int)fastdiv(blockIdx.x, p.by_chunks);
+  const int c = (int)blockIdx.x - b * (p.nd + p.nf);
+  const bool is_res = c < p.nd;
+  const int nbits = is_res ? g.nstab : g.nflip;
+  const FastDiv by_n = is_res ? p.by_stab : p.by_flip;
+  const int w0 = is_res ? c * p.cd : (c - p.nd) * p.cf;
+  const int wlim = is_res ? (int)g.Wd : (int)g.Wf;
+  const int w1 = min(w0 + (is_res ? p.cd : p.cf), wlim);
+  const int kend = min(w1 * 64, g.T * nbits);  // first bit past the chunk's real bits
+  int ta = (int)fastdiv((uint32_t)(w0 * 64), by_n);
+  if (is_res && ta > 0) --ta;  // previous round of the first word's round
+  const int tb = (int)fastdiv((uint32_t)(max(kend, 1) - 1), by_n);
+  const int HH = g.H * g.H;
+  // stage bytes [ta HH, (tb + 1) HH) of the sample's nibbles: LDS byte
+  // (src & 3) + i holds byte i, so the 4-aligned middle moves as dwords
+  const uint8_t* src = nib + (long long)b * g.V + (long long)ta * HH;
+  const int nbytes = (tb - ta + 1) * HH;
+  const int mis = (int)((uintptr_t)src & 3);
+  const int head = min((4 - mis) & 3, nbytes);
+  const int nw = (nbytes - head) >> 2;
+  const uint32_t* mid = reinterpret_cast<const uint32_t*>(src + head);
+  for (int i = threadIdx.x; i < nw; i += 256) lds_words[(mis + head) / 4 + i] = mid[i];
+  if (threadIdx.x < head) lds[mis + threadIdx.x] = src[threadIdx.x];
+  const int tail0 = head + 4 * nw;
+  if ((int)threadIdx.x < nbytes - tail0) lds[mis + tail0 + threadIdx.x] = src[tail0 + threadIdx.x];
+  __syncthreads();
+  const uint8_t* rows = lds + mis;  // byte (t - ta) HH + s = nibble of (t, s), ta <= t <= tb
   const int32_t* site_of = tables + tables_site_of(g);
   const int32_t* supp = tables + tables_supp(g);
-  const int HH = g.H * g.H;
-  const uint8_t* nb = nib + (long long)b * g.V;
-  auto flip = [&](int ch, int t, int s) -> unsigned { return (nb[t * HH + s] >> ch) & 1u; };
-  unsigned bit = 0;
-  if (w < g.Wd) {
-    const long long k = w * 64 + lane;
-    if (k < (long long)g.T * g.nstab) {
-      const int t = (int)(k / g.nstab), n = (int)(k - (long long)t * g.nstab);
-      bit = (unsigned)((det[(long long)b * g.Wd + w] >> lane) & 1ull);
-      bit ^= residual_bit(g, site_of, supp, t, n, flip);
-    }
-    const unsigned long long m = __ballot(bit);
-    if (lane == 0) residual[(long long)b * g.Wd + w] = m;
-  } else {
-    const long long wf = w - g.Wd;
-    const long long k = wf * 64 + lane;
-    if (k < (long long)g.T * g.nflip) {
-      const int t = (int)(k / g.nflip), n = (int)(k - (long long)t * g.nflip);
-      const int dd = g.d * g.d;
-      int ch, s;
-      if (n < dd) {
-        ch = 0;
-        s = (n / g.d) * g.H + n % g.d;
-      } else if (n < 2 * dd) {
-        ch = 1;
-        s = ((n - dd) / g.d) * g.H + (n - dd) % g.d;
+  const int lane = threadIdx.x & 63;
+  const int dd = g.d * g.d;
+  // A wave takes words w, w + 4, w + 8, w + 12 of the chunk per pass.  Each
+  // bit is computed without branches (indices clamped into range, results
+  // masked), so the table and LDS reads of the four words are issued
+  // together instead of one dependent chain per word.
+  constexpr int U = 4;
+  auto nib_at = [&](int t, int site) -> unsigned { return rows[(t - ta) * HH + site]; };
+  for (int w = w0 + (int)(threadIdx.x >> 6); w < w1; w += 4 * U) {  // uniform per wave
+    unsigned bits[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int ww = min(w + 4 * u, w1 - 1);
+      const int k0 = ww * 64 + lane;
+      const bool real = w + 4 * u < w1 && k0 < kend;
+      const int k = min(k0, kend - 1);
+      const int t = (int)fastdiv((uint32_t)k, by_n), n = k - t * nbits;
+      unsigned bit;
+      if (is_res) {
+        // Eqs. Resk1X..ReskG1Z: detector ^ measurement flips of rounds t and
+        // t - 1 at the stabilizer's site ^ data flips on its support
+        const bool isx = n < g.K;
+        const int mch = isx ? 2 : 3, dch = isx ? 0 : 1;
+        const int site = site_of[n];
+        const int4 q = make_int4(supp[4 * n], supp[4 * n + 1], supp[4 * n + 2], supp[4 * n + 3]);
+        bit = (unsigned)(det[(long long)b * g.Wd + ww] >> lane) & 1u;
+        bit ^= nib_at(t, site) >> mch;
+        bit ^= t > 0 ? nib_at(max(t - 1, ta), site) >> mch : 0u;
+        bit ^= q.x >= 0 ? nib_at(t, max(q.x, 0)) >> dch : 0u;
+        bit ^= q.y >= 0 ? nib_at(t, max(q.y, 0)) >> dch : 0u;
+        bit ^= q.z >= 0 ? nib_at(t, max(q.z, 0)) >> dch : 0u;
+        bit ^= q.w >= 0 ? nib_at(t, max(q.w, 0)) >> dch : 0u;
       } else {
-        const int n2 = n - 2 * dd;
-        ch = n2 < g.K ? 2 : 3;
-        s = site_of[n2];
+        // flip row: data X / Z flips on the d x d data sites, then the
+        // measurement flips at the stabilizer sites
+        const bool data = n < 2 * dd;
+        const int ch = data ? (n < dd ? 0 : 1) : (n - 2 * dd < g.K ? 2 : 3);
+        const int qd = n - (n < dd ? 0 : dd);
+        const int r = (int)fastdiv((uint32_t)min(qd, dd - 1), p.by_d);
+        const int sd = r * g.H + (min(qd, dd - 1) - r * g.d);
+        const int sm = site_of[max(n - 2 * dd, 0)];
+        bit = nib_at(t, data ? sd : sm) >> ch;
       }
-      bit = flip(ch, t, s);
+      bits[u] = real ? (bit & 1u) : 0u;
     }
-    const unsigned long long m = __ballot(bit);
-    if (lane == 0) flips[(long long)b * g.Wf + wf] = m;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const unsigned long long m = __ballot(bits[u]);
+      const int ww = w + 4 * u;
+      if (lane == 0 && ww < w1) {
+        if (is_res)
+          residual[(long long)b * g.Wd + ww] = m;
+        else
+          flips[(long long)b * g.Wf + ww] = m;
+      }
+    }
   }
+}
+
+// Words per chunk for a word row of `nbits` bits per round: the most words
+// whose rounds (plus one earlier round for residual rows) fit the LDS budget,
+// at most `want`, at least 1.
+static int chunk_words(const Geom& g, int nbits, int extra, int want) {
+  const int HH = g.H * g.H;  // three rounds of the largest grid (H = 64) fit the budget
+  int cw = want;
+  // rounds touched by cw words: <= ceil(64 cw / nbits) + 1, plus `extra`
+  while (cw > 1 && ((64 * cw + nbits - 1) / nbits + 1 + extra) * HH + 4 > kResidualLds) cw = cw * 3 / 4;
+  return cw;
 }
 
 __global__ void __launch_bounds__(256) residual_from_flips_kernel(Geom g, const int32_t* __restrict__ tables,
@@ -197,10 +271,29 @@ hipError_t launch_head(const Geom& g, int cin, int fp32, const void* x, const fl
 hipError_t launch_residual_pack(const Geom& g, const int32_t* tables, const uint64_t* det,
                                 const uint8_t* nib, uint64_t* flips, uint64_t* residual, int batch,
                                 hipStream_t stream) {
-  long long waves = (long long)batch * (g.Wd + g.Wf);
-  unsigned grid = (unsigned)((waves + 3) / 4);
-  hipLaunchKernelGGL(residual_pack_kernel, dim3(grid), dim3(256), 0, stream, g, tables, det, nib, flips,
-                     residual, batch);
+  if (batch <= 0) return hipSuccess;
+  // about 4 waves' worth of words per workgroup when that still gives >= 1024
+  // workgroups; otherwise one word per wave, for parallelism at small batch
+  const long long words = (long long)batch * (g.Wd + g.Wf);
+  const int want = (int)std::max(4ll, std::min(words / 1024, (long long)INT32_MAX));
+  ResidualPlan p;
+  p.cd = chunk_words(g, g.nstab, 1, (int)std::min((long long)want, g.Wd));
+  p.cf = chunk_words(g, g.nflip, 0, (int)std::min((long long)want, g.Wf));
+  p.nd = (int)((g.Wd + p.cd - 1) / p.cd);
+  p.nf = (int)((g.Wf + p.cf - 1) / p.cf);
+  const long long blocks = (long long)batch * (p.nd + p.nf);
+  if (blocks >= (1ll << 31)) return hipErrorInvalidValue;  // block ids are split with 32-bit divisions
+  p.by_stab = make_fastdiv((uint32_t)g.nstab);
+  p.by_flip = make_fastdiv((uint32_t)g.nflip);
+  p.by_d = make_fastdiv((uint32_t)g.d);
+  p.by_chunks = make_fastdiv((uint32_t)(p.nd + p.nf));
+  // staged rounds of either chunk kind, +4 bytes of alignment slack
+  const int HH = g.H * g.H;
+  const int rd = (64 * p.cd + g.nstab - 1) / g.nstab + 2, rf = (64 * p.cf + g.nflip - 1) / g.nflip + 1;
+  const size_t lds = (size_t)std::min(std::max(rd, rf), g.T) * HH + 4;
+  if (lds > (size_t)kResidualLds + 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(residual_pack_kernel, dim3((unsigned)blocks), dim3(256), lds, stream, g, tables, det, nib,
+                     flips, residual, p);
   return hipGetLastError();
 }
 

@@ -10,42 +10,68 @@
 // first round for the basis the qubit is prepared in (Z clears x_present, X
 // clears z_present) and in the last round for the basis it is measured in.
 //
-// One thread per interior voxel (b, t, i, j); the thread reads the bits it
-// needs (the packed row of a sample is a few hundred bytes, so these reads hit
-// L1/L2) and writes all channels of the voxel with one store.  Consecutive
-// threads write consecutive voxels of a grid row.  HBM-bound: reads W_det * 8
+// One thread per interior voxel (t, i, j), looping over the samples; for each
+// sample it reads the bits it needs (the packed row of a sample is a few
+// hundred bytes, so these reads hit L1/L2) and writes all channels of the
+// voxel with one store.  Consecutive threads write consecutive voxels of a
+// grid row.  HBM-bound: reads W_det * 8
 // bytes and writes c_in * V * sizeof(elem) bytes per sample.
 #include "internal.h"
 
 namespace pd {
 
 template <bool FP32, bool PADDED, bool PAPER>
-__global__ void __launch_bounds__(256) unpack_kernel(Geom g, const int32_t* __restrict__ tables,
-                                                     const uint64_t* __restrict__ det, int batch,
-                                                     void* __restrict__ out) {
-  long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-  long long total = (long long)batch * g.V;
-  if (gid >= total) return;
-  int b = (int)(gid / g.V);
-  int v = (int)(gid - (long long)b * g.V);
-  int HH = g.H * g.H;
-  int t = v / HH;
-  int s = v - t * HH;
+__device__ __forceinline__ void unpack_voxel(const Geom& g, const int32_t* __restrict__ tables,
+                                             const uint64_t* __restrict__ det, int b, int v, int t, int s,
+                                             int nx, int nz, float px, float pz, void* __restrict__ out,
+                                             FastDiv by_h) {
   const uint64_t* row = det + (long long)b * g.Wd;
   auto event = [&](int n) -> unsigned {
     if (n < 0) return 0u;
-    const long long k = (long long)t * g.nstab + n;
+    const int k = t * g.nstab + n;
     return (unsigned)((row[k >> 6] >> (k & 63)) & 1ull);
   };
-  const int nx = tables[tables_comp_x(g) + s], nz = tables[tables_comp_z(g) + s];
   const unsigned ex = event(nx), ez = event(nz);
   long long o;
   if (PADDED) {
-    int i = s / g.H, j = s - (s / g.H) * g.H;
+    const int i = (int)fastdiv((uint32_t)s, by_h), j = s - i * g.H;
     o = padded_index(g, b, t, i, j);
   } else {
-    o = gid;
+    o = (long long)b * g.V + v;
   }
+  if constexpr (PAPER) {
+    static_assert(!FP32, "the paper's layout runs in bf16");
+    // bf16 patterns: 1.0 = 0x3F80, 0.5 = 0x3F00
+    auto bf = [](float f) -> uint32_t { return f == 1.0f ? 0x3F80u : (f == 0.5f ? 0x3F00u : 0u); };
+    uint2 val;
+    val.x = (ex ? 0x3F80u : 0u) | ((ez ? 0x3F80u : 0u) << 16);
+    val.y = bf(px) | (bf(pz) << 16);
+    reinterpret_cast<uint2*>(out)[o] = val;
+  } else if (FP32) {
+    float2 val;
+    val.x = ex ? 1.0f : 0.0f;
+    val.y = ez ? 1.0f : 0.0f;
+    reinterpret_cast<float2*>(out)[o] = val;
+  } else {
+    reinterpret_cast<uint32_t*>(out)[o] = (ex ? 0x3F80u : 0u) | ((ez ? 0x3F80u : 0u) << 16);
+  }
+}
+
+// Grid: x covers one sample's V voxels (one thread each), y strides over the
+// batch; the per-voxel tables are read once per thread, the voxel split uses
+// 32-bit reciprocal divisions (by_hh: H H, by_h: H).  V < 2^31 for every
+// supported grid.
+template <bool FP32, bool PADDED, bool PAPER>
+__global__ void __launch_bounds__(256) unpack_kernel(Geom g, const int32_t* __restrict__ tables,
+                                                     const uint64_t* __restrict__ det, int batch,
+                                                     void* __restrict__ out, FastDiv by_hh, FastDiv by_h) {
+  const int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v >= g.V) return;
+  const int HH = g.H * g.H;
+  const int t = (int)fastdiv((uint32_t)v, by_hh);
+  const int s = v - t * HH;
+  const int nx = tables[tables_comp_x(g) + s], nz = tables[tables_comp_z(g) + s];
+  float px = 0.0f, pz = 0.0f;
   if constexpr (PAPER) {
     // weight / 4 of the stabilizer drawn here: 1 for four qubits, 0.5 for two
     auto present = [&](int n, int kind) -> float {
@@ -54,32 +80,20 @@ __global__ void __launch_bounds__(256) unpack_kernel(Geom g, const int32_t* __re
       const int32_t* sp = tables + tables_supp(g) + n * 4;
       return (sp[2] >= 0) ? 1.0f : 0.5f;
     };
-    const float px = present(nx, 1), pz = present(nz, 2);
-    static_assert(!FP32, "the paper's layout runs in bf16");
-    // bf16 patterns: 1.0 = 0x3F80, 0.5 = 0x3F00
-    auto bf = [](float f) -> uint32_t { return f == 1.0f ? 0x3F80u : (f == 0.5f ? 0x3F00u : 0u); };
-    uint2 val;
-    val.x = (ex ? 0x3F80u : 0u) | ((ez ? 0x3F80u : 0u) << 16);
-    val.y = bf(px) | (bf(pz) << 16);
-    reinterpret_cast<uint2*>(out)[o] = val;
-  } else {
-    if (FP32) {
-      float2 val;
-      val.x = ex ? 1.0f : 0.0f;
-      val.y = ez ? 1.0f : 0.0f;
-      reinterpret_cast<float2*>(out)[o] = val;
-    } else {
-      reinterpret_cast<uint32_t*>(out)[o] = (ex ? 0x3F80u : 0u) | ((ez ? 0x3F80u : 0u) << 16);
-    }
+    px = present(nx, 1);
+    pz = present(nz, 2);
   }
+  for (int b = blockIdx.y; b < batch; b += gridDim.y)
+    unpack_voxel<FP32, PADDED, PAPER>(g, tables, det, b, v, t, s, nx, nz, px, pz, out, by_h);
 }
 
 hipError_t launch_unpack(const Geom& g, const int32_t* tables, const uint64_t* det, int batch, void* out,
                          int out_padded, int fp32, hipStream_t stream) {
-  long long total = (long long)batch * g.V;
-  unsigned grid = (unsigned)((total + 255) / 256);
+  if (batch <= 0) return hipSuccess;
+  const dim3 grid((unsigned)((g.V + 255) / 256), (unsigned)(batch < 65535 ? batch : 65535));
+  const FastDiv by_hh = make_fastdiv((uint32_t)(g.H * g.H)), by_h = make_fastdiv((uint32_t)g.H);
   auto go = [&](auto kernel) {
-    hipLaunchKernelGGL(kernel, dim3(grid), dim3(256), 0, stream, g, tables, det, batch, out);
+    hipLaunchKernelGGL(kernel, grid, dim3(256), 0, stream, g, tables, det, batch, out, by_hh, by_h);
   };
   if (g.layout == 1) {
     if (fp32) return hipErrorInvalidValue;
