@@ -145,6 +145,27 @@ std::vector<int32_t> build_tables(const Geom& g) {
         (x ? comp_x : comp_z)[site] = n;
         ++n;
       }
+  // residual stencils and flip-row sites (grid indices < 2^16: H <= 64)
+  int32_t* sten = t.data() + pd::tables_sten(g);
+  for (int k = 0; k < g.nstab; ++k) {
+    const int32_t* q = supp + 4 * k;
+    const int q2 = q[2] >= 0 ? q[2] : q[0], q3 = q[3] >= 0 ? q[3] : q[0];  // weight two: q2 = q3 cancel
+    sten[4 * k] = site_of[k] | ((k < g.K ? 2 : 3) << 16);
+    sten[4 * k + 1] = q[0] | (q[1] << 16);
+    sten[4 * k + 2] = q2 | (q3 << 16);
+    sten[4 * k + 3] = 0;
+  }
+  int32_t* fsite = t.data() + pd::tables_fsite(g);
+  for (int k = 0; k < g.nflip; ++k) {
+    const int dd = d * d;
+    if (k < 2 * dd) {
+      const int r = (k % dd) / d, c = (k % dd) % d;
+      fsite[k] = (r * H + c) | ((k < dd ? 0 : 1) << 16);
+    } else {
+      const int m = k - 2 * dd;
+      fsite[k] = site_of[m] | ((m < g.K ? 2 : 3) << 16);
+    }
+  }
   return t;
 }
 

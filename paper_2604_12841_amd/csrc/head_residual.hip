@@ -103,13 +103,77 @@ __device__ __forceinline__ unsigned residual_bit(const Geom& g, const int32_t* _
 // within a sample fit 32 bits (T nflip < 2^31), so index splits are 32-bit
 // reciprocal divisions.
 struct ResidualPlan {
-  FastDiv by_stab, by_flip, by_d, by_chunks;
+  FastDiv by_stab, by_flip, by_chunks;
   int cd, cf;  // words per residual / flip chunk
   int nd, nf;  // residual / flip chunks per sample
 };
 
 // LDS bytes a launch may stage (rounds of T x H x H nibble rows).
 constexpr int kResidualLds = 32768;
+
+// The words [w0, w1) of one row kind of sample b, from the staged nibble rows
+// (rows[(t - ta) HH + s] = nibble of round t, site s) and the per-bit
+// descriptors of the tables (sten for residual rows, fsite for flip rows).  A
+// wave takes words w, w + 4, w + 8, w + 12 per pass: first every descriptor
+// and detector read of the four words, then the LDS reads, so the reads go
+// out together instead of one dependent chain per word.  Indices are clamped
+// into range and bits past the row masked, so the body has no branches.
+template <bool RES>
+__device__ __forceinline__ void chunk_words_build(const Geom& g, const uint8_t* rows, int ta, int HH,
+                                                  const int32_t* __restrict__ tables,
+                                                  const uint64_t* __restrict__ det, uint64_t* __restrict__ out,
+                                                  int b, int w0, int w1, int kend, FastDiv by_n, int nbits,
+                                                  int lane) {
+  constexpr int U = 4;
+  const long long row_words = RES ? g.Wd : g.Wf;
+  const u32x4* sten = reinterpret_cast<const u32x4*>(tables + tables_sten(g));
+  const uint32_t* fsite = reinterpret_cast<const uint32_t*>(tables + tables_fsite(g));
+  for (int w = w0 + (int)(threadIdx.x >> 6); w < w1; w += 4 * U) {  // uniform per wave
+    int t[U];
+    u32x4 ds[U];
+    unsigned dw[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int ww = min(w + 4 * u, w1 - 1);
+      const int k = min(ww * 64 + lane, kend - 1);
+      t[u] = (int)fastdiv((uint32_t)k, by_n);
+      const int n = k - t[u] * nbits;
+      if constexpr (RES) {
+        ds[u] = sten[n];
+        dw[u] = (unsigned)(det[(long long)b * g.Wd + ww] >> lane);
+      } else {
+        ds[u][0] = fsite[n];
+      }
+    }
+    unsigned bits[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint8_t* row = rows + (t[u] - ta) * HH;
+      unsigned bit;
+      if constexpr (RES) {
+        // Eqs. Resk1X..ReskG1Z: detector ^ measurement flips of rounds t and
+        // t - 1 at the stabilizer's site ^ data flips on its support (the
+        // data channel is mch - 2: 0 for X checks, 1 for Z checks)
+        const unsigned site = ds[u][0] & 0xffffu, mch = ds[u][0] >> 16;
+        const unsigned m0 = row[site], m1 = row[(t[u] > ta ? -HH : 0) + (int)site];
+        const unsigned dsum = row[ds[u][1] & 0xffffu] ^ row[ds[u][1] >> 16] ^ row[ds[u][2] & 0xffffu] ^
+                              row[ds[u][2] >> 16];
+        bit = dw[u] ^ ((m0 ^ (t[u] > 0 ? m1 : 0u)) >> mch) ^ (dsum >> (mch - 2u));
+      } else {
+        // flip row: data X / Z flips on the d x d data sites, then the
+        // measurement flips at the stabilizer sites
+        bit = (unsigned)row[ds[u][0] & 0xffffu] >> (ds[u][0] >> 16);
+      }
+      const bool real = w + 4 * u < w1 && (w + 4 * u) * 64 + lane < kend;
+      bits[u] = real ? (bit & 1u) : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const unsigned long long m = __ballot(bits[u]);
+      if (lane == 0 && w + 4 * u < w1) out[(long long)b * row_words + w + 4 * u] = m;
+    }
+  }
+}
 
 __global__ void __launch_bounds__(256) residual_pack_kernel(Geom g, const int32_t* __restrict__ tables,
                                                             const uint64_t* __restrict__ det,
@@ -145,65 +209,11 @@ __global__ void __launch_bounds__(256) residual_pack_kernel(Geom g, const int32_
   if ((int)threadIdx.x < nbytes - tail0) lds[mis + tail0 + threadIdx.x] = src[tail0 + threadIdx.x];
   __syncthreads();
   const uint8_t* rows = lds + mis;  // byte (t - ta) HH + s = nibble of (t, s), ta <= t <= tb
-  const int32_t* site_of = tables + tables_site_of(g);
-  const int32_t* supp = tables + tables_supp(g);
   const int lane = threadIdx.x & 63;
-  const int dd = g.d * g.d;
-  // A wave takes words w, w + 4, w + 8, w + 12 of the chunk per pass.  Each
-  // bit is computed without branches (indices clamped into range, results
-  // masked), so the table and LDS reads of the four words are issued
-  // together instead of one dependent chain per word.
-  constexpr int U = 4;
-  auto nib_at = [&](int t, int site) -> unsigned { return rows[(t - ta) * HH + site]; };
-  for (int w = w0 + (int)(threadIdx.x >> 6); w < w1; w += 4 * U) {  // uniform per wave
-    unsigned bits[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int ww = min(w + 4 * u, w1 - 1);
-      const int k0 = ww * 64 + lane;
-      const bool real = w + 4 * u < w1 && k0 < kend;
-      const int k = min(k0, kend - 1);
-      const int t = (int)fastdiv((uint32_t)k, by_n), n = k - t * nbits;
-      unsigned bit;
-      if (is_res) {
-        // Eqs. Resk1X..ReskG1Z: detector ^ measurement flips of rounds t and
-        // t - 1 at the stabilizer's site ^ data flips on its support
-        const bool isx = n < g.K;
-        const int mch = isx ? 2 : 3, dch = isx ? 0 : 1;
-        const int site = site_of[n];
-        const int4 q = make_int4(supp[4 * n], supp[4 * n + 1], supp[4 * n + 2], supp[4 * n + 3]);
-        bit = (unsigned)(det[(long long)b * g.Wd + ww] >> lane) & 1u;
-        bit ^= nib_at(t, site) >> mch;
-        bit ^= t > 0 ? nib_at(max(t - 1, ta), site) >> mch : 0u;
-        bit ^= q.x >= 0 ? nib_at(t, max(q.x, 0)) >> dch : 0u;
-        bit ^= q.y >= 0 ? nib_at(t, max(q.y, 0)) >> dch : 0u;
-        bit ^= q.z >= 0 ? nib_at(t, max(q.z, 0)) >> dch : 0u;
-        bit ^= q.w >= 0 ? nib_at(t, max(q.w, 0)) >> dch : 0u;
-      } else {
-        // flip row: data X / Z flips on the d x d data sites, then the
-        // measurement flips at the stabilizer sites
-        const bool data = n < 2 * dd;
-        const int ch = data ? (n < dd ? 0 : 1) : (n - 2 * dd < g.K ? 2 : 3);
-        const int qd = n - (n < dd ? 0 : dd);
-        const int r = (int)fastdiv((uint32_t)min(qd, dd - 1), p.by_d);
-        const int sd = r * g.H + (min(qd, dd - 1) - r * g.d);
-        const int sm = site_of[max(n - 2 * dd, 0)];
-        bit = nib_at(t, data ? sd : sm) >> ch;
-      }
-      bits[u] = real ? (bit & 1u) : 0u;
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const unsigned long long m = __ballot(bits[u]);
-      const int ww = w + 4 * u;
-      if (lane == 0 && ww < w1) {
-        if (is_res)
-          residual[(long long)b * g.Wd + ww] = m;
-        else
-          flips[(long long)b * g.Wf + ww] = m;
-      }
-    }
-  }
+  if (is_res)
+    chunk_words_build<true>(g, rows, ta, HH, tables, det, residual, b, w0, w1, kend, by_n, nbits, lane);
+  else
+    chunk_words_build<false>(g, rows, ta, HH, tables, det, flips, b, w0, w1, kend, by_n, nbits, lane);
 }
 
 // Words per chunk for a word row of `nbits` bits per round: the most words
@@ -285,7 +295,6 @@ hipError_t launch_residual_pack(const Geom& g, const int32_t* tables, const uint
   if (blocks >= (1ll << 31)) return hipErrorInvalidValue;  // block ids are split with 32-bit divisions
   p.by_stab = make_fastdiv((uint32_t)g.nstab);
   p.by_flip = make_fastdiv((uint32_t)g.nflip);
-  p.by_d = make_fastdiv((uint32_t)g.d);
   p.by_chunks = make_fastdiv((uint32_t)(p.nd + p.nf));
   // staged rounds of either chunk kind, +4 bytes of alignment slack
   const int HH = g.H * g.H;

@@ -247,11 +247,19 @@ hipError_t launch_residual_from_flips(const Geom& g, const int32_t* tables, cons
 //                        stabilizer can share a site)
 //   supp[nstab][4]       grid indices of the data qubits of stabilizer n (data
 //                        qubit (r, c) is grid site r*H+c), -1 pads
+//   sten[nstab][4]       residual stencil of stabilizer n, 16-byte aligned:
+//                        {site | mch << 16, q0 | q1 << 16, q2 | q3 << 16, 0},
+//                        mch = 2 (X) or 3 (Z) the measurement channel; a
+//                        weight-two stabilizer repeats q0 as q2 and q3, whose
+//                        two reads then cancel in the XOR
+//   fsite[nflip]         flip bit n of a round: site | channel << 16
 __host__ __device__ inline int tables_site_of(const Geom&) { return 0; }
 __host__ __device__ inline int tables_comp_x(const Geom& g) { return g.nstab; }
 __host__ __device__ inline int tables_comp_z(const Geom& g) { return g.nstab + g.H * g.H; }
 __host__ __device__ inline int tables_supp(const Geom& g) { return g.nstab + 2 * g.H * g.H; }
-__host__ __device__ inline int tables_size(const Geom& g) { return 5 * g.nstab + 2 * g.H * g.H; }
+__host__ __device__ inline int tables_sten(const Geom& g) { return (5 * g.nstab + 2 * g.H * g.H + 3) & ~3; }
+__host__ __device__ inline int tables_fsite(const Geom& g) { return tables_sten(g) + 4 * g.nstab; }
+__host__ __device__ inline int tables_size(const Geom& g) { return tables_fsite(g) + g.nflip; }
 
 // Flip nibble of grid site s (bit 0 Z data, 1 X data, 2 X measurement, 3 Z
 // measurement correction) from the four logits, keeping each channel only
