@@ -185,7 +185,9 @@ float bf16_value(float f) {
 }
 
 // Tiling plan for the 3x3x3 layers: the candidate with the fewest MFMA rows
-// per sample whose double-buffered 32-channel staging fits in LDS.
+// per sample whose double-buffered 32-channel staging fits in LDS (cost 2 x
+// rows; ties go to per-sample tiles, then boxes of 16-voxel rows, then the
+// smaller span).
 
 long long flat_span(const Geom& g, long long seg_len, long long nseg, int batch) {
   // exact maximum staged span (line space, see pd::Tiling) over all tiles of
@@ -231,7 +233,7 @@ Tiling plan_tiling(const Geom& g, int max_batch) {
     t.sa = pd::line_plane(g);
     t.sb = g.H;
     t.span = (int)std::min<long long>(flat_span(g, g.V, 1, 1), 1 << 30);
-    consider(t, (long long)t.tiles_per_seg * pd::kTileRows);
+    consider(t, 2ll * t.tiles_per_seg * pd::kTileRows);
   }
   // flat across samples (rows per sample ~ V); the span bound covers any batch
   if (max_batch > 1) {
@@ -243,7 +245,7 @@ Tiling plan_tiling(const Geom& g, int max_batch) {
     t.sb = g.H;
     int nb = std::min(max_batch, 256);
     t.span = (int)std::min<long long>(flat_span(g, (long long)nb * g.V, 1, nb), 1 << 30);
-    consider(t, (long long)g.V + 1);  // +1: prefer per-sample tiles at equal cost
+    consider(t, 2ll * g.V + 2);  // +2: prefer per-sample tiles at equal cost
   }
   // boxes
   for (int BJ = 1; BJ <= std::min(g.H, 256); ++BJ)
@@ -261,10 +263,12 @@ Tiling plan_tiling(const Geom& g, int max_batch) {
       t.sa = (BI + 2) * (BJ + 2);
       t.sb = BJ + 2;
       t.span = (BT + 2) * (BI + 2) * (BJ + 2);
-      // a 16-lane LDS read spans two staged lines unless BJ is a multiple of
-      // 16, which costs about one extra LDS cycle per read: weigh it as rows
+      // (a box row of BJ < 16 voxels, whose 16-lane LDS reads span two staged
+      // lines, costs little: at d = T = 25 a 5x3x16 box and a 9x13x2 box
+      // reach 0.54 and 0.53 of peak per MFMA row, so the row count decides,
+      // and BJ = 16 only breaks ties)
       const long long rows = (long long)t.ntT * t.ntI * t.ntJ * pd::kTileRows;
-      consider(t, (BJ % 16 == 0) ? rows : rows + rows / 4);
+      consider(t, 2 * rows + (BJ % 16 != 0));
     }
   return best;
 }

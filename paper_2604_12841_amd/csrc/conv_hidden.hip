@@ -625,6 +625,11 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
       // loaded RING - 1 steps ahead, staging rounds in the shadow of row
       // block 0.
       u32x4 av[MB][AQ];
+      // Wave priority: a SIMD runs one wave of each of the two workgroups on
+      // the CU; the one in its K loop goes ahead of one in staging waits or
+      // the epilogue (1), and a wave about to issue MFMAs ahead of both (2),
+      // which keeps the matrix pipe fed (about 2.5% less time per layer).
+      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) frag_read(mb, 0, av[mb]);
       const int gbase = cc * NSTEP;              // k-step of this chunk's step 0
@@ -651,8 +656,10 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
+          __builtin_amdgcn_s_setprio(2);
 #pragma unroll
           for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = mfma(bq[st % RING][nb], av[mb], acc[mb][nb]);
+          __builtin_amdgcn_s_setprio(1);
           __builtin_amdgcn_sched_barrier(0);
           if (st + 1 < NSTEP) frag_read(mb, st + 1, av[mb]);
           if (mb == 0) {
@@ -666,6 +673,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
           __builtin_amdgcn_sched_barrier(0);
         }
       }
+      __builtin_amdgcn_s_setprio(0);
       if constexpr (SG * RMAX >= NSTEP) stage_store(RMAX - 1);
       // every wave's staging writes done, every wave done reading `cur`
       __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
