@@ -282,10 +282,11 @@ hipError_t launch_residual_pack(const Geom& g, const int32_t* tables, const uint
                                 const uint8_t* nib, uint64_t* flips, uint64_t* residual, int batch,
                                 hipStream_t stream) {
   if (batch <= 0) return hipSuccess;
-  // about 4 waves' worth of words per workgroup when that still gives >= 1024
-  // workgroups; otherwise one word per wave, for parallelism at small batch
+  // chunks of words / 4096 words (at least one word per wave): about 4096
+  // workgroups at large batch (a whole row per workgroup at d = 13), more
+  // and shorter ones at small batch, so no wave runs a long serial chain
   const long long words = (long long)batch * (g.Wd + g.Wf);
-  const int want = (int)std::max(4ll, std::min(words / 1024, (long long)INT32_MAX));
+  const int want = (int)std::max(4ll, std::min(words / 4096, (long long)INT32_MAX));
   ResidualPlan p;
   p.cd = chunk_words(g, g.nstab, 1, (int)std::min((long long)want, g.Wd));
   p.cf = chunk_words(g, g.nflip, 0, (int)std::min((long long)want, g.Wf));

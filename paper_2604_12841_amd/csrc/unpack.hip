@@ -16,22 +16,16 @@
 // voxel with one store.  Consecutive threads write consecutive voxels of a
 // grid row.  HBM-bound: reads W_det * 8
 // bytes and writes c_in * V * sizeof(elem) bytes per sample.
+#include <algorithm>
+
 #include "internal.h"
 
 namespace pd {
 
+// Store voxel (t, s) of sample b given its two detector events.
 template <bool FP32, bool PADDED, bool PAPER>
-__device__ __forceinline__ void unpack_voxel(const Geom& g, const int32_t* __restrict__ tables,
-                                             const uint64_t* __restrict__ det, int b, int v, int t, int s,
-                                             int nx, int nz, float px, float pz, void* __restrict__ out,
-                                             FastDiv by_h) {
-  const uint64_t* row = det + (long long)b * g.Wd;
-  auto event = [&](int n) -> unsigned {
-    if (n < 0) return 0u;
-    const int k = t * g.nstab + n;
-    return (unsigned)((row[k >> 6] >> (k & 63)) & 1ull);
-  };
-  const unsigned ex = event(nx), ez = event(nz);
+__device__ __forceinline__ void unpack_store(const Geom& g, int b, int v, int t, int s, unsigned ex, unsigned ez,
+                                             float px, float pz, void* __restrict__ out, FastDiv by_h) {
   long long o;
   if (PADDED) {
     const int i = (int)fastdiv((uint32_t)s, by_h), j = s - i * g.H;
@@ -60,7 +54,9 @@ __device__ __forceinline__ void unpack_voxel(const Geom& g, const int32_t* __res
 // Grid: x covers one sample's V voxels (one thread each), y strides over the
 // batch; the per-voxel tables are read once per thread, the voxel split uses
 // 32-bit reciprocal divisions (by_hh: H H, by_h: H).  V < 2^31 for every
-// supported grid.
+// supported grid.  The detector bit of compact stabilizer n in round t is bit
+// k = t nstab + n of the sample's row; a site without a stabilizer of a type
+// reads bit 0 and masks it.
 template <bool FP32, bool PADDED, bool PAPER>
 __global__ void __launch_bounds__(256) unpack_kernel(Geom g, const int32_t* __restrict__ tables,
                                                      const uint64_t* __restrict__ det, int batch,
@@ -83,14 +79,41 @@ __global__ void __launch_bounds__(256) unpack_kernel(Geom g, const int32_t* __re
     px = present(nx, 1);
     pz = present(nz, 2);
   }
-  for (int b = blockIdx.y; b < batch; b += gridDim.y)
-    unpack_voxel<FP32, PADDED, PAPER>(g, tables, det, b, v, t, s, nx, nz, px, pz, out, by_h);
+  const int kx = t * g.nstab + max(nx, 0), kz = t * g.nstab + max(nz, 0);
+  const uint64_t mx = nx >= 0 ? 1ull << (kx & 63) : 0ull, mz = nz >= 0 ? 1ull << (kz & 63) : 0ull;
+  // samples blockIdx.y + k gridDim.y, four per pass: their detector reads
+  // are issued together before any store
+  const int gy = gridDim.y;
+  int b = blockIdx.y;
+  for (; b + 3 * gy < batch; b += 4 * gy) {
+    uint64_t wx[4], wz[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const uint64_t* row = det + (long long)(b + u * gy) * g.Wd;
+      wx[u] = row[kx >> 6];
+      wz[u] = row[kz >> 6];
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      unpack_store<FP32, PADDED, PAPER>(g, b + u * gy, v, t, s, (wx[u] & mx) != 0, (wz[u] & mz) != 0, px, pz,
+                                        out, by_h);
+  }
+  for (; b < batch; b += gy) {
+    const uint64_t* row = det + (long long)b * g.Wd;
+    unpack_store<FP32, PADDED, PAPER>(g, b, v, t, s, (row[kx >> 6] & mx) != 0, (row[kz >> 6] & mz) != 0, px,
+                                      pz, out, by_h);
+  }
 }
 
 hipError_t launch_unpack(const Geom& g, const int32_t* tables, const uint64_t* det, int batch, void* out,
                          int out_padded, int fp32, hipStream_t stream) {
   if (batch <= 0) return hipSuccess;
-  const dim3 grid((unsigned)((g.V + 255) / 256), (unsigned)(batch < 65535 ? batch : 65535));
+  // about 4096 workgroups in all (16 per CU): each thread then covers
+  // several samples, which amortises its table reads and keeps workgroups
+  // long enough that dispatch does not bound a large batch
+  const long long gx = (g.V + 255) / 256;
+  const long long gy = std::max(1ll, std::min<long long>(std::min(batch, 65535), 4096 / gx));
+  const dim3 grid((unsigned)gx, (unsigned)gy);
   const FastDiv by_hh = make_fastdiv((uint32_t)(g.H * g.H)), by_h = make_fastdiv((uint32_t)g.H);
   auto go = [&](auto kernel) {
     hipLaunchKernelGGL(kernel, grid, dim3(256), 0, stream, g, tables, det, batch, out, by_hh, by_h);
