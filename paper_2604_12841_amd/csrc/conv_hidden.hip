@@ -629,6 +629,9 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
       // the CU; the one in its K loop goes ahead of one in staging waits or
       // the epilogue (1), and a wave about to issue MFMAs ahead of both (2),
       // which keeps the matrix pipe fed (about 2.5% less time per layer).
+      // The fp8 loop, with half the MFMA cycles per fragment read, also
+      // issues the next fragment reads at 2 (a further 2.5% at d = 13; no
+      // gain in bf16).
       __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) frag_read(mb, 0, av[mb]);
@@ -659,9 +662,10 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
           __builtin_amdgcn_s_setprio(2);
 #pragma unroll
           for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = mfma(bq[st % RING][nb], av[mb], acc[mb][nb]);
-          __builtin_amdgcn_s_setprio(1);
+          if constexpr (!F8) __builtin_amdgcn_s_setprio(1);
           __builtin_amdgcn_sched_barrier(0);
           if (st + 1 < NSTEP) frag_read(mb, st + 1, av[mb]);
+          if constexpr (F8) __builtin_amdgcn_s_setprio(1);  // fp8: the fragment reads go out at 2 too
           if (mb == 0) {
             if (st >= SG && st % SG == 0 && st / SG - 1 < RMAX) stage_store(st / SG - 1);
             if (st % SG == 0 && st / SG < RMAX) {
