@@ -34,7 +34,7 @@ typedef __attribute__((address_space(3))) u32x4 lds_u32x4_w;
 typedef __attribute__((address_space(3))) uint32_t lds_u32_w;
 
 constexpr int WAVES = 4;  // waves per workgroup
-constexpr int BPW = 2;    // 32-voxel blocks per wave
+constexpr int BPW = 2;    // 32-voxel blocks per wave on large launches (1 on small ones)
 
 // Divisors of the interior-voxel decode u -> (b, t, i, j).
 struct Decode {
@@ -82,14 +82,14 @@ __device__ __forceinline__ void gather(const Geom& g, const void* __restrict__ p
 }
 
 // Each workgroup stages the weight fragments in LDS once; each of its waves
-// then handles BPW consecutive 32-voxel blocks.
+// then handles bpw consecutive 32-voxel blocks.
 // F8: y holds E4M3 codes.
 template <int CIN, int COUT, int ACT, bool F8>
 __global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, const void* __restrict__ planes,
                                                                 void* __restrict__ y, int ystride,
                                                                 const u32x4* __restrict__ wfrag,
                                                                 const float* __restrict__ bias, Decode dc,
-                                                                int nvox) {
+                                                                int nvox, int bpw) {
   constexpr int NB = COUT / 32;
   constexpr int ESZ = F8 ? 1 : 2;        // bytes per output value
   constexpr int OSTR = COUT * ESZ + 16;  // padded LDS row stride (bytes)
@@ -106,8 +106,8 @@ __global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, const vo
   __syncthreads();
 
 #pragma unroll 1
-  for (int j = 0; j < BPW; ++j) {
-    const int u0 = ((blockIdx.x * WAVES + wave) * BPW + j) * 32;
+  for (int j = 0; j < bpw; ++j) {
+    const int u0 = ((blockIdx.x * WAVES + wave) * bpw + j) * 32;
     if (u0 >= nvox) break;
     const bool valid = u0 + l32 < nvox;
     const long long p = valid ? voxel_padded(g, dc, u0 + l32) : -1;
@@ -174,7 +174,11 @@ __global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, const vo
 hipError_t launch_conv_first(const Geom& g, int cin, int cout, int act, const void* planes, void* y, int ystride,
                              const void* wfrag, const float* bias, int batch, int fp8, hipStream_t stream) {
   const long long nvox = (long long)batch * g.V;  // < 2^31 (host check)
-  const long long nblk = (nvox + 32 * WAVES * BPW - 1) / (32 * WAVES * BPW);
+  // two blocks per wave amortise the weight staging once the launch has
+  // 512 or more workgroups of them; below that (small batches) one block per
+  // wave doubles the waves on a mostly idle chip
+  const int bpw = nvox >= 512LL * 32 * WAVES * BPW ? BPW : 1;
+  const long long nblk = (nvox + 32 * WAVES * bpw - 1) / (32 * WAVES * bpw);
   Decode dc;
   dc.by_v = make_fastdiv((uint32_t)g.V);
   dc.by_hh = make_fastdiv((uint32_t)(g.H * g.H));
@@ -185,11 +189,11 @@ hipError_t launch_conv_first(const Geom& g, int cin, int cout, int act, const vo
     if (fp8)
       hipLaunchKernelGGL((conv_first_kernel<I, C, decltype(A)::value, true>), dim3((unsigned)nblk),
                          dim3(64 * WAVES), lds, stream, g, planes, y, ystride, (const u32x4*)wfrag, bias, dc,
-                         (int)nvox);
+                         (int)nvox, bpw);
     else
       hipLaunchKernelGGL((conv_first_kernel<I, C, decltype(A)::value, false>), dim3((unsigned)nblk),
                          dim3(64 * WAVES), lds, stream, g, planes, y, ystride, (const u32x4*)wfrag, bias, dc,
-                         (int)nvox);
+                         (int)nvox, bpw);
   };
   if ((cin != 2 && cin != 4) || (cout != 64 && cout != 128) || act < 0 || act > 2) return hipErrorInvalidValue;
   with_activation(act, [&](auto A) {
