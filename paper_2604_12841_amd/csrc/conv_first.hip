@@ -82,14 +82,15 @@ __device__ __forceinline__ void gather(const Geom& g, const void* __restrict__ p
 }
 
 // Each workgroup stages the weight fragments in LDS once; each of its waves
-// then handles bpw consecutive 32-voxel blocks.
+// then handles bpw consecutive work units: a unit is a 32-voxel block and,
+// with hsplit = 2 (small launches, c_out = 128), one half of its channels.
 // F8: y holds E4M3 codes.
 template <int CIN, int COUT, int ACT, bool F8>
 __global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, const void* __restrict__ planes,
                                                                 void* __restrict__ y, int ystride,
                                                                 const u32x4* __restrict__ wfrag,
                                                                 const float* __restrict__ bias, Decode dc,
-                                                                int nvox, int bpw) {
+                                                                int nvox, int bpw, int hsplit) {
   constexpr int NB = COUT / 32;
   constexpr int ESZ = F8 ? 1 : 2;        // bytes per output value
   constexpr int OSTR = COUT * ESZ + 16;  // padded LDS row stride (bytes)
@@ -107,8 +108,11 @@ __global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, const vo
 
 #pragma unroll 1
   for (int j = 0; j < bpw; ++j) {
-    const int u0 = ((blockIdx.x * WAVES + wave) * bpw + j) * 32;
+    const int unit = (blockIdx.x * WAVES + wave) * bpw + j;
+    const int blk = hsplit == 1 ? unit : unit >> 1, part = unit - blk * hsplit;
+    const int u0 = blk * 32;
     if (u0 >= nvox) break;
+    const int hb = part * (NB / hsplit), he = hb + NB / hsplit;  // this unit's 32-channel blocks
     const bool valid = u0 + l32 < nvox;
     const long long p = valid ? voxel_padded(g, dc, u0 + l32) : -1;
     u32x4 bx[KS];
@@ -119,6 +123,7 @@ __global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, const vo
     constexpr int NH = NB < 2 ? NB : 2;
 #pragma unroll
     for (int h0 = 0; h0 < NB; h0 += NH) {
+      if (h0 < hb || h0 >= he) continue;  // uniform per wave
       f32x16 acc[NH];
 #pragma unroll
       for (int nb = 0; nb < NH; ++nb)
@@ -155,11 +160,14 @@ __global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, const vo
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's tile is in LDS
     __builtin_amdgcn_wave_barrier();
-    // whole rows: 32 rows x GPR granules of 16 bytes, 64 lanes at a time
+    // the unit's part of each row: 32 rows x gpp granules of 16 bytes, 64
+    // lanes at a time
+    const int gpp = GPR / hsplit, c0 = part * gpp;
 #pragma unroll
     for (int k = 0; k < 32 * GPR / 64; ++k) {
+      if (k * 64 >= 32 * gpp) break;  // uniform
       const int qq = k * 64 + lane;
-      const int row = qq / GPR, c = qq % GPR;
+      const int row = qq / gpp, c = c0 + qq % gpp;
       const int pr = ((__attribute__((address_space(3))) const int*)prow)[row];
       const u32x4 val = *(lds_u32x4*)(tile + row * OSTR + c * 16);
       if (pr >= 0) *reinterpret_cast<u32x4*>((char*)y + (long long)pr * ystride * ESZ + c * 16) = val;
@@ -178,7 +186,10 @@ hipError_t launch_conv_first(const Geom& g, int cin, int cout, int act, const vo
   // 512 or more workgroups of them; below that (small batches) one block per
   // wave doubles the waves on a mostly idle chip
   const int bpw = nvox >= 512LL * 32 * WAVES * BPW ? BPW : 1;
-  const long long nblk = (nvox + 32 * WAVES * bpw - 1) / (32 * WAVES * bpw);
+  // ... and below 256 workgroups of single blocks, 128-channel layers split
+  // each block's channels over two waves
+  const int hsplit = (bpw == 1 && cout == 128 && nvox < 256LL * 32 * WAVES) ? 2 : 1;
+  const long long nblk = (nvox * hsplit + 32 * WAVES * bpw - 1) / (32 * WAVES * bpw);
   Decode dc;
   dc.by_v = make_fastdiv((uint32_t)g.V);
   dc.by_hh = make_fastdiv((uint32_t)(g.H * g.H));
@@ -189,11 +200,11 @@ hipError_t launch_conv_first(const Geom& g, int cin, int cout, int act, const vo
     if (fp8)
       hipLaunchKernelGGL((conv_first_kernel<I, C, decltype(A)::value, true>), dim3((unsigned)nblk),
                          dim3(64 * WAVES), lds, stream, g, planes, y, ystride, (const u32x4*)wfrag, bias, dc,
-                         (int)nvox, bpw);
+                         (int)nvox, bpw, hsplit);
     else
       hipLaunchKernelGGL((conv_first_kernel<I, C, decltype(A)::value, false>), dim3((unsigned)nblk),
                          dim3(64 * WAVES), lds, stream, g, planes, y, ystride, (const u32x4*)wfrag, bias, dc,
-                         (int)nvox, bpw);
+                         (int)nvox, bpw, hsplit);
   };
   if ((cin != 2 && cin != 4) || (cout != 64 && cout != 128) || act < 0 || act > 2) return hipErrorInvalidValue;
   with_activation(act, [&](auto A) {
