@@ -735,14 +735,35 @@ __global__ void __launch_bounds__(256) split_finish_kernel(Geom g, Tiling tl, in
   // pre-activation of channels c .. c + 7 of this row: the sum over the
   // tile's parts in part order (fp8: times the channel's weight scale), plus
   // the bias
+  // Parts are added strictly in part order; from four parts on they are read
+  // four at a time, so the four reads go out together.
   auto sum8 = [&](int c, float (&v)[8]) {
-    for (int p = 0; p < ksplit; ++p) {
-      const float* src = partial + ((size_t)((tile << kshift) + p) * kTileRows + r) * cout + c;
-      const float4 a = *reinterpret_cast<const float4*>(src);
-      const float4 b = *reinterpret_cast<const float4*>(src + 4);
-      const float t[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+    if (ksplit < 4) {
+      for (int p = 0; p < ksplit; ++p) {
+        const float* src = partial + ((size_t)((tile << kshift) + p) * kTileRows + r) * cout + c;
+        const float4 a = *reinterpret_cast<const float4*>(src);
+        const float4 b = *reinterpret_cast<const float4*>(src + 4);
+        const float t[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
 #pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = p == 0 ? t[e] : v[e] + t[e];
+        for (int e = 0; e < 8; ++e) v[e] = p == 0 ? t[e] : v[e] + t[e];
+      }
+    }
+    for (int p0 = 0; p0 < ksplit && ksplit >= 4; p0 += 4) {
+      float4 a[4], b[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int p = p0 + q;  // < ksplit: ksplit is a power of two >= 4
+        const float* src = partial + ((size_t)((tile << kshift) + p) * kTileRows + r) * cout + c;
+        a[q] = *reinterpret_cast<const float4*>(src);
+        b[q] = *reinterpret_cast<const float4*>(src + 4);
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int p = p0 + q;
+        const float t[8] = {a[q].x, a[q].y, a[q].z, a[q].w, b[q].x, b[q].y, b[q].z, b[q].w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = p == 0 ? t[e] : v[e] + t[e];
+      }
     }
 #pragma unroll
     for (int e = 0; e < 8; ++e) v[e] = F8 ? __builtin_fmaf(v[e], bias[cout + c + e], bias[c + e]) : v[e] + bias[c + e];
