@@ -157,3 +157,29 @@ def test_buffer_reuse_at_other_row_widths(cuda):
     st = compare(d, T, "fp32", *oracle.run(d, T, det, lf, wf, bf16=False), flips, res, logits)
     say("  reuse at other widths fp32", st)
     assert_parity(st, "fp32")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+def test_layer1_same_at_any_launch_size(cuda, dtype):
+    """Layer 1 divides its work by launch size (two 32-voxel blocks per wave
+    on large launches; one block, and for 128 channels its two 64-channel
+    halves on two waves, on small ones): a sample's layer-1 activations are
+    bit-identical either way (no split sums in layer 1)."""
+    d = T = 5
+    layers = workload.layer_spec(3, 128)
+    weights = workload.he_normal_weights(layers, 81)
+    B = 800  # 800 x 180 voxels: past the large-launch threshold
+    det, _ = workload.make_inputs(d, T, B, 0.01, 0.01, 82)
+    pre = pdx.Predecoder(weights, d, T, layers, dtype, max_batch=B)
+    ddet = torch.from_numpy(np.ascontiguousarray(det).view(np.int64)).cuda()
+    H = pre.grid
+    el = torch.uint8 if dtype == "fp8" else torch.int16
+    big = torch.empty((B, T, H, H, 128), dtype=el, device="cuda")
+    pre.activations(ddet, 0, big)
+    one = torch.empty((1, T, H, H, 128), dtype=el, device="cuda")
+    for s in (0, 517, B - 1):
+        say("layer 1", dtype, "sample", s)
+        pre.activations(ddet[s:s + 1], 0, one, batch=1)
+        torch.cuda.synchronize()
+        assert torch.equal(one[0].cpu(), big[s].cpu())
+    pre.close()
