@@ -69,7 +69,8 @@ def _load():
         lib.oracle_unpack_paper.restype = None
         lib.oracle_forward_grid.argtypes = [i32, i32, i32, vp, i32, vp, vp, i32, vp]
         lib.oracle_forward_grid.restype = None
-        lib.oracle_forward_grid_fp8_perturbed.argtypes = [i32, i32, i32, vp, i32, vp, vp, ctypes.c_double, vp]
+        lib.oracle_forward_grid_fp8_perturbed.argtypes = [i32, i32, i32, vp, i32, vp, vp, ctypes.c_double,
+                                                          ctypes.c_uint64, vp]
         lib.oracle_forward_grid_fp8_perturbed.restype = None
         lib.oracle_flips_residual_paper.argtypes = [i32, i32, i32, vp, vp, vp, vp]
         lib.oracle_flips_residual_paper.restype = None
@@ -77,6 +78,8 @@ def _load():
         lib.oracle_resnet_weight_count.restype = i64
         lib.oracle_forward_resnet.argtypes = [i32, i32, i32, vp, i32, vp, vp, i32, vp]
         lib.oracle_forward_resnet.restype = None
+        lib.oracle_conv_sums.argtypes = [i32, i32, i32, vp, i32, i32, i32, vp, vp, vp, i32]
+        lib.oracle_conv_sums.restype = None
         lib.oracle_e4m3_value.argtypes = [i32]
         lib.oracle_e4m3_value.restype = ctypes.c_double
         lib.oracle_e4m3_code.argtypes = [ctypes.c_float]
@@ -176,13 +179,14 @@ def weight_count(layers):
     return int(_load().oracle_weight_count(len(layers), _ptr(spec)))
 
 
-def forward(d, T, planes, layers, weights, bf16, layout="plaquette", fp8=False, fp8_sum_eps=0.0):
+def forward(d, T, planes, layers, weights, bf16, layout="plaquette", fp8=False, fp8_sum_eps=None, fp8_sum_seed=0):
     """Network forward.  planes [B][c_in][T][H][H] float64; layers: list of
     (c_in, c_out, k, act); weights: flat fp32.  Returns logits
     [B][c_out_last][T][H][H] float64 (fp32-valued in bf16 and fp8 mode).
     bf16 / fp8 select the quantisation points of that precision (fp8 wins);
-    fp8_sum_eps > 0 (fp8 only): every sum of products moved by a hashed
-    u * eps * sum|products|, u in [-1, 1) (sizes the fp8 parity tolerance)."""
+    fp8_sum_eps (fp8 only; None: the plain forward): every sum of products
+    moved by a hashed u * eps * sum|products|, u in [-1, 1), the pattern
+    chosen by fp8_sum_seed (sizes the fp8 parity bounds)."""
     planes = np.ascontiguousarray(planes, dtype=np.float64)
     weights = np.ascontiguousarray(weights, dtype=np.float32)
     spec = np.ascontiguousarray(np.array([list(l) for l in layers], dtype=np.int32).ravel())
@@ -194,11 +198,11 @@ def forward(d, T, planes, layers, weights, bf16, layout="plaquette", fp8=False, 
         raise ValueError("planes shape mismatch")
     co = layers[-1][1]
     out = np.zeros((B, co, T, H, H), dtype=np.float64)
-    if fp8_sum_eps > 0:
+    if fp8_sum_eps is not None:
         if not fp8:
             raise ValueError("fp8_sum_eps applies to the fp8 forward")
         _load().oracle_forward_grid_fp8_perturbed(H, T, B, _ptr(planes), len(layers), _ptr(spec), _ptr(weights),
-                                                  float(fp8_sum_eps), _ptr(out))
+                                                  float(fp8_sum_eps), int(fp8_sum_seed), _ptr(out))
     else:
         prec = 2 if fp8 else (1 if bf16 else 0)
         _load().oracle_forward_grid(H, T, B, _ptr(planes), len(layers), _ptr(spec), _ptr(weights), prec,
@@ -301,6 +305,24 @@ def forward_resnet(d, T, planes, blocks, weights, bf16, layout="plaquette", acc3
     prec = (2 if acc32 else 1) if bf16 else 0
     _load().oracle_forward_resnet(H, T, B, _ptr(planes), len(blocks), _ptr(spec), _ptr(weights), prec, _ptr(out))
     return out
+
+
+def conv_sums(x, w, bias, acc32=False):
+    """One conv3d of the residual-network forward (cross-correlation, zero
+    padding (k-1)/2): x [B][c_in][T][H][H], w [c_out][c_in][k][k][k], bias
+    [c_out], all float64 -> [B][c_out][T][H][H]; sums over (c_in, kt, ki, kj)
+    in that order, in fp64, or with acc32 each product rounded to fp32 and
+    added to an fp32 sum."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    w = np.ascontiguousarray(w, dtype=np.float64)
+    bias = np.ascontiguousarray(bias, dtype=np.float64)
+    B, ci, T, H, _ = x.shape
+    co, k = w.shape[0], w.shape[2]
+    if w.shape != (co, ci, k, k, k) or bias.shape != (co,) or k % 2 != 1:
+        raise ValueError("conv_sums shapes")
+    y = np.zeros((B, co, T, H, H), dtype=np.float64)
+    _load().oracle_conv_sums(H, T, B, _ptr(x), ci, co, k, _ptr(w), _ptr(bias), _ptr(y), int(bool(acc32)))
+    return y
 
 
 def run_resnet(d, T, det, blocks, weights, bf16, layout="paper", first=None, last=None):

@@ -276,11 +276,15 @@ int oracle_e4m3_scale_exp(double amax) {
 }
 
 /* GELU, tanh approximation (Table hyperparameters):
- *   0.5 y (1 + tanh(sqrt(2/pi) (y + 0.044715 y^3))). */
+ *   0.5 y (1 + tanh(u)),  u = sqrt(2/pi) (y + 0.044715 y^3),
+ * evaluated as y / (1 + exp(-2u)), the same function (1 + tanh(u) =
+ * 2 / (1 + exp(-2u))): in fp64, 1 + tanh(u) cancels once tanh(u) is within a
+ * few ulps of -1 (u below about -18, y below about -5.5) and loses every
+ * digit of the small result, which this form keeps. */
 double oracle_gelu_tanh(double y) {
   const double pi = 3.14159265358979323846;
   double u = sqrt(2.0 / pi) * (y + 0.044715 * y * y * y);
-  return 0.5 * y * (1.0 + tanh(u));
+  return y / (1.0 + exp(-2.0 * u));
 }
 
 enum { ACT_NONE = 0, ACT_GELU_TANH = 1, ACT_RELU = 2 };
@@ -323,11 +327,12 @@ static double unit_hash(uint64_t key) {
 }
 
 /* eps > 0 (fp8 only; test infrastructure): every sum of products is moved
- * by u eps sum |products|, u in [-1, 1) hashed from (layer, sample, channel,
- * voxel): a summation whose error is bounded by eps relative to the sum of
- * magnitudes, used to size the fp8 parity tolerance. */
+ * by u eps sum |products|, u in [-1, 1) hashed from (seed, layer, sample,
+ * channel, voxel): a summation whose error is bounded by eps relative to the
+ * sum of magnitudes, used to size the fp8 parity bounds.  Different seeds
+ * give independent patterns of such errors. */
 static void forward_impl(int H, int T, int B, const double* planes, int n_layers, const int* spec,
-                         const float* weights, int prec, double eps, double* logits) {
+                         const float* weights, int prec, double eps, uint64_t seed, double* logits) {
   const int bf16 = prec == 1, fp8 = prec == 2;
   int64_t V = (int64_t)T * H * H;
   int cmax = spec[0];
@@ -379,53 +384,70 @@ static void forward_impl(int H, int T, int B, const double* planes, int n_layers
       for (int co = 0; co < co_n; ++co) {
         const double* x = xa + (int64_t)b * cmax * V;
         double* y = xb + (int64_t)b * cmax * V + (int64_t)co * V;
-        for (int t = 0; t < T; ++t)
-          for (int i = 0; i < H; ++i)
-            for (int j = 0; j < H; ++j) {
-              double acc = 0.0, mag = 0.0;
-              for (int ci = 0; ci < ci_n; ++ci)
-                for (int kt = 0; kt < k; ++kt) {
+        /* acc[v] = sum over (ci, kt, ki, kj), in that order, of w * x at the
+         * tap's input voxel (taps outside the volume contribute nothing);
+         * mag[v] the same sum of magnitudes.  The voxel loops sit inside the
+         * tap loops so that each tap sweeps the input contiguously; every
+         * output still adds its products in the order above. */
+        double* acc = (double*)calloc((size_t)V, sizeof(double));
+        double* mag = (double*)calloc((size_t)V, sizeof(double));
+        for (int ci = 0; ci < ci_n; ++ci)
+          for (int kt = 0; kt < k; ++kt)
+            for (int ki = 0; ki < k; ++ki)
+              for (int kj = 0; kj < k; ++kj) {
+                const double wv = wl[(((int64_t)co * ci_n + ci) * k + kt) * k * k + ki * k + kj];
+                for (int t = 0; t < T; ++t) {
                   int tt = t + kt - p;
                   if (tt < 0 || tt >= T) continue;
-                  for (int ki = 0; ki < k; ++ki) {
+                  for (int i = 0; i < H; ++i) {
                     int ii = i + ki - p;
                     if (ii < 0 || ii >= H) continue;
-                    for (int kj = 0; kj < k; ++kj) {
-                      int jj = j + kj - p;
-                      if (jj < 0 || jj >= H) continue;
-                      const double pr = wl[(((int64_t)co * ci_n + ci) * k + kt) * k * k + ki * k + kj] *
-                                        x[(((int64_t)ci * T + tt) * H + ii) * H + jj];
-                      acc += pr;
-                      mag += fabs(pr);
+                    const double* xr = x + (((int64_t)ci * T + tt) * H + ii) * H;
+                    double* ar = acc + ((int64_t)t * H + i) * H;
+                    double* mr = mag + ((int64_t)t * H + i) * H;
+                    /* the j whose tap column j + kj - p lies in [0, H) */
+                    const int j0 = p - kj > 0 ? p - kj : 0, j1 = H + p - kj < H ? H + p - kj : H;
+                    for (int j = j0; j < j1; ++j) {
+                      const double pr = wv * xr[j + kj - p];
+                      ar[j] += pr;
+                      mr[j] += fabs(pr);
                     }
                   }
                 }
+              }
+        for (int t = 0; t < T; ++t)
+          for (int i = 0; i < H; ++i)
+            for (int j = 0; j < H; ++j) {
+              const int64_t v = ((int64_t)t * H + i) * H + j;
+              double a = acc[v];
               if (eps > 0.0) {
                 const uint64_t key = ((((((uint64_t)l * 65536 + b) * 4096 + co) * 2048 + t) * 256 + i) * 256) + j;
-                acc += unit_hash(key) * eps * mag;
+                a += unit_hash(key ^ (seed * 0xd1b54a32d192ed03ull)) * eps * mag[v];
               }
-              double v;
+              double out;
               if (fp8) {
-                float pre = (float)(acc + bl[co]);
+                float pre = (float)(a + bl[co]);
                 if (last) {
-                  v = (double)pre; /* fp32 logit */
+                  out = (double)pre; /* fp32 logit */
                 } else {
-                  float a = (float)activation(act, (double)pre);
-                  v = oracle_round_e4m3(a);
+                  float av = (float)activation(act, (double)pre);
+                  out = oracle_round_e4m3(av);
                 }
               } else if (bf16) {
-                float pre = (float)(acc + bl[co]);
+                float pre = (float)(a + bl[co]);
                 if (last) {
-                  v = (double)pre; /* fp32 logit */
+                  out = (double)pre; /* fp32 logit */
                 } else {
-                  float a = (float)activation(act, (double)pre);
-                  v = (double)oracle_round_bf16(a);
+                  float av = (float)activation(act, (double)pre);
+                  out = (double)oracle_round_bf16(av);
                 }
               } else {
-                v = last ? acc + bl[co] : activation(act, acc + bl[co]);
+                out = last ? a + bl[co] : activation(act, a + bl[co]);
               }
-              y[((int64_t)t * H + i) * H + j] = v;
+              y[v] = out;
             }
+        free(acc);
+        free(mag);
       }
     double* tmp = xa;
     xa = xb;
@@ -447,13 +469,14 @@ static void forward_impl(int H, int T, int B, const double* planes, int n_layers
 
 void oracle_forward_grid(int H, int T, int B, const double* planes, int n_layers, const int* spec,
                          const float* weights, int prec, double* logits) {
-  forward_impl(H, T, B, planes, n_layers, spec, weights, prec, 0.0, logits);
+  forward_impl(H, T, B, planes, n_layers, spec, weights, prec, 0.0, 0, logits);
 }
 
-/* fp8 forward with the bounded summation error described at forward_impl. */
+/* fp8 forward with the bounded summation error described at forward_impl
+ * (eps = 0: the plain fp8 forward). */
 void oracle_forward_grid_fp8_perturbed(int H, int T, int B, const double* planes, int n_layers, const int* spec,
-                                       const float* weights, double eps, double* logits) {
-  forward_impl(H, T, B, planes, n_layers, spec, weights, 2, eps, logits);
+                                       const float* weights, double eps, uint64_t seed, double* logits) {
+  forward_impl(H, T, B, planes, n_layers, spec, weights, 2, eps, seed, logits);
 }
 
 /* The same on the (d+1) x (d+1) plaquette grid. */
@@ -639,34 +662,45 @@ static void conv_sums(int H, int T, int B, const double* x, int ci_n, int co_n, 
   const int p = (k - 1) / 2;
 #pragma omp parallel for collapse(2) schedule(dynamic)
   for (int b = 0; b < B; ++b)
-    for (int co = 0; co < co_n; ++co)
-      for (int t = 0; t < T; ++t)
-        for (int i = 0; i < H; ++i)
-          for (int j = 0; j < H; ++j) {
-            double acc = 0.0;
-            float accf = 0.0f;
-            for (int ci = 0; ci < ci_n; ++ci)
-              for (int kt = 0; kt < k; ++kt) {
+    for (int co = 0; co < co_n; ++co) {
+      /* per output voxel, the products in (ci, kt, ki, kj) order; the voxel
+       * loops sit inside the tap loops (each output's order is unchanged) */
+      double* acc = (double*)calloc((size_t)V, sizeof(double));
+      float* accf = (float*)calloc((size_t)V, sizeof(float));
+      for (int ci = 0; ci < ci_n; ++ci)
+        for (int kt = 0; kt < k; ++kt)
+          for (int ki = 0; ki < k; ++ki)
+            for (int kj = 0; kj < k; ++kj) {
+              const double wv = w[(((int64_t)co * ci_n + ci) * k + kt) * k * k + ki * k + kj];
+              for (int t = 0; t < T; ++t) {
                 const int tt = t + kt - p;
                 if (tt < 0 || tt >= T) continue;
-                for (int ki = 0; ki < k; ++ki) {
+                for (int i = 0; i < H; ++i) {
                   const int ii = i + ki - p;
                   if (ii < 0 || ii >= H) continue;
-                  for (int kj = 0; kj < k; ++kj) {
-                    const int jj = j + kj - p;
-                    if (jj < 0 || jj >= H) continue;
-                    const double pr = w[(((int64_t)co * ci_n + ci) * k + kt) * k * k + ki * k + kj] *
-                                      x[(((int64_t)b * ci_n + ci) * T + tt) * H * H + (int64_t)ii * H + jj];
-                    if (acc32)
-                      accf += (float)pr;
-                    else
-                      acc += pr;
-                  }
+                  const double* xr = x + (((int64_t)b * ci_n + ci) * T + tt) * H * H + (int64_t)ii * H;
+                  const int64_t o = ((int64_t)t * H + i) * H;
+                  /* the j whose tap column j + kj - p lies in [0, H) */
+                  const int j0 = p - kj > 0 ? p - kj : 0, j1 = H + p - kj < H ? H + p - kj : H;
+                  if (acc32)
+                    for (int j = j0; j < j1; ++j) accf[o + j] += (float)(wv * xr[j + kj - p]);
+                  else
+                    for (int j = j0; j < j1; ++j) acc[o + j] += wv * xr[j + kj - p];
                 }
               }
-            if (acc32) acc = (double)accf;
-            y[((int64_t)b * co_n + co) * V + ((int64_t)t * H + i) * H + j] = acc + bias[co];
-          }
+            }
+      for (int64_t v = 0; v < V; ++v)
+        y[((int64_t)b * co_n + co) * V + v] = (acc32 ? (double)accf[v] : acc[v]) + bias[co];
+      free(acc);
+      free(accf);
+    }
+}
+
+/* conv_sums as a library entry (test infrastructure: pins its two
+ * summation modes). */
+void oracle_conv_sums(int H, int T, int B, const double* x, int ci_n, int co_n, int k, const double* w,
+                      const double* bias, double* y, int acc32) {
+  conv_sums(H, T, B, x, ci_n, co_n, k, w, bias, y, acc32);
 }
 
 /* Number of floats of a residual network's weights: per block (c_in, c_mid,

@@ -58,6 +58,21 @@ def test_bf16_rounding_matches_torch():
     np.testing.assert_array_equal(oracle.round_bf16(x), ref)
 
 
+def _gelu_decimal(y, digits=160):
+    """0.5 y (1 + tanh(u)), u = sqrt(2/pi) (y + 0.044715 y^3), written as
+    printed and evaluated with `digits` significant digits (tanh from exp),
+    enough to keep 1 + tanh(u) exact to fp64 precision down to y = -12."""
+    import decimal
+    from decimal import Decimal as D
+    with decimal.localcontext() as ctx:
+        ctx.prec = digits
+        pi = D("3.14159265358979323846264338327950288419716939937510582097494459230781640628620899862803482534211706")
+        yd = D(float(y))
+        u = (D(2) / pi).sqrt() * (yd + D("0.044715") * yd ** 3)
+        e2 = (2 * u).exp()
+        return float(D("0.5") * yd * (1 + (e2 - 1) / (e2 + 1)))
+
+
 def test_gelu_tanh_matches_library_and_limits():
     x = np.linspace(-12, 12, 4001)
     ref = F.gelu(torch.from_numpy(x), approximate="tanh").numpy()
@@ -65,6 +80,23 @@ def test_gelu_tanh_matches_library_and_limits():
     assert oracle.gelu_tanh(np.array([0.0]))[0] == 0.0
     assert abs(oracle.gelu_tanh(np.array([30.0]))[0] - 30.0) < 1e-12
     assert abs(oracle.gelu_tanh(np.array([-30.0]))[0]) < 1e-12
+
+
+def test_gelu_tanh_relative_accuracy_against_160_digits():
+    """Relative error of a few fp64 ulps (times |2u|, the argument of the
+    exponential) everywhere, including large negative
+    y, where the result is tiny (the printed form's 1 + tanh(u) cancels in
+    fp64 there: torch's fp64 GELU is off by 5 % at y = -7.09 and returns 0
+    below y = -7.6)."""
+    ys = np.concatenate([np.linspace(-12, 12, 481), [-7.08542042, -7.82862299, -1e-3, 1e-3, -0.7517]])
+    got = oracle.gelu_tanh(ys)
+    ref = np.array([_gelu_decimal(v) for v in ys])
+    rel = np.abs(got - ref) / np.maximum(np.abs(ref), 1e-300)
+    # exp(-2u) inherits the rounding error of its argument: |2u| ulps
+    two_u = 2 * np.sqrt(2 / np.pi) * np.abs(ys + 0.044715 * ys ** 3)
+    bound = (8 + 4 * two_u) * 2.0 ** -53
+    assert (rel <= bound).all(), (ys[np.argmax(rel / bound)], (rel / bound).max())
+    assert (got[ys < -5] != 0).all() and (got[ys < 0] < 0).all()
 
 
 def test_cross_correlation_orientation_on_2x2x2():
