@@ -9,9 +9,12 @@ can then round to the other neighbour, and the difference (one E4M3 step)
 spreads through the later layers.  The model: the oracle's fp8 forward with
 every sum moved by u EPS sum|products| (u in [-1, 1), hashed), EPS = 2^-16,
 which bounds that error over any number of sums (triangle inequality), against
-the exact oracle.  On every fp8 parity case (tests/fp8_cases.py) this records
-the max abs logit difference (and, for information, the fraction of logits
-that differ by more than 1e-3); the bound is MARGIN times the largest.
+the exact oracle, for SEEDS independent hashed patterns.  On every fp8 parity
+case (tests/fp8_cases.py) this records the max abs logit difference over the
+patterns (and, for information, the fraction of logits that differ by more
+than 1e-3); the bound is MARGIN times the largest.  The parity tests use it as
+the logit bound and as the excuse band of the flips (sites whose oracle
+|logit| is within it).
 
 Run from the repository root:  python tests/golden/make_fp8_tolerance.py
 """
@@ -31,6 +34,7 @@ from fp8_cases import FP8_CASES, case_inputs  # noqa: E402
 MARGIN = 2.0
 FAR_ABS = 1e-3
 EPS = 2.0 ** -16
+SEEDS = 4
 
 
 def main():
@@ -39,17 +43,20 @@ def main():
         d, T, layers, weights, det, layout, first, last = case_inputs(case)
         planes = oracle.unpack_paper(d, T, det, first, last) if layout == "paper" else oracle.unpack(d, T, det)
         a = oracle.forward(d, T, planes, layers, weights, False, layout, fp8=True)
-        b = oracle.forward(d, T, planes, layers, weights, False, layout, fp8=True, fp8_sum_eps=EPS)
-        err = np.abs(a - b)
+        err = np.zeros_like(a)
+        for seed in range(SEEDS):
+            b = oracle.forward(d, T, planes, layers, weights, False, layout, fp8=True, fp8_sum_eps=EPS,
+                               fp8_sum_seed=seed)
+            err = np.maximum(err, np.abs(a - b))
         row = dict(name=case["name"], max_abs=float(err.max()), frac_far=float((err > FAR_ABS).mean()),
                    median_abs_logit=float(np.median(np.abs(a))))
         print(row, flush=True)
         rows.append(row)
     out = dict(
         note="fp8 parity bounds: MARGIN x the largest difference between the oracle's exact fp8 forward and "
-             "the same with every sum moved by up to EPS sum|products| over the fp8 parity cases "
-             "(make_fp8_tolerance.py)",
-        margin=MARGIN, far_abs=FAR_ABS, eps=EPS,
+             "the same with every sum moved by up to EPS sum|products| (SEEDS hashed patterns) over the fp8 "
+             "parity cases (make_fp8_tolerance.py)",
+        margin=MARGIN, far_abs=FAR_ABS, eps=EPS, seeds=SEEDS,
         tol_max_abs_logit_err=MARGIN * max(r["max_abs"] for r in rows),
         cases=rows)
     with open(os.path.join(HERE, "fp8_tolerance.json"), "w") as f:
