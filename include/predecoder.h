@@ -213,8 +213,13 @@ pd_status predecoder_unpack(pd_predecoder* h, void* hip_stream, const uint64_t* 
  * PD_DTYPE_BF16, E4M3 codes as uint8 for PD_DTYPE_FP8).  For inspecting and
  * testing one layer at a time (Sec. IV.B, Fig. ConvArch: the activations
  * between the conv layers); a head that predecoder_run fuses into that layer
- * is not run.  PD_ERR_INVALID_ARG for a layer out of range, PD_ERR_UNSUPPORTED
- * for PD_DTYPE_FP32.  Asynchronous on hip_stream. */
+ * is not run.  On a residual network (predecoder_create_resnet) `layer`
+ * counts its convs block by block -- conv1, the 1x1x1 projection if the
+ * block has one, conv2 (with the shortcut added and the activation applied)
+ * -- up to but not including the last block's conv2 (the output layer), and
+ * c_out is that conv's width (Fig. Model8Representation).
+ * PD_ERR_INVALID_ARG for a layer out of range, PD_ERR_UNSUPPORTED for
+ * PD_DTYPE_FP32.  Asynchronous on hip_stream. */
 pd_status predecoder_activations(pd_predecoder* h, void* hip_stream, const uint64_t* det,
                                  int32_t batch, int32_t layer, void* out);
 
@@ -286,7 +291,8 @@ void predecoder_graph_destroy(pd_graph* g); /* NULL is a no-op; waits for the de
  * {64, 128, 256, 512}, c_out == c_mid inside the network (others
  * PD_ERR_UNSUPPORTED).  predecoder_run / residual / unpack / stage_times /
  * destroy take the handle like any other (stages: unpack, one per block,
- * residual); predecoder_activations gives PD_ERR_UNSUPPORTED. */
+ * residual); predecoder_activations returns the output of any conv but the
+ * last (see there). */
 typedef struct pd_block {
   int32_t c_in, c_mid, c_out; /* conv1: c_in -> c_mid, conv2: c_mid -> c_out */
   int32_t act;                /* pd_act after conv1 and after the shortcut add */

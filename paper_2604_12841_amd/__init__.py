@@ -158,13 +158,31 @@ def weight_count(layers):
     return int(lib().predecoder_weight_count(_layers(layers), len(layers)))
 
 
-def _ptr(t):
-    """Raw device pointer of a tensor (or None)."""
+def _ptr(t, what="buffer", nbytes=0, elem=None):
+    """Raw device pointer of a tensor (or None), after checking that it is a
+    contiguous device tensor with elements of `elem` bytes (one of them, if a
+    tuple) and at least `nbytes` bytes: the kernels behind the C ABI read and
+    write that many bytes and cannot check a raw pointer themselves."""
     if t is None:
         return None
+    if not getattr(t, "is_cuda", False):
+        raise ValueError("%s must be a device (GPU) tensor" % what)
     if not t.is_contiguous():
-        raise ValueError("device buffers must be contiguous")
+        raise ValueError("%s must be contiguous" % what)
+    if elem is not None and t.element_size() not in (elem if isinstance(elem, tuple) else (elem,)):
+        raise ValueError("%s has %d-byte elements, expected %s" % (what, t.element_size(), elem))
+    have = t.numel() * t.element_size()
+    if have < nbytes:
+        raise ValueError("%s holds %d bytes, the call uses %d" % (what, have, nbytes))
     return ctypes.c_void_p(t.data_ptr())
+
+
+def _batch(batch, first):
+    """The batch of a call: given, or the leading dimension of `first`."""
+    b = int(first.shape[0]) if batch is None else int(batch)
+    if b < 1:
+        raise ValueError("batch must be >= 1")
+    return b
 
 
 def _stream(stream):
@@ -210,35 +228,68 @@ class Predecoder:
         if st != PD_OK:
             raise PredecoderError(st, what)
 
+    # ---- argument marshalling: every buffer checked against what the call
+    # reads or writes for `batch` samples ----
+
+    def _io(self, det, flips, residual, logits, batch):
+        """Pointers of a run's buffers (det, flips, residual, logits or None)."""
+        return (_ptr(det, "det", batch * self.det_words * 8, 8),
+                _ptr(flips, "flips", batch * self.flip_words * 8, 8),
+                _ptr(residual, "residual", batch * self.det_words * 8, 8),
+                _ptr(logits, "logits", batch * 4 * self.T * self.grid ** 2 * 4, 4))
+
+    def stop_channels(self, layer):
+        """Channels of what predecoder_activations returns for `layer`: a
+        hidden layer's width, or for a residual network the width of conv
+        number `layer` (per block: conv1, the projection if any, conv2)."""
+        if self.blocks is None:
+            if not 0 <= layer < len(self.layers) - 1:
+                raise ValueError("layer out of range")
+            return self.layers[layer][1]
+        outs = []
+        for ci, cm, co, _a in self.blocks:
+            outs += [cm] + ([co] if ci != co else []) + [co]
+        if not 0 <= layer < len(outs) - 1:
+            raise ValueError("layer out of range")
+        return outs[layer]
+
     def run(self, det, flips, residual, logits=None, batch=None, stream=None):
         """det [B][W_det] uint64-valued int64 tensor -> flips [B][W_flip], residual [B][W_det] (in place)."""
-        batch = det.shape[0] if batch is None else batch
-        self._check(lib().predecoder_run(self._h, _stream(stream), _ptr(det), batch, _ptr(flips),
-                                         _ptr(residual), _ptr(logits)), "predecoder_run")
+        batch = _batch(batch, det)
+        pd, pf, pr, pl = self._io(det, flips, residual, logits, batch)
+        self._check(lib().predecoder_run(self._h, _stream(stream), pd, batch, pf, pr, pl), "predecoder_run")
 
     def residual(self, det, flips, residual, batch=None, stream=None):
-        batch = det.shape[0] if batch is None else batch
-        self._check(lib().predecoder_residual(self._h, _stream(stream), _ptr(det), _ptr(flips), batch,
-                                              _ptr(residual)), "predecoder_residual")
+        batch = _batch(batch, det)
+        pd, pf, pr, _ = self._io(det, flips, residual, None, batch)
+        self._check(lib().predecoder_residual(self._h, _stream(stream), pd, pf, batch, pr), "predecoder_residual")
 
     def unpack(self, det, planes, batch=None, stream=None):
-        batch = det.shape[0] if batch is None else batch
-        self._check(lib().predecoder_unpack(self._h, _stream(stream), _ptr(det), batch, _ptr(planes)),
-                    "predecoder_unpack")
+        """det -> planes [B][T][H][H][c_in] (bf16 bits, or fp32 on an fp32 handle)."""
+        batch = _batch(batch, det)
+        c_in = 4 if self.layout == LAYOUT_PAPER else 2
+        elem = 4 if self.dtype == DTYPE_FP32 else 2
+        pd = _ptr(det, "det", batch * self.det_words * 8, 8)
+        pp = _ptr(planes, "planes", batch * self.T * self.grid ** 2 * c_in * elem, elem)
+        self._check(lib().predecoder_unpack(self._h, _stream(stream), pd, batch, pp), "predecoder_unpack")
 
     def activations(self, det, layer, out, batch=None, stream=None):
-        """Output activations of hidden layer `layer` -> out [B][T][H][H][c_out] (bf16 bits as int16,
-        E4M3 codes as uint8)."""
-        batch = det.shape[0] if batch is None else batch
-        self._check(lib().predecoder_activations(self._h, _stream(stream), _ptr(det), batch, layer, _ptr(out)),
+        """Output activations of hidden layer `layer` (residual networks: of conv number `layer`) -> out
+        [B][T][H][H][c_out] (bf16 bits as int16, E4M3 codes as uint8)."""
+        batch = _batch(batch, det)
+        elem = 1 if self.dtype == DTYPE_FP8 else 2
+        pd = _ptr(det, "det", batch * self.det_words * 8, 8)
+        po = _ptr(out, "out", batch * self.T * self.grid ** 2 * self.stop_channels(layer) * elem, elem)
+        self._check(lib().predecoder_activations(self._h, _stream(stream), pd, batch, layer, po),
                     "predecoder_activations")
 
     def graph(self, det, flips, residual, logits=None, batch=None):
         """Records one run with these buffers; returns a Graph to replay it."""
-        batch = det.shape[0] if batch is None else batch
+        batch = _batch(batch, det)
+        pd, pf, pr, pl = self._io(det, flips, residual, logits, batch)
         g = ctypes.c_void_p()
-        self._check(lib().predecoder_graph_create(self._h, _ptr(det), batch, _ptr(flips), _ptr(residual),
-                                                  _ptr(logits), ctypes.byref(g)), "predecoder_graph_create")
+        self._check(lib().predecoder_graph_create(self._h, pd, batch, pf, pr, pl, ctypes.byref(g)),
+                    "predecoder_graph_create")
         return Graph(g)
 
     @property
@@ -247,10 +298,11 @@ class Predecoder:
 
     def stage_times(self, det, flips, residual, n_iter, batch=None, stream=None):
         """Mean milliseconds of each stage over n_iter runs (blocks until done)."""
-        batch = det.shape[0] if batch is None else batch
+        batch = _batch(batch, det)
+        pd, pf, pr, _ = self._io(det, flips, residual, None, batch)
         out = (ctypes.c_float * self.num_stages)()
-        self._check(lib().predecoder_stage_times(self._h, _stream(stream), _ptr(det), batch, _ptr(flips),
-                                                 _ptr(residual), n_iter, out), "predecoder_stage_times")
+        self._check(lib().predecoder_stage_times(self._h, _stream(stream), pd, batch, pf, pr, n_iter, out),
+                    "predecoder_stage_times")
         return list(out)
 
     def close(self):
@@ -300,7 +352,11 @@ class Stream:
 
     def run(self, det, flips, residual, stream=None):
         """det [n_streams][W_det] -> flips [n_streams][W_flip], residual [n_streams][W_det] (device, in place)."""
-        st = lib().predecoder_stream_run(self._h, _stream(stream), _ptr(det), _ptr(flips), _ptr(residual))
+        n = self.n_streams
+        pd = _ptr(det, "det", n * self.det_words * 8, 8)
+        pf = _ptr(flips, "flips", n * self.flip_words * 8, 8)
+        pr = _ptr(residual, "residual", n * self.det_words * 8, 8)
+        st = lib().predecoder_stream_run(self._h, _stream(stream), pd, pf, pr)
         if st != PD_OK:
             raise PredecoderError(st, "predecoder_stream_run")
 

@@ -22,6 +22,31 @@
 using pd::Geom;
 using pd::Tiling;
 
+namespace {
+
+// Device memory one run works in besides its inputs, outputs, weights and
+// tables: the input planes, the activation buffers, the projection outputs of
+// residual blocks, the flip nibbles and the parked sums of split K loops.
+// A handle owns one (sized for max_batch at create); predecoder_run_static
+// lays one over the library's static scratch array for each call.
+struct Workspace {
+  void* planes = nullptr;                      // [batch * S][c_in], zero halo
+  void* act[3] = {nullptr, nullptr, nullptr};  // activations [batch * S][cmax]; act[2]: residual networks only
+  void* pbuf = nullptr;                        // projection outputs [batch * S][pmax] (residual networks)
+  uint8_t* nib = nullptr;                      // [batch][T][H][H] flip nibbles
+  float* partial = nullptr;                    // split K loops of small batches: fp32 sums of up to max_units units
+  long long max_units = 0;
+  size_t act_bytes = 0;                        // size of each activation buffer
+  // Row width (bytes per voxel) of the data each activation buffer holds, 0
+  // while it is all zero.  The 3x3x3 kernels read the zero halo around the
+  // interior voxels; a buffer written with one row width and then with
+  // another would show the old interior rows as halo, so it is zeroed first
+  // (prepare_rows).
+  int act_row[3] = {0, 0, 0};
+};
+
+}  // namespace
+
 struct pd_predecoder {
   Geom g;                        // includes the layout and the boundary bases
   int dtype = 0;
@@ -29,9 +54,7 @@ struct pd_predecoder {
   int device = 0;
   std::vector<pd_layer> layers;
   Tiling tiling{};               // shared by every 3x3x3 layer (bf16 path)
-  void* planes = nullptr;        // [max_batch * S][2]
-  void* act[2] = {nullptr, nullptr};  // [max_batch * S][cmax]
-  uint8_t* nib = nullptr;        // [max_batch][T][H][H] flip nibbles
+  Workspace ws;                  // sized for max_batch
   int32_t* tables = nullptr;
   std::vector<void*> wdev;       // per conv layer: fragments (bf16) or [tap][ci][co] (fp32)
   std::vector<size_t> wslice;    // per conv layer: bytes of the fragments of one 128-channel slice of a
@@ -44,19 +67,9 @@ struct pd_predecoder {
   // in), proj_w / proj_b its projection (null for an identity shortcut)
   std::vector<pd_block> blocks;
   std::vector<float*> proj_w, proj_b;
-  void* act3 = nullptr;          // third activation buffer [max_batch * S][cmax]
-  void* pbuf = nullptr;          // projection outputs [max_batch * S][pmax]
-  // Row width (bytes per voxel) of the data each activation buffer (act[0],
-  // act[1], act3) holds, 0 while it is all zero.  The 3x3x3 kernels read the
-  // zero halo around the interior voxels; a buffer written with one row
-  // width and then with another would show the old interior rows as halo, so
-  // it is zeroed first (prepare_rows).
-  int act_row[3] = {0, 0, 0};
-  size_t act_bytes = 0;          // size of each activation buffer
-  int cmax = 0;
+  int cmax = 0;                  // widest activation row (channels)
+  int pmax = 0;                  // widest projection output (channels; residual networks)
   int n_cu = 256;                // compute units: one persistent conv workgroup each
-  float* partial = nullptr;      // split K loops of small batches: fp32 sums of up to max_units units
-  long long max_units = 0;
 };
 
 // One recorded predecoder_run (predecoder_graph_create).
@@ -406,31 +419,31 @@ void free_all(pd_predecoder* h) {
   auto f = [](void* p) {
     if (p) (void)hipFree(p);
   };
-  f(h->planes);
-  f(h->act[0]);
-  f(h->act[1]);
-  f(h->act3);
-  f(h->pbuf);
+  f(h->ws.planes);
+  f(h->ws.act[0]);
+  f(h->ws.act[1]);
+  f(h->ws.act[2]);
+  f(h->ws.pbuf);
   for (float* p : h->proj_w) f(p);
   for (float* p : h->proj_b) f(p);
-  h->act3 = h->pbuf = nullptr;
+  h->ws.act[2] = h->ws.pbuf = nullptr;
   h->proj_w.clear();
   h->proj_b.clear();
-  f(h->nib);
+  f(h->ws.nib);
   f(h->tables);
   for (void* p : h->wdev) f(p);
   for (float* p : h->bdev) f(p);
   f(h->head_w);
   f(h->head_b);
-  f(h->partial);
-  h->planes = h->act[0] = h->act[1] = nullptr;
-  h->nib = nullptr;
+  f(h->ws.partial);
+  h->ws.planes = h->ws.act[0] = h->ws.act[1] = nullptr;
+  h->ws.nib = nullptr;
   h->tables = nullptr;
   h->wdev.clear();
   h->wslice.clear();
   h->bdev.clear();
   h->head_w = h->head_b = nullptr;
-  h->partial = nullptr;
+  h->ws.partial = nullptr;
 }
 
 // bf16 A fragments (weights) for v_mfma_f32_32x32x16_bf16: lane l of
@@ -516,19 +529,34 @@ pd_status check_launch(hipError_t e) {
   return PD_OK;
 }
 
-// Enqueues the whole path.  ev (optional) receives one event record before
-// each stage and one after the last.  stop_layer >= 0: stop after that
-// hidden layer, whose activations are then written (no head fused into it).
-// Before a layer writes rows of row_bytes into activation buffer idx: zero
-// the buffer if it holds rows of another width (see act_row).
-pd_status prepare_rows(pd_predecoder* h, int idx, int row_bytes, hipStream_t st) {
-  void* bufs[3] = {h->act[0], h->act[1], h->act3};
-  if (h->act_row[idx] != 0 && h->act_row[idx] != row_bytes) {
-    pd_status s = check_launch(pd::launch_zero(bufs[idx], h->act_bytes, st));
+// Before a layer writes rows of row_bytes into activation buffer idx of ws:
+// zero the buffer if it holds rows of another width (see act_row).
+pd_status prepare_rows(Workspace& ws, int idx, int row_bytes, hipStream_t st) {
+  if (ws.act_row[idx] != 0 && ws.act_row[idx] != row_bytes) {
+    pd_status s = check_launch(pd::launch_zero(ws.act[idx], ws.act_bytes, st));
     if (s != PD_OK) return s;
   }
-  h->act_row[idx] = row_bytes;
+  ws.act_row[idx] = row_bytes;
   return PD_OK;
+}
+
+// Where a stopped run left the activations it was asked for (see
+// enqueue_run's stop argument).
+struct StopAt {
+  const void* buf = nullptr;
+  int row_bytes = 0;
+};
+
+// Split of a layer's K loop over 2^k workgroups per tile while tiles x parts
+// stay within the workspace's units (one per compute unit for a handle's
+// own: small batches, where a tile's K loop is the layer's latency); parts
+// must divide the layer's input-channel chunks.  Past one unit per CU the
+// parked fp32 sums cost more than the shorter loops gain.
+pd::Split_k split_for(const Workspace& ws, const Tiling& t, int cin, int fp8) {
+  const int kch = pd::conv_hidden_chunk_channels(fp8);
+  pd::Split_k sk{0, ws.partial, ws.max_units};
+  while ((cin / kch) % (2 << sk.kshift) == 0 && (t.ntiles << (sk.kshift + 1)) <= ws.max_units) ++sk.kshift;
+  return sk;
 }
 
 // The path of a residual network (Model 6, Sec. VI, Fig. Model8Representation):
@@ -537,16 +565,13 @@ pd_status prepare_rows(pd_predecoder* h, int idx, int row_bytes, hipStream_t st)
 // next x with the shortcut added before the activation; the last block's
 // conv2 is the output layer (logits, threshold) with the shortcut added.
 // Three activation buffers rotate so that x, hb and the output differ.
-pd_status enqueue_resnet(pd_predecoder* h, hipStream_t st, const uint64_t* det, int batch, uint64_t* flips,
-                         uint64_t* residual, float* logits, hipEvent_t* ev) {
+// stop >= 0: stop after conv number `stop` of the network (counting, block
+// by block, conv1, the projection if the block has one, then conv2; the last
+// conv2, the output layer, is not counted) and report its output in *at.
+pd_status enqueue_resnet(pd_predecoder* h, Workspace& ws, hipStream_t st, const uint64_t* det, int batch,
+                         uint64_t* flips, uint64_t* residual, float* logits, hipEvent_t* ev, int stop, StopAt* at) {
   const Geom& g = h->g;
   const int hidden_wgs = h->n_cu * pd::conv_hidden_workgroups_per_cu();
-  const int kch = pd::conv_hidden_chunk_channels(0);
-  auto split_for = [&](const Tiling& t, int cin) -> pd::Split_k {
-    pd::Split_k sk{0, h->partial, h->max_units};
-    while ((cin / kch) % (2 << sk.kshift) == 0 && (t.ntiles << (sk.kshift + 1)) <= h->max_units) ++sk.kshift;
-    return sk;
-  };
   int e = 0;
   auto mark = [&]() -> pd_status {
     if (ev && hipEventRecord(ev[e++], st) != hipSuccess) return PD_ERR_DEVICE;
@@ -554,22 +579,28 @@ pd_status enqueue_resnet(pd_predecoder* h, hipStream_t st, const uint64_t* det, 
   };
   pd_status s;
   if ((s = mark()) != PD_OK) return s;
-  if ((s = check_launch(pd::launch_unpack(g, h->tables, det, batch, h->planes, 1, 0, st))) != PD_OK) return s;
+  if ((s = check_launch(pd::launch_unpack(g, h->tables, det, batch, ws.planes, 1, 0, st))) != PD_OK) return s;
   Tiling tl = h->tiling;
   tiling_for_batch(&tl, g, batch);
-  void* bufs[3] = {h->act[0], h->act[1], h->act3};
-  const void* x = h->planes;
-  int xi = -1;  // index of x in bufs (-1: the planes)
+  const void* x = ws.planes;
+  int xi = -1;     // index of x in ws.act (-1: the planes)
+  int conv = 0;    // convs run so far (the numbering of `stop`)
+  auto stopped = [&](const void* buf, int row_bytes) {
+    if (conv++ != stop) return false;
+    at->buf = buf;
+    at->row_bytes = row_bytes;
+    return true;
+  };
   const int nb = (int)h->blocks.size();
   for (int k = 0; k < nb; ++k) {
     if ((s = mark()) != PD_OK) return s;
     const pd_block& B = h->blocks[k];
     const bool last = k == nb - 1;
     const int hi = (xi + 1) % 3, yi = (xi + 2 + (xi < 0 ? 1 : 0)) % 3;
-    void* hb = bufs[hi];
-    void* yb = bufs[yi];
-    if ((s = prepare_rows(h, hi, B.c_mid * 2, st)) != PD_OK) return s;
-    if (!last && (s = prepare_rows(h, yi, B.c_out * 2, st)) != PD_OK) return s;
+    void* hb = ws.act[hi];
+    void* yb = ws.act[yi];
+    if ((s = prepare_rows(ws, hi, B.c_mid * 2, st)) != PD_OK) return s;
+    if (!last && (s = prepare_rows(ws, yi, B.c_out * 2, st)) != PD_OK) return s;
     // conv1: x -> hb
     {
       const int nsl = B.c_mid > 128 ? B.c_mid / 128 : 1, cw = B.c_mid / nsl;
@@ -581,50 +612,60 @@ pd_status enqueue_resnet(pd_predecoder* h, hipStream_t st, const uint64_t* det, 
                                                  batch, 0, st));
         else
           s = check_launch(pd::launch_conv_hidden(g, tl, B.c_in, cw, B.act, x, yq, B.c_mid, wq,
-                                                  h->bdev[2 * k] + q * cw, 0, nullptr, nullptr, h->tables, h->nib,
-                                                  nullptr, batch, hidden_wgs, split_for(tl, B.c_in), 0, nullptr, 0,
-                                                  st));
+                                                  h->bdev[2 * k] + q * cw, 0, nullptr, nullptr, h->tables, ws.nib,
+                                                  nullptr, batch, hidden_wgs, split_for(ws, tl, B.c_in, 0), 0,
+                                                  nullptr, 0, st));
       }
       if (s != PD_OK) return s;
+      if (stopped(hb, B.c_mid * 2)) return PD_OK;
     }
     // shortcut
     const uint16_t* sc = (const uint16_t*)x;
     int sc_stride = B.c_in;
     if (h->proj_w[k]) {
-      s = check_launch(pd::launch_proj(g, x, B.c_in, B.c_in, h->proj_w[k], h->proj_b[k], B.c_out, h->pbuf, B.c_out,
+      s = check_launch(pd::launch_proj(g, x, B.c_in, B.c_in, h->proj_w[k], h->proj_b[k], B.c_out, ws.pbuf, B.c_out,
                                        batch, st));
       if (s != PD_OK) return s;
-      sc = (const uint16_t*)h->pbuf;
+      sc = (const uint16_t*)ws.pbuf;
       sc_stride = B.c_out;
+      if (stopped(ws.pbuf, B.c_out * 2)) return PD_OK;
     }
     // conv2: hb -> the next x (or the logits) with the shortcut added
     if (last) {
       s = check_launch(pd::launch_conv_hidden(g, tl, B.c_mid, 4, 0, hb, nullptr, 0, h->wdev[2 * k + 1],
-                                              h->bdev[2 * k + 1], 2, nullptr, nullptr, h->tables, h->nib, logits,
-                                              batch, hidden_wgs, split_for(tl, B.c_mid), 0, sc, sc_stride, st));
+                                              h->bdev[2 * k + 1], 2, nullptr, nullptr, h->tables, ws.nib, logits,
+                                              batch, hidden_wgs, split_for(ws, tl, B.c_mid, 0), 0, sc, sc_stride, st));
     } else {
       const int nsl = B.c_out > 128 ? B.c_out / 128 : 1, cw = B.c_out / nsl;
       for (int q = 0; q < nsl && s == PD_OK; ++q) {
         const void* wq = (const char*)h->wdev[2 * k + 1] + q * h->wslice[2 * k + 1];
         s = check_launch(pd::launch_conv_hidden(g, tl, B.c_mid, cw, B.act, hb, (uint16_t*)yb + (size_t)q * cw,
                                                 B.c_out, wq, h->bdev[2 * k + 1] + q * cw, 4, nullptr, nullptr,
-                                                h->tables, h->nib, nullptr, batch, hidden_wgs,
-                                                split_for(tl, B.c_mid), 0, sc + (size_t)q * cw, sc_stride, st));
+                                                h->tables, ws.nib, nullptr, batch, hidden_wgs,
+                                                split_for(ws, tl, B.c_mid, 0), 0, sc + (size_t)q * cw, sc_stride, st));
       }
     }
     if (s != PD_OK) return s;
+    if (!last && stopped(yb, B.c_out * 2)) return PD_OK;
     x = yb;
     xi = yi;
   }
+  if (stop >= 0) return PD_ERR_INVALID_ARG;  // no such conv
   if ((s = mark()) != PD_OK) return s;
-  if ((s = check_launch(pd::launch_residual_pack(g, h->tables, det, h->nib, flips, residual, batch, st))) != PD_OK)
+  if ((s = check_launch(pd::launch_residual_pack(g, h->tables, det, ws.nib, flips, residual, batch, st))) != PD_OK)
     return s;
   return mark();
 }
 
-pd_status enqueue_run(pd_predecoder* h, hipStream_t st, const uint64_t* det, int batch, uint64_t* flips,
-                      uint64_t* residual, float* logits, hipEvent_t* ev, int stop_layer = -1) {
-  if (!h->blocks.empty()) return enqueue_resnet(h, st, det, batch, flips, residual, logits, ev);
+// Enqueues the whole path in workspace ws.  ev (optional) receives one event
+// record before each stage and one after the last.  stop >= 0: stop after
+// that hidden layer (residual networks: that conv, see enqueue_resnet), whose
+// output activations are then written (no head fused into it) and reported
+// in *at.
+pd_status enqueue_run(pd_predecoder* h, Workspace& ws, hipStream_t st, const uint64_t* det, int batch,
+                      uint64_t* flips, uint64_t* residual, float* logits, hipEvent_t* ev, int stop = -1,
+                      StopAt* at = nullptr) {
+  if (!h->blocks.empty()) return enqueue_resnet(h, ws, st, det, batch, flips, residual, logits, ev, stop, at);
   const Geom& g = h->g;
   const int fp32 = h->dtype == PD_DTYPE_FP32;
   const int fp8 = h->dtype == PD_DTYPE_FP8;
@@ -634,18 +675,6 @@ pd_status enqueue_run(pd_predecoder* h, hipStream_t st, const uint64_t* det, int
   // epilogue on the MFMA paths) or a 3x3x3 output layer of its own
   const bool out3 = h->layers[n - 1].k == 3;
   const int hidden_wgs = h->n_cu * pd::conv_hidden_workgroups_per_cu();
-  // Split a layer's K loop over 2^k workgroups per tile while tiles x parts
-  // stay within one unit per compute unit (small batches: a tile's K loop is
-  // then the layer's latency); parts must divide the layer's 16-channel
-  // chunks.  Past one unit per CU the parked fp32 sums cost more than the
-  // shorter loops gain.
-  const int kch = pd::conv_hidden_chunk_channels(fp8);
-  auto split_for = [&](const Tiling& t, int cin) -> pd::Split_k {
-    pd::Split_k sk{0, h->partial, h->max_units};
-    while ((cin / kch) % (2 << sk.kshift) == 0 && (t.ntiles << (sk.kshift + 1)) <= h->max_units)
-      ++sk.kshift;
-    return sk;
-  };
   int e = 0;
   auto mark = [&]() -> pd_status {
     if (ev && hipEventRecord(ev[e++], st) != hipSuccess) return PD_ERR_DEVICE;
@@ -653,24 +682,25 @@ pd_status enqueue_run(pd_predecoder* h, hipStream_t st, const uint64_t* det, int
   };
   pd_status s;
   if ((s = mark()) != PD_OK) return s;
-  s = check_launch(pd::launch_unpack(g, h->tables, det, batch, h->planes, 1, fp32, st));
+  s = check_launch(pd::launch_unpack(g, h->tables, det, batch, ws.planes, 1, fp32, st));
   if (s != PD_OK) return s;
-  const void* x = h->planes;
+  const void* x = ws.planes;
   Tiling tl = h->tiling;
   if (!fp32) tiling_for_batch(&tl, g, batch);
   bool head_done = false;  // nibbles written by a fused head
   for (int l = 0; l < n - 1; ++l) {
     if ((s = mark()) != PD_OK) return s;
-    void* y = h->act[l & 1];
+    void* y = ws.act[l & 1];
     const pd_layer& L = h->layers[l];
-    if ((s = prepare_rows(h, l & 1, L.c_out * (fp32 ? 4 : aelem), st)) != PD_OK) return s;
-    const bool fuse_head = !fp32 && !out3 && l == n - 2 && stop_layer < 0;
+    const int row_bytes = L.c_out * (fp32 ? 4 : aelem);
+    if ((s = prepare_rows(ws, l & 1, row_bytes, st)) != PD_OK) return s;
+    const bool fuse_head = !fp32 && !out3 && l == n - 2 && stop < 0;
     if (fp32) {
       s = check_launch(pd::launch_conv_fp32(g, L.c_in, L.c_out, L.act, (const float*)x, (float*)y,
                                             (const float*)h->wdev[l], h->bdev[l], batch, st));
     } else if (l == 0 && fuse_head && L.c_in == 2) {  // one hidden layer: layer 1 carries the head
       s = check_launch(pd::launch_conv_single(g, tl, L.c_out, L.act, x, h->wdev[l], h->bdev[l], h->head_w,
-                                              h->head_b, h->tables, h->nib, logits, batch, h->n_cu, st));
+                                              h->head_b, h->tables, ws.nib, logits, batch, h->n_cu, st));
       head_done = true;
     } else {
       // a 256-wide layer runs as two slices of 128 output channels over the
@@ -686,30 +716,45 @@ pd_status enqueue_run(pd_predecoder* h, hipStream_t st, const uint64_t* det, int
         else  // the last hidden layer may carry the head and the threshold in its epilogue
           s = check_launch(pd::launch_conv_hidden(g, tl, L.c_in, cw, L.act, x, yk, L.c_out, wk,
                                                   h->bdev[l] + k * cw * (fp8 ? 2 : 1), fuse_head ? 1 : 0,
-                                                  h->head_w, h->head_b, h->tables, h->nib, logits, batch,
-                                                  hidden_wgs, split_for(tl, L.c_in), fp8, nullptr, 0, st));
+                                                  h->head_w, h->head_b, h->tables, ws.nib, logits, batch,
+                                                  hidden_wgs, split_for(ws, tl, L.c_in, fp8), fp8, nullptr, 0, st));
       }
       head_done = fuse_head && l > 0;
     }
     if (s != PD_OK) return s;
-    if (l == stop_layer) return PD_OK;
+    if (l == stop) {
+      at->buf = y;
+      at->row_bytes = row_bytes;
+      return PD_OK;
+    }
     x = y;
   }
+  if (stop >= 0) return PD_ERR_INVALID_ARG;  // no such hidden layer
   if ((s = mark()) != PD_OK) return s;
   if (out3) {
     const pd_layer& L = h->layers[n - 1];
     s = check_launch(pd::launch_conv_hidden(g, tl, L.c_in, L.c_out, L.act, x, nullptr, 0, h->wdev[n - 1],
-                                            h->bdev[n - 1], 2, nullptr, nullptr, h->tables, h->nib, logits,
-                                            batch, hidden_wgs, split_for(tl, L.c_in), fp8, nullptr, 0, st));
+                                            h->bdev[n - 1], 2, nullptr, nullptr, h->tables, ws.nib, logits,
+                                            batch, hidden_wgs, split_for(ws, tl, L.c_in, fp8), fp8, nullptr, 0, st));
   } else if (!head_done) {  // fp32, or a one-hidden-layer network on the paper's layout
     s = check_launch(pd::launch_head(g, h->layers[n - 1].c_in, fp32, x, h->head_w, h->head_b, h->tables,
-                                     h->nib, logits, batch, st));
+                                     ws.nib, logits, batch, st));
   }
   if (s != PD_OK) return s;
   if ((s = mark()) != PD_OK) return s;
-  s = check_launch(pd::launch_residual_pack(g, h->tables, det, h->nib, flips, residual, batch, st));
+  s = check_launch(pd::launch_residual_pack(g, h->tables, det, ws.nib, flips, residual, batch, st));
   if (s != PD_OK) return s;
   return mark();
+}
+
+// Number of convs predecoder_activations can stop after: the hidden layers,
+// or for a residual network every conv but the output layer (conv1, the
+// projection if any, conv2 per block).
+int n_stop_points(const pd_predecoder* h) {
+  if (h->blocks.empty()) return (int)h->layers.size() - 1;
+  int n = 0;
+  for (const pd_block& B : h->blocks) n += 2 + (B.c_in != B.c_out ? 1 : 0);
+  return n - 1;
 }
 
 }  // namespace
@@ -826,23 +871,23 @@ pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d
     return st;
   };
   const size_t cin0 = (size_t)layers[0].c_in;
-  if ((s = dev_alloc(&h->planes, vox * cin0 * elem)) != PD_OK) return fail(s);
-  h->act_bytes = vox * cmax * aelem;
-  if ((s = dev_alloc(&h->act[0], vox * cmax * aelem)) != PD_OK) return fail(s);
-  if ((s = dev_alloc(&h->act[1], vox * cmax * aelem)) != PD_OK) return fail(s);
-  if ((s = dev_alloc(&h->nib, (size_t)max_batch * g.V)) != PD_OK) return fail(s);
+  if ((s = dev_alloc(&h->ws.planes, vox * cin0 * elem)) != PD_OK) return fail(s);
+  h->ws.act_bytes = vox * cmax * aelem;
+  if ((s = dev_alloc(&h->ws.act[0], vox * cmax * aelem)) != PD_OK) return fail(s);
+  if ((s = dev_alloc(&h->ws.act[1], vox * cmax * aelem)) != PD_OK) return fail(s);
+  if ((s = dev_alloc(&h->ws.nib, (size_t)max_batch * g.V)) != PD_OK) return fail(s);
   if (dtype != PD_DTYPE_FP32) {
     // parked fp32 sums of split K loops: room for one unit per compute unit
-    h->max_units = h->n_cu;
-    if ((s = dev_alloc(&h->partial, (size_t)h->max_units * pd::conv_hidden_partial_floats_per_unit() * 4)) !=
+    h->ws.max_units = h->n_cu;
+    if ((s = dev_alloc(&h->ws.partial, (size_t)h->ws.max_units * pd::conv_hidden_partial_floats_per_unit() * 4)) !=
         PD_OK)
       return fail(s);
   }
   std::vector<int32_t> tab = build_tables(g);
   if ((s = upload(&h->tables, tab.data(), tab.size() * sizeof(int32_t))) != PD_OK) return fail(s);
-  if (hipMemset(h->planes, 0, vox * cin0 * elem) != hipSuccess ||
-      hipMemset(h->act[0], 0, vox * cmax * aelem) != hipSuccess ||
-      hipMemset(h->act[1], 0, vox * cmax * aelem) != hipSuccess)
+  if (hipMemset(h->ws.planes, 0, vox * cin0 * elem) != hipSuccess ||
+      hipMemset(h->ws.act[0], 0, vox * cmax * aelem) != hipSuccess ||
+      hipMemset(h->ws.act[1], 0, vox * cmax * aelem) != hipSuccess)
     return fail(PD_ERR_DEVICE);
 
   const float* src = weights;
@@ -1031,6 +1076,7 @@ pd_status predecoder_create_resnet(const float* weights, size_t n_weights, int32
     if (blocks[k].c_in != blocks[k].c_out) pmax = std::max(pmax, (int)blocks[k].c_out);
   }
   h->cmax = cmax;
+  h->pmax = pmax;
   pd_status s = PD_OK;
   auto fail = [&](pd_status st) {
     free_all(h);
@@ -1039,21 +1085,21 @@ pd_status predecoder_create_resnet(const float* weights, size_t n_weights, int32
   };
   const size_t vox = (size_t)max_batch * (size_t)g.S;
   const size_t cin0 = (size_t)blocks[0].c_in;
-  if ((s = dev_alloc(&h->planes, vox * cin0 * 2)) != PD_OK) return fail(s);
-  h->act_bytes = vox * cmax * 2;
-  if ((s = dev_alloc(&h->act[0], vox * cmax * 2)) != PD_OK) return fail(s);
-  if ((s = dev_alloc(&h->act[1], vox * cmax * 2)) != PD_OK) return fail(s);
-  if ((s = dev_alloc(&h->act3, vox * cmax * 2)) != PD_OK) return fail(s);
-  if ((s = dev_alloc(&h->pbuf, vox * pmax * 2)) != PD_OK) return fail(s);
-  if ((s = dev_alloc(&h->nib, (size_t)max_batch * g.V)) != PD_OK) return fail(s);
-  h->max_units = h->n_cu;
-  if ((s = dev_alloc(&h->partial, (size_t)h->max_units * pd::conv_hidden_partial_floats_per_unit() * 4)) != PD_OK)
+  if ((s = dev_alloc(&h->ws.planes, vox * cin0 * 2)) != PD_OK) return fail(s);
+  h->ws.act_bytes = vox * cmax * 2;
+  if ((s = dev_alloc(&h->ws.act[0], vox * cmax * 2)) != PD_OK) return fail(s);
+  if ((s = dev_alloc(&h->ws.act[1], vox * cmax * 2)) != PD_OK) return fail(s);
+  if ((s = dev_alloc(&h->ws.act[2], vox * cmax * 2)) != PD_OK) return fail(s);
+  if ((s = dev_alloc(&h->ws.pbuf, vox * pmax * 2)) != PD_OK) return fail(s);
+  if ((s = dev_alloc(&h->ws.nib, (size_t)max_batch * g.V)) != PD_OK) return fail(s);
+  h->ws.max_units = h->n_cu;
+  if ((s = dev_alloc(&h->ws.partial, (size_t)h->ws.max_units * pd::conv_hidden_partial_floats_per_unit() * 4)) != PD_OK)
     return fail(s);
   std::vector<int32_t> tab = build_tables(g);
   if ((s = upload(&h->tables, tab.data(), tab.size() * sizeof(int32_t))) != PD_OK) return fail(s);
-  if (hipMemset(h->planes, 0, vox * cin0 * 2) != hipSuccess || hipMemset(h->act[0], 0, vox * cmax * 2) != hipSuccess ||
-      hipMemset(h->act[1], 0, vox * cmax * 2) != hipSuccess || hipMemset(h->act3, 0, vox * cmax * 2) != hipSuccess ||
-      hipMemset(h->pbuf, 0, vox * pmax * 2) != hipSuccess)
+  if (hipMemset(h->ws.planes, 0, vox * cin0 * 2) != hipSuccess || hipMemset(h->ws.act[0], 0, vox * cmax * 2) != hipSuccess ||
+      hipMemset(h->ws.act[1], 0, vox * cmax * 2) != hipSuccess || hipMemset(h->ws.act[2], 0, vox * cmax * 2) != hipSuccess ||
+      hipMemset(h->ws.pbuf, 0, vox * pmax * 2) != hipSuccess)
     return fail(PD_ERR_DEVICE);
   // weights: per conv, BatchNorm folded in (g = scale / sqrt(var + 1e-5) in
   // fp64; weights fp32(w g), rounded to bf16 by the fragment builder; bias
@@ -1110,8 +1156,9 @@ pd_status predecoder_run(pd_predecoder* h, void* hip_stream, const uint64_t* det
                          uint64_t* flips, uint64_t* residual, float* logits) {
   if (!h || !det || !flips || !residual) return PD_ERR_INVALID_ARG;
   if (batch < 1 || batch > h->max_batch) return PD_ERR_INVALID_ARG;
-  return enqueue_run(h, (hipStream_t)hip_stream, det, batch, flips, residual, logits, nullptr);
+  return enqueue_run(h, h->ws, (hipStream_t)hip_stream, det, batch, flips, residual, logits, nullptr);
 }
+
 
 pd_status predecoder_residual(pd_predecoder* h, void* hip_stream, const uint64_t* det,
                               const uint64_t* flips, int32_t batch, uint64_t* residual) {
@@ -1125,14 +1172,13 @@ pd_status predecoder_activations(pd_predecoder* h, void* hip_stream, const uint6
                                  int32_t layer, void* out) {
   if (!h || !det || !out) return PD_ERR_INVALID_ARG;
   if (batch < 1 || batch > h->max_batch) return PD_ERR_INVALID_ARG;
-  if (!h->blocks.empty()) return PD_ERR_UNSUPPORTED;
-  if (layer < 0 || layer >= (int)h->layers.size() - 1) return PD_ERR_INVALID_ARG;
+  if (layer < 0 || layer >= n_stop_points(h)) return PD_ERR_INVALID_ARG;
   if (h->dtype == PD_DTYPE_FP32) return PD_ERR_UNSUPPORTED;
   const hipStream_t st = (hipStream_t)hip_stream;
-  pd_status s = enqueue_run(h, st, det, batch, nullptr, nullptr, nullptr, nullptr, layer);
+  StopAt at;
+  pd_status s = enqueue_run(h, h->ws, st, det, batch, nullptr, nullptr, nullptr, nullptr, layer, &at);
   if (s != PD_OK) return s;
-  const int bytes = h->layers[layer].c_out * (h->dtype == PD_DTYPE_FP8 ? 1 : 2);
-  return check_launch(pd::launch_extract(h->g, h->act[layer & 1], bytes, batch, out, st));
+  return check_launch(pd::launch_extract(h->g, at.buf, at.row_bytes, batch, out, st));
 }
 
 pd_status predecoder_unpack(pd_predecoder* h, void* hip_stream, const uint64_t* det, int32_t batch,
@@ -1158,7 +1204,7 @@ pd_status predecoder_stage_times(pd_predecoder* h, void* hip_stream, const uint6
     }
   hipStream_t st = (hipStream_t)hip_stream;
   for (int it = 0; it < n_iter && s == PD_OK; ++it)
-    s = enqueue_run(h, st, det, batch, flips, residual, nullptr, ev.data() + (size_t)it * ne);
+    s = enqueue_run(h, h->ws, st, det, batch, flips, residual, nullptr, ev.data() + (size_t)it * ne);
   if (s == PD_OK && hipStreamSynchronize(st) != hipSuccess) s = PD_ERR_DEVICE;
   if (s == PD_OK) {
     for (int k = 0; k < ns; ++k) ms_per_stage[k] = 0.0f;
@@ -1207,11 +1253,11 @@ pd_status predecoder_graph_create(pd_predecoder* h, const uint64_t* det, int32_t
   // one run first: the handle's buffers reach the state every later run
   // starts from, so the recorded sequence (with any buffer clearing it
   // needs) is the one each replay repeats
-  pd_status s = enqueue_run(h, gr->stream, det, batch, flips, residual, logits, nullptr);
+  pd_status s = enqueue_run(h, h->ws, gr->stream, det, batch, flips, residual, logits, nullptr);
   if (s != PD_OK) return fail(s);
   if (hipStreamSynchronize(gr->stream) != hipSuccess) return fail(PD_ERR_DEVICE);
   if (hipStreamBeginCapture(gr->stream, hipStreamCaptureModeThreadLocal) != hipSuccess) return fail(PD_ERR_DEVICE);
-  s = enqueue_run(h, gr->stream, det, batch, flips, residual, logits, nullptr);
+  s = enqueue_run(h, h->ws, gr->stream, det, batch, flips, residual, logits, nullptr);
   hipGraph_t graph = nullptr;
   const hipError_t ec = hipStreamEndCapture(gr->stream, &graph);
   gr->graph = graph;

@@ -177,7 +177,7 @@ int conv_hidden_chunk_channels(int fp8);  // input channels per K-loop chunk
 size_t conv_hidden_partial_floats_per_unit();
 int conv_hidden_workgroups_per_cu();
 
-// Copies the interior voxel rows (row_bytes each, a multiple of 16) of a
+// Copies the interior voxel rows (row_bytes each, a multiple of 8) of a
 // zero-halo activation buffer to out [batch][T][H][H] rows.
 hipError_t launch_extract(const Geom& g, const void* act, int row_bytes, int batch, void* out, hipStream_t stream);
 

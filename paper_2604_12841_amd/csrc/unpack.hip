@@ -142,10 +142,11 @@ hipError_t launch_unpack(const Geom& g, const int32_t* tables, const uint64_t* d
 
 namespace pd {
 
-// One thread per 16-byte granule of an interior voxel row: out[(b, t, i, j)]
-// <- act[padded (b, t, i, j)].
-__global__ void __launch_bounds__(256) extract_kernel(Geom g, const uint4* __restrict__ act, int gran, int batch,
-                                                      uint4* __restrict__ out) {
+// One thread per granule (16 or 8 bytes) of an interior voxel row:
+// out[(b, t, i, j)] <- act[padded (b, t, i, j)].
+template <typename G>
+__global__ void __launch_bounds__(256) extract_kernel(Geom g, const G* __restrict__ act, int gran, int batch,
+                                                      G* __restrict__ out) {
   const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   const long long total = (long long)batch * g.V * gran;
   if (gid >= total) return;
@@ -160,11 +161,18 @@ __global__ void __launch_bounds__(256) extract_kernel(Geom g, const uint4* __res
 }
 
 hipError_t launch_extract(const Geom& g, const void* act, int row_bytes, int batch, void* out, hipStream_t stream) {
-  if (row_bytes <= 0 || row_bytes % 16 != 0) return hipErrorInvalidValue;
-  const int gran = row_bytes / 16;
-  const long long total = (long long)batch * g.V * gran;
-  hipLaunchKernelGGL(extract_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream, g,
-                     (const uint4*)act, gran, batch, (uint4*)out);
+  if (row_bytes <= 0 || row_bytes % 8 != 0) return hipErrorInvalidValue;
+  if (row_bytes % 16 == 0) {
+    const int gran = row_bytes / 16;
+    const long long total = (long long)batch * g.V * gran;
+    hipLaunchKernelGGL(extract_kernel<uint4>, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream, g,
+                       (const uint4*)act, gran, batch, (uint4*)out);
+  } else {  // rows of four bf16 channels (a projection to the 4 output channels)
+    const int gran = row_bytes / 8;
+    const long long total = (long long)batch * g.V * gran;
+    hipLaunchKernelGGL(extract_kernel<uint2>, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream, g,
+                       (const uint2*)act, gran, batch, (uint2*)out);
+  }
   return hipGetLastError();
 }
 

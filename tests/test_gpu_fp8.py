@@ -14,6 +14,7 @@ import oracle
 import paper_2604_12841_amd as pdx
 from fp8_cases import FP8_CASES, case_inputs
 from paper_2604_12841_amd import workload
+import tight
 from parity import _padding_zero, assert_parity, compare, config_case, run_gpu, say
 
 torch = pytest.importorskip("torch")
@@ -82,22 +83,19 @@ def test_fp8_deterministic(cuda):
 # predecoder_activations gives each hidden layer's E4M3 output.  Layer by
 # layer, the test recomputes the layer in fp64 from the GPU's own input (the
 # planes for layer 1, else the previous layer's GPU codes) with the oracle's
-# quantisation points (E4M3 through PyTorch's float8_e4m3fn, pinned equal to
-# the oracle's codes): every output code must equal the expected one, except
-# where the GPU's summation error (up to EPS_MM x sum|products|: the matrix
-# instruction's own rounding, about 2^-16.4 of it on gfx950, plus fp32
-# additions) or its activation arithmetic (REL_ACT) can move the value
-# across an E4M3 rounding boundary; there the code must be one of the
-# codes reachable within those bounds.  The logits are then checked from
-# the GPU's last hidden codes to the bound of their own sums, with nothing
-# excused.
+# quantisation points, under the rule of tight.py: every output code must
+# equal the expected one, except where the GPU's summation error (EPS_MM x
+# sum|products| for the fp8 instruction, EPS_32 for layer 1's bf16 one) or
+# its activation arithmetic can move the value across an E4M3 rounding
+# boundary; there the code must be one of the codes reachable within those
+# bounds.  The logits are then checked from the GPU's last hidden codes to
+# the bound of their own sums, with nothing excused.
 EPS_MM = 2.0 ** -16 + 2.0 ** -18
 EPS_32 = 2.0 ** -17
-REL_ACT = 2.0 ** -20
 
 
 def _q8(t):
-    return t.float().clamp(-448.0, 448.0).to(torch.float8_e4m3fn).double()
+    return tight.q_e4m3(t)
 
 
 def _layer_weights(weights, layers):
@@ -114,51 +112,47 @@ def _layer_weights(weights, layers):
     return out
 
 
-def _act(v, act):
-    F = torch.nn.functional
-    v = v.float().double()
-    if act == workload.GELU_TANH:
-        v = F.gelu(v, approximate="tanh")
-    elif act == workload.RELU:
-        v = F.relu(v)
-    return v.float().double()
-
-
-def _expected_codes(y, eps_abs, act):
-    """E4M3 activations of pre-activations y, and the values reachable when y
-    moves by up to eps_abs and the activation by up to REL_ACT (sampled at
-    the ends and the middle of the window, both directions of REL_ACT)."""
-    cands = [_q8(_act(y, act))]
-    for dy in (-1.0, -0.5, 0.5, 1.0):
-        for r in (1 - REL_ACT, 1 + REL_ACT):
-            cands.append(_q8(_act(y + dy * eps_abs, act) * r))
-    amb = torch.zeros_like(y, dtype=torch.bool)
-    for c in cands[1:]:
-        amb |= c != cands[0]
-    if act == workload.GELU_TANH:  # not monotonic around its minimum (y ~ -0.75)
-        amb |= (y - eps_abs < -0.7517) & (y + eps_abs > -0.7517)
-    return cands, amb
-
-
-def _gpu_codes(pre, det, layer, c_out):
+def _gpu_codes(pre, det, layer, c_out, rows=None):
+    """E4M3 outputs of hidden layer `layer` for the whole batch of det, as
+    fp64 [B'][c_out][T][H][H] (B' = the samples in rows, default all)."""
     B, T, H = det.shape[0], pre.T, pre.grid
     out = torch.empty((B, T, H, H, c_out), dtype=torch.uint8, device="cuda")
     pre.activations(torch.from_numpy(np.ascontiguousarray(det).view(np.int64)).cuda(), layer, out)
     torch.cuda.synchronize()
+    if rows is not None:
+        out = out[torch.as_tensor(rows, device="cuda")]
     return out.cpu().view(torch.float8_e4m3fn).double().permute(0, 4, 1, 2, 3).contiguous()
 
 
 def _check_layer(name, got, y, eps_abs, act):
-    cands, amb = _expected_codes(y, eps_abs, act)
-    exact_bad = int(((got != cands[0]) & ~amb).sum())
-    in_window = torch.zeros_like(amb)
-    for c in cands:
-        in_window |= got == c
-    window_bad = int((~in_window & amb).sum())
-    say("  %s: codes %d, ambiguous %d (%.4f), differing there %d, mismatches %d + %d" %
-        (name, got.numel(), int(amb.sum()), float(amb.float().mean()), int(((got != cands[0]) & amb).sum()),
-         exact_bad, window_bad))
-    assert exact_bad == 0 and window_bad == 0
+    tight.check_stored(name, got, y, eps_abs, act, tight.q_e4m3, say=say)
+
+
+def _tight_network(pre, det, layers, weights, layout, first, last, rows=None):
+    """Every hidden layer's codes, then the logits (of the samples in rows)."""
+    d, T = pre.d, pre.T
+    sel = det if rows is None else det[rows]
+    wq = _layer_weights(weights, layers)
+    x = torch.from_numpy(oracle.unpack_paper(d, T, sel, first, last) if layout == "paper"
+                         else oracle.unpack(d, T, sel))
+    for l in range(len(layers) - 1):
+        ci, co, k, act = layers[l]
+        w, b = wq[l]
+        y = tight.conv(x, w, b)
+        eps = (EPS_32 if l == 0 else EPS_MM) * tight.conv_mag(x, w)
+        got = _gpu_codes(pre, det, l, co, rows)
+        _check_layer("layer %d" % (l + 1), got, y, eps, act)
+        x = got
+    _, _, logits = run_gpu(pre, det)
+    if rows is not None:
+        logits = logits[rows]
+    w, b = wq[-1]
+    k = layers[-1][2]
+    ref = tight.conv(x, w, b, k)
+    bound = (EPS_MM if k == 3 else EPS_32) * tight.conv_mag(x, w, k=k) + 2.0 ** -22 * ref.abs() + 1e-6
+    err = (torch.from_numpy(logits.astype(np.float64)) - ref).abs()
+    say("  logits: max err %.3g, max err / bound %.3f" % (float(err.max()), float((err / bound).max())))
+    assert bool((err <= bound).all())
 
 
 TIGHT = [
@@ -183,25 +177,17 @@ def test_fp8_layers_tight(cuda, net, batch):
     first = last = "Z" if layout == "paper" else None
     say("fp8 tight:", net["name"], "batch", batch)
     pre = pdx.Predecoder(weights, d, T, layers, "fp8", max_batch=batch, layout=layout, first=first, last=last)
-    F = torch.nn.functional
-    wq = _layer_weights(weights, layers)
-    x = torch.from_numpy(oracle.unpack_paper(d, T, det, first, last) if layout == "paper"
-                         else oracle.unpack(d, T, det))
-    for l in range(len(layers) - 1):
-        ci, co, k, act = layers[l]
-        w, b = wq[l]
-        y = F.conv3d(x, w, b, padding=1)
-        eps = (EPS_32 if l == 0 else EPS_MM) * F.conv3d(x.abs(), w.abs(), padding=1)
-        got = _gpu_codes(pre, det, l, co)
-        _check_layer("layer %d" % (l + 1), got, y, eps, act)
-        x = got
-    _, _, logits = run_gpu(pre, det)
+    _tight_network(pre, det, layers, weights, layout, first, last)
     pre.close()
-    w, b = wq[-1]
-    k = layers[-1][2]
-    ref = F.conv3d(x, w, b, padding=(k - 1) // 2)
-    bound = (EPS_MM if k == 3 else EPS_32) * F.conv3d(x.abs(), w.abs(), padding=(k - 1) // 2) \
-        + 2.0 ** -22 * ref.abs() + 1e-6
-    err = (torch.from_numpy(logits.astype(np.float64)) - ref).abs()
-    say("  logits: max err %.3g, max err / bound %.3f" % (float(err.max()), float((err / bound).max())))
-    assert bool((err <= bound).all())
+
+
+def test_fp8_layers_tight_full_size(cuda):
+    """Workload 3's network (8 x 128, d = 13, T = 13) in fp8 at its full
+    batch of 4096, the launch configuration the benchmark times: every
+    layer's codes and the logits of three samples (first, middle, last)."""
+    d, T, _, layers, weights, det, _ = config_case(3)
+    rows = [0, 2048, det.shape[0] - 1]
+    say("fp8 tight full size: d", d, "T", T, "B", det.shape[0], "samples", rows)
+    pre = pdx.Predecoder(weights, d, T, layers, "fp8", max_batch=det.shape[0])
+    _tight_network(pre, det, layers, weights, "plaquette", None, None, rows)
+    pre.close()

@@ -3,17 +3,21 @@ Model8Representation) against the oracle's residual forward in bf16 mode,
 through the C ABI: Model 6 itself on small volumes, projections in a middle
 block (widening and narrowing, which also reuse activation buffers at other
 row widths), 256-wide slices, ReLU and linear blocks, both layouts, batch 1
-(split K loops) and larger batches.  Logits within the bound that
-tests/golden/make_resnet_tolerance.py derives from the oracle alone; flips
-and residual bits exact outside the sites that bound excuses."""
+(split K loops) and larger batches.  End to end: logits within the bound
+that tests/golden/make_resnet_tolerance.py derives from the oracle alone;
+flips and residual bits exact outside the sites that bound excuses.  Per
+conv: every stored bf16 activation exact outside the fp32-summation window
+of tight.py, and the logits within their own sums' bound."""
 import json
 import os
 
+import numpy as np
 import pytest
 
 import oracle
 import paper_2604_12841_amd as pdx
-from parity import assert_parity, compare, run_gpu, say
+import tight
+from parity import assert_flips_follow_logits, assert_parity, compare, run_gpu, say
 from resnet_cases import RESNET_CASES, case_inputs
 
 torch = pytest.importorskip("torch")
@@ -47,3 +51,107 @@ def test_resnet_parity(cuda, case):
     say("  stats", st)
     assert_parity(st, "bf16", tol=TOL)
     assert (flips == f2).all() and (res == r2).all() and (logits == l2).all()
+
+
+# ---- per-conv tight checks ---------------------------------------------
+#
+# predecoder_activations of a residual network stops after any conv but the
+# output layer (per block: conv1, the projection if the block has one,
+# conv2) and returns what that conv stored (bf16).  Each conv is recomputed
+# in fp64 from the GPU's own inputs -- the folded weights and biases as the
+# library uses them (BatchNorm folded in fp64, weights rounded to bf16,
+# biases to fp32), the shortcut the GPU stored -- under the rule of tight.py.
+# The logits are then checked against the fp64 output conv of the GPU's last
+# block input and intermediate, within the bound of their own fp32 sums, and
+# the flips and residual against the threshold of the GPU's own logits;
+# nothing is excused anywhere.
+
+def _folded(weights, blocks):
+    """Per block: (w1, b1, w2, b2, wp, bp) as fp64 tensors, BatchNorm folded
+    (g = scale / sqrt(var + 1e-5) in fp64, w bf16(fp32(w g)), b fp32((b -
+    mean) g + shift)); wp, bp the projection (bf16 weights, fp32 bias) or
+    None."""
+    out, off = [], 0
+
+    def take(n):
+        nonlocal off
+        a = weights[off:off + n].astype(np.float64)
+        off += n
+        return a
+
+    for ci, cm, co, _act in blocks:
+        convs = []
+        for cin, cout in ((ci, cm), (cm, co)):
+            w = take(cout * cin * 27).reshape(cout, cin, 3, 3, 3)
+            b = take(cout)
+            scale, shift, mean, var = (take(cout) for _ in range(4))
+            g = scale / np.sqrt(var + 1e-5)
+            wf = tight.q_bf16(torch.from_numpy((w * g.reshape(-1, 1, 1, 1, 1)).astype(np.float32).astype(np.float64)))
+            bf = torch.from_numpy(((b - mean) * g + shift).astype(np.float32).astype(np.float64))
+            convs += [wf, bf]
+        wp = bp = None
+        if ci != co:
+            wp = tight.q_bf16(torch.from_numpy(take(co * ci).reshape(co, ci, 1, 1, 1)))
+            bp = torch.from_numpy(take(co).astype(np.float32).astype(np.float64))
+        out.append(tuple(convs) + (wp, bp))
+    assert off == weights.size
+    return out
+
+
+def _stored(pre, ddet, conv, c_out):
+    B, T, H = ddet.shape[0], pre.T, pre.grid
+    out = torch.empty((B, T, H, H, c_out), dtype=torch.int16, device="cuda")
+    pre.activations(ddet, conv, out)
+    torch.cuda.synchronize()
+    return tight.bf16_bits_to_double(out.cpu()).permute(0, 4, 1, 2, 3).contiguous()
+
+
+@pytest.mark.parametrize("case", RESNET_CASES, ids=[c["name"] for c in RESNET_CASES])
+def test_resnet_convs_tight(cuda, case):
+    blocks, d, T, B, layout = case["blocks"], case["d"], case["T"], case["B"], case["layout"]
+    weights, det, first, last = case_inputs(case)
+    say("resnet tight", case["name"], "blocks", blocks, "d", d, "T", T, "B", B)
+    pre = pdx.Predecoder(weights, d, T, None, "bf16", max_batch=B, layout=layout, first=first, last=last,
+                         blocks=blocks)
+    ddet = torch.from_numpy(det.view(np.int64)).cuda()
+    x = torch.from_numpy(oracle.unpack_paper(d, T, det, first, last) if layout == "paper"
+                         else oracle.unpack(d, T, det))
+    conv = 0
+    for k, ((ci, cm, co, act), (w1, b1, w2, b2, wp, bp)) in enumerate(zip(blocks, _folded(weights, blocks))):
+        # conv1: bf16 instructions over 27 c_in products, + bias, activation
+        y = tight.conv(x, w1, b1)
+        eps = tight.eps_bf16_mfma(27 * ci) * tight.conv_mag(x, w1, b1) + tight.U32 * y.abs()
+        h = _stored(pre, ddet, conv, cm)
+        tight.check_stored("block %d conv1" % (k + 1), h, y, eps, act, tight.q_bf16, say=say)
+        conv += 1
+        # shortcut: the block input, or its 1x1x1 projection (an fp32 FMA chain)
+        if wp is not None:
+            s_exact = tight.conv(x, wp, bp, k=1)
+            eps = tight.eps_fma_chain(ci) * tight.conv_mag(x, wp, bp, k=1) + tight.U32 * s_exact.abs()
+            s = _stored(pre, ddet, conv, co)
+            tight.check_stored("block %d projection" % (k + 1), s, s_exact, eps, tight.NONE, tight.q_bf16, say=say)
+            conv += 1
+        else:
+            s = x
+        # conv2 + shortcut: (sum + bias) + shortcut in fp32, then the activation
+        y = tight.conv(h, w2, b2) + s
+        eps = tight.eps_bf16_mfma(27 * cm) * tight.conv_mag(h, w2, b2) + 2 * tight.U32 * (y.abs() + s.abs())
+        if k < len(blocks) - 1:
+            x = _stored(pre, ddet, conv, co)
+            tight.check_stored("block %d conv2" % (k + 1), x, y, eps, act, tight.q_bf16, say=say)
+            conv += 1
+    # the output layer: logits of a full run against the GPU's own last inputs
+    flips, res, logits = run_gpu(pre, det)
+    # the library has no conv after the last one to stop at (past the
+    # binding's own range check, through the C ABI)
+    import ctypes
+    out = torch.empty((B, T, pre.grid, pre.grid, 8), dtype=torch.int16, device="cuda")
+    st = pdx.lib().predecoder_activations(pre._h, ctypes.c_void_p(torch.cuda.current_stream().cuda_stream),
+                                          ctypes.c_void_p(ddet.data_ptr()), B, conv, ctypes.c_void_p(out.data_ptr()))
+    assert st == pdx.PD_ERR_INVALID_ARG
+    pre.close()
+    err = (torch.from_numpy(logits.astype(np.float64)) - y).abs()
+    bound = eps + 1e-6
+    say("  logits: max err %.3g, max err / bound %.3f" % (float(err.max()), float((err / bound).max())))
+    assert bool((err <= bound).all())
+    assert_flips_follow_logits(d, T, det, logits, flips, res, layout)
