@@ -1,0 +1,86 @@
+"""GPU parity at the shapes the committed timing profiles measure: Models 1,
+2, 4 and 5 of Table models in the paper's layout at 13^3, 21^3 and 31^3
+(batch 1, where the K loops are split, and batch 64), in bf16 and, for
+Models 1, 4 and 5, in fp8; Model 6 at 13^3 and 21^3 (batch 1 and 16).  Each
+run is the launch configuration the benchmark times (one handle, the whole
+batch); sampled samples (first and last) are compared with the oracle under
+the parity rule of parity.py, every sample's residual with the oracle's
+residual of the GPU's flips, and every sample's flips and residual with the
+threshold of the GPU's own logits."""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2604_12841_amd as pdx
+from parity import TOL, assert_flips_follow_logits, assert_parity, compare, run_gpu, say
+from paper_2604_12841_amd import workload
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+RESNET_TOL = json.load(open(os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                                         "resnet_tolerance.json")))["tol_max_abs_logit_err"]
+
+
+@pytest.fixture(scope="module")
+def cuda():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch.device("cuda")
+
+
+def _inputs(d, B):
+    # the benchmark's paper-model inputs: p = q = 0.003, noise seed 5000 + d
+    det, _ = workload.make_inputs(d, d, B, 0.003, 0.003, 5000 + d)
+    return det
+
+
+def _check(d, T, dtype, det, rows, flips, res, logits, ref, tol):
+    B = det.shape[0]
+    st = compare(d, T, dtype, *ref, flips[rows], res[rows], logits[rows], layout="paper", tol=tol)
+    say("  samples", rows, "of", B, st)
+    assert_parity(st, dtype, tol=tol)
+    np.testing.assert_array_equal(res, oracle.residual_from_flips(d, T, det, flips))
+    assert_flips_follow_logits(d, T, det, logits, flips, res, layout="paper")
+
+
+CASES = [(m, d, b, dt) for dt in ("bf16", "fp8") for m in (1, 2, 4, 5) for d in (13, 21, 31) for b in (1, 64)
+         if dt == "bf16" or (m != 2 and d == 31)]
+
+
+@pytest.mark.parametrize("model,d,batch,dtype", CASES, ids=["m%d_d%d_b%d_%s" % c for c in CASES])
+def test_paper_model_at_timed_shape(cuda, model, d, batch, dtype):
+    T = d
+    layers = workload.paper_model_layers(model)
+    weights = workload.he_normal_weights(layers, 4000 + model)  # the benchmark's weights
+    det = _inputs(d, batch)
+    rows = [0] if batch == 1 else [0, batch - 1]
+    say("Model", model, "d = T =", d, "batch", batch, dtype)
+    pre = pdx.Predecoder(weights, d, T, layers, dtype, max_batch=batch, layout="paper", first="Z", last="Z")
+    flips, res, logits = run_gpu(pre, det)
+    pre.close()
+    ref = oracle.run(d, T, det[rows], layers, weights, bf16=dtype == "bf16", layout="paper", first="Z", last="Z",
+                     fp8=dtype == "fp8")
+    _check(d, T, dtype, det, rows, flips, res, logits, ref, TOL[dtype])
+
+
+M6_CASES = [(13, 1), (13, 16), (21, 1)]
+
+
+@pytest.mark.parametrize("d,batch", M6_CASES, ids=["d%d_b%d" % c for c in M6_CASES])
+def test_model6_at_timed_shape(cuda, d, batch):
+    T = d
+    blocks = workload.MODEL6_BLOCKS
+    weights = workload.resnet_weights(blocks, 4006)  # the benchmark's weights
+    det = _inputs(d, batch)
+    rows = [0] if batch == 1 else [0, batch - 1]
+    say("Model 6 d = T =", d, "batch", batch)
+    pre = pdx.Predecoder(weights, d, T, None, "bf16", max_batch=batch, layout="paper", first="Z", last="Z",
+                         blocks=blocks)
+    flips, res, logits = run_gpu(pre, det)
+    pre.close()
+    ref = oracle.run_resnet(d, T, det[rows], blocks, weights, bf16=True, layout="paper", first="Z", last="Z")
+    _check(d, T, "bf16", det, rows, flips, res, logits, ref, RESNET_TOL)
