@@ -128,7 +128,8 @@ typedef enum pd_status {
   PD_ERR_INVALID_ARG = 1,
   PD_ERR_UNSUPPORTED = 2,
   PD_ERR_OUT_OF_MEMORY = 3,
-  PD_ERR_DEVICE = 4
+  PD_ERR_DEVICE = 4,
+  PD_ERR_TOO_LARGE = 5 /* predecoder_run_static: the batch needs more than its static array */
 } pd_status;
 
 typedef enum pd_act { PD_ACT_NONE = 0, PD_ACT_GELU_TANH = 1, PD_ACT_RELU = 2 } pd_act;
@@ -268,6 +269,41 @@ pd_status predecoder_graph_create(pd_predecoder* h, const uint64_t* det, int32_t
                                   uint64_t* residual, float* logits, pd_graph** out);
 pd_status predecoder_graph_launch(pd_graph* g, void* hip_stream);
 void predecoder_graph_destroy(pd_graph* g); /* NULL is a no-op; waits for the device */
+
+/* ---- A run that allocates nothing ----
+ *
+ * For callers that cannot allocate device memory while they run the path:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation.  predecoder_run_static takes the arguments of predecoder_run
+ * and runs the same kernels, but keeps the workspace -- input planes,
+ * activation buffers, projection outputs of residual networks, flip nibbles
+ * and the parked sums of split K loops -- in a static device array of
+ * PD_STATIC_SCRATCH_BYTES bytes that the library holds on every device it
+ * runs on until the process ends, instead of the handle's own workspace.  It
+ * calls no allocating routine (the handle is made beforehand with
+ * predecoder_create*, which does allocate).
+ *   Size: with S = (T + 2)(H + 2)^2 padded voxels and V = T H^2 voxels per
+ *   sample, each region rounded up to 256 bytes: batch S c_in e (planes; e = 4
+ *   for PD_DTYPE_FP32, else 2), two (residual networks: three) activation
+ *   buffers of batch S cmax a (cmax the widest activation row; a = 4 fp32, 2
+ *   bf16, 1 fp8), for residual networks batch S pmax 2 (the widest projection),
+ *   and batch V (flip nibbles) must fit, else PD_ERR_TOO_LARGE before any
+ *   device work.  What is left holds the parked sums of small batches' split K
+ *   loops (128 KiB per unit, up to the handle's one per compute unit); with
+ *   fewer units a layer may split less than predecoder_run splits it, and the
+ *   results then differ by the fp32 summation order, as two batch sizes can.
+ *   With room for all units the results are bit-identical to predecoder_run's.
+ *   (Batch 1 with 128 channels on the plaquette grid needs about 2 MB before
+ *   the parked sums at d = 13 and 20 MB at d = 31.)
+ * Every call on one device uses that device's one array, which keeps the last
+ * call's contents: each call clears what must start at zero (with a fill
+ * kernel on hip_stream, no memset), and calls that overlap on one device --
+ * from two streams or threads, with any handles -- race and give wrong
+ * results; the caller serialises them.  Asynchronous on hip_stream; the first
+ * call on a device looks up the array's device address (no allocation). */
+#define PD_STATIC_SCRATCH_BYTES (64u << 20)
+pd_status predecoder_run_static(pd_predecoder* h, void* hip_stream, const uint64_t* det, int32_t batch,
+                                uint64_t* flips, uint64_t* residual, float* logits);
 
 /* ---- Residual networks (Model 6, Sec. VI, Fig. Model8Representation) ----
  *

@@ -24,7 +24,8 @@ LAYOUT_PLAQUETTE, LAYOUT_PAPER = 0, 1
 BOUNDARY_NONE, BOUNDARY_Z, BOUNDARY_X = 0, 1, 2
 _LAYOUTS = {"plaquette": LAYOUT_PLAQUETTE, "paper": LAYOUT_PAPER}
 _BOUNDARIES = {None: BOUNDARY_NONE, "none": BOUNDARY_NONE, "Z": BOUNDARY_Z, "X": BOUNDARY_X}
-PD_OK, PD_ERR_INVALID_ARG, PD_ERR_UNSUPPORTED, PD_ERR_OUT_OF_MEMORY, PD_ERR_DEVICE = range(5)
+PD_OK, PD_ERR_INVALID_ARG, PD_ERR_UNSUPPORTED, PD_ERR_OUT_OF_MEMORY, PD_ERR_DEVICE, PD_ERR_TOO_LARGE = range(6)
+STATIC_SCRATCH_BYTES = 64 << 20  # PD_STATIC_SCRATCH_BYTES
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpredecoder.so")
 
@@ -36,7 +37,7 @@ EXPORTS = ("predecoder_create", "predecoder_create_ex", "predecoder_run", "prede
            "predecoder_weight_count", "predecoder_stream_windows", "predecoder_stream_create",
            "predecoder_stream_run", "predecoder_stream_destroy", "predecoder_resnet_weight_count",
            "predecoder_create_resnet", "predecoder_graph_create", "predecoder_graph_launch",
-           "predecoder_graph_destroy")
+           "predecoder_graph_destroy", "predecoder_run_static")
 
 
 class PredecoderError(RuntimeError):
@@ -120,6 +121,8 @@ def lib():
         L.predecoder_graph_launch.restype = i32
         L.predecoder_graph_destroy.argtypes = [vp]
         L.predecoder_graph_destroy.restype = None
+        L.predecoder_run_static.argtypes = [vp, vp, vp, i32, vp, vp, vp]
+        L.predecoder_run_static.restype = i32
         _lib = L
     return _lib
 
@@ -258,6 +261,14 @@ class Predecoder:
         batch = _batch(batch, det)
         pd, pf, pr, pl = self._io(det, flips, residual, logits, batch)
         self._check(lib().predecoder_run(self._h, _stream(stream), pd, batch, pf, pr, pl), "predecoder_run")
+
+    def run_static(self, det, flips, residual, logits=None, batch=None, stream=None):
+        """run() with the workspace in the library's static device array (allocates nothing; calls that
+        overlap on one device race)."""
+        batch = _batch(batch, det)
+        pd, pf, pr, pl = self._io(det, flips, residual, logits, batch)
+        self._check(lib().predecoder_run_static(self._h, _stream(stream), pd, batch, pf, pr, pl),
+                    "predecoder_run_static")
 
     def residual(self, det, flips, residual, batch=None, stream=None):
         batch = _batch(batch, det)

@@ -768,6 +768,7 @@ const char* predecoder_status_string(pd_status s) {
     case PD_ERR_UNSUPPORTED: return "unsupported shape";
     case PD_ERR_OUT_OF_MEMORY: return "out of device memory";
     case PD_ERR_DEVICE: return "device error";
+    case PD_ERR_TOO_LARGE: return "batch too large for the library's static scratch array";
   }
   return "unknown status";
 }
@@ -1159,6 +1160,66 @@ pd_status predecoder_run(pd_predecoder* h, void* hip_stream, const uint64_t* det
   return enqueue_run(h, h->ws, (hipStream_t)hip_stream, det, batch, flips, residual, logits, nullptr);
 }
 
+}  // extern "C"
+
+namespace pd {
+
+pd_status run_in_region(pd_predecoder* h, hipStream_t st, const uint64_t* det, int batch, uint64_t* flips,
+                        uint64_t* residual, float* logits, void* base, size_t bytes) {
+  if (!h || !det || !flips || !residual || !base) return PD_ERR_INVALID_ARG;
+  if (batch < 1 || batch > h->max_batch) return PD_ERR_INVALID_ARG;
+  const Geom& g = h->g;
+  const bool resnet = !h->blocks.empty();
+  const int fp32 = h->dtype == PD_DTYPE_FP32, fp8 = h->dtype == PD_DTYPE_FP8;
+  const size_t elem = fp32 ? 4 : 2;                 // input planes
+  const size_t aelem = fp32 ? 4 : (fp8 ? 1 : 2);   // activations
+  const size_t cin0 = resnet ? (size_t)h->blocks[0].c_in : (size_t)h->layers[0].c_in;
+  const size_t vox = (size_t)batch * (size_t)g.S;
+  // regions of 256-byte aligned offsets: planes, activations, projection
+  // outputs (residual networks), flip nibbles, then the parked sums
+  size_t off = 0;
+  auto carve = [&](size_t n) {
+    const size_t at = (off + 255) & ~(size_t)255;
+    off = at + ((n + 255) & ~(size_t)255);
+    return at;
+  };
+  const size_t planes_bytes = vox * cin0 * elem, act_bytes = vox * (size_t)h->cmax * aelem;
+  const size_t o_planes = carve(planes_bytes);
+  size_t o_act[3] = {carve(act_bytes), carve(act_bytes), 0};
+  size_t o_pbuf = 0;
+  if (resnet) {
+    o_act[2] = carve(act_bytes);
+    o_pbuf = carve(vox * (size_t)h->pmax * 2);
+  }
+  const size_t o_nib = carve((size_t)batch * g.V);
+  if (off > bytes) return PD_ERR_TOO_LARGE;
+  char* b = (char*)base;
+  Workspace ws;
+  ws.planes = b + o_planes;
+  for (int k = 0; k < (resnet ? 3 : 2); ++k) ws.act[k] = b + o_act[k];
+  ws.pbuf = resnet ? (void*)(b + o_pbuf) : nullptr;
+  ws.nib = (uint8_t*)(b + o_nib);
+  ws.act_bytes = act_bytes;
+  if (!fp32) {  // what is left holds the parked sums of up to the handle's own number of units
+    const size_t unit = pd::conv_hidden_partial_floats_per_unit() * 4;
+    const size_t o_part = carve(0);
+    const long long fit = (long long)((bytes - std::min(bytes, o_part)) / unit);
+    ws.max_units = std::min(h->ws.max_units, fit);
+    ws.partial = (float*)(b + o_part);
+  }
+  // the zero halos the 3x3x3 layers read: the planes and every activation
+  // buffer start all zero (a fill kernel, so that the call can be captured
+  // into a graph); the other regions are written before they are read
+  pd_status s = check_launch(launch_zero(ws.planes, (planes_bytes + 15) & ~(size_t)15, st));
+  for (int k = 0; k < (resnet ? 3 : 2) && s == PD_OK; ++k)
+    s = check_launch(launch_zero(ws.act[k], (act_bytes + 15) & ~(size_t)15, st));
+  if (s != PD_OK) return s;
+  return enqueue_run(h, ws, st, det, batch, flips, residual, logits, nullptr);
+}
+
+}  // namespace pd
+
+extern "C" {
 
 pd_status predecoder_residual(pd_predecoder* h, void* hip_stream, const uint64_t* det,
                               const uint64_t* flips, int32_t batch, uint64_t* residual) {

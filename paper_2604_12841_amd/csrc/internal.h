@@ -4,7 +4,10 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <stddef.h>
 #include <stdint.h>
+
+#include "../../include/predecoder.h"
 
 namespace pd {
 
@@ -212,6 +215,16 @@ hipError_t launch_stream_gather(const uint64_t* det, long long row_words, const 
 hipError_t launch_stream_scatter(const StreamWindow* win, const uint64_t* const* group_flips,
                                  const long long* group_words, int n_streams, int core, int n_rounds, int F,
                                  long long row_words, uint64_t* flips, hipStream_t stream);
+
+// predecoder_run of handle h with its workspace laid out in the `bytes` of
+// device memory at `base` instead of the handle's own (input planes,
+// activation buffers, projection outputs, flip nibbles, then as many units of
+// parked split-K sums as fit, at most the handle's own number): the planes
+// and activation buffers are cleared with a fill kernel first; nothing is
+// allocated.  PD_ERR_TOO_LARGE when the regions before the parked sums do not
+// fit.  Asynchronous on st.
+pd_status run_in_region(pd_predecoder* h, hipStream_t st, const uint64_t* det, int batch, uint64_t* flips,
+                        uint64_t* residual, float* logits, void* base, size_t bytes);
 
 // Persistent workgroups of a conv launch: one per CU (n_workgroups), a
 // multiple of 8 (one per XCD round-robin slot), never more than the tiles
