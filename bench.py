@@ -12,7 +12,6 @@ algorithmic FLOPs / its mean HIP-event duration) and the CPU oracle timed on a
 bounded sample of the same workload.
 """
 import argparse
-import glob
 import hashlib
 import json
 import os
@@ -30,14 +29,24 @@ PEAK_FP8_TFLOPS = 5000.0   # MI355X dense fp8 MFMA
 PEAK_HBM_GBS = 8000.0
 
 
+# The translation unit of the dominant kernel (the hidden conv layer): its
+# source and every header it includes.
+KERNEL_SOURCES = ("paper_2604_12841_amd/csrc/conv_hidden.hip", "paper_2604_12841_amd/csrc/tiles.h",
+                  "paper_2604_12841_amd/csrc/activation.h", "paper_2604_12841_amd/csrc/internal.h",
+                  "include/predecoder.h")
+
+
 def kernel_source_hash():
-    """sha256 over the HIP sources (csrc/*.hip, *.h, sorted by name)."""
+    """sha256 over the code of the dominant kernel's translation unit
+    (KERNEL_SOURCES with comments and whitespace runs removed, so that an
+    edit of prose alone keeps a counter summary valid)."""
     h = hashlib.sha256()
-    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2604_12841_amd", "csrc", "*.hip")) +
-                    glob.glob(os.path.join(ROOT, "paper_2604_12841_amd", "csrc", "*.h"))):
-        h.update(os.path.basename(f).encode())
-        with open(f, "rb") as fh:
-            h.update(fh.read())
+    for f in KERNEL_SOURCES:
+        text = open(os.path.join(ROOT, f)).read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(f.encode())
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()
 
 
@@ -54,6 +63,69 @@ def counted_traffic(profile):
     if not m_hash or not m_bytes or m_hash.group(1) != kernel_source_hash():
         return None
     return int(m_bytes.group(1))
+
+
+def measure_peaks(torch, pdx, stream, iters=20000, copy_mib=1024, reps=5):
+    """The ceilings measured on this device (predecoder_peak_mfma /
+    predecoder_peak_copy, HIP events on `stream`): back-to-back bf16 and fp8
+    matrix instructions on all-zero and on random operands (four workgroups of
+    four waves per compute unit), and a plain 1 GiB device copy."""
+    n_wg = 4 * torch.cuda.get_device_properties(0).multi_processor_count
+    out = torch.empty(n_wg * 256, dtype=torch.float32, device="cuda")
+    g = torch.Generator().manual_seed(7)
+    rand = {
+        "bf16": torch.randn(2048, generator=g).to(torch.bfloat16).view(torch.uint8),
+        "fp8": torch.randn(4096, generator=g).to(torch.float8_e4m3fn).view(torch.uint8),
+    }
+    res = {}
+
+    def timed(fn):
+        for _ in range(2):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e-3
+
+    for dt in ("bf16", "fp8"):
+        for kind in ("zero", "random"):
+            ops = torch.zeros(4096, dtype=torch.uint8) if kind == "zero" else rand[dt]
+            ops = ops.cuda()
+            flops = []
+            t = timed(lambda: flops.append(pdx.peak_mfma(dt, ops, iters, n_wg, out, stream=stream)))
+            res["mfma_%s_%s_tflops" % (dt, kind)] = flops[0] / t / 1e12
+    n = copy_mib << 20
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    t = timed(lambda: pdx.peak_copy(src, dst, n, stream=stream))
+    res["hbm_copy_gbs"] = 2 * n / t / 1e9
+    res["how"] = ("predecoder_peak_mfma: %d workgroups x 4 waves, %d x 4 back-to-back v_mfma_f32_32x32x16_bf16 / "
+                  "32x32x64 fp8 per wave, mean of %d launches; predecoder_peak_copy: %d MiB read + written"
+                  % (n_wg, iters, reps, copy_mib))
+    del src, dst
+    return res
+
+
+def graph_replays(torch, pre, ddet, flips, res, stream, n, warmup):
+    """Median / p10 / p90 of `n` recorded-run replays (each timed with its own
+    HIP events on `stream`) after `warmup` untimed ones."""
+    g = pre.graph(ddet, flips, res)
+    for _ in range(warmup):
+        g.launch(stream=stream)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+    ev[0].record(stream)
+    for k in range(n):
+        g.launch(stream=stream)
+        ev[k + 1].record(stream)
+    torch.cuda.synchronize()
+    g.close()
+    ms = np.array([ev[k].elapsed_time(ev[k + 1]) for k in range(n)])
+    return {"replays": n, "warmup": warmup, "median_ms": float(np.median(ms)),
+            "p10_ms": float(np.percentile(ms, 10)), "p90_ms": float(np.percentile(ms, 90)),
+            "min_ms": float(ms.min()), "max_ms": float(ms.max())}
 
 
 def flops_per_sample(layers, H, T):
@@ -195,6 +267,12 @@ def main():
                     help="time replays of a recorded run (HIP graph) instead of predecoder_run calls")
     ap.add_argument("--core", type=int, default=None, help="--stream: committed rounds per window (default d)")
     ap.add_argument("--buffer", type=int, default=None, help="--stream: rounds read on each side (default d)")
+    ap.add_argument("--replays", type=int, default=100,
+                    help="recorded-run (HIP graph) replays timed one by one for the median / p10 / p90 (0: skip)")
+    ap.add_argument("--replay-warmup", type=int, default=200, help="untimed replays before them")
+    ap.add_argument("--no-peaks", action="store_true", help="skip the measured MFMA / HBM ceilings")
+    ap.add_argument("--peaks", action="store_true",
+                    help="only measure the MFMA and HBM ceilings of this device and print them")
     ap.add_argument("--dtype", choices=["bf16", "fp8"], default=None,
                     help="operand precision (default: the workload's, bf16 for the benchmark workload); fp8 = "
                          "E4M3 weights and activations with fp32 accumulation, the paper's deployment precision")
@@ -209,6 +287,13 @@ def main():
     import paper_2604_12841_amd as pdx
     from paper_2604_12841_amd import workload
 
+    if args.peaks:
+        torch.cuda.set_device(0)
+        pk = measure_peaks(torch, pdx, torch.cuda.current_stream())
+        print(json.dumps({"metric": "measured MI355X ceilings", "measured_peaks": pk,
+                          "published": {"mfma_bf16_tflops": PEAK_BF16_TFLOPS, "mfma_fp8_tflops": PEAK_FP8_TFLOPS,
+                                        "hbm_gbs": PEAK_HBM_GBS}}), flush=True)
+        return
     paper = args.paper_model is not None
     if args.paper_model == 6:
         return bench_model6(args, torch, pdx, workload)
@@ -274,6 +359,12 @@ def main():
 
     # Per-stage HIP-event times on the same stream (unpack, each layer, head, residual).
     stages = pre.stage_times(ddet, flips, res, args.stage_iters, stream=stream)
+    # the paper's protocol: replays of a recorded run, each timed (median, p10, p90)
+    replays = graph_replays(torch, pre, ddet, flips, res, stream, args.replays, args.replay_warmup) \
+        if args.replays > 0 else None
+    if replays:
+        print("graph replays: median %.3f ms (p10 %.3f, p90 %.3f)" % (replays["median_ms"], replays["p10_ms"],
+                                                                      replays["p90_ms"]), file=sys.stderr, flush=True)
     n = len(layers)
     # hidden C->C layers whose epilogue writes activations (with a 1x1x1 head
     # the last hidden layer also applies the head and is timed separately in
@@ -323,6 +414,10 @@ def main():
             "unpack": B * (pre.det_words * 8 + V * in_bytes) / (stages[0] * 1e-3) / 1e9,
             "residual_repack": B * (V + pre.det_words * 16 + pre.flip_words * 8) / (stages[n + 1] * 1e-3) / 1e9,
         },
+        "graph_replays": None if replays is None else dict(
+            replays, rounds_per_s_median=rounds / (replays["median_ms"] * 1e-3),
+            us_per_round_median=replays["median_ms"] * 1e3 / rounds,
+            us_per_round_latency_median=replays["median_ms"] * 1e3 / T),
         "roofline": {
             "kernel": "conv3d 3x3x3 %d->%d implicit GEMM (%s MFMA) + bias/GELU epilogue"
                       % (ci, co, "fp8 e4m3" if fp8 else "bf16"),
@@ -335,6 +430,14 @@ def main():
                                        % (ci, co, d, T, B, "_fp8" if fp8 else "")),
         },
     }
+
+    if not args.no_peaks:
+        pk = measure_peaks(torch, pdx, stream)
+        mp = pk["mfma_%s_random_tflops" % ("fp8" if fp8 else "bf16")]
+        out["measured_peaks"] = pk
+        out["roofline"].update(measured_peak=mp, frac_of_measured=achieved / mp)
+        out["mfma_frac_end_to_end_of_measured"] = total_flops / (ms * 1e-3) / (mp * 1e12)
+        print("measured peaks:", {k: round(v, 1) for k, v in pk.items() if k != "how"}, file=sys.stderr, flush=True)
 
     if paper:
         # the paper times Table models at batch 1 (Table runtimes, GB300, FP8,
@@ -364,28 +467,52 @@ def main():
         return
 
     if not args.no_cpu_baseline:
+        # the oracle on a bounded sample of the same workload, built for this
+        # host (-march=native), with all its threads and with one; and the
+        # parity of the GPU's outputs for those samples (the timed launch
+        # configuration: the whole batch, logits kept) against it
         import oracle
+        sys.path.insert(0, os.path.join(ROOT, "tests"))
+        from parity import compare
         ns = args.cpu_samples or {1: 64, 2: 128, 3: 48, 4: 1, 5: 4}[args.workload]
         ns = min(ns, B)
-        oracle.build()
+        oracle.use_native()
         oracle.unpack(d, T, det[:1])  # load the library outside the timed region
+        bf16 = cfg["dtype"] == "bf16"
         t0 = time.perf_counter()
-        oracle.run(d, T, det[:ns], layers, weights, bf16=(cfg["dtype"] == "bf16"), fp8=fp8)
+        ref = oracle.run(d, T, det[:ns], layers, weights, bf16=bf16, fp8=fp8)
         dt = time.perf_counter() - t0
         cores = oracle.num_threads()
+        n1 = max(1, min(ns, int(round(ns / cores))))
+        oracle.set_num_threads(1)
+        t0 = time.perf_counter()
+        oracle.run(d, T, det[:n1], layers, weights, bf16=bf16, fp8=fp8)
+        dt1 = time.perf_counter() - t0
+        oracle.set_num_threads(cores)
         out["cpu_baseline"] = {
             "value": ns * T / dt, "unit": "rounds/s", "cores": cores, "kind": "oracle",
-            "sample": "%d of the %d samples (%.1f s, fp64 oracle with %s rounding points, "
+            "sample": "%d of the %d samples (%.1f s, fp64 oracle with %s rounding points, gcc -O3 -march=native, "
                       "OpenMP over samples x output channels, %d host CPUs visible)"
                       % (ns, B, dt, cfg["dtype"], len(os.sched_getaffinity(0))),
+            "single_thread": {"value": n1 * T / dt1, "unit": "rounds/s", "cores": 1,
+                              "sample": "%d of the %d samples (%.1f s)" % (n1, B, dt1)},
         }
+        logits = torch.empty((B, 4, T, grid, grid), dtype=torch.float32, device="cuda")
+        pre.run(ddet, flips, res, logits, stream=stream)
+        torch.cuda.synchronize()
+        u64 = lambda t: t[:ns].cpu().numpy().view(np.uint64)
+        st = compare(d, T, cfg["dtype"], *ref, u64(flips), u64(res), logits[:ns].cpu().numpy())
+        out["parity"] = dict(st, samples=ns, rule="logits within the dtype's bound; flips and residual bit-exact "
+                                                  "outside sites whose oracle |logit| <= it")
+        del logits
     pre.close()
     if args.copy_mib:
+        # a plain device copy of known size (HBM byte-counter calibration)
         n = args.copy_mib << 20
         src = torch.ones(n, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
         torch.cuda.synchronize()
-        dst.copy_(src)
+        pdx.peak_copy(src, dst, n, stream=stream)
         torch.cuda.synchronize()
         out["copy_calibration_mib"] = args.copy_mib
     print(json.dumps(out), flush=True)

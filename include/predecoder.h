@@ -389,6 +389,33 @@ pd_status predecoder_stream_run(pd_stream* s, void* hip_stream, const uint64_t* 
 /* Releases the driver (NULL is a no-op); waits for the device. */
 void predecoder_stream_destroy(pd_stream* s);
 
+/* ---- Measurement aids ----
+ *
+ * The ceilings the roofline fractions are quoted against, measured on the
+ * device at hand (the paper times its engines on its own GPUs, Sec. VI, GPU
+ * runtimes; the published MI355X peaks are the reference here).  The caller
+ * times them with events on hip_stream.
+ *
+ * predecoder_peak_mfma: n_workgroups workgroups of four waves, each wave
+ * issuing iters x 4 back-to-back matrix instructions (four independent
+ * accumulators) on register operands: v_mfma_f32_32x32x16_bf16 for
+ * PD_DTYPE_BF16 (32768 FLOP each), the 32x32x64 E4M3 instruction for
+ * PD_DTYPE_FP8 (131072 FLOP each).  operands: device, 4096 bytes; lane l of
+ * every wave takes its A operand from bytes [64 l, 64 l + 32) and its B
+ * operand from [64 l + 32, 64 l + 64) (bf16: the first 16 of each); all
+ * zero or random values give the two ends of the power-limited clock.  out:
+ * device, n_workgroups x 256 floats (one sum per lane, so no instruction is
+ * dead).  PD_ERR_INVALID_ARG for null pointers, iters or n_workgroups < 1, or
+ * another dtype.  Asynchronous on hip_stream. */
+pd_status predecoder_peak_mfma(void* hip_stream, int32_t dtype, const void* operands, int32_t iters,
+                               int32_t n_workgroups, float* out);
+
+/* predecoder_peak_copy: dst[0, bytes) = src[0, bytes), device buffers that
+ * do not overlap, bytes a nonzero multiple of 16 (one 16-byte load and
+ * store per lane): reads and writes `bytes` each.  PD_ERR_INVALID_ARG
+ * otherwise.  Asynchronous on hip_stream. */
+pd_status predecoder_peak_copy(void* hip_stream, const void* src, void* dst, size_t bytes);
+
 #ifdef __cplusplus
 }
 #endif

@@ -20,24 +20,43 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "oracle.c")
 _LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_NATIVE_PATH = os.path.join(_HERE, "liboracle_native.so")
 _lib = None
+_native = False
+# ISO C (no contraction of a * b + c into one rounding), OpenMP over samples
+# and output channels
+_FLAGS = ["-O3", "-fopenmp", "-fPIC", "-shared", "-std=c11", "-ffp-contract=off"]
 
 
-def build(force=False):
-    """Compile oracle.c into liboracle.so (gcc, OpenMP over samples and output channels)."""
-    if force or not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
-        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
-        subprocess.check_call(["gcc", "-O3", "-fopenmp", "-fPIC", "-shared", "-std=c11", _SRC,
-                               "-o", tmp, "-lm"])
-        os.replace(tmp, _LIB_PATH)
-    return _LIB_PATH
+def build(force=False, native=False):
+    """Compile oracle.c into liboracle.so (portable), or with native=True into
+    liboracle_native.so for the CPU it is built on (-march=native; the same
+    IEEE operations in the same order, so the same results, only vector
+    instructions of that CPU).  The native build is made on the machine that
+    times it."""
+    path = _NATIVE_PATH if native else _LIB_PATH
+    if force or not os.path.exists(path) or os.path.getmtime(path) < os.path.getmtime(_SRC):
+        tmp = path + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc"] + _FLAGS + (["-march=native"] if native else []) + [_SRC, "-o", tmp, "-lm"])
+        os.replace(tmp, path)
+    return path
+
+
+def use_native():
+    """Build (on this machine) and use the -march=native library from now on
+    (the CPU baseline's timing).  Must come before any other oracle call."""
+    global _native
+    if _lib is not None and not _native:
+        raise RuntimeError("the portable oracle library is already loaded")
+    build(force=True, native=True)
+    _native = True
 
 
 def _load():
     global _lib
     if _lib is None:
-        build()
-        lib = ctypes.CDLL(_LIB_PATH)
+        path = _NATIVE_PATH if _native else build()
+        lib = ctypes.CDLL(path)
         i32, i64, vp = ctypes.c_int, ctypes.c_int64, ctypes.c_void_p
         lib.oracle_site_kind.argtypes = [i32, i32, i32]
         lib.oracle_site_kind.restype = i32
@@ -268,6 +287,14 @@ def num_threads():
     lib = _load()
     lib.oracle_num_threads.restype = ctypes.c_int
     return int(lib.oracle_num_threads())
+
+
+def set_num_threads(n):
+    """Threads for the oracle's parallel loops from now on."""
+    lib = _load()
+    lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
+    lib.oracle_set_num_threads.restype = None
+    lib.oracle_set_num_threads(int(n))
 
 
 def run(d, T, det, layers, weights, bf16, layout="plaquette", first=None, last=None, fp8=False):

@@ -839,3 +839,8 @@ void oracle_forward_resnet(int H, int T, int B, const double* planes, int n_bloc
 /* Threads an OpenMP parallel region of the oracle uses (reported with the
  * CPU timing; not part of the method). */
 int oracle_num_threads(void) { return omp_get_max_threads(); }
+
+/* Sets that number (the CPU timing's single-thread figure); n >= 1. */
+void oracle_set_num_threads(int n) {
+  if (n >= 1) omp_set_num_threads(n);
+}

@@ -37,7 +37,7 @@ EXPORTS = ("predecoder_create", "predecoder_create_ex", "predecoder_run", "prede
            "predecoder_weight_count", "predecoder_stream_windows", "predecoder_stream_create",
            "predecoder_stream_run", "predecoder_stream_destroy", "predecoder_resnet_weight_count",
            "predecoder_create_resnet", "predecoder_graph_create", "predecoder_graph_launch",
-           "predecoder_graph_destroy", "predecoder_run_static")
+           "predecoder_graph_destroy", "predecoder_run_static", "predecoder_peak_mfma", "predecoder_peak_copy")
 
 
 class PredecoderError(RuntimeError):
@@ -123,6 +123,10 @@ def lib():
         L.predecoder_graph_destroy.restype = None
         L.predecoder_run_static.argtypes = [vp, vp, vp, i32, vp, vp, vp]
         L.predecoder_run_static.restype = i32
+        L.predecoder_peak_mfma.argtypes = [vp, i32, vp, i32, i32, vp]
+        L.predecoder_peak_mfma.restype = i32
+        L.predecoder_peak_copy.argtypes = [vp, vp, vp, sz]
+        L.predecoder_peak_copy.restype = i32
         _lib = L
     return _lib
 
@@ -326,6 +330,26 @@ class Predecoder:
             self.close()
         except Exception:
             pass
+
+
+def peak_mfma(dtype, operands, iters, n_workgroups, out, stream=None):
+    """Back-to-back matrix instructions (predecoder_peak_mfma): operands, 4096-byte device tensor; out,
+    n_workgroups x 256 float32 device tensor.  Returns the FLOPs launched."""
+    dt = _DTYPES[dtype] if isinstance(dtype, str) else int(dtype)
+    po = _ptr(operands, "operands", 4096)
+    pout = _ptr(out, "out", n_workgroups * 256 * 4, 4)
+    st = lib().predecoder_peak_mfma(_stream(stream), dt, po, int(iters), int(n_workgroups), pout)
+    if st != PD_OK:
+        raise PredecoderError(st, "predecoder_peak_mfma")
+    return n_workgroups * 4 * iters * 4 * (131072 if dt == DTYPE_FP8 else 32768)
+
+
+def peak_copy(src, dst, nbytes, stream=None):
+    """dst[:nbytes] = src[:nbytes] with the library's copy kernel (predecoder_peak_copy)."""
+    ps, pd = _ptr(src, "src", nbytes), _ptr(dst, "dst", nbytes)
+    st = lib().predecoder_peak_copy(_stream(stream), ps, pd, int(nbytes))
+    if st != PD_OK:
+        raise PredecoderError(st, "predecoder_peak_copy")
 
 
 def stream_windows(n_rounds, core, buffer):
