@@ -289,6 +289,16 @@ Tiling plan_tiling(const Geom& g, int max_batch) {
 void tiling_for_batch(Tiling* t, const Geom& g, int batch) {
   t->div_a = pd::make_fastdiv((uint32_t)t->sa);
   t->div_b = pd::make_fastdiv((uint32_t)t->sb);
+  t->dv_V = pd::make_fastdiv((uint32_t)g.V);
+  t->dv_HH = pd::make_fastdiv((uint32_t)(g.H * g.H));
+  t->dv_H = pd::make_fastdiv((uint32_t)g.H);
+  if (t->mode == 1) {
+    t->dv_per = pd::make_fastdiv((uint32_t)(t->ntT * t->ntI * t->ntJ));
+    t->dv_ntij = pd::make_fastdiv((uint32_t)(t->ntI * t->ntJ));
+    t->dv_ntj = pd::make_fastdiv((uint32_t)t->ntJ);
+    t->dv_bij = pd::make_fastdiv((uint32_t)(t->BI * t->BJ));
+    t->dv_bj = pd::make_fastdiv((uint32_t)t->BJ);
+  }
   if (t->mode == 0) {
     if (t->seg_len < 0 || t->tiles_per_seg == 0) {
       // flat across samples
@@ -298,6 +308,7 @@ void tiling_for_batch(Tiling* t, const Geom& g, int batch) {
     } else {
       t->ntiles = (long long)batch * t->tiles_per_seg;
     }
+    t->dv_tps = pd::make_fastdiv((uint32_t)t->tiles_per_seg);
   } else {
     t->ntiles = (long long)batch * t->ntT * t->ntI * t->ntJ;
   }
@@ -547,15 +558,36 @@ struct StopAt {
   int row_bytes = 0;
 };
 
-// Split of a layer's K loop over 2^k workgroups per tile while tiles x parts
-// stay within the workspace's units (one per compute unit for a handle's
-// own: small batches, where a tile's K loop is the layer's latency); parts
-// must divide the layer's input-channel chunks.  Past one unit per CU the
-// parked fp32 sums cost more than the shorter loops gain.
-pd::Split_k split_for(const Workspace& ws, const Tiling& t, int cin, int fp8) {
+// Split of a layer's K loop over 2^k workgroups per tile.  Only small
+// batches split (tiles x parts within the workspace's units, one per compute
+// unit for a handle's own: past that the parked fp32 sums cost more than the
+// shorter loops gain); parts must divide the layer's input-channel chunks.
+// Among the splits that fit, the one with the least estimated time of a
+// workgroup's unit: its chunks, then either the tile's epilogue (bias,
+// activation and stores, done by the tile's single workgroup) or parking the
+// fp32 sums plus the second, elementwise kernel that finishes all tiles in
+// parallel.  Microseconds per unit on MI355X at batch 1, from per-phase
+// timestamps inside the kernel: a 16-channel chunk 2.5 (64 output channels)
+// or 3.9 (128); the activation epilogue 3.3 or 7.3; parking 1.75 or 3.4;
+// the finishing kernel with its launch about 8.  (For 64 channels at 25^3
+// one unsplit launch beats two parts by 3 us; for 128 channels at 13^3 the
+// split saves 20 us.)  fp8 chunks are 32 channels with about half a bf16
+// chunk's matrix time per channel.
+pd::Split_k split_for(const Workspace& ws, const Tiling& t, int cin, int cout, int fp8) {
   const int kch = pd::conv_hidden_chunk_channels(fp8);
+  const int nch = cin / kch;
+  const double wide = cout > 64 ? 1.0 : 0.0;
+  const double chunk = (2.5 + 1.4 * wide) * (fp8 ? 1.1 : 1.0), epi = 3.3 + 4.0 * wide, park = 1.75 + 1.65 * wide;
+  const double finish = 8.0;
   pd::Split_k sk{0, ws.partial, ws.max_units};
-  while ((cin / kch) % (2 << sk.kshift) == 0 && (t.ntiles << (sk.kshift + 1)) <= ws.max_units) ++sk.kshift;
+  double best = nch * chunk + epi;
+  for (int k = 1; nch % (1 << k) == 0 && (t.ntiles << k) <= ws.max_units; ++k) {
+    const double est = (nch >> k) * chunk + park + finish;
+    if (est < best) {
+      best = est;
+      sk.kshift = k;
+    }
+  }
   return sk;
 }
 
@@ -613,7 +645,7 @@ pd_status enqueue_resnet(pd_predecoder* h, Workspace& ws, hipStream_t st, const 
         else
           s = check_launch(pd::launch_conv_hidden(g, tl, B.c_in, cw, B.act, x, yq, B.c_mid, wq,
                                                   h->bdev[2 * k] + q * cw, 0, nullptr, nullptr, h->tables, ws.nib,
-                                                  nullptr, batch, hidden_wgs, split_for(ws, tl, B.c_in, 0), 0,
+                                                  nullptr, batch, hidden_wgs, split_for(ws, tl, B.c_in, cw, 0), 0,
                                                   nullptr, 0, st));
       }
       if (s != PD_OK) return s;
@@ -634,7 +666,7 @@ pd_status enqueue_resnet(pd_predecoder* h, Workspace& ws, hipStream_t st, const 
     if (last) {
       s = check_launch(pd::launch_conv_hidden(g, tl, B.c_mid, 4, 0, hb, nullptr, 0, h->wdev[2 * k + 1],
                                               h->bdev[2 * k + 1], 2, nullptr, nullptr, h->tables, ws.nib, logits,
-                                              batch, hidden_wgs, split_for(ws, tl, B.c_mid, 0), 0, sc, sc_stride, st));
+                                              batch, hidden_wgs, split_for(ws, tl, B.c_mid, 32, 0), 0, sc, sc_stride, st));
     } else {
       const int nsl = B.c_out > 128 ? B.c_out / 128 : 1, cw = B.c_out / nsl;
       for (int q = 0; q < nsl && s == PD_OK; ++q) {
@@ -642,7 +674,7 @@ pd_status enqueue_resnet(pd_predecoder* h, Workspace& ws, hipStream_t st, const 
         s = check_launch(pd::launch_conv_hidden(g, tl, B.c_mid, cw, B.act, hb, (uint16_t*)yb + (size_t)q * cw,
                                                 B.c_out, wq, h->bdev[2 * k + 1] + q * cw, 4, nullptr, nullptr,
                                                 h->tables, ws.nib, nullptr, batch, hidden_wgs,
-                                                split_for(ws, tl, B.c_mid, 0), 0, sc + (size_t)q * cw, sc_stride, st));
+                                                split_for(ws, tl, B.c_mid, cw, 0), 0, sc + (size_t)q * cw, sc_stride, st));
       }
     }
     if (s != PD_OK) return s;
@@ -717,7 +749,7 @@ pd_status enqueue_run(pd_predecoder* h, Workspace& ws, hipStream_t st, const uin
           s = check_launch(pd::launch_conv_hidden(g, tl, L.c_in, cw, L.act, x, yk, L.c_out, wk,
                                                   h->bdev[l] + k * cw * (fp8 ? 2 : 1), fuse_head ? 1 : 0,
                                                   h->head_w, h->head_b, h->tables, ws.nib, logits, batch,
-                                                  hidden_wgs, split_for(ws, tl, L.c_in, fp8), fp8, nullptr, 0, st));
+                                                  hidden_wgs, split_for(ws, tl, L.c_in, cw, fp8), fp8, nullptr, 0, st));
       }
       head_done = fuse_head && l > 0;
     }
@@ -735,7 +767,7 @@ pd_status enqueue_run(pd_predecoder* h, Workspace& ws, hipStream_t st, const uin
     const pd_layer& L = h->layers[n - 1];
     s = check_launch(pd::launch_conv_hidden(g, tl, L.c_in, L.c_out, L.act, x, nullptr, 0, h->wdev[n - 1],
                                             h->bdev[n - 1], 2, nullptr, nullptr, h->tables, ws.nib, logits,
-                                            batch, hidden_wgs, split_for(ws, tl, L.c_in, fp8), fp8, nullptr, 0, st));
+                                            batch, hidden_wgs, split_for(ws, tl, L.c_in, 32, fp8), fp8, nullptr, 0, st));
   } else if (!head_done) {  // fp32, or a one-hidden-layer network on the paper's layout
     s = check_launch(pd::launch_head(g, h->layers[n - 1].c_in, fp32, x, h->head_w, h->head_b, h->tables,
                                      ws.nib, logits, batch, st));

@@ -449,14 +449,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
   if (unit < 0) return;
   int tile = unit >> kshift;
 
-  auto source_of = [&](int t) {
-    StageSrc src;
-    long long p;
-    int lb;
-    tile_row(g, tl, t, 0, batch, &p, &lb, &src.origin);
-    src.bo = box_origin(g, tl, src.origin);
-    return src;
-  };
+  auto source_of = [&](int t) { return tile_source(g, tl, t, batch); };
   long long cur_base = stage_base<MODE>(g, source_of(tile));
   uint32_t soff[RMAX];  // this lane's staging offsets of the tile being staged
   {
@@ -725,7 +718,9 @@ __global__ void __launch_bounds__(256) split_finish_kernel(Geom g, Tiling tl, in
                                                            uint8_t* __restrict__ nib, float* __restrict__ logits,
                                                            int batch, const uint16_t* __restrict__ sc, int sc_stride) {
   constexpr bool ROWS8 = EPI == EPI_ACT || EPI == EPI_ADD;  // one thread per (row, 8 channels)
-  const int groups = ROWS8 ? cout / 8 : 1;
+  // the head: one thread per (row, 8 channels) too, the rows' partial head
+  // sums reduced over the row's consecutive lanes
+  const int groups = (ROWS8 || EPI == EPI_HEAD) ? cout / 8 : 1;
   const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   if (gid >= tl.ntiles * kTileRows * groups) return;
   const int tile = (int)(gid / (kTileRows * groups));
@@ -810,18 +805,25 @@ __global__ void __launch_bounds__(256) split_finish_kernel(Geom g, Tiling tl, in
         lg[3] += __uint_as_float(sv.y & 0xFFFF0000u);
       }
     } else {
+      // this lane's 8 channels, then the sum over the row's groups (cout / 8
+      // consecutive lanes, all active: a row is in range for all or none)
+      const int c = grp * 8;
+      float v[8];
+      sum8(c, v);
 #pragma unroll
-      for (int o2 = 0; o2 < 4; ++o2) lg[o2] = head_b[o2];
-      for (int c = 0; c < cout; c += 8) {
-        float v[8];
-        sum8(c, v);
+      for (int o2 = 0; o2 < 4; ++o2) lg[o2] = 0.0f;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float a = F8 ? e4m3_round(act_fn<ACT>(v[e])) : bf16_round(act_fn<ACT>(v[e]));
+      for (int e = 0; e < 8; ++e) {
+        const float a = F8 ? e4m3_round(act_fn<ACT>(v[e])) : bf16_round(act_fn<ACT>(v[e]));
 #pragma unroll
-          for (int o2 = 0; o2 < 4; ++o2) lg[o2] += head_w[o2 * cout + c + e] * a;
-        }
+        for (int o2 = 0; o2 < 4; ++o2) lg[o2] += head_w[o2 * cout + c + e] * a;
       }
+      for (int m = groups >> 1; m >= 1; m >>= 1)
+#pragma unroll
+        for (int o2 = 0; o2 < 4; ++o2) lg[o2] += __shfl_xor(lg[o2], m);
+      if (grp != 0) return;
+#pragma unroll
+      for (int o2 = 0; o2 < 4; ++o2) lg[o2] += head_b[o2];
     }
     const int HH = g.H * g.H;
     const int s = i * g.H + j;
@@ -870,7 +872,9 @@ hipError_t launch_one(const Geom& g, const Tiling& tl, int act, const void* x, v
                                                    nib, logits, batch, n_workgroups, sk.kshift, sk.partial, nullptr,
                                                    0, stream);
   if (e != hipSuccess) return e;
-  const long long threads = tl.ntiles * kTileRows * (EPI == EPI_ACT || EPI == EPI_ADD ? COUT / 8 : 1);
+  const long long threads =
+      tl.ntiles * kTileRows * (EPI == EPI_ACT || EPI == EPI_ADD || EPI == EPI_HEAD ? COUT / 8 : 1);
+  static_assert(EPI != EPI_HEAD || (64 % (COUT / 8) == 0), "a row's head lanes lie in one wave");
   with_activation(act, [&](auto A) {
     hipLaunchKernelGGL((split_finish_kernel<EPI, decltype(A)::value, F8>), dim3((unsigned)((threads + 255) / 256)),
                        dim3(256), 0, stream, g, tl, COUT, sk.kshift, sk.partial, bias, y, ystride, head_w, head_b,

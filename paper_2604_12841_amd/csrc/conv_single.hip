@@ -103,14 +103,7 @@ __global__ void __launch_bounds__(NT) conv_single_kernel(Geom g, Tiling tl, int 
   int tile = tile_of(blockIdx.x, gridDim.x, 0, ntiles);
   if (tile < 0) return;
 
-  auto source_of = [&](int t) {
-    StageSrc src;
-    long long p;
-    int lb;
-    tile_row(g, tl, t, 0, batch, &p, &lb, &src.origin);
-    src.bo = box_origin(g, tl, src.origin);
-    return src;
-  };
+  auto source_of = [&](int t) { return tile_source(g, tl, t, batch); };
 
   // First tile: stage its planes synchronously.
   {

@@ -83,6 +83,9 @@ __host__ __device__ inline uint32_t fastdiv(uint32_t n, FastDiv f) {
 #endif
 }
 
+// n / d for any divisor d >= 1 (make_fastdiv(1) has m = 0: the quotient is n).
+__host__ __device__ inline uint32_t fdiv(uint32_t n, FastDiv f) { return f.m ? fastdiv(n, f) : n; }
+
 struct Tiling {
   int mode;
   long long seg_len;
@@ -92,6 +95,9 @@ struct Tiling {
   int span;      // staged voxels per tile (upper bound), sizes the LDS buffers
   long long ntiles;
   FastDiv div_a, div_b;  // staging decode: mode 0 by PU and H; mode 1 by (BI+2)(BJ+2) and BJ+2
+  // tile and row decoding (tiles.h): mode 0 by tiles_per_seg, V, H^2 and H;
+  // mode 1 by the tiles per sample, ntI ntJ, ntJ, BI BJ and BJ
+  FastDiv dv_tps, dv_V, dv_HH, dv_H, dv_per, dv_ntij, dv_ntj, dv_bij, dv_bj;
 };
 
 __host__ __device__ inline int line_plane(const Geom& g) { return (g.H + 2) * g.H; }

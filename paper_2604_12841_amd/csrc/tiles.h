@@ -11,19 +11,23 @@ namespace pd {
 // else its padded output index (pidx) and its column j (col).  Also the LDS
 // voxel of the row's (0,0,0) tap (lds_base) and the staging origin: the
 // line-space index of staged voxel 0 (mode 0) or its padded index (mode 1).
-// 32-bit voxel counts: the host guarantees max_batch * V < 2^31.
+// 32-bit voxel counts: the host guarantees max_batch * V < 2^31.  Divisions
+// by the run-time sizes use the Tiling's precomputed multipliers (a plain
+// integer division costs tens of instructions per lane, which small
+// batches, with one tile per workgroup, pay in full).
 __host__ __device__ inline bool tile_row(const Geom& g, const Tiling& tl, int tile, int r, int batch,
                                          long long* pidx, int* lds_base, long long* stage_origin,
                                          int* col = nullptr) {
   const int HH = g.H * g.H;
   if (tl.mode == 0) {
-    const int seg = tile / tl.tiles_per_seg;
+    const int seg = (int)fdiv((uint32_t)tile, tl.dv_tps);
     const int k0 = (tile - seg * tl.tiles_per_seg) * kTileRows;
     const int u0 = seg * (int)tl.seg_len + k0;
-    const int b0 = u0 / g.V;
+    const int b0 = (int)fdiv((uint32_t)u0, tl.dv_V);
     const int v0 = u0 - b0 * g.V;
-    const int t0 = v0 / HH, s0 = v0 - t0 * HH;
-    const long long l0 = line_index(g, b0, t0, s0 / g.H, s0 % g.H);
+    const int t0 = (int)fdiv((uint32_t)v0, tl.dv_HH), s0 = v0 - t0 * HH;
+    const int i0 = (int)fdiv((uint32_t)s0, tl.dv_H);
+    const long long l0 = line_index(g, b0, t0, i0, s0 - i0 * g.H);
     *stage_origin = l0 - (line_plane(g) + g.H + 1);
     const int u = u0 + r;
     if (k0 + r >= tl.seg_len || u >= batch * g.V) {
@@ -31,25 +35,25 @@ __host__ __device__ inline bool tile_row(const Geom& g, const Tiling& tl, int ti
       if (col) *col = -1;
       return false;
     }
-    const int b = u / g.V;
+    const int b = (int)fdiv((uint32_t)u, tl.dv_V);
     const int v = u - b * g.V;
-    const int t = v / HH, s = v - t * HH;
-    const int i = s / g.H, j = s - i * g.H;
+    const int t = (int)fdiv((uint32_t)v, tl.dv_HH), s = v - t * HH;
+    const int i = (int)fdiv((uint32_t)s, tl.dv_H), j = s - i * g.H;
     *pidx = padded_index(g, b, t, i, j);
     *lds_base = (int)(line_index(g, b, t, i, j) - l0);
     if (col) *col = j;
     return true;
   } else {
-    const int per = tl.ntT * tl.ntI * tl.ntJ;
-    const int b = tile / per;
+    const int per = tl.ntT * tl.ntI * tl.ntJ, ntij = tl.ntI * tl.ntJ;
+    const int b = (int)fdiv((uint32_t)tile, tl.dv_per);
     const int rem = tile - b * per;
-    const int tt = rem / (tl.ntI * tl.ntJ);
-    const int ti = (rem / tl.ntJ) % tl.ntI;
-    const int tj = rem % tl.ntJ;
+    const int tt = (int)fdiv((uint32_t)rem, tl.dv_ntij), rem2 = rem - tt * ntij;
+    const int ti = (int)fdiv((uint32_t)rem2, tl.dv_ntj), tj = rem2 - ti * tl.ntJ;
     const int t0 = tt * tl.BT, i0 = ti * tl.BI, j0 = tj * tl.BJ;
     *stage_origin = (long long)b * g.S + (long long)t0 * g.P + (long long)i0 * g.Wp + j0;
     const int bij = tl.BI * tl.BJ;
-    const int a = r / bij, c = (r / tl.BJ) % tl.BI, e = r % tl.BJ;
+    const int a = (int)fdiv((uint32_t)r, tl.dv_bij), ra = r - a * bij;
+    const int c = (int)fdiv((uint32_t)ra, tl.dv_bj), e = ra - c * tl.BJ;
     const int t = t0 + a, i = i0 + c, j = j0 + e;
     const bool ok = (r < tl.BT * bij) && t < g.T && i < g.H && j < g.H;
     *lds_base = ok ? (a * (tl.BI + 2) + c) * (tl.BJ + 2) + e : 0;
@@ -66,25 +70,29 @@ __host__ __device__ inline bool tile_row_coords(const Geom& g, const Tiling& tl,
                                                 int* b, int* t, int* i, int* j) {
   const int HH = g.H * g.H;
   if (tl.mode == 0) {
-    const int seg = tile / tl.tiles_per_seg;
+    const int seg = (int)fdiv((uint32_t)tile, tl.dv_tps);
     const int k0 = (tile - seg * tl.tiles_per_seg) * kTileRows;
     const int u = seg * (int)tl.seg_len + k0 + r;
     if (k0 + r >= tl.seg_len || u >= batch * g.V) return false;
-    *b = u / g.V;
+    *b = (int)fdiv((uint32_t)u, tl.dv_V);
     const int v = u - *b * g.V;
-    *t = v / HH;
+    *t = (int)fdiv((uint32_t)v, tl.dv_HH);
     const int s = v - *t * HH;
-    *i = s / g.H;
+    *i = (int)fdiv((uint32_t)s, tl.dv_H);
     *j = s - *i * g.H;
     return true;
   }
-  const int per = tl.ntT * tl.ntI * tl.ntJ;
-  *b = tile / per;
+  const int per = tl.ntT * tl.ntI * tl.ntJ, ntij = tl.ntI * tl.ntJ;
+  *b = (int)fdiv((uint32_t)tile, tl.dv_per);
   const int rem = tile - *b * per;
+  const int tt = (int)fdiv((uint32_t)rem, tl.dv_ntij), rem2 = rem - tt * ntij;
+  const int ti = (int)fdiv((uint32_t)rem2, tl.dv_ntj), tj = rem2 - ti * tl.ntJ;
   const int bij = tl.BI * tl.BJ;
-  *t = (rem / (tl.ntI * tl.ntJ)) * tl.BT + r / bij;
-  *i = ((rem / tl.ntJ) % tl.ntI) * tl.BI + (r / tl.BJ) % tl.BI;
-  *j = (rem % tl.ntJ) * tl.BJ + r % tl.BJ;
+  const int a = (int)fdiv((uint32_t)r, tl.dv_bij), ra = r - a * bij;
+  const int c = (int)fdiv((uint32_t)ra, tl.dv_bj), e = ra - c * tl.BJ;
+  *t = tt * tl.BT + a;
+  *i = ti * tl.BI + c;
+  *j = tj * tl.BJ + e;
   return r < tl.BT * bij && *t < g.T && *i < g.H && *j < g.H;
 }
 
@@ -140,6 +148,26 @@ struct StageSrc {
   long long origin;
   BoxOrigin bo;
 };
+
+// The staging source of tile `tile` (mode 1: the box origin in padded
+// coordinates is the tile's first interior voxel, (t0, i0, j0) = (tt BT,
+// ti BI, tj BJ), shifted by the one-voxel halo).
+__host__ __device__ inline StageSrc tile_source(const Geom& g, const Tiling& tl, int tile, int batch) {
+  StageSrc src;
+  long long p;
+  int lb;
+  tile_row(g, tl, tile, 0, batch, &p, &lb, &src.origin);
+  src.bo = BoxOrigin{0, 0, 0};
+  if (tl.mode == 1) {
+    const int per = tl.ntT * tl.ntI * tl.ntJ, ntij = tl.ntI * tl.ntJ;
+    const int b = (int)fdiv((uint32_t)tile, tl.dv_per);
+    const int rem = tile - b * per;
+    const int tt = (int)fdiv((uint32_t)rem, tl.dv_ntij), rem2 = rem - tt * ntij;
+    const int ti = (int)fdiv((uint32_t)rem2, tl.dv_ntj), tj = rem2 - ti * tl.ntJ;
+    src.bo = BoxOrigin{tt * tl.BT, ti * tl.BI, tj * tl.BJ};
+  }
+  return src;
+}
 
 // Global padded voxel of staged voxel vv; -1 when it is outside the batch or
 // the sample's padded box (such voxels only feed rows that are discarded).
