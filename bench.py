@@ -255,8 +255,9 @@ def main():
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="also run one plain device copy of this many MiB (calibrates HBM byte counters)")
     ap.add_argument("--paper-model", type=int, default=None,
-                    help="time a model of Table models (1, 2, 4 or 5) in the paper's own layout (D x D grid, four "
-                         "input channels, 3x3x3 output layer) at d = T = --d instead of a workload")
+                    help="time a model of Table models (1 to 5; 6: the residual network) in the paper's own layout "
+                         "(D x D grid, four input channels, 3x3x3 (Model 3: 5x5x5) output layer) at d = T = --d "
+                         "instead of a workload")
     ap.add_argument("--d", type=int, default=None,
                     help="distance and rounds d = T: for --paper-model (default 13), or to run a workload's "
                          "network and noise at another distance (a sweep over d)")
@@ -372,9 +373,9 @@ def main():
     last_hidden = n - 1 if layers[-1][2] == 3 else n - 2
     hidden = [i for i in range(1, last_hidden) if layers[i][0] == layers[i][1]]
     conv_ms = float(np.mean([stages[1 + i] for i in hidden]))
-    ci, co = layers[hidden[0]][0], layers[hidden[0]][1]
+    ci, co, kk = layers[hidden[0]][0], layers[hidden[0]][1], layers[hidden[0]][2]
     V = T * grid ** 2
-    conv_flops = 2.0 * ci * co * 27 * V * B
+    conv_flops = 2.0 * ci * co * kk ** 3 * V * B
     achieved = conv_flops / (conv_ms * 1e-3) / 1e12
     print("stages ms:", ["%.3f" % s for s in stages], file=sys.stderr, flush=True)
 
@@ -419,8 +420,8 @@ def main():
             us_per_round_median=replays["median_ms"] * 1e3 / rounds,
             us_per_round_latency_median=replays["median_ms"] * 1e3 / T),
         "roofline": {
-            "kernel": "conv3d 3x3x3 %d->%d implicit GEMM (%s MFMA) + bias/GELU epilogue"
-                      % (ci, co, "fp8 e4m3" if fp8 else "bf16"),
+            "kernel": "conv3d %dx%dx%d %d->%d implicit GEMM (%s MFMA) + bias/GELU epilogue"
+                      % (kk, kk, kk, ci, co, "fp8 e4m3" if fp8 else "bf16"),
             "bound": "mfma",
             "achieved": achieved,
             "peak": peak,

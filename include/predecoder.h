@@ -97,7 +97,10 @@
  * the paper layout.  BF16 and FP8: hidden widths 64, 128 or 256 (a layer
  * after a 256-wide one needs a 3x3x3 output layer); FP8 needs two hidden
  * layers when the output layer is 1x1x1.  FP32 (plaquette layout only):
- * hidden widths 8 .. 128, multiples of 8.
+ * hidden widths 8 .. 128, multiples of 8.  5x5x5 networks (Model 3 of
+ * Table models): the paper layout, PD_DTYPE_BF16, every layer k == 5 (the
+ * output layer too), at least two hidden layers, all of one width, 64 or
+ * 128.
  *
  * Errors.  Every function is nothrow and never aborts.  Host-checkable misuse
  * gives PD_ERR_INVALID_ARG before any device call; a failed HIP call or

@@ -53,7 +53,8 @@ struct pd_predecoder {
   int max_batch = 0;
   int device = 0;
   std::vector<pd_layer> layers;
-  Tiling tiling{};               // shared by every 3x3x3 layer (bf16 path)
+  int ks = 3;                    // kernel size of the conv layers: 3, or 5 (Model 3 of Table models)
+  Tiling tiling{};               // shared by every k x k x k layer (bf16 and fp8 paths)
   Workspace ws;                  // sized for max_batch
   int32_t* tables = nullptr;
   std::vector<void*> wdev;       // per conv layer: fragments (bf16) or [tap][ci][co] (fp32)
@@ -99,17 +100,18 @@ bool layer_chain_ok(const pd_layer* l, int n, int layout) {
 }
 
 Geom make_geom(int d, int T, int layout = PD_LAYOUT_PLAQUETTE, int first = PD_BOUNDARY_NONE,
-               int last = PD_BOUNDARY_NONE) {
+               int last = PD_BOUNDARY_NONE, int pad = 1) {
   Geom g;
   g.d = d;
   g.T = T;
   g.layout = layout;
   g.first = first;
   g.last = last;
+  g.pad = pad;
   g.H = layout == PD_LAYOUT_PAPER ? d : d + 1;  // the data qubits, or the plaquettes
-  g.Wp = g.H + 2;
+  g.Wp = g.H + 2 * pad;
   g.P = g.Wp * g.Wp;
-  g.S = (long long)(T + 2) * g.P;
+  g.S = (long long)(T + 2 * pad) * g.P;
   g.V = T * g.H * g.H;
   g.nstab = d * d - 1;
   g.K = g.nstab / 2;
@@ -223,8 +225,11 @@ long long flat_span(const Geom& g, long long seg_len, long long nseg, int batch)
   return best;
 }
 
-Tiling plan_tiling(const Geom& g, int max_batch) {
-  const int kMaxSpan = std::min(pd::conv_single_max_span(), pd::conv_hidden_max_span());
+Tiling plan_tiling(const Geom& g, int max_batch, int ks = 3) {
+  // 5x5x5 layers: their own (larger) staging buffers, box tiles on a halo of two
+  const int kMaxSpan = ks == 3 ? std::min(pd::conv_single_max_span(), pd::conv_hidden_max_span(3))
+                               : pd::conv_hidden_max_span(5);
+  const int p = g.pad;
   Tiling best{};
   long long best_rows = -1;
   int best_span = 0;
@@ -237,8 +242,8 @@ Tiling plan_tiling(const Geom& g, int max_batch) {
       best_span = t.span;
     }
   };
-  // flat, tiles inside one sample
-  {
+  // flat, tiles inside one sample (a halo of one only)
+  if (p == 1) {
     Tiling t{};
     t.mode = 0;
     t.seg_len = g.V;
@@ -249,7 +254,7 @@ Tiling plan_tiling(const Geom& g, int max_batch) {
     consider(t, 2ll * t.tiles_per_seg * pd::kTileRows);
   }
   // flat across samples (rows per sample ~ V); the span bound covers any batch
-  if (max_batch > 1) {
+  if (max_batch > 1 && p == 1) {
     Tiling t{};
     t.mode = 0;
     t.seg_len = -1;  // set per run to batch * V
@@ -273,9 +278,9 @@ Tiling plan_tiling(const Geom& g, int max_batch) {
       t.ntT = (g.T + BT - 1) / BT;
       t.ntI = (g.H + BI - 1) / BI;
       t.ntJ = (g.H + BJ - 1) / BJ;
-      t.sa = (BI + 2) * (BJ + 2);
-      t.sb = BJ + 2;
-      t.span = (BT + 2) * (BI + 2) * (BJ + 2);
+      t.sa = (BI + 2 * p) * (BJ + 2 * p);
+      t.sb = BJ + 2 * p;
+      t.span = (BT + 2 * p) * (BI + 2 * p) * (BJ + 2 * p);
       // (a box row of BJ < 16 voxels, whose 16-lane LDS reads span two staged
       // lines, costs little: at d = T = 25 a 5x3x16 box and a 9x13x2 box
       // reach 0.54 and 0.53 of peak per MFMA row, so the row count decides,
@@ -314,9 +319,25 @@ void tiling_for_batch(Tiling* t, const Geom& g, int batch) {
   }
 }
 
+// Kernel size of a network's conv layers: 5 when its first layer is 5x5x5
+// (Model 3 of Table models), else 3.
+int network_ks(const pd_layer* l) { return l[0].k == 5 ? 5 : 3; }
+
 bool supported(const Geom& g, const pd_layer* l, int n, int dtype) {
   if (g.d > kMaxD || g.T > kMaxT) return false;
   if (n < 2) return false;  // at least one hidden 3x3x3 layer before the head
+  if (network_ks(l) == 5) {
+    // 5x5x5 networks (Model 3 of Table models): the paper layout, bf16, every
+    // layer 5x5x5 (the output layer too), one hidden width, 64 or 128
+    if (g.layout != PD_LAYOUT_PAPER || dtype != PD_DTYPE_BF16 || n < 3) return false;
+    const int w = l[0].c_out;
+    if (w != 64 && w != 128) return false;
+    for (int i = 0; i < n; ++i) {
+      if (l[i].k != 5) return false;
+      if (i < n - 1 && l[i].c_out != w) return false;
+    }
+    return true;
+  }
   if (g.layout == PD_LAYOUT_PAPER && dtype == PD_DTYPE_FP32) return false;
   const bool mfma = dtype != PD_DTYPE_FP32;
   // fp8 with a 1x1x1 head needs its head fused into a hidden layer after the
@@ -461,16 +482,17 @@ void free_all(pd_predecoder* h) {
 // fragment (k-step, channel block nb) holds W[co = 32 nb + l % 32][k0 + 8 (l / 32) + e],
 // e = 0..7; output channels past c_out (the 4 filters of an output layer fill
 // one block of 32) are zero.  Layer 1 (c_in = 2 or 4): k = c_in * tap + ci over
-// ceil(27 c_in / 16) k-steps (taps >= 27 are zero).  Other layers: [chunk of
-// 16 c_in][tap][nb] with ci = 16 chunk + 8 (l / 32) + e.
-std::vector<uint16_t> conv_fragments(const float* w, int cin, int cout) {
+// ceil(k^3 c_in / 16) k-steps (taps past the last are zero).  Other layers:
+// [chunk of 16 c_in][tap][nb] with ci = 16 chunk + 8 (l / 32) + e.
+std::vector<uint16_t> conv_fragments(const float* w, int cin, int cout, int k = 3) {
   const int nbt = cout < 32 ? 1 : cout / 32;
+  const int taps = k * k * k;
   std::vector<uint16_t> f;
   auto W = [&](int co, int ci, int tap) -> uint16_t {
-    return co < cout ? bf16_bits(w[((size_t)co * cin + ci) * 27 + tap]) : 0;
+    return co < cout ? bf16_bits(w[((size_t)co * cin + ci) * taps + tap]) : 0;
   };
   if (cin == 2 || cin == 4) {
-    const int ks_n = (27 * cin + 15) / 16;
+    const int ks_n = (taps * cin + 15) / 16;
     f.assign((size_t)ks_n * nbt * 64 * 8, 0);
     for (int ks = 0; ks < ks_n; ++ks)
       for (int nb = 0; nb < nbt; ++nb)
@@ -478,18 +500,18 @@ std::vector<uint16_t> conv_fragments(const float* w, int cin, int cout) {
           for (int e = 0; e < 8; ++e) {
             int k = ks * 16 + 8 * (l / 32) + e;
             int tap = k / cin, ci = k % cin, co = nb * 32 + l % 32;
-            f[(((size_t)ks * nbt + nb) * 64 + l) * 8 + e] = tap < 27 ? W(co, ci, tap) : 0;
+            f[(((size_t)ks * nbt + nb) * 64 + l) * 8 + e] = tap < taps ? W(co, ci, tap) : 0;
           }
   } else {
     const int nch = cin / 16;
-    f.assign((size_t)nch * 27 * nbt * 64 * 8, 0);
+    f.assign((size_t)nch * taps * nbt * 64 * 8, 0);
     for (int c = 0; c < nch; ++c)
-      for (int tap = 0; tap < 27; ++tap)
+      for (int tap = 0; tap < taps; ++tap)
         for (int nb = 0; nb < nbt; ++nb)
           for (int l = 0; l < 64; ++l)
             for (int e = 0; e < 8; ++e) {
               int ci = c * 16 + 8 * (l / 32) + e, co = nb * 32 + l % 32;
-              size_t idx = ((((size_t)c * 27 + tap) * nbt + nb) * 64 + l) * 8 + e;
+              size_t idx = ((((size_t)c * taps + tap) * nbt + nb) * 64 + l) * 8 + e;
               f[idx] = W(co, ci, tap);
             }
   }
@@ -572,12 +594,13 @@ struct StopAt {
 // the finishing kernel with its launch about 8.  (For 64 channels at 25^3
 // one unsplit launch beats two parts by 3 us; for 128 channels at 13^3 the
 // split saves 20 us.)  fp8 chunks are 32 channels with about half a bf16
-// chunk's matrix time per channel.
-pd::Split_k split_for(const Workspace& ws, const Tiling& t, int cin, int cout, int fp8) {
+// chunk's matrix time per channel; a 5x5x5 chunk has 125 taps instead of 27.
+pd::Split_k split_for(const Workspace& ws, const Tiling& t, int cin, int cout, int fp8, int ks = 3) {
   const int kch = pd::conv_hidden_chunk_channels(fp8);
   const int nch = cin / kch;
   const double wide = cout > 64 ? 1.0 : 0.0;
-  const double chunk = (2.5 + 1.4 * wide) * (fp8 ? 1.1 : 1.0), epi = 3.3 + 4.0 * wide, park = 1.75 + 1.65 * wide;
+  const double chunk = (2.5 + 1.4 * wide) * (fp8 ? 1.1 : 1.0) * (ks * ks * ks) / 27.0;
+  const double epi = 3.3 + 4.0 * wide, park = 1.75 + 1.65 * wide;
   const double finish = 8.0;
   pd::Split_k sk{0, ws.partial, ws.max_units};
   double best = nch * chunk + epi;
@@ -603,7 +626,7 @@ pd::Split_k split_for(const Workspace& ws, const Tiling& t, int cin, int cout, i
 pd_status enqueue_resnet(pd_predecoder* h, Workspace& ws, hipStream_t st, const uint64_t* det, int batch,
                          uint64_t* flips, uint64_t* residual, float* logits, hipEvent_t* ev, int stop, StopAt* at) {
   const Geom& g = h->g;
-  const int hidden_wgs = h->n_cu * pd::conv_hidden_workgroups_per_cu();
+  const int hidden_wgs = h->n_cu * pd::conv_hidden_workgroups_per_cu(3);
   int e = 0;
   auto mark = [&]() -> pd_status {
     if (ev && hipEventRecord(ev[e++], st) != hipSuccess) return PD_ERR_DEVICE;
@@ -641,12 +664,12 @@ pd_status enqueue_resnet(pd_predecoder* h, Workspace& ws, hipStream_t st, const 
         void* yq = (uint16_t*)hb + (size_t)q * cw;
         if (k == 0)
           s = check_launch(pd::launch_conv_first(g, B.c_in, cw, B.act, x, yq, B.c_mid, wq, h->bdev[2 * k] + q * cw,
-                                                 batch, 0, st));
+                                                 batch, 0, 3, st));
         else
           s = check_launch(pd::launch_conv_hidden(g, tl, B.c_in, cw, B.act, x, yq, B.c_mid, wq,
                                                   h->bdev[2 * k] + q * cw, 0, nullptr, nullptr, h->tables, ws.nib,
                                                   nullptr, batch, hidden_wgs, split_for(ws, tl, B.c_in, cw, 0), 0,
-                                                  nullptr, 0, st));
+                                                  nullptr, 0, 3, st));
       }
       if (s != PD_OK) return s;
       if (stopped(hb, B.c_mid * 2)) return PD_OK;
@@ -666,7 +689,8 @@ pd_status enqueue_resnet(pd_predecoder* h, Workspace& ws, hipStream_t st, const 
     if (last) {
       s = check_launch(pd::launch_conv_hidden(g, tl, B.c_mid, 4, 0, hb, nullptr, 0, h->wdev[2 * k + 1],
                                               h->bdev[2 * k + 1], 2, nullptr, nullptr, h->tables, ws.nib, logits,
-                                              batch, hidden_wgs, split_for(ws, tl, B.c_mid, 32, 0), 0, sc, sc_stride, st));
+                                              batch, hidden_wgs, split_for(ws, tl, B.c_mid, 32, 0), 0, sc, sc_stride, 3,
+                                              st));
     } else {
       const int nsl = B.c_out > 128 ? B.c_out / 128 : 1, cw = B.c_out / nsl;
       for (int q = 0; q < nsl && s == PD_OK; ++q) {
@@ -674,7 +698,8 @@ pd_status enqueue_resnet(pd_predecoder* h, Workspace& ws, hipStream_t st, const 
         s = check_launch(pd::launch_conv_hidden(g, tl, B.c_mid, cw, B.act, hb, (uint16_t*)yb + (size_t)q * cw,
                                                 B.c_out, wq, h->bdev[2 * k + 1] + q * cw, 4, nullptr, nullptr,
                                                 h->tables, ws.nib, nullptr, batch, hidden_wgs,
-                                                split_for(ws, tl, B.c_mid, cw, 0), 0, sc + (size_t)q * cw, sc_stride, st));
+                                                split_for(ws, tl, B.c_mid, cw, 0), 0, sc + (size_t)q * cw, sc_stride, 3,
+                                                st));
       }
     }
     if (s != PD_OK) return s;
@@ -704,9 +729,10 @@ pd_status enqueue_run(pd_predecoder* h, Workspace& ws, hipStream_t st, const uin
   const int aelem = fp8 ? 1 : 2;  // bytes per activation value (MFMA paths)
   const int n = (int)h->layers.size();
   // the last layer: a 1x1x1 head (fused into the last hidden layer's
-  // epilogue on the MFMA paths) or a 3x3x3 output layer of its own
-  const bool out3 = h->layers[n - 1].k == 3;
-  const int hidden_wgs = h->n_cu * pd::conv_hidden_workgroups_per_cu();
+  // epilogue on the MFMA paths) or a 3x3x3 (5x5x5) output layer of its own
+  const bool out3 = h->layers[n - 1].k > 1;
+  const int ks = h->ks;
+  const int hidden_wgs = h->n_cu * pd::conv_hidden_workgroups_per_cu(h->ks);
   int e = 0;
   auto mark = [&]() -> pd_status {
     if (ev && hipEventRecord(ev[e++], st) != hipSuccess) return PD_ERR_DEVICE;
@@ -744,12 +770,13 @@ pd_status enqueue_run(pd_predecoder* h, Workspace& ws, hipStream_t st, const uin
         void* yk = (char*)y + (size_t)k * cw * aelem;
         if (l == 0)
           s = check_launch(pd::launch_conv_first(g, L.c_in, cw, L.act, x, yk, L.c_out, wk, h->bdev[l] + k * cw,
-                                                 batch, fp8, st));
+                                                 batch, fp8, ks, st));
         else  // the last hidden layer may carry the head and the threshold in its epilogue
           s = check_launch(pd::launch_conv_hidden(g, tl, L.c_in, cw, L.act, x, yk, L.c_out, wk,
                                                   h->bdev[l] + k * cw * (fp8 ? 2 : 1), fuse_head ? 1 : 0,
                                                   h->head_w, h->head_b, h->tables, ws.nib, logits, batch,
-                                                  hidden_wgs, split_for(ws, tl, L.c_in, cw, fp8), fp8, nullptr, 0, st));
+                                                  hidden_wgs, split_for(ws, tl, L.c_in, cw, fp8, ks), fp8, nullptr, 0,
+                                                  ks, st));
       }
       head_done = fuse_head && l > 0;
     }
@@ -767,7 +794,8 @@ pd_status enqueue_run(pd_predecoder* h, Workspace& ws, hipStream_t st, const uin
     const pd_layer& L = h->layers[n - 1];
     s = check_launch(pd::launch_conv_hidden(g, tl, L.c_in, L.c_out, L.act, x, nullptr, 0, h->wdev[n - 1],
                                             h->bdev[n - 1], 2, nullptr, nullptr, h->tables, ws.nib, logits,
-                                            batch, hidden_wgs, split_for(ws, tl, L.c_in, 32, fp8), fp8, nullptr, 0, st));
+                                            batch, hidden_wgs, split_for(ws, tl, L.c_in, 32, fp8, ks), fp8, nullptr, 0,
+                                            ks, st));
   } else if (!head_done) {  // fp32, or a one-hidden-layer network on the paper's layout
     s = check_launch(pd::launch_head(g, h->layers[n - 1].c_in, fp32, x, h->head_w, h->head_b, h->tables,
                                      ws.nib, logits, batch, st));
@@ -856,7 +884,9 @@ pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d
     return PD_ERR_INVALID_ARG;
   if (!layer_chain_ok(layers, n_layers, o.layout)) return PD_ERR_INVALID_ARG;
   if (n_weights != predecoder_weight_count(layers, n_layers)) return PD_ERR_INVALID_ARG;
-  Geom g = make_geom(d, T, o.layout, o.first_round, o.last_round);
+  const int ks = network_ks(layers);
+  // the zero halo holds every tap of a layer: one voxel, two for 5x5x5 layers
+  Geom g = make_geom(d, T, o.layout, o.first_round, o.last_round, (ks - 1) / 2);
   if (!supported(g, layers, n_layers, dtype)) return PD_ERR_UNSUPPORTED;
   // kernels index voxels of a batch with 32-bit integers
   if ((long long)max_batch * g.V >= (1ll << 31) || (long long)max_batch * (g.Wd + g.Wf) >= (1ll << 31) ||
@@ -875,6 +905,7 @@ pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d
   h->dtype = dtype;
   h->max_batch = max_batch;
   h->layers.assign(layers, layers + n_layers);
+  h->ks = ks;
   if (hipGetDevice(&h->device) != hipSuccess ||
       hipDeviceGetAttribute(&h->n_cu, hipDeviceAttributeMultiprocessorCount, h->device) != hipSuccess ||
       h->n_cu < 1) {
@@ -886,8 +917,10 @@ pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d
   for (int i = 0; i < n_layers - 1; ++i) cmax = std::max(cmax, (int)layers[i].c_out);
   h->cmax = cmax;
   if (dtype != PD_DTYPE_FP32) {
-    h->tiling = plan_tiling(g, max_batch);
-    if (h->tiling.span <= 0 || h->tiling.span > std::min(pd::conv_single_max_span(), pd::conv_hidden_max_span())) {
+    h->tiling = plan_tiling(g, max_batch, ks);
+    const int max_span = ks == 3 ? std::min(pd::conv_single_max_span(), pd::conv_hidden_max_span(3))
+                                 : pd::conv_hidden_max_span(5);
+    if (h->tiling.span <= 0 || h->tiling.span > max_span) {
       delete h;
       return PD_ERR_UNSUPPORTED;
     }
@@ -934,13 +967,13 @@ pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d
     std::vector<uint8_t> codes;
     std::vector<float> scale, wq;
     if (dtype == PD_DTYPE_FP8) quantize_e4m3(w, L.c_out, nw / L.c_out, &codes, &scale, &wq);
-    if (i == n_layers - 1 && L.k == 3) {  // a 3x3x3 output layer: 4 filters padded to one block of 32
+    if (i == n_layers - 1 && L.k > 1) {  // a 3x3x3 (5x5x5) output layer: 4 filters padded to one block of 32
       void* wd = nullptr;
       if (dtype == PD_DTYPE_FP8) {
         std::vector<uint8_t> f = conv_fragments_fp8(codes.data(), L.c_in, L.c_out);
         s = upload(&wd, f.data(), f.size());
       } else {
-        std::vector<uint16_t> f = conv_fragments(w, L.c_in, L.c_out);
+        std::vector<uint16_t> f = conv_fragments(w, L.c_in, L.c_out, L.k);
         s = upload(&wd, f.data(), f.size() * 2);
       }
       h->wdev.push_back(wd);
@@ -998,7 +1031,7 @@ pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d
         std::vector<uint16_t> f2 = conv_fragments(wv + (size_t)128 * L.c_in * 27, L.c_in, 128);
         f.insert(f.end(), f2.begin(), f2.end());
       } else {
-        f = conv_fragments(wv, L.c_in, L.c_out);
+        f = conv_fragments(wv, L.c_in, L.c_out, L.k);
       }
       s = upload(&wd, f.data(), f.size() * 2);
     } else {
@@ -1099,7 +1132,7 @@ pd_status predecoder_create_resnet(const float* weights, size_t n_weights, int32
     return PD_ERR_DEVICE;
   }
   h->tiling = plan_tiling(g, max_batch);
-  if (h->tiling.span <= 0 || h->tiling.span > pd::conv_hidden_max_span()) {
+  if (h->tiling.span <= 0 || h->tiling.span > pd::conv_hidden_max_span(3)) {
     delete h;
     return PD_ERR_UNSUPPORTED;
   }

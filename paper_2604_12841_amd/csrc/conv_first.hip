@@ -4,16 +4,19 @@
 // activation + bf16 epilogue fused in, when it is not also the last hidden
 // layer.
 //
-// K = 27 taps x c_in channels is tiny (padded to 4 or 7 MFMA k-steps of 16),
+// K = k^3 taps x c_in channels is small (27 taps: 4 or 7 MFMA k-steps of 16;
+// 125 taps of a 5x5x5 layer with 4 channels: 32),
 // so the layer is bound by its epilogue (one activation per output value)
 // and its output write, not by the matrix cores.  It streams: each wave takes
 // a few blocks of 32 consecutive interior voxels x all c_out channels.
 //   * B operand (16 k x 32 voxels, k = c_in tap + channel): lane l gathers,
 //     for voxel l % 32, the 8 / c_in taps of its half of the k-step, each as
 //     one load of all c_in bf16 channels of a plane voxel, straight from the
-//     zero-halo planes, which stay in L2; taps past 26 contribute zero.
+//     zero-halo planes, which stay in L2; taps past the last contribute zero.
 //   * A operand: the layer's weight fragments (k-steps x c_out/32 blocks,
-//     16 bytes per lane each), staged in LDS once per workgroup.
+//     16 bytes per lane each), staged in LDS once per workgroup (a 5x5x5
+//     layer to 128 channels fills 128 KB with them, so its workgroups have
+//     two waves instead of four).
 //   * Epilogue: + bias, activation, bf16 (or, on the fp8 path, E4M3: one
 //     byte per value); the wave transposes its 32 x c_out tile through its
 //     own LDS slice and writes whole voxel rows with 16-byte stores.
@@ -33,8 +36,14 @@ typedef __attribute__((address_space(3))) const u32x4 lds_u32x4;
 typedef __attribute__((address_space(3))) u32x4 lds_u32x4_w;
 typedef __attribute__((address_space(3))) uint32_t lds_u32_w;
 
-constexpr int WAVES = 4;  // waves per workgroup
-constexpr int BPW = 2;    // 32-voxel blocks per wave on large launches (1 on small ones)
+constexpr int BPW = 2;  // 32-voxel blocks per wave on large launches (1 on small ones)
+
+// Waves per workgroup: four, two when the weight fragments of a 5x5x5 layer
+// to 128 channels (128 KB) leave LDS room for only two waves' tiles.
+template <int KS, int COUT>
+constexpr int waves() {
+  return KS == 5 && COUT == 128 ? 2 : 4;
+}
 
 // Divisors of the interior-voxel decode u -> (b, t, i, j).
 struct Decode {
@@ -52,25 +61,29 @@ __device__ __forceinline__ long long voxel_padded(const Geom& g, const Decode& d
   return padded_index(g, b, t, i, s - i * g.H);
 }
 
-// k-steps of 16 covering K = 27 c_in.
-template <int CIN>
+// k-steps of 16 covering K = KS^3 c_in.
+template <int CIN, int KS>
 constexpr int ksteps() {
-  return (27 * CIN + 15) / 16;
+  return (KS * KS * KS * CIN + 15) / 16;
 }
 
 // B fragments for this lane's voxel (padded index p): k = 16 ks + 8 half + e,
-// i.e. taps (16 ks + 8 half) / CIN + q, q < 8 / CIN, all CIN channels each.
-template <int CIN>
+// i.e. taps (16 ks + 8 half) / CIN + q, q < 8 / CIN, all CIN channels each;
+// tap (dt, di, dj) reads the voxel (dt - h, di - h, dj - h) away, h =
+// (KS - 1) / 2 (within the halo).
+template <int CIN, int KS>
 __device__ __forceinline__ void gather(const Geom& g, const void* __restrict__ planes, long long p, bool valid,
-                                       int half, u32x4 (&bx)[ksteps<CIN>()]) {
+                                       int half, u32x4 (&bx)[ksteps<CIN, KS>()]) {
   constexpr int TPF = 8 / CIN;  // taps per lane per k-step
+  constexpr int TAPS = KS * KS * KS, HW = (KS - 1) / 2;
 #pragma unroll
-  for (int ks = 0; ks < ksteps<CIN>(); ++ks)
+  for (int ks = 0; ks < ksteps<CIN, KS>(); ++ks)
 #pragma unroll
     for (int q = 0; q < TPF; ++q) {
-      const int tap = (16 * ks + 8 * half) / CIN + q;  // >= 27 only in the last k-step
-      const long long at = p + (long long)(tap / 9 - 1) * g.P + (long long)((tap / 3) % 3 - 1) * g.Wp + (tap % 3 - 1);
-      const bool in = valid && tap < 27;
+      const int tap = (16 * ks + 8 * half) / CIN + q;  // >= TAPS only in the last k-step
+      const int dt = tap / (KS * KS), di = (tap / KS) % KS, dj = tap % KS;
+      const long long at = p + (long long)(dt - HW) * g.P + (long long)(di - HW) * g.Wp + (dj - HW);
+      const bool in = valid && tap < TAPS;
       if constexpr (CIN == 2) {
         bx[ks][q] = in ? reinterpret_cast<const uint32_t*>(planes)[at] : 0u;
       } else {
@@ -85,17 +98,18 @@ __device__ __forceinline__ void gather(const Geom& g, const void* __restrict__ p
 // then handles bpw consecutive work units: a unit is a 32-voxel block and,
 // with hsplit = 2 (small launches, c_out = 128), one half of its channels.
 // F8: y holds E4M3 codes.
-template <int CIN, int COUT, int ACT, bool F8>
-__global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, const void* __restrict__ planes,
-                                                                void* __restrict__ y, int ystride,
-                                                                const u32x4* __restrict__ wfrag,
-                                                                const float* __restrict__ bias, Decode dc,
-                                                                int nvox, int bpw, int hsplit) {
+template <int CIN, int COUT, int ACT, bool F8, int KSZ>
+__global__ void __launch_bounds__((64 * waves<KSZ, COUT>())) conv_first_kernel(Geom g, const void* __restrict__ planes,
+                                                                          void* __restrict__ y, int ystride,
+                                                                          const u32x4* __restrict__ wfrag,
+                                                                          const float* __restrict__ bias, Decode dc,
+                                                                          int nvox, int bpw, int hsplit) {
+  constexpr int WAVES = waves<KSZ, COUT>();
   constexpr int NB = COUT / 32;
   constexpr int ESZ = F8 ? 1 : 2;        // bytes per output value
   constexpr int OSTR = COUT * ESZ + 16;  // padded LDS row stride (bytes)
   constexpr int GPR = COUT * ESZ / 16;   // 16-byte granules per voxel row
-  constexpr int KS = ksteps<CIN>();
+  constexpr int KS = ksteps<CIN, KSZ>();
   constexpr int WFR = KS * NB * 64;    // weight fragments x lanes (16 bytes each)
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -116,7 +130,7 @@ __global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, const vo
     const bool valid = u0 + l32 < nvox;
     const long long p = valid ? voxel_padded(g, dc, u0 + l32) : -1;
     u32x4 bx[KS];
-    gather<CIN>(g, planes, p, valid, half, bx);
+    gather<CIN, KSZ>(g, planes, p, valid, half, bx);
     if (half == 0) ((__attribute__((address_space(3))) int*)prow)[l32] = (int)p;
     // channel halves of 64 (NH blocks of 32) one after the other: fewer
     // live accumulators, more waves per SIMD to hide the gathers
@@ -180,8 +194,11 @@ __global__ void __launch_bounds__(64 * WAVES) conv_first_kernel(Geom g, const vo
 }  // namespace
 
 hipError_t launch_conv_first(const Geom& g, int cin, int cout, int act, const void* planes, void* y, int ystride,
-                             const void* wfrag, const float* bias, int batch, int fp8, hipStream_t stream) {
+                             const void* wfrag, const float* bias, int batch, int fp8, int ks, hipStream_t stream) {
   const long long nvox = (long long)batch * g.V;  // < 2^31 (host check)
+  if ((cin != 2 && cin != 4) || (cout != 64 && cout != 128) || act < 0 || act > 2) return hipErrorInvalidValue;
+  if ((ks != 3 && ks != 5) || (ks - 1) / 2 > g.pad || (ks == 5 && (cin != 4 || fp8))) return hipErrorInvalidValue;
+  const int WAVES = ks == 5 && cout == 128 ? 2 : 4;
   // two blocks per wave amortise the weight staging once the launch has
   // 512 or more workgroups of them; below that (small batches) one block per
   // wave doubles the waves on a mostly idle chip
@@ -194,28 +211,43 @@ hipError_t launch_conv_first(const Geom& g, int cin, int cout, int act, const vo
   dc.by_v = make_fastdiv((uint32_t)g.V);
   dc.by_hh = make_fastdiv((uint32_t)(g.H * g.H));
   dc.by_h = make_fastdiv((uint32_t)g.H);
-  auto launch = [&](auto CI, auto CO, auto A) {
-    constexpr int C = decltype(CO)::value, I = decltype(CI)::value;
-    const size_t lds = (size_t)ksteps<I>() * (C / 32) * 64 * 16 + (size_t)WAVES * 32 * (C * 2 + 16 + 4);
-    if (fp8)
-      hipLaunchKernelGGL((conv_first_kernel<I, C, decltype(A)::value, true>), dim3((unsigned)nblk),
-                         dim3(64 * WAVES), lds, stream, g, planes, y, ystride, (const u32x4*)wfrag, bias, dc,
-                         (int)nvox, bpw, hsplit);
-    else
-      hipLaunchKernelGGL((conv_first_kernel<I, C, decltype(A)::value, false>), dim3((unsigned)nblk),
-                         dim3(64 * WAVES), lds, stream, g, planes, y, ystride, (const u32x4*)wfrag, bias, dc,
-                         (int)nvox, bpw, hsplit);
+  auto launch = [&](auto CI, auto CO, auto A, auto K) {
+    constexpr int C = decltype(CO)::value, I = decltype(CI)::value, KZ = decltype(K)::value;
+    constexpr int W = waves<KZ, C>();
+    const size_t lds = (size_t)ksteps<I, KZ>() * (C / 32) * 64 * 16 + (size_t)W * 32 * (C * 2 + 16 + 4);
+    static_assert(ksteps<I, KZ>() * (C / 32) * 64 * 16 + W * 32 * (C * 2 + 16 + 4) <= 160 * 1024, "LDS");
+    if constexpr (KZ == 5) {  // bf16 only; more than 64 KB of LDS
+      if (hipFuncSetAttribute((const void*)conv_first_kernel<I, C, decltype(A)::value, false, KZ>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+        return;
+      hipLaunchKernelGGL((conv_first_kernel<I, C, decltype(A)::value, false, KZ>), dim3((unsigned)nblk),
+                         dim3(64 * W), lds, stream, g, planes, y, ystride, (const u32x4*)wfrag, bias, dc, (int)nvox,
+                         bpw, hsplit);
+    } else if (fp8) {
+      hipLaunchKernelGGL((conv_first_kernel<I, C, decltype(A)::value, true, KZ>), dim3((unsigned)nblk), dim3(64 * W),
+                         lds, stream, g, planes, y, ystride, (const u32x4*)wfrag, bias, dc, (int)nvox, bpw, hsplit);
+    } else {
+      hipLaunchKernelGGL((conv_first_kernel<I, C, decltype(A)::value, false, KZ>), dim3((unsigned)nblk),
+                         dim3(64 * W), lds, stream, g, planes, y, ystride, (const u32x4*)wfrag, bias, dc, (int)nvox,
+                         bpw, hsplit);
+    }
   };
-  if ((cin != 2 && cin != 4) || (cout != 64 && cout != 128) || act < 0 || act > 2) return hipErrorInvalidValue;
   with_activation(act, [&](auto A) {
     using I2 = std::integral_constant<int, 2>;
     using I4 = std::integral_constant<int, 4>;
     using C64 = std::integral_constant<int, 64>;
     using C128 = std::integral_constant<int, 128>;
-    if (cin == 2 && cout == 64) launch(I2(), C64(), A);
-    if (cin == 2 && cout == 128) launch(I2(), C128(), A);
-    if (cin == 4 && cout == 64) launch(I4(), C64(), A);
-    if (cin == 4 && cout == 128) launch(I4(), C128(), A);
+    using K3 = std::integral_constant<int, 3>;
+    using K5 = std::integral_constant<int, 5>;
+    if (ks == 3) {
+      if (cin == 2 && cout == 64) launch(I2(), C64(), A, K3());
+      if (cin == 2 && cout == 128) launch(I2(), C128(), A, K3());
+      if (cin == 4 && cout == 64) launch(I4(), C64(), A, K3());
+      if (cin == 4 && cout == 128) launch(I4(), C128(), A, K3());
+    } else {
+      if (cout == 64) launch(I4(), C64(), A, K5());
+      if (cout == 128) launch(I4(), C128(), A, K5());
+    }
   });
   return hipGetLastError();
 }

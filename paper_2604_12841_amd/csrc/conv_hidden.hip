@@ -63,38 +63,55 @@ typedef __attribute__((address_space(3))) u32x2 lds_u32x2_w;
 
 constexpr int NT = 256;       // threads per workgroup: 4 wave64
 constexpr int KC = 16;        // input channels per LDS chunk (one MFMA k-step)
-constexpr int STEPS = 27;     // k-steps per chunk: one per tap
-constexpr int BRING = 3;      // weight-fragment ring depth (prefetch distance BRING - 1)
 constexpr int VSTRIDE = 48;   // LDS bytes per staged voxel (32 of channels + 16 of padding)
-constexpr int BUF_VOX = 800;            // staged voxels a staging buffer holds
-constexpr int MAX_SPAN = BUF_VOX - 1;    // staged voxels per tile (the last slot takes overflow writes)
-// Every chunk is staged with RMAX rounds of NT 16-byte granules, stored
-// unconditionally (a conditional store would let the compiler sink the load
-// next to it): granules past the footprint load zeros into slots past the
-// footprint, and granules past the buffer all go to its last slot.
-constexpr int RMAX = 7;
-static_assert(RMAX * NT >= 2 * MAX_SPAN && (RMAX * NT) % 32 == 0, "staging rounds cover the largest footprint");
-static_assert(STEPS % BRING == 0, "the weight ring lines up with chunk boundaries");
-static_assert(RMAX * 3 + 3 <= STEPS, "staging rounds fit in a chunk");
-constexpr int ABUF = BUF_VOX * VSTRIDE;  // bytes per staging buffer
+
+// Per kernel size KS (3 or 5): the k-steps of a bf16 chunk (one per tap), the
+// weight-fragment ring depth (prefetch distance RING - 1; it divides the
+// k-steps of a chunk so that ring slots line up with chunk boundaries), the
+// staged voxels a staging buffer holds (the last slot takes overflow writes)
+// and the workgroups per CU.  KS = 3: two workgroups per CU, so each SIMD
+// runs one wave of each and one workgroup's epilogue, barriers and staging
+// stalls overlap the other's matrix work.  KS = 5: a 256-voxel tile's halo
+// of two makes its footprint about 4.5 times the tile (a 4 x 8 x 8 box
+// stages 8 x 12 x 12 voxels), so one workgroup per CU with larger staging
+// buffers; its 125-step chunks keep the matrix pipe busy between barriers.
+template <int KS>
+struct Conv {
+  static constexpr int TAPS = KS * KS * KS;
+  static constexpr int BRING = KS == 3 ? 3 : 5;
+  static constexpr int BUF_VOX = KS == 3 ? 800 : 1600;
+  static constexpr int MAX_SPAN = BUF_VOX - 1;
+  static constexpr int WG_PER_CU = KS == 3 ? 2 : 1;
+  // Every chunk is staged with RMAX rounds of NT 16-byte granules, stored
+  // unconditionally (a conditional store would let the compiler sink the
+  // load next to it): granules past the footprint load zeros into slots
+  // past the footprint, and granules past the buffer all go to its last
+  // slot.
+  static constexpr int RMAX = (2 * MAX_SPAN + NT - 1) / NT;
+  static constexpr int ABUF = BUF_VOX * VSTRIDE;  // bytes per staging buffer
+  static_assert(RMAX * NT >= 2 * MAX_SPAN && (RMAX * NT) % 32 == 0, "staging rounds cover the largest footprint");
+  static_assert(TAPS % BRING == 0, "the weight ring lines up with chunk boundaries");
+  static_assert(RMAX * 3 + 3 <= TAPS, "staging rounds fit in a chunk");
+};
 
 // The fp8 (E4M3) variant keeps the 32 staged bytes per voxel and chunk, now
 // 32 channels, and runs v_mfma_f32_32x32x64_f8f6f4: k = 64 is two taps x 32
 // channels, the first half-wave's lanes holding a voxel's 32 channels at tap
-// 2 s, the second half-wave's at tap 2 s + 1 (tap 27 does not exist: its
-// weights are zero).  14 k-steps per chunk; staging round k loads at step
-// 2 k and stores at step 2 k + 2 (the last one after the chunk's last
-// step); the weight ring is 2 deep (32 bytes per lane and block).
-template <bool F8>
+// 2 s, the second half-wave's at tap 2 s + 1 (the tap past the last does not
+// exist: its weights are zero).  ceil(taps / 2) k-steps per chunk (14 for
+// 3x3x3); staging round k loads at step 2 k and stores at step 2 k + 2 (the
+// last one after the chunk's last step); the weight ring is 2 deep (32
+// bytes per lane and block).
+template <bool F8, int KS>
 struct Prec {
-  static constexpr int KCH = F8 ? 32 : KC;        // input channels per chunk
-  static constexpr int NSTEP = F8 ? 14 : STEPS;   // k-steps per chunk
-  static constexpr int RING = F8 ? 2 : BRING;     // weight ring depth
+  static constexpr int KCH = F8 ? 32 : KC;                                  // input channels per chunk
+  static constexpr int NSTEP = F8 ? (Conv<KS>::TAPS + 1) / 2 : Conv<KS>::TAPS;  // k-steps per chunk
+  static constexpr int RING = F8 ? (KS == 3 ? 2 : 3) : Conv<KS>::BRING;     // weight ring depth
   static constexpr int SG = F8 ? 2 : 3;           // steps between staging rounds
   static constexpr int ESZ = F8 ? 1 : 2;          // bytes per activation value
   static constexpr int WFRAG = F8 ? 2048 : 1024;  // bytes of one weight fragment (64 lanes)
   static_assert(NSTEP % RING == 0, "the weight ring lines up with chunk boundaries");
-  static_assert(SG * (RMAX - 1) < NSTEP, "staging rounds load within a chunk");
+  static_assert(SG * (Conv<KS>::RMAX - 1) < NSTEP, "staging rounds load within a chunk");
   static_assert(KCH * ESZ == 32, "a chunk stages 32 bytes per voxel");
 };
 
@@ -106,9 +123,11 @@ __host__ __device__ inline int stage_gran(int q) { return (q >> 4) & 1; }
 
 // LDS byte (relative to a staging buffer) of staging granule q; voxels past
 // the buffer all go to its last slot.
+template <int KS>
 __host__ __device__ inline int stage_slot(int q) {
+  constexpr int BV = Conv<KS>::BUF_VOX;
   const int v = stage_voxel(q);
-  return (v < BUF_VOX - 1 ? v : BUF_VOX - 1) * VSTRIDE + stage_gran(q) * 16;
+  return (v < BV - 1 ? v : BV - 1) * VSTRIDE + stage_gran(q) * 16;
 }
 
 // Epilogue modes: the activations of a hidden layer, a hidden layer with the
@@ -141,14 +160,15 @@ struct Split {
 // per-channel weight scales [COUT] (fp8) and the head weights [4][COUT].
 // The head epilogue puts its partial sums in the staging buffer the tile
 // read last.
-template <int COUT>
+template <int COUT, int KS>
 struct Lds {
+  static constexpr int ABUF = Conv<KS>::ABUF;
   static constexpr int zero = 2 * ABUF;
   static constexpr int bias = zero + 512;
   static constexpr int headw = bias + 2 * COUT * 4;
   static constexpr int total = headw + 4 * COUT * 4;
   static_assert(zero % 256 == 0, "zero region must be 256-aligned");
-  static_assert(2 * total <= 160 * 1024, "two workgroups per CU");
+  static_assert(Conv<KS>::WG_PER_CU * total <= 160 * 1024, "the workgroups of a CU fit its LDS");
   static_assert(Split<COUT>::WN * kTileRows * 4 * 4 <= ABUF, "head partials fit a staging buffer");
   static_assert((NT / 64) * 64 * 128 <= ABUF, "epilogue transposition slices fit a staging buffer");
 };
@@ -200,23 +220,27 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t stage_rsrc(const void* x, long
 }
 
 // F8: E4M3 activations and weights (bias holds [COUT] biases then [COUT]
-// per-channel weight scales; y and x hold one byte per value).
-template <int CIN, int COUT, int EPI, int MODE, bool F8>
-__global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
+// per-channel weight scales; y and x hold one byte per value).  KS: the
+// kernel size, 3 or 5 (5: box tiles on a halo of two).
+template <int CIN, int COUT, int EPI, int MODE, bool F8, int KS>
+__global__ void __launch_bounds__(NT)
+__attribute__((amdgpu_waves_per_eu(Conv<KS>::WG_PER_CU, Conv<KS>::WG_PER_CU)))
 conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void* __restrict__ y,
                    int ystride, const u32x4* __restrict__ wfrag, const float* __restrict__ bias,
                    const float* __restrict__ head_w, const float* __restrict__ head_b,
                    const int32_t* __restrict__ tables, uint8_t* __restrict__ nib,
                    float* __restrict__ logits, int batch, int kshift_arg, float* __restrict__ partial,
                    const uint16_t* __restrict__ sc, int sc_stride) {
+  static_assert(KS == 3 || MODE == 1, "5x5x5 layers run on box tiles");
   extern __shared__ __attribute__((aligned(16))) char smem[];
   using W = Split<COUT>;
-  using L = Lds<COUT>;
+  using L = Lds<COUT, KS>;
   constexpr int MB = W::MB;
   constexpr int NB = W::NB;
   constexpr int NBT = COUT / 32;  // 32-channel blocks in total
-  using P = Prec<F8>;
+  using P = Prec<F8, KS>;
   constexpr int KCH = P::KCH, NSTEP = P::NSTEP, RING = P::RING, SG = P::SG;
+  constexpr int RMAX = Conv<KS>::RMAX, ABUF = L::ABUF, TAPS = Conv<KS>::TAPS;
   constexpr int ROW = CIN * P::ESZ;  // bytes per input voxel row
   constexpr int NCHUNK = CIN / KCH;
   constexpr int TSTEPS = NCHUNK * NSTEP;  // k-steps of the layer
@@ -464,7 +488,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
 #pragma unroll
     for (int k = 0; k < RMAX; ++k) {
       const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(rs, soff[k], 0, 0);
-      *(lds_u32x4_w*)(lds + stage_slot(k * NT + tid)) = v;
+      *(lds_u32x4_w*)(lds + stage_slot<KS>(k * NT + tid)) = v;
     }
   }
 
@@ -548,7 +572,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
       // LDS offset of tap `tap` relative to a row's (0,0,0) tap, and the
       // mask that sends a halo-column tap of a flat tile to `zero`
       auto tap_off = [&](int tap) -> uint32_t {
-        const int dt = tap / 9, di = (tap / 3) % 3, dj = tap % 3;
+        const int dt = tap / (KS * KS), di = (tap / KS) % KS, dj = tap % KS;
         return (uint32_t)((dt * tl.sa + di * tl.sb + dj) * VSTRIDE);
       };
       auto tap_mask = [&](int mb, int tap) -> uint32_t {
@@ -576,7 +600,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
           // hoisted out of the chunk loop (it would hold 14 x 4 registers)
           uint32_t hm = hmask;
           asm volatile("" : "+v"(hm));
-          const int t0 = 2 * st, t1 = 2 * st + 1 < 27 ? 2 * st + 1 : 2 * st;  // tap 27: zero weights
+          const int t0 = 2 * st, t1 = 2 * st + 1 < TAPS ? 2 * st + 1 : 2 * st;  // the tap past the last: zero weights
           const uint32_t o0 = tap_off(t0), o1 = tap_off(t1);
           uint32_t a = rbase[mb] + o0 + ((o1 - o0) & hm);
           if (MODE == 0) {
@@ -638,7 +662,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
         // used (transposition or head partials): wait for every wave to
         // leave it
         if (k == 0 && chunk == 0) __builtin_amdgcn_s_barrier();
-        *(lds_u32x4_w*)(oth + stage_slot(k * NT + tid)) = stg;
+        *(lds_u32x4_w*)(oth + stage_slot<KS>(k * NT + tid)) = stg;
       };
 #pragma unroll
       for (int st = 0; st < NSTEP; ++st) {
@@ -837,40 +861,42 @@ __global__ void __launch_bounds__(256) split_finish_kernel(Geom g, Tiling tl, in
 
 // Launches one instance of the hidden kernel (the LDS size attribute set on
 // its first use).
-template <int CIN, int COUT, int EPI, int MODE, bool F8>
+template <int CIN, int COUT, int EPI, int MODE, bool F8, int KS>
 hipError_t launch_hidden(const Geom& g, const Tiling& tl, int act, const void* x, void* y, int ystride,
                          const void* wfrag, const float* bias, const float* head_w, const float* head_b,
                          const int32_t* tables, uint8_t* nib, float* logits, int batch, int n_workgroups,
                          int kshift, float* partial, const uint16_t* sc, int sc_stride, hipStream_t stream) {
+  using L = Lds<COUT, KS>;
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)conv_hidden_kernel<CIN, COUT, EPI, MODE, F8>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, Lds<COUT>::total);
+    hipError_t e = hipFuncSetAttribute((const void*)conv_hidden_kernel<CIN, COUT, EPI, MODE, F8, KS>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, L::total);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
   const long long nwg = conv_workgroups(tl.ntiles << kshift, n_workgroups);
-  hipLaunchKernelGGL((conv_hidden_kernel<CIN, COUT, EPI, MODE, F8>), dim3((unsigned)nwg), dim3(NT),
-                     (size_t)Lds<COUT>::total, stream, g, tl, act, x, y, ystride, (const u32x4*)wfrag, bias, head_w,
+  hipLaunchKernelGGL((conv_hidden_kernel<CIN, COUT, EPI, MODE, F8, KS>), dim3((unsigned)nwg), dim3(NT),
+                     (size_t)L::total, stream, g, tl, act, x, y, ystride, (const u32x4*)wfrag, bias, head_w,
                      head_b, tables, nib, logits, batch, kshift, partial, sc, sc_stride);
   return hipSuccess;
 }
 
-template <int CIN, int COUT, int EPI, int MODE, bool F8>
+template <int CIN, int COUT, int EPI, int MODE, bool F8, int KS>
 hipError_t launch_one(const Geom& g, const Tiling& tl, int act, const void* x, void* y, int ystride,
                       const void* wfrag, const float* bias, const float* head_w, const float* head_b,
                       const int32_t* tables, uint8_t* nib, float* logits, int batch, int n_workgroups,
                       const Split_k& sk, const uint16_t* sc, int sc_stride, hipStream_t stream) {
   hipError_t e;
   if (sk.kshift == 0) {
-    e = launch_hidden<CIN, COUT, EPI, MODE, F8>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b, tables,
-                                                nib, logits, batch, n_workgroups, 0, nullptr, sc, sc_stride, stream);
+    e = launch_hidden<CIN, COUT, EPI, MODE, F8, KS>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b,
+                                                    tables, nib, logits, batch, n_workgroups, 0, nullptr, sc,
+                                                    sc_stride, stream);
     return e != hipSuccess ? e : hipGetLastError();
   }
   // K loops split: park the parts, then add them and finish the tiles
-  e = launch_hidden<CIN, COUT, EPI_PARK, MODE, F8>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b, tables,
-                                                   nib, logits, batch, n_workgroups, sk.kshift, sk.partial, nullptr,
-                                                   0, stream);
+  e = launch_hidden<CIN, COUT, EPI_PARK, MODE, F8, KS>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b,
+                                                       tables, nib, logits, batch, n_workgroups, sk.kshift,
+                                                       sk.partial, nullptr, 0, stream);
   if (e != hipSuccess) return e;
   const long long threads =
       tl.ntiles * kTileRows * (EPI == EPI_ACT || EPI == EPI_ADD || EPI == EPI_HEAD ? COUT / 8 : 1);
@@ -887,17 +913,24 @@ template <bool F8>
 hipError_t launch_case(const Geom& g, const Tiling& tl, int cin, int cout, int act, const void* x, void* y,
                        int ystride, const void* wfrag, const float* bias, int head, const float* head_w,
                        const float* head_b, const int32_t* tables, uint8_t* nib, float* logits, int batch,
-                       int n_workgroups, const Split_k& sk, const uint16_t* sc, int sc_stride, hipStream_t stream) {
-#define PD_HIDDEN_CASE(CI, CO, E)                                                                  \
-  if (cin == CI && cout == CO && head == E) {                                                     \
-    if (tl.mode == 0)                                                                              \
-      return launch_one<CI, CO, E, 0, F8>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b, \
-                                          tables, nib, logits, batch, n_workgroups, sk, sc,        \
-                                          sc_stride, stream);                                       \
-    return launch_one<CI, CO, E, 1, F8>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b,   \
-                                        tables, nib, logits, batch, n_workgroups, sk, sc,          \
-                                        sc_stride, stream);                                         \
+                       int n_workgroups, const Split_k& sk, const uint16_t* sc, int sc_stride, int ks,
+                       hipStream_t stream) {
+#define PD_HIDDEN_CASE(CI, CO, E)                                                                      \
+  if (ks == 3 && cin == CI && cout == CO && head == E) {                                              \
+    if (tl.mode == 0)                                                                                  \
+      return launch_one<CI, CO, E, 0, F8, 3>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b,  \
+                                             tables, nib, logits, batch, n_workgroups, sk, sc,          \
+                                             sc_stride, stream);                                         \
+    return launch_one<CI, CO, E, 1, F8, 3>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b,    \
+                                           tables, nib, logits, batch, n_workgroups, sk, sc, sc_stride, \
+                                           stream);                                                      \
   }
+// 5x5x5 layers (Model 3 of Table models): box tiles only
+#define PD_HIDDEN_CASE5(CI, CO, E)                                                                     \
+  if (ks == 5 && cin == CI && cout == CO && head == E && tl.mode == 1)                                \
+    return launch_one<CI, CO, E, 1, F8, 5>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b,    \
+                                           tables, nib, logits, batch, n_workgroups, sk, sc, sc_stride, \
+                                           stream);
   PD_HIDDEN_CASE(64, 64, EPI_ACT)
   PD_HIDDEN_CASE(128, 128, EPI_ACT)
   PD_HIDDEN_CASE(64, 128, EPI_ACT)
@@ -908,11 +941,18 @@ hipError_t launch_case(const Geom& g, const Tiling& tl, int cin, int cout, int a
   PD_HIDDEN_CASE(128, 128, EPI_HEAD)
   PD_HIDDEN_CASE(64, 128, EPI_HEAD)
   PD_HIDDEN_CASE(128, 64, EPI_HEAD)
+  if constexpr (!F8) {
+    PD_HIDDEN_CASE5(64, 64, EPI_ACT)
+    PD_HIDDEN_CASE5(128, 128, EPI_ACT)
+  }
   if (cout == 4) cout = 32;  // the output layer's 4 filters fill one padded block
   PD_HIDDEN_CASE(64, 32, EPI_OUT)
   PD_HIDDEN_CASE(128, 32, EPI_OUT)
   PD_HIDDEN_CASE(256, 32, EPI_OUT)
-  if constexpr (!F8) {  // the residual network's layers (bf16)
+  if constexpr (!F8) {
+    PD_HIDDEN_CASE5(64, 32, EPI_OUT)
+    PD_HIDDEN_CASE5(128, 32, EPI_OUT)
+    // the residual network's layers (bf16)
     PD_HIDDEN_CASE(512, 32, EPI_OUT)
     PD_HIDDEN_CASE(512, 128, EPI_ACT)
     PD_HIDDEN_CASE(64, 64, EPI_ADD)
@@ -921,33 +961,37 @@ hipError_t launch_case(const Geom& g, const Tiling& tl, int cin, int cout, int a
     PD_HIDDEN_CASE(512, 128, EPI_ADD)
   }
 #undef PD_HIDDEN_CASE
+#undef PD_HIDDEN_CASE5
   return hipErrorInvalidValue;
 }
 
 }  // namespace
 
-int conv_hidden_max_span() { return MAX_SPAN; }
+int conv_hidden_max_span(int ks) { return ks == 5 ? Conv<5>::MAX_SPAN : Conv<3>::MAX_SPAN; }
 size_t conv_hidden_partial_floats_per_unit() { return (size_t)kTileRows * 128; }
-int conv_hidden_workgroups_per_cu() { return 2; }
+int conv_hidden_workgroups_per_cu(int ks) { return ks == 5 ? Conv<5>::WG_PER_CU : Conv<3>::WG_PER_CU; }
 
 hipError_t launch_conv_hidden(const Geom& g, const Tiling& tl, int cin, int cout, int act, const void* x,
                               void* y, int ystride, const void* wfrag, const float* bias, int head,
                               const float* head_w, const float* head_b, const int32_t* tables, uint8_t* nib,
                               float* logits, int batch, int n_workgroups, const Split_k& sk, int fp8,
-                              const uint16_t* sc, int sc_stride, hipStream_t stream) {
-  if (tl.span <= 0 || tl.span > MAX_SPAN) return hipErrorInvalidValue;
+                              const uint16_t* sc, int sc_stride, int ks, hipStream_t stream) {
+  if (ks != 3 && ks != 5) return hipErrorInvalidValue;
+  if (tl.span <= 0 || tl.span > conv_hidden_max_span(ks)) return hipErrorInvalidValue;
+  // the halo holds every tap: a 5x5x5 layer needs the two-voxel halo (and box tiles)
+  if ((ks - 1) / 2 > g.pad || (tl.mode == 0 && g.pad != 1)) return hipErrorInvalidValue;
   // parts per tile: a power of two dividing the layer's chunks, with room
   // for every unit's sums
-  const int nchunk = cin / (fp8 ? Prec<true>::KCH : Prec<false>::KCH);
+  const int nchunk = cin / (fp8 ? Prec<true, 3>::KCH : Prec<false, 3>::KCH);
   if (sk.kshift < 0 || nchunk % (1 << sk.kshift) != 0 || (sk.kshift > 0 && (tl.ntiles << sk.kshift) > sk.max_units))
     return hipErrorInvalidValue;
   if (fp8)
     return launch_case<true>(g, tl, cin, cout, act, x, y, ystride, wfrag, bias, head, head_w, head_b, tables, nib,
-                             logits, batch, n_workgroups, sk, sc, sc_stride, stream);
+                             logits, batch, n_workgroups, sk, sc, sc_stride, ks, stream);
   return launch_case<false>(g, tl, cin, cout, act, x, y, ystride, wfrag, bias, head, head_w, head_b, tables, nib,
-                            logits, batch, n_workgroups, sk, sc, sc_stride, stream);
+                            logits, batch, n_workgroups, sk, sc, sc_stride, ks, stream);
 }
 
-int conv_hidden_chunk_channels(int fp8) { return fp8 ? Prec<true>::KCH : Prec<false>::KCH; }
+int conv_hidden_chunk_channels(int fp8) { return fp8 ? Prec<true, 3>::KCH : Prec<false, 3>::KCH; }
 
 }  // namespace pd

@@ -11,15 +11,17 @@
 
 namespace pd {
 
-// Padded activation layout (NTHWC with a one-voxel zero halo in t, i and j;
-// H = d + 1 on the plaquette grid, d on the paper layout):
+// Padded activation layout (NTHWC with a zero halo of `pad` voxels in t, i
+// and j -- 1, or 2 for a network with 5x5x5 layers; H = d + 1 on the
+// plaquette grid, d on the paper layout):
 //   voxel (b, t, i, j), 0 <= t < T, 0 <= i, j < H, lives at padded index
-//   b * S + (t + 1) * P + (i + 1) * Wp + (j + 1),  Wp = H + 2, P = Wp^2,
-//   S = (T + 2) * P,
+//   b * S + (t + pad) * P + (i + pad) * Wp + (j + pad),  Wp = H + 2 pad,
+//   P = Wp^2, S = (T + 2 pad) * P,
 // channels contiguous.  The halo is zeroed once at create and never written,
-// so a 3x3x3 tap is a pure index shift.
+// so a k x k x k tap (k <= 2 pad + 1) is a pure index shift.
 struct Geom {
   int d, T, H, Wp, P;
+  int pad;      // halo width
   long long S;  // padded voxels per sample
   int V;        // interior voxels per sample, T * H * H
   int K;        // stabilizers of each type, (d^2 - 1) / 2
@@ -38,7 +40,7 @@ struct Geom {
 };
 
 __host__ __device__ inline long long padded_index(const Geom& g, int b, int t, int i, int j) {
-  return (long long)b * g.S + (long long)(t + 1) * g.P + (long long)(i + 1) * g.Wp + (j + 1);
+  return (long long)b * g.S + (long long)(t + g.pad) * g.P + (long long)(i + g.pad) * g.Wp + (j + g.pad);
 }
 
 // Output-row tiling of one conv launch.  A tile is up to 256 output voxels:
@@ -52,9 +54,11 @@ __host__ __device__ inline long long padded_index(const Geom& g, int b, int t, i
 //    consecutive staged voxels.  The zero halo columns are not staged: a tap
 //    that falls on one reads a zero region instead.  The staged span runs
 //    from u(first row) - (PU + H + 1) to u(last row) + (PU + H + 1).
+//    (Mode 0 needs pad = 1.)
 //  mode 1 (box): a BT x BI x BJ box of (t, i, j); the staged input is the
-//    (BT+2) x (BI+2) x (BJ+2) padded box around it, halo included.
-// In both modes the LDS voxel of row r for tap (dt, di, dj) in {0,1,2}^3 is
+//    (BT+2 pad) x (BI+2 pad) x (BJ+2 pad) padded box around it, halo
+//    included.
+// In both modes the LDS voxel of row r for tap (dt, di, dj) in {0..k-1}^3 is
 // row_base(r) + dt * sa + di * sb + dj.
 // Division by a runtime constant d >= 2 for numerators n < 2^31:
 // q = mulhi(n, m) >> s with s = ceil(log2 d) - 1, m = floor(2^(32+s) / d) + 1.
@@ -132,8 +136,9 @@ hipError_t launch_unpack(const Geom& g, const int32_t* tables, const uint64_t* d
 // fp8: y holds E4M3 codes (one byte per value; the planes and the bf16
 // weight fragments are unchanged, the weights being E4M3 values times their
 // power-of-two scales, which bf16 represents exactly).
+// ks: kernel size 3, or 5 (c_in = 4, bf16, a halo of two).
 hipError_t launch_conv_first(const Geom& g, int cin, int cout, int act, const void* planes, void* y,
-                             int ystride, const void* wfrag, const float* bias, int batch, int fp8,
+                             int ystride, const void* wfrag, const float* bias, int batch, int fp8, int ks,
                              hipStream_t stream);
 
 // A network with one hidden layer: layer 1 (as launch_conv_first) with the
@@ -176,15 +181,17 @@ struct Split_k {
   long long max_units;
 };
 
+// ks: kernel size 3, or 5 (box tiles, a halo of two; bf16 c_in / c_out of
+// 64 or 128, activations and the output layer).
 hipError_t launch_conv_hidden(const Geom& g, const Tiling& tl, int cin, int cout, int act, const void* x,
                               void* y, int ystride, const void* wfrag, const float* bias, int head,
                               const float* head_w, const float* head_b, const int32_t* tables, uint8_t* nib,
                               float* logits, int batch, int n_workgroups, const Split_k& sk, int fp8,
-                              const uint16_t* sc, int sc_stride, hipStream_t stream);
-int conv_hidden_max_span();
+                              const uint16_t* sc, int sc_stride, int ks, hipStream_t stream);
+int conv_hidden_max_span(int ks);         // staged voxels a tile may need
 int conv_hidden_chunk_channels(int fp8);  // input channels per K-loop chunk
 size_t conv_hidden_partial_floats_per_unit();
-int conv_hidden_workgroups_per_cu();
+int conv_hidden_workgroups_per_cu(int ks);
 
 // Copies the interior voxel rows (row_bytes each, a multiple of 8) of a
 // zero-halo activation buffer to out [batch][T][H][H] rows.

@@ -56,7 +56,7 @@ __host__ __device__ inline bool tile_row(const Geom& g, const Tiling& tl, int ti
     const int c = (int)fdiv((uint32_t)ra, tl.dv_bj), e = ra - c * tl.BJ;
     const int t = t0 + a, i = i0 + c, j = j0 + e;
     const bool ok = (r < tl.BT * bij) && t < g.T && i < g.H && j < g.H;
-    *lds_base = ok ? (a * (tl.BI + 2) + c) * (tl.BJ + 2) + e : 0;
+    *lds_base = ok ? (a * (tl.BI + 2 * g.pad) + c) * (tl.BJ + 2 * g.pad) + e : 0;
     if (col) *col = ok ? j : -1;
     if (!ok) return false;
     *pidx = padded_index(g, b, t, i, j);
@@ -121,12 +121,12 @@ __host__ __device__ inline long long staged_voxel(const Geom& g, const Tiling& t
     const long long p = line_to_padded(g, origin + vv);
     return (p < limit) ? p : 0;
   }
-  const int bj2 = tl.BJ + 2, bij2 = (tl.BI + 2) * bj2;
+  const int bj2 = tl.BJ + 2 * g.pad, bij2 = (tl.BI + 2 * g.pad) * bj2;
   const int a = vv / bij2;
   const int rem = vv - a * bij2;
   const int c = rem / bj2;
   const int e = rem - c * bj2;
-  if (bo.t0 + a >= g.T + 2 || bo.i0 + c >= g.Wp || bo.j0 + e >= g.Wp) return 0;
+  if (bo.t0 + a >= g.T + 2 * g.pad || bo.i0 + c >= g.Wp || bo.j0 + e >= g.Wp) return 0;
   return origin + (long long)a * g.P + (long long)c * g.Wp + e;
 }
 
@@ -151,7 +151,7 @@ struct StageSrc {
 
 // The staging source of tile `tile` (mode 1: the box origin in padded
 // coordinates is the tile's first interior voxel, (t0, i0, j0) = (tt BT,
-// ti BI, tj BJ), shifted by the one-voxel halo).
+// ti BI, tj BJ), shifted by the halo).
 __host__ __device__ inline StageSrc tile_source(const Geom& g, const Tiling& tl, int tile, int batch) {
   StageSrc src;
   long long p;
@@ -187,7 +187,7 @@ __host__ __device__ inline long long staged_voxel_fast(const Geom& g, const Tili
   const int rem = vv - a * tl.sa;
   const int c = (int)fastdiv((uint32_t)rem, tl.div_b);
   const int e = rem - c * tl.sb;
-  if (src.bo.t0 + a >= g.T + 2 || src.bo.i0 + c >= g.Wp || src.bo.j0 + e >= g.Wp) return -1;
+  if (src.bo.t0 + a >= g.T + 2 * g.pad || src.bo.i0 + c >= g.Wp || src.bo.j0 + e >= g.Wp) return -1;
   return src.origin + (long long)a * g.P + (long long)c * g.Wp + e;
   }
 }

@@ -184,10 +184,14 @@ def test_create_ex_rejects_misuse(case):
 
 @pytest.mark.parametrize("layers,dtype", [
     (workload.paper_model_layers(1), pdx.DTYPE_FP32),                  # fp32 on the paper layout
-    (workload.paper_model_layers(3), pdx.DTYPE_BF16),                  # 5x5x5 kernels (Model 3)
     (workload.paper_layer_spec([256, 256, 4], [3, 3, 1]), pdx.DTYPE_BF16),  # width 256 with a 1x1x1 head
     (workload.paper_layer_spec([192, 4], [3, 3]), pdx.DTYPE_BF16),     # width 192
     (workload.paper_model_layers(3), pdx.DTYPE_FP8),                   # 5x5x5 kernels in fp8
+    (workload.paper_layer_spec([128, 128, 4], [5, 3, 3]), pdx.DTYPE_BF16),  # 5x5x5 mixed with 3x3x3
+    (workload.paper_layer_spec([128, 128, 4], [5, 5, 1]), pdx.DTYPE_BF16),  # 5x5x5 with a 1x1x1 head
+    (workload.paper_layer_spec([256, 4], [5, 5]), pdx.DTYPE_BF16),     # 5x5x5 at width 256
+    (workload.paper_layer_spec([64, 4], [5, 5]), pdx.DTYPE_BF16),      # one 5x5x5 hidden layer
+    (workload.paper_layer_spec([64, 128, 4], [5, 5, 5]), pdx.DTYPE_BF16),  # 5x5x5 widths that change
 ])
 def test_create_ex_unsupported_models(layers, dtype):
     w = np.zeros(pdx.weight_count(layers), np.float32)
@@ -197,6 +201,15 @@ def test_create_ex_unsupported_models(layers, dtype):
 @pytest.mark.skipif(gpu_available(), reason="checks the no-device error path")
 def test_create_ex_without_device_reports_device_error():
     assert _create_ex(WP, 5, 3, PAPER, pdx.LAYOUT_PAPER, pdx.BOUNDARY_Z, pdx.BOUNDARY_X) == pdx.PD_ERR_DEVICE
+
+
+@pytest.mark.skipif(gpu_available(), reason="checks the no-device error path")
+def test_model3_passes_validation():
+    """Model 3 of Table models (5x5x5 kernels) in bf16 on the paper layout is
+    supported: create gets as far as the device check."""
+    layers = workload.paper_model_layers(3)
+    w = np.zeros(pdx.weight_count(layers), np.float32)
+    assert _create_ex(w, 13, 13, layers, pdx.LAYOUT_PAPER, pdx.BOUNDARY_Z, pdx.BOUNDARY_Z) == pdx.PD_ERR_DEVICE
 
 
 # ---- residual networks (Model 6) ----

@@ -92,3 +92,56 @@ def test_paper_layout_fp32_is_unsupported(cuda):
     with pytest.raises(pdx.PredecoderError) as e:
         pdx.Predecoder(w, 5, 3, layers, "fp32", max_batch=1, layout="paper")
     assert e.value.status == pdx.PD_ERR_UNSUPPORTED
+
+
+# ---- 5x5x5 kernels (Model 3 of Table models) -----------------------------
+
+@pytest.mark.parametrize("d,T,B,filters", [
+    (5, 5, 2, [64, 64, 4]),                # the smallest 5x5x5 network, a halo of two
+    (7, 6, 3, [128, 128, 4]),
+    (9, 4, 1, [64, 64, 64, 4]),             # three 64-wide 5x5x5 layers
+    (13, 13, 1, [128, 128, 128, 4]),        # Model 3 at 13^3, batch 1 (split K loops)
+    (13, 13, 2, [128, 128, 128, 4]),        # ... batch 2
+    (31, 2, 1, [64, 64, 4]),                # box tiles across a 31 x 31 grid
+])
+def test_paper_models_5x5x5(cuda, d, T, B, filters):
+    check(d, T, B, workload.paper_layer_spec(filters, [5] * len(filters)), seed=500 + d + len(filters))
+
+
+def test_5x5x5_layers_tight(cuda):
+    """Model 3's layer list at d = 7, batch 2: every layer's stored bf16
+    activations from the GPU's own input under the rule of tests/tight.py
+    (bf16 matrix instructions over 125 taps x c_in products), then the
+    logits from the GPU's last hidden activations within their own sums'
+    bound, and the flips and residual from the GPU's logits."""
+    import tight
+    from parity import assert_flips_follow_logits
+    d = T = 7
+    B = 2
+    layers = workload.paper_model_layers(3)
+    weights = workload.he_normal_weights(layers, 4003)
+    det, _ = workload.make_inputs(d, T, B, 0.02, 0.02, 5007)
+    pre = pdx.Predecoder(weights, d, T, layers, "bf16", max_batch=B, layout="paper", first="Z", last="Z")
+    ddet = dev_u64(det)
+    x = torch.from_numpy(oracle.unpack_paper(d, T, det, "Z", "Z"))
+    off = 0
+    for l, (ci, co, k, act) in enumerate(layers):
+        nw = co * ci * k ** 3
+        w = tight.q_bf16(torch.from_numpy(weights[off:off + nw].reshape(co, ci, k, k, k).astype(np.float64)))
+        b = torch.from_numpy(weights[off + nw:off + nw + co].astype(np.float64))
+        off += nw + co
+        y = tight.conv(x, w, b, k)
+        eps = tight.eps_bf16_mfma(ci * k ** 3) * tight.conv_mag(x, w, b, k) + tight.U32 * y.abs()
+        if l < len(layers) - 1:
+            out = torch.empty((B, T, d, d, co), dtype=torch.int16, device="cuda")
+            pre.activations(ddet, l, out)
+            torch.cuda.synchronize()
+            got = tight.bf16_bits_to_double(out.cpu()).permute(0, 4, 1, 2, 3).contiguous()
+            tight.check_stored("layer %d (5x5x5)" % (l + 1), got, y, eps, act, tight.q_bf16, say=say)
+            x = got
+    flips, res, logits = run_gpu(pre, det)
+    pre.close()
+    err = (torch.from_numpy(logits.astype(np.float64)) - y).abs()
+    say("  logits: max err %.3g, max err / bound %.3f" % (float(err.max()), float((err / (eps + 1e-6)).max())))
+    assert bool((err <= eps + 1e-6).all())
+    assert_flips_follow_logits(d, T, det, logits, flips, res, layout="paper")
