@@ -14,12 +14,16 @@
 //     one load of all c_in bf16 channels of a plane voxel, straight from the
 //     zero-halo planes, which stay in L2; taps past the last contribute zero.
 //   * A operand: the layer's weight fragments (k-steps x c_out/32 blocks,
-//     16 bytes per lane each), staged in LDS once per workgroup (a 5x5x5
-//     layer to 128 channels fills 128 KB with them, so its workgroups have
-//     two waves instead of four).
+//     16 bytes per lane each), staged in LDS once per workgroup.  A 5x5x5
+//     layer's fragments are 32 k-steps deep (64 KB per 64 channels), so
+//     each of its workgroups takes one 64-channel part of the output (and
+//     stages only that part's fragments) and each wave several blocks,
+//     which amortise the staging.
 //   * Epilogue: + bias, activation, bf16 (or, on the fp8 path, E4M3: one
 //     byte per value); the wave transposes its 32 x c_out tile through its
 //     own LDS slice and writes whole voxel rows with 16-byte stores.
+#include <algorithm>
+
 #include "activation.h"
 #include "internal.h"
 
@@ -38,11 +42,10 @@ typedef __attribute__((address_space(3))) uint32_t lds_u32_w;
 
 constexpr int BPW = 2;  // 32-voxel blocks per wave on large launches (1 on small ones)
 
-// Waves per workgroup: four, two when the weight fragments of a 5x5x5 layer
-// to 128 channels (128 KB) leave LDS room for only two waves' tiles.
+// Waves per workgroup.
 template <int KS, int COUT>
 constexpr int waves() {
-  return KS == 5 && COUT == 128 ? 2 : 4;
+  return 4;
 }
 
 // Divisors of the interior-voxel decode u -> (b, t, i, j).
@@ -97,6 +100,8 @@ __device__ __forceinline__ void gather(const Geom& g, const void* __restrict__ p
 // Each workgroup stages the weight fragments in LDS once; each of its waves
 // then handles bpw consecutive work units: a unit is a 32-voxel block and,
 // with hsplit = 2 (small launches, c_out = 128), one half of its channels.
+// 5x5x5 layers (WGPART): the part is the workgroup's (blockIdx % hsplit)
+// and the workgroup stages only the fragments of that part's channels.
 // F8: y holds E4M3 codes.
 template <int CIN, int COUT, int ACT, bool F8, int KSZ>
 __global__ void __launch_bounds__((64 * waves<KSZ, COUT>())) conv_first_kernel(Geom g, const void* __restrict__ planes,
@@ -110,20 +115,29 @@ __global__ void __launch_bounds__((64 * waves<KSZ, COUT>())) conv_first_kernel(G
   constexpr int OSTR = COUT * ESZ + 16;  // padded LDS row stride (bytes)
   constexpr int GPR = COUT * ESZ / 16;   // 16-byte granules per voxel row
   constexpr int KS = ksteps<CIN, KSZ>();
-  constexpr int WFR = KS * NB * 64;    // weight fragments x lanes (16 bytes each)
+  constexpr bool WGPART = KSZ == 5;
+  const int NBS = WGPART ? NB / hsplit : NB;  // 32-channel blocks staged in LDS
+  const int WFR = KS * NBS * 64;              // weight fragments x lanes (16 bytes each)
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, l32 = lane & 31;
+  const int wgpart = WGPART ? (int)(blockIdx.x % hsplit) : 0;
+  const int wgblk = WGPART ? (int)(blockIdx.x / hsplit) : (int)blockIdx.x;
+  const int sb0 = wgpart * NBS;  // first staged block
   lds_u32x4_w* const wl = (lds_u32x4_w*)smem;
   lds_char* const tile = (lds_char*)smem + WFR * 16 + wave * 32 * OSTR;
   int* const prow = (int*)((lds_char*)smem + WFR * 16 + WAVES * 32 * OSTR) + wave * 32;  // row -> padded index
-  for (int e = tid; e < WFR; e += 64 * WAVES) wl[e] = wfrag[e];
+  for (int e = tid; e < WFR; e += 64 * WAVES) {
+    const int ks = e / (NBS * 64), r = e - ks * NBS * 64;
+    wl[e] = wfrag[(ks * NB + sb0) * 64 + r];
+  }
   __syncthreads();
 
 #pragma unroll 1
   for (int j = 0; j < bpw; ++j) {
-    const int unit = (blockIdx.x * WAVES + wave) * bpw + j;
-    const int blk = hsplit == 1 ? unit : unit >> 1, part = unit - blk * hsplit;
+    const int unit = (wgblk * WAVES + wave) * bpw + j;
+    const int blk = (WGPART || hsplit == 1) ? unit : unit >> 1;
+    const int part = WGPART ? wgpart : unit - blk * hsplit;
     const int u0 = blk * 32;
     if (u0 >= nvox) break;
     const int hb = part * (NB / hsplit), he = hb + NB / hsplit;  // this unit's 32-channel blocks
@@ -147,7 +161,7 @@ __global__ void __launch_bounds__((64 * waves<KSZ, COUT>())) conv_first_kernel(G
       for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
         for (int nb = 0; nb < NH; ++nb) {
-          const u32x4 wf = *(const lds_u32x4*)(smem + ((ks * NB + h0 + nb) * 64 + lane) * 16);
+          const u32x4 wf = *(const lds_u32x4*)(smem + ((ks * NBS + h0 + nb - sb0) * 64 + lane) * 16);
           acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, wf),
                                                             __builtin_bit_cast(bf16x8, bx[ks]), acc[nb], 0, 0, 0);
         }
@@ -198,15 +212,26 @@ hipError_t launch_conv_first(const Geom& g, int cin, int cout, int act, const vo
   const long long nvox = (long long)batch * g.V;  // < 2^31 (host check)
   if ((cin != 2 && cin != 4) || (cout != 64 && cout != 128) || act < 0 || act > 2) return hipErrorInvalidValue;
   if ((ks != 3 && ks != 5) || (ks - 1) / 2 > g.pad || (ks == 5 && (cin != 4 || fp8))) return hipErrorInvalidValue;
-  const int WAVES = ks == 5 && cout == 128 ? 2 : 4;
-  // two blocks per wave amortise the weight staging once the launch has
-  // 512 or more workgroups of them; below that (small batches) one block per
-  // wave doubles the waves on a mostly idle chip
-  const int bpw = nvox >= 512LL * 32 * WAVES * BPW ? BPW : 1;
-  // ... and below 256 workgroups of single blocks, 128-channel layers split
-  // each block's channels over two waves
-  const int hsplit = (bpw == 1 && cout == 128 && nvox < 256LL * 32 * WAVES) ? 2 : 1;
-  const long long nblk = (nvox * hsplit + 32 * WAVES * bpw - 1) / (32 * WAVES * bpw);
+  const int WAVES = 4;
+  int bpw, hsplit;
+  long long nblk;
+  if (ks == 3) {
+    // two blocks per wave amortise the weight staging once the launch has
+    // 512 or more workgroups of them; below that (small batches) one block
+    // per wave doubles the waves on a mostly idle chip
+    bpw = nvox >= 512LL * 32 * WAVES * BPW ? BPW : 1;
+    // ... and below 256 workgroups of single blocks, 128-channel layers
+    // split each block's channels over two waves
+    hsplit = (bpw == 1 && cout == 128 && nvox < 256LL * 32 * WAVES) ? 2 : 1;
+    nblk = (nvox * hsplit + 32 * WAVES * bpw - 1) / (32 * WAVES * bpw);
+  } else {
+    // 5x5x5: workgroups of one 64-channel part; up to 8 blocks per wave while
+    // the launch keeps 1024 or more workgroups
+    hsplit = cout / 64;
+    const long long blocks = (nvox + 31) / 32;
+    bpw = (int)std::max(1LL, std::min(8LL, blocks * hsplit / (1024LL * WAVES)));
+    nblk = (blocks + (long long)WAVES * bpw - 1) / ((long long)WAVES * bpw) * hsplit;
+  }
   Decode dc;
   dc.by_v = make_fastdiv((uint32_t)g.V);
   dc.by_hh = make_fastdiv((uint32_t)(g.H * g.H));
@@ -214,8 +239,9 @@ hipError_t launch_conv_first(const Geom& g, int cin, int cout, int act, const vo
   auto launch = [&](auto CI, auto CO, auto A, auto K) {
     constexpr int C = decltype(CO)::value, I = decltype(CI)::value, KZ = decltype(K)::value;
     constexpr int W = waves<KZ, C>();
-    const size_t lds = (size_t)ksteps<I, KZ>() * (C / 32) * 64 * 16 + (size_t)W * 32 * (C * 2 + 16 + 4);
-    static_assert(ksteps<I, KZ>() * (C / 32) * 64 * 16 + W * 32 * (C * 2 + 16 + 4) <= 160 * 1024, "LDS");
+    constexpr int NBS = KZ == 5 ? 2 : C / 32;  // staged 32-channel blocks (5x5x5: one 64-channel part)
+    const size_t lds = (size_t)ksteps<I, KZ>() * NBS * 64 * 16 + (size_t)W * 32 * (C * 2 + 16 + 4);
+    static_assert(ksteps<I, KZ>() * NBS * 64 * 16 + W * 32 * (C * 2 + 16 + 4) <= 160 * 1024, "LDS");
     if constexpr (KZ == 5) {  // bf16 only; more than 64 KB of LDS
       if (hipFuncSetAttribute((const void*)conv_first_kernel<I, C, decltype(A)::value, false, KZ>,
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)

@@ -145,3 +145,26 @@ def test_5x5x5_layers_tight(cuda):
     say("  logits: max err %.3g, max err / bound %.3f" % (float(err.max()), float((err / (eps + 1e-6)).max())))
     assert bool((err <= eps + 1e-6).all())
     assert_flips_follow_logits(d, T, det, logits, flips, res, layout="paper")
+
+
+def test_5x5x5_layer1_same_at_any_launch_size(cuda):
+    """The 5x5x5 first layer gives each wave up to eight 32-voxel blocks on
+    large launches and one on small ones, one 64-channel half per workgroup
+    either way: a sample's layer-1 activations are bit-identical at batch 1
+    and inside a batch of 240 (eight blocks per wave at d = 13)."""
+    d = T = 13
+    B = 240
+    layers = workload.paper_model_layers(3)
+    weights = workload.he_normal_weights(layers, 4003)
+    det, _ = workload.make_inputs(d, T, B, 0.01, 0.01, 5013)
+    pre = pdx.Predecoder(weights, d, T, layers, "bf16", max_batch=B, layout="paper", first="Z", last="Z")
+    ddet = dev_u64(det)
+    big = torch.empty((B, T, d, d, 128), dtype=torch.int16, device="cuda")
+    pre.activations(ddet, 0, big)
+    one = torch.empty((1, T, d, d, 128), dtype=torch.int16, device="cuda")
+    for s in (0, 117, B - 1):
+        say("5x5x5 layer 1 sample", s)
+        pre.activations(ddet[s:s + 1], 0, one, batch=1)
+        torch.cuda.synchronize()
+        assert torch.equal(one[0].cpu(), big[s].cpu())
+    pre.close()
