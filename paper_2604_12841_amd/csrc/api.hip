@@ -60,7 +60,7 @@ struct pd_predecoder {
   std::vector<void*> wdev;       // per conv layer: fragments (bf16) or [tap][ci][co] (fp32)
   std::vector<size_t> wslice;    // per conv layer: bytes of the fragments of one 128-channel slice of a
                                  // 256-wide layer (run as two slices), 0 otherwise
-  std::vector<float*> bdev;      // per conv layer: bias fp32
+  std::vector<float*> bdev;      // per conv layer: bias fp32 (a 3x3x3 output layer: [4] biases, [4] scales)
   float* head_w = nullptr;       // [4][c_in] fp32 (bf16-valued on the bf16 path)
   float* head_b = nullptr;       // [4]
   // residual network (predecoder_create_resnet): its blocks; wdev / wslice /
@@ -537,6 +537,34 @@ std::vector<uint8_t> conv_fragments_fp8(const uint8_t* codes, int cin, int cout)
   return f;
 }
 
+// Fragments of a 3x3x3 output layer of four filters for launch_conv_out:
+// fragment (row block rb, k-step st), lane l: row m = l % 32 stands for tap
+// 8 rb + m / 4 (zero past the last tap) and filter m % 4; bf16: 8 values,
+// ci = 16 st + 8 (l / 32) + e; fp8 (codes): 32 codes, ci = 64 st + 32 (l /
+// 32) + e.  Byte layout [rb][st][lane][16 or 32].
+std::vector<uint8_t> out_fragments(const float* w, const uint8_t* codes, int cin, bool fp8) {
+  const int kstep = fp8 ? 64 : 16, nks = cin / kstep, lb = fp8 ? 32 : 16;
+  std::vector<uint8_t> f((size_t)4 * nks * 64 * lb, 0);
+  for (int rb = 0; rb < 4; ++rb)
+    for (int st = 0; st < nks; ++st)
+      for (int l = 0; l < 64; ++l) {
+        const int m = l % 32, tap = 8 * rb + m / 4, co = m % 4;
+        if (tap >= 27) continue;
+        uint8_t* dst = &f[(((size_t)rb * nks + st) * 64 + l) * lb];
+        for (int e = 0; e < (fp8 ? 32 : 8); ++e) {
+          const int ci = st * kstep + (fp8 ? 32 : 8) * (l / 32) + e;
+          const size_t src = ((size_t)co * cin + ci) * 27 + tap;
+          if (fp8) {
+            dst[e] = codes[src];
+          } else {
+            const uint16_t v = bf16_bits(w[src]);
+            std::memcpy(dst + 2 * e, &v, 2);
+          }
+        }
+      }
+  return f;
+}
+
 // bf16 fragments of a layer whose outputs run in slices of 128 channels
 // when c_out > 128 (slices back to back; *slice = bytes of one slice, 0 when
 // there is a single launch).
@@ -687,10 +715,8 @@ pd_status enqueue_resnet(pd_predecoder* h, Workspace& ws, hipStream_t st, const 
     }
     // conv2: hb -> the next x (or the logits) with the shortcut added
     if (last) {
-      s = check_launch(pd::launch_conv_hidden(g, tl, B.c_mid, 4, 0, hb, nullptr, 0, h->wdev[2 * k + 1],
-                                              h->bdev[2 * k + 1], 2, nullptr, nullptr, h->tables, ws.nib, logits,
-                                              batch, hidden_wgs, split_for(ws, tl, B.c_mid, 32, 0), 0, sc, sc_stride, 3,
-                                              st));
+      s = check_launch(pd::launch_conv_out(g, B.c_mid, hb, h->wdev[2 * k + 1], h->bdev[2 * k + 1], h->tables,
+                                           ws.nib, logits, batch, h->n_cu, 0, sc, sc_stride, st));
     } else {
       const int nsl = B.c_out > 128 ? B.c_out / 128 : 1, cw = B.c_out / nsl;
       for (int q = 0; q < nsl && s == PD_OK; ++q) {
@@ -790,7 +816,11 @@ pd_status enqueue_run(pd_predecoder* h, Workspace& ws, hipStream_t st, const uin
   }
   if (stop >= 0) return PD_ERR_INVALID_ARG;  // no such hidden layer
   if ((s = mark()) != PD_OK) return s;
-  if (out3) {
+  if (out3 && h->layers[n - 1].k == 3) {
+    const pd_layer& L = h->layers[n - 1];
+    s = check_launch(pd::launch_conv_out(g, L.c_in, x, h->wdev[n - 1], h->bdev[n - 1], h->tables, ws.nib, logits,
+                                         batch, h->n_cu, fp8, nullptr, 0, st));
+  } else if (out3) {
     const pd_layer& L = h->layers[n - 1];
     s = check_launch(pd::launch_conv_hidden(g, tl, L.c_in, L.c_out, L.act, x, nullptr, 0, h->wdev[n - 1],
                                             h->bdev[n - 1], 2, nullptr, nullptr, h->tables, ws.nib, logits,
@@ -967,7 +997,26 @@ pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d
     std::vector<uint8_t> codes;
     std::vector<float> scale, wq;
     if (dtype == PD_DTYPE_FP8) quantize_e4m3(w, L.c_out, nw / L.c_out, &codes, &scale, &wq);
-    if (i == n_layers - 1 && L.k > 1) {  // a 3x3x3 (5x5x5) output layer: 4 filters padded to one block of 32
+    if (i == n_layers - 1 && L.k == 3) {  // a 3x3x3 output layer: rows (tap, filter)
+      if (!pd::conv_out_supported(L.c_in, dtype == PD_DTYPE_FP8, 3, g.H)) return fail(PD_ERR_UNSUPPORTED);
+      std::vector<uint8_t> f = out_fragments(w, codes.data(), L.c_in, dtype == PD_DTYPE_FP8);
+      void* wd = nullptr;
+      s = upload(&wd, f.data(), f.size());
+      h->wdev.push_back(wd);
+      h->wslice.push_back(0);
+      if (s != PD_OK) return fail(s);
+      std::vector<float> bp(8, 1.0f);
+      for (int o2 = 0; o2 < 4; ++o2) {
+        bp[o2] = b[o2];
+        if (dtype == PD_DTYPE_FP8) bp[4 + o2] = scale[o2];
+      }
+      float* bd = nullptr;
+      s = upload(&bd, bp.data(), bp.size() * 4);
+      h->bdev.push_back(bd);
+      if (s != PD_OK) return fail(s);
+      break;
+    }
+    if (i == n_layers - 1 && L.k > 1) {  // a 5x5x5 output layer: 4 filters padded to one block of 32
       void* wd = nullptr;
       if (dtype == PD_DTYPE_FP8) {
         std::vector<uint8_t> f = conv_fragments_fp8(codes.data(), L.c_in, L.c_out);
@@ -1187,10 +1236,17 @@ pd_status predecoder_create_resnet(const float* weights, size_t n_weights, int32
         bf[o2] = (float)(((double)b[o2] - bn[2 * cout + o2]) * gg + bn[cout + o2]);
       }
       size_t slice = 0;
-      std::vector<uint16_t> f = (c == 1 && k == n_blocks - 1) ? conv_fragments(wf.data(), cin, cout)
-                                                             : fragments_sliced(wf.data(), cin, cout, &slice);
       void* wd = nullptr;
-      s = upload(&wd, f.data(), f.size() * 2);
+      if (c == 1 && k == n_blocks - 1) {  // the output conv, 4 filters: rows (tap, filter)
+        if (!pd::conv_out_supported(cin, 0, 3, g.H)) return fail(PD_ERR_UNSUPPORTED);
+        std::vector<uint8_t> f = out_fragments(wf.data(), nullptr, cin, false);
+        s = upload(&wd, f.data(), f.size());
+        bf.resize(8);
+        std::fill(bf.begin() + 4, bf.end(), 1.0f);  // [4] biases, then [4] weight scales of 1
+      } else {
+        std::vector<uint16_t> f = fragments_sliced(wf.data(), cin, cout, &slice);
+        s = upload(&wd, f.data(), f.size() * 2);
+      }
       h->wdev.push_back(wd);
       h->wslice.push_back(slice);
       if (s != PD_OK) return fail(s);

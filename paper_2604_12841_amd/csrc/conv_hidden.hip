@@ -131,13 +131,12 @@ __host__ __device__ inline int stage_slot(int q) {
 }
 
 // Epilogue modes: the activations of a hidden layer, a hidden layer with the
-// 1x1x1 head fused in, or the 3x3x3 output layer itself (4 filters, padded to
-// one block of 32 MFMA rows); EPI_PARK: one part of a split K loop, whose
+// 1x1x1 head fused in, or the 5x5x5 output layer itself (4 filters, padded to
+// one block of 32 MFMA rows; the 3x3x3 one has a kernel of its own); EPI_PARK: one part of a split K loop, whose
 // fp32 sums are parked for split_finish_kernel.  Only EPI_PARK kernels split
 // (the others see a split of 1 at compile time and keep their registers for
 // the epilogue).  EPI_ADD: EPI_ACT with a bf16 shortcut row added to the
-// pre-activation (the second conv of a residual block); the output layer adds
-// a shortcut too when one is given (the last block of a residual network).
+// pre-activation (the second conv of a residual block).
 enum Epi { EPI_ACT = 0, EPI_HEAD = 1, EPI_OUT = 2, EPI_PARK = 3, EPI_ADD = 4 };
 
 // Wave split of the 256 x COUT output tile: WN waves across the channels
@@ -946,14 +945,11 @@ hipError_t launch_case(const Geom& g, const Tiling& tl, int cin, int cout, int a
     PD_HIDDEN_CASE5(128, 128, EPI_ACT)
   }
   if (cout == 4) cout = 32;  // the output layer's 4 filters fill one padded block
-  PD_HIDDEN_CASE(64, 32, EPI_OUT)
-  PD_HIDDEN_CASE(128, 32, EPI_OUT)
-  PD_HIDDEN_CASE(256, 32, EPI_OUT)
   if constexpr (!F8) {
+    // the 5x5x5 output layer (3x3x3 ones run on launch_conv_out)
     PD_HIDDEN_CASE5(64, 32, EPI_OUT)
     PD_HIDDEN_CASE5(128, 32, EPI_OUT)
     // the residual network's layers (bf16)
-    PD_HIDDEN_CASE(512, 32, EPI_OUT)
     PD_HIDDEN_CASE(512, 128, EPI_ACT)
     PD_HIDDEN_CASE(64, 64, EPI_ADD)
     PD_HIDDEN_CASE(128, 128, EPI_ADD)

@@ -193,6 +193,21 @@ int conv_hidden_chunk_channels(int fp8);  // input channels per K-loop chunk
 size_t conv_hidden_partial_floats_per_unit();
 int conv_hidden_workgroups_per_cu(int ks);
 
+// The 3x3x3 output layer of four filters with the threshold (and the last
+// residual block's shortcut) fused in, over rectangles of the grid streamed
+// through the rounds: fragments of conv_out_fragment_bytes(c_in, fp8) bytes
+// ([row block][k-step][lane], rows (tap, filter)), bias [4] then the four
+// weight scales (1 on the bf16 path); sc: optional bf16 shortcut rows (4
+// channels at sc_stride).  Supported: c_in 64, 128, 256, or 512 (bf16), a
+// halo of one, grids whose rectangles fit (conv_out_split: the split of
+// an H x H grid into rectangles of at most maxv voxels with their rims).
+hipError_t launch_conv_out(const Geom& g, int cin, const void* x, const void* wfrag, const float* bias,
+                           const int32_t* tables, uint8_t* nib, float* logits, int batch, int n_cu, int fp8,
+                           const uint16_t* sc, int sc_stride, hipStream_t stream);
+size_t conv_out_fragment_bytes(int cin, int fp8);
+bool conv_out_supported(int cin, int fp8, int ks, int H);
+long long conv_out_split(int H, int maxv, int* nsi, int* nsj);
+
 // Copies the interior voxel rows (row_bytes each, a multiple of 8) of a
 // zero-halo activation buffer to out [batch][T][H][H] rows.
 hipError_t launch_extract(const Geom& g, const void* act, int row_bytes, int batch, void* out, hipStream_t stream);
@@ -291,16 +306,26 @@ __host__ __device__ inline int tables_size(const Geom& g) { return tables_fsite(
 // measurement correction) from the four logits, keeping each channel only
 // where it is defined (Eqs. ZcorreJK..SynZCorrJK): data qubits for 0/1, the
 // site of an X / Z stabilizer for 2 / 3; a logit of exactly 0 is no flip.
+// The flip bits a grid site can carry (its data-qubit bits when it is a
+// data qubit, a measurement bit per stabilizer type on it), and the nibble
+// of a site from these and its four logits (threshold: logit > 0).
+__device__ __forceinline__ unsigned flip_allowed(const Geom& g, const int32_t* __restrict__ tables, int i, int j) {
+  const int s = i * g.H + j;
+  unsigned m = (i < g.d && j < g.d) ? 3u : 0u;
+  if (tables[tables_comp_x(g) + s] >= 0) m |= 4u;
+  if (tables[tables_comp_z(g) + s] >= 0) m |= 8u;
+  return m;
+}
+
+__device__ __forceinline__ unsigned flip_bits(unsigned allowed, const float* lg) {
+  const unsigned b = (lg[0] > 0.0f ? 1u : 0u) | (lg[1] > 0.0f ? 2u : 0u) | (lg[2] > 0.0f ? 4u : 0u) |
+                     (lg[3] > 0.0f ? 8u : 0u);
+  return allowed & b;
+}
+
 __device__ __forceinline__ unsigned flip_nibble(const Geom& g, const int32_t* __restrict__ tables, int i, int j,
                                                 const float* lg) {
-  const int s = i * g.H + j;
-  const bool data = (i < g.d) && (j < g.d);
-  unsigned bits = 0;
-  if (data && lg[0] > 0.0f) bits |= 1u;
-  if (data && lg[1] > 0.0f) bits |= 2u;
-  if (tables[tables_comp_x(g) + s] >= 0 && lg[2] > 0.0f) bits |= 4u;
-  if (tables[tables_comp_z(g) + s] >= 0 && lg[3] > 0.0f) bits |= 8u;
-  return bits;
+  return flip_bits(flip_allowed(g, tables, i, j), lg);
 }
 
 }  // namespace pd

@@ -162,6 +162,7 @@ TIGHT = [
          layers=[(2, 64, 3, 1), (64, 128, 3, 1), (128, 64, 3, 1), (64, 4, 1, 0)], d=7),
     dict(name="paper_m1", layout="paper", layers=workload.paper_model_layers(1), d=7),
     dict(name="paper_256", layout="paper", layers=workload.paper_layer_spec([256, 256, 4], [3, 3, 3]), d=5),
+    dict(name="paper_64_d17", layout="paper", layers=workload.paper_layer_spec([64, 64, 4], [3, 3, 3]), d=17),
 ]
 
 
