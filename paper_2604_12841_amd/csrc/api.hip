@@ -68,6 +68,8 @@ struct pd_predecoder {
   // in), proj_w / proj_b its projection (null for an identity shortcut)
   std::vector<pd_block> blocks;
   std::vector<float*> proj_w, proj_b;
+  void* out_proj_frag = nullptr;  // the last block's projection as fragments of launch_conv_out (when it
+                                  // runs there, fused into the output conv), else null
   int cmax = 0;                  // widest activation row (channels)
   int pmax = 0;                  // widest projection output (channels; residual networks)
   int n_cu = 256;                // compute units: one persistent conv workgroup each
@@ -458,6 +460,8 @@ void free_all(pd_predecoder* h) {
   f(h->ws.pbuf);
   for (float* p : h->proj_w) f(p);
   for (float* p : h->proj_b) f(p);
+  f(h->out_proj_frag);
+  h->out_proj_frag = nullptr;
   h->ws.act[2] = h->ws.pbuf = nullptr;
   h->proj_w.clear();
   h->proj_b.clear();
@@ -702,30 +706,52 @@ pd_status enqueue_resnet(pd_predecoder* h, Workspace& ws, hipStream_t st, const 
       if (s != PD_OK) return s;
       if (stopped(hb, B.c_mid * 2)) return PD_OK;
     }
-    // shortcut
+    // shortcut: the block input, or its 1x1x1 projection -- computed by the
+    // epilogue of conv2 from an input of a few channels (the first block),
+    // by its own kernel otherwise, and by its own kernel when it is the
+    // conv the caller stops at
     const uint16_t* sc = (const uint16_t*)x;
     int sc_stride = B.c_in;
+    const float* pw = nullptr;  // set: conv2 projects sc itself
+    const float* pb = nullptr;
     if (h->proj_w[k]) {
-      s = check_launch(pd::launch_proj(g, x, B.c_in, B.c_in, h->proj_w[k], h->proj_b[k], B.c_out, ws.pbuf, B.c_out,
-                                       batch, st));
-      if (s != PD_OK) return s;
-      sc = (const uint16_t*)ws.pbuf;
-      sc_stride = B.c_out;
-      if (stopped(ws.pbuf, B.c_out * 2)) return PD_OK;
+      // fused: into conv2's epilogue (an input of a few channels), or into
+      // the output conv (its fragments built at create)
+      const bool fuse = (last ? h->out_proj_frag != nullptr : B.c_in <= 8) && stop != conv;
+      if (fuse) {
+        pw = h->proj_w[k];
+        pb = h->proj_b[k];
+        ++conv;  // the projection's stop number
+      } else {
+        s = check_launch(pd::launch_proj(g, x, B.c_in, B.c_in, h->proj_w[k], h->proj_b[k], B.c_out, ws.pbuf,
+                                         B.c_out, batch, st));
+        if (s != PD_OK) return s;
+        sc = (const uint16_t*)ws.pbuf;
+        sc_stride = B.c_out;
+        if (stopped(ws.pbuf, B.c_out * 2)) return PD_OK;
+      }
     }
     // conv2: hb -> the next x (or the logits) with the shortcut added
-    if (last) {
+    if (last && pw) {  // the projection fused into the output conv
       s = check_launch(pd::launch_conv_out(g, B.c_mid, hb, h->wdev[2 * k + 1], h->bdev[2 * k + 1], h->tables,
-                                           ws.nib, logits, batch, h->n_cu, 0, sc, sc_stride, st));
+                                           ws.nib, logits, batch, h->n_cu, 0, nullptr, 0, x, h->out_proj_frag, pb,
+                                           st));
+    } else if (last) {
+      s = check_launch(pd::launch_conv_out(g, B.c_mid, hb, h->wdev[2 * k + 1], h->bdev[2 * k + 1], h->tables,
+                                           ws.nib, logits, batch, h->n_cu, 0, sc, sc_stride, nullptr, nullptr,
+                                           nullptr, st));
     } else {
       const int nsl = B.c_out > 128 ? B.c_out / 128 : 1, cw = B.c_out / nsl;
       for (int q = 0; q < nsl && s == PD_OK; ++q) {
         const void* wq = (const char*)h->wdev[2 * k + 1] + q * h->wslice[2 * k + 1];
+        // slice q: its shortcut channels (or projection rows)
+        const uint16_t* scq = pw ? sc : sc + (size_t)q * cw;
+        const float* pwq = pw ? pw + (size_t)q * cw * B.c_in : nullptr;
+        const float* pbq = pw ? pb + (size_t)q * cw : nullptr;
         s = check_launch(pd::launch_conv_hidden(g, tl, B.c_mid, cw, B.act, hb, (uint16_t*)yb + (size_t)q * cw,
-                                                B.c_out, wq, h->bdev[2 * k + 1] + q * cw, 4, nullptr, nullptr,
-                                                h->tables, ws.nib, nullptr, batch, hidden_wgs,
-                                                split_for(ws, tl, B.c_mid, cw, 0), 0, sc + (size_t)q * cw, sc_stride, 3,
-                                                st));
+                                                B.c_out, wq, h->bdev[2 * k + 1] + q * cw, 4, pwq, pbq, h->tables,
+                                                ws.nib, nullptr, batch, hidden_wgs,
+                                                split_for(ws, tl, B.c_mid, cw, 0), 0, scq, sc_stride, 3, st));
       }
     }
     if (s != PD_OK) return s;
@@ -819,7 +845,7 @@ pd_status enqueue_run(pd_predecoder* h, Workspace& ws, hipStream_t st, const uin
   if (out3 && h->layers[n - 1].k == 3) {
     const pd_layer& L = h->layers[n - 1];
     s = check_launch(pd::launch_conv_out(g, L.c_in, x, h->wdev[n - 1], h->bdev[n - 1], h->tables, ws.nib, logits,
-                                         batch, h->n_cu, fp8, nullptr, 0, st));
+                                         batch, h->n_cu, fp8, nullptr, 0, nullptr, nullptr, nullptr, st));
   } else if (out3) {
     const pd_layer& L = h->layers[n - 1];
     s = check_launch(pd::launch_conv_hidden(g, tl, L.c_in, L.c_out, L.act, x, nullptr, 0, h->wdev[n - 1],
@@ -1263,6 +1289,19 @@ pd_status predecoder_create_resnet(const float* weights, size_t n_weights, int32
       for (size_t e = 0; e < np; ++e) w16[e] = bf16_value(src[e]);
       s = upload(&pw, w16.data(), np * 4);
       if (s == PD_OK) s = upload(&pb, src + np, (size_t)B.c_out * 4);
+      // the last block's projection from a wide input runs inside the output
+      // conv: fragments [k-step][lane], lane l's row l % 32 (filters 0..3,
+      // the rest zero), ci = 16 k-step + 8 (l / 32) + e
+      if (s == PD_OK && k == n_blocks - 1 && B.c_in == B.c_mid && B.c_in >= 256) {
+        std::vector<uint16_t> pf(pd::conv_out_proj_fragment_bytes(B.c_in) / 2, 0);
+        for (int st = 0; st < B.c_in / 16; ++st)
+          for (int l = 0; l < 64; ++l)
+            for (int e = 0; e < 8; ++e) {
+              const int co = l % 32, ci = st * 16 + 8 * (l / 32) + e;
+              if (co < B.c_out) pf[((size_t)st * 64 + l) * 8 + e] = bf16_bits(src[(size_t)co * B.c_in + ci]);
+            }
+        s = upload(&h->out_proj_frag, pf.data(), pf.size() * 2);
+      }
       src += np + B.c_out;
     }
     h->proj_w.push_back(pw);

@@ -135,8 +135,12 @@ __host__ __device__ inline int stage_slot(int q) {
 // one block of 32 MFMA rows; the 3x3x3 one has a kernel of its own); EPI_PARK: one part of a split K loop, whose
 // fp32 sums are parked for split_finish_kernel.  Only EPI_PARK kernels split
 // (the others see a split of 1 at compile time and keep their registers for
-// the epilogue).  EPI_ADD: EPI_ACT with a bf16 shortcut row added to the
-// pre-activation (the second conv of a residual block).
+// the epilogue).  EPI_ADD: EPI_ACT with the block's shortcut added to the
+// pre-activation (the second conv of a residual block): the bf16 row of sc
+// at the output voxel, or, when head_w is given, its 1x1x1 projection
+// computed here from the sc_stride (<= 8) bf16 channels of sc's row
+// (head_w [c_out][sc_stride] and head_b [c_out] in those slots:
+// bf16(head_b + sum_ci head_w x_ci), an fp32 FMA chain in channel order).
 enum Epi { EPI_ACT = 0, EPI_HEAD = 1, EPI_OUT = 2, EPI_PARK = 3, EPI_ADD = 4 };
 
 // Wave split of the 256 x COUT output tile: WN waves across the channels
@@ -216,6 +220,28 @@ __host__ __device__ inline uint32_t stage_offset(const Geom& g, const Tiling& tl
 template <int ROW>
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t stage_rsrc(const void* x, long long base, int cb) {
   return __builtin_amdgcn_make_buffer_rsrc((void*)((const char*)x + base * ROW + cb), 0, kStageRange, 0x00020000);
+}
+
+// The projected shortcut of channels co .. co + N - 1 at padded voxel p:
+// bf16(b[c] + sum_ci w[c][ci] x[p][ci]) over the pc channels of x's row.
+template <int N>
+__device__ __forceinline__ void project_shortcut(const uint16_t* __restrict__ x, int pc, long long p,
+                                                 const float* __restrict__ w, const float* __restrict__ b, int co,
+                                                 float (&s)[N]) {
+  float a[N];
+#pragma unroll
+  for (int o = 0; o < N; ++o) a[o] = b[co + o];
+  for (int ci = 0; ci < pc; ++ci) {
+    const float xv = __uint_as_float((uint32_t)x[p * pc + ci] << 16);
+#pragma unroll
+    for (int o = 0; o < N; ++o) a[o] = __builtin_fmaf(w[(co + o) * pc + ci], xv, a[o]);
+  }
+#pragma unroll
+  for (int o = 0; o < N; o += 2) {
+    const uint32_t pk = bf16_pack(a[o], a[o + 1]);
+    s[o] = __uint_as_float(pk << 16);
+    s[o + 1] = __uint_as_float(pk & 0xFFFF0000u);
+  }
 }
 
 // F8: E4M3 activations and weights (bias holds [COUT] biases then [COUT]
@@ -350,11 +376,18 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
                         e4m3_pack4(v0, v1, v2, v3);
                   } else {
                     float4 sh = {0.0f, 0.0f, 0.0f, 0.0f};
-                    if constexpr (EPI == EPI_ADD) {  // the block's shortcut, 4 bf16 channels of this row
+                    if constexpr (EPI == EPI_ADD) {  // the block's shortcut, 4 channels of this row
                       if (pidx[mb] >= 0) {
-                        const u32x2 sv = *reinterpret_cast<const u32x2*>(sc + (long long)pidx[mb] * sc_stride + co);
-                        sh = float4{__uint_as_float(sv.x << 16), __uint_as_float(sv.x & 0xFFFF0000u),
-                                    __uint_as_float(sv.y << 16), __uint_as_float(sv.y & 0xFFFF0000u)};
+                        if (head_w) {  // projected from sc's few channels
+                          float pj[4];
+                          project_shortcut<4>(sc, sc_stride, pidx[mb], head_w, head_b, co, pj);
+                          sh = float4{pj[0], pj[1], pj[2], pj[3]};
+                        } else {
+                          const u32x2 sv =
+                              *reinterpret_cast<const u32x2*>(sc + (long long)pidx[mb] * sc_stride + co);
+                          sh = float4{__uint_as_float(sv.x << 16), __uint_as_float(sv.x & 0xFFFF0000u),
+                                      __uint_as_float(sv.y << 16), __uint_as_float(sv.y & 0xFFFF0000u)};
+                        }
                       }
                     }
                     const float v0 = act_fn<ACT>(acc[mb][nb][4 * q + 0] + bv.x + sh.x);
@@ -793,12 +826,19 @@ __global__ void __launch_bounds__(256) split_finish_kernel(Geom g, Tiling tl, in
     float v[8];
     sum8(grp * 8, v);
     if constexpr (EPI == EPI_ADD) {  // the block's shortcut
-      const uint4 sv = *reinterpret_cast<const uint4*>(sc + pidx * sc_stride + grp * 8);
-      const uint32_t sw[4] = {sv.x, sv.y, sv.z, sv.w};
+      if (head_w) {  // projected from sc's few channels
+        float pj[8];
+        project_shortcut<8>(sc, sc_stride, pidx, head_w, head_b, grp * 8, pj);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        v[2 * e] += __uint_as_float(sw[e] << 16);
-        v[2 * e + 1] += __uint_as_float(sw[e] & 0xFFFF0000u);
+        for (int e = 0; e < 8; ++e) v[e] += pj[e];
+      } else {
+        const uint4 sv = *reinterpret_cast<const uint4*>(sc + pidx * sc_stride + grp * 8);
+        const uint32_t sw[4] = {sv.x, sv.y, sv.z, sv.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          v[2 * e] += __uint_as_float(sw[e] << 16);
+          v[2 * e + 1] += __uint_as_float(sw[e] & 0xFFFF0000u);
+        }
       }
     }
     if constexpr (F8) {
@@ -974,6 +1014,8 @@ hipError_t launch_conv_hidden(const Geom& g, const Tiling& tl, int cin, int cout
                               const uint16_t* sc, int sc_stride, int ks, hipStream_t stream) {
   if (ks != 3 && ks != 5) return hipErrorInvalidValue;
   if (tl.span <= 0 || tl.span > conv_hidden_max_span(ks)) return hipErrorInvalidValue;
+  // a shortcut projected in the epilogue: from at most 8 channels of sc
+  if (head == 4 && head_w && (!head_b || !sc || sc_stride < 1 || sc_stride > 8)) return hipErrorInvalidValue;
   // the halo holds every tap: a 5x5x5 layer needs the two-voxel halo (and box tiles)
   if ((ks - 1) / 2 > g.pad || (tl.mode == 0 && g.pad != 1)) return hipErrorInvalidValue;
   // parts per tile: a power of two dividing the layer's chunks, with room

@@ -30,14 +30,24 @@
 // so the only recomputation is the rim (and one round at each end of a
 // range of rounds).
 //
+// Residual networks: the last block's shortcut is added to the logits --
+// the block input itself, or its 1x1x1 projection (c_in -> 4) computed here
+// as more k-steps of the same GEMM: each wave group takes half of the block
+// input's channels against projection fragments whose rows 0..3 are the
+// four filters, into an accumulator of its own; the two halves land in two
+// more LDS slots and the output's own voxel adds them, the projection's
+// bias, and rounds to bf16 (the stored shortcut of the unfused path).
+//
 // Waves: wave w takes row blocks 2 (w % 2), 2 (w % 2) + 1 and voxel blocks
 // w / 2, w / 2 + 2, ...: each weight fragment feeds up to four MFMAs and
-// each activation fragment two.  A 128-channel chunk's weight fragments for
-// the wave's two row blocks are 64 registers (bf16; fp8: 32); with c_in <=
-// 128 they are loaded once per unit.  The activation fragments are read from
+// each activation fragment two.  With c_in <= 128 the weight fragments of
+// the wave's two row blocks (64 registers for 128 bf16 channels) are loaded
+// once per unit; wider inputs run in chunks of 64 channels, each chunk's
+// fragments loaded per round.  The activation fragments are read from
 // global memory (L2) straight into registers, 16 bytes per lane (fp8: 32).
 #include <algorithm>
 
+#include "activation.h"
 #include "internal.h"
 
 namespace pd {
@@ -64,8 +74,9 @@ constexpr int NRB = 4;       // row blocks of 32 rows: row 32 rb + m is tap 8 rb
 constexpr int MV = 256;
 constexpr int PSTR = MV + 1;
 constexpr int BPW = MV / 64;  // voxel blocks per wave
-constexpr size_t kLds = (size_t)32 * PSTR * 16;
-static_assert(kLds <= 160 * 1024, "P fits the LDS of a CU");
+// LDS bytes: 32 row slots, and 2 more for the projection's halves
+constexpr size_t lds_bytes(bool proj) { return (size_t)(proj ? 34 : 32) * PSTR * 16; }
+static_assert(lds_bytes(true) <= 160 * 1024, "P fits the LDS of a CU");
 
 template <bool F8>
 struct OutPrec {
@@ -109,19 +120,27 @@ __device__ __forceinline__ Unit unit_of(const Geom& g, int u, int nch, int nsi, 
 
 // wfrag: [rb][k-step][lane] fragments of LQ x 16 bytes (rows past tap 26 are
 // zero); bias: [4] biases, then [4] weight scales (1 on the bf16 path).
-template <int CIN, bool F8>
+// PROJ (bf16): px holds the block input (CIN channels, the layout of x),
+// pfrag its projection fragments [k-step][lane] (rows 0..3 the filters),
+// pbias the projection's 4 biases.
+template <int CIN, bool F8, bool PROJ>
 __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1)))
 conv_out_kernel(Geom g, int nch, int nsi, int nsj, const void* __restrict__ x, const u32x4* __restrict__ wfrag,
                 const float* __restrict__ bias, const int32_t* __restrict__ tables, uint8_t* __restrict__ nib,
-                float* __restrict__ logits, const uint16_t* __restrict__ sc, int sc_stride) {
+                float* __restrict__ logits, const uint16_t* __restrict__ sc, int sc_stride,
+                const void* __restrict__ px, const u32x4* __restrict__ pfrag, const float* __restrict__ pbias) {
+  static_assert(!PROJ || !F8, "projected shortcuts run on the bf16 path");
   using PR = OutPrec<F8>;
   constexpr int KSTEP = PR::KSTEP, LQ = PR::LQ;
   constexpr int ESZ = F8 ? 1 : 2;
   constexpr int ROW = CIN * ESZ;                      // bytes per activation row
-  constexpr int CH = CIN < 128 ? CIN : 128;           // input channels per chunk
+  constexpr int CH = CIN <= 128 ? CIN : 64;           // input channels per chunk (wider inputs: 64, fewer registers)
   constexpr int NCH = CIN / CH;                       // chunks
   constexpr int KPC = CH / KSTEP;                     // k-steps per chunk
   constexpr int NKS = CIN / KSTEP;                    // k-steps in all
+  constexpr int NPC = PROJ ? NCH / 2 : 0;             // projection chunks per wave group (half the input)
+  constexpr int NCT = NCH + NPC;                      // chunks of a round
+  static_assert(!PROJ || NCH % 2 == 0, "the projection's channels split in two");
   extern __shared__ __attribute__((aligned(16))) char smem[];
   lds_f32x4* const pl = (lds_f32x4*)smem;
 
@@ -181,9 +200,16 @@ conv_out_kernel(Geom g, int nch, int nsi, int nsj, const void* __restrict__ x, c
     sca[o] = bias[4 + o];
   }
 
-  // weight fragments of one chunk for the wave's two row blocks
+  // weight fragments of one chunk for the wave's two row blocks (a
+  // projection chunk: its fragments in wa[0])
   u32x4 wa[2][KPC][LQ];
   auto load_w = [&](int c) {
+    if (PROJ && c >= NCH) {
+      const int k0 = (rp * NPC + c - NCH) * KPC;
+#pragma unroll
+      for (int s = 0; s < KPC; ++s) wa[0][s][0] = pfrag[(size_t)(k0 + s) * 64 + lane];
+      return;
+    }
 #pragma unroll
     for (int r = 0; r < 2; ++r)
 #pragma unroll
@@ -195,15 +221,23 @@ conv_out_kernel(Geom g, int nch, int nsi, int nsj, const void* __restrict__ x, c
   if constexpr (NCH == 1) load_w(0);
 
   f32x4 run[3];  // running sums of output rounds tin - 1, tin, tin + 1
+  f32x4 shr[2];  // PROJ: the projected shortcuts of output rounds tin - 1, tin
 #pragma unroll
   for (int k = 0; k < 3; ++k) run[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+  shr[0] = shr[1] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float pbs[4];
+#pragma unroll
+  for (int o = 0; o < 4; ++o) pbs[o] = PROJ ? pbias[o] : 0.0f;
 
-  auto emit = [&](int t, const f32x4& s) {
+  auto emit = [&](int t, const f32x4& s, const f32x4& sh) {
     if (!owner || t < un.t0 || t >= un.t1) return;
     float lg[4];
 #pragma unroll
     for (int o = 0; o < 4; ++o) lg[o] = F8 ? __builtin_fmaf(s[o], sca[o], bs[o]) : s[o] + bs[o];
-    if (sc) {  // residual shortcut of the last block: 4 bf16 channels
+    if (PROJ) {
+#pragma unroll
+      for (int o = 0; o < 4; ++o) lg[o] += sh[o];
+    } else if (sc) {  // residual shortcut of the last block: 4 bf16 channels
       const uint2 sv = *reinterpret_cast<const uint2*>(sc + padded_index(g, un.b, t, oi, oj) * sc_stride);
       lg[0] += __uint_as_float(sv.x << 16);
       lg[1] += __uint_as_float(sv.x & 0xFFFF0000u);
@@ -223,8 +257,13 @@ conv_out_kernel(Geom g, int nch, int nsi, int nsj, const void* __restrict__ x, c
   // as soon as its MFMAs have issued, so the loads run under the rest of
   // the round (the other blocks, the partials' store and the sums)
   u32x4 xb[BPW][KPC][LQ];
+  const long long pdelta = PROJ ? (const char*)px - (const char*)x : 0;  // the block input's rows
   auto load_x = [&](int k, int t, int c) {
-    const char* src = bsrc[k] + (long long)t * g.P * ROW + c * CH * ESZ;
+    const char* src = bsrc[k] + (long long)t * g.P * ROW;
+    if (PROJ && c >= NCH)
+      src += pdelta + (rp * NPC + c - NCH) * CH * ESZ;
+    else
+      src += c * CH * ESZ;
 #pragma unroll
     for (int s = 0; s < KPC; ++s)
 #pragma unroll
@@ -238,6 +277,7 @@ conv_out_kernel(Geom g, int nch, int nsi, int nsj, const void* __restrict__ x, c
   for (int tin = ta; tin < tb; ++tin) {
     // ---- partials of round tin: P = W x for the wave's blocks and row blocks
     f32x16 acc[BPW][2];
+    f32x16 accp[PROJ ? BPW : 1];  // the projection's half (rows 0..3)
 #pragma unroll
     for (int k = 0; k < BPW; ++k)
 #pragma unroll
@@ -245,21 +285,34 @@ conv_out_kernel(Geom g, int nch, int nsi, int nsj, const void* __restrict__ x, c
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[k][r][e] = 0.0f;
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      if constexpr (NCH > 1) load_w(c);
-      const bool more = c + 1 < NCH || tin + 1 < tb;  // a next (round, chunk) to prefetch
-      const int tn = c + 1 < NCH ? tin : tin + 1, cn = c + 1 < NCH ? c + 1 : 0;
+    for (int k = 0; k < (PROJ ? BPW : 1); ++k)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) accp[k][e] = 0.0f;
+#pragma unroll 1
+    for (int c = 0; c < NCT; ++c) {
+      if constexpr (NCT > 1) load_w(c);
+      const bool more = c + 1 < NCT || tin + 1 < tb;  // a next (round, chunk) to prefetch
+      const int tn = c + 1 < NCT ? tin : tin + 1, cn = c + 1 < NCT ? c + 1 : 0;
 #pragma unroll
       for (int k = 0; k < BPW; ++k) {
         if (k >= nbw) break;  // uniform per wave
+        if (PROJ && c >= NCH) {
 #pragma unroll
-        for (int s = 0; s < KPC; ++s)
-#pragma unroll
-          for (int r = 0; r < 2; ++r) {
-            u32x4 a2[2] = {wa[r][s][0], wa[r][s][LQ - 1]};
-            u32x4 b2[2] = {xb[k][s][0], xb[k][s][LQ - 1]};
-            acc[k][r] = mma(a2, b2, acc[k][r], F8);
+          for (int s = 0; s < KPC; ++s) {
+            u32x4 a2[2] = {wa[0][s][0], wa[0][s][0]};
+            u32x4 b2[2] = {xb[k][s][0], xb[k][s][0]};
+            accp[k] = mma(a2, b2, accp[k], false);
           }
+        } else {
+#pragma unroll
+          for (int s = 0; s < KPC; ++s)
+#pragma unroll
+            for (int r = 0; r < 2; ++r) {
+              u32x4 a2[2] = {wa[r][s][0], wa[r][s][LQ - 1]};
+              u32x4 b2[2] = {xb[k][s][0], xb[k][s][LQ - 1]};
+              acc[k][r] = mma(a2, b2, acc[k][r], F8);
+            }
+        }
         if (more) load_x(k, tn, cn);
       }
     }
@@ -277,6 +330,9 @@ conv_out_kernel(Geom g, int nch, int nsi, int nsj, const void* __restrict__ x, c
           pl[slot * PSTR + v] = f32x4{acc[k][r][4 * q], acc[k][r][4 * q + 1], acc[k][r][4 * q + 2],
                                       acc[k][r][4 * q + 3]};
         }
+      // the projection's half: rows 0..3 (the first half-wave's q = 0) into slot 32 + rp
+      if (PROJ && half == 0)
+        pl[(32 + rp) * PSTR + v] = f32x4{accp[k][0], accp[k][1], accp[k][2], accp[k][3]};
     }
     // LDS-only barriers: a full fence would also wait for the prefetch loads
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's partials are in LDS
@@ -291,17 +347,27 @@ conv_out_kernel(Geom g, int nch, int nsi, int nsj, const void* __restrict__ x, c
 #pragma unroll
         for (int n = 0; n < 9; ++n) run[2 - kt] += p[n];
       }
+      if (PROJ) {  // the output's own voxel in round tin: its projected shortcut, rounded to bf16
+        const f32x4 a = pl[32 * PSTR + nbr[4]], b = pl[33 * PSTR + nbr[4]];
+        float sp[4];
+#pragma unroll
+        for (int o = 0; o < 4; ++o) sp[o] = (a[o] + b[o]) + pbs[o];
+        const uint32_t p01 = bf16_pack(sp[0], sp[1]), p23 = bf16_pack(sp[2], sp[3]);
+        shr[1] = f32x4{__uint_as_float(p01 << 16), __uint_as_float(p01 & 0xFFFF0000u), __uint_as_float(p23 << 16),
+                       __uint_as_float(p23 & 0xFFFF0000u)};
+      }
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the sums' reads are done before the next stores
     __builtin_amdgcn_s_barrier();
     // output round tin - 1 is complete
-    emit(tin - 1, run[0]);
+    emit(tin - 1, run[0], shr[0]);
     run[0] = run[1];
     run[1] = run[2];
     run[2] = f32x4{0.f, 0.f, 0.f, 0.f};
+    shr[0] = shr[1];
   }
   // the last round when no round follows it
-  if (tb == g.T) emit(tb - 1, run[0]);
+  if (tb == g.T) emit(tb - 1, run[0], shr[0]);
 }
 
 }  // namespace
@@ -342,8 +408,11 @@ long long conv_out_split(int H, int maxv, int* nsi, int* nsj) {
 
 hipError_t launch_conv_out(const Geom& g, int cin, const void* x, const void* wfrag, const float* bias,
                            const int32_t* tables, uint8_t* nib, float* logits, int batch, int n_cu, int fp8,
-                           const uint16_t* sc, int sc_stride, hipStream_t stream) {
+                           const uint16_t* sc, int sc_stride, const void* px, const void* pfrag,
+                           const float* pbias, hipStream_t stream) {
   if (g.pad != 1 || batch < 1 || !conv_out_supported(cin, fp8, 3, g.H)) return hipErrorInvalidValue;
+  const bool proj = px != nullptr;
+  if (proj && (fp8 || cin < 256 || !pfrag || !pbias || sc)) return hipErrorInvalidValue;
   int nsi = 1, nsj = 1;
   conv_out_split(g.H, MV, &nsi, &nsj);
   // rounds per unit: the split of T that minimises (units per CU, rounded
@@ -364,28 +433,37 @@ hipError_t launch_conv_out(const Geom& g, int cin, const void* x, const void* wf
   }
   const long long units = per * nch;
   if (units > 0x7fffffffLL) return hipErrorInvalidValue;
-  auto go = [&](auto kern) -> hipError_t {
-    hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLds);
+  auto go = [&](auto kern, bool p) -> hipError_t {
+    const size_t lds = lds_bytes(p);
+    hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(kern, dim3((unsigned)units), dim3(NT), kLds, stream, g, nch, nsi, nsj, x,
-                       (const u32x4*)wfrag, bias, tables, nib, logits, sc, sc_stride);
+    hipLaunchKernelGGL(kern, dim3((unsigned)units), dim3(NT), lds, stream, g, nch, nsi, nsj, x,
+                       (const u32x4*)wfrag, bias, tables, nib, logits, sc, sc_stride, px, (const u32x4*)pfrag,
+                       pbias);
     return hipGetLastError();
   };
-  if (fp8) {
+  if (proj) {
     switch (cin) {
-      case 64: return go(conv_out_kernel<64, true>);
-      case 128: return go(conv_out_kernel<128, true>);
-      case 256: return go(conv_out_kernel<256, true>);
+      case 256: return go(conv_out_kernel<256, false, true>, true);
+      case 512: return go(conv_out_kernel<512, false, true>, true);
+    }
+  } else if (fp8) {
+    switch (cin) {
+      case 64: return go(conv_out_kernel<64, true, false>, false);
+      case 128: return go(conv_out_kernel<128, true, false>, false);
+      case 256: return go(conv_out_kernel<256, true, false>, false);
     }
   } else {
     switch (cin) {
-      case 64: return go(conv_out_kernel<64, false>);
-      case 128: return go(conv_out_kernel<128, false>);
-      case 256: return go(conv_out_kernel<256, false>);
-      case 512: return go(conv_out_kernel<512, false>);
+      case 64: return go(conv_out_kernel<64, false, false>, false);
+      case 128: return go(conv_out_kernel<128, false, false>, false);
+      case 256: return go(conv_out_kernel<256, false, false>, false);
+      case 512: return go(conv_out_kernel<512, false, false>, false);
     }
   }
   return hipErrorInvalidValue;
 }
+
+size_t conv_out_proj_fragment_bytes(int cin) { return (size_t)(cin / 16) * 64 * 16; }
 
 }  // namespace pd

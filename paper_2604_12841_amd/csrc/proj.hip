@@ -1,7 +1,8 @@
 // proj.hip -- the 1x1x1 projection shortcut of a residual block (Model 6,
 // Sec. VI, Fig. Model8Representation): y[p][co] = bf16(b[co] + sum_ci
 // w[co][ci] x[p][ci]) for every interior voxel p of the zero-halo layout,
-// fp32 sums in channel order.  HBM-bound and small next to the block's two
+// an fp32 FMA chain in channel order (the same chain the second conv's
+// epilogue runs when it projects a block input of a few channels itself).  HBM-bound and small next to the block's two
 // convolutions: one thread per (voxel, 4 output channels), reading the
 // voxel's c_in bf16 inputs (16 bytes at a time when c_in is a multiple of 8)
 // and the (L1-resident) weights.
@@ -29,7 +30,7 @@ __global__ void __launch_bounds__(256) proj_kernel(Geom g, const uint16_t* __res
   float acc[4] = {b[c0], b[c0 + 1], b[c0 + 2], b[c0 + 3]};
   auto add = [&](int ci, float xv) {
 #pragma unroll
-    for (int o = 0; o < 4; ++o) acc[o] += w[(long long)(c0 + o) * cin + ci] * xv;
+    for (int o = 0; o < 4; ++o) acc[o] = __builtin_fmaf(w[(long long)(c0 + o) * cin + ci], xv, acc[o]);
   };
   if (cin % 8 == 0) {
     for (int ci = 0; ci < cin; ci += 8) {
