@@ -27,7 +27,10 @@ _BOUNDARIES = {None: BOUNDARY_NONE, "none": BOUNDARY_NONE, "Z": BOUNDARY_Z, "X":
 PD_OK, PD_ERR_INVALID_ARG, PD_ERR_UNSUPPORTED, PD_ERR_OUT_OF_MEMORY, PD_ERR_DEVICE, PD_ERR_TOO_LARGE = range(6)
 STATIC_SCRATCH_BYTES = 64 << 20  # PD_STATIC_SCRATCH_BYTES
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpredecoder.so")
+# PD_LIBRARY: another build of the library to load (the host-sanitizer build
+# of build.py --sanitize); by default the in-tree libpredecoder.so
+LIB_PATH = os.environ.get("PD_LIBRARY") or os.path.join(os.path.dirname(os.path.abspath(__file__)),
+                                                         "libpredecoder.so")
 
 # Every symbol declared in include/predecoder.h.
 EXPORTS = ("predecoder_create", "predecoder_create_ex", "predecoder_run", "predecoder_residual", "predecoder_unpack",
