@@ -97,6 +97,9 @@ def _load():
         lib.oracle_resnet_weight_count.restype = i64
         lib.oracle_forward_resnet.argtypes = [i32, i32, i32, vp, i32, vp, vp, i32, vp]
         lib.oracle_forward_resnet.restype = None
+        lib.oracle_forward_resnet_fp8_perturbed.argtypes = [i32, i32, i32, vp, i32, vp, vp, ctypes.c_double,
+                                                             ctypes.c_uint64, vp]
+        lib.oracle_forward_resnet_fp8_perturbed.restype = None
         lib.oracle_conv_sums.argtypes = [i32, i32, i32, vp, i32, i32, i32, vp, vp, vp, i32]
         lib.oracle_conv_sums.restype = None
         lib.oracle_e4m3_value.argtypes = [i32]
@@ -315,10 +318,13 @@ def resnet_weight_count(blocks, bn_per_channel=4):
     return int(_load().oracle_resnet_weight_count(len(blocks), _ptr(spec), bn_per_channel))
 
 
-def forward_resnet(d, T, planes, blocks, weights, bf16, layout="plaquette", acc32=False):
+def forward_resnet(d, T, planes, blocks, weights, bf16, layout="plaquette", acc32=False, fp8=False,
+                   fp8_sum_eps=None, fp8_sum_seed=0):
     """Residual network forward (Model 6, Sec. VI, Fig. Model8Representation).  planes [B][c_in][T][H][H];
     blocks: (c_in, c_mid, c_out, act); returns logits [B][4][T][H][H].  acc32 (bf16 only): the conv sums
-    in fp32 (sizes the parity tolerance)."""
+    in fp32 (sizes the parity tolerance).  fp8: the E4M3 precision points (folded weights per output
+    channel, every stored tensor); fp8_sum_eps (test infrastructure) moves every sum by up to that
+    fraction of its sum of magnitudes, hashed per fp8_sum_seed (sizes the fp8 parity tolerance)."""
     planes = np.ascontiguousarray(planes, dtype=np.float64)
     weights = np.ascontiguousarray(weights, dtype=np.float32)
     spec = np.ascontiguousarray(np.array([list(b) for b in blocks], dtype=np.int32).ravel())
@@ -329,7 +335,13 @@ def forward_resnet(d, T, planes, blocks, weights, bf16, layout="plaquette", acc3
     if planes.shape[1:] != (blocks[0][0], T, H, H) or blocks[-1][2] != 4:
         raise ValueError("planes / blocks mismatch")
     out = np.zeros((B, 4, T, H, H), dtype=np.float64)
-    prec = (2 if acc32 else 1) if bf16 else 0
+    if fp8_sum_eps is not None:
+        if not fp8:
+            raise ValueError("fp8_sum_eps needs fp8")
+        _load().oracle_forward_resnet_fp8_perturbed(H, T, B, _ptr(planes), len(blocks), _ptr(spec), _ptr(weights),
+                                                    float(fp8_sum_eps), int(fp8_sum_seed), _ptr(out))
+        return out
+    prec = 3 if fp8 else ((2 if acc32 else 1) if bf16 else 0)
     _load().oracle_forward_resnet(H, T, B, _ptr(planes), len(blocks), _ptr(spec), _ptr(weights), prec, _ptr(out))
     return out
 
@@ -352,12 +364,12 @@ def conv_sums(x, w, bias, acc32=False):
     return y
 
 
-def run_resnet(d, T, det, blocks, weights, bf16, layout="paper", first=None, last=None):
+def run_resnet(d, T, det, blocks, weights, bf16, layout="paper", first=None, last=None, fp8=False):
     """The whole path with a residual network: (logits, flips, residual)."""
     if layout == "paper":
-        logits = forward_resnet(d, T, unpack_paper(d, T, det, first, last), blocks, weights, bf16, layout)
+        logits = forward_resnet(d, T, unpack_paper(d, T, det, first, last), blocks, weights, bf16, layout, fp8=fp8)
         flips, res = flips_residual_paper(d, T, logits, det)
     else:
-        logits = forward_resnet(d, T, unpack(d, T, det), blocks, weights, bf16)
+        logits = forward_resnet(d, T, unpack(d, T, det), blocks, weights, bf16, fp8=fp8)
         flips, res = flips_residual(d, T, logits, det)
     return logits, flips, res

@@ -655,9 +655,12 @@ void oracle_residual_from_flips(int d, int T, int B, const uint64_t* det, const 
 
 /* y[b][co][v] = bias[co] + sum_{ci, taps} w[co][ci][taps] x[b][ci][v + tap]
  * on a T x H x H volume with zero padding, k = 1 or 3; fp64 sums (acc32:
- * fp32 sums in this loop order, another valid summation). */
-static void conv_sums(int H, int T, int B, const double* x, int ci_n, int co_n, int k, const double* w,
-                      const double* bias, double* y, int acc32) {
+ * fp32 sums in this loop order, another valid summation).  eps > 0 (test
+ * infrastructure, fp64 sums): each sum moved by u eps sum |products|, u in
+ * [-1, 1) hashed from (seed, key, sample, channel, voxel), as in the fp8
+ * forward above. */
+static void conv_sums_eps(int H, int T, int B, const double* x, int ci_n, int co_n, int k, const double* w,
+                          const double* bias, double* y, int acc32, double eps, uint64_t seed, uint64_t key) {
   const int64_t V = (int64_t)T * H * H;
   const int p = (k - 1) / 2;
 #pragma omp parallel for collapse(2) schedule(dynamic)
@@ -666,6 +669,7 @@ static void conv_sums(int H, int T, int B, const double* x, int ci_n, int co_n, 
       /* per output voxel, the products in (ci, kt, ki, kj) order; the voxel
        * loops sit inside the tap loops (each output's order is unchanged) */
       double* acc = (double*)calloc((size_t)V, sizeof(double));
+      double* mag = eps > 0.0 ? (double*)calloc((size_t)V, sizeof(double)) : NULL;
       float* accf = (float*)calloc((size_t)V, sizeof(float));
       for (int ci = 0; ci < ci_n; ++ci)
         for (int kt = 0; kt < k; ++kt)
@@ -686,14 +690,28 @@ static void conv_sums(int H, int T, int B, const double* x, int ci_n, int co_n, 
                     for (int j = j0; j < j1; ++j) accf[o + j] += (float)(wv * xr[j + kj - p]);
                   else
                     for (int j = j0; j < j1; ++j) acc[o + j] += wv * xr[j + kj - p];
+                  if (mag)
+                    for (int j = j0; j < j1; ++j) mag[o + j] += fabs(wv * xr[j + kj - p]);
                 }
               }
             }
-      for (int64_t v = 0; v < V; ++v)
-        y[((int64_t)b * co_n + co) * V + v] = (acc32 ? (double)accf[v] : acc[v]) + bias[co];
+      for (int64_t v = 0; v < V; ++v) {
+        double a = acc32 ? (double)accf[v] : acc[v];
+        if (mag) {
+          const uint64_t hk = (((key * 65536 + (uint64_t)b) * 4096 + (uint64_t)co) << 24) + (uint64_t)v;
+          a += unit_hash(hk ^ (seed * 0xd1b54a32d192ed03ull)) * eps * mag[v];
+        }
+        y[((int64_t)b * co_n + co) * V + v] = a + bias[co];
+      }
       free(acc);
+      free(mag);
       free(accf);
     }
+}
+
+static void conv_sums(int H, int T, int B, const double* x, int ci_n, int co_n, int k, const double* w,
+                      const double* bias, double* y, int acc32) {
+  conv_sums_eps(H, T, B, x, ci_n, co_n, k, w, bias, y, acc32, 0.0, 0, 0);
 }
 
 /* conv_sums as a library entry (test infrastructure: pins its two
@@ -731,13 +749,21 @@ int64_t oracle_resnet_weight_count(int n_blocks, const int* spec, int bn_per_cha
  * rounding the pre-activation (and the activation) to fp32; the sum
  * BN2(conv2 h) + s rounded to fp32 once.  prec 2: prec 1 with the conv sums
  * taken in fp32 (test infrastructure: another valid summation, which sizes
- * the parity tolerance of residual networks).  planes [B][c_in0][T][H][H];
+ * the parity tolerance of residual networks).  prec 3 (fp8): the fp8
+ * reading of the plain networks applied to the folded convs -- weights
+ * fp32(w g) quantised per output channel to e4m3(w / 2^e) 2^e (2^e the
+ * smallest power of two with max |w| / 2^e <= 448), the projection's
+ * weights likewise, biases fp32, every stored tensor (the input planes, h,
+ * P(x), y) rounded to E4M3 after rounding to fp32, the sum BN2(conv2 h) + s
+ * rounded to fp32 once; exact (fp64) sums.  planes [B][c_in0][T][H][H];
  * logits [B][4][T][H][H]. */
-void oracle_forward_resnet(int H, int T, int B, const double* planes, int n_blocks, const int* spec,
-                           const float* weights, int prec, double* logits) {
+static void forward_resnet_impl(int H, int T, int B, const double* planes, int n_blocks, const int* spec,
+                                const float* weights, int prec, double sum_eps, uint64_t seed, double* logits) {
   const double eps = 1e-5;
   const int64_t V = (int64_t)T * H * H;
-  const int acc32 = prec == 2;
+  const int acc32 = prec == 2, fp8 = prec == 3;
+  /* a stored tensor's value from its fp32 value, in the mode's precision */
+#define STORE(v) (fp8 ? oracle_round_e4m3((float)(v)) : (double)oracle_round_bf16((float)(v)))
   int cmax = spec[0];
   for (int k = 0; k < n_blocks; ++k)
     for (int q = 1; q < 3; ++q) cmax = spec[4 * k + q] > cmax ? spec[4 * k + q] : cmax;
@@ -746,7 +772,7 @@ void oracle_forward_resnet(int H, int T, int B, const double* planes, int n_bloc
   double* s = (double*)malloc(sizeof(double) * (size_t)B * cmax * V);
   double* y = (double*)malloc(sizeof(double) * (size_t)B * cmax * V);
   const int c0 = spec[0];
-  for (int64_t e = 0; e < (int64_t)B * c0 * V; ++e) x[e] = prec ? (double)oracle_round_bf16((float)planes[e]) : planes[e];
+  for (int64_t e = 0; e < (int64_t)B * c0 * V; ++e) x[e] = prec ? STORE(planes[e]) : planes[e];
   const float* src = weights;
   for (int k = 0; k < n_blocks; ++k) {
     const int ci = spec[4 * k], cm = spec[4 * k + 1], co = spec[4 * k + 2], act = spec[4 * k + 3];
@@ -764,9 +790,17 @@ void oracle_forward_resnet(int H, int T, int B, const double* planes, int n_bloc
       for (int e = 0; e < 4 * cout; ++e) bnp[c][e] = (double)src[nw + cout + e];
       for (int o = 0; o < cout; ++o) {
         const double g = bnp[c][o] / sqrt(bnp[c][3 * cout + o] + eps);
+        double* row = cw[c] + o * (int64_t)cin * 27;
         for (int64_t e = 0; e < (int64_t)cin * 27; ++e) {
           const double wv = (double)src[o * (int64_t)cin * 27 + e];
-          cw[c][o * (int64_t)cin * 27 + e] = prec ? (double)oracle_round_bf16((float)(wv * g)) : wv;
+          row[e] = fp8 ? (double)(float)(wv * g) : (prec ? (double)oracle_round_bf16((float)(wv * g)) : wv);
+        }
+        if (fp8) { /* one power-of-two scale per output channel */
+          double amax = 0.0;
+          for (int64_t e = 0; e < (int64_t)cin * 27; ++e) amax = fmax(amax, fabs(row[e]));
+          const int ex = oracle_e4m3_scale_exp(amax);
+          for (int64_t e = 0; e < (int64_t)cin * 27; ++e)
+            row[e] = ldexp(oracle_round_e4m3((float)ldexp(row[e], -ex)), ex);
         }
         const double bv = (double)src[nw + o];
         cb[c][o] = prec ? (double)(float)((bv - bnp[c][2 * cout + o]) * g + bnp[c][cout + o]) : bv;
@@ -774,13 +808,13 @@ void oracle_forward_resnet(int H, int T, int B, const double* planes, int n_bloc
       src += nw + cout + 4 * cout;
     }
     /* h = act(BN1(conv1 x)) */
-    conv_sums(H, T, B, x, ci, cm, 3, cw[0], cb[0], h, acc32);
+    conv_sums_eps(H, T, B, x, ci, cm, 3, cw[0], cb[0], h, acc32, sum_eps, seed, 3 * (uint64_t)k);
     for (int b = 0; b < B; ++b)
       for (int o = 0; o < cm; ++o)
         for (int64_t v = 0; v < V; ++v) {
           double* z = &h[((int64_t)b * cm + o) * V + v];
           if (prec) {
-            *z = (double)oracle_round_bf16((float)activation(act, (double)(float)*z));
+            *z = STORE(activation(act, (double)(float)*z));
           } else {
             const double g = bnp[0][o] / sqrt(bnp[0][3 * cm + o] + eps);
             *z = activation(act, (*z - bnp[0][2 * cm + o]) * g + bnp[0][cm + o]);
@@ -791,19 +825,27 @@ void oracle_forward_resnet(int H, int T, int B, const double* planes, int n_bloc
       const int64_t np = (int64_t)co * ci;
       double* pw = (double*)malloc(sizeof(double) * np);
       double* pb = (double*)malloc(sizeof(double) * co);
-      for (int64_t e = 0; e < np; ++e) pw[e] = prec ? (double)oracle_round_bf16(src[e]) : (double)src[e];
+      for (int64_t e = 0; e < np; ++e) pw[e] = (prec && !fp8) ? (double)oracle_round_bf16(src[e]) : (double)src[e];
+      if (fp8)
+        for (int o = 0; o < co; ++o) { /* one power-of-two scale per output channel */
+          double amax = 0.0;
+          for (int e = 0; e < ci; ++e) amax = fmax(amax, fabs(pw[o * (int64_t)ci + e]));
+          const int ex = oracle_e4m3_scale_exp(amax);
+          for (int e = 0; e < ci; ++e)
+            pw[o * (int64_t)ci + e] = ldexp(oracle_round_e4m3((float)ldexp(pw[o * (int64_t)ci + e], -ex)), ex);
+        }
       for (int o = 0; o < co; ++o) pb[o] = (double)src[np + o];
       src += np + co;
-      conv_sums(H, T, B, x, ci, co, 1, pw, pb, s, acc32);
+      conv_sums_eps(H, T, B, x, ci, co, 1, pw, pb, s, acc32, sum_eps, seed, 3 * (uint64_t)k + 1);
       if (prec)
-        for (int64_t e = 0; e < (int64_t)B * co * V; ++e) s[e] = (double)oracle_round_bf16((float)s[e]);
+        for (int64_t e = 0; e < (int64_t)B * co * V; ++e) s[e] = STORE(s[e]);
       free(pw);
       free(pb);
     } else {
       memcpy(s, x, sizeof(double) * (size_t)B * co * V);
     }
     /* y = act(BN2(conv2 h) + s) */
-    conv_sums(H, T, B, h, cm, co, 3, cw[1], cb[1], y, acc32);
+    conv_sums_eps(H, T, B, h, cm, co, 3, cw[1], cb[1], y, acc32, sum_eps, seed, 3 * (uint64_t)k + 2);
     for (int b = 0; b < B; ++b)
       for (int o = 0; o < co; ++o)
         for (int64_t v = 0; v < V; ++v) {
@@ -818,7 +860,7 @@ void oracle_forward_resnet(int H, int T, int B, const double* planes, int n_bloc
           if (last)
             y[e] = pre;
           else
-            y[e] = prec ? (double)oracle_round_bf16((float)activation(act, pre)) : activation(act, pre);
+            y[e] = prec ? STORE(activation(act, pre)) : activation(act, pre);
         }
     double* t = x;
     x = y;
@@ -834,6 +876,20 @@ void oracle_forward_resnet(int H, int T, int B, const double* planes, int n_bloc
   free(h);
   free(s);
   free(y);
+#undef STORE
+}
+
+void oracle_forward_resnet(int H, int T, int B, const double* planes, int n_blocks, const int* spec,
+                           const float* weights, int prec, double* logits) {
+  forward_resnet_impl(H, T, B, planes, n_blocks, spec, weights, prec, 0.0, 0, logits);
+}
+
+/* The fp8 residual forward (prec 3) with every sum of products moved by up
+ * to eps sum |products| (test infrastructure: sizes the fp8 parity bound of
+ * residual networks; eps = 0 is the plain fp8 forward). */
+void oracle_forward_resnet_fp8_perturbed(int H, int T, int B, const double* planes, int n_blocks, const int* spec,
+                                         const float* weights, double eps, uint64_t seed, double* logits) {
+  forward_resnet_impl(H, T, B, planes, n_blocks, spec, weights, 3, eps, seed, logits);
 }
 
 /* Threads an OpenMP parallel region of the oracle uses (reported with the

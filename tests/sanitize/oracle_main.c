@@ -42,6 +42,8 @@ void oracle_conv_sums(int H, int T, int B, const double* x, int ci_n, int co_n, 
 int64_t oracle_resnet_weight_count(int n_blocks, const int* spec, int bn_per_channel);
 void oracle_forward_resnet(int H, int T, int B, const double* planes, int n_blocks, const int* spec,
                            const float* weights, int prec, double* logits);
+void oracle_forward_resnet_fp8_perturbed(int H, int T, int B, const double* planes, int n_blocks, const int* spec,
+                                         const float* weights, double eps, uint64_t seed, double* logits);
 void oracle_set_num_threads(int n);
 
 static uint64_t rng = 0x9e3779b97f4a7c15ull;
@@ -145,7 +147,8 @@ int main(void) {
   float* rw = malloc(sizeof(float) * rn);
   for (int64_t e = 0; e < rn; ++e) rw[e] = (float)(0.5 + 0.4 * (urand() - 0.5));
   double* rl = malloc(sizeof(double) * B * 4 * T * d * d);
-  for (int p = 0; p < 3; ++p) oracle_forward_resnet(d, T, B, pp, 2, rspec, rw, p, rl);
+  for (int p = 0; p < 4; ++p) oracle_forward_resnet(d, T, B, pp, 2, rspec, rw, p, rl);
+  oracle_forward_resnet_fp8_perturbed(d, T, B, pp, 2, rspec, rw, 1e-4, 3, rl);
   (void)oracle_resnet_weight_count(2, rspec, 2);
   free(det); free(site_of); free(index_of); free(pl); free(pp); free(w);
   for (int p = 0; p < 3; ++p) free(lg[p]);

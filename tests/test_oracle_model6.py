@@ -133,3 +133,84 @@ def test_model6_receptive_field_is_17():
     t, i, j = np.nonzero(y > 0)
     radius = np.maximum(np.maximum(np.abs(t - 9), np.abs(i - 9)), np.abs(j - 9))
     assert radius.max() == 8
+
+
+def _q_e4m3(t):
+    """PyTorch's own E4M3 rounding (saturating at 448 as the OCP format's
+    largest finite value)."""
+    return t.float().clamp(-448.0, 448.0).to(torch.float8_e4m3fn).double()
+
+
+def _scaled_e4m3(w):
+    """Per output channel: e4m3(w / 2^e) 2^e, 2^e the smallest power of two
+    with max |w| / 2^e <= 448 (written from that definition with frexp)."""
+    out = torch.empty_like(w)
+    for o in range(w.shape[0]):
+        amax = float(w[o].abs().max())
+        if amax == 0.0:
+            e = 0
+        else:
+            m, ex = np.frexp(amax / 448.0)  # amax / 448 = m 2^ex, m in [0.5, 1)
+            e = int(ex) - 1 if m == 0.5 else int(ex)
+        out[o] = _q_e4m3(w[o] / 2.0 ** e) * 2.0 ** e
+    return out
+
+
+def torch_resnet_fp8(planes, blocks, weights):
+    """The fp8 quantisation points: the folded weights fp32(w g) scaled per
+    output channel to E4M3, the projections likewise, biases fp32, every
+    stored tensor (planes, h, P(x), y) E4M3 after an fp32 pre-activation and
+    activation, the residual sum rounded to fp32 once."""
+    f32 = lambda t: t.float().double()  # noqa: E731
+    x = _q_e4m3(torch.from_numpy(planes))
+    for k, ((ci, cm, co, act), p) in enumerate(zip(blocks, _split(blocks, weights))):
+        def fold(t):
+            g = p["scale" + t] / torch.sqrt(p["var" + t] + EPS)
+            return (_scaled_e4m3(f32(p["w" + t] * g.reshape(-1, 1, 1, 1, 1))),
+                    f32((p["b" + t] - p["mean" + t]) * g + p["shift" + t]))
+        w1, b1 = fold("1")
+        w2, b2 = fold("2")
+        h = _q_e4m3(f32(_act(f32(F.conv3d(x, w1, b1, padding=1)), act)))
+        s = _q_e4m3(f32(F.conv3d(x, _scaled_e4m3(p["pw"]), p["pb"]))) if ci != co else x
+        y = f32(F.conv3d(h, w2, b2, padding=1) + s)
+        x = y if k == len(blocks) - 1 else _q_e4m3(f32(_act(y, act)))
+    return x.numpy()
+
+
+@pytest.mark.parametrize("blocks,d,T,B,layout", [
+    (workload.resnet_blocks([16, 16, 16, 16]), 5, 5, 2, "paper"),
+    ([(4, 8, 8, G), (8, 16, 16, G), (16, 8, 4, G)], 3, 6, 1, "paper"),        # widths change: projections
+    ([(2, 16, 16, workload.RELU), (16, 16, 4, workload.RELU)], 5, 3, 2, "plaquette"),
+])
+def test_resnet_fp8_matches_torch(blocks, d, T, B, layout):
+    """The oracle's fp8 residual forward against the same network written
+    with PyTorch's float8_e4m3fn rounding and conv3d (fp64 sums)."""
+    weights = workload.resnet_weights(blocks, seed=d * 10 + T + 1)
+    rng = np.random.default_rng(d + T + 1)
+    H = d if layout == "paper" else d + 1
+    planes = (rng.random((B, blocks[0][0], T, H, H)) < 0.2).astype(np.float64)
+    got = oracle.forward_resnet(d, T, planes, blocks, weights, False, layout, fp8=True)
+    np.testing.assert_allclose(got, torch_resnet_fp8(planes, blocks, weights), rtol=0, atol=1e-9)
+    exact = oracle.forward_resnet(d, T, planes, blocks, weights, False, layout)
+    assert np.abs(got - exact).max() > 1e-3  # the rounding points do act
+
+
+def test_resnet_fp8_perturbed_sums():
+    """eps = 0 is the plain fp8 forward; eps > 0 moves the logits, by seed."""
+    blocks = workload.resnet_blocks([16, 16, 16])
+    d = T = 5
+    weights = workload.resnet_weights(blocks, seed=71)
+    rng = np.random.default_rng(72)
+    planes = (rng.random((2, 4, T, d, d)) < 0.2).astype(np.float64)
+    plain = oracle.forward_resnet(d, T, planes, blocks, weights, False, "paper", fp8=True)
+    zero = oracle.forward_resnet(d, T, planes, blocks, weights, False, "paper", fp8=True, fp8_sum_eps=0.0,
+                                 fp8_sum_seed=5)
+    np.testing.assert_array_equal(plain, zero)
+    a = oracle.forward_resnet(d, T, planes, blocks, weights, False, "paper", fp8=True, fp8_sum_eps=2.0 ** -16,
+                              fp8_sum_seed=1)
+    b = oracle.forward_resnet(d, T, planes, blocks, weights, False, "paper", fp8=True, fp8_sum_eps=2.0 ** -16,
+                              fp8_sum_seed=2)
+    a2 = oracle.forward_resnet(d, T, planes, blocks, weights, False, "paper", fp8=True, fp8_sum_eps=2.0 ** -16,
+                               fp8_sum_seed=1)
+    np.testing.assert_array_equal(a, a2)
+    assert np.abs(a - plain).max() > 0 and np.abs(a - b).max() > 0
