@@ -137,14 +137,17 @@ def flops_per_sample(layers, H, T):
 def bench_model6(args, torch, pdx, workload):
     """Model 6 (Sec. VI, Fig. Model8Representation: four residual blocks, 512
     channels, BatchNorm folded at create) in the paper's layout at d = T =
-    --d, batch --batch, bf16 with fp32 accumulation."""
+    --d, batch --batch, bf16 (or --dtype fp8: E4M3) with fp32 accumulation."""
     d = T = args.d or 13
     B = args.batch or 1
+    dtype = args.dtype or "bf16"
+    fp8 = dtype == "fp8"
+    peak = PEAK_FP8_TFLOPS if fp8 else PEAK_BF16_TFLOPS
     blocks = workload.MODEL6_BLOCKS
     weights = workload.resnet_weights(blocks, 4006)
     det, _ = workload.make_inputs(d, T, B, 0.003, 0.003, 5000 + d)
     torch.cuda.set_device(0)
-    pre = pdx.Predecoder(weights, d, T, None, "bf16", max_batch=B, layout="paper", first="Z", last="Z",
+    pre = pdx.Predecoder(weights, d, T, None, dtype, max_batch=B, layout="paper", first="Z", last="Z",
                          blocks=blocks)
     ddet = torch.from_numpy(det.view(np.int64)).cuda()
     flips = torch.empty((B, pre.flip_words), dtype=torch.int64, device="cuda")
@@ -174,17 +177,18 @@ def bench_model6(args, torch, pdx, workload):
         "metric": "us/round (pre-decode+residual), Model 6 (residual network) in the paper's layout at d=T=%d" % d,
         "value": ms * 1e3 / (B * T), "unit": "us/round", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": ms, "rounds_per_s": B * T / (ms * 1e-3), "higher_is_better": False, "scaling": "weak",
-        "vs_baseline": None, "dtype": "bf16",
+        "vs_baseline": None, "dtype": "fp8-e4m3" if fp8 else "bf16",
         "data": "synthetic (seeded phenomenological noise p=q=0.003, He-normal convs, random BatchNorm statistics)",
         "config": {"workload": "Model 6 of Sec. VI (blocks %s, BatchNorm folded), paper layout, d=T=%d, batch %d; "
-                               "bf16 / fp32 accumulate" % (blocks, d, B),
+                               "%s / fp32 accumulate" % (blocks, d, B, "E4M3" if fp8 else "bf16"),
                    "d": d, "T": T, "batch": B, "model": 6},
-        "mfma_frac_end_to_end": total / (ms * 1e-3) / (PEAK_BF16_TFLOPS * 1e12),
+        "mfma_frac_end_to_end": total / (ms * 1e-3) / (peak * 1e12),
         "stage_ms": {"unpack": stages[0], **{"block%d" % (k + 1): stages[1 + k] for k in range(len(blocks))},
                      "residual_repack": stages[-1]},
-        "roofline": {"kernel": "block 2: two conv3d 3x3x3 512->512 (bf16 MFMA, four 128-channel slices each)",
-                     "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None},
+        "roofline": {"kernel": "block 2: two conv3d 3x3x3 512->512 (%s MFMA, four 128-channel slices each)"
+                               % ("fp8" if fp8 else "bf16"),
+                     "bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                     "frac": achieved / peak, "traffic": None},
     }
     print(json.dumps(out), flush=True)
 

@@ -223,7 +223,9 @@ pd_status predecoder_unpack(pd_predecoder* h, void* hip_stream, const uint64_t* 
  * -- up to but not including the last block's conv2 (the output layer), and
  * c_out is that conv's width (Fig. Model8Representation).
  * PD_ERR_INVALID_ARG for a layer out of range, PD_ERR_UNSUPPORTED for
- * PD_DTYPE_FP32.  Asynchronous on hip_stream. */
+ * PD_DTYPE_FP32 and for the projection of an fp8 residual network (it is
+ * computed inside the next conv, never stored).  Asynchronous on
+ * hip_stream. */
 pd_status predecoder_activations(pd_predecoder* h, void* hip_stream, const uint64_t* det,
                                  int32_t batch, int32_t layer, void* out);
 
@@ -326,9 +328,15 @@ pd_status predecoder_run_static(pd_predecoder* h, void* hip_stream, const uint64
  * sqrt(var + eps) in fp64; weights bf16(fp32(w g)); bias fp32((b - mean) g +
  * shift)); projection weights bf16; every tensor stored between kernels
  * (activations, projection outputs) bf16; the conv2 sum plus the shortcut is
- * taken in fp32 before the activation.  Supported: PD_DTYPE_BF16, c_mid in
- * {64, 128, 256, 512}, c_out == c_mid inside the network (others
- * PD_ERR_UNSUPPORTED).  predecoder_run / residual / unpack / stage_times /
+ * taken in fp32 before the activation.  PD_DTYPE_FP8: the folded weights
+ * fp32(w g) and the projection weights as E4M3 codes with one power-of-two
+ * scale per output channel (the fp8 reading of the plain networks), every
+ * stored tensor E4M3.  The projections are computed inside the convs that
+ * use them: the first block's (from its 2 or 4 input channels) in conv2's
+ * epilogue, the last block's (when its c_in == c_mid) in the output conv;
+ * fp8 handles allow no other projection.  Supported: PD_DTYPE_BF16 and
+ * PD_DTYPE_FP8, c_mid in {64, 128, 256, 512}, c_out == c_mid inside the
+ * network (others PD_ERR_UNSUPPORTED).  predecoder_run / residual / unpack / stage_times /
  * destroy take the handle like any other (stages: unpack, one per block,
  * residual); predecoder_activations returns the output of any conv but the
  * last (see there). */

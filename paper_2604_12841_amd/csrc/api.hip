@@ -70,6 +70,7 @@ struct pd_predecoder {
   std::vector<float*> proj_w, proj_b;
   void* out_proj_frag = nullptr;  // the last block's projection as fragments of launch_conv_out (when it
                                   // runs there, fused into the output conv), else null
+  float* out_proj_bias = nullptr; // ... its [4] biases and [4] weight scales
   int cmax = 0;                  // widest activation row (channels)
   int pmax = 0;                  // widest projection output (channels; residual networks)
   int n_cu = 256;                // compute units: one persistent conv workgroup each
@@ -461,7 +462,9 @@ void free_all(pd_predecoder* h) {
   for (float* p : h->proj_w) f(p);
   for (float* p : h->proj_b) f(p);
   f(h->out_proj_frag);
+  f(h->out_proj_bias);
   h->out_proj_frag = nullptr;
+  h->out_proj_bias = nullptr;
   h->ws.act[2] = h->ws.pbuf = nullptr;
   h->proj_w.clear();
   h->proj_b.clear();
@@ -658,6 +661,9 @@ pd::Split_k split_for(const Workspace& ws, const Tiling& t, int cin, int cout, i
 pd_status enqueue_resnet(pd_predecoder* h, Workspace& ws, hipStream_t st, const uint64_t* det, int batch,
                          uint64_t* flips, uint64_t* residual, float* logits, hipEvent_t* ev, int stop, StopAt* at) {
   const Geom& g = h->g;
+  const int fp8 = h->dtype == PD_DTYPE_FP8;
+  const int ae = fp8 ? 1 : 2;  // bytes per activation value
+  const int bs = fp8 ? 2 : 1;  // bias floats per channel (fp8: biases, then weight scales, per slice)
   const int hidden_wgs = h->n_cu * pd::conv_hidden_workgroups_per_cu(3);
   int e = 0;
   auto mark = [&]() -> pd_status {
@@ -686,43 +692,43 @@ pd_status enqueue_resnet(pd_predecoder* h, Workspace& ws, hipStream_t st, const 
     const int hi = (xi + 1) % 3, yi = (xi + 2 + (xi < 0 ? 1 : 0)) % 3;
     void* hb = ws.act[hi];
     void* yb = ws.act[yi];
-    if ((s = prepare_rows(ws, hi, B.c_mid * 2, st)) != PD_OK) return s;
-    if (!last && (s = prepare_rows(ws, yi, B.c_out * 2, st)) != PD_OK) return s;
+    if ((s = prepare_rows(ws, hi, B.c_mid * ae, st)) != PD_OK) return s;
+    if (!last && (s = prepare_rows(ws, yi, B.c_out * ae, st)) != PD_OK) return s;
     // conv1: x -> hb
     {
       const int nsl = B.c_mid > 128 ? B.c_mid / 128 : 1, cw = B.c_mid / nsl;
       for (int q = 0; q < nsl && s == PD_OK; ++q) {
         const void* wq = (const char*)h->wdev[2 * k] + q * h->wslice[2 * k];
-        void* yq = (uint16_t*)hb + (size_t)q * cw;
-        if (k == 0)
+        void* yq = (char*)hb + (size_t)q * cw * ae;
+        if (k == 0)  // layer 1 (fp8: bf16 matrix work on the dequantised weights, E4M3 output)
           s = check_launch(pd::launch_conv_first(g, B.c_in, cw, B.act, x, yq, B.c_mid, wq, h->bdev[2 * k] + q * cw,
-                                                 batch, 0, 3, st));
+                                                 batch, fp8, 3, st));
         else
           s = check_launch(pd::launch_conv_hidden(g, tl, B.c_in, cw, B.act, x, yq, B.c_mid, wq,
-                                                  h->bdev[2 * k] + q * cw, 0, nullptr, nullptr, h->tables, ws.nib,
-                                                  nullptr, batch, hidden_wgs, split_for(ws, tl, B.c_in, cw, 0), 0,
-                                                  nullptr, 0, 3, st));
+                                                  h->bdev[2 * k] + (size_t)q * cw * bs, 0, nullptr, nullptr, h->tables,
+                                                  ws.nib, nullptr, batch, hidden_wgs,
+                                                  split_for(ws, tl, B.c_in, cw, fp8), fp8, nullptr, 0, 3, st));
       }
       if (s != PD_OK) return s;
-      if (stopped(hb, B.c_mid * 2)) return PD_OK;
+      if (stopped(hb, B.c_mid * ae)) return PD_OK;
     }
     // shortcut: the block input, or its 1x1x1 projection -- computed by the
-    // epilogue of conv2 from an input of a few channels (the first block),
-    // by its own kernel otherwise, and by its own kernel when it is the
-    // conv the caller stops at
+    // epilogue of conv2 from an input of a few channels (the first block)
+    // or by the output conv (the last block, its fragments built at create),
+    // else by its own kernel (bf16), which also serves a caller that stops
+    // at the projection
     const uint16_t* sc = (const uint16_t*)x;
     int sc_stride = B.c_in;
     const float* pw = nullptr;  // set: conv2 projects sc itself
     const float* pb = nullptr;
     if (h->proj_w[k]) {
-      // fused: into conv2's epilogue (an input of a few channels), or into
-      // the output conv (its fragments built at create)
       const bool fuse = (last ? h->out_proj_frag != nullptr : B.c_in <= 8) && stop != conv;
       if (fuse) {
         pw = h->proj_w[k];
         pb = h->proj_b[k];
         ++conv;  // the projection's stop number
       } else {
+        if (fp8) return PD_ERR_UNSUPPORTED;  // no stored fp8 projection
         s = check_launch(pd::launch_proj(g, x, B.c_in, B.c_in, h->proj_w[k], h->proj_b[k], B.c_out, ws.pbuf,
                                          B.c_out, batch, st));
         if (s != PD_OK) return s;
@@ -734,28 +740,28 @@ pd_status enqueue_resnet(pd_predecoder* h, Workspace& ws, hipStream_t st, const 
     // conv2: hb -> the next x (or the logits) with the shortcut added
     if (last && pw) {  // the projection fused into the output conv
       s = check_launch(pd::launch_conv_out(g, B.c_mid, hb, h->wdev[2 * k + 1], h->bdev[2 * k + 1], h->tables,
-                                           ws.nib, logits, batch, h->n_cu, 0, nullptr, 0, x, h->out_proj_frag, pb,
-                                           st));
+                                           ws.nib, logits, batch, h->n_cu, fp8, nullptr, 0, x, h->out_proj_frag,
+                                           h->out_proj_bias, st));
     } else if (last) {
       s = check_launch(pd::launch_conv_out(g, B.c_mid, hb, h->wdev[2 * k + 1], h->bdev[2 * k + 1], h->tables,
-                                           ws.nib, logits, batch, h->n_cu, 0, sc, sc_stride, nullptr, nullptr,
+                                           ws.nib, logits, batch, h->n_cu, fp8, sc, sc_stride, nullptr, nullptr,
                                            nullptr, st));
     } else {
       const int nsl = B.c_out > 128 ? B.c_out / 128 : 1, cw = B.c_out / nsl;
       for (int q = 0; q < nsl && s == PD_OK; ++q) {
         const void* wq = (const char*)h->wdev[2 * k + 1] + q * h->wslice[2 * k + 1];
         // slice q: its shortcut channels (or projection rows)
-        const uint16_t* scq = pw ? sc : sc + (size_t)q * cw;
+        const uint16_t* scq = pw ? sc : (const uint16_t*)((const char*)sc + (size_t)q * cw * ae);
         const float* pwq = pw ? pw + (size_t)q * cw * B.c_in : nullptr;
         const float* pbq = pw ? pb + (size_t)q * cw : nullptr;
-        s = check_launch(pd::launch_conv_hidden(g, tl, B.c_mid, cw, B.act, hb, (uint16_t*)yb + (size_t)q * cw,
-                                                B.c_out, wq, h->bdev[2 * k + 1] + q * cw, 4, pwq, pbq, h->tables,
-                                                ws.nib, nullptr, batch, hidden_wgs,
-                                                split_for(ws, tl, B.c_mid, cw, 0), 0, scq, sc_stride, 3, st));
+        s = check_launch(pd::launch_conv_hidden(g, tl, B.c_mid, cw, B.act, hb, (char*)yb + (size_t)q * cw * ae,
+                                                B.c_out, wq, h->bdev[2 * k + 1] + (size_t)q * cw * bs, 4, pwq, pbq,
+                                                h->tables, ws.nib, nullptr, batch, hidden_wgs,
+                                                split_for(ws, tl, B.c_mid, cw, fp8), fp8, scq, sc_stride, 3, st));
       }
     }
     if (s != PD_OK) return s;
-    if (!last && stopped(yb, B.c_out * 2)) return PD_OK;
+    if (!last && stopped(yb, B.c_out * ae)) return PD_OK;
     x = yb;
     xi = yi;
   }
@@ -1166,9 +1172,19 @@ pd_status predecoder_create_resnet(const float* weights, size_t n_weights, int32
     if (k > 0 && B.c_in != blocks[k - 1].c_out) return PD_ERR_INVALID_ARG;
   }
   if (n_weights != predecoder_resnet_weight_count(blocks, n_blocks)) return PD_ERR_INVALID_ARG;
-  // what the kernels run: bf16; widths 64, 128, 256 or 512 with c_out = c_mid
-  // inside the network
-  if (dtype != PD_DTYPE_BF16) return PD_ERR_UNSUPPORTED;
+  // what the kernels run: bf16 or fp8; widths 64, 128, 256 or 512 with
+  // c_out = c_mid inside the network; fp8: projections only where they are
+  // fused (the first block, from its few input channels, and the last, with
+  // c_in = c_mid)
+  if (dtype != PD_DTYPE_BF16 && dtype != PD_DTYPE_FP8) return PD_ERR_UNSUPPORTED;
+  if (dtype == PD_DTYPE_FP8)
+    for (int k = 0; k < n_blocks; ++k) {
+      const pd_block& B = blocks[k];
+      if (B.c_in == B.c_out) continue;
+      const bool first_ok = k == 0 && B.c_in <= 8 && n_blocks > 1;
+      const bool last_ok = k == n_blocks - 1 && B.c_in == B.c_mid;
+      if (!first_ok && !last_ok) return PD_ERR_UNSUPPORTED;
+    }
   auto width_ok = [](int c) { return c == 64 || c == 128 || c == 256 || c == 512; };
   // conv1 of a later block runs the hidden kernel from c_in to slices of
   // min(c_mid, 128) channels: the instantiated pairs
@@ -1243,8 +1259,10 @@ pd_status predecoder_create_resnet(const float* weights, size_t n_weights, int32
       hipMemset(h->ws.pbuf, 0, vox * pmax * 2) != hipSuccess)
     return fail(PD_ERR_DEVICE);
   // weights: per conv, BatchNorm folded in (g = scale / sqrt(var + 1e-5) in
-  // fp64; weights fp32(w g), rounded to bf16 by the fragment builder; bias
-  // fp32((b - mean) g + shift))
+  // fp64; weights fp32(w g), rounded to bf16 by the fragment builder or, on
+  // the fp8 path, quantised per output channel to E4M3; bias fp32((b - mean)
+  // g + shift))
+  const bool fp8 = dtype == PD_DTYPE_FP8;
   const float* src = weights;
   for (int k = 0; k < n_blocks; ++k) {
     const pd_block& B = blocks[k];
@@ -1261,16 +1279,36 @@ pd_status predecoder_create_resnet(const float* weights, size_t n_weights, int32
         for (size_t e = 0; e < (size_t)cin * 27; ++e) wf[o2 * (size_t)cin * 27 + e] = (float)((double)w[o2 * (size_t)cin * 27 + e] * gg);
         bf[o2] = (float)(((double)b[o2] - bn[2 * cout + o2]) * gg + bn[cout + o2]);
       }
+      // fp8: the folded weights' E4M3 codes and per-channel scales (and the
+      // values they stand for, for layer 1's bf16 fragments)
+      std::vector<uint8_t> codes;
+      std::vector<float> scale, wq;
+      if (fp8) quantize_e4m3(wf.data(), cout, (size_t)cin * 27, &codes, &scale, &wq);
       size_t slice = 0;
       void* wd = nullptr;
       if (c == 1 && k == n_blocks - 1) {  // the output conv, 4 filters: rows (tap, filter)
-        if (!pd::conv_out_supported(cin, 0, 3, g.H)) return fail(PD_ERR_UNSUPPORTED);
-        std::vector<uint8_t> f = out_fragments(wf.data(), nullptr, cin, false);
+        if (!pd::conv_out_supported(cin, fp8, 3, g.H)) return fail(PD_ERR_UNSUPPORTED);
+        std::vector<uint8_t> f = out_fragments(wf.data(), codes.data(), cin, fp8);
         s = upload(&wd, f.data(), f.size());
         bf.resize(8);
-        std::fill(bf.begin() + 4, bf.end(), 1.0f);  // [4] biases, then [4] weight scales of 1
+        for (int o2 = 0; o2 < 4; ++o2) bf[4 + o2] = fp8 ? scale[o2] : 1.0f;  // [4] biases, then [4] weight scales
+      } else if (fp8 && !(c == 0 && k == 0)) {
+        // E4M3 fragments per 128-channel slice; per slice its biases, then its scales
+        const int cw = cout > 128 ? 128 : cout, nsl = cout / cw;
+        std::vector<uint8_t> f;
+        std::vector<float> bd;
+        for (int q = 0; q < nsl; ++q) {
+          std::vector<uint8_t> fq = conv_fragments_fp8(codes.data() + (size_t)q * cw * cin * 27, cin, cw);
+          if (nsl > 1) slice = fq.size();
+          f.insert(f.end(), fq.begin(), fq.end());
+          bd.insert(bd.end(), bf.begin() + (size_t)q * cw, bf.begin() + (size_t)(q + 1) * cw);
+          bd.insert(bd.end(), scale.begin() + (size_t)q * cw, scale.begin() + (size_t)(q + 1) * cw);
+        }
+        bf = bd;
+        s = upload(&wd, f.data(), f.size());
       } else {
-        std::vector<uint16_t> f = fragments_sliced(wf.data(), cin, cout, &slice);
+        // bf16 fragments (fp8 layer 1: of the E4M3 values times their scales, exact in bf16)
+        std::vector<uint16_t> f = fragments_sliced(fp8 ? wq.data() : wf.data(), cin, cout, &slice);
         s = upload(&wd, f.data(), f.size() * 2);
       }
       h->wdev.push_back(wd);
@@ -1284,23 +1322,46 @@ pd_status predecoder_create_resnet(const float* weights, size_t n_weights, int32
     float* pw = nullptr;
     float* pb = nullptr;
     if (B.c_in != B.c_out) {
+      // weights: bf16 values, or (fp8) E4M3 codes with per-channel scales and
+      // the values they stand for
       const size_t np = (size_t)B.c_out * B.c_in;
-      std::vector<float> w16(np);
-      for (size_t e = 0; e < np; ++e) w16[e] = bf16_value(src[e]);
-      s = upload(&pw, w16.data(), np * 4);
+      std::vector<uint8_t> pcodes;
+      std::vector<float> pscale, pvals;
+      if (fp8) {
+        quantize_e4m3(src, B.c_out, B.c_in, &pcodes, &pscale, &pvals);
+      } else {
+        pvals.resize(np);
+        for (size_t e = 0; e < np; ++e) pvals[e] = bf16_value(src[e]);
+      }
+      s = upload(&pw, pvals.data(), np * 4);
       if (s == PD_OK) s = upload(&pb, src + np, (size_t)B.c_out * 4);
-      // the last block's projection from a wide input runs inside the output
+      // the last block's projection (c_in = c_mid) runs inside the output
       // conv: fragments [k-step][lane], lane l's row l % 32 (filters 0..3,
-      // the rest zero), ci = 16 k-step + 8 (l / 32) + e
-      if (s == PD_OK && k == n_blocks - 1 && B.c_in == B.c_mid && B.c_in >= 256) {
-        std::vector<uint16_t> pf(pd::conv_out_proj_fragment_bytes(B.c_in) / 2, 0);
-        for (int st = 0; st < B.c_in / 16; ++st)
+      // the rest zero), bf16: ci = 16 k-step + 8 (l / 32) + e; fp8 codes:
+      // ci = 64 k-step + 32 (l / 32) + e; then [4] biases and [4] scales
+      if (s == PD_OK && k == n_blocks - 1 && B.c_in == B.c_mid) {
+        const int kstep = fp8 ? 64 : 16, lb = fp8 ? 32 : 16, per = fp8 ? 32 : 8;
+        std::vector<uint8_t> pf(pd::conv_out_proj_fragment_bytes(B.c_in, fp8), 0);
+        for (int st = 0; st < B.c_in / kstep; ++st)
           for (int l = 0; l < 64; ++l)
-            for (int e = 0; e < 8; ++e) {
-              const int co = l % 32, ci = st * 16 + 8 * (l / 32) + e;
-              if (co < B.c_out) pf[((size_t)st * 64 + l) * 8 + e] = bf16_bits(src[(size_t)co * B.c_in + ci]);
+            for (int e = 0; e < per; ++e) {
+              const int co = l % 32, ci = st * kstep + per * (l / 32) + e;
+              if (co >= B.c_out) continue;
+              uint8_t* dst = &pf[((size_t)st * 64 + l) * lb];
+              if (fp8) {
+                dst[e] = pcodes[(size_t)co * B.c_in + ci];
+              } else {
+                const uint16_t v = bf16_bits(src[(size_t)co * B.c_in + ci]);
+                std::memcpy(dst + 2 * e, &v, 2);
+              }
             }
-        s = upload(&h->out_proj_frag, pf.data(), pf.size() * 2);
+        s = upload(&h->out_proj_frag, pf.data(), pf.size());
+        std::vector<float> pbias(8, 1.0f);
+        for (int o2 = 0; o2 < 4; ++o2) {
+          pbias[o2] = src[np + o2];
+          if (fp8) pbias[4 + o2] = pscale[o2];
+        }
+        if (s == PD_OK) s = upload(&h->out_proj_bias, pbias.data(), pbias.size() * 4);
       }
       src += np + B.c_out;
     }

@@ -137,10 +137,11 @@ __host__ __device__ inline int stage_slot(int q) {
 // (the others see a split of 1 at compile time and keep their registers for
 // the epilogue).  EPI_ADD: EPI_ACT with the block's shortcut added to the
 // pre-activation (the second conv of a residual block): the bf16 row of sc
-// at the output voxel, or, when head_w is given, its 1x1x1 projection
-// computed here from the sc_stride (<= 8) bf16 channels of sc's row
+// at the output voxel (fp8: E4M3 codes), or, when head_w is given, its 1x1x1
+// projection computed here from the sc_stride (<= 8) channels of sc's row
 // (head_w [c_out][sc_stride] and head_b [c_out] in those slots:
-// bf16(head_b + sum_ci head_w x_ci), an fp32 FMA chain in channel order).
+// bf16(head_b + sum_ci head_w x_ci), an fp32 FMA chain in channel order;
+// fp8: E4M3 of the same).
 enum Epi { EPI_ACT = 0, EPI_HEAD = 1, EPI_OUT = 2, EPI_PARK = 3, EPI_ADD = 4 };
 
 // Wave split of the 256 x COUT output tile: WN waves across the channels
@@ -223,8 +224,10 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t stage_rsrc(const void* x, long
 }
 
 // The projected shortcut of channels co .. co + N - 1 at padded voxel p:
-// bf16(b[c] + sum_ci w[c][ci] x[p][ci]) over the pc channels of x's row.
-template <int N>
+// b[c] + sum_ci w[c][ci] x[p][ci] over the pc channels of x's row (the
+// network's input planes, bf16 on both paths), an fp32 FMA chain in channel
+// order, rounded to bf16 (F8: to E4M3).
+template <int N, bool F8>
 __device__ __forceinline__ void project_shortcut(const uint16_t* __restrict__ x, int pc, long long p,
                                                  const float* __restrict__ w, const float* __restrict__ b, int co,
                                                  float (&s)[N]) {
@@ -238,9 +241,46 @@ __device__ __forceinline__ void project_shortcut(const uint16_t* __restrict__ x,
   }
 #pragma unroll
   for (int o = 0; o < N; o += 2) {
-    const uint32_t pk = bf16_pack(a[o], a[o + 1]);
-    s[o] = __uint_as_float(pk << 16);
-    s[o + 1] = __uint_as_float(pk & 0xFFFF0000u);
+    if constexpr (F8) {
+      s[o] = e4m3_round(a[o]);
+      s[o + 1] = e4m3_round(a[o + 1]);
+    } else {
+      const uint32_t pk = bf16_pack(a[o], a[o + 1]);
+      s[o] = __uint_as_float(pk << 16);
+      s[o + 1] = __uint_as_float(pk & 0xFFFF0000u);
+    }
+  }
+}
+
+// The block's shortcut of channels co .. co + N - 1 at padded voxel p: its
+// stored row in sc (bf16, or F8 E4M3 codes), or with w given its
+// projection from sc's few channels (the input planes).
+template <int N, bool F8>
+__device__ __forceinline__ void shortcut_of(const uint16_t* __restrict__ sc, int sc_stride, long long p,
+                                            const float* __restrict__ w, const float* __restrict__ b, int co,
+                                            float (&s)[N]) {
+  if (w) {
+    project_shortcut<N, F8>(sc, sc_stride, p, w, b, co, s);
+  } else if constexpr (F8) {
+    const uint8_t* r = (const uint8_t*)sc + p * sc_stride + co;
+#pragma unroll
+    for (int o = 0; o < N; o += 4) {
+      const uint32_t q = *reinterpret_cast<const uint32_t*>(r + o);
+      s[o] = __builtin_amdgcn_cvt_f32_fp8((int)q, 0);
+      s[o + 1] = __builtin_amdgcn_cvt_f32_fp8((int)q, 1);
+      s[o + 2] = __builtin_amdgcn_cvt_f32_fp8((int)q, 2);
+      s[o + 3] = __builtin_amdgcn_cvt_f32_fp8((int)q, 3);
+    }
+  } else {
+    const uint16_t* r = sc + p * sc_stride + co;
+#pragma unroll
+    for (int o = 0; o < N; o += 4) {
+      const u32x2 q = *reinterpret_cast<const u32x2*>(r + o);
+      s[o] = __uint_as_float(q.x << 16);
+      s[o + 1] = __uint_as_float(q.x & 0xFFFF0000u);
+      s[o + 2] = __uint_as_float(q.y << 16);
+      s[o + 3] = __uint_as_float(q.y & 0xFFFF0000u);
+    }
   }
 }
 
@@ -367,10 +407,14 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
                   const int mb = 2 * ps + m;
                   const int r = m * 32 + l32;
                   if constexpr (F8) {
-                    const float v0 = act_fn<ACT>(__builtin_fmaf(acc[mb][nb][4 * q + 0], sv.x, bv.x));
-                    const float v1 = act_fn<ACT>(__builtin_fmaf(acc[mb][nb][4 * q + 1], sv.y, bv.y));
-                    const float v2 = act_fn<ACT>(__builtin_fmaf(acc[mb][nb][4 * q + 2], sv.z, bv.z));
-                    const float v3 = act_fn<ACT>(__builtin_fmaf(acc[mb][nb][4 * q + 3], sv.w, bv.w));
+                    float sh[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+                    if constexpr (EPI == EPI_ADD) {  // the block's shortcut, 4 channels of this row
+                      if (pidx[mb] >= 0) shortcut_of<4, true>(sc, sc_stride, pidx[mb], head_w, head_b, co, sh);
+                    }
+                    const float v0 = act_fn<ACT>(__builtin_fmaf(acc[mb][nb][4 * q + 0], sv.x, bv.x) + sh[0]);
+                    const float v1 = act_fn<ACT>(__builtin_fmaf(acc[mb][nb][4 * q + 1], sv.y, bv.y) + sh[1]);
+                    const float v2 = act_fn<ACT>(__builtin_fmaf(acc[mb][nb][4 * q + 2], sv.z, bv.z) + sh[2]);
+                    const float v3 = act_fn<ACT>(__builtin_fmaf(acc[mb][nb][4 * q + 3], sv.w, bv.w) + sh[3]);
                     const int c = c8 >> 1;  // granule; byte (c8 & 1) 8 + 4 half within it
                     *(lds_u32_w*)(tb + r * 128 + ((c ^ (r & 7)) << 4) + (c8 & 1) * 8 + half * 4) =
                         e4m3_pack4(v0, v1, v2, v3);
@@ -378,16 +422,9 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
                     float4 sh = {0.0f, 0.0f, 0.0f, 0.0f};
                     if constexpr (EPI == EPI_ADD) {  // the block's shortcut, 4 channels of this row
                       if (pidx[mb] >= 0) {
-                        if (head_w) {  // projected from sc's few channels
-                          float pj[4];
-                          project_shortcut<4>(sc, sc_stride, pidx[mb], head_w, head_b, co, pj);
-                          sh = float4{pj[0], pj[1], pj[2], pj[3]};
-                        } else {
-                          const u32x2 sv =
-                              *reinterpret_cast<const u32x2*>(sc + (long long)pidx[mb] * sc_stride + co);
-                          sh = float4{__uint_as_float(sv.x << 16), __uint_as_float(sv.x & 0xFFFF0000u),
-                                      __uint_as_float(sv.y << 16), __uint_as_float(sv.y & 0xFFFF0000u)};
-                        }
+                        float pj[4];
+                        shortcut_of<4, false>(sc, sc_stride, pidx[mb], head_w, head_b, co, pj);
+                        sh = float4{pj[0], pj[1], pj[2], pj[3]};
                       }
                     }
                     const float v0 = act_fn<ACT>(acc[mb][nb][4 * q + 0] + bv.x + sh.x);
@@ -826,20 +863,10 @@ __global__ void __launch_bounds__(256) split_finish_kernel(Geom g, Tiling tl, in
     float v[8];
     sum8(grp * 8, v);
     if constexpr (EPI == EPI_ADD) {  // the block's shortcut
-      if (head_w) {  // projected from sc's few channels
-        float pj[8];
-        project_shortcut<8>(sc, sc_stride, pidx, head_w, head_b, grp * 8, pj);
+      float pj[8];
+      shortcut_of<8, F8>(sc, sc_stride, pidx, head_w, head_b, grp * 8, pj);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] += pj[e];
-      } else {
-        const uint4 sv = *reinterpret_cast<const uint4*>(sc + pidx * sc_stride + grp * 8);
-        const uint32_t sw[4] = {sv.x, sv.y, sv.z, sv.w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          v[2 * e] += __uint_as_float(sw[e] << 16);
-          v[2 * e + 1] += __uint_as_float(sw[e] & 0xFFFF0000u);
-        }
-      }
+      for (int e = 0; e < 8; ++e) v[e] += pj[e];
     }
     if constexpr (F8) {
       const uint32_t w0 = e4m3_pack4(act_fn<ACT>(v[0]), act_fn<ACT>(v[1]), act_fn<ACT>(v[2]), act_fn<ACT>(v[3]));
@@ -980,6 +1007,12 @@ hipError_t launch_case(const Geom& g, const Tiling& tl, int cin, int cout, int a
   PD_HIDDEN_CASE(128, 128, EPI_HEAD)
   PD_HIDDEN_CASE(64, 128, EPI_HEAD)
   PD_HIDDEN_CASE(128, 64, EPI_HEAD)
+  // the residual network's layers (bf16 and fp8)
+  PD_HIDDEN_CASE(512, 128, EPI_ACT)
+  PD_HIDDEN_CASE(64, 64, EPI_ADD)
+  PD_HIDDEN_CASE(128, 128, EPI_ADD)
+  PD_HIDDEN_CASE(256, 128, EPI_ADD)
+  PD_HIDDEN_CASE(512, 128, EPI_ADD)
   if constexpr (!F8) {
     PD_HIDDEN_CASE5(64, 64, EPI_ACT)
     PD_HIDDEN_CASE5(128, 128, EPI_ACT)
@@ -989,12 +1022,6 @@ hipError_t launch_case(const Geom& g, const Tiling& tl, int cin, int cout, int a
     // the 5x5x5 output layer (3x3x3 ones run on launch_conv_out)
     PD_HIDDEN_CASE5(64, 32, EPI_OUT)
     PD_HIDDEN_CASE5(128, 32, EPI_OUT)
-    // the residual network's layers (bf16)
-    PD_HIDDEN_CASE(512, 128, EPI_ACT)
-    PD_HIDDEN_CASE(64, 64, EPI_ADD)
-    PD_HIDDEN_CASE(128, 128, EPI_ADD)
-    PD_HIDDEN_CASE(256, 128, EPI_ADD)
-    PD_HIDDEN_CASE(512, 128, EPI_ADD)
   }
 #undef PD_HIDDEN_CASE
 #undef PD_HIDDEN_CASE5

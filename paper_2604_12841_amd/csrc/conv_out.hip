@@ -32,11 +32,12 @@
 //
 // Residual networks: the last block's shortcut is added to the logits --
 // the block input itself, or its 1x1x1 projection (c_in -> 4) computed here
-// as more k-steps of the same GEMM: each wave group takes half of the block
-// input's channels against projection fragments whose rows 0..3 are the
-// four filters, into an accumulator of its own; the two halves land in two
-// more LDS slots and the output's own voxel adds them, the projection's
-// bias, and rounds to bf16 (the stored shortcut of the unfused path).
+// as more k-steps of the same GEMM: the wave groups take alternate chunks of
+// the block input's channels against projection fragments whose rows 0..3
+// are the four filters, into an accumulator of their own; the two groups'
+// sums land in two more LDS slots and the output's own voxel adds them,
+// scales them (fp8), adds the projection's bias and rounds to the stored
+// precision (bf16, or E4M3), the shortcut of the unfused path.
 //
 // Waves: wave w takes row blocks 2 (w % 2), 2 (w % 2) + 1 and voxel blocks
 // w / 2, w / 2 + 2, ...: each weight fragment feeds up to four MFMAs and
@@ -120,33 +121,34 @@ __device__ __forceinline__ Unit unit_of(const Geom& g, int u, int nch, int nsi, 
 
 // wfrag: [rb][k-step][lane] fragments of LQ x 16 bytes (rows past tap 26 are
 // zero); bias: [4] biases, then [4] weight scales (1 on the bf16 path).
-// PROJ (bf16): px holds the block input (CIN channels, the layout of x),
-// pfrag its projection fragments [k-step][lane] (rows 0..3 the filters),
-// pbias the projection's 4 biases.
+// PROJ: px holds the block input (CIN channels, the layout of x), pfrag its
+// projection fragments [k-step][lane] (LQ x 16 bytes, rows 0..3 the
+// filters), pbias the projection's 4 biases then its 4 weight scales.
 template <int CIN, bool F8, bool PROJ>
 __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1)))
 conv_out_kernel(Geom g, int nch, int nsi, int nsj, const void* __restrict__ x, const u32x4* __restrict__ wfrag,
                 const float* __restrict__ bias, const int32_t* __restrict__ tables, uint8_t* __restrict__ nib,
                 float* __restrict__ logits, const uint16_t* __restrict__ sc, int sc_stride,
                 const void* __restrict__ px, const u32x4* __restrict__ pfrag, const float* __restrict__ pbias) {
-  static_assert(!PROJ || !F8, "projected shortcuts run on the bf16 path");
   using PR = OutPrec<F8>;
   constexpr int KSTEP = PR::KSTEP, LQ = PR::LQ;
   constexpr int ESZ = F8 ? 1 : 2;
   constexpr int ROW = CIN * ESZ;                      // bytes per activation row
-  constexpr int CH = CIN <= 128 ? CIN : 64;           // input channels per chunk (wider inputs: 64, fewer registers)
+  // input channels per chunk: all of them up to 128 (weights loaded once per
+  // unit), else (and with a projection, whose chunks reload them) 64
+  constexpr int CH = (CIN <= 128 && !PROJ) ? CIN : 64;
   constexpr int NCH = CIN / CH;                       // chunks
   constexpr int KPC = CH / KSTEP;                     // k-steps per chunk
   constexpr int NKS = CIN / KSTEP;                    // k-steps in all
-  constexpr int NPC = PROJ ? NCH / 2 : 0;             // projection chunks per wave group (half the input)
-  constexpr int NCT = NCH + NPC;                      // chunks of a round
-  static_assert(!PROJ || NCH % 2 == 0, "the projection's channels split in two");
   extern __shared__ __attribute__((aligned(16))) char smem[];
   lds_f32x4* const pl = (lds_f32x4*)smem;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, l32 = lane & 31;
   const int rp = wave & 1, bh = wave >> 1;  // row blocks 2 rp, 2 rp + 1; voxel blocks bh, bh + 2, ...
+  // chunks of a round: the conv's, then (PROJ) the projection chunks rp,
+  // rp + 2, ... of the block input
+  const int nct = NCH + (PROJ ? (NCH - rp + 1) / 2 : 0);
 
   const Unit un = unit_of(g, blockIdx.x, nch, nsi, nsj);
   const int H = g.H;
@@ -205,9 +207,11 @@ conv_out_kernel(Geom g, int nch, int nsi, int nsj, const void* __restrict__ x, c
   u32x4 wa[2][KPC][LQ];
   auto load_w = [&](int c) {
     if (PROJ && c >= NCH) {
-      const int k0 = (rp * NPC + c - NCH) * KPC;
+      const int k0 = (rp + 2 * (c - NCH)) * KPC;
 #pragma unroll
-      for (int s = 0; s < KPC; ++s) wa[0][s][0] = pfrag[(size_t)(k0 + s) * 64 + lane];
+      for (int s = 0; s < KPC; ++s)
+#pragma unroll
+        for (int q = 0; q < LQ; ++q) wa[0][s][q] = pfrag[((size_t)(k0 + s) * 64 + lane) * LQ + q];
       return;
     }
 #pragma unroll
@@ -225,9 +229,12 @@ conv_out_kernel(Geom g, int nch, int nsi, int nsj, const void* __restrict__ x, c
 #pragma unroll
   for (int k = 0; k < 3; ++k) run[k] = f32x4{0.f, 0.f, 0.f, 0.f};
   shr[0] = shr[1] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float pbs[4];
+  float pbs[4], psc[4];
 #pragma unroll
-  for (int o = 0; o < 4; ++o) pbs[o] = PROJ ? pbias[o] : 0.0f;
+  for (int o = 0; o < 4; ++o) {
+    pbs[o] = PROJ ? pbias[o] : 0.0f;
+    psc[o] = PROJ ? pbias[4 + o] : 1.0f;
+  }
 
   auto emit = [&](int t, const f32x4& s, const f32x4& sh) {
     if (!owner || t < un.t0 || t >= un.t1) return;
@@ -237,12 +244,21 @@ conv_out_kernel(Geom g, int nch, int nsi, int nsj, const void* __restrict__ x, c
     if (PROJ) {
 #pragma unroll
       for (int o = 0; o < 4; ++o) lg[o] += sh[o];
-    } else if (sc) {  // residual shortcut of the last block: 4 bf16 channels
-      const uint2 sv = *reinterpret_cast<const uint2*>(sc + padded_index(g, un.b, t, oi, oj) * sc_stride);
-      lg[0] += __uint_as_float(sv.x << 16);
-      lg[1] += __uint_as_float(sv.x & 0xFFFF0000u);
-      lg[2] += __uint_as_float(sv.y << 16);
-      lg[3] += __uint_as_float(sv.y & 0xFFFF0000u);
+    } else if (sc) {  // residual shortcut of the last block: 4 channels (bf16, or E4M3 codes)
+      const long long pi = padded_index(g, un.b, t, oi, oj) * sc_stride;
+      if constexpr (F8) {
+        const uint32_t q = *reinterpret_cast<const uint32_t*>((const uint8_t*)sc + pi);
+        lg[0] += __builtin_amdgcn_cvt_f32_fp8((int)q, 0);
+        lg[1] += __builtin_amdgcn_cvt_f32_fp8((int)q, 1);
+        lg[2] += __builtin_amdgcn_cvt_f32_fp8((int)q, 2);
+        lg[3] += __builtin_amdgcn_cvt_f32_fp8((int)q, 3);
+      } else {
+        const uint2 sv = *reinterpret_cast<const uint2*>(sc + pi);
+        lg[0] += __uint_as_float(sv.x << 16);
+        lg[1] += __uint_as_float(sv.x & 0xFFFF0000u);
+        lg[2] += __uint_as_float(sv.y << 16);
+        lg[3] += __uint_as_float(sv.y & 0xFFFF0000u);
+      }
     }
     const int HH = H * H, s2 = oi * H + oj;
     nib[(long long)un.b * g.V + (long long)t * HH + s2] = (uint8_t)flip_bits(allowed, lg);
@@ -261,7 +277,7 @@ conv_out_kernel(Geom g, int nch, int nsi, int nsj, const void* __restrict__ x, c
   auto load_x = [&](int k, int t, int c) {
     const char* src = bsrc[k] + (long long)t * g.P * ROW;
     if (PROJ && c >= NCH)
-      src += pdelta + (rp * NPC + c - NCH) * CH * ESZ;
+      src += pdelta + (rp + 2 * (c - NCH)) * CH * ESZ;
     else
       src += c * CH * ESZ;
 #pragma unroll
@@ -289,19 +305,19 @@ conv_out_kernel(Geom g, int nch, int nsi, int nsj, const void* __restrict__ x, c
 #pragma unroll
       for (int e = 0; e < 16; ++e) accp[k][e] = 0.0f;
 #pragma unroll 1
-    for (int c = 0; c < NCT; ++c) {
-      if constexpr (NCT > 1) load_w(c);
-      const bool more = c + 1 < NCT || tin + 1 < tb;  // a next (round, chunk) to prefetch
-      const int tn = c + 1 < NCT ? tin : tin + 1, cn = c + 1 < NCT ? c + 1 : 0;
+    for (int c = 0; c < nct; ++c) {
+      if (NCH > 1 || PROJ) load_w(c);
+      const bool more = c + 1 < nct || tin + 1 < tb;  // a next (round, chunk) to prefetch
+      const int tn = c + 1 < nct ? tin : tin + 1, cn = c + 1 < nct ? c + 1 : 0;
 #pragma unroll
       for (int k = 0; k < BPW; ++k) {
         if (k >= nbw) break;  // uniform per wave
         if (PROJ && c >= NCH) {
 #pragma unroll
           for (int s = 0; s < KPC; ++s) {
-            u32x4 a2[2] = {wa[0][s][0], wa[0][s][0]};
-            u32x4 b2[2] = {xb[k][s][0], xb[k][s][0]};
-            accp[k] = mma(a2, b2, accp[k], false);
+            u32x4 a2[2] = {wa[0][s][0], wa[0][s][LQ - 1]};
+            u32x4 b2[2] = {xb[k][s][0], xb[k][s][LQ - 1]};
+            accp[k] = mma(a2, b2, accp[k], F8);
           }
         } else {
 #pragma unroll
@@ -347,14 +363,18 @@ conv_out_kernel(Geom g, int nch, int nsi, int nsj, const void* __restrict__ x, c
 #pragma unroll
         for (int n = 0; n < 9; ++n) run[2 - kt] += p[n];
       }
-      if (PROJ) {  // the output's own voxel in round tin: its projected shortcut, rounded to bf16
+      if (PROJ) {  // the output's own voxel in round tin: its projected shortcut, rounded as stored
         const f32x4 a = pl[32 * PSTR + nbr[4]], b = pl[33 * PSTR + nbr[4]];
         float sp[4];
 #pragma unroll
-        for (int o = 0; o < 4; ++o) sp[o] = (a[o] + b[o]) + pbs[o];
-        const uint32_t p01 = bf16_pack(sp[0], sp[1]), p23 = bf16_pack(sp[2], sp[3]);
-        shr[1] = f32x4{__uint_as_float(p01 << 16), __uint_as_float(p01 & 0xFFFF0000u), __uint_as_float(p23 << 16),
-                       __uint_as_float(p23 & 0xFFFF0000u)};
+        for (int o = 0; o < 4; ++o) sp[o] = __builtin_fmaf(a[o] + b[o], psc[o], pbs[o]);
+        if constexpr (F8) {
+          shr[1] = f32x4{e4m3_round(sp[0]), e4m3_round(sp[1]), e4m3_round(sp[2]), e4m3_round(sp[3])};
+        } else {
+          const uint32_t p01 = bf16_pack(sp[0], sp[1]), p23 = bf16_pack(sp[2], sp[3]);
+          shr[1] = f32x4{__uint_as_float(p01 << 16), __uint_as_float(p01 & 0xFFFF0000u),
+                         __uint_as_float(p23 << 16), __uint_as_float(p23 & 0xFFFF0000u)};
+        }
       }
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the sums' reads are done before the next stores
@@ -378,7 +398,7 @@ size_t conv_out_fragment_bytes(int cin, int fp8) {
 
 bool conv_out_supported(int cin, int fp8, int ks, int H) {
   if (ks != 3) return false;
-  if (!(cin == 64 || cin == 128 || cin == 256 || (cin == 512 && !fp8))) return false;
+  if (!(cin == 64 || cin == 128 || cin == 256 || cin == 512)) return false;
   int nsi, nsj;
   return conv_out_split(H, MV, &nsi, &nsj) > 0;
 }
@@ -412,7 +432,7 @@ hipError_t launch_conv_out(const Geom& g, int cin, const void* x, const void* wf
                            const float* pbias, hipStream_t stream) {
   if (g.pad != 1 || batch < 1 || !conv_out_supported(cin, fp8, 3, g.H)) return hipErrorInvalidValue;
   const bool proj = px != nullptr;
-  if (proj && (fp8 || cin < 256 || !pfrag || !pbias || sc)) return hipErrorInvalidValue;
+  if (proj && (!pfrag || !pbias || sc)) return hipErrorInvalidValue;
   int nsi = 1, nsj = 1;
   conv_out_split(g.H, MV, &nsi, &nsj);
   // rounds per unit: the split of T that minimises (units per CU, rounded
@@ -442,8 +462,17 @@ hipError_t launch_conv_out(const Geom& g, int cin, const void* x, const void* wf
                        pbias);
     return hipGetLastError();
   };
-  if (proj) {
+  if (proj && fp8) {
     switch (cin) {
+      case 64: return go(conv_out_kernel<64, true, true>, true);
+      case 128: return go(conv_out_kernel<128, true, true>, true);
+      case 256: return go(conv_out_kernel<256, true, true>, true);
+      case 512: return go(conv_out_kernel<512, true, true>, true);
+    }
+  } else if (proj) {
+    switch (cin) {
+      case 64: return go(conv_out_kernel<64, false, true>, true);
+      case 128: return go(conv_out_kernel<128, false, true>, true);
       case 256: return go(conv_out_kernel<256, false, true>, true);
       case 512: return go(conv_out_kernel<512, false, true>, true);
     }
@@ -452,6 +481,7 @@ hipError_t launch_conv_out(const Geom& g, int cin, const void* x, const void* wf
       case 64: return go(conv_out_kernel<64, true, false>, false);
       case 128: return go(conv_out_kernel<128, true, false>, false);
       case 256: return go(conv_out_kernel<256, true, false>, false);
+      case 512: return go(conv_out_kernel<512, true, false>, false);
     }
   } else {
     switch (cin) {
@@ -464,6 +494,6 @@ hipError_t launch_conv_out(const Geom& g, int cin, const void* x, const void* wf
   return hipErrorInvalidValue;
 }
 
-size_t conv_out_proj_fragment_bytes(int cin) { return (size_t)(cin / 16) * 64 * 16; }
+size_t conv_out_proj_fragment_bytes(int cin, int fp8) { return (size_t)(cin / (fp8 ? 64 : 16)) * 64 * (fp8 ? 32 : 16); }
 
 }  // namespace pd

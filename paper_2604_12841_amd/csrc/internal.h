@@ -198,11 +198,11 @@ int conv_hidden_workgroups_per_cu(int ks);
 // through the rounds: fragments of conv_out_fragment_bytes(c_in, fp8) bytes
 // ([row block][k-step][lane], rows (tap, filter)), bias [4] then the four
 // weight scales (1 on the bf16 path); sc: optional bf16 shortcut rows (4
-// channels at sc_stride); px (bf16, c_in 256 or 512, no sc): the block
+// channels at sc_stride; E4M3 codes on the fp8 path); px (no sc): the block
 // input whose 1x1x1 projection is the shortcut, pfrag its fragments
-// (conv_out_proj_fragment_bytes: [k-step][lane], 16 bytes, rows 0..3 the
-// filters) and pbias its 4 biases.  Supported: c_in 64, 128, 256, or 512
-// (bf16), a halo of one, grids whose rectangles fit (conv_out_split: the
+// (conv_out_proj_fragment_bytes: [k-step][lane], 16 bytes (fp8: 32 of
+// codes), rows 0..3 the filters) and pbias its 4 biases then 4 weight
+// scales.  Supported: c_in 64, 128, 256 or 512, a halo of one, grids whose rectangles fit (conv_out_split: the
 // split of an H x H grid into rectangles of at most maxv voxels with their
 // rims).
 hipError_t launch_conv_out(const Geom& g, int cin, const void* x, const void* wfrag, const float* bias,
@@ -210,7 +210,7 @@ hipError_t launch_conv_out(const Geom& g, int cin, const void* x, const void* wf
                            const uint16_t* sc, int sc_stride, const void* px, const void* pfrag,
                            const float* pbias, hipStream_t stream);
 size_t conv_out_fragment_bytes(int cin, int fp8);
-size_t conv_out_proj_fragment_bytes(int cin);
+size_t conv_out_proj_fragment_bytes(int cin, int fp8);
 bool conv_out_supported(int cin, int fp8, int ks, int H);
 long long conv_out_split(int H, int maxv, int* nsi, int* nsj);
 

@@ -21,6 +21,11 @@ RESNET_CASES = [
 ]
 
 
+# the cases the fp8 path runs (projections only in the first and the last
+# block, where they are fused)
+RESNET_FP8_CASES = [c for c in RESNET_CASES if c["name"] not in ("mid_projection", "narrowing")]
+
+
 def case_inputs(case):
     """(weights, det, first, last) of a case."""
     weights = workload.resnet_weights(case["blocks"], seed=81 + case["d"])

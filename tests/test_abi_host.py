@@ -252,7 +252,11 @@ def test_create_resnet_rejects_misuse(blocks, n_weights):
 
 
 @pytest.mark.parametrize("blocks,dtype", [
-    (RB, pdx.DTYPE_FP8),                                # bf16 only
+    (RB, pdx.DTYPE_FP32),                               # bf16 and fp8 only
+    # fp8: a projection in a middle block (its projection kernel is bf16 only)
+    ([(4, 64, 64, 1), (64, 128, 128, 1), (128, 128, 4, 1)], pdx.DTYPE_FP8),
+    # fp8: a last-block projection whose input width differs from c_mid
+    ([(4, 64, 64, 1), (64, 128, 4, 1)], pdx.DTYPE_FP8),
     ([(4, 96, 96, 1), (96, 96, 4, 1)], pdx.DTYPE_BF16),  # width 96
     ([(4, 64, 128, 1), (128, 128, 4, 1)], pdx.DTYPE_BF16),  # c_out != c_mid inside the network
 ])
@@ -262,8 +266,9 @@ def test_create_resnet_unsupported(blocks, dtype):
 
 
 @pytest.mark.skipif(gpu_available(), reason="checks the no-device error path")
-def test_create_resnet_without_device_reports_device_error():
-    assert _create_resnet(RW, 5, 3, RB) == pdx.PD_ERR_DEVICE
+@pytest.mark.parametrize("dtype", [pdx.DTYPE_BF16, pdx.DTYPE_FP8])
+def test_create_resnet_without_device_reports_device_error(dtype):
+    assert _create_resnet(RW, 5, 3, RB, dtype=dtype) == pdx.PD_ERR_DEVICE
 
 
 def test_graph_create_rejects_null_handle():

@@ -66,11 +66,13 @@ def test_resnet_parity(cuda, case):
 # the flips and residual against the threshold of the GPU's own logits;
 # nothing is excused anywhere.
 
-def _folded(weights, blocks):
+def _folded(weights, blocks, quant=None):
     """Per block: (w1, b1, w2, b2, wp, bp) as fp64 tensors, BatchNorm folded
     (g = scale / sqrt(var + 1e-5) in fp64, w bf16(fp32(w g)), b fp32((b -
     mean) g + shift)); wp, bp the projection (bf16 weights, fp32 bias) or
-    None."""
+    None.  quant: another rounding of the fp32 weights [c_out][...] (the fp8
+    path's per-channel scaled E4M3) in place of bf16."""
+    quant = quant or tight.q_bf16
     out, off = [], 0
 
     def take(n):
@@ -86,12 +88,12 @@ def _folded(weights, blocks):
             b = take(cout)
             scale, shift, mean, var = (take(cout) for _ in range(4))
             g = scale / np.sqrt(var + 1e-5)
-            wf = tight.q_bf16(torch.from_numpy((w * g.reshape(-1, 1, 1, 1, 1)).astype(np.float32).astype(np.float64)))
+            wf = quant(torch.from_numpy((w * g.reshape(-1, 1, 1, 1, 1)).astype(np.float32).astype(np.float64)))
             bf = torch.from_numpy(((b - mean) * g + shift).astype(np.float32).astype(np.float64))
             convs += [wf, bf]
         wp = bp = None
         if ci != co:
-            wp = tight.q_bf16(torch.from_numpy(take(co * ci).reshape(co, ci, 1, 1, 1)))
+            wp = quant(torch.from_numpy(take(co * ci).reshape(co, ci, 1, 1, 1).astype(np.float32).astype(np.float64)))
             bp = torch.from_numpy(take(co).astype(np.float32).astype(np.float64))
         out.append(tuple(convs) + (wp, bp))
     assert off == weights.size

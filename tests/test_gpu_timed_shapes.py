@@ -2,7 +2,7 @@
 to 5 of Table models in the paper's layout at 13^3, 21^3 and 31^3
 (batch 1, where the K loops are split, and batch 64), in bf16 and, for
 Models 1, 2, 4 and 5, in fp8; Model 6 at 13^3, 21^3 and 31^3 (batch 1 and
-16).  Each
+16) in bf16 and fp8.  Each
 run is the launch configuration the benchmark times (one handle, the whole
 batch); sampled samples (first and last) are compared with the oracle under
 the parity rule of parity.py, every sample's residual with the oracle's
@@ -68,21 +68,24 @@ def test_paper_model_at_timed_shape(cuda, model, d, batch, dtype):
     _check(d, T, dtype, det, rows, flips, res, logits, ref, TOL[dtype])
 
 
-M6_CASES = [(13, 1), (13, 16), (21, 1), (21, 16), (31, 1), (31, 16)]
+RESNET_FP8_TOL = json.load(open(os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                                             "resnet_fp8_tolerance.json")))["tol_max_abs_logit_err"]
+M6_CASES = [(d, b, dt) for dt in ("bf16", "fp8") for d in (13, 21, 31) for b in (1, 16)]
 
 
-@pytest.mark.parametrize("d,batch", M6_CASES, ids=["d%d_b%d" % c for c in M6_CASES])
-def test_model6_at_timed_shape(cuda, d, batch):
+@pytest.mark.parametrize("d,batch,dtype", M6_CASES, ids=["d%d_b%d_%s" % c for c in M6_CASES])
+def test_model6_at_timed_shape(cuda, d, batch, dtype):
     T = d
     blocks = workload.MODEL6_BLOCKS
     weights = workload.resnet_weights(blocks, 4006)  # the benchmark's weights
     det = _inputs(d, batch)
     rows = [0] if batch == 1 else [0, batch - 1]
-    say("Model 6 d = T =", d, "batch", batch)
-    pre = pdx.Predecoder(weights, d, T, None, "bf16", max_batch=batch, layout="paper", first="Z", last="Z",
+    say("Model 6 d = T =", d, "batch", batch, dtype)
+    pre = pdx.Predecoder(weights, d, T, None, dtype, max_batch=batch, layout="paper", first="Z", last="Z",
                          blocks=blocks)
     flips, res, logits = run_gpu(pre, det)
     pre.close()
-    ref = oracle.run_resnet(d, T, det[rows], blocks, weights, bf16=True, layout="paper", first="Z", last="Z")
-    _check(d, T, "bf16", det, rows, flips, res, logits, ref, RESNET_TOL)
+    ref = oracle.run_resnet(d, T, det[rows], blocks, weights, bf16=dtype == "bf16", layout="paper", first="Z",
+                            last="Z", fp8=dtype == "fp8")
+    _check(d, T, dtype, det, rows, flips, res, logits, ref, RESNET_TOL if dtype == "bf16" else RESNET_FP8_TOL)
 
