@@ -630,7 +630,9 @@ struct StopAt {
 // one unsplit launch beats two parts by 3 us; for 128 channels at 13^3 the
 // split saves 20 us.)  fp8 chunks are 32 channels with about half a bf16
 // chunk's matrix time per channel; a 5x5x5 chunk has 125 taps instead of 27.
-pd::Split_k split_for(const Workspace& ws, const Tiling& t, int cin, int cout, int fp8, int ks = 3) {
+// nsl: the layer's output-channel slices of cout channels, all in the one
+// launch (each is a unit of its own per tile and part).
+pd::Split_k split_for(const Workspace& ws, const Tiling& t, int cin, int cout, int fp8, int ks = 3, int nsl = 1) {
   const int kch = pd::conv_hidden_chunk_channels(fp8);
   const int nch = cin / kch;
   const double wide = cout > 64 ? 1.0 : 0.0;
@@ -638,8 +640,9 @@ pd::Split_k split_for(const Workspace& ws, const Tiling& t, int cin, int cout, i
   const double epi = 3.3 + 4.0 * wide, park = 1.75 + 1.65 * wide;
   const double finish = 8.0;
   pd::Split_k sk{0, ws.partial, ws.max_units};
+  while ((1 << sk.lsl) < nsl) ++sk.lsl;
   double best = nch * chunk + epi;
-  for (int k = 1; nch % (1 << k) == 0 && (t.ntiles << k) <= ws.max_units; ++k) {
+  for (int k = 1; nch % (1 << k) == 0 && (t.ntiles << (k + sk.lsl)) <= ws.max_units; ++k) {
     const double est = (nch >> k) * chunk + park + finish;
     if (est < best) {
       best = est;
@@ -663,7 +666,6 @@ pd_status enqueue_resnet(pd_predecoder* h, Workspace& ws, hipStream_t st, const 
   const Geom& g = h->g;
   const int fp8 = h->dtype == PD_DTYPE_FP8;
   const int ae = fp8 ? 1 : 2;  // bytes per activation value
-  const int bs = fp8 ? 2 : 1;  // bias floats per channel (fp8: biases, then weight scales, per slice)
   const int hidden_wgs = h->n_cu * pd::conv_hidden_workgroups_per_cu(3);
   int e = 0;
   auto mark = [&]() -> pd_status {
@@ -694,20 +696,24 @@ pd_status enqueue_resnet(pd_predecoder* h, Workspace& ws, hipStream_t st, const 
     void* yb = ws.act[yi];
     if ((s = prepare_rows(ws, hi, B.c_mid * ae, st)) != PD_OK) return s;
     if (!last && (s = prepare_rows(ws, yi, B.c_out * ae, st)) != PD_OK) return s;
-    // conv1: x -> hb
+    // conv1: x -> hb (a layer wider than 128 channels: slices of 128 output
+    // channels, each with its fragments, biases (fp8: and scales) and output
+    // columns; the hidden kernel runs all of them in one launch)
     {
       const int nsl = B.c_mid > 128 ? B.c_mid / 128 : 1, cw = B.c_mid / nsl;
-      for (int q = 0; q < nsl && s == PD_OK; ++q) {
-        const void* wq = (const char*)h->wdev[2 * k] + q * h->wslice[2 * k];
-        void* yq = (char*)hb + (size_t)q * cw * ae;
-        if (k == 0)  // layer 1 (fp8: bf16 matrix work on the dequantised weights, E4M3 output)
+      if (k == 0) {
+        for (int q = 0; q < nsl && s == PD_OK; ++q) {
+          const void* wq = (const char*)h->wdev[2 * k] + q * h->wslice[2 * k];
+          void* yq = (char*)hb + (size_t)q * cw * ae;
+          // layer 1 (fp8: bf16 matrix work on the dequantised weights, E4M3 output)
           s = check_launch(pd::launch_conv_first(g, B.c_in, cw, B.act, x, yq, B.c_mid, wq, h->bdev[2 * k] + q * cw,
                                                  batch, fp8, 3, st));
-        else
-          s = check_launch(pd::launch_conv_hidden(g, tl, B.c_in, cw, B.act, x, yq, B.c_mid, wq,
-                                                  h->bdev[2 * k] + (size_t)q * cw * bs, 0, nullptr, nullptr, h->tables,
-                                                  ws.nib, nullptr, batch, hidden_wgs,
-                                                  split_for(ws, tl, B.c_in, cw, fp8), fp8, nullptr, 0, 3, st));
+        }
+      } else {
+        s = check_launch(pd::launch_conv_hidden(g, tl, B.c_in, cw, B.act, x, hb, B.c_mid, h->wdev[2 * k],
+                                                h->bdev[2 * k], 0, nullptr, nullptr, h->tables, ws.nib, nullptr,
+                                                batch, hidden_wgs, split_for(ws, tl, B.c_in, cw, fp8, 3, nsl), fp8,
+                                                nullptr, 0, 3, st));
       }
       if (s != PD_OK) return s;
       if (stopped(hb, B.c_mid * ae)) return PD_OK;
@@ -746,19 +752,12 @@ pd_status enqueue_resnet(pd_predecoder* h, Workspace& ws, hipStream_t st, const 
       s = check_launch(pd::launch_conv_out(g, B.c_mid, hb, h->wdev[2 * k + 1], h->bdev[2 * k + 1], h->tables,
                                            ws.nib, logits, batch, h->n_cu, fp8, sc, sc_stride, nullptr, nullptr,
                                            nullptr, st));
-    } else {
+    } else {  // slices as for conv1, each also with its shortcut channels (or projection rows)
       const int nsl = B.c_out > 128 ? B.c_out / 128 : 1, cw = B.c_out / nsl;
-      for (int q = 0; q < nsl && s == PD_OK; ++q) {
-        const void* wq = (const char*)h->wdev[2 * k + 1] + q * h->wslice[2 * k + 1];
-        // slice q: its shortcut channels (or projection rows)
-        const uint16_t* scq = pw ? sc : (const uint16_t*)((const char*)sc + (size_t)q * cw * ae);
-        const float* pwq = pw ? pw + (size_t)q * cw * B.c_in : nullptr;
-        const float* pbq = pw ? pb + (size_t)q * cw : nullptr;
-        s = check_launch(pd::launch_conv_hidden(g, tl, B.c_mid, cw, B.act, hb, (char*)yb + (size_t)q * cw * ae,
-                                                B.c_out, wq, h->bdev[2 * k + 1] + (size_t)q * cw * bs, 4, pwq, pbq,
-                                                h->tables, ws.nib, nullptr, batch, hidden_wgs,
-                                                split_for(ws, tl, B.c_mid, cw, fp8), fp8, scq, sc_stride, 3, st));
-      }
+      s = check_launch(pd::launch_conv_hidden(g, tl, B.c_mid, cw, B.act, hb, yb, B.c_out, h->wdev[2 * k + 1],
+                                              h->bdev[2 * k + 1], 4, pw, pb, h->tables, ws.nib, nullptr, batch,
+                                              hidden_wgs, split_for(ws, tl, B.c_mid, cw, fp8, 3, nsl), fp8, sc,
+                                              sc_stride, 3, st));
     }
     if (s != PD_OK) return s;
     if (!last && stopped(yb, B.c_out * ae)) return PD_OK;
@@ -821,20 +820,21 @@ pd_status enqueue_run(pd_predecoder* h, Workspace& ws, hipStream_t st, const uin
     } else {
       // a 256-wide layer runs as two slices of 128 output channels over the
       // same input (slice k: its fragments, biases (fp8: and scales) and
-      // output channels)
+      // output channels): two launches of layer 1's kernel, one of the
+      // hidden kernel
       const int nsl = h->wslice[l] ? 2 : 1, cw = L.c_out / nsl;
-      for (int k = 0; k < nsl && s == PD_OK; ++k) {
-        const void* wk = (const char*)h->wdev[l] + k * h->wslice[l];
-        void* yk = (char*)y + (size_t)k * cw * aelem;
-        if (l == 0)
+      if (l == 0) {
+        for (int k = 0; k < nsl && s == PD_OK; ++k) {
+          const void* wk = (const char*)h->wdev[l] + k * h->wslice[l];
+          void* yk = (char*)y + (size_t)k * cw * aelem;
           s = check_launch(pd::launch_conv_first(g, L.c_in, cw, L.act, x, yk, L.c_out, wk, h->bdev[l] + k * cw,
                                                  batch, fp8, ks, st));
-        else  // the last hidden layer may carry the head and the threshold in its epilogue
-          s = check_launch(pd::launch_conv_hidden(g, tl, L.c_in, cw, L.act, x, yk, L.c_out, wk,
-                                                  h->bdev[l] + k * cw * (fp8 ? 2 : 1), fuse_head ? 1 : 0,
-                                                  h->head_w, h->head_b, h->tables, ws.nib, logits, batch,
-                                                  hidden_wgs, split_for(ws, tl, L.c_in, cw, fp8, ks), fp8, nullptr, 0,
-                                                  ks, st));
+        }
+      } else {  // the last hidden layer may carry the head and the threshold in its epilogue
+        s = check_launch(pd::launch_conv_hidden(g, tl, L.c_in, cw, L.act, x, y, L.c_out, h->wdev[l], h->bdev[l],
+                                                fuse_head ? 1 : 0, h->head_w, h->head_b, h->tables, ws.nib, logits,
+                                                batch, hidden_wgs, split_for(ws, tl, L.c_in, cw, fp8, ks, nsl), fp8,
+                                                nullptr, 0, ks, st));
       }
       head_done = fuse_head && l > 0;
     }

@@ -164,13 +164,17 @@ struct Split {
 // per-channel weight scales [COUT] (fp8) and the head weights [4][COUT].
 // The head epilogue puts its partial sums in the staging buffer the tile
 // read last.
+constexpr int kMaxSlices = 4;  // output-channel slices of one launch
+
 template <int COUT, int KS>
 struct Lds {
   static constexpr int ABUF = Conv<KS>::ABUF;
   static constexpr int zero = 2 * ABUF;
+  // biases (fp8: then the weight scales) of up to kMaxSlices output-channel
+  // slices; a head's weights (never sliced) follow one slice's
   static constexpr int bias = zero + 512;
   static constexpr int headw = bias + 2 * COUT * 4;
-  static constexpr int total = headw + 4 * COUT * 4;
+  static constexpr int total = bias + (2 * kMaxSlices > 6 ? 2 * kMaxSlices : 6) * COUT * 4;
   static_assert(zero % 256 == 0, "zero region must be 256-aligned");
   static_assert(Conv<KS>::WG_PER_CU * total <= 160 * 1024, "the workgroups of a CU fit its LDS");
   static_assert(Split<COUT>::WN * kTileRows * 4 * 4 <= ABUF, "head partials fit a staging buffer");
@@ -295,7 +299,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
                    const float* __restrict__ head_w, const float* __restrict__ head_b,
                    const int32_t* __restrict__ tables, uint8_t* __restrict__ nib,
                    float* __restrict__ logits, int batch, int kshift_arg, float* __restrict__ partial,
-                   const uint16_t* __restrict__ sc, int sc_stride) {
+                   const uint16_t* __restrict__ sc, int sc_stride, int lsl) {
   static_assert(KS == 3 || MODE == 1, "5x5x5 layers run on box tiles");
   extern __shared__ __attribute__((aligned(16))) char smem[];
   using W = Split<COUT>;
@@ -322,14 +326,21 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
   const int kshift = EPI == EPI_PARK ? kshift_arg : 0;
   const int ksplit = 1 << kshift;
   const int NCU = NCHUNK >> kshift;  // chunks per unit
-  const int nunits = ntiles << kshift;
+  // Output-channel slices (a layer wider than COUT in one launch): 2^lsl
+  // slices of COUT channels, unit u = ((tile << lsl | slice) << kshift) | part;
+  // slice q has its own weight fragments (the layer's TSTEPS k-steps, after
+  // q slices' worth), biases (COUT, fp8: and COUT scales) and output
+  // columns (and shortcut columns, or projection rows).
+  const int nunits = ntiles << (kshift + lsl);
+  constexpr int BSL = (F8 ? 2 : 1) * COUT;  // bias floats per slice
+  auto slice_of = [&](int u) { return (u >> kshift) & ((1 << lsl) - 1); };
 
   lds_char* const lds = (lds_char*)smem;
   lds_char* const zero = lds + L::zero;
   lds_float* const bias_s = (lds_float*)(lds + L::bias);
   lds_float* const scale_s = bias_s + COUT;  // fp8: per-channel weight scales
   lds_float* const headw_s = (lds_float*)(lds + L::headw);
-  for (int e = tid; e < (F8 ? 2 : 1) * COUT; e += NT) bias_s[e] = bias[e];
+  for (int e = tid; e < (BSL << lsl); e += NT) bias_s[e] = bias[e];
   if (tid < 128) ((lds_u32_w*)zero)[tid] = 0u;
   const uint32_t zero_addr = (uint32_t)(uintptr_t)zero;
   if (EPI == EPI_HEAD)
@@ -339,7 +350,12 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
   // holds channels co .. co + 3, co = 64 wn + 32 nb + 8 q + 4 half, of voxel
   // row wm ROWS + 32 mb + l32); ebuf: a staging buffer free for the
   // transposition / head partials.
-  auto finish_tile = [&](int tile, lds_char* const ebuf, f32x16 (&acc)[MB][NB]) {
+  auto finish_tile = [&](int tile, int slice, lds_char* const ebuf, f32x16 (&acc)[MB][NB]) {
+      // this slice's output columns, and its shortcut columns or projection rows
+      char* const ysl = (char*)y + (size_t)slice * COUT * P::ESZ;
+      const uint16_t* const scs = head_w ? sc : (const uint16_t*)((const char*)sc + (size_t)slice * COUT * P::ESZ);
+      const float* const hws = head_w ? head_w + (size_t)slice * COUT * sc_stride : nullptr;
+      const float* const hbs = head_w ? head_b + (size_t)slice * COUT : nullptr;
       // output row of each row block (recomputed: not kept live through the K loop)
       int pidx[MB];
 #pragma unroll
@@ -399,9 +415,10 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
               for (int q = 0; q < 4; ++q) {
                 const int c8 = nb * 4 + q;  // 8-channel group of the wave's 64 channels
                 const int co = wn * 64 + c8 * 8 + half * 4;
-                const float4 bv = {bias_s[co], bias_s[co + 1], bias_s[co + 2], bias_s[co + 3]};
+                const lds_float* const bsl = bias_s + slice * BSL;  // this slice's biases, then scales
+                const float4 bv = {bsl[co], bsl[co + 1], bsl[co + 2], bsl[co + 3]};
                 float4 sv = {1.0f, 1.0f, 1.0f, 1.0f};
-                if constexpr (F8) sv = float4{scale_s[co], scale_s[co + 1], scale_s[co + 2], scale_s[co + 3]};
+                if constexpr (F8) sv = float4{bsl[COUT + co], bsl[COUT + co + 1], bsl[COUT + co + 2], bsl[COUT + co + 3]};
 #pragma unroll
                 for (int m = 0; m < 2; ++m) {
                   const int mb = 2 * ps + m;
@@ -409,7 +426,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
                   if constexpr (F8) {
                     float sh[4] = {0.0f, 0.0f, 0.0f, 0.0f};
                     if constexpr (EPI == EPI_ADD) {  // the block's shortcut, 4 channels of this row
-                      if (pidx[mb] >= 0) shortcut_of<4, true>(sc, sc_stride, pidx[mb], head_w, head_b, co, sh);
+                      if (pidx[mb] >= 0) shortcut_of<4, true>(scs, sc_stride, pidx[mb], hws, hbs, co, sh);
                     }
                     const float v0 = act_fn<ACT>(__builtin_fmaf(acc[mb][nb][4 * q + 0], sv.x, bv.x) + sh[0]);
                     const float v1 = act_fn<ACT>(__builtin_fmaf(acc[mb][nb][4 * q + 1], sv.y, bv.y) + sh[1]);
@@ -423,7 +440,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
                     if constexpr (EPI == EPI_ADD) {  // the block's shortcut, 4 channels of this row
                       if (pidx[mb] >= 0) {
                         float pj[4];
-                        shortcut_of<4, false>(sc, sc_stride, pidx[mb], head_w, head_b, co, pj);
+                        shortcut_of<4, false>(scs, sc_stride, pidx[mb], hws, hbs, co, pj);
                         sh = float4{pj[0], pj[1], pj[2], pj[3]};
                       }
                     }
@@ -447,7 +464,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
               const u32x4 v = *(lds_u32x4*)(tb + r * 128 + ((c ^ (r & 7)) << 4));
               const int pr = __shfl(pidx[2 * ps + (F8 ? it2 >> 1 : it2 >> 2)], r & 31);
               if (pr >= 0)
-                *reinterpret_cast<u32x4*>((char*)y + ((long long)pr * ystride + wn * 64) * P::ESZ + c * 16) = v;
+                *reinterpret_cast<u32x4*>(ysl + ((long long)pr * ystride + wn * 64) * P::ESZ + c * 16) = v;
             }
             __builtin_amdgcn_s_waitcnt(0xc07f);  // the reads are done before the next pass writes
             __builtin_amdgcn_wave_barrier();
@@ -540,7 +557,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
 
   int unit = tile_of(blockIdx.x, gridDim.x, 0, nunits);
   if (unit < 0) return;
-  int tile = unit >> kshift;
+  int tile = unit >> (kshift + lsl);
 
   auto source_of = [&](int t) { return tile_source(g, tl, t, batch); };
   long long cur_base = stage_base<MODE>(g, source_of(tile));
@@ -566,7 +583,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
   // the fragment's offset as the scalar one (no per-load address arithmetic)
   constexpr int WQ = F8 ? 2 : 1;  // 16-byte pieces per lane and fragment
   const __amdgpu_buffer_rsrc_t wres =
-      __builtin_amdgcn_make_buffer_rsrc((void*)wfrag, 0, TSTEPS * NBT * P::WFRAG, 0x00020000);
+      __builtin_amdgcn_make_buffer_rsrc((void*)wfrag, 0, (TSTEPS * NBT * P::WFRAG) << lsl, 0x00020000);
   const uint32_t woff = (uint32_t)((wn * NB * 64 + lane) * 16 * WQ);
   auto wload = [&](int gs, int nb, u32x4 (&dst)[WQ]) {
 #pragma unroll
@@ -579,15 +596,18 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
 #pragma unroll
   for (int st = 0; st < RING - 1; ++st)
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) wload((unit & (ksplit - 1)) * NCU * NSTEP + st, nb, bq[st][nb]);
+    for (int nb = 0; nb < NB; ++nb)
+      wload(slice_of(unit) * TSTEPS + (unit & (ksplit - 1)) * NCU * NSTEP + st, nb, bq[st][nb]);
   __syncthreads();  // staged chunk, bias, zero region and head weights visible
 
   int gchunk = 0;  // chunks processed by this workgroup (selects the LDS buffer)
   for (int it = 0; unit >= 0; ++it) {
     const int c0 = (unit & (ksplit - 1)) * NCU;  // first chunk of this unit
+    const int slice = slice_of(unit);
     const int next_unit = tile_of(blockIdx.x, gridDim.x, it + 1, nunits);
-    const int next = next_unit >= 0 ? next_unit >> kshift : -1;
+    const int next = next_unit >= 0 ? next_unit >> (kshift + lsl) : -1;
     const int next_c0 = next_unit >= 0 ? (next_unit & (ksplit - 1)) * NCU : 0;
+    const int next_slice = next_unit >= 0 ? slice_of(next_unit) : 0;
     const StageSrc next_src = source_of(next >= 0 ? next : tile);
     const long long next_base = stage_base<MODE>(g, next_src);
     // rows of this lane: voxel wm ROWS + 32 mb + l32 of the tile; LDS
@@ -721,8 +741,8 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
       __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) frag_read(mb, 0, av[mb]);
-      const int gbase = cc * NSTEP;              // k-step of this chunk's step 0
-      const int nbase = next_c0 * NSTEP - NSTEP;  // ... of the next unit's first chunk, minus NSTEP
+      const int gbase = slice * TSTEPS + cc * NSTEP;                  // k-step of this chunk's step 0
+      const int nbase = next_slice * TSTEPS + next_c0 * NSTEP - NSTEP;  // ... of the next unit's first chunk, minus NSTEP
       // staging of the next chunk: round k is loaded at step SG k and stored
       // to LDS at step SG (k + 1), just before round k + 1 is loaded (a round
       // that would be stored past the last step is stored after it)
@@ -785,7 +805,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
                 float4{acc[mb][nb][4 * q], acc[mb][nb][4 * q + 1], acc[mb][nb][4 * q + 2], acc[mb][nb][4 * q + 3]};
           }
     } else {
-      finish_tile(tile, lds + ((gchunk - 1) & 1) * ABUF, acc);
+      finish_tile(tile, slice, lds + ((gchunk - 1) & 1) * ABUF, acc);
     }
     unit = next_unit;
     tile = next;
@@ -809,17 +829,31 @@ __global__ void __launch_bounds__(256) split_finish_kernel(Geom g, Tiling tl, in
                                                            const float* __restrict__ head_b,
                                                            const int32_t* __restrict__ tables,
                                                            uint8_t* __restrict__ nib, float* __restrict__ logits,
-                                                           int batch, const uint16_t* __restrict__ sc, int sc_stride) {
+                                                           int batch, const uint16_t* __restrict__ sc, int sc_stride,
+                                                           int lsl) {
   constexpr bool ROWS8 = EPI == EPI_ACT || EPI == EPI_ADD;  // one thread per (row, 8 channels)
   // the head: one thread per (row, 8 channels) too, the rows' partial head
   // sums reduced over the row's consecutive lanes
   const int groups = (ROWS8 || EPI == EPI_HEAD) ? cout / 8 : 1;
   const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (gid >= tl.ntiles * kTileRows * groups) return;
-  const int tile = (int)(gid / (kTileRows * groups));
-  const int rem = (int)(gid - (long long)tile * kTileRows * groups);
+  if (gid >= ((long long)tl.ntiles << lsl) * kTileRows * groups) return;
+  // (tile, output-channel slice) of this thread: activations only, the head
+  // and the output layer run unsliced (lsl = 0)
+  const int ts = (int)(gid / (kTileRows * groups));
+  const int tile = ts >> lsl, slice = ts & ((1 << lsl) - 1);
+  const int rem = (int)(gid - (long long)ts * kTileRows * groups);
   const int r = rem / groups, grp = rem - r * groups;
   const int ksplit = 1 << kshift;
+  if (lsl) {  // this slice's biases, outputs, and shortcut columns or projection rows
+    bias += (size_t)slice * (F8 ? 2 : 1) * cout;
+    y = (char*)y + (size_t)slice * cout * (F8 ? 1 : 2);
+    if (head_w) {
+      head_w += (size_t)slice * cout * sc_stride;
+      head_b += (size_t)slice * cout;
+    } else if (sc) {
+      sc = (const uint16_t*)((const char*)sc + (size_t)slice * cout * (F8 ? 1 : 2));
+    }
+  }
   // pre-activation of channels c .. c + 7 of this row: the sum over the
   // tile's parts in part order (fp8: times the channel's weight scale), plus
   // the bias
@@ -828,7 +862,7 @@ __global__ void __launch_bounds__(256) split_finish_kernel(Geom g, Tiling tl, in
   auto sum8 = [&](int c, float (&v)[8]) {
     if (ksplit < 4) {
       for (int p = 0; p < ksplit; ++p) {
-        const float* src = partial + ((size_t)((tile << kshift) + p) * kTileRows + r) * cout + c;
+        const float* src = partial + ((size_t)((ts << kshift) + p) * kTileRows + r) * cout + c;
         const float4 a = *reinterpret_cast<const float4*>(src);
         const float4 b = *reinterpret_cast<const float4*>(src + 4);
         const float t[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
@@ -841,7 +875,7 @@ __global__ void __launch_bounds__(256) split_finish_kernel(Geom g, Tiling tl, in
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int p = p0 + q;  // < ksplit: ksplit is a power of two >= 4
-        const float* src = partial + ((size_t)((tile << kshift) + p) * kTileRows + r) * cout + c;
+        const float* src = partial + ((size_t)((ts << kshift) + p) * kTileRows + r) * cout + c;
         a[q] = *reinterpret_cast<const float4*>(src);
         b[q] = *reinterpret_cast<const float4*>(src + 4);
       }
@@ -931,7 +965,8 @@ template <int CIN, int COUT, int EPI, int MODE, bool F8, int KS>
 hipError_t launch_hidden(const Geom& g, const Tiling& tl, int act, const void* x, void* y, int ystride,
                          const void* wfrag, const float* bias, const float* head_w, const float* head_b,
                          const int32_t* tables, uint8_t* nib, float* logits, int batch, int n_workgroups,
-                         int kshift, float* partial, const uint16_t* sc, int sc_stride, hipStream_t stream) {
+                         int kshift, float* partial, const uint16_t* sc, int sc_stride, int lsl,
+                         hipStream_t stream) {
   using L = Lds<COUT, KS>;
   static bool attr_set = false;
   if (!attr_set) {
@@ -940,10 +975,10 @@ hipError_t launch_hidden(const Geom& g, const Tiling& tl, int act, const void* x
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  const long long nwg = conv_workgroups(tl.ntiles << kshift, n_workgroups);
+  const long long nwg = conv_workgroups(tl.ntiles << (kshift + lsl), n_workgroups);
   hipLaunchKernelGGL((conv_hidden_kernel<CIN, COUT, EPI, MODE, F8, KS>), dim3((unsigned)nwg), dim3(NT),
                      (size_t)L::total, stream, g, tl, act, x, y, ystride, (const u32x4*)wfrag, bias, head_w,
-                     head_b, tables, nib, logits, batch, kshift, partial, sc, sc_stride);
+                     head_b, tables, nib, logits, batch, kshift, partial, sc, sc_stride, lsl);
   return hipSuccess;
 }
 
@@ -956,21 +991,21 @@ hipError_t launch_one(const Geom& g, const Tiling& tl, int act, const void* x, v
   if (sk.kshift == 0) {
     e = launch_hidden<CIN, COUT, EPI, MODE, F8, KS>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b,
                                                     tables, nib, logits, batch, n_workgroups, 0, nullptr, sc,
-                                                    sc_stride, stream);
+                                                    sc_stride, sk.lsl, stream);
     return e != hipSuccess ? e : hipGetLastError();
   }
   // K loops split: park the parts, then add them and finish the tiles
   e = launch_hidden<CIN, COUT, EPI_PARK, MODE, F8, KS>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b,
                                                        tables, nib, logits, batch, n_workgroups, sk.kshift,
-                                                       sk.partial, nullptr, 0, stream);
+                                                       sk.partial, nullptr, 0, sk.lsl, stream);
   if (e != hipSuccess) return e;
-  const long long threads =
-      tl.ntiles * kTileRows * (EPI == EPI_ACT || EPI == EPI_ADD || EPI == EPI_HEAD ? COUT / 8 : 1);
+  const long long threads = ((long long)tl.ntiles << sk.lsl) * kTileRows *
+                            (EPI == EPI_ACT || EPI == EPI_ADD || EPI == EPI_HEAD ? COUT / 8 : 1);
   static_assert(EPI != EPI_HEAD || (64 % (COUT / 8) == 0), "a row's head lanes lie in one wave");
   with_activation(act, [&](auto A) {
     hipLaunchKernelGGL((split_finish_kernel<EPI, decltype(A)::value, F8>), dim3((unsigned)((threads + 255) / 256)),
                        dim3(256), 0, stream, g, tl, COUT, sk.kshift, sk.partial, bias, y, ystride, head_w, head_b,
-                       tables, nib, logits, batch, sc, sc_stride);
+                       tables, nib, logits, batch, sc, sc_stride, sk.lsl);
   });
   return hipGetLastError();
 }
@@ -1048,7 +1083,12 @@ hipError_t launch_conv_hidden(const Geom& g, const Tiling& tl, int cin, int cout
   // parts per tile: a power of two dividing the layer's chunks, with room
   // for every unit's sums
   const int nchunk = cin / (fp8 ? Prec<true, 3>::KCH : Prec<false, 3>::KCH);
-  if (sk.kshift < 0 || nchunk % (1 << sk.kshift) != 0 || (sk.kshift > 0 && (tl.ntiles << sk.kshift) > sk.max_units))
+  if (sk.kshift < 0 || nchunk % (1 << sk.kshift) != 0 ||
+      (sk.kshift > 0 && (tl.ntiles << (sk.kshift + sk.lsl)) > sk.max_units))
+    return hipErrorInvalidValue;
+  // output-channel slices: up to kMaxSlices, of activation layers (a head or
+  // an output layer needs every channel of a voxel in one unit)
+  if (sk.lsl < 0 || (1 << sk.lsl) > kMaxSlices || (sk.lsl > 0 && head != EPI_ACT && head != EPI_ADD))
     return hipErrorInvalidValue;
   if (fp8)
     return launch_case<true>(g, tl, cin, cout, act, x, y, ystride, wfrag, bias, head, head_w, head_b, tables, nib,

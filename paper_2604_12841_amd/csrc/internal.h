@@ -179,6 +179,7 @@ struct Split_k {
   int kshift;
   float* partial;
   long long max_units;
+  int lsl = 0;  // 2^lsl output-channel slices of c_out channels in one launch
 };
 
 // ks: kernel size 3, or 5 (box tiles, a halo of two; bf16 c_in / c_out of
