@@ -631,8 +631,10 @@ struct StopAt {
 // split saves 20 us.)  fp8 chunks are 32 channels with about half a bf16
 // chunk's matrix time per channel; a 5x5x5 chunk has 125 taps instead of 27.
 // nsl: the layer's output-channel slices of cout channels, all in the one
-// launch (each is a unit of its own per tile and part).
-pd::Split_k split_for(const Workspace& ws, const Tiling& t, int cin, int cout, int fp8, int ks = 3, int nsl = 1) {
+// launch (each is a unit of its own per tile and part).  unit_us (optional):
+// the estimate for an unsplit unit.
+pd::Split_k split_for(const Workspace& ws, const Tiling& t, int cin, int cout, int fp8, int ks = 3, int nsl = 1,
+                      double* unit_us = nullptr) {
   const int kch = pd::conv_hidden_chunk_channels(fp8);
   const int nch = cin / kch;
   const double wide = cout > 64 ? 1.0 : 0.0;
@@ -642,6 +644,7 @@ pd::Split_k split_for(const Workspace& ws, const Tiling& t, int cin, int cout, i
   pd::Split_k sk{0, ws.partial, ws.max_units};
   while ((1 << sk.lsl) < nsl) ++sk.lsl;
   double best = nch * chunk + epi;
+  if (unit_us) *unit_us = best;
   for (int k = 1; nch % (1 << k) == 0 && (t.ntiles << (k + sk.lsl)) <= ws.max_units; ++k) {
     const double est = (nch >> k) * chunk + park + finish;
     if (est < best) {
@@ -650,6 +653,67 @@ pd::Split_k split_for(const Workspace& ws, const Tiling& t, int cin, int cout, i
     }
   }
   return sk;
+}
+
+// One hidden-kernel layer over the batch (nsl output-channel slices of cw
+// channels; see launch_conv_hidden for the rest).  Usually one launch.  When
+// the layer's units (tiles x slices) fill the workgroup slots a few times
+// over and leave a short remainder, two: the first samples, whose units fill
+// whole rounds, unsplit; then the last few samples (a sub-batch: every
+// per-sample pointer moved on by their offset) with their K loops split over
+// the otherwise idle chip and finished by the second kernel.  A remainder of
+// r units would otherwise take a whole unit's time on r slots (40 of 552
+// units at Model 6's 13^3 batch 16 took about a third of the layer); the
+// split saves that time but one fraction 2^-k, and costs the parked sums,
+// the finishing kernel and one more kernel boundary: about 45 us in all,
+// from MI355X timings of splits of 128 to 512 input channels (Models 1, 2
+// and 6 at 13^3), so only long units split.  (Model 6 at 13^3 batch 16 in
+// bf16: the last 2 of the 16 samples split in two, 5 % less time per round.)
+constexpr long long kMaxTailRounds = 4;  // past this, a remainder costs little
+constexpr double kTailCostUs = 45.0;
+
+pd_status run_hidden(const pd_predecoder* h, Workspace& ws, const Tiling& tl, int cin, int cw, int nsl, int act,
+                     const void* x, void* y, int ystride, const void* wfrag, const float* bias, int head,
+                     const float* head_w, const float* head_b, float* logits, int batch, int fp8,
+                     const uint16_t* sc, int sc_stride, int ks, hipStream_t st) {
+  const Geom& g = h->g;
+  const int slots = h->n_cu * pd::conv_hidden_workgroups_per_cu(ks);
+  // samples b0 .. b0 + nb - 1 with tiling t and split sk
+  auto launch = [&](const Tiling& t, const pd::Split_k& sk, int b0, int nb) {
+    const int esz = fp8 ? 1 : 2;                  // bytes per activation value
+    const long long pv = (long long)b0 * g.S;     // padded voxels before sample b0
+    const uint16_t* scb = !sc ? nullptr
+                              : (const uint16_t*)((const char*)sc + pv * sc_stride * (head_w ? 2 : esz));
+    return check_launch(pd::launch_conv_hidden(
+        g, t, cin, cw, act, (const char*)x + pv * cin * esz, y ? (char*)y + pv * ystride * esz : nullptr, ystride,
+        wfrag, bias, head, head_w, head_b, h->tables, ws.nib + (long long)b0 * g.V,
+        logits ? logits + (long long)b0 * 4 * g.T * g.H * g.H : nullptr, nb, slots, sk, fp8, scb, sc_stride, ks,
+        st));
+  };
+  const pd::Split_k sk = split_for(ws, tl, cin, cw, fp8, ks, nsl);
+  const long long units = tl.ntiles * nsl, q = units / slots, r = units % slots;
+  if (sk.kshift == 0 && q >= 1 && q <= kMaxTailRounds && r > 0 && batch > 1) {
+    // the most first samples whose tiles fit q full rounds (tiles grow with
+    // the batch: per sample, or one flat run of batch x V voxels)
+    const Tiling& base = h->tiling;
+    const long long fit = q * slots / nsl;  // tiles
+    const bool flat = base.mode == 0 && (base.seg_len < 0 || base.tiles_per_seg == 0);
+    const long long per = base.mode == 1 ? (long long)base.ntT * base.ntI * base.ntJ : base.tiles_per_seg;
+    const long long first = flat ? fit * pd::kTileRows / g.V : fit / per;
+    if (first >= 1 && first < batch) {
+      const int nb = batch - (int)first;
+      Tiling th = base, tt = base;
+      tiling_for_batch(&th, g, (int)first);
+      tiling_for_batch(&tt, g, nb);
+      double unit_us = 0.0;
+      const pd::Split_k tsk = split_for(ws, tt, cin, cw, fp8, ks, nsl, &unit_us);
+      if (tsk.kshift > 0 && unit_us * (1.0 - 1.0 / (1 << tsk.kshift)) > kTailCostUs) {
+        const pd_status s = launch(th, sk, 0, batch - nb);
+        return s != PD_OK ? s : launch(tt, tsk, batch - nb, nb);
+      }
+    }
+  }
+  return launch(tl, sk, 0, batch);
 }
 
 // The path of a residual network (Model 6, Sec. VI, Fig. Model8Representation):
@@ -666,7 +730,6 @@ pd_status enqueue_resnet(pd_predecoder* h, Workspace& ws, hipStream_t st, const 
   const Geom& g = h->g;
   const int fp8 = h->dtype == PD_DTYPE_FP8;
   const int ae = fp8 ? 1 : 2;  // bytes per activation value
-  const int hidden_wgs = h->n_cu * pd::conv_hidden_workgroups_per_cu(3);
   int e = 0;
   auto mark = [&]() -> pd_status {
     if (ev && hipEventRecord(ev[e++], st) != hipSuccess) return PD_ERR_DEVICE;
@@ -710,10 +773,8 @@ pd_status enqueue_resnet(pd_predecoder* h, Workspace& ws, hipStream_t st, const 
                                                  batch, fp8, 3, st));
         }
       } else {
-        s = check_launch(pd::launch_conv_hidden(g, tl, B.c_in, cw, B.act, x, hb, B.c_mid, h->wdev[2 * k],
-                                                h->bdev[2 * k], 0, nullptr, nullptr, h->tables, ws.nib, nullptr,
-                                                batch, hidden_wgs, split_for(ws, tl, B.c_in, cw, fp8, 3, nsl), fp8,
-                                                nullptr, 0, 3, st));
+        s = run_hidden(h, ws, tl, B.c_in, cw, nsl, B.act, x, hb, B.c_mid, h->wdev[2 * k], h->bdev[2 * k], 0, nullptr,
+                       nullptr, nullptr, batch, fp8, nullptr, 0, 3, st);
       }
       if (s != PD_OK) return s;
       if (stopped(hb, B.c_mid * ae)) return PD_OK;
@@ -754,10 +815,8 @@ pd_status enqueue_resnet(pd_predecoder* h, Workspace& ws, hipStream_t st, const 
                                            nullptr, st));
     } else {  // slices as for conv1, each also with its shortcut channels (or projection rows)
       const int nsl = B.c_out > 128 ? B.c_out / 128 : 1, cw = B.c_out / nsl;
-      s = check_launch(pd::launch_conv_hidden(g, tl, B.c_mid, cw, B.act, hb, yb, B.c_out, h->wdev[2 * k + 1],
-                                              h->bdev[2 * k + 1], 4, pw, pb, h->tables, ws.nib, nullptr, batch,
-                                              hidden_wgs, split_for(ws, tl, B.c_mid, cw, fp8, 3, nsl), fp8, sc,
-                                              sc_stride, 3, st));
+      s = run_hidden(h, ws, tl, B.c_mid, cw, nsl, B.act, hb, yb, B.c_out, h->wdev[2 * k + 1], h->bdev[2 * k + 1], 4,
+                     pw, pb, nullptr, batch, fp8, sc, sc_stride, 3, st);
     }
     if (s != PD_OK) return s;
     if (!last && stopped(yb, B.c_out * ae)) return PD_OK;
@@ -789,7 +848,6 @@ pd_status enqueue_run(pd_predecoder* h, Workspace& ws, hipStream_t st, const uin
   // epilogue on the MFMA paths) or a 3x3x3 (5x5x5) output layer of its own
   const bool out3 = h->layers[n - 1].k > 1;
   const int ks = h->ks;
-  const int hidden_wgs = h->n_cu * pd::conv_hidden_workgroups_per_cu(h->ks);
   int e = 0;
   auto mark = [&]() -> pd_status {
     if (ev && hipEventRecord(ev[e++], st) != hipSuccess) return PD_ERR_DEVICE;
@@ -831,10 +889,8 @@ pd_status enqueue_run(pd_predecoder* h, Workspace& ws, hipStream_t st, const uin
                                                  batch, fp8, ks, st));
         }
       } else {  // the last hidden layer may carry the head and the threshold in its epilogue
-        s = check_launch(pd::launch_conv_hidden(g, tl, L.c_in, cw, L.act, x, y, L.c_out, h->wdev[l], h->bdev[l],
-                                                fuse_head ? 1 : 0, h->head_w, h->head_b, h->tables, ws.nib, logits,
-                                                batch, hidden_wgs, split_for(ws, tl, L.c_in, cw, fp8, ks, nsl), fp8,
-                                                nullptr, 0, ks, st));
+        s = run_hidden(h, ws, tl, L.c_in, cw, nsl, L.act, x, y, L.c_out, h->wdev[l], h->bdev[l], fuse_head ? 1 : 0,
+                       h->head_w, h->head_b, logits, batch, fp8, nullptr, 0, ks, st);
       }
       head_done = fuse_head && l > 0;
     }
@@ -854,10 +910,8 @@ pd_status enqueue_run(pd_predecoder* h, Workspace& ws, hipStream_t st, const uin
                                          batch, h->n_cu, fp8, nullptr, 0, nullptr, nullptr, nullptr, st));
   } else if (out3) {
     const pd_layer& L = h->layers[n - 1];
-    s = check_launch(pd::launch_conv_hidden(g, tl, L.c_in, L.c_out, L.act, x, nullptr, 0, h->wdev[n - 1],
-                                            h->bdev[n - 1], 2, nullptr, nullptr, h->tables, ws.nib, logits,
-                                            batch, hidden_wgs, split_for(ws, tl, L.c_in, 32, fp8, ks), fp8, nullptr, 0,
-                                            ks, st));
+    s = run_hidden(h, ws, tl, L.c_in, L.c_out, 1, L.act, x, nullptr, 0, h->wdev[n - 1], h->bdev[n - 1], 2, nullptr,
+                   nullptr, logits, batch, fp8, nullptr, 0, ks, st);
   } else if (!head_done) {  // fp32, or a one-hidden-layer network on the paper's layout
     s = check_launch(pd::launch_head(g, h->layers[n - 1].c_in, fp32, x, h->head_w, h->head_b, h->tables,
                                      ws.nib, logits, batch, st));

@@ -89,3 +89,36 @@ def test_model6_at_timed_shape(cuda, d, batch, dtype):
                             last="Z", fp8=dtype == "fp8")
     _check(d, T, dtype, det, rows, flips, res, logits, ref, RESNET_TOL if dtype == "bf16" else RESNET_FP8_TOL)
 
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+def test_model6_batch_and_its_sub_batches(cuda, dtype):
+    """Model 6 at 13^3, batch 16, whose units overfill the chip's workgroup
+    slots by a short remainder: the last samples then run as a sub-batch of
+    their own with split K loops.  Some split point b must exist such that
+    samples [0, b) run alone give exactly the batch's flips, residual and
+    logits (the same unsplit launches), and samples [b, 16) run alone agree
+    with the batch's within the logit tolerance, flips and residual exact
+    outside its band (alone, they may split their K loops differently)."""
+    d = T = 13
+    batch = 16
+    blocks = workload.MODEL6_BLOCKS
+    weights = workload.resnet_weights(blocks, 4006)
+    det = _inputs(d, batch)
+    tol = RESNET_TOL if dtype == "bf16" else RESNET_FP8_TOL
+    say("Model 6 sub-batches, d = T =", d, "batch", batch, dtype)
+    pre = pdx.Predecoder(weights, d, T, None, dtype, max_batch=batch, layout="paper", first="Z", last="Z",
+                         blocks=blocks)
+    flips, res, logits = run_gpu(pre, det)
+    found = None
+    for b in range(batch - 1, 0, -1):
+        if all(np.array_equal(x, z[:b]) for x, z in zip(run_gpu(pre, det[:b]), (flips, res, logits))):
+            found = b
+            break
+    assert found is not None
+    f2, r2, l2 = run_gpu(pre, det[found:])
+    pre.close()
+    st = compare(d, T, dtype, logits[found:].astype(np.float64), flips[found:], res[found:], f2, r2, l2,
+                 layout="paper", tol=tol)
+    say("  first", found, "samples exact; the rest alone against the batch:", st)
+    assert_parity(st, dtype, tol=tol)
