@@ -185,7 +185,7 @@ def bench_model6(args, torch, pdx, workload):
         "mfma_frac_end_to_end": total / (ms * 1e-3) / (peak * 1e12),
         "stage_ms": {"unpack": stages[0], **{"block%d" % (k + 1): stages[1 + k] for k in range(len(blocks))},
                      "residual_repack": stages[-1]},
-        "roofline": {"kernel": "block 2: two conv3d 3x3x3 512->512 (%s MFMA, four 128-channel slices each)"
+        "roofline": {"kernel": "block 2: two conv3d 3x3x3 512->512 (%s MFMA, four 128-channel output slices in one launch each)"
                                % ("fp8" if fp8 else "bf16"),
                      "bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak, "traffic": None},
