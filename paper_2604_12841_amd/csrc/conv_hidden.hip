@@ -308,7 +308,12 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
   constexpr int NB = W::NB;
   constexpr int NBT = COUT / 32;  // 32-channel blocks in total
   using P = Prec<F8, KS>;
-  constexpr int KCH = P::KCH, NSTEP = P::NSTEP, RING = P::RING, SG = P::SG;
+  constexpr int KCH = P::KCH, NSTEP = P::NSTEP, SG = P::SG;
+  // weight ring depth: 32-channel slices (small batches, one workgroup per
+  // CU, two MFMAs per k-step) prefetch a third of a chunk ahead, since the
+  // short steps alone cannot cover a load's latency
+  constexpr int RING = (COUT == 32 && KS == 3) ? (F8 ? 7 : 9) : P::RING;
+  static_assert(NSTEP % RING == 0, "the weight ring lines up with chunk boundaries");
   constexpr int RMAX = Conv<KS>::RMAX, ABUF = L::ABUF, TAPS = Conv<KS>::TAPS;
   constexpr int ROW = CIN * P::ESZ;  // bytes per input voxel row
   constexpr int NCHUNK = CIN / KCH;
@@ -399,12 +404,15 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
       } else if constexpr (EPI == EPI_ACT || EPI == EPI_ADD) {
         // bias + activation + bf16, transposed through this wave's slice of
         // the staging buffer the tile read last (64 rows x 128 bytes, granule
-        // c of row r at c ^ (r % 8)), then stored as whole 128-byte halves of
-        // voxel rows, 8 rows per instruction.  The next tile's first staging
-        // store waits at a barrier until every wave is done here.
-        // (fp8: 64 bytes per row, four 16-byte granules of 16 channels)
+        // c of row r at c ^ (r % 8)), then stored as the wave's whole part of
+        // each voxel row (NB x 32 channels: 128 bytes, 8 rows per
+        // instruction, for NB = 2).  The next tile's first staging store
+        // waits at a barrier until every wave is done here.
+        // (fp8: one byte per channel, 16-byte granules of 16 channels)
         lds_char* const tb = ebuf + wave * (64 * 128);
-        constexpr int GR = F8 ? 4 : 8;  // 16-byte granules of a row's 64 channels
+        constexpr int GR = (F8 ? 2 : 4) * NB;  // 16-byte granules of a row's NB x 32 channels
+        constexpr int LGR = GR == 8 ? 3 : (GR == 4 ? 2 : 1);
+        static_assert((1 << LGR) == GR, "granules per row: a power of two");
         with_activation(act, [&](auto A) {
           constexpr int ACT = decltype(A)::value;
 #pragma unroll
@@ -413,8 +421,8 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
             for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
               for (int q = 0; q < 4; ++q) {
-                const int c8 = nb * 4 + q;  // 8-channel group of the wave's 64 channels
-                const int co = wn * 64 + c8 * 8 + half * 4;
+                const int c8 = nb * 4 + q;  // 8-channel group of the wave's NB x 32 channels
+                const int co = wn * NB * 32 + c8 * 8 + half * 4;
                 const lds_float* const bsl = bias_s + slice * BSL;  // this slice's biases, then scales
                 const float4 bv = {bsl[co], bsl[co + 1], bsl[co + 2], bsl[co + 3]};
                 float4 sv = {1.0f, 1.0f, 1.0f, 1.0f};
@@ -460,11 +468,11 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
 #pragma unroll
             for (int it2 = 0; it2 < GR; ++it2) {
               const int gi = it2 * 64 + lane;
-              const int r = F8 ? gi >> 2 : gi >> 3, c = F8 ? gi & 3 : gi & 7;
+              const int r = gi >> LGR, c = gi & (GR - 1);
               const u32x4 v = *(lds_u32x4*)(tb + r * 128 + ((c ^ (r & 7)) << 4));
-              const int pr = __shfl(pidx[2 * ps + (F8 ? it2 >> 1 : it2 >> 2)], r & 31);
+              const int pr = __shfl(pidx[2 * ps + (it2 >> (LGR - 1))], r & 31);  // rows 32.. from it2 = GR / 2
               if (pr >= 0)
-                *reinterpret_cast<u32x4*>(ysl + ((long long)pr * ystride + wn * 64) * P::ESZ + c * 16) = v;
+                *reinterpret_cast<u32x4*>(ysl + ((long long)pr * ystride + wn * NB * 32) * P::ESZ + c * 16) = v;
             }
             __builtin_amdgcn_s_waitcnt(0xc07f);  // the reads are done before the next pass writes
             __builtin_amdgcn_wave_barrier();
@@ -1033,6 +1041,7 @@ hipError_t launch_case(const Geom& g, const Tiling& tl, int cin, int cout, int a
                                            tables, nib, logits, batch, n_workgroups, sk, sc, sc_stride, \
                                            stream);
   PD_HIDDEN_CASE(64, 64, EPI_ACT)
+  PD_HIDDEN_CASE(64, 32, EPI_ACT)  // a 64-wide layer in two slices (small batches)
   PD_HIDDEN_CASE(128, 128, EPI_ACT)
   PD_HIDDEN_CASE(64, 128, EPI_ACT)
   PD_HIDDEN_CASE(128, 64, EPI_ACT)

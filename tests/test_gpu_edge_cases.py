@@ -193,3 +193,46 @@ def test_layer1_same_at_any_launch_size(cuda, dtype):
         torch.cuda.synchronize()
         assert torch.equal(one[0].cpu(), big[s].cpu())
     pre.close()
+
+
+@pytest.mark.parametrize("B", [1, 40])
+def test_64_wide_layers_tight(cuda, B):
+    """The 6 x 64 network at d = T = 9: at batch 1 each 64 -> 64 layer runs
+    as two slices of 32 output channels (twice the workgroups), at batch 40
+    whole.  Either way every hidden layer's stored bf16 activations are
+    checked from the GPU's own input under the rule of tests/tight.py, then
+    the logits from the GPU's last hidden activations within their own sums'
+    bound."""
+    import tight
+    from parity import dev_u64
+    d = T = 9
+    H = d + 1
+    layers = workload.layer_spec(6, 64)
+    weights = workload.he_normal_weights(layers, 81)
+    det, _ = workload.make_inputs(d, T, B, 0.02, 0.02, 82)
+    say("6 x 64 layers, tight, d = T =", d, "batch", B)
+    pre = pdx.Predecoder(weights, d, T, layers, "bf16", max_batch=B)
+    ddet = dev_u64(det)
+    x = torch.from_numpy(oracle.unpack(d, T, det))
+    off = 0
+    for l, (ci, co, k, act) in enumerate(layers):
+        nw = co * ci * k ** 3
+        w = tight.q_bf16(torch.from_numpy(weights[off:off + nw].reshape(co, ci, k, k, k).astype(np.float64)))
+        b = torch.from_numpy(weights[off + nw:off + nw + co].astype(np.float64))
+        off += nw + co
+        y = tight.conv(x, w, b, k)
+        # the 1x1x1 head sums on the vector ALU: an fp32 chain's bound
+        e = tight.eps_bf16_mfma(ci * k ** 3) if k > 1 else tight.eps_fma_chain(ci)
+        eps = e * tight.conv_mag(x, w, b, k) + tight.U32 * y.abs()
+        if l < len(layers) - 1:
+            out = torch.empty((B, T, H, H, co), dtype=torch.int16, device="cuda")
+            pre.activations(ddet, l, out)
+            torch.cuda.synchronize()
+            got = tight.bf16_bits_to_double(out.cpu()).permute(0, 4, 1, 2, 3).contiguous()
+            tight.check_stored("layer %d" % (l + 1), got, y, eps, act, tight.q_bf16, say=say)
+            x = got
+    _, _, logits = run_gpu(pre, det)
+    pre.close()
+    err = (torch.from_numpy(logits.astype(np.float64)) - y).abs()
+    say("  logits: max err %.3g, max err / bound %.3f" % (float(err.max()), float((err / (eps + 1e-6)).max())))
+    assert bool((err <= eps + 1e-6).all())
