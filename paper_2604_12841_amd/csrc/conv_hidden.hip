@@ -576,6 +576,36 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
     for (int k = 0; k < RMAX; ++k) soff[k] = stage_offset<ROW, MODE>(g, tl, src, cur_base, limit, tl.span, k, tid);
   }
 
+  // weight fragment (k-step gs, block nb of this wave's channels): buffer
+  // loads with this lane's slot (16 bytes; fp8: 32) as the vector offset and
+  // the fragment's offset as the scalar one (no per-load address arithmetic)
+  constexpr int WQ = F8 ? 2 : 1;  // 16-byte pieces per lane and fragment
+  const uint32_t wbytes = (uint32_t)(TSTEPS * NBT * P::WFRAG) << lsl;
+  const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc((void*)wfrag, 0, wbytes, 0x00020000);
+
+  // Small-batch launches of 32-channel slices have one workgroup per CU or
+  // fewer, whose short k-steps would each wait on their weight fragments
+  // coming from memory one after the other.  First the XCD's workgroups warm
+  // its L2 with all the layer's fragments, each loading a share at once (up
+  // to 32 KB), alongside the first chunk's staging; the values are folded
+  // into one register, kept to the end of the prologue.  (fp8 at d = 25,
+  // batch 1: 8 % less time per round.  Split K loops, whose k-steps are
+  // four times as long, gained nothing from it.)
+  constexpr bool WARM = COUT == 32 && KS == 3;
+  uint32_t warm = 0;
+  if constexpr (WARM) {
+    const uint32_t per = (gridDim.x >> 3) > 0 ? (gridDim.x >> 3) : 1u;  // this XCD's workgroups
+    const uint32_t share = ((wbytes + per - 1) / per + NT * 16 - 1) / (NT * 16) * (NT * 16);
+    const uint32_t b0 = (blockIdx.x >> 3) * share;
+    u32x4 pf[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i)  // offsets past the fragments read zeros
+      pf[i] = (uint32_t)i * NT * 16 < share ? __builtin_amdgcn_raw_buffer_load_b128(wres, b0 + (i * NT + tid) * 16, 0, 0)
+                                             : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int i = 0; i < 8; ++i) warm ^= pf[i].x;
+  }
+
   // First tile: stage its first chunk synchronously.
   {
     const __amdgpu_buffer_rsrc_t rs = stage_rsrc<ROW>(x, cur_base, (unit & (ksplit - 1)) * NCU * 32);
@@ -585,13 +615,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
       *(lds_u32x4_w*)(lds + stage_slot<KS>(k * NT + tid)) = v;
     }
   }
-
-  // weight fragment (k-step gs, block nb of this wave's channels): buffer
-  // loads with this lane's slot (16 bytes; fp8: 32) as the vector offset and
-  // the fragment's offset as the scalar one (no per-load address arithmetic)
-  constexpr int WQ = F8 ? 2 : 1;  // 16-byte pieces per lane and fragment
-  const __amdgpu_buffer_rsrc_t wres =
-      __builtin_amdgcn_make_buffer_rsrc((void*)wfrag, 0, (TSTEPS * NBT * P::WFRAG) << lsl, 0x00020000);
+  if constexpr (WARM) asm volatile("" ::"v"(warm));
   const uint32_t woff = (uint32_t)((wn * NB * 64 + lane) * 16 * WQ);
   auto wload = [&](int gs, int nb, u32x4 (&dst)[WQ]) {
 #pragma unroll
@@ -733,12 +757,15 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
                                                          __builtin_bit_cast(bf16x8, a[0]), c, 0, 0, 0);
         }
       };
-      // One register set of activation fragments: av[mb] is re-read for the
-      // next step as soon as this step's two MFMAs on it have issued, so it
-      // has the other row blocks' MFMAs to arrive.  Weight fragments are
-      // loaded RING - 1 steps ahead, staging rounds in the shadow of row
-      // block 0.
-      u32x4 av[MB][AQ];
+      // One register set of activation fragments (two for 32-channel
+      // slices): av[mb] is re-read for the next step as soon as this step's
+      // two MFMAs on it have issued, so it has the other row blocks' MFMAs to
+      // arrive.  Weight fragments are loaded RING - 1 steps ahead, staging
+      // rounds in the shadow of row block 0.
+      // AD: steps between a fragment's read and its use -- two for 32-channel
+      // slices, whose two MFMAs per step alone do not cover a read's latency
+      constexpr int AD = (COUT == 32 && KS == 3) ? 2 : 1;
+      u32x4 av[AD][MB][AQ];
       // Wave priority: a SIMD runs one wave of each of the two workgroups on
       // the CU; the one in its K loop goes ahead of one in staging waits or
       // the epilogue (1), and a wave about to issue MFMAs ahead of both (2),
@@ -748,7 +775,9 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
       // gain in bf16).
       __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) frag_read(mb, 0, av[mb]);
+      for (int d = 0; d < AD; ++d)
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) frag_read(mb, d, av[d][mb]);
       const int gbase = slice * TSTEPS + cc * NSTEP;                  // k-step of this chunk's step 0
       const int nbase = next_slice * TSTEPS + next_c0 * NSTEP - NSTEP;  // ... of the next unit's first chunk, minus NSTEP
       // staging of the next chunk: round k is loaded at step SG k and stored
@@ -775,10 +804,10 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
         for (int mb = 0; mb < MB; ++mb) {
           __builtin_amdgcn_s_setprio(2);
 #pragma unroll
-          for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = mfma(bq[st % RING][nb], av[mb], acc[mb][nb]);
+          for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = mfma(bq[st % RING][nb], av[st % AD][mb], acc[mb][nb]);
           if constexpr (!F8) __builtin_amdgcn_s_setprio(1);
           __builtin_amdgcn_sched_barrier(0);
-          if (st + 1 < NSTEP) frag_read(mb, st + 1, av[mb]);
+          if (st + AD < NSTEP) frag_read(mb, st + AD, av[st % AD][mb]);
           if constexpr (F8) __builtin_amdgcn_s_setprio(1);  // fp8: the fragment reads go out at 2 too
           if (mb == 0) {
             if (st >= SG && st % SG == 0 && st / SG - 1 < RMAX) stage_store(st / SG - 1);
