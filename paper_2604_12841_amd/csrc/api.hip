@@ -61,9 +61,10 @@ struct pd_predecoder {
   std::vector<size_t> wslice;    // per conv layer: bytes of the fragments of one 128-channel slice of a
                                  // 256-wide layer (run as two slices), 0 otherwise
   std::vector<float*> bdev;      // per conv layer: bias fp32 (a 3x3x3 output layer: [4] biases, [4] scales)
-  // per 64 -> 64 conv layer run by the hidden kernel (else null): its
-  // fragments and biases (fp8: and scales) as two slices of 32 output
-  // channels, for small batches (twice the workgroups per layer)
+  // per conv layer of 64 or 128 input and output channels run by the hidden
+  // kernel (else null): its fragments and biases (fp8: and scales) as slices
+  // of 32 output channels, for small batches (two or four times the
+  // workgroups per layer)
   std::vector<void*> wnarrow;
   std::vector<float*> bnarrow;
   float* head_w = nullptr;       // [4][c_in] fp32 (bf16-valued on the bf16 path)
@@ -897,11 +898,13 @@ pd_status enqueue_run(pd_predecoder* h, Workspace& ws, hipStream_t st, const uin
           s = check_launch(pd::launch_conv_first(g, L.c_in, cw, L.act, x, yk, L.c_out, wk, h->bdev[l] + k * cw,
                                                  batch, fp8, ks, st));
         }
-      } else if (!fuse_head && l < (int)h->wnarrow.size() && h->wnarrow[l] && tl.ntiles * 2 <= h->n_cu) {
-        // a small batch: a 64-wide layer as two 32-channel slices, twice the
-        // workgroups (still at most one per CU) for the same staging
-        s = run_hidden(h, ws, tl, L.c_in, 32, 2, L.act, x, y, L.c_out, h->wnarrow[l], h->bnarrow[l], 0, nullptr,
-                       nullptr, logits, batch, fp8, nullptr, 0, ks, st);
+      } else if (!fuse_head && l < (int)h->wnarrow.size() && h->wnarrow[l] &&
+                 tl.ntiles * (L.c_out / 32) <= h->n_cu) {
+        // a small batch: a 64- or 128-wide layer as 32-channel slices, two or
+        // four times the workgroups (still at most one per CU) for the same
+        // staging, in place of splitting its K loops
+        s = run_hidden(h, ws, tl, L.c_in, 32, L.c_out / 32, L.act, x, y, L.c_out, h->wnarrow[l], h->bnarrow[l], 0,
+                       nullptr, nullptr, logits, batch, fp8, nullptr, 0, ks, st);
       } else {  // the last hidden layer may carry the head and the threshold in its epilogue
         s = run_hidden(h, ws, tl, L.c_in, cw, nsl, L.act, x, y, L.c_out, h->wdev[l], h->bdev[l], fuse_head ? 1 : 0,
                        h->head_w, h->head_b, logits, batch, fp8, nullptr, 0, ks, st);
@@ -1198,28 +1201,33 @@ pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d
     s = upload(&bd, bias_dev.data(), bias_dev.size() * 4);
     h->bdev.push_back(bd);
     if (s != PD_OK) return fail(s);
-    // a 64 -> 64 layer of the hidden kernel: also as two 32-channel slices
-    // (fragments back to back; per slice its biases, then (fp8) its scales)
+    // a 64- or 128-wide layer of the hidden kernel: also as 32-channel
+    // slices (fragments back to back; per slice its biases, then (fp8) its
+    // scales)
     h->wnarrow.resize(h->wdev.size(), nullptr);
     h->bnarrow.resize(h->wdev.size(), nullptr);
-    if (i > 0 && L.k == 3 && L.c_in == 64 && L.c_out == 64 && dtype != PD_DTYPE_FP32) {
+    if (i > 0 && L.k == 3 && (L.c_in == 64 || L.c_in == 128) && (L.c_out == 64 || L.c_out == 128) &&
+        dtype != PD_DTYPE_FP32) {
       std::vector<float> bn;
       void* wn = nullptr;
+      const int nq = L.c_out / 32;
       if (dtype == PD_DTYPE_FP8) {
-        std::vector<uint8_t> f = conv_fragments_fp8(codes.data(), L.c_in, 32);
-        std::vector<uint8_t> f2 = conv_fragments_fp8(codes.data() + (size_t)32 * L.c_in * 27, L.c_in, 32);
-        f.insert(f.end(), f2.begin(), f2.end());
-        s = upload(&wn, f.data(), f.size());
-        for (int q = 0; q < 2; ++q) {
+        std::vector<uint8_t> f;
+        for (int q = 0; q < nq; ++q) {
+          std::vector<uint8_t> fq = conv_fragments_fp8(codes.data() + (size_t)32 * q * L.c_in * 27, L.c_in, 32);
+          f.insert(f.end(), fq.begin(), fq.end());
           bn.insert(bn.end(), b + 32 * q, b + 32 * (q + 1));
           bn.insert(bn.end(), scale.begin() + 32 * q, scale.begin() + 32 * (q + 1));
         }
+        s = upload(&wn, f.data(), f.size());
       } else {
-        std::vector<uint16_t> f = conv_fragments(w, L.c_in, 32);
-        std::vector<uint16_t> f2 = conv_fragments(w + (size_t)32 * L.c_in * 27, L.c_in, 32);
-        f.insert(f.end(), f2.begin(), f2.end());
+        std::vector<uint16_t> f;
+        for (int q = 0; q < nq; ++q) {
+          std::vector<uint16_t> fq = conv_fragments(w + (size_t)32 * q * L.c_in * 27, L.c_in, 32);
+          f.insert(f.end(), fq.begin(), fq.end());
+        }
         s = upload(&wn, f.data(), f.size() * 2);
-        bn.assign(b, b + 64);
+        bn.assign(b, b + L.c_out);
       }
       h->wnarrow.back() = wn;
       if (s != PD_OK) return fail(s);

@@ -1070,7 +1070,8 @@ hipError_t launch_case(const Geom& g, const Tiling& tl, int cin, int cout, int a
                                            tables, nib, logits, batch, n_workgroups, sk, sc, sc_stride, \
                                            stream);
   PD_HIDDEN_CASE(64, 64, EPI_ACT)
-  PD_HIDDEN_CASE(64, 32, EPI_ACT)  // a 64-wide layer in two slices (small batches)
+  PD_HIDDEN_CASE(64, 32, EPI_ACT)   // 64- and 128-wide layers in 32-channel slices (small batches)
+  PD_HIDDEN_CASE(128, 32, EPI_ACT)
   PD_HIDDEN_CASE(128, 128, EPI_ACT)
   PD_HIDDEN_CASE(64, 128, EPI_ACT)
   PD_HIDDEN_CASE(128, 64, EPI_ACT)
