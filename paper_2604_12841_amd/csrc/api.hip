@@ -63,10 +63,10 @@ struct pd_predecoder {
   std::vector<float*> bdev;      // per conv layer: bias fp32 (a 3x3x3 output layer: [4] biases, [4] scales)
   // per conv layer of 64 or 128 input and output channels run by the hidden
   // kernel (else null): its fragments and biases (fp8: and scales) as slices
-  // of 32 output channels, for small batches (two or four times the
-  // workgroups per layer)
-  std::vector<void*> wnarrow;
-  std::vector<float*> bnarrow;
+  // of 32 output channels, and (128 output channels) as slices of 64, for
+  // small batches (two or four times the workgroups per layer)
+  std::vector<void*> wnarrow, whalf;
+  std::vector<float*> bnarrow, bhalf;
   float* head_w = nullptr;       // [4][c_in] fp32 (bf16-valued on the bf16 path)
   float* head_b = nullptr;       // [4]
   // residual network (predecoder_create_resnet): its blocks; wdev / wslice /
@@ -480,6 +480,8 @@ void free_all(pd_predecoder* h) {
   for (float* p : h->bdev) f(p);
   for (void* p : h->wnarrow) f(p);
   for (float* p : h->bnarrow) f(p);
+  for (void* p : h->whalf) f(p);
+  for (float* p : h->bhalf) f(p);
   f(h->head_w);
   f(h->head_b);
   f(h->ws.partial);
@@ -491,6 +493,8 @@ void free_all(pd_predecoder* h) {
   h->bdev.clear();
   h->wnarrow.clear();
   h->bnarrow.clear();
+  h->whalf.clear();
+  h->bhalf.clear();
   h->head_w = h->head_b = nullptr;
   h->ws.partial = nullptr;
 }
@@ -905,6 +909,10 @@ pd_status enqueue_run(pd_predecoder* h, Workspace& ws, hipStream_t st, const uin
         // staging, in place of splitting its K loops
         s = run_hidden(h, ws, tl, L.c_in, 32, L.c_out / 32, L.act, x, y, L.c_out, h->wnarrow[l], h->bnarrow[l], 0,
                        nullptr, nullptr, logits, batch, fp8, nullptr, 0, ks, st);
+      } else if (!fuse_head && l < (int)h->whalf.size() && h->whalf[l] && tl.ntiles * 2 <= h->n_cu) {
+        // ... or, with too many tiles for that, a 128-wide one as two slices of 64
+        s = run_hidden(h, ws, tl, L.c_in, 64, 2, L.act, x, y, L.c_out, h->whalf[l], h->bhalf[l], 0, nullptr, nullptr,
+                       logits, batch, fp8, nullptr, 0, ks, st);
       } else {  // the last hidden layer may carry the head and the threshold in its epilogue
         s = run_hidden(h, ws, tl, L.c_in, cw, nsl, L.act, x, y, L.c_out, h->wdev[l], h->bdev[l], fuse_head ? 1 : 0,
                        h->head_w, h->head_b, logits, batch, fp8, nullptr, 0, ks, st);
@@ -1201,37 +1209,38 @@ pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d
     s = upload(&bd, bias_dev.data(), bias_dev.size() * 4);
     h->bdev.push_back(bd);
     if (s != PD_OK) return fail(s);
-    // a 64- or 128-wide layer of the hidden kernel: also as 32-channel
-    // slices (fragments back to back; per slice its biases, then (fp8) its
-    // scales)
-    h->wnarrow.resize(h->wdev.size(), nullptr);
-    h->bnarrow.resize(h->wdev.size(), nullptr);
-    if (i > 0 && L.k == 3 && (L.c_in == 64 || L.c_in == 128) && (L.c_out == 64 || L.c_out == 128) &&
-        dtype != PD_DTYPE_FP32) {
-      std::vector<float> bn;
-      void* wn = nullptr;
-      const int nq = L.c_out / 32;
+    // a 64- or 128-wide layer of the hidden kernel: also as slices of sw
+    // output channels (fragments back to back; per slice its biases, then
+    // (fp8) its scales)
+    auto slices = [&](int sw, void** wn, float** bn) -> pd_status {
+      std::vector<float> bq;
+      pd_status st;
       if (dtype == PD_DTYPE_FP8) {
         std::vector<uint8_t> f;
-        for (int q = 0; q < nq; ++q) {
-          std::vector<uint8_t> fq = conv_fragments_fp8(codes.data() + (size_t)32 * q * L.c_in * 27, L.c_in, 32);
+        for (int q = 0; q < L.c_out / sw; ++q) {
+          std::vector<uint8_t> fq = conv_fragments_fp8(codes.data() + (size_t)sw * q * L.c_in * 27, L.c_in, sw);
           f.insert(f.end(), fq.begin(), fq.end());
-          bn.insert(bn.end(), b + 32 * q, b + 32 * (q + 1));
-          bn.insert(bn.end(), scale.begin() + 32 * q, scale.begin() + 32 * (q + 1));
+          bq.insert(bq.end(), b + sw * q, b + sw * (q + 1));
+          bq.insert(bq.end(), scale.begin() + sw * q, scale.begin() + sw * (q + 1));
         }
-        s = upload(&wn, f.data(), f.size());
+        st = upload(wn, f.data(), f.size());
       } else {
         std::vector<uint16_t> f;
-        for (int q = 0; q < nq; ++q) {
-          std::vector<uint16_t> fq = conv_fragments(w + (size_t)32 * q * L.c_in * 27, L.c_in, 32);
+        for (int q = 0; q < L.c_out / sw; ++q) {
+          std::vector<uint16_t> fq = conv_fragments(w + (size_t)sw * q * L.c_in * 27, L.c_in, sw);
           f.insert(f.end(), fq.begin(), fq.end());
         }
-        s = upload(&wn, f.data(), f.size() * 2);
-        bn.assign(b, b + L.c_out);
+        st = upload(wn, f.data(), f.size() * 2);
+        bq.assign(b, b + L.c_out);
       }
-      h->wnarrow.back() = wn;
-      if (s != PD_OK) return fail(s);
-      s = upload(&h->bnarrow.back(), bn.data(), bn.size() * 4);
+      return st != PD_OK ? st : upload(bn, bq.data(), bq.size() * 4);
+    };
+    for (auto* v : {&h->wnarrow, &h->whalf}) v->resize(h->wdev.size(), nullptr);
+    for (auto* v : {&h->bnarrow, &h->bhalf}) v->resize(h->wdev.size(), nullptr);
+    if (i > 0 && L.k == 3 && (L.c_in == 64 || L.c_in == 128) && (L.c_out == 64 || L.c_out == 128) &&
+        dtype != PD_DTYPE_FP32) {
+      s = slices(32, &h->wnarrow.back(), &h->bnarrow.back());
+      if (s == PD_OK && L.c_out == 128) s = slices(64, &h->whalf.back(), &h->bhalf.back());
     }
     if (s != PD_OK) return fail(s);
   }
