@@ -61,10 +61,10 @@ struct pd_predecoder {
   std::vector<size_t> wslice;    // per conv layer: bytes of the fragments of one 128-channel slice of a
                                  // 256-wide layer (run as two slices), 0 otherwise
   std::vector<float*> bdev;      // per conv layer: bias fp32 (a 3x3x3 output layer: [4] biases, [4] scales)
-  // per conv layer of 64 or 128 input and output channels run by the hidden
+  // per conv layer of 64 to 256 input and output channels run by the hidden
   // kernel (else null): its fragments and biases (fp8: and scales) as slices
-  // of 32 output channels, and (128 output channels) as slices of 64, for
-  // small batches (two or four times the workgroups per layer)
+  // of 32 output channels, and (128 or 256 output channels) as slices of 64,
+  // for small batches (more workgroups per layer)
   std::vector<void*> wnarrow, whalf;
   std::vector<float*> bnarrow, bhalf;
   float* head_w = nullptr;       // [4][c_in] fp32 (bf16-valued on the bf16 path)
@@ -881,7 +881,8 @@ pd_status enqueue_run(pd_predecoder* h, Workspace& ws, hipStream_t st, const uin
     const pd_layer& L = h->layers[l];
     const int row_bytes = L.c_out * (fp32 ? 4 : aelem);
     if ((s = prepare_rows(ws, l & 1, row_bytes, st)) != PD_OK) return s;
-    const bool fuse_head = !fp32 && !out3 && l == n - 2 && stop < 0;
+    const bool head_layer = !fp32 && !out3 && l == n - 2;  // carries the head unless the run stops at it
+    const bool fuse_head = head_layer && stop < 0;
     if (fp32) {
       s = check_launch(pd::launch_conv_fp32(g, L.c_in, L.c_out, L.act, (const float*)x, (float*)y,
                                             (const float*)h->wdev[l], h->bdev[l], batch, st));
@@ -902,17 +903,20 @@ pd_status enqueue_run(pd_predecoder* h, Workspace& ws, hipStream_t st, const uin
           s = check_launch(pd::launch_conv_first(g, L.c_in, cw, L.act, x, yk, L.c_out, wk, h->bdev[l] + k * cw,
                                                  batch, fp8, ks, st));
         }
-      } else if (!fuse_head && l < (int)h->wnarrow.size() && h->wnarrow[l] &&
+      } else if (!head_layer && l < (int)h->wnarrow.size() && h->wnarrow[l] &&
                  tl.ntiles * (L.c_out / 32) <= h->n_cu) {
-        // a small batch: a 64- or 128-wide layer as 32-channel slices, two or
-        // four times the workgroups (still at most one per CU) for the same
-        // staging, in place of splitting its K loops
+        // a small batch: a 64- to 256-wide layer as 32-channel slices, two to
+        // eight times the workgroups (still at most one per CU) for the same
+        // staging, in place of splitting its K loops (a 256-channel input's
+        // long loops may still split).  The layer that carries the head is
+        // never sliced, also when a run stops at it, so that its exported
+        // activations are the ones the head reads.
         s = run_hidden(h, ws, tl, L.c_in, 32, L.c_out / 32, L.act, x, y, L.c_out, h->wnarrow[l], h->bnarrow[l], 0,
                        nullptr, nullptr, logits, batch, fp8, nullptr, 0, ks, st);
-      } else if (!fuse_head && l < (int)h->whalf.size() && h->whalf[l] && tl.ntiles * 2 <= h->n_cu) {
-        // ... or, with too many tiles for that, a 128-wide one as two slices of 64
-        s = run_hidden(h, ws, tl, L.c_in, 64, 2, L.act, x, y, L.c_out, h->whalf[l], h->bhalf[l], 0, nullptr, nullptr,
-                       logits, batch, fp8, nullptr, 0, ks, st);
+      } else if (!head_layer && l < (int)h->whalf.size() && h->whalf[l] && tl.ntiles * (L.c_out / 64) <= h->n_cu) {
+        // ... or, with too many tiles for that, a 128- or 256-wide one as slices of 64
+        s = run_hidden(h, ws, tl, L.c_in, 64, L.c_out / 64, L.act, x, y, L.c_out, h->whalf[l], h->bhalf[l], 0,
+                       nullptr, nullptr, logits, batch, fp8, nullptr, 0, ks, st);
       } else {  // the last hidden layer may carry the head and the threshold in its epilogue
         s = run_hidden(h, ws, tl, L.c_in, cw, nsl, L.act, x, y, L.c_out, h->wdev[l], h->bdev[l], fuse_head ? 1 : 0,
                        h->head_w, h->head_b, logits, batch, fp8, nullptr, 0, ks, st);
@@ -1237,10 +1241,13 @@ pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d
     };
     for (auto* v : {&h->wnarrow, &h->whalf}) v->resize(h->wdev.size(), nullptr);
     for (auto* v : {&h->bnarrow, &h->bhalf}) v->resize(h->wdev.size(), nullptr);
-    if (i > 0 && L.k == 3 && (L.c_in == 64 || L.c_in == 128) && (L.c_out == 64 || L.c_out == 128) &&
-        dtype != PD_DTYPE_FP32) {
-      s = slices(32, &h->wnarrow.back(), &h->bnarrow.back());
-      if (s == PD_OK && L.c_out == 128) s = slices(64, &h->whalf.back(), &h->bhalf.back());
+    // (256 input channels: 32-channel slices in fp8 only, no 64-channel
+    // ones -- in bf16 their 16-chunk K loops measured slower than the split
+    // loops of 128-channel slices, at batch 1 of Models 2 and 5)
+    auto width_ok = [](int c) { return c == 64 || c == 128 || c == 256; };
+    if (i > 0 && L.k == 3 && width_ok(L.c_in) && width_ok(L.c_out) && dtype != PD_DTYPE_FP32) {
+      if (L.c_in <= 128 || dtype == PD_DTYPE_FP8) s = slices(32, &h->wnarrow.back(), &h->bnarrow.back());
+      if (s == PD_OK && L.c_in <= 128 && L.c_out >= 128) s = slices(64, &h->whalf.back(), &h->bhalf.back());
     }
     if (s != PD_OK) return fail(s);
   }

@@ -164,17 +164,19 @@ struct Split {
 // per-channel weight scales [COUT] (fp8) and the head weights [4][COUT].
 // The head epilogue puts its partial sums in the staging buffer the tile
 // read last.
-constexpr int kMaxSlices = 4;  // output-channel slices of one launch
+// output-channel slices of one launch: up to 8 of 32 channels (a 256-wide
+// layer), else up to 4
+__host__ __device__ constexpr int max_slices(int cout) { return cout == 32 ? 8 : 4; }
 
 template <int COUT, int KS>
 struct Lds {
   static constexpr int ABUF = Conv<KS>::ABUF;
   static constexpr int zero = 2 * ABUF;
-  // biases (fp8: then the weight scales) of up to kMaxSlices output-channel
-  // slices; a head's weights (never sliced) follow one slice's
+  // biases (fp8: then the weight scales) of up to max_slices(COUT)
+  // output-channel slices; a head's weights (never sliced) follow one slice's
   static constexpr int bias = zero + 512;
   static constexpr int headw = bias + 2 * COUT * 4;
-  static constexpr int total = bias + (2 * kMaxSlices > 6 ? 2 * kMaxSlices : 6) * COUT * 4;
+  static constexpr int total = bias + (2 * max_slices(COUT) > 6 ? 2 * max_slices(COUT) : 6) * COUT * 4;
   static_assert(zero % 256 == 0, "zero region must be 256-aligned");
   static_assert(Conv<KS>::WG_PER_CU * total <= 160 * 1024, "the workgroups of a CU fit its LDS");
   static_assert(Split<COUT>::WN * kTileRows * 4 * 4 <= ABUF, "head partials fit a staging buffer");
@@ -1070,8 +1072,9 @@ hipError_t launch_case(const Geom& g, const Tiling& tl, int cin, int cout, int a
                                            tables, nib, logits, batch, n_workgroups, sk, sc, sc_stride, \
                                            stream);
   PD_HIDDEN_CASE(64, 64, EPI_ACT)
-  PD_HIDDEN_CASE(64, 32, EPI_ACT)   // 64- and 128-wide layers in 32-channel slices (small batches)
+  PD_HIDDEN_CASE(64, 32, EPI_ACT)   // 64- to 256-wide layers in 32-channel slices (small batches)
   PD_HIDDEN_CASE(128, 32, EPI_ACT)
+  PD_HIDDEN_CASE(256, 32, EPI_ACT)
   PD_HIDDEN_CASE(128, 128, EPI_ACT)
   PD_HIDDEN_CASE(64, 128, EPI_ACT)
   PD_HIDDEN_CASE(128, 64, EPI_ACT)
@@ -1125,9 +1128,9 @@ hipError_t launch_conv_hidden(const Geom& g, const Tiling& tl, int cin, int cout
   if (sk.kshift < 0 || nchunk % (1 << sk.kshift) != 0 ||
       (sk.kshift > 0 && (tl.ntiles << (sk.kshift + sk.lsl)) > sk.max_units))
     return hipErrorInvalidValue;
-  // output-channel slices: up to kMaxSlices, of activation layers (a head or
+  // output-channel slices: up to max_slices, of activation layers (a head or
   // an output layer needs every channel of a voxel in one unit)
-  if (sk.lsl < 0 || (1 << sk.lsl) > kMaxSlices || (sk.lsl > 0 && head != EPI_ACT && head != EPI_ADD))
+  if (sk.lsl < 0 || (1 << sk.lsl) > max_slices(cout) || (sk.lsl > 0 && head != EPI_ACT && head != EPI_ADD))
     return hipErrorInvalidValue;
   if (fp8)
     return launch_case<true>(g, tl, cin, cout, act, x, y, ystride, wfrag, bias, head, head_w, head_b, tables, nib,

@@ -195,22 +195,23 @@ def test_layer1_same_at_any_launch_size(cuda, dtype):
     pre.close()
 
 
-@pytest.mark.parametrize("B", [1, 40])
-def test_64_wide_layers_tight(cuda, B):
-    """The 6 x 64 network at d = T = 9: at batch 1 each 64 -> 64 layer runs
-    as two slices of 32 output channels (twice the workgroups), at batch 40
-    whole.  Either way every hidden layer's stored bf16 activations are
-    checked from the GPU's own input under the rule of tests/tight.py, then
-    the logits from the GPU's last hidden activations within their own sums'
-    bound."""
+@pytest.mark.parametrize("width,n,B", [(64, 6, 1), (64, 6, 40), (128, 4, 1), (128, 4, 20), (128, 4, 40)])
+def test_sliced_layers_tight(cuda, width, n, B):
+    """n hidden layers of 64 or 128 channels at d = T = 9 (4, 70 and 141
+    tiles at batches 1, 20 and 40): at batch 1 each C -> C layer but the
+    last runs as 32-channel output slices, at batch 20 a 128-wide one as two
+    slices of 64, at batch 40 whole.  Either way every hidden layer's stored
+    bf16 activations are checked from the GPU's own input under the rule of
+    tests/tight.py, then the logits from the GPU's last hidden activations
+    within their own sums' bound."""
     import tight
     from parity import dev_u64
     d = T = 9
     H = d + 1
-    layers = workload.layer_spec(6, 64)
-    weights = workload.he_normal_weights(layers, 81)
+    layers = workload.layer_spec(n, width)
+    weights = workload.he_normal_weights(layers, 81 + width)
     det, _ = workload.make_inputs(d, T, B, 0.02, 0.02, 82)
-    say("6 x 64 layers, tight, d = T =", d, "batch", B)
+    say("%d x %d layers, tight, d = T =" % (n, width), d, "batch", B)
     pre = pdx.Predecoder(weights, d, T, layers, "bf16", max_batch=B)
     ddet = dev_u64(det)
     x = torch.from_numpy(oracle.unpack(d, T, det))

@@ -163,6 +163,8 @@ TIGHT = [
     dict(name="paper_m1", layout="paper", layers=workload.paper_model_layers(1), d=7),
     dict(name="paper_256", layout="paper", layers=workload.paper_layer_spec([256, 256, 4], [3, 3, 3]), d=5),
     dict(name="paper_64_d17", layout="paper", layers=workload.paper_layer_spec([64, 64, 4], [3, 3, 3]), d=17),
+    # 70 tiles at batch 40: the 128-wide layers as two slices of 64 (batch 1: four of 32)
+    dict(name="plaq_4x128_head_d7", layout="plaquette", layers=workload.layer_spec(4, 128), d=7),
 ]
 
 
