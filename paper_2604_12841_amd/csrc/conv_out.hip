@@ -433,25 +433,38 @@ hipError_t launch_conv_out(const Geom& g, int cin, const void* x, const void* wf
   if (g.pad != 1 || batch < 1 || !conv_out_supported(cin, fp8, 3, g.H)) return hipErrorInvalidValue;
   const bool proj = px != nullptr;
   if (proj && (!pfrag || !pbias || sc)) return hipErrorInvalidValue;
-  int nsi = 1, nsj = 1;
-  conv_out_split(g.H, MV, &nsi, &nsj);
-  // rounds per unit: the split of T that minimises (units per CU, rounded
-  // up) x (input rounds per unit)
-  const long long per = (long long)batch * nsi * nsj;
-  int nch = 1;
+  // Rectangles and rounds per unit: from the split with the fewest staged
+  // voxels up to three more parts each way, and every split of T, the one
+  // that minimises (units per CU, rounded up) x (input rounds per unit) x
+  // (staged voxels per round + a fixed cost per round of about 128 voxels'
+  // worth).  Large batches keep the fewest staged voxels; small ones take
+  // smaller rectangles, which fill more of the chip.
+  int s0i = 1, s0j = 1;
+  conv_out_split(g.H, MV, &s0i, &s0j);
+  int nsi = s0i, nsj = s0j, nch = 1;
   long long best = -1;
-  for (int c = 1; c <= g.T; ++c) {
-    const long long units = per * c;
-    if (units > 0x7fffffffLL) break;
-    const long long waves = (units + n_cu - 1) / n_cu;
-    const long long rounds = (g.T + c - 1) / c + (c > 1 ? 2 : 0);
-    const long long cost = waves * rounds;
-    if (best < 0 || cost < best) {
-      best = cost;
-      nch = c;
+  for (int sj = s0j; sj <= std::min(g.H, s0j + 3); ++sj) {
+    const int cols = sj == 1 ? g.H : std::min(g.H, (g.H + sj - 1) / sj + 2);
+    for (int si = s0i; si <= std::min(g.H, s0i + 3); ++si) {
+      const int rows = si == 1 ? g.H : std::min(g.H, (g.H + si - 1) / si + 2);
+      if (rows * cols > MV) continue;
+      const long long per = (long long)batch * si * sj;
+      for (int c = 1; c <= g.T; ++c) {
+        const long long units = per * c;
+        if (units > 0x7fffffffLL) break;
+        const long long waves = (units + n_cu - 1) / n_cu;
+        const long long rounds = (g.T + c - 1) / c + (c > 1 ? 2 : 0);
+        const long long cost = waves * rounds * (rows * cols + 128);
+        if (best < 0 || cost < best) {
+          best = cost;
+          nsi = si;
+          nsj = sj;
+          nch = c;
+        }
+      }
     }
   }
-  const long long units = per * nch;
+  const long long units = (long long)batch * nsi * nsj * nch;
   if (units > 0x7fffffffLL) return hipErrorInvalidValue;
   auto go = [&](auto kern, bool p) -> hipError_t {
     const size_t lds = lds_bytes(p);
