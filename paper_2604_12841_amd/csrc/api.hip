@@ -24,9 +24,12 @@ using pd::Tiling;
 
 namespace {
 
+constexpr size_t kSchedWords = 256;  // the hidden kernel's unit counters: 8 XCDs x 2 x 16 words
+
 // Device memory one run works in besides its inputs, outputs, weights and
 // tables: the input planes, the activation buffers, the projection outputs of
-// residual blocks, the flip nibbles and the parked sums of split K loops.
+// residual blocks, the flip nibbles, the parked sums of split K loops and the
+// hidden kernel's unit counters.
 // A handle owns one (sized for max_batch at create); predecoder_run_static
 // lays one over the library's static scratch array for each call.
 struct Workspace {
@@ -36,6 +39,7 @@ struct Workspace {
   uint8_t* nib = nullptr;                      // [batch][T][H][H] flip nibbles
   float* partial = nullptr;                    // split K loops of small batches: fp32 sums of up to max_units units
   long long max_units = 0;
+  uint32_t* sched = nullptr;                   // the hidden kernel's unit counters (kSchedWords, zero between launches)
   size_t act_bytes = 0;                        // size of each activation buffer
   // Row width (bytes per voxel) of the data each activation buffer holds, 0
   // while it is all zero.  The 3x3x3 kernels read the zero halo around the
@@ -485,6 +489,7 @@ void free_all(pd_predecoder* h) {
   f(h->head_w);
   f(h->head_b);
   f(h->ws.partial);
+  f(h->ws.sched);
   h->ws.planes = h->ws.act[0] = h->ws.act[1] = nullptr;
   h->ws.nib = nullptr;
   h->tables = nullptr;
@@ -497,6 +502,7 @@ void free_all(pd_predecoder* h) {
   h->bhalf.clear();
   h->head_w = h->head_b = nullptr;
   h->ws.partial = nullptr;
+  h->ws.sched = nullptr;
 }
 
 // bf16 A fragments (weights) for v_mfma_f32_32x32x16_bf16: lane l of
@@ -656,6 +662,7 @@ pd::Split_k split_for(const Workspace& ws, const Tiling& t, int cin, int cout, i
   const double epi = 3.3 + 4.0 * wide, park = 1.75 + 1.65 * wide;
   const double finish = 8.0;
   pd::Split_k sk{0, ws.partial, ws.max_units};
+  sk.sched = ws.sched;
   while ((1 << sk.lsl) < nsl) ++sk.lsl;
   double best = nch * chunk + epi;
   if (unit_us) *unit_us = best;
@@ -1093,6 +1100,8 @@ pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d
     if ((s = dev_alloc(&h->ws.partial, (size_t)h->ws.max_units * pd::conv_hidden_partial_floats_per_unit() * 4)) !=
         PD_OK)
       return fail(s);
+    if ((s = dev_alloc(&h->ws.sched, kSchedWords * 4)) != PD_OK) return fail(s);
+    if (hipMemset(h->ws.sched, 0, kSchedWords * 4) != hipSuccess) return fail(PD_ERR_DEVICE);
   }
   std::vector<int32_t> tab = build_tables(g);
   if ((s = upload(&h->tables, tab.data(), tab.size() * sizeof(int32_t))) != PD_OK) return fail(s);
@@ -1372,6 +1381,8 @@ pd_status predecoder_create_resnet(const float* weights, size_t n_weights, int32
   h->ws.max_units = h->n_cu;
   if ((s = dev_alloc(&h->ws.partial, (size_t)h->ws.max_units * pd::conv_hidden_partial_floats_per_unit() * 4)) != PD_OK)
     return fail(s);
+  if ((s = dev_alloc(&h->ws.sched, kSchedWords * 4)) != PD_OK) return fail(s);
+  if (hipMemset(h->ws.sched, 0, kSchedWords * 4) != hipSuccess) return fail(PD_ERR_DEVICE);
   std::vector<int32_t> tab = build_tables(g);
   if ((s = upload(&h->tables, tab.data(), tab.size() * sizeof(int32_t))) != PD_OK) return fail(s);
   if (hipMemset(h->ws.planes, 0, vox * cin0 * 2) != hipSuccess || hipMemset(h->ws.act[0], 0, vox * cmax * 2) != hipSuccess ||
@@ -1533,6 +1544,7 @@ pd_status run_in_region(pd_predecoder* h, hipStream_t st, const uint64_t* det, i
     o_pbuf = carve(vox * (size_t)h->pmax * 2);
   }
   const size_t o_nib = carve((size_t)batch * g.V);
+  const size_t o_sched = fp32 ? 0 : carve(kSchedWords * 4);
   if (off > bytes) return PD_ERR_TOO_LARGE;
   char* b = (char*)base;
   Workspace ws;
@@ -1554,6 +1566,10 @@ pd_status run_in_region(pd_predecoder* h, hipStream_t st, const uint64_t* det, i
   pd_status s = check_launch(launch_zero(ws.planes, (planes_bytes + 15) & ~(size_t)15, st));
   for (int k = 0; k < (resnet ? 3 : 2) && s == PD_OK; ++k)
     s = check_launch(launch_zero(ws.act[k], (act_bytes + 15) & ~(size_t)15, st));
+  if (!fp32 && s == PD_OK) {  // the hidden kernel's unit counters start at zero (and stay so between launches)
+    ws.sched = (uint32_t*)(b + o_sched);
+    s = check_launch(launch_zero(ws.sched, kSchedWords * 4, st));
+  }
   if (s != PD_OK) return s;
   return enqueue_run(h, ws, st, det, batch, flips, residual, logits, nullptr);
 }

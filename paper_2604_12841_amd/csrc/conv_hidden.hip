@@ -176,7 +176,9 @@ struct Lds {
   // output-channel slices; a head's weights (never sliced) follow one slice's
   static constexpr int bias = zero + 512;
   static constexpr int headw = bias + 2 * COUT * 4;
-  static constexpr int total = bias + (2 * max_slices(COUT) > 6 ? 2 * max_slices(COUT) : 6) * COUT * 4;
+  // two unit numbers handed between the waves (dynamic scheduling)
+  static constexpr int sched = bias + (2 * max_slices(COUT) > 6 ? 2 * max_slices(COUT) : 6) * COUT * 4;
+  static constexpr int total = sched + 16;
   static_assert(zero % 256 == 0, "zero region must be 256-aligned");
   static_assert(Conv<KS>::WG_PER_CU * total <= 160 * 1024, "the workgroups of a CU fit its LDS");
   static_assert(Split<COUT>::WN * kTileRows * 4 * 4 <= ABUF, "head partials fit a staging buffer");
@@ -301,7 +303,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
                    const float* __restrict__ head_w, const float* __restrict__ head_b,
                    const int32_t* __restrict__ tables, uint8_t* __restrict__ nib,
                    float* __restrict__ logits, int batch, int kshift_arg, float* __restrict__ partial,
-                   const uint16_t* __restrict__ sc, int sc_stride, int lsl) {
+                   const uint16_t* __restrict__ sc, int sc_stride, int lsl, uint32_t* __restrict__ sched) {
   static_assert(KS == 3 || MODE == 1, "5x5x5 layers run on box tiles");
   extern __shared__ __attribute__((aligned(16))) char smem[];
   using W = Split<COUT>;
@@ -565,8 +567,46 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
       }
   };
 
+  // Units: each XCD takes a contiguous range (tile_of).  A workgroup's first
+  // two units are fixed (the k-th and (k + n)-th of its XCD's range, n = the
+  // XCD's workgroups); with `sched` (a launch of more units than that), the
+  // rest are taken in turn from a per-XCD counter, so that workgroups that
+  // run faster take more of them (fixed shares left the last workgroups of
+  // an XCD finishing about 14 % of the layer after the first).  Thread 0
+  // takes unit it + 2 at the top of iteration it and hands it over in LDS
+  // slot it % 2 at the end of the iteration's first chunk, read by every
+  // wave at the top of iteration it + 1 (a chunk's barrier in between).  Counters sit in separate 64-byte lines
+  // (grab, then done, per XCD); the last workgroup of an XCD to finish puts
+  // both back to zero for the next launch.  Only the bf16 128-wide 3x3x3
+  // activation and head instances take it: the 8 x 128 networks at d = 13
+  // and 31 gain about 3 %; the fp8 and 64-wide ones gained nothing, and the
+  // counters' registers made the fp8 head instance spill in its K loop (and
+  // the shortcut-adding ones spill more).
+  constexpr bool DYN = COUT == 128 && !F8 && KS == 3 && (EPI == EPI_ACT || EPI == EPI_HEAD);
+  if (!DYN) sched = nullptr;
+  const int xcd = blockIdx.x & 7, nwx = gridDim.x >> 3, per_xcd = (nunits + 7) >> 3;
+  uint32_t* const grab = sched ? sched + xcd * 32 : nullptr;
+  uint32_t* const done = sched ? sched + xcd * 32 + 16 : nullptr;
+  lds_u32_w* const dyn_s = (lds_u32_w*)(lds + L::sched);
+  auto finish_sched = [&]() {
+    if (sched && tid == 0 &&
+        __hip_atomic_fetch_add(done, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == (uint32_t)nwx - 1) {
+      __hip_atomic_store(grab, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(done, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  };
+  auto dyn_unit = [&](uint32_t c) -> int {  // unit of the c-th counter value (-1: none left)
+    const long long local = 2ll * nwx + c;
+    if (local >= per_xcd) return -1;
+    const long long u = (long long)xcd * per_xcd + local;
+    return u < nunits ? (int)u : -1;
+  };
+
   int unit = tile_of(blockIdx.x, gridDim.x, 0, nunits);
-  if (unit < 0) return;
+  if (unit < 0) {
+    finish_sched();
+    return;
+  }
   int tile = unit >> (kshift + lsl);
 
   auto source_of = [&](int t) { return tile_source(g, tl, t, batch); };
@@ -638,7 +678,16 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
   for (int it = 0; unit >= 0; ++it) {
     const int c0 = (unit & (ksplit - 1)) * NCU;  // first chunk of this unit
     const int slice = slice_of(unit);
-    const int next_unit = tile_of(blockIdx.x, gridDim.x, it + 1, nunits);
+    int next_unit;
+    if (!sched || it == 0) {
+      next_unit = tile_of(blockIdx.x, gridDim.x, it + 1, nunits);
+    } else {
+      next_unit = (int)__builtin_amdgcn_readfirstlane(dyn_s[(it - 1) & 1]);
+    }
+    // unit it + 2 (written to LDS at the end of the first chunk, so that no
+    // wave waits here for the counter)
+    uint32_t grabbed = 0;
+    if (sched && tid == 0) grabbed = __hip_atomic_fetch_add(grab, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const int next = next_unit >= 0 ? next_unit >> (kshift + lsl) : -1;
     const int next_c0 = next_unit >= 0 ? (next_unit & (ksplit - 1)) * NCU : 0;
     const int next_slice = next_unit >= 0 ? slice_of(next_unit) : 0;
@@ -824,6 +873,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
       }
       __builtin_amdgcn_s_setprio(0);
       if constexpr (SG * RMAX >= NSTEP) stage_store(RMAX - 1);
+      if (sched && tid == 0 && chunk == 0) dyn_s[it & 1] = (uint32_t)dyn_unit(grabbed);
       // every wave's staging writes done, every wave done reading `cur`
       __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
       __builtin_amdgcn_s_barrier();
@@ -851,6 +901,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
     cur_base = next_base;
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  finish_sched();
 }
 
 // Second kernel of a split K loop: one thread per (tile row, 8 channels)
@@ -1005,7 +1056,7 @@ hipError_t launch_hidden(const Geom& g, const Tiling& tl, int act, const void* x
                          const void* wfrag, const float* bias, const float* head_w, const float* head_b,
                          const int32_t* tables, uint8_t* nib, float* logits, int batch, int n_workgroups,
                          int kshift, float* partial, const uint16_t* sc, int sc_stride, int lsl,
-                         hipStream_t stream) {
+                         uint32_t* sched, hipStream_t stream) {
   using L = Lds<COUT, KS>;
   static bool attr_set = false;
   if (!attr_set) {
@@ -1014,10 +1065,12 @@ hipError_t launch_hidden(const Geom& g, const Tiling& tl, int act, const void* x
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  const long long nwg = conv_workgroups(tl.ntiles << (kshift + lsl), n_workgroups);
+  const long long nunits = tl.ntiles << (kshift + lsl);
+  const long long nwg = conv_workgroups(nunits, n_workgroups);
+  if (nunits <= 2 * nwg) sched = nullptr;  // every unit is one of the two fixed ones
   hipLaunchKernelGGL((conv_hidden_kernel<CIN, COUT, EPI, MODE, F8, KS>), dim3((unsigned)nwg), dim3(NT),
                      (size_t)L::total, stream, g, tl, act, x, y, ystride, (const u32x4*)wfrag, bias, head_w,
-                     head_b, tables, nib, logits, batch, kshift, partial, sc, sc_stride, lsl);
+                     head_b, tables, nib, logits, batch, kshift, partial, sc, sc_stride, lsl, sched);
   return hipSuccess;
 }
 
@@ -1030,13 +1083,13 @@ hipError_t launch_one(const Geom& g, const Tiling& tl, int act, const void* x, v
   if (sk.kshift == 0) {
     e = launch_hidden<CIN, COUT, EPI, MODE, F8, KS>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b,
                                                     tables, nib, logits, batch, n_workgroups, 0, nullptr, sc,
-                                                    sc_stride, sk.lsl, stream);
+                                                    sc_stride, sk.lsl, sk.sched, stream);
     return e != hipSuccess ? e : hipGetLastError();
   }
   // K loops split: park the parts, then add them and finish the tiles
   e = launch_hidden<CIN, COUT, EPI_PARK, MODE, F8, KS>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b,
                                                        tables, nib, logits, batch, n_workgroups, sk.kshift,
-                                                       sk.partial, nullptr, 0, sk.lsl, stream);
+                                                       sk.partial, nullptr, 0, sk.lsl, sk.sched, stream);
   if (e != hipSuccess) return e;
   const long long threads = ((long long)tl.ntiles << sk.lsl) * kTileRows *
                             (EPI == EPI_ACT || EPI == EPI_ADD || EPI == EPI_HEAD ? COUT / 8 : 1);
