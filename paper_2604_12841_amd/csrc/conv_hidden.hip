@@ -572,17 +572,20 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
   // XCD's workgroups); with `sched` (a launch of more units than that), the
   // rest are taken in turn from a per-XCD counter, so that workgroups that
   // run faster take more of them (fixed shares left the last workgroups of
-  // an XCD finishing about 14 % of the layer after the first).  Thread 0
+  // an XCD finishing 10-20 % of the layer after the first).  Thread 0
   // takes unit it + 2 at the top of iteration it and hands it over in LDS
   // slot it % 2 at the end of the iteration's first chunk, read by every
   // wave at the top of iteration it + 1 (a chunk's barrier in between).  Counters sit in separate 64-byte lines
   // (grab, then done, per XCD); the last workgroup of an XCD to finish puts
   // both back to zero for the next launch.  Only the bf16 128-wide 3x3x3
-  // activation and head instances take it: the 8 x 128 networks at d = 13
-  // and 31 gain about 3 %; the fp8 and 64-wide ones gained nothing, and the
-  // counters' registers made the fp8 head instance spill in its K loop (and
-  // the shortcut-adding ones spill more).
-  constexpr bool DYN = COUT == 128 && !F8 && KS == 3 && (EPI == EPI_ACT || EPI == EPI_HEAD);
+  // activation and head instances on box tiles take it: the 8 x 128 network
+  // at d = 31 gains about 3 %.  On flat tiles (d = 13) it gained 1.7 % but
+  // fetched half as much again from HBM (the fixed shares keep an XCD's
+  // workgroups on neighbouring tiles' chunks at the same time, whose lines
+  // L2 then serves to all of them); the fp8 and 64-wide layers gained
+  // nothing, and the counters' registers made the fp8 head instance spill
+  // in its K loop (and the shortcut-adding ones spill more).
+  constexpr bool DYN = COUT == 128 && !F8 && KS == 3 && MODE == 1 && (EPI == EPI_ACT || EPI == EPI_HEAD);
   if (!DYN) sched = nullptr;
   const int xcd = blockIdx.x & 7, nwx = gridDim.x >> 3, per_xcd = (nunits + 7) >> 3;
   uint32_t* const grab = sched ? sched + xcd * 32 : nullptr;
