@@ -303,7 +303,8 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
                    const float* __restrict__ head_w, const float* __restrict__ head_b,
                    const int32_t* __restrict__ tables, uint8_t* __restrict__ nib,
                    float* __restrict__ logits, int batch, int kshift_arg, float* __restrict__ partial,
-                   const uint16_t* __restrict__ sc, int sc_stride, int lsl, uint32_t* __restrict__ sched) {
+                   const uint16_t* __restrict__ sc, int sc_stride, int lsl, uint32_t* __restrict__ sched,
+                   int nstat) {
   static_assert(KS == 3 || MODE == 1, "5x5x5 layers run on box tiles");
   extern __shared__ __attribute__((aligned(16))) char smem[];
   using W = Split<COUT>;
@@ -568,24 +569,26 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
   };
 
   // Units: each XCD takes a contiguous range (tile_of).  A workgroup's first
-  // two units are fixed (the k-th and (k + n)-th of its XCD's range, n = the
-  // XCD's workgroups); with `sched` (a launch of more units than that), the
-  // rest are taken in turn from a per-XCD counter, so that workgroups that
-  // run faster take more of them (fixed shares left the last workgroups of
-  // an XCD finishing 10-20 % of the layer after the first).  Thread 0
-  // takes unit it + 2 at the top of iteration it and hands it over in LDS
-  // slot it % 2 at the end of the iteration's first chunk, read by every
-  // wave at the top of iteration it + 1 (a chunk's barrier in between).  Counters sit in separate 64-byte lines
-  // (grab, then done, per XCD); the last workgroup of an XCD to finish puts
-  // both back to zero for the next launch.  Only the bf16 128-wide 3x3x3
-  // activation and head instances on box tiles take it: the 8 x 128 network
-  // at d = 31 gains about 3 %.  On flat tiles (d = 13) it gained 1.7 % but
-  // fetched half as much again from HBM (the fixed shares keep an XCD's
-  // workgroups on neighbouring tiles' chunks at the same time, whose lines
-  // L2 then serves to all of them); the fp8 and 64-wide layers gained
-  // nothing, and the counters' registers made the fp8 head instance spill
-  // in its K loop (and the shortcut-adding ones spill more).
-  constexpr bool DYN = COUT == 128 && !F8 && KS == 3 && MODE == 1 && (EPI == EPI_ACT || EPI == EPI_HEAD);
+  // nstat units are fixed (the k-th, (k + n)-th, ... of its XCD's range, n =
+  // the XCD's workgroups); with `sched` (a launch of more units than two per
+  // workgroup), the rest are taken in turn from a per-XCD counter, so that
+  // workgroups that run faster take more of them (fixed shares left the
+  // last workgroups of an XCD finishing 10-20 % of the layer after the
+  // first).  Thread 0 takes unit it + 2 at the top of iteration it and hands
+  // it over in LDS slot it % 2 at the end of the iteration's first chunk,
+  // read by every wave at the top of iteration it + 1 (a chunk's barrier in
+  // between).  Counters sit in separate 64-byte lines (grab, then done, per
+  // XCD); the last workgroup of an XCD to finish puts both back to zero for
+  // the next launch.  Box tiles fix two units (c5: about 3 % less time);
+  // flat tiles fix seven eighths of a workgroup's share: fixed shares keep
+  // an XCD's workgroups on neighbouring tiles' chunks together, whose lines
+  // L2 then serves to all of them, and counters from the third unit on
+  // fetched half as much again from HBM (c3: 1.7 % less time); from seven
+  // eighths on, 7 % more for 2.2 % less time.  Only the bf16 128-wide 3x3x3
+  // activation and head instances take counters: the fp8 and 64-wide layers
+  // gained nothing, and the counters' registers made the fp8 head instance
+  // spill in its K loop (and the shortcut-adding ones spill more).
+  constexpr bool DYN = COUT == 128 && !F8 && KS == 3 && (EPI == EPI_ACT || EPI == EPI_HEAD);
   if (!DYN) sched = nullptr;
   const int xcd = blockIdx.x & 7, nwx = gridDim.x >> 3, per_xcd = (nunits + 7) >> 3;
   uint32_t* const grab = sched ? sched + xcd * 32 : nullptr;
@@ -599,7 +602,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
     }
   };
   auto dyn_unit = [&](uint32_t c) -> int {  // unit of the c-th counter value (-1: none left)
-    const long long local = 2ll * nwx + c;
+    const long long local = (long long)nstat * nwx + c;
     if (local >= per_xcd) return -1;
     const long long u = (long long)xcd * per_xcd + local;
     return u < nunits ? (int)u : -1;
@@ -682,7 +685,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
     const int c0 = (unit & (ksplit - 1)) * NCU;  // first chunk of this unit
     const int slice = slice_of(unit);
     int next_unit;
-    if (!sched || it == 0) {
+    if (!sched || it + 1 < nstat) {
       next_unit = tile_of(blockIdx.x, gridDim.x, it + 1, nunits);
     } else {
       next_unit = (int)__builtin_amdgcn_readfirstlane(dyn_s[(it - 1) & 1]);
@@ -690,7 +693,8 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
     // unit it + 2 (written to LDS at the end of the first chunk, so that no
     // wave waits here for the counter)
     uint32_t grabbed = 0;
-    if (sched && tid == 0) grabbed = __hip_atomic_fetch_add(grab, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (sched && tid == 0 && it + 2 >= nstat)
+      grabbed = __hip_atomic_fetch_add(grab, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const int next = next_unit >= 0 ? next_unit >> (kshift + lsl) : -1;
     const int next_c0 = next_unit >= 0 ? (next_unit & (ksplit - 1)) * NCU : 0;
     const int next_slice = next_unit >= 0 ? slice_of(next_unit) : 0;
@@ -876,7 +880,7 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
       }
       __builtin_amdgcn_s_setprio(0);
       if constexpr (SG * RMAX >= NSTEP) stage_store(RMAX - 1);
-      if (sched && tid == 0 && chunk == 0) dyn_s[it & 1] = (uint32_t)dyn_unit(grabbed);
+      if (sched && tid == 0 && chunk == 0 && it + 2 >= nstat) dyn_s[it & 1] = (uint32_t)dyn_unit(grabbed);
       // every wave's staging writes done, every wave done reading `cur`
       __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
       __builtin_amdgcn_s_barrier();
@@ -1071,9 +1075,13 @@ hipError_t launch_hidden(const Geom& g, const Tiling& tl, int act, const void* x
   const long long nunits = tl.ntiles << (kshift + lsl);
   const long long nwg = conv_workgroups(nunits, n_workgroups);
   if (nunits <= 2 * nwg) sched = nullptr;  // every unit is one of the two fixed ones
+  // fixed units per workgroup before the counters: two on box tiles; on flat
+  // tiles seven eighths of a workgroup's share
+  const long long share = (nunits + 7) / 8 / (nwg / 8);
+  const int nstat = tl.mode == 0 ? (int)std::max(2ll, share * 7 / 8) : 2;
   hipLaunchKernelGGL((conv_hidden_kernel<CIN, COUT, EPI, MODE, F8, KS>), dim3((unsigned)nwg), dim3(NT),
                      (size_t)L::total, stream, g, tl, act, x, y, ystride, (const u32x4*)wfrag, bias, head_w,
-                     head_b, tables, nib, logits, batch, kshift, partial, sc, sc_stride, lsl, sched);
+                     head_b, tables, nib, logits, batch, kshift, partial, sc, sc_stride, lsl, sched, nstat);
   return hipSuccess;
 }
 

@@ -182,7 +182,7 @@ struct Split_k {
   int lsl = 0;  // 2^lsl output-channel slices of c_out channels in one launch
   // 256 zeroed words (per XCD: a grab and a done counter, 64 bytes apart):
   // a launch of more than two units per workgroup takes its units after the
-  // first two from these counters and leaves them zero; null: fixed shares
+  // fixed ones from these counters and leaves them zero; null: fixed shares
   uint32_t* sched = nullptr;
 };
 
