@@ -584,11 +584,12 @@ conv_hidden_kernel(Geom g, Tiling tl, int act, const void* __restrict__ x, void*
   // an XCD's workgroups on neighbouring tiles' chunks together, whose lines
   // L2 then serves to all of them, and counters from the third unit on
   // fetched half as much again from HBM (c3: 1.7 % less time); from seven
-  // eighths on, 7 % more for 2.2 % less time.  Only the bf16 128-wide 3x3x3
-  // activation and head instances take counters: the fp8 and 64-wide layers
-  // gained nothing, and the counters' registers made the fp8 head instance
-  // spill in its K loop (and the shortcut-adding ones spill more).
-  constexpr bool DYN = COUT == 128 && !F8 && KS == 3 && (EPI == EPI_ACT || EPI == EPI_HEAD);
+  // eighths on, 7 % more for 2.2 % less time.  Only the 128-wide 3x3x3
+  // activation instances and the bf16 head ones take counters (fp8: 0.5 %
+  // less time at c3, 1.4 % at c5): the 64-wide layers gained nothing, and the
+  // counters' registers made the fp8 head instance spill in its K loop (and
+  // the shortcut-adding ones spill more).
+  constexpr bool DYN = COUT == 128 && KS == 3 && (EPI == EPI_ACT || (EPI == EPI_HEAD && !F8));
   if (!DYN) sched = nullptr;
   const int xcd = blockIdx.x & 7, nwx = gridDim.x >> 3, per_xcd = (nunits + 7) >> 3;
   uint32_t* const grab = sched ? sched + xcd * 32 : nullptr;
