@@ -191,7 +191,10 @@ pd_status predecoder_create_ex(const float* weights, size_t n_weights, int32_t d
  * logits:   device or NULL; if given, [batch][4][T][H][H] fp32 outputs of
  *           the last layer at every grid site (channel order as in `flips`;
  *           H = d + 1 on the plaquette layout, d on the paper layout).
- * 1 <= batch <= max_batch.  Asynchronous on hip_stream. */
+ * 1 <= batch <= max_batch.  Asynchronous on hip_stream.  The run works in the
+ * handle's workspace (activations, parked sums, the hidden kernel's unit
+ * counters): runs of one handle must not overlap (one stream, or the caller
+ * orders them); separate handles are independent. */
 pd_status predecoder_run(pd_predecoder* h, void* hip_stream, const uint64_t* det, int32_t batch,
                          uint64_t* flips, uint64_t* residual, float* logits);
 
