@@ -26,11 +26,16 @@
 //     is loaded in 7 rounds spread over the current chunk's 27 k-steps (one
 //     per tap) and written to the other buffer.
 //   * A staged voxel occupies 48 bytes of LDS.  The LDS serves a 16-byte read
-//     16 lanes at a time over 16 groups of 16 bytes; granule g of voxel v sits
-//     in group (3 v + g) mod 16, so 16 consecutive staged voxels hit 16
-//     distinct groups.  Flat tiles stage only the real columns; reads of the
-//     left / right halo column are redirected to a 256-byte zero region with
-//     the same low address bits (same group).
+//     over 16 groups of 16 bytes; granule g of voxel v sits in group
+//     (3 v + g) mod 16, so 16 consecutive staged voxels hit 16 distinct
+//     groups, and a fragment read of 32 consecutive staged voxels (flat
+//     tiles) or the staging stores meet no group twice in one LDS cycle
+//     (measured).  A read whose 32 voxels come from two rows of a box, with
+//     the rows' halo voxels between them, costs a few cycles more, which the
+//     LDS pipe absorbs (it is less than half busy here).  Flat tiles stage
+//     only the real columns; reads of the left / right halo column are
+//     redirected to a 256-byte zero region with the same low address bits
+//     (same group).
 //   * The 27 k-steps of a chunk are unrolled and software pipelined:
 //     activation fragments are read one step ahead, weight fragments
 //     (arranged at create time in MFMA operand order, one coalesced 16-byte
