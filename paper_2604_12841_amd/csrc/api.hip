@@ -910,16 +910,23 @@ pd_status enqueue_run(pd_predecoder* h, Workspace& ws, hipStream_t st, const uin
           s = check_launch(pd::launch_conv_first(g, L.c_in, cw, L.act, x, yk, L.c_out, wk, h->bdev[l] + k * cw,
                                                  batch, fp8, ks, st));
         }
-      } else if (!head_layer && l < (int)h->wnarrow.size() && h->wnarrow[l] &&
-                 tl.ntiles * (L.c_out / 32) <= h->n_cu) {
+      } else if (l < (int)h->wnarrow.size() && h->wnarrow[l] && tl.ntiles * (L.c_out / 32) <= h->n_cu &&
+                 (!head_layer || (L.c_in <= 128 && (tl.ntiles * (L.c_out / 32)) <= ws.max_units &&
+                                  split_for(ws, tl, L.c_in, L.c_out, fp8, ks).kshift > 0))) {
         // a small batch: a 64- to 256-wide layer as 32-channel slices, two to
         // eight times the workgroups (still at most one per CU) for the same
         // staging, in place of splitting its K loops (a 256-channel input's
-        // long loops may still split).  The layer that carries the head is
-        // never sliced, also when a run stops at it, so that its exported
-        // activations are the ones the head reads.
-        s = run_hidden(h, ws, tl, L.c_in, 32, L.c_out / 32, L.act, x, y, L.c_out, h->wnarrow[l], h->bnarrow[l], 0,
-                       nullptr, nullptr, logits, batch, fp8, nullptr, 0, ks, st);
+        // long loops may still split).  The layer that carries the head, when
+        // unsliced it would split its K loops and finish in a second kernel
+        // anyway: its slices park their sums and that kernel finishes whole
+        // rows with the head (d = 13, batch 1, 8 x 128: 2.6 % less time per
+        // round in bf16, 4 % in fp8; a head layer that runs whole in one
+        // launch stays so, the extra kernel costing more: 3 % at d = 25,
+        // 6 x 64).  A run that stops at it slices it the same way, so that
+        // its exported activations are the ones the head reads.
+        s = run_hidden(h, ws, tl, L.c_in, 32, L.c_out / 32, L.act, x, y, L.c_out, h->wnarrow[l], h->bnarrow[l],
+                       fuse_head ? 1 : 0, fuse_head ? h->head_w : nullptr, fuse_head ? h->head_b : nullptr, logits,
+                       batch, fp8, nullptr, 0, ks, st);
       } else if (!head_layer && l < (int)h->whalf.size() && h->whalf[l] && tl.ntiles * (L.c_out / 64) <= h->n_cu) {
         // ... or, with too many tiles for that, a 128- or 256-wide one as slices of 64
         s = run_hidden(h, ws, tl, L.c_in, 64, L.c_out / 64, L.act, x, y, L.c_out, h->whalf[l], h->bhalf[l], 0,

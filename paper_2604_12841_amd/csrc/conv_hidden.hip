@@ -935,19 +935,21 @@ __global__ void __launch_bounds__(256) split_finish_kernel(Geom g, Tiling tl, in
                                                            int batch, const uint16_t* __restrict__ sc, int sc_stride,
                                                            int lsl) {
   constexpr bool ROWS8 = EPI == EPI_ACT || EPI == EPI_ADD;  // one thread per (row, 8 channels)
-  // the head: one thread per (row, 8 channels) too, the rows' partial head
-  // sums reduced over the row's consecutive lanes
-  const int groups = (ROWS8 || EPI == EPI_HEAD) ? cout / 8 : 1;
+  // the head: one thread per (row, 8 channels) too, of every slice of the
+  // row (hsl: the slices a row's lanes span), the rows' partial head sums
+  // reduced over the row's consecutive lanes
+  const int hsl = EPI == EPI_HEAD ? lsl : 0, tsl = lsl - hsl;
+  const int groups = (ROWS8 || EPI == EPI_HEAD) ? (cout << hsl) / 8 : 1;
   const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (gid >= ((long long)tl.ntiles << lsl) * kTileRows * groups) return;
-  // (tile, output-channel slice) of this thread: activations only, the head
-  // and the output layer run unsliced (lsl = 0)
+  if (gid >= ((long long)tl.ntiles << tsl) * kTileRows * groups) return;
+  // (tile, output-channel slice) of this thread: activations only; the head
+  // and the output layer take whole rows
   const int ts = (int)(gid / (kTileRows * groups));
-  const int tile = ts >> lsl, slice = ts & ((1 << lsl) - 1);
+  const int tile = ts >> tsl, slice = ts & ((1 << tsl) - 1);
   const int rem = (int)(gid - (long long)ts * kTileRows * groups);
   const int r = rem / groups, grp = rem - r * groups;
   const int ksplit = 1 << kshift;
-  if (lsl) {  // this slice's biases, outputs, and shortcut columns or projection rows
+  if (tsl) {  // this slice's biases, outputs, and shortcut columns or projection rows
     bias += (size_t)slice * (F8 ? 2 : 1) * cout;
     y = (char*)y + (size_t)slice * cout * (F8 ? 1 : 2);
     if (head_w) {
@@ -957,15 +959,16 @@ __global__ void __launch_bounds__(256) split_finish_kernel(Geom g, Tiling tl, in
       sc = (const uint16_t*)((const char*)sc + (size_t)slice * cout * (F8 ? 1 : 2));
     }
   }
-  // pre-activation of channels c .. c + 7 of this row: the sum over the
+  // pre-activation of channels c .. c + 7 of this row in the slice whose
+  // units are u << kshift .. (part p: + p) and biases bs: the sum over the
   // tile's parts in part order (fp8: times the channel's weight scale), plus
   // the bias
   // Parts are added strictly in part order; from four parts on they are read
   // four at a time, so the four reads go out together.
-  auto sum8 = [&](int c, float (&v)[8]) {
+  auto sum8 = [&](int u, const float* bs, int c, float (&v)[8]) {
     if (ksplit < 4) {
       for (int p = 0; p < ksplit; ++p) {
-        const float* src = partial + ((size_t)((ts << kshift) + p) * kTileRows + r) * cout + c;
+        const float* src = partial + ((size_t)((u << kshift) + p) * kTileRows + r) * cout + c;
         const float4 a = *reinterpret_cast<const float4*>(src);
         const float4 b = *reinterpret_cast<const float4*>(src + 4);
         const float t[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
@@ -978,7 +981,7 @@ __global__ void __launch_bounds__(256) split_finish_kernel(Geom g, Tiling tl, in
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int p = p0 + q;  // < ksplit: ksplit is a power of two >= 4
-        const float* src = partial + ((size_t)((ts << kshift) + p) * kTileRows + r) * cout + c;
+        const float* src = partial + ((size_t)((u << kshift) + p) * kTileRows + r) * cout + c;
         a[q] = *reinterpret_cast<const float4*>(src);
         b[q] = *reinterpret_cast<const float4*>(src + 4);
       }
@@ -991,14 +994,14 @@ __global__ void __launch_bounds__(256) split_finish_kernel(Geom g, Tiling tl, in
       }
     }
 #pragma unroll
-    for (int e = 0; e < 8; ++e) v[e] = F8 ? __builtin_fmaf(v[e], bias[cout + c + e], bias[c + e]) : v[e] + bias[c + e];
+    for (int e = 0; e < 8; ++e) v[e] = F8 ? __builtin_fmaf(v[e], bs[cout + c + e], bs[c + e]) : v[e] + bs[c + e];
   };
   if constexpr (ROWS8) {
     long long pidx, o;
     int lb;
     if (!tile_row(g, tl, tile, r, batch, &pidx, &lb, &o)) return;
     float v[8];
-    sum8(grp * 8, v);
+    sum8(ts, bias, grp * 8, v);
     if constexpr (EPI == EPI_ADD) {  // the block's shortcut
       float pj[8];
       shortcut_of<8, F8>(sc, sc_stride, pidx, head_w, head_b, grp * 8, pj);
@@ -1021,7 +1024,7 @@ __global__ void __launch_bounds__(256) split_finish_kernel(Geom g, Tiling tl, in
     float lg[4];
     if constexpr (EPI == EPI_OUT) {
       float v[8];
-      sum8(0, v);
+      sum8(ts, bias, 0, v);
 #pragma unroll
       for (int o2 = 0; o2 < 4; ++o2) lg[o2] = v[o2];
       if (sc) {  // residual shortcut of the last block
@@ -1032,18 +1035,19 @@ __global__ void __launch_bounds__(256) split_finish_kernel(Geom g, Tiling tl, in
         lg[3] += __uint_as_float(sv.y & 0xFFFF0000u);
       }
     } else {
-      // this lane's 8 channels, then the sum over the row's groups (cout / 8
-      // consecutive lanes, all active: a row is in range for all or none)
-      const int c = grp * 8;
+      // this lane's 8 channels (of slice c / cout), then the sum over the
+      // row's groups (consecutive lanes, all active: a row is in range for
+      // all or none)
+      const int c = grp * 8, sl = c / cout, cl = c - sl * cout;
       float v[8];
-      sum8(c, v);
+      sum8((tile << hsl) | sl, bias + (size_t)sl * (F8 ? 2 : 1) * cout, cl, v);
 #pragma unroll
       for (int o2 = 0; o2 < 4; ++o2) lg[o2] = 0.0f;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float a = F8 ? e4m3_round(act_fn<ACT>(v[e])) : bf16_round(act_fn<ACT>(v[e]));
 #pragma unroll
-        for (int o2 = 0; o2 < 4; ++o2) lg[o2] += head_w[o2 * cout + c + e] * a;
+        for (int o2 = 0; o2 < 4; ++o2) lg[o2] += head_w[o2 * (cout << hsl) + c + e] * a;
       }
       for (int m = groups >> 1; m >= 1; m >>= 1)
 #pragma unroll
@@ -1097,11 +1101,17 @@ hipError_t launch_one(const Geom& g, const Tiling& tl, int act, const void* x, v
                       const int32_t* tables, uint8_t* nib, float* logits, int batch, int n_workgroups,
                       const Split_k& sk, const uint16_t* sc, int sc_stride, hipStream_t stream) {
   hipError_t e;
-  if (sk.kshift == 0) {
-    e = launch_hidden<CIN, COUT, EPI, MODE, F8, KS>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b,
-                                                    tables, nib, logits, batch, n_workgroups, 0, nullptr, sc,
-                                                    sc_stride, sk.lsl, sk.sched, stream);
-    return e != hipSuccess ? e : hipGetLastError();
+  // a head over 32-channel output slices (a small batch): every unit parks
+  // its slice's sums, and the second kernel finishes whole rows, head and
+  // threshold included
+  constexpr bool PARK_ONLY = EPI == EPI_HEAD && COUT == 32;
+  if constexpr (!PARK_ONLY) {
+    if (sk.kshift == 0) {
+      e = launch_hidden<CIN, COUT, EPI, MODE, F8, KS>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b,
+                                                      tables, nib, logits, batch, n_workgroups, 0, nullptr, sc,
+                                                      sc_stride, sk.lsl, sk.sched, stream);
+      return e != hipSuccess ? e : hipGetLastError();
+    }
   }
   // K loops split: park the parts, then add them and finish the tiles
   e = launch_hidden<CIN, COUT, EPI_PARK, MODE, F8, KS>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b,
@@ -1111,6 +1121,7 @@ hipError_t launch_one(const Geom& g, const Tiling& tl, int act, const void* x, v
   const long long threads = ((long long)tl.ntiles << sk.lsl) * kTileRows *
                             (EPI == EPI_ACT || EPI == EPI_ADD || EPI == EPI_HEAD ? COUT / 8 : 1);
   static_assert(EPI != EPI_HEAD || (64 % (COUT / 8) == 0), "a row's head lanes lie in one wave");
+  if (EPI == EPI_HEAD && (COUT << sk.lsl) / 8 > 64) return hipErrorInvalidValue;
   with_activation(act, [&](auto A) {
     hipLaunchKernelGGL((split_finish_kernel<EPI, decltype(A)::value, F8>), dim3((unsigned)((threads + 255) / 256)),
                        dim3(256), 0, stream, g, tl, COUT, sk.kshift, sk.partial, bias, y, ystride, head_w, head_b,
@@ -1154,6 +1165,8 @@ hipError_t launch_case(const Geom& g, const Tiling& tl, int cin, int cout, int a
   PD_HIDDEN_CASE(128, 128, EPI_HEAD)
   PD_HIDDEN_CASE(64, 128, EPI_HEAD)
   PD_HIDDEN_CASE(128, 64, EPI_HEAD)
+  PD_HIDDEN_CASE(64, 32, EPI_HEAD)  // the head layer in 32-channel slices (small batches)
+  PD_HIDDEN_CASE(128, 32, EPI_HEAD)
   // the residual network's layers (bf16 and fp8)
   PD_HIDDEN_CASE(512, 128, EPI_ACT)
   PD_HIDDEN_CASE(64, 64, EPI_ADD)
@@ -1198,9 +1211,14 @@ hipError_t launch_conv_hidden(const Geom& g, const Tiling& tl, int cin, int cout
   if (sk.kshift < 0 || nchunk % (1 << sk.kshift) != 0 ||
       (sk.kshift > 0 && (tl.ntiles << (sk.kshift + sk.lsl)) > sk.max_units))
     return hipErrorInvalidValue;
-  // output-channel slices: up to max_slices, of activation layers (a head or
-  // an output layer needs every channel of a voxel in one unit)
-  if (sk.lsl < 0 || (1 << sk.lsl) > max_slices(cout) || (sk.lsl > 0 && head != EPI_ACT && head != EPI_ADD))
+  // output-channel slices: up to max_slices, of activation layers, or of 32
+  // channels for a head (whose rows the second kernel finishes; an output
+  // layer needs every channel of a voxel in one unit)
+  if (sk.lsl < 0 || (1 << sk.lsl) > max_slices(cout) ||
+      (sk.lsl > 0 && head != EPI_ACT && head != EPI_ADD && !(head == EPI_HEAD && cout == 32)))
+    return hipErrorInvalidValue;
+  // a sliced head parks every unit's sums, also with whole K loops
+  if (head == EPI_HEAD && cout == 32 && (!sk.partial || (tl.ntiles << (sk.kshift + sk.lsl)) > sk.max_units))
     return hipErrorInvalidValue;
   if (fp8)
     return launch_case<true>(g, tl, cin, cout, act, x, y, ystride, wfrag, bias, head, head_w, head_b, tables, nib,

@@ -198,12 +198,14 @@ def test_layer1_same_at_any_launch_size(cuda, dtype):
 @pytest.mark.parametrize("width,n,B", [(64, 6, 1), (64, 6, 40), (128, 4, 1), (128, 4, 20), (128, 4, 40)])
 def test_sliced_layers_tight(cuda, width, n, B):
     """n hidden layers of 64 or 128 channels at d = T = 9 (4, 70 and 141
-    tiles at batches 1, 20 and 40): at batch 1 each C -> C layer but the
-    last runs as 32-channel output slices, at batch 20 a 128-wide one as two
-    slices of 64, at batch 40 whole.  Either way every hidden layer's stored
-    bf16 activations are checked from the GPU's own input under the rule of
-    tests/tight.py, then the logits from the GPU's last hidden activations
-    within their own sums' bound."""
+    tiles at batches 1, 20 and 40): at batch 1 each C -> C layer runs as
+    32-channel output slices (the last, which carries the head, where whole
+    it would split its K loops: the 128-wide one, its slices' sums then
+    finished with the head by the second kernel), at batch 20 a 128-wide one
+    but the last as two slices of 64, at batch 40 whole.  Either way every
+    hidden layer's stored bf16 activations are checked from the GPU's own
+    input under the rule of tests/tight.py, then the logits from the GPU's
+    last hidden activations within their own sums' bound."""
     import tight
     from parity import dev_u64
     d = T = 9
