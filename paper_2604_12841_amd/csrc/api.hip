@@ -927,10 +927,14 @@ pd_status enqueue_run(pd_predecoder* h, Workspace& ws, hipStream_t st, const uin
         s = run_hidden(h, ws, tl, L.c_in, 32, L.c_out / 32, L.act, x, y, L.c_out, h->wnarrow[l], h->bnarrow[l],
                        fuse_head ? 1 : 0, fuse_head ? h->head_w : nullptr, fuse_head ? h->head_b : nullptr, logits,
                        batch, fp8, nullptr, 0, ks, st);
-      } else if (!head_layer && l < (int)h->whalf.size() && h->whalf[l] && tl.ntiles * (L.c_out / 64) <= h->n_cu) {
-        // ... or, with too many tiles for that, a 128- or 256-wide one as slices of 64
-        s = run_hidden(h, ws, tl, L.c_in, 64, L.c_out / 64, L.act, x, y, L.c_out, h->whalf[l], h->bhalf[l], 0,
-                       nullptr, nullptr, logits, batch, fp8, nullptr, 0, ks, st);
+      } else if (l < (int)h->whalf.size() && h->whalf[l] && tl.ntiles * (L.c_out / 64) <= h->n_cu &&
+                 (!head_layer || (L.c_in <= 128 && (tl.ntiles * (L.c_out / 64)) <= ws.max_units &&
+                                  split_for(ws, tl, L.c_in, L.c_out, fp8, ks).kshift > 0))) {
+        // ... or, with too many tiles for that, a 128- or 256-wide one as
+        // slices of 64 (the head layer as above)
+        s = run_hidden(h, ws, tl, L.c_in, 64, L.c_out / 64, L.act, x, y, L.c_out, h->whalf[l], h->bhalf[l],
+                       fuse_head ? 1 : 0, fuse_head ? h->head_w : nullptr, fuse_head ? h->head_b : nullptr, logits,
+                       batch, fp8, nullptr, 0, ks, st);
       } else {  // the last hidden layer may carry the head and the threshold in its epilogue
         s = run_hidden(h, ws, tl, L.c_in, cw, nsl, L.act, x, y, L.c_out, h->wdev[l], h->bdev[l], fuse_head ? 1 : 0,
                        h->head_w, h->head_b, logits, batch, fp8, nullptr, 0, ks, st);

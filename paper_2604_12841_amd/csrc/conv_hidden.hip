@@ -1101,12 +1101,12 @@ hipError_t launch_one(const Geom& g, const Tiling& tl, int act, const void* x, v
                       const int32_t* tables, uint8_t* nib, float* logits, int batch, int n_workgroups,
                       const Split_k& sk, const uint16_t* sc, int sc_stride, hipStream_t stream) {
   hipError_t e;
-  // a head over 32-channel output slices (a small batch): every unit parks
-  // its slice's sums, and the second kernel finishes whole rows, head and
-  // threshold included
+  // a head over output slices (a small batch): every unit parks its
+  // slice's sums, and the second kernel finishes whole rows, head and
+  // threshold included (32-channel slices exist only for this)
   constexpr bool PARK_ONLY = EPI == EPI_HEAD && COUT == 32;
   if constexpr (!PARK_ONLY) {
-    if (sk.kshift == 0) {
+    if (sk.kshift == 0 && !(EPI == EPI_HEAD && sk.lsl > 0)) {
       e = launch_hidden<CIN, COUT, EPI, MODE, F8, KS>(g, tl, act, x, y, ystride, wfrag, bias, head_w, head_b,
                                                       tables, nib, logits, batch, n_workgroups, 0, nullptr, sc,
                                                       sc_stride, sk.lsl, sk.sched, stream);
@@ -1212,14 +1212,14 @@ hipError_t launch_conv_hidden(const Geom& g, const Tiling& tl, int cin, int cout
       (sk.kshift > 0 && (tl.ntiles << (sk.kshift + sk.lsl)) > sk.max_units))
     return hipErrorInvalidValue;
   // output-channel slices: up to max_slices, of activation layers, or of 32
-  // channels for a head (whose rows the second kernel finishes; an output
-  // layer needs every channel of a voxel in one unit)
+  // or 64 channels for a head (whose rows the second kernel finishes; an
+  // output layer needs every channel of a voxel in one unit)
+  const bool head_slices = head == EPI_HEAD && (cout == 32 || (cout == 64 && sk.lsl > 0));
   if (sk.lsl < 0 || (1 << sk.lsl) > max_slices(cout) ||
-      (sk.lsl > 0 && head != EPI_ACT && head != EPI_ADD && !(head == EPI_HEAD && cout == 32)))
+      (sk.lsl > 0 && head != EPI_ACT && head != EPI_ADD && !head_slices))
     return hipErrorInvalidValue;
   // a sliced head parks every unit's sums, also with whole K loops
-  if (head == EPI_HEAD && cout == 32 && (!sk.partial || (tl.ntiles << (sk.kshift + sk.lsl)) > sk.max_units))
-    return hipErrorInvalidValue;
+  if (head_slices && (!sk.partial || (tl.ntiles << (sk.kshift + sk.lsl)) > sk.max_units)) return hipErrorInvalidValue;
   if (fp8)
     return launch_case<true>(g, tl, cin, cout, act, x, y, ystride, wfrag, bias, head, head_w, head_b, tables, nib,
                              logits, batch, n_workgroups, sk, sc, sc_stride, ks, stream);
