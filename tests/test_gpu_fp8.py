@@ -47,14 +47,16 @@ def test_fp8_parity(cuda, case):
     assert_parity(st, "fp8")
 
 
-def test_fp8_full_size_sampled(cuda):
-    """Workload 3 (d = 13, T = 13, 8 x 128) at its full batch of 4096 in fp8:
-    three samples against the oracle, every sample's residual against the
-    oracle's residual of the GPU flips; then the same samples alone (a small
-    batch, whose K loops are split) against the full batch."""
-    d, T, _, layers, weights, det, _ = config_case(3)
+@pytest.mark.parametrize("cfg", [3, 5])
+def test_fp8_full_size_sampled(cuda, cfg):
+    """Workloads 3 (d = T = 13, batch 4096, flat tiles) and 5 (d = T = 31,
+    batch 256, box tiles), 8 x 128, at their full batch in fp8: three samples
+    against the oracle, every sample's residual against the oracle's residual
+    of the GPU flips; then the same samples alone (a small batch, whose K
+    loops are split) against the full batch."""
+    d, T, _, layers, weights, det, _ = config_case(cfg)
     B = det.shape[0]
-    idx = [0, 2048, 4095]
+    idx = [0, B // 2, B - 1]
     say("fp8 full size d", d, "T", T, "B", B)
     flips, res, logits = _gpu(d, T, layers, weights, det, "plaquette", None, None)
     np.testing.assert_array_equal(res, oracle.residual_from_flips(d, T, det, flips))

@@ -7,7 +7,9 @@ run is the launch configuration the benchmark times (one handle, the whole
 batch); sampled samples (first and last) are compared with the oracle under
 the parity rule of parity.py, every sample's residual with the oracle's
 residual of the GPU's flips, and every sample's flips and residual with the
-threshold of the GPU's own logits."""
+threshold of the GPU's own logits.  Also the two plaquette-grid networks of
+the d = 5 ... 31 sweep at batch 1 from d = 13 up (the latency rows, where
+layers run as output slices or split K loops, the head layer included)."""
 import json
 import os
 
@@ -122,3 +124,26 @@ def test_model6_batch_and_its_sub_batches(cuda, dtype):
                  layout="paper", tol=tol)
     say("  first", found, "samples exact; the rest alone against the batch:", st)
     assert_parity(st, dtype, tol=tol)
+
+
+SWEEP_B1 = [(w, d, dt) for dt in ("bf16", "fp8") for w in (3, 4) for d in (13, 17, 21, 25, 31)]
+
+
+@pytest.mark.parametrize("wl,d,dtype", SWEEP_B1, ids=["w%d_d%d_b1_%s" % c for c in SWEEP_B1])
+def test_plaquette_network_at_batch_one(cuda, wl, d, dtype):
+    """The sweep's batch-1 runs (`bench.py --workload W --d D --batch 1`):
+    the workload's network and weights, its noise, d = T."""
+    c = workload.CONFIGS[wl]
+    layers = workload.config_layers(wl)
+    weights = workload.config_weights(wl)
+    det, _ = workload.make_inputs(d, d, 1, c["p"], c["q"], 2000 + wl)
+    say("workload", wl, "network at d = T =", d, "batch 1", dtype)
+    pre = pdx.Predecoder(weights, d, d, layers, dtype, max_batch=1)
+    flips, res, logits = run_gpu(pre, det)
+    pre.close()
+    ref = oracle.run(d, d, det, layers, weights, bf16=dtype == "bf16", fp8=dtype == "fp8")
+    st = compare(d, d, dtype, *ref, flips, res, logits, tol=TOL[dtype])
+    say("  stats", st)
+    assert_parity(st, dtype, tol=TOL[dtype])
+    np.testing.assert_array_equal(res, oracle.residual_from_flips(d, d, det, flips))
+    assert_flips_follow_logits(d, d, det, logits, flips, res)
