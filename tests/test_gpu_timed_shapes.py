@@ -8,8 +8,9 @@ batch); sampled samples (first and last) are compared with the oracle under
 the parity rule of parity.py, every sample's residual with the oracle's
 residual of the GPU's flips, and every sample's flips and residual with the
 threshold of the GPU's own logits.  Also the two plaquette-grid networks of
-the d = 5 ... 31 sweep at batch 1 from d = 13 up (the latency rows, where
-layers run as output slices or split K loops, the head layer included)."""
+the d = 5 ... 31 sweep: at batch 1 from d = 13 up (the latency rows, where
+layers run as output slices or split K loops, the head layer included), and
+batched at the d that the benchmark workloads do not cover."""
 import json
 import os
 
@@ -144,6 +145,36 @@ def test_plaquette_network_at_batch_one(cuda, wl, d, dtype):
     ref = oracle.run(d, d, det, layers, weights, bf16=dtype == "bf16", fp8=dtype == "fp8")
     st = compare(d, d, dtype, *ref, flips, res, logits, tol=TOL[dtype])
     say("  stats", st)
+    assert_parity(st, dtype, tol=TOL[dtype])
+    np.testing.assert_array_equal(res, oracle.residual_from_flips(d, d, det, flips))
+    assert_flips_follow_logits(d, d, det, logits, flips, res)
+
+
+SWEEP_BATCHED = [(w, d, dt) for dt in ("bf16", "fp8") for w in (3, 4) for d in (5, 7, 9, 17, 21, 25)]
+
+
+def sweep_batch(d):
+    # the sweep's batch: about the d = 13, batch 4096 voxel count per step
+    return max(16, round(4096 * 13 * 14 * 14 / (d * (d + 1) ** 2)))
+
+
+@pytest.mark.parametrize("wl,d,dtype", SWEEP_BATCHED, ids=["w%d_d%d_%s" % c for c in SWEEP_BATCHED])
+def test_plaquette_network_batched_at_sweep_shape(cuda, wl, d, dtype):
+    """The sweep's batched runs (`bench.py --workload W --d D --batch B`, B
+    from sweep_batch): the first and the last sample against the oracle."""
+    c = workload.CONFIGS[wl]
+    layers = workload.config_layers(wl)
+    weights = workload.config_weights(wl)
+    B = sweep_batch(d)
+    det, _ = workload.make_inputs(d, d, B, c["p"], c["q"], 2000 + wl)
+    rows = [0, B - 1]
+    say("workload", wl, "network at d = T =", d, "batch", B, dtype)
+    pre = pdx.Predecoder(weights, d, d, layers, dtype, max_batch=B)
+    flips, res, logits = run_gpu(pre, det)
+    pre.close()
+    ref = oracle.run(d, d, det[rows], layers, weights, bf16=dtype == "bf16", fp8=dtype == "fp8")
+    st = compare(d, d, dtype, *ref, flips[rows], res[rows], logits[rows], tol=TOL[dtype])
+    say("  samples", rows, "stats", st)
     assert_parity(st, dtype, tol=TOL[dtype])
     np.testing.assert_array_equal(res, oracle.residual_from_flips(d, d, det, flips))
     assert_flips_follow_logits(d, d, det, logits, flips, res)
